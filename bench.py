@@ -1,0 +1,233 @@
+#!/usr/bin/env python3
+"""Throughput of the SDM hot path on one MI355X.
+
+One step = one pass of the layer's sparse path over one batch of synthetic
+input of the 1.4B-shaped workload (B=8, H=16, T=4096, d_k=d_v=128,
+N=65536 slots per head, top-32 reads and writes, bf16 inputs, fp32 memory):
+addressing of the read queries and of the write keys, then the forward scan.
+The memory table stays resident in HBM and carries from one step to the next
+(the state-carry property: each step is a further 4096 tokens of every
+stream; the work per step does not depend on the table's contents).
+
+A second measurement times the training step (forward with the undo log +
+backward with addressing gradients) on the training workload (B=4, H=16,
+T=4096), reported under "train".
+
+Printed: one JSON line.  `value` is forward tokens/s (B*T positions, all
+heads) over the timed steps; `roofline` gives the forward scan kernel's
+algorithmic HBM bytes per launch over its mean event-timed duration;
+`cpu_baseline` is the CPU oracle timed on a bounded sample of the same
+workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "SDM layer tokens/sec (fwd, fwd+bwd) at 1 GPU; achieved HBM GB/s vs peak"
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fwd_scan_c1.json")
+SCAN_SRC = os.path.join(ROOT, "paper_2607_07386_amd", "csrc", "scan_fwd.hip")
+
+
+def fwd_scan_bytes_per_token_head(W, R, d_v, in_bytes):
+    """Bytes the forward scan must move per (token, head): W rows gathered and
+    W scattered, R rows gathered (fp32 rows of d_v), the value vector in, the
+    output vector out."""
+    return (2 * W + R) * d_v * 4 + d_v * in_bytes + d_v * 4
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, inp, n_streams, T_sample):
+    """The oracle (fp64 C, OpenMP) on n_streams (b, h) streams x T_sample tokens:
+    addressing of both sides + forward scan.  Returns tokens/s (positions across
+    all H heads, i.e. token-heads / H)."""
+    import numpy as np
+
+    import oracle
+    oracle.build(force=False)
+    streams = list(range(n_streams))
+    T = T_sample
+    x_q = inp.q.f32.reshape(-1, w.T, w.d_k)[streams, :T][:, None].astype(np.float64)
+    x_k = inp.k.f32.reshape(-1, w.T, w.d_k)[streams, :T][:, None].astype(np.float64)
+    v = inp.v.f32.reshape(-1, w.T, w.d_v)[streams, :T].astype(np.float64)
+    al = inp.alpha.f32.reshape(-1, w.T)[streams, :T].astype(np.float64)
+    be = inp.beta.f32.reshape(-1, w.T)[streams, :T].astype(np.float64)
+    cb = inp.codebook.f32.astype(np.float64)
+    mem = np.zeros((n_streams, w.N, w.d_v))
+    t0 = time.perf_counter()
+    ri, rv, wi, wv = [], [], [], []
+    for i, s in enumerate(streams):
+        h = inp.heads[s]
+        a = oracle.address(x_q[i:i + 1], cb[h][None], w.N, w.topk)
+        b = oracle.address(x_k[i:i + 1], cb[h][None], w.N, w.topk)
+        ri.append(a[0]); rv.append(a[1]); wi.append(b[0]); wv.append(b[1])
+    cat = lambda xs: np.concatenate(xs)[:, 0]
+    oracle.scan_fwd(cat(wi), cat(wv), cat(ri), cat(rv), v, al, be, mem)
+    dt = time.perf_counter() - t0
+    return dict(value=n_streams * T / w.H / dt, unit="tokens/s", cores=oracle.max_threads(),
+                kind="oracle", wall_s=round(dt, 3),
+                sample=f"{n_streams} of {w.B * w.H} (b,h) streams x {T} tokens of the same workload; "
+                       f"address(q)+address(k)+forward scan, fp64; tokens/s = streams*T/H/wall")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--no-train", action="store_true", help="skip the training-step measurement")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-streams", type=int, default=16)
+    ap.add_argument("--cpu-tokens", type=int, default=4096)
+    ap.add_argument("--only", choices=["fwd", "train"], default=None,
+                    help="run one leg only (profiling runs)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2607_07386_amd import sdm
+
+    def to_dev(st):
+        if st.dtype == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(st.bits).view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(st.f32)).to(dev)
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    out = {"metric": METRIC}
+    w = synth.WORKLOADS[1]
+
+    # ------------------------------------------------------------ forward
+    if args.only in (None, "fwd"):
+        log("generating forward workload inputs")
+        inp = synth.Inputs(w)
+        q, k, v = to_dev(inp.q), to_dev(inp.k), to_dev(inp.v)
+        al, be, cb = to_dev(inp.alpha), to_dev(inp.beta), to_dev(inp.codebook)
+        B, H, T = w.B, w.H, w.T
+        mem = torch.empty((B, H, w.N, w.d_v), dtype=torch.float32, device=dev)
+        sdm.mem_init(mem, None)
+        ws = sdm.fwd_workspace(B, H, T, w.topk, w.topk, dev)
+        y = torch.empty((B, H, T, w.d_v), dtype=torch.float32, device=dev)
+        bufs = {}
+
+        def step():
+            r_idx, r_val = sdm.address(q, cb, w.N, w.topk)
+            w_idx, w_val = sdm.address(k, cb, w.N, w.topk)
+            sdm.scan_fwd(w_idx, w_val, r_idx, r_val, v, al, be, mem, workspace=ws, y=y)
+            bufs["last"] = (r_idx, w_idx)
+
+        log("warmup")
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        sdm.profile_enable(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        log(f"timing {args.steps} steps")
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        kern = {name: sdm.profile_read(name) for name in ("address", "fwd_prep", "fwd_scan")}
+        sdm.profile_enable(False)
+        tokens = B * T
+        scan_ms = kern["fwd_scan"][0] / max(kern["fwd_scan"][1], 1)
+        unit_bytes = fwd_scan_bytes_per_token_head(w.topk, w.topk, w.d_v, 2)
+        launch_bytes = unit_bytes * B * H * T
+        achieved = launch_bytes / (scan_ms * 1e-3) / 1e9
+        traffic = None
+        if os.path.exists(TRAFFIC_FILE):
+            tr = json.load(open(TRAFFIC_FILE))
+            src_hash = hashlib.sha256(open(SCAN_SRC, "rb").read()).hexdigest()
+            if tr.get("scan_fwd_sha256") == src_hash:
+                traffic = tr.get("hbm_bytes_per_launch")
+        out.update({
+            "value": round(tokens / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+            "data": "synthetic",
+            "config": {"workload": "1.4B-shaped SDM layer forward: B=8 H=16 T=4096 d_k=d_v=128 "
+                                   "N=65536 top-32 reads/writes, bf16 q/k/v/gates, fp32 memory",
+                       "global_batch": B, "seq_len": T, "heads": H, "slots_per_head": w.N,
+                       "topk": w.topk, "inputs": "bf16", "state": "f32", "parallelism": "none (1 GPU)"},
+            "kernels_ms": {n: round(v[0] / max(v[1], 1), 4) for n, v in kern.items()},
+            "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                         "kernel": "scan_fwd_kernel", "algorithmic_bytes_per_token_head": unit_bytes,
+                         "algorithmic_bytes_per_launch": launch_bytes, "kernel_ms": round(scan_ms, 4)},
+        })
+        if not args.no_cpu_baseline:
+            log("cpu baseline (oracle)")
+            out["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_streams, min(args.cpu_tokens, w.T))
+        del q, k, v, al, be, cb, mem, ws, y, bufs
+        torch.cuda.empty_cache()
+
+    # ------------------------------------------------------------ training step
+    if not args.no_train and args.only in (None, "train"):
+        wt = synth.WORKLOADS[4]
+        log("generating training workload inputs")
+        inp = synth.Inputs(wt)
+        q, k, v = to_dev(inp.q), to_dev(inp.k), to_dev(inp.v)
+        al, be, cb = to_dev(inp.alpha), to_dev(inp.beta), to_dev(inp.codebook)
+        dy = torch.from_numpy(inp.dy()).to(dev)
+        B, H, T = wt.B, wt.H, wt.T
+        mem = torch.zeros((B, H, wt.N, wt.d_v), dtype=torch.float32, device=dev)
+        saved = sdm.saved_buffer(B, H, T, wt.topk, wt.d_v, dev)
+        fws = sdm.fwd_workspace(B, H, T, wt.topk, wt.topk, dev)
+        bws = sdm.bwd_workspace(B, H, T, wt.topk, wt.topk, wt.d_v, dev)
+        dmem0 = torch.empty_like(mem)
+        y = torch.empty((B, H, T, wt.d_v), dtype=torch.float32, device=dev)
+
+        def tstep():
+            r_idx, r_val = sdm.address(q, cb, wt.N, wt.topk)
+            w_idx, w_val = sdm.address(k, cb, wt.N, wt.topk)
+            sdm.scan_fwd(w_idx, w_val, r_idx, r_val, v, al, be, mem, saved=saved, workspace=fws, y=y)
+            sdm.scan_bwd(w_idx, w_val, r_idx, r_val, v, al, be, mem, saved, dy, cb_q=cb, cb_k=cb,
+                         d_k=wt.d_k, chunk=wt.chunk, workspace=bws, dmem0=dmem0)
+
+        for _ in range(args.warmup):
+            tstep()
+        torch.cuda.synchronize()
+        sdm.profile_enable(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        log(f"timing {args.steps} training steps")
+        e0.record(stream)
+        for _ in range(args.steps):
+            tstep()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        tms = e0.elapsed_time(e1) / args.steps
+        kern = {n: sdm.profile_read(n) for n in ("address", "fwd_prep", "fwd_scan", "bwd_prep",
+                                                   "bwd_scan", "bwd_reduce", "address_bwd", "mem_init")}
+        sdm.profile_enable(False)
+        out["train"] = {
+            "value": round(B * T / (tms * 1e-3), 1), "unit": "tokens/s", "ms_per_step": round(tms, 4),
+            "workload": "training step: B=4 H=16 T=4096 d_k=d_v=128 N=65536 top-32, chunk 64; "
+                        "address(q,k) + forward with undo log + backward (dq, dk, dv, dalpha, dbeta, dM0)",
+            "kernels_ms": {n: round(v[0] / max(v[1], 1), 4) for n, v in kern.items()},
+        }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

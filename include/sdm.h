@@ -1,0 +1,208 @@
+/*
+ * sdm.h — C ABI of the Sparse Delta Memory (SDM) hot path on MI355X (gfx950).
+ *
+ * Paper: "Sparse Delta Memory", arXiv 2607.07386.  The layer keeps, per
+ * (batch, head) stream, an explicit memory table M of N slots x d_v values.
+ * Each token selects W write slots and R read slots by product-key
+ * addressing, applies a gated delta-rule write to the W rows only, and reads
+ * a weighted sum of the R rows (Sec. 3.1, Eqs. sdm-decay, sdm-write,
+ * sdm-read).
+ *
+ * Conventions shared by every entry point
+ *   - All tensor arguments are DEVICE pointers, contiguous row-major with the
+ *     innermost dimension last, at least 16-byte aligned.  Offsets are 64-bit.
+ *   - The caller owns every buffer.  The library allocates no device memory;
+ *     buffers it needs beyond inputs and outputs come in as `workspace`, sized
+ *     by the matching *_workspace_bytes() call.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  A return of
+ *     SDM_OK means the work was enqueued on it; completion is asynchronous.
+ *   - Arguments are validated on the host before anything is launched.  On
+ *     any error nothing is launched, no output is touched, the call returns a
+ *     negative status and sdm_last_error() (thread-local) describes it.  No
+ *     entry point prints, throws or aborts.
+ *   - Entry points are stateless and reentrant; calls on different streams
+ *     may run concurrently if their buffers do not overlap.
+ *   - dtype codes: SDM_F32 (IEEE fp32) or SDM_BF16 (bfloat16).  Memory
+ *     tables, outputs and gradients are always fp32.
+ */
+#ifndef SDM_H_
+#define SDM_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum sdm_dtype { SDM_F32 = 0, SDM_BF16 = 1 };
+
+enum sdm_status {
+    SDM_OK = 0,
+    SDM_ERR_INVALID_ARG = -1,   /* a size, pointer or alignment rule is violated */
+    SDM_ERR_UNSUPPORTED = -2,   /* legal, but outside what the kernels implement */
+    SDM_ERR_WORKSPACE = -3,     /* workspace / saved buffer too small */
+    SDM_ERR_HIP = -4,           /* a HIP runtime call failed (launch, attribute) */
+    SDM_ERR_DEVICE_CHECK = -5   /* a device-side index check found a bad slot id */
+};
+
+/* ------------------------------------------------------------------------
+ * sdm_address — product-key addressing of one side (write keys or read
+ * queries).  Sec. 2 "Product Key Memory" and Sec. 3.1 step 1: the projected
+ * vector is split into two halves that give two score vectors s0, s1 of
+ * length sqrt(N); slot (a, b) scores s0[a] + s1[b] and has flat id
+ * a*sqrt(N) + b; the top-k slots are found through
+ * top_k(s0 (+) s1) = top_k(top_k(s0) (+) top_k(s1)).  The weights are the
+ * softmax of the selected scores (Sec. 4 "SDM Configuration") and the
+ * selected ids are returned sorted ascending (App. A.2).
+ *
+ *   x         [B, H, T, d_k] in x_dtype: the projected keys (write side) or
+ *             queries (read side).
+ *   codebook  [H, 2, sqrt(N), d_k/2] in x_dtype: per-head sub-key codebooks;
+ *             s_h[j] = <x[h*d_k/2 : (h+1)*d_k/2], codebook[head][h][j]>.
+ *             NULL selects direct mode, which needs d_k == 2*sqrt(N) and takes
+ *             s0 = x[0:sqrt(N)], s1 = x[sqrt(N):2*sqrt(N)] as the scores.
+ *   N         slots per head; must be a perfect square, sqrt(N) <= 1024.
+ *   topk      slots selected per token, 1 <= topk <= min(sqrt(N), 64).
+ *   idx       out [B, H, T, topk] int32: selected slot ids, ascending.
+ *   val       out [B, H, T, topk] fp32: softmax weights, in idx order.
+ *   score     optional out [B, H, T, topk] fp32: the raw selected scores.
+ * Ranking: score descending, ties to the lower flat id.  Scores are formed
+ * in fp32 (bf16 products accumulated in fp32 on the matrix cores).
+ * Codebook mode needs d_k even and d_k/2 <= 256.
+ * ---------------------------------------------------------------------- */
+int sdm_address(const void* x, int x_dtype, const void* codebook,
+                int B, int H, int T, int d_k, int64_t N, int topk,
+                int32_t* idx, float* val, float* score, void* stream);
+
+/* ------------------------------------------------------------------------
+ * sdm_scan_fwd — the sparse gated delta recurrence, in place on the memory
+ * table.  For every (b, h) stream and t = 0 .. T-1 (Sec. 3.1 steps 2-3):
+ *   P_n = M[i_n]                  the W write rows as left by step t-1
+ *   D_n = alpha_t P_n             Eq. (sdm-decay), written rows only
+ *   u   = sum_n kappa_n D_n       read-back of the decayed rows (Fig. 2)
+ *   e   = beta_t (v_t - u)
+ *   M[i_n] = D_n + kappa_n e      Eq. (sdm-write)
+ *   y_t = sum_m rho_m M[j_m]      Eq. (sdm-read) on the post-write memory
+ * Slots outside the write set are left bit-for-bit unchanged.
+ *
+ *   w_idx, w_val  [B, H, T, W] int32 / fp32: write slots i_n, weights kappa_n.
+ *   r_idx, r_val  [B, H, T, R] int32 / fp32: read slots j_m, weights rho_m.
+ *                 Any weights are accepted (not only softmax outputs).  Slot
+ *                 ids must lie in [0, N) and be distinct within a token; out of
+ *                 range ids are clamped on the device (never dereferenced out
+ *                 of bounds) and reported by sdm_check_device_errors().
+ *   v             [B, H, T, d_v] in in_dtype.
+ *   alpha, beta   [B, H, T] in in_dtype: forget and input gates.
+ *   mem           [B, H, N, d_v] fp32, in: M_0, out: M_T.
+ *   y             out [B, H, T, d_v] fp32.
+ *   saved         NULL for inference.  For training, out
+ *                 [B, H, T, W, d_v] fp32: the pre-write rows P of every token
+ *                 (the undo log of App. A.3); saved_bytes must be at least
+ *                 sdm_scan_saved_bytes().
+ *   workspace     at least sdm_scan_fwd_workspace_bytes() bytes, 256-B aligned.
+ * Limits: 1 <= W, R <= 64; d_v % 4 == 0; d_v <= 4096; T == 0 is a no-op.
+ * ---------------------------------------------------------------------- */
+int sdm_scan_fwd(const int32_t* w_idx, const float* w_val, int W,
+                 const int32_t* r_idx, const float* r_val, int R,
+                 const void* v, const void* alpha, const void* beta, int in_dtype,
+                 float* mem, int B, int H, int T, int d_v, int64_t N,
+                 float* y, float* saved, size_t saved_bytes,
+                 void* workspace, size_t ws_bytes, void* stream);
+
+size_t sdm_scan_fwd_workspace_bytes(int B, int H, int T, int W, int R);
+size_t sdm_scan_saved_bytes(int B, int H, int T, int W, int d_v);
+
+/* ------------------------------------------------------------------------
+ * sdm_scan_bwd — reverse mode of sdm_scan_fwd plus the addressing gradient.
+ * Past memory states are recovered by undoing the in-place writes from the
+ * saved pre-write rows (App. A.3); per token the forward intermediates
+ * (D_n, u, e) are recomputed from those rows.  Per stream, t = T-1 .. 0,
+ * with G the adjoint of the memory (initialised from dmem_T):
+ *   read    rbar_m = <dy_t, M_t[j_m]>;  G[j_m] += rho_m dy_t
+ *   write   g_n = G[i_n]; ebar = sum_n kappa_n g_n; dv_t = beta ebar;
+ *           dbeta_t = <ebar, v_t - u>; kbar_n = <g_n, e> - beta <ebar, D_n>;
+ *           Dbar_n = g_n - beta kappa_n ebar; dalpha_t = sum_n <Dbar_n, P_n>;
+ *           G[i_n] = alpha Dbar_n
+ *   undo    M[i_n] = P_n
+ * The weight gradients then pass through the softmax and the product-key
+ * scores to the projected vectors (the selection itself has no gradient):
+ *   sbar_n = w_n (wbar_n - sum_m w_m wbar_m); s0bar[a] += sbar_n,
+ *   s1bar[b] += sbar_n; xbar_h = sum_j shbar[j] codebook[h][j]
+ *   (direct mode: xbar = [s0bar, s1bar]).
+ *
+ *   cb_q, cb_k    codebooks of the read / write side ([H,2,sqrt(N),d_k/2]
+ *                 in cb_dtype) or NULL for direct mode; may be the same pointer.
+ *   w_idx .. beta, in_dtype, W, R, N, d_v: exactly as given to sdm_scan_fwd.
+ *   mem           in: M_T (as left by sdm_scan_fwd), out: M_0, bit-exact.
+ *   saved         the buffer filled by sdm_scan_fwd.
+ *   dy            [B, H, T, d_v] fp32: gradient of y.
+ *   dmem_T        optional [B, H, N, d_v] fp32 gradient of M_T (NULL = 0).
+ *                 May alias dmem0.
+ *   chunk         tokens per backward chunk (> 0); results do not depend on it.
+ *   dq, dk        optional out [B, H, T, d_k] fp32 (NULL = not computed).
+ *   dv            out [B, H, T, d_v] fp32.
+ *   dalpha, dbeta out [B, H, T] fp32.
+ *   dmem0         out [B, H, N, d_v] fp32: gradient of M_0.
+ *   dw_val, dr_val optional out [B, H, T, W] / [B, H, T, R] fp32.
+ *   workspace     at least sdm_scan_bwd_workspace_bytes() bytes, 256-B aligned.
+ * ---------------------------------------------------------------------- */
+int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k,
+                 const int32_t* w_idx, const float* w_val, int W,
+                 const int32_t* r_idx, const float* r_val, int R,
+                 const void* v, const void* alpha, const void* beta, int in_dtype,
+                 float* mem, const float* saved, size_t saved_bytes,
+                 const float* dy, const float* dmem_T, int chunk,
+                 int B, int H, int T, int d_v, int64_t N,
+                 float* dq, float* dk, float* dv, float* dalpha, float* dbeta,
+                 float* dmem0, float* dw_val, float* dr_val,
+                 void* workspace, size_t ws_bytes, void* stream);
+
+size_t sdm_scan_bwd_workspace_bytes(int B, int H, int T, int W, int R, int d_v);
+
+/* ------------------------------------------------------------------------
+ * sdm_mem_init — initial memory per call.  The learned initial state M_0 of
+ * Sec. 3.1 ("Learned Initial State") is one [H, N, d_v] parameter shared by
+ * all sequences; every sequence starts from its own copy:
+ *   dst[b, h] = m0[h] for every b   (m0 != NULL)
+ *   dst = 0                         (m0 == NULL)
+ *   dst  out [B, H, N, d_v] fp32;  m0  [H, N, d_v] fp32 or NULL.
+ * ---------------------------------------------------------------------- */
+int sdm_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int d_v, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Per-kernel timing with HIP events, off by default.  While enabled, every
+ * kernel the library launches is bracketed by two HIP events recorded on the
+ * stream it is launched on; sdm_profile_read() waits for the recorded events
+ * and returns the summed elapsed time and launch count of one kernel kind
+ * since the last sdm_profile_enable(1).  Events come from a pool that is
+ * grown on first use and reused afterwards.  Not meant for concurrent use
+ * from several host threads.
+ * ---------------------------------------------------------------------- */
+enum sdm_kernel {
+    SDM_K_ADDRESS = 0, SDM_K_FWD_PREP = 1, SDM_K_FWD_SCAN = 2, SDM_K_BWD_PREP = 3,
+    SDM_K_BWD_SCAN = 4, SDM_K_BWD_REDUCE = 5, SDM_K_ADDRESS_BWD = 6, SDM_K_MEM_INIT = 7,
+    SDM_K_COUNT = 8
+};
+int sdm_profile_enable(int on);
+int sdm_profile_read(int kernel, double* total_ms, int64_t* launches);
+
+/* ------------------------------------------------------------------------
+ * Diagnostics.
+ *   sdm_check_device_errors  synchronises `stream`, then reports whether
+ *       any scan since the last check clamped an out-of-range slot id
+ *       (SDM_ERR_DEVICE_CHECK) and clears the flag held in `workspace`.
+ *   sdm_status_string        static text for a status code.
+ *   sdm_last_error           thread-local text of the last failure.
+ *   sdm_version              library version string.
+ * ---------------------------------------------------------------------- */
+int sdm_check_device_errors(void* workspace, void* stream);
+const char* sdm_status_string(int status);
+const char* sdm_last_error(void);
+const char* sdm_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SDM_H_ */

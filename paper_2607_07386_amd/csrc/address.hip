@@ -1,0 +1,378 @@
+// Product-key addressing (Sec. 2 "Product Key Memory", Sec. 3.1 step 1,
+// Sec. 4 softmax-normalised activations, App. A.2 sort-by-index) and its
+// backward, for gfx950.
+//
+// One workgroup = 4 waves = a tile of 16 tokens of one (b, h) stream.
+//  A. sub-key scores of the tile into LDS: bf16 codebooks on the matrix
+//     cores (v_mfma_f32_16x16x32_bf16: 16 tokens x 16 sub-keys x 32 deep),
+//     fp32 codebooks with plain FMAs, direct mode by copying x.
+//  B. per token (one wave): top-k of each half under (score desc, id asc)
+//     by bisection of the k-th largest order-preserving key with wave
+//     ballots, then the shortlist ranked by the same order.
+//  C. candidates (i, j) of the two ranked shortlists with (i+1)(j+1) <= k
+//     (every other pair has >= k pairs ranked above it), bisection again,
+//     ties to the lower flat id, then sort by id and softmax.
+#include "sdm_common.h"
+#include "sdm_internal.h"
+
+namespace {
+
+constexpr int ATILE = 16;     // tokens per workgroup
+constexpr int AWAVES = 4;
+constexpr int MAXK = 64;
+constexpr int MAXCAND_E = 5;  // ceil(303 / 64): pruned candidates for k <= 64
+
+struct Entry {
+    float score;
+    int id;
+};
+
+// k-th largest key: the largest tau with #{key >= tau} >= k.
+template <int E>
+__device__ uint32_t kth_key(const uint32_t (&key)[E], int k) {
+    uint32_t tau = 0u;
+    for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t cand = tau | (1u << bit);
+        int cnt = 0;
+#pragma unroll
+        for (int e = 0; e < E; ++e) cnt += popc64(__ballot(key[e] >= cand));
+        if (cnt >= k) tau = cand;
+    }
+    return tau;
+}
+
+// Mark the k selected elements: keys above tau, then keys equal to tau in
+// increasing id until k are taken.  Invalid elements carry key 0 and id
+// INT_MAX and are never taken (all valid keys are > 0).
+template <int E>
+__device__ void select_topk(const uint32_t (&key)[E], const int (&id)[E], int k, bool (&sel)[E]) {
+    const uint32_t tau = kth_key<E>(key, k);
+    int n_gt = 0, n_eq = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        n_gt += popc64(__ballot(key[e] > tau));
+        n_eq += popc64(__ballot(key[e] == tau));
+    }
+    const int need = k - n_gt;
+    if (n_eq == need) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) sel[e] = key[e] >= tau;
+        return;
+    }
+#pragma unroll
+    for (int e = 0; e < E; ++e) sel[e] = key[e] > tau;
+    for (int r = 0; r < need; ++r) {
+        int best = 0x7fffffff;
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            if (key[e] == tau && !sel[e]) best = min(best, id[e]);
+        best = wave_min_i(best);
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            if (key[e] == tau && id[e] == best) sel[e] = true;
+    }
+}
+
+// Write the selected (score, id) pairs, in element order, to buf[0 .. k).
+template <int E>
+__device__ void compact(const bool (&sel)[E], const float (&sc)[E], const int (&id)[E], Entry* buf) {
+    int base = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const unsigned long long m = __ballot(sel[e]);
+        if (sel[e]) {
+            const int p = base + mbcnt64(m);
+            buf[p].score = sc[e];
+            buf[p].id = id[e];
+        }
+        base += popc64(m);
+    }
+}
+
+// Stage-1 selection of one half: top-k of s sub-scores, ranked (score desc,
+// id asc) into out[0 .. k).
+template <int E>
+__device__ void half_topk(const float* sc_row, int s, int k, Entry* scratch, Entry* out) {
+    const int lane = lane_id();
+    uint32_t key[E];
+    float sc[E];
+    int id[E];
+    bool sel[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int g = e * SDM_WAVE + lane;
+        const bool ok = g < s;
+        sc[e] = ok ? sc_row[g] : 0.f;
+        key[e] = ok ? ord_key(sc[e]) : 0u;
+        id[e] = ok ? g : 0x7fffffff;
+    }
+    select_topk<E>(key, id, k, sel);
+    compact<E>(sel, sc, id, scratch);
+    wait_lds();
+    if (lane < k) {
+        const Entry me = scratch[lane];
+        const uint32_t mk = ord_key(me.score);
+        int rank = 0;
+        for (int j = 0; j < k; ++j) {
+            const Entry o = scratch[j];
+            const uint32_t ok = ord_key(o.score);
+            rank += (ok > mk) || (ok == mk && o.id < me.id);
+        }
+        out[rank] = me;
+    }
+    wait_lds();
+}
+
+template <typename XT, int MODE, int E>   // MODE 0: direct, 1: codebook FMA, 2: codebook MFMA (bf16)
+__global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restrict__ x,
+                                                            const XT* __restrict__ cb, int H, int T,
+                                                            int dk, int s, int k,
+                                                            int32_t* __restrict__ idx,
+                                                            float* __restrict__ val,
+                                                            float* __restrict__ score) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    float* scores = reinterpret_cast<float*>(smem);                          // [ATILE][2*s]
+    Entry* scratch = reinterpret_cast<Entry*>(scores + (size_t)ATILE * 2 * s);  // [AWAVES][3][MAXK]
+    uint32_t* pairs = reinterpret_cast<uint32_t*>(scratch + AWAVES * 3 * MAXK);  // [ncand]
+    __shared__ int s_ncand;
+
+    const int stream = blockIdx.y;
+    const int h = stream % H;
+    const int t0 = blockIdx.x * ATILE;
+    const int tid = threadIdx.x;
+    const int wave = tid / SDM_WAVE;
+    const int lane = lane_id();
+    const XT* xs = x + ((size_t)stream * T) * dk;
+
+    // pair table of the pruned stage-2 candidates
+    if (tid < k) {
+        int off = 0;
+        for (int i = 0; i < tid; ++i) off += k / (i + 1);
+        const int cnt = k / (tid + 1);
+        for (int j = 0; j < cnt; ++j) pairs[off + j] = ((uint32_t)tid << 16) | (uint32_t)j;
+        if (tid == k - 1) s_ncand = off + cnt;
+    }
+
+    // ---- A: sub-scores of the 16-token tile -------------------------------
+    if constexpr (MODE == 0) {
+        for (int i = tid; i < ATILE * 2 * s; i += blockDim.x) {
+            const int tt = i / (2 * s), j = i % (2 * s);
+            const int t = t0 + tt;
+            scores[i] = t < T ? to_f32(xs[(size_t)t * dk + j]) : 0.f;
+        }
+    } else if constexpr (MODE == 1) {
+        const int dh = dk / 2;
+        const XT* cbh = cb + (size_t)h * 2 * s * dh;
+        for (int i = tid; i < ATILE * 2 * s; i += blockDim.x) {
+            const int tt = i / (2 * s), hj = i % (2 * s);
+            const int half = hj / s, j = hj % s;
+            const int t = t0 + tt;
+            float acc = 0.f;
+            if (t < T) {
+                const XT* xr = xs + (size_t)t * dk + half * dh;
+                const XT* cr = cbh + ((size_t)half * s + j) * dh;
+                for (int c = 0; c < dh; ++c) acc = fmaf(to_f32(xr[c]), to_f32(cr[c]), acc);
+            }
+            scores[i] = acc;
+        }
+    } else {
+        // MFMA 16x16x32: A[i][kk] = x[t0+i][half*dh + kk], B[kk][j] = cb[half][j0+j][kk].
+        // Lane l supplies row/col (l % 16) and k-slice 8*(l/16) .. +7 of each 32-deep step;
+        // result acc[v] is D[4*(l/16) + v][l % 16].
+        const int dh = dk / 2;
+        const XT* cbh = cb + (size_t)h * 2 * s * dh;
+        const int ntile = (s + 15) / 16;
+        const int r16 = lane % 16, q = lane / 16;
+        const int t = t0 + r16;
+        for (int job = wave; job < 2 * ntile; job += AWAVES) {
+            const int half = job / ntile;
+            const int j0 = (job % ntile) * 16;
+            const int j = j0 + r16;
+            sdm_f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            for (int kk = 0; kk < dh; kk += 32) {
+                const int kc = kk + 8 * q;
+                sdm_bf16x8 a, b;
+                if (t < T && kc < dh)
+                    a = *reinterpret_cast<const sdm_bf16x8*>(xs + (size_t)t * dk + half * dh + kc);
+                else
+                    a = sdm_bf16x8{};
+                if (j < s && kc < dh)
+                    b = *reinterpret_cast<const sdm_bf16x8*>(cbh + ((size_t)half * s + j) * dh + kc);
+                else
+                    b = sdm_bf16x8{};
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
+            }
+            if (j < s) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) scores[(size_t)(4 * q + v) * 2 * s + half * s + j] = acc[v];
+            }
+        }
+    }
+    __syncthreads();
+
+    // ---- B, C: one wave per token --------------------------------------
+    const int ncand = s_ncand;
+    Entry* scr = scratch + wave * 3 * MAXK;
+    Entry* listA = scr + MAXK;
+    Entry* listB = scr + 2 * MAXK;
+    for (int tt = wave; tt < ATILE; tt += AWAVES) {
+        const int t = t0 + tt;
+        if (t >= T) break;
+        const float* row = scores + (size_t)tt * 2 * s;
+        half_topk<E>(row, s, k, scr, listA);
+        half_topk<E>(row + s, s, k, scr, listB);
+
+        uint32_t key[MAXCAND_E];
+        float sc[MAXCAND_E];
+        int id[MAXCAND_E];
+        bool sel[MAXCAND_E];
+#pragma unroll
+        for (int e = 0; e < MAXCAND_E; ++e) {
+            const int c = e * SDM_WAVE + lane;
+            if (c < ncand) {
+                const uint32_t pr = pairs[c];
+                const Entry a = listA[pr >> 16], b = listB[pr & 0xffffu];
+                sc[e] = a.score + b.score;
+                key[e] = ord_key(sc[e]);
+                id[e] = a.id * s + b.id;
+            } else {
+                sc[e] = 0.f;
+                key[e] = 0u;
+                id[e] = 0x7fffffff;
+            }
+        }
+        select_topk<MAXCAND_E>(key, id, k, sel);
+        compact<MAXCAND_E>(sel, sc, id, scr);
+        wait_lds();
+        float my_sc = -INFINITY;
+        int my_id = 0, rank = 0;
+        if (lane < k) {
+            my_sc = scr[lane].score;
+            my_id = scr[lane].id;
+            for (int j = 0; j < k; ++j) rank += scr[j].id < my_id;
+        }
+        const float mx = wave_max(my_sc);
+        const float ex = lane < k ? expf(my_sc - mx) : 0.f;
+        const float z = wave_sum(ex);
+        if (lane < k) {
+            const size_t o = ((size_t)stream * T + t) * k + rank;
+            idx[o] = my_id;
+            val[o] = ex / z;
+            if (score) score[o] = my_sc;
+        }
+        wait_lds();
+    }
+}
+
+// Backward of the weights through softmax and the sub-key scores: one wave
+// per token, lanes over the d_k outputs.
+template <typename XT, bool CODEBOOK>
+__global__ __launch_bounds__(256) void address_bwd_kernel(const XT* __restrict__ cb, int H, int T,
+                                                          int dk, int s, int k,
+                                                          const int32_t* __restrict__ idx,
+                                                          const float* __restrict__ val,
+                                                          const float* __restrict__ dval,
+                                                          float* __restrict__ dx, int64_t ntok) {
+    const int lane = lane_id();
+    const int64_t r = (int64_t)blockIdx.x * (blockDim.x / SDM_WAVE) + threadIdx.x / SDM_WAVE;
+    if (r >= ntok) return;
+    const int h = (int)((r / T) % H);
+    const int32_t* I = idx + r * k;
+    const float* w = val + r * k;
+    const float* wb = dval + r * k;
+    float p = 0.f;
+    for (int n = lane; n < k; n += SDM_WAVE) p = fmaf(w[n], wb[n], p);
+    const float dot = wave_sum(p);
+    float* out = dx + r * dk;
+    if constexpr (CODEBOOK) {
+        const int dh = dk / 2;
+        const XT* cbh = cb + (size_t)h * 2 * s * dh;
+        for (int c = lane; c < dk; c += SDM_WAVE) {
+            const int half = c / dh, cc = c % dh;
+            float acc = 0.f;
+            for (int n = 0; n < k; ++n) {
+                const float g = w[n] * (wb[n] - dot);
+                const int id = min(max(I[n], 0), s * s - 1);   // never read outside the codebook
+                const int sub = half ? (id % s) : (id / s);
+                acc = fmaf(g, to_f32(cbh[((size_t)half * s + sub) * dh + cc]), acc);
+            }
+            out[c] = acc;
+        }
+    } else {
+        for (int c = lane; c < dk; c += SDM_WAVE) {
+            const int half = c / s, j = c % s;
+            float acc = 0.f;
+            for (int n = 0; n < k; ++n) {
+                const int sub = half ? (I[n] % s) : (I[n] / s);
+                if (sub == j) acc += w[n] * (wb[n] - dot);
+            }
+            out[c] = acc;
+        }
+    }
+}
+
+template <typename XT, int MODE>
+hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, int dk, int s,
+                            int k, int32_t* idx, float* val, float* score, hipStream_t st) {
+    const int E = (s + SDM_WAVE - 1) / SDM_WAVE;
+    dim3 grid((T + ATILE - 1) / ATILE, B * H);
+    const size_t sm = (size_t)ATILE * 2 * s * sizeof(float) + AWAVES * 3 * MAXK * sizeof(Entry) +
+                      320 * sizeof(uint32_t);
+    const XT* xp = static_cast<const XT*>(x);
+    const XT* cp = static_cast<const XT*>(cb);
+#define SDM_ADDR_CASE(EE)                                                                       \
+    {                                                                                           \
+        auto kfn = address_kernel<XT, MODE, EE>;                                                \
+        hipError_t e = hipFuncSetAttribute((const void*)kfn,                                    \
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm); \
+        if (e != hipSuccess) return e;                                                          \
+        hipLaunchKernelGGL(kfn, grid, dim3(ATILE * 16), sm, st, xp, cp, H, T, dk, s, k, idx,    \
+                           val, score);                                                         \
+        return hipGetLastError();                                                               \
+    }
+    if (E <= 1) SDM_ADDR_CASE(1)
+    if (E <= 2) SDM_ADDR_CASE(2)
+    if (E <= 4) SDM_ADDR_CASE(4)
+    if (E <= 8) SDM_ADDR_CASE(8)
+    SDM_ADDR_CASE(16)
+#undef SDM_ADDR_CASE
+}
+
+}  // namespace
+
+hipError_t sdm_launch_address(const void* x, int x_dtype, const void* cb, int B, int H, int T,
+                              int dk, int s, int k, int32_t* idx, float* val, float* score,
+                              hipStream_t st) {
+    if (x_dtype == SDM_DT_BF16) {
+        if (!cb) return launch_address_e<bf16_t, 0>(x, cb, B, H, T, dk, s, k, idx, val, score, st);
+        if ((dk / 2) % 8 == 0)
+            return launch_address_e<bf16_t, 2>(x, cb, B, H, T, dk, s, k, idx, val, score, st);
+        return launch_address_e<bf16_t, 1>(x, cb, B, H, T, dk, s, k, idx, val, score, st);
+    }
+    if (!cb) return launch_address_e<float, 0>(x, cb, B, H, T, dk, s, k, idx, val, score, st);
+    return launch_address_e<float, 1>(x, cb, B, H, T, dk, s, k, idx, val, score, st);
+}
+
+hipError_t sdm_launch_address_bwd(const void* cb, int cb_dtype, int B, int H, int T, int dk, int s,
+                                  int k, const int32_t* idx, const float* val, const float* dval,
+                                  float* dx, hipStream_t st) {
+    const int64_t ntok = (int64_t)B * H * T;
+    if (ntok == 0) return hipSuccess;
+    dim3 grid((unsigned)((ntok + 3) / 4));
+    if (cb_dtype == SDM_DT_BF16) {
+        if (cb)
+            hipLaunchKernelGGL((address_bwd_kernel<bf16_t, true>), grid, dim3(256), 0, st,
+                               static_cast<const bf16_t*>(cb), H, T, dk, s, k, idx, val, dval, dx, ntok);
+        else
+            hipLaunchKernelGGL((address_bwd_kernel<bf16_t, false>), grid, dim3(256), 0, st,
+                               static_cast<const bf16_t*>(cb), H, T, dk, s, k, idx, val, dval, dx, ntok);
+    } else {
+        if (cb)
+            hipLaunchKernelGGL((address_bwd_kernel<float, true>), grid, dim3(256), 0, st,
+                               static_cast<const float*>(cb), H, T, dk, s, k, idx, val, dval, dx, ntok);
+        else
+            hipLaunchKernelGGL((address_bwd_kernel<float, false>), grid, dim3(256), 0, st,
+                               static_cast<const float*>(cb), H, T, dk, s, k, idx, val, dval, dx, ntok);
+    }
+    return hipGetLastError();
+}

@@ -1,0 +1,348 @@
+// C ABI of the SDM hot path: host-side validation, workspace sizing and
+// launch on the caller's stream.  Declarations and contracts: include/sdm.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "../../include/sdm.h"
+#include "sdm_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int status, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return status;
+}
+
+int hip_fail(hipError_t e, const char* where) {
+    return fail(SDM_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int isqrt64(int64_t n) {
+    if (n <= 0) return -1;
+    int64_t s = (int64_t)std::llround(std::sqrt((double)n));
+    while (s * s > n) --s;
+    while ((s + 1) * (s + 1) <= n) ++s;
+    return s * s == n ? (int)s : -1;
+}
+
+bool valid_dtype(int d) { return d == SDM_F32 || d == SDM_BF16; }
+
+constexpr int kMaxStreams = 65535;
+
+int check_scan_common(const int32_t* w_idx, const float* w_val, int W, const int32_t* r_idx,
+                      const float* r_val, int R, const void* v, const void* alpha,
+                      const void* beta, int in_dtype, const float* mem, int B, int H, int T,
+                      int d_v, int64_t N) {
+    if (B < 0 || H < 0 || T < 0) return fail(SDM_ERR_INVALID_ARG, "B, H, T must be >= 0");
+    if ((int64_t)B * H > kMaxStreams) return fail(SDM_ERR_UNSUPPORTED, "B*H must be <= %d", kMaxStreams);
+    if (W < 1 || R < 1) return fail(SDM_ERR_INVALID_ARG, "W and R must be >= 1");
+    if (W > 64 || R > 64) return fail(SDM_ERR_UNSUPPORTED, "W and R must be <= 64");
+    if (d_v < 4 || d_v % 4 != 0) return fail(SDM_ERR_INVALID_ARG, "d_v must be a positive multiple of 4");
+    if (d_v > 4096) return fail(SDM_ERR_UNSUPPORTED, "d_v must be <= 4096");
+    if (N < 1 || N > (int64_t)1 << 31) return fail(SDM_ERR_INVALID_ARG, "N must be in [1, 2^31]");
+    if (!valid_dtype(in_dtype)) return fail(SDM_ERR_INVALID_ARG, "in_dtype must be SDM_F32 or SDM_BF16");
+    if (!w_idx || !w_val || !r_idx || !r_val || !v || !alpha || !beta || !mem)
+        return fail(SDM_ERR_INVALID_ARG, "null input pointer");
+    if (!aligned(w_idx, 16) || !aligned(w_val, 16) || !aligned(r_idx, 16) || !aligned(r_val, 16) ||
+        !aligned(v, 16) || !aligned(alpha, 4) || !aligned(beta, 4) || !aligned(mem, 16))
+        return fail(SDM_ERR_INVALID_ARG, "misaligned pointer (16-byte alignment required)");
+    return SDM_OK;
+}
+
+// ---- event profiler ----
+struct ProfState {
+    std::mutex mu;
+    bool on = false;
+    std::vector<hipEvent_t> pool;                 // free events
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> done[SDM_K_COUNT];
+    hipEvent_t open_ev[SDM_K_COUNT] = {};
+};
+ProfState& prof() {
+    static ProfState p;
+    return p;
+}
+hipEvent_t take_event(ProfState& p) {
+    if (!p.pool.empty()) {
+        hipEvent_t e = p.pool.back();
+        p.pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+}  // namespace
+
+void sdm_prof_begin(int k, hipStream_t st) {
+    ProfState& p = prof();
+    if (!p.on) return;
+    std::lock_guard<std::mutex> g(p.mu);
+    hipEvent_t e = take_event(p);
+    if (e && hipEventRecord(e, st) == hipSuccess) p.open_ev[k] = e;
+}
+
+void sdm_prof_end(int k, hipStream_t st) {
+    ProfState& p = prof();
+    if (!p.on) return;
+    std::lock_guard<std::mutex> g(p.mu);
+    hipEvent_t b = p.open_ev[k];
+    p.open_ev[k] = nullptr;
+    if (!b) return;
+    hipEvent_t e = take_event(p);
+    if (e && hipEventRecord(e, st) == hipSuccess) p.done[k].push_back({b, e});
+}
+
+extern "C" {
+
+int sdm_profile_enable(int on) {
+    ProfState& p = prof();
+    std::lock_guard<std::mutex> g(p.mu);
+    for (int k = 0; k < SDM_K_COUNT; ++k) {
+        for (auto& pr : p.done[k]) {
+            (void)hipEventSynchronize(pr.second);
+            p.pool.push_back(pr.first);
+            p.pool.push_back(pr.second);
+        }
+        p.done[k].clear();
+    }
+    p.on = on != 0;
+    return SDM_OK;
+}
+
+int sdm_profile_read(int kernel, double* total_ms, int64_t* launches) {
+    g_err[0] = 0;
+    if (kernel < 0 || kernel >= SDM_K_COUNT || !total_ms || !launches)
+        return fail(SDM_ERR_INVALID_ARG, "bad kernel id or null output");
+    ProfState& p = prof();
+    std::lock_guard<std::mutex> g(p.mu);
+    double tot = 0.0;
+    for (auto& pr : p.done[kernel]) {
+        hipError_t e = hipEventSynchronize(pr.second);
+        float ms = 0.f;
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, pr.first, pr.second);
+        if (e != hipSuccess) return hip_fail(e, "sdm_profile_read");
+        tot += ms;
+    }
+    *total_ms = tot;
+    *launches = (int64_t)p.done[kernel].size();
+    return SDM_OK;
+}
+
+
+const char* sdm_version(void) { return "sdm-mi355x 0.1 (gfx950)"; }
+
+const char* sdm_last_error(void) { return g_err; }
+
+const char* sdm_status_string(int status) {
+    switch (status) {
+        case SDM_OK: return "ok";
+        case SDM_ERR_INVALID_ARG: return "invalid argument";
+        case SDM_ERR_UNSUPPORTED: return "unsupported configuration";
+        case SDM_ERR_WORKSPACE: return "workspace or saved buffer too small";
+        case SDM_ERR_HIP: return "HIP runtime error";
+        case SDM_ERR_DEVICE_CHECK: return "device-side index check failed";
+        default: return "unknown status";
+    }
+}
+
+int sdm_address(const void* x, int x_dtype, const void* codebook, int B, int H, int T, int d_k,
+                int64_t N, int topk, int32_t* idx, float* val, float* score, void* stream) {
+    g_err[0] = 0;
+    if (B < 0 || H < 0 || T < 0) return fail(SDM_ERR_INVALID_ARG, "B, H, T must be >= 0");
+    if ((int64_t)B * H > kMaxStreams) return fail(SDM_ERR_UNSUPPORTED, "B*H must be <= %d", kMaxStreams);
+    if (!valid_dtype(x_dtype)) return fail(SDM_ERR_INVALID_ARG, "x_dtype must be SDM_F32 or SDM_BF16");
+    const int s = isqrt64(N);
+    if (s < 0) return fail(SDM_ERR_INVALID_ARG, "N=%lld is not a perfect square", (long long)N);
+    if (s > 1024) return fail(SDM_ERR_UNSUPPORTED, "sqrt(N) must be <= 1024");
+    if (topk < 1 || topk > s) return fail(SDM_ERR_INVALID_ARG, "topk must be in [1, sqrt(N)]");
+    if (topk > 64) return fail(SDM_ERR_UNSUPPORTED, "topk must be <= 64");
+    if (d_k < 1) return fail(SDM_ERR_INVALID_ARG, "d_k must be >= 1");
+    if (codebook) {
+        if (d_k % 2) return fail(SDM_ERR_INVALID_ARG, "codebook mode needs an even d_k");
+        if (d_k / 2 > 256) return fail(SDM_ERR_UNSUPPORTED, "codebook mode needs d_k/2 <= 256");
+        if (!aligned(codebook, 16)) return fail(SDM_ERR_INVALID_ARG, "misaligned codebook");
+    } else if (d_k != 2 * s) {
+        return fail(SDM_ERR_INVALID_ARG, "direct mode needs d_k == 2*sqrt(N)");
+    }
+    if (!x || !idx || !val) return fail(SDM_ERR_INVALID_ARG, "null pointer");
+    if (!aligned(x, 16) || !aligned(idx, 4) || !aligned(val, 4) || (score && !aligned(score, 4)))
+        return fail(SDM_ERR_INVALID_ARG, "misaligned pointer");
+    if ((int64_t)B * H * T == 0) return SDM_OK;
+    hipError_t e;
+    {
+        SdmProfScope ps(SDM_K_ADDRESS, (hipStream_t)stream);
+        e = sdm_launch_address(x, x_dtype, codebook, B, H, T, d_k, s, topk, idx, val, score,
+                               (hipStream_t)stream);
+    }
+    if (e != hipSuccess) return hip_fail(e, "sdm_address launch");
+    return SDM_OK;
+}
+
+size_t sdm_scan_fwd_workspace_bytes(int B, int H, int T, int W, int R) {
+    if (B < 0 || H < 0 || T < 0 || W < 1 || R < 1) return 0;
+    return sdm_fwd_ws_bytes(B, H, T, W, R);
+}
+
+size_t sdm_scan_saved_bytes(int B, int H, int T, int W, int d_v) {
+    if (B < 0 || H < 0 || T < 0 || W < 0 || d_v < 0) return 0;
+    return (size_t)B * H * T * W * d_v * sizeof(float);
+}
+
+size_t sdm_scan_bwd_workspace_bytes(int B, int H, int T, int W, int R, int d_v) {
+    if (B < 0 || H < 0 || T < 0 || W < 1 || R < 1 || d_v < 1) return 0;
+    return sdm_bwd_ws_bytes(B, H, T, W, R, d_v);
+}
+
+int sdm_scan_fwd(const int32_t* w_idx, const float* w_val, int W, const int32_t* r_idx,
+                 const float* r_val, int R, const void* v, const void* alpha, const void* beta,
+                 int in_dtype, float* mem, int B, int H, int T, int d_v, int64_t N, float* y,
+                 float* saved, size_t saved_bytes, void* workspace, size_t ws_bytes, void* stream) {
+    g_err[0] = 0;
+    int rc = check_scan_common(w_idx, w_val, W, r_idx, r_val, R, v, alpha, beta, in_dtype, mem, B,
+                               H, T, d_v, N);
+    if (rc != SDM_OK) return rc;
+    if (!y || !aligned(y, 16)) return fail(SDM_ERR_INVALID_ARG, "y must be a 16-byte aligned pointer");
+    if (saved) {
+        if (!aligned(saved, 16)) return fail(SDM_ERR_INVALID_ARG, "misaligned saved buffer");
+        if (saved_bytes < sdm_scan_saved_bytes(B, H, T, W, d_v))
+            return fail(SDM_ERR_WORKSPACE, "saved buffer too small: %zu < %zu", saved_bytes,
+                        sdm_scan_saved_bytes(B, H, T, W, d_v));
+    }
+    const size_t need = sdm_fwd_ws_bytes(B, H, T, W, R);
+    if (!workspace || !aligned(workspace, 256))
+        return fail(SDM_ERR_INVALID_ARG, "workspace must be a 256-byte aligned pointer");
+    if (ws_bytes < need) return fail(SDM_ERR_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, need);
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e = sdm_launch_zero_words(workspace, 4, st);
+    if (e != hipSuccess) return hip_fail(e, "sdm_scan_fwd flag reset");
+    if ((int64_t)B * H * T == 0) return SDM_OK;
+    ScanFwdArgs a;
+    a.w_idx = w_idx; a.w_val = w_val; a.r_idx = r_idx; a.r_val = r_val;
+    a.v = v; a.alpha = alpha; a.beta = beta; a.in_dtype = in_dtype;
+    a.mem = mem; a.B = B; a.H = H; a.T = T; a.dv = d_v; a.W = W; a.R = R; a.N = N;
+    a.y = y; a.saved = saved; a.ws = static_cast<unsigned char*>(workspace);
+    e = sdm_launch_scan_fwd(a, st);
+    if (e != hipSuccess) return hip_fail(e, "sdm_scan_fwd launch");
+    return SDM_OK;
+}
+
+int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, const int32_t* w_idx,
+                 const float* w_val, int W, const int32_t* r_idx, const float* r_val, int R,
+                 const void* v, const void* alpha, const void* beta, int in_dtype, float* mem,
+                 const float* saved, size_t saved_bytes, const float* dy, const float* dmem_T,
+                 int chunk, int B, int H, int T, int d_v, int64_t N, float* dq, float* dk,
+                 float* dv, float* dalpha, float* dbeta, float* dmem0, float* dw_val,
+                 float* dr_val, void* workspace, size_t ws_bytes, void* stream) {
+    g_err[0] = 0;
+    int rc = check_scan_common(w_idx, w_val, W, r_idx, r_val, R, v, alpha, beta, in_dtype, mem, B,
+                               H, T, d_v, N);
+    if (rc != SDM_OK) return rc;
+    if (chunk < 1) return fail(SDM_ERR_INVALID_ARG, "chunk must be >= 1");
+    if (!saved || !dy || !dv || !dalpha || !dbeta || !dmem0)
+        return fail(SDM_ERR_INVALID_ARG, "null pointer (saved, dy, dv, dalpha, dbeta, dmem0 are required)");
+    if (!aligned(saved, 16) || !aligned(dy, 16) || !aligned(dv, 16) || !aligned(dmem0, 16) ||
+        (dmem_T && !aligned(dmem_T, 16)))
+        return fail(SDM_ERR_INVALID_ARG, "misaligned pointer (16-byte alignment required)");
+    if (saved_bytes < sdm_scan_saved_bytes(B, H, T, W, d_v))
+        return fail(SDM_ERR_WORKSPACE, "saved buffer too small");
+    const int s = isqrt64(N);
+    if (dq || dk) {
+        if (!valid_dtype(cb_dtype)) return fail(SDM_ERR_INVALID_ARG, "cb_dtype must be SDM_F32 or SDM_BF16");
+        if (s < 0) return fail(SDM_ERR_INVALID_ARG, "addressing gradients need a perfect-square N");
+        if (W > s || R > s) return fail(SDM_ERR_INVALID_ARG, "W, R must be <= sqrt(N) for addressing gradients");
+        if (dq && !cb_q && d_k != 2 * s) return fail(SDM_ERR_INVALID_ARG, "direct mode needs d_k == 2*sqrt(N)");
+        if (dk && !cb_k && d_k != 2 * s) return fail(SDM_ERR_INVALID_ARG, "direct mode needs d_k == 2*sqrt(N)");
+        if ((cb_q || cb_k) && (d_k % 2 || d_k < 2)) return fail(SDM_ERR_INVALID_ARG, "codebook mode needs an even d_k");
+    }
+    const size_t need = sdm_bwd_ws_bytes(B, H, T, W, R, d_v);
+    if (!workspace || !aligned(workspace, 256))
+        return fail(SDM_ERR_INVALID_ARG, "workspace must be a 256-byte aligned pointer");
+    if (ws_bytes < need) return fail(SDM_ERR_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, need);
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e = sdm_launch_zero_words(workspace, 4, st);
+    if (e != hipSuccess) return hip_fail(e, "sdm_scan_bwd flag reset");
+    // adjoint of the memory starts as dL/dM_T
+    const size_t memel = (size_t)B * H * N * d_v;
+    {
+        SdmProfScope ps(SDM_K_MEM_INIT, st);
+        if (dmem_T == nullptr)
+            e = sdm_launch_mem_init(dmem0, nullptr, B, H, N, d_v, st);
+        else if (dmem_T != dmem0)
+            e = sdm_launch_copy(dmem0, dmem_T, memel, st);
+    }
+    if (e != hipSuccess) return hip_fail(e, "sdm_scan_bwd adjoint init");
+    if ((int64_t)B * H * T == 0) return SDM_OK;
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    const size_t ST = (size_t)B * H * T;
+    float* spare = reinterpret_cast<float*>(ws + need - ST * (W + R) * sizeof(float));
+    ScanBwdArgs a;
+    a.w_idx = w_idx; a.w_val = w_val; a.r_idx = r_idx; a.r_val = r_val;
+    a.v = v; a.alpha = alpha; a.beta = beta; a.in_dtype = in_dtype;
+    a.mem = mem; a.saved = saved; a.dy = dy; a.chunk = chunk;
+    a.B = B; a.H = H; a.T = T; a.dv = d_v; a.W = W; a.R = R; a.N = N;
+    a.dv_out = dv; a.dalpha = dalpha; a.dbeta = dbeta; a.G = dmem0;
+    a.dw_val = dw_val ? dw_val : spare;
+    a.dr_val = dr_val ? dr_val : spare + ST * W;
+    a.ws = ws;
+    e = sdm_launch_scan_bwd(a, st);
+    if (e != hipSuccess) return hip_fail(e, "sdm_scan_bwd launch");
+    if (dq) {
+        SdmProfScope ps(SDM_K_ADDRESS_BWD, st);
+        e = sdm_launch_address_bwd(cb_q, cb_dtype, B, H, T, d_k, s, R, r_idx, r_val, a.dr_val, dq, st);
+        if (e != hipSuccess) return hip_fail(e, "sdm_scan_bwd dq");
+    }
+    if (dk) {
+        SdmProfScope ps(SDM_K_ADDRESS_BWD, st);
+        e = sdm_launch_address_bwd(cb_k, cb_dtype, B, H, T, d_k, s, W, w_idx, w_val, a.dw_val, dk, st);
+        if (e != hipSuccess) return hip_fail(e, "sdm_scan_bwd dk");
+    }
+    return SDM_OK;
+}
+
+int sdm_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int d_v, void* stream) {
+    g_err[0] = 0;
+    if (B < 0 || H < 0 || N < 0 || d_v < 0) return fail(SDM_ERR_INVALID_ARG, "negative size");
+    if (d_v % 4) return fail(SDM_ERR_INVALID_ARG, "d_v must be a multiple of 4");
+    if (!dst || !aligned(dst, 16) || (m0 && !aligned(m0, 16)))
+        return fail(SDM_ERR_INVALID_ARG, "null or misaligned pointer");
+    hipError_t e;
+    {
+        SdmProfScope ps(SDM_K_MEM_INIT, (hipStream_t)stream);
+        e = sdm_launch_mem_init(dst, m0, B, H, N, d_v, (hipStream_t)stream);
+    }
+    if (e != hipSuccess) return hip_fail(e, "sdm_mem_init launch");
+    return SDM_OK;
+}
+
+int sdm_check_device_errors(void* workspace, void* stream) {
+    g_err[0] = 0;
+    if (!workspace) return fail(SDM_ERR_INVALID_ARG, "null workspace");
+    hipStream_t st = (hipStream_t)stream;
+    unsigned int flag = 0;
+    hipError_t e = hipMemcpyAsync(&flag, workspace, sizeof(flag), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, "sdm_check_device_errors");
+    if (flag) {
+        e = sdm_launch_zero_words(workspace, 1, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+        if (e != hipSuccess) return hip_fail(e, "sdm_check_device_errors clear");
+        return fail(SDM_ERR_DEVICE_CHECK, "a slot id outside [0, N) was clamped");
+    }
+    return SDM_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,559 @@
+// Backward of the sparse gated-delta scan for gfx950.
+//
+// Reverse mode of the forward recurrence with the in-place + undo scheme of
+// App. A.3: the forward left M_T in the table and saved, per token, the W
+// pre-write rows P.  Going t = T-1 .. 0, each step reads M_t and the adjoint
+// G on its slots, recomputes D = alpha P, u and e from P (the forward
+// intermediates are not stored), updates G and undoes the write with P.
+//
+// As in the forward, one wave owns one (stream, column slice) for the whole
+// sequence.  Rows are prefetched PD tokens ahead (in reverse order); a row
+// that a token processed after the load was issued but before its use would
+// have modified is taken from LDS rings of the last PD tokens' undo rows
+// (for M) and adjoint rows (for G), as recorded by the prep kernel.
+// Per-token scalars (dalpha, dbeta, weight gradients) are sums over all d_v
+// columns: each slice writes its partial sums and a reduction kernel adds
+// the slices.
+#include <algorithm>
+
+#include "sdm_common.h"
+#include "sdm_internal.h"
+#include "../../include/sdm.h"
+
+namespace {
+
+constexpr int G = 4;
+constexpr int MAX_WPB = 4;
+constexpr int LDS_LIMIT = 160 * 1024;
+constexpr int PT = 64;
+
+template <int PD>
+__global__ __launch_bounds__(256) void bwd_prep_kernel(const int32_t* __restrict__ w_idx,
+                                                       const float* __restrict__ w_val,
+                                                       const int32_t* __restrict__ r_idx,
+                                                       const float* __restrict__ r_val,
+                                                       const void* __restrict__ alpha,
+                                                       const void* __restrict__ beta, int in_dtype,
+                                                       int T, int W, int R, int64_t N,
+                                                       unsigned char* __restrict__ recs,
+                                                       unsigned int* __restrict__ err) {
+    extern __shared__ int sl[];   // [(PT + PD - 1)][W + R] clamped slots, write then read
+    const BwdRec L = bwd_rec_layout(W, R);
+    const int stream = blockIdx.y;
+    const int t0 = blockIdx.x * PT;
+    const int ntok = min(PT, T - t0);
+    const int nrow = W + R;
+    const int span = min(PT + PD - 1, T - t0);   // tokens t0 .. t0+span-1 (later tokens included)
+    const size_t sbase = (size_t)stream * T;
+    unsigned int bad = 0;
+    for (int i = threadIdx.x; i < span * nrow; i += blockDim.x) {
+        const int t = t0 + i / nrow, r = i % nrow;
+        int s = r < W ? w_idx[(sbase + t) * W + r] : r_idx[(sbase + t) * R + (r - W)];
+        if (s < 0 || s >= N) {
+            bad = 1;
+            s = 0;
+        }
+        sl[i] = s;
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < ntok * nrow; i += blockDim.x) {
+        const int tl = i / nrow, r = i % nrow;
+        const int t = t0 + tl;
+        unsigned char* rec = recs + (sbase + t) * L.bytes;
+        const int slot = sl[i];
+        if (r < W) {
+            reinterpret_cast<int*>(rec)[r] = slot;
+            reinterpret_cast<float*>(rec + L.off_wval)[r] = w_val[(sbase + t) * W + r];
+        } else {
+            reinterpret_cast<int*>(rec + L.off_rslot)[r - W] = slot;
+            reinterpret_cast<float*>(rec + L.off_rval)[r - W] = r_val[(sbase + t) * R + (r - W)];
+        }
+        // G source: latest (smallest d) later token touching the slot; within a
+        // token the write adjoint (entry R + n) supersedes the read adjoint (entry m).
+        short lg = -1;
+        if (r < W) {   // d = 0: this token's read adjoint already updated G[slot]
+            const int* rl = sl + tl * nrow + W;
+            for (int m = 0; m < R; ++m)
+                if (rl[m] == slot) {
+                    lg = (short)m;
+                    break;
+                }
+        }
+        for (int d = 1; d < PD && lg < 0; ++d) {
+            if (t + d >= T) break;
+            const int* wl = sl + (tl + d) * nrow;
+            for (int n = 0; n < W; ++n)
+                if (wl[n] == slot) {
+                    lg = (short)((d << 8) | (R + n));
+                    break;
+                }
+            if (lg >= 0) break;
+            for (int m = 0; m < R; ++m)
+                if (wl[W + m] == slot) {
+                    lg = (short)((d << 8) | m);
+                    break;
+                }
+        }
+        if (r < W) {
+            reinterpret_cast<short*>(rec + L.off_lgw)[r] = lg;
+        } else {
+            reinterpret_cast<short*>(rec + L.off_lgr)[r - W] = lg;
+            // M source for a read row: the earliest later token that undid a write to it
+            short lm = -1;
+            for (int d = 1; d < PD && lm < 0; ++d) {
+                if (t + d >= T) break;
+                const int* wl = sl + (tl + d) * nrow;
+                for (int n = 0; n < W; ++n)
+                    if (wl[n] == slot) {
+                        lm = (short)((d << 8) | n);
+                        break;
+                    }
+            }
+            reinterpret_cast<short*>(rec + L.off_lm)[r - W] = lm;
+        }
+    }
+    for (int tl = threadIdx.x; tl < ntok; tl += blockDim.x) {
+        const size_t o = sbase + t0 + tl;
+        float al, be;
+        if (in_dtype == SDM_DT_BF16) {
+            al = to_f32(static_cast<const bf16_t*>(alpha)[o]);
+            be = to_f32(static_cast<const bf16_t*>(beta)[o]);
+        } else {
+            al = static_cast<const float*>(alpha)[o];
+            be = static_cast<const float*>(beta)[o];
+        }
+        unsigned char* rec = recs + o * L.bytes;
+        reinterpret_cast<float*>(rec + L.off_ab)[0] = al;
+        reinterpret_cast<float*>(rec + L.off_ab)[1] = be;
+    }
+    if (bad) atomicOr(err, 1u);
+}
+
+template <int PD>
+__host__ __device__ constexpr int bstage_lead() {
+    return ((G + PD + G - 1) / G) * G;
+}
+template <int PD>
+__host__ __device__ constexpr int bstage_slots() {
+    return bstage_lead<PD>() <= 8 ? 8 : (bstage_lead<PD>() <= 16 ? 16 : 32);
+}
+
+// Staging of the records (and v slices) of the G tokens [u1 - G + 1, u1] (clamped at 0),
+// the order the backward visits them in.  Loads are unconditional; indices past
+// the valid range are clamped and the surplus is never stored.
+template <typename VT, int SW>
+__device__ __forceinline__ void bstage_load(u4v (&st)[4], u2v& stv, const unsigned char* srec,
+                                            const VT* sv, int u1, int dv, int slice, int rec_bytes,
+                                            int lane) {
+    constexpr int VB = SW * (int)sizeof(VT);
+    constexpr int ppt = VB / 8;
+    const int ub1 = max(u1, 0);
+    const int u0 = max(0, ub1 - G + 1);
+    const int cnt = ub1 - u0 + 1;
+    const u4v* src = reinterpret_cast<const u4v*>(srec + (size_t)u0 * rec_bytes);
+    const int last = cnt * rec_bytes / 16 - 1;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) st[r] = src[min(r * SDM_WAVE + lane, last)];
+    const int tk = min(lane / ppt, cnt - 1);
+    const int pc = min(lane % ppt, (dv - slice * SW) * (int)sizeof(VT) / 8 - 1);
+    stv = *reinterpret_cast<const u2v*>(
+        reinterpret_cast<const unsigned char*>(sv + (size_t)(u0 + tk) * dv) + pc * 8);
+}
+
+template <typename VT, int SW, int NS>
+__device__ __forceinline__ void bstage_store(const u4v (&st)[4], u2v stv, unsigned char* rring,
+                                             unsigned char* vring, int u1, int rec_bytes, int lane) {
+    constexpr int VB = SW * (int)sizeof(VT);
+    constexpr int ppt = VB / 8;
+    if (u1 < 0) return;
+    const int u0 = max(0, u1 - G + 1);
+    const int cnt = u1 - u0 + 1;
+    const int nchunk = cnt * rec_bytes / 16;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int c = r * SDM_WAVE + lane;
+        if (c < nchunk) {
+            const int tk = (c * 16) / rec_bytes;   // records are whole 16-byte chunks
+            const int within = c * 16 - tk * rec_bytes;
+            *reinterpret_cast<u4v*>(rring + ((u0 + tk) & (NS - 1)) * rec_bytes + within) = st[r];
+        }
+    }
+    const int tk = lane / ppt, pc = lane % ppt;
+    if (tk < cnt) *reinterpret_cast<u2v*>(vring + ((u0 + tk) & (NS - 1)) * VB + pc * 8) = stv;
+}
+
+template <int K>
+struct BwdBuf {
+    v4f Mr[K], Gr[K], Gw[K], Ps[K];
+    v4f Dy;
+};
+
+struct BwdCtx {
+    const unsigned char* rring;
+    const unsigned char* vring;
+    float* gring;     // [PD][R + W][SW]: adjoint rows after the token (read part, then write part)
+    float* pring;     // [PD][W][SW]: undo rows of the token
+    float* mtab;      // this lane's columns of row 0 of the stream's memory table
+    float* gtab;      // same for the adjoint table
+    const float* ssaved;  // saved rows of the stream, this lane's columns
+    const float* sdy;     // dy of the stream, this lane's columns
+    float* sdv;           // dv of the stream, this lane's columns
+    float* spart;         // partial scalars of this (slice, stream)
+    BwdRec L;
+    int dv, W, R, rg, cq;
+    bool colok;
+};
+
+template <int K, int RG, int NS>
+__device__ __forceinline__ void bissue_rows(BwdBuf<K>& b, const BwdCtx& c, int u) {
+    const unsigned char* rec = c.rring + (u & (NS - 1)) * c.L.bytes;
+    b.Dy = ld4(c.sdy + (size_t)u * c.dv);
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        const int m = min(c.rg + RG * k, c.R - 1);
+        const int n = min(c.rg + RG * k, c.W - 1);
+        const size_t rs = (size_t)reinterpret_cast<const int*>(rec + c.L.off_rslot)[m] * c.dv;
+        const size_t ws = (size_t)reinterpret_cast<const int*>(rec)[n] * c.dv;
+        b.Mr[k] = ld4(c.mtab + rs);
+        b.Gr[k] = ld4(c.gtab + rs);
+        b.Gw[k] = ld4(c.gtab + ws);
+        b.Ps[k] = ld4(c.ssaved + ((size_t)u * c.W + n) * c.dv);
+    }
+}
+
+template <typename VT, int SW, int PD, int K, int NS>
+__device__ __forceinline__ void bwd_token(const BwdCtx& c, const BwdBuf<K>& b, int t, int lane) {
+    constexpr int CQ = SW / 4;
+    constexpr int RG = SDM_WAVE / CQ;
+    constexpr int VB = SW * (int)sizeof(VT);
+    const BwdRec& L = c.L;
+    const int RW = c.R + c.W;
+    const unsigned char* rec = c.rring + (t & (NS - 1)) * L.bytes;
+    const float al = reinterpret_cast<const float*>(rec + L.off_ab)[0];
+    const float be = reinterpret_cast<const float*>(rec + L.off_ab)[1];
+    const short* lm = reinterpret_cast<const short*>(rec + L.off_lm);
+    const short* lgr = reinterpret_cast<const short*>(rec + L.off_lgr);
+    const short* lgw = reinterpret_cast<const short*>(rec + L.off_lgw);
+    const v4f yb = b.Dy;
+    float* prow = c.spart + (size_t)t * (RW + 2);
+
+    // ---- read adjoint: rbar_m = <dy, M_t[j_m]>, G[j_m] += rho_m dy ----
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        const int m = c.rg + RG * k;
+        const bool rok = m < c.R;
+        const int mm = rok ? m : 0;
+        const int l1 = lm[mm];
+        const int i1 = l1 >= 0 ? (((t + (l1 >> 8)) & (PD - 1)) * c.W + (l1 & 255)) : 0;
+        const v4f Mv = v4sel(l1 >= 0, ld4(c.pring + i1 * SW + c.cq * 4), b.Mr[k]);
+        float rb = c.colok ? v4dot(yb, Mv) : 0.f;
+#pragma unroll
+        for (int q = 1; q < CQ; q <<= 1) rb += __shfl_xor(rb, q, SDM_WAVE);
+        if (rok && c.cq == 0) prow[m] = rb;
+        const int l2 = lgr[mm];
+        const int i2 = l2 >= 0 ? (((t + (l2 >> 8)) & (PD - 1)) * RW + (l2 & 255)) : 0;
+        v4f g = v4sel(l2 >= 0, ld4(c.gring + i2 * SW + c.cq * 4), b.Gr[k]);
+        const float rho = rok ? reinterpret_cast<const float*>(rec + L.off_rval)[mm] : 0.f;
+        g = v4fma(rho, yb, g);
+        if (rok) {
+            st4(c.gring + ((t & (PD - 1)) * RW + m) * SW + c.cq * 4, g);
+            if (c.colok) st4(c.gtab + (size_t)reinterpret_cast<const int*>(rec + L.off_rslot)[m] * c.dv, g);
+        }
+    }
+    // ---- write adjoint ----
+    v4f gn[K], D[K];
+    float kap[K];
+    v4f up = v4zero(), ebp = v4zero();
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        const int n = c.rg + RG * k;
+        const bool rok = n < c.W;
+        const int nn = rok ? n : 0;
+        const int l = lgw[nn];
+        const int ig = l >= 0 ? (((t + (l >> 8)) & (PD - 1)) * RW + (l & 255)) : 0;
+        gn[k] = v4sel(rok, v4sel(l >= 0, ld4(c.gring + ig * SW + c.cq * 4), b.Gw[k]), v4zero());
+        D[k] = v4sel(rok, al * b.Ps[k], v4zero());
+        kap[k] = rok ? reinterpret_cast<const float*>(rec + L.off_wval)[nn] : 0.f;
+        up = v4fma(kap[k], D[k], up);
+        ebp = v4fma(kap[k], gn[k], ebp);
+    }
+#pragma unroll
+    for (int m = CQ; m < SDM_WAVE; m <<= 1) {
+        up += v4shfl_xor(up, m);
+        ebp += v4shfl_xor(ebp, m);
+    }
+    const v4f vv = ld4v(reinterpret_cast<const VT*>(c.vring + (t & (NS - 1)) * VB) + c.cq * 4);
+    const v4f vmu = vv - up;
+    const v4f e = be * vmu;
+    if (c.rg == 0 && c.colok) st4(c.sdv + (size_t)t * c.dv, be * ebp);
+    float bb = c.colok ? v4dot(ebp, vmu) : 0.f;
+    float ab = 0.f;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        const int n = c.rg + RG * k;
+        if (n < c.W) {
+            float kb = c.colok ? (v4dot(gn[k], e) - be * v4dot(ebp, D[k])) : 0.f;
+#pragma unroll
+            for (int q = 1; q < CQ; q <<= 1) kb += __shfl_xor(kb, q, SDM_WAVE);
+            if (c.cq == 0) prow[c.R + n] = kb;
+            const v4f Db = v4fma(-be * kap[k], ebp, gn[k]);
+            if (c.colok) ab += v4dot(Db, b.Ps[k]);
+            const v4f gnew = al * Db;
+            st4(c.gring + ((t & (PD - 1)) * RW + c.R + n) * SW + c.cq * 4, gnew);
+            st4(c.pring + ((t & (PD - 1)) * c.W + n) * SW + c.cq * 4, b.Ps[k]);
+            if (c.colok) {
+                const size_t ws = (size_t)reinterpret_cast<const int*>(rec)[n] * c.dv;
+                st4(c.gtab + ws, gnew);
+                st4(c.mtab + ws, b.Ps[k]);
+            }
+        }
+    }
+#pragma unroll
+    for (int q = 1; q < CQ; q <<= 1) bb += __shfl_xor(bb, q, SDM_WAVE);
+    ab = wave_sum(ab);
+    if (lane == 0) {
+        prow[RW] = bb;
+        prow[RW + 1] = ab;
+    }
+}
+
+// Partial scalars per (slice, stream, t): [R] rbar, [W] kbar, dbeta, dalpha.
+template <typename VT, int SW, int PD, int K>
+__global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
+    const unsigned char* __restrict__ recs, const VT* __restrict__ v, float* __restrict__ mem,
+    const float* __restrict__ saved, const float* __restrict__ dy, float* __restrict__ Gtab,
+    float* __restrict__ dv_out, float* __restrict__ part, int T, int dv, int W, int R, int64_t N,
+    int n_slices, int S, int lds_per_wave) {
+    constexpr int CQ = SW / 4;
+    constexpr int RG = SDM_WAVE / CQ;
+    constexpr int LEAD = bstage_lead<PD>();
+    constexpr int NS = bstage_slots<PD>();
+    constexpr int VB = SW * (int)sizeof(VT);
+    static_assert(PD % G == 0, "prefetch depth must be a multiple of the staging block");
+    static_assert(NS >= LEAD && NS >= PD, "record ring too small");
+
+    const int lane = lane_id();
+    const int wave = threadIdx.x / SDM_WAVE;
+    const int slice = blockIdx.x * (blockDim.x / SDM_WAVE) + wave;
+    if (slice >= n_slices) return;
+    const int stream = blockIdx.y;
+
+    BwdCtx c;
+    c.L = bwd_rec_layout(W, R);
+    c.dv = dv;
+    c.W = W;
+    c.R = R;
+    c.rg = lane / CQ;
+    c.cq = lane % CQ;
+    const int col_raw = slice * SW + c.cq * 4;
+    c.colok = col_raw < dv;
+    const int col = c.colok ? col_raw : dv - 4;
+
+    extern __shared__ __align__(16) unsigned char smem[];
+    unsigned char* rring = smem + (size_t)wave * lds_per_wave;
+    unsigned char* vring = rring + NS * c.L.bytes;
+    c.rring = rring;
+    c.vring = vring;
+    c.gring = reinterpret_cast<float*>(vring + NS * VB);
+    c.pring = c.gring + PD * (R + W) * SW;
+    c.mtab = mem + (size_t)stream * N * dv + col;
+    c.gtab = Gtab + (size_t)stream * N * dv + col;
+    c.ssaved = saved + (size_t)stream * T * W * dv + col;
+    c.sdy = dy + (size_t)stream * T * dv + col;
+    c.sdv = dv_out + (size_t)stream * T * dv + col;
+    c.spart = part + ((size_t)slice * S + stream) * T * (W + R + 2);
+
+    const unsigned char* srec = recs + (size_t)stream * T * c.L.bytes;
+    const VT* sv = v + (size_t)stream * T * dv + slice * SW;
+
+    u4v st[4];
+    u2v stv;
+    BwdBuf<K> buf[PD];
+
+    // Step i processes token t = T-1-i.  Staging blocks are the G tokens
+    // ending at T-1-i for i % G == 0.
+    const int T1 = T - 1;
+    for (int i0 = 0; i0 < LEAD - G; i0 += G) {
+        bstage_load<VT, SW>(st, stv, srec, sv, T1 - i0, dv, slice, c.L.bytes, lane);
+        bstage_store<VT, SW, NS>(st, stv, rring, vring, T1 - i0, c.L.bytes, lane);
+    }
+    bstage_load<VT, SW>(st, stv, srec, sv, T1 - (LEAD - G), dv, slice, c.L.bytes, lane);
+#pragma unroll
+    for (int j = 0; j < PD; ++j) bissue_rows<K, RG, NS>(buf[j], c, max(T1 - j, 0));
+
+    const int Tfull = T - T % PD;
+    for (int i0 = 0; i0 < Tfull; i0 += PD) {
+#pragma unroll
+        for (int j = 0; j < PD; ++j) {
+            const int t = T1 - (i0 + j);
+            if (j % G == 0) {
+                bstage_store<VT, SW, NS>(st, stv, rring, vring, t - (LEAD - G), c.L.bytes, lane);
+                bstage_load<VT, SW>(st, stv, srec, sv, t - LEAD, dv, slice, c.L.bytes, lane);
+            }
+            bwd_token<VT, SW, PD, K, NS>(c, buf[j], t, lane);
+            bissue_rows<K, RG, NS>(buf[j], c, max(t - PD, 0));
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < PD; ++j) {
+        const int i = Tfull + j;
+        if (i < T) bwd_token<VT, SW, PD, K, NS>(c, buf[j], T1 - i, lane);
+    }
+}
+
+// Sum the per-slice partial scalars: rbar -> dr_val, kbar -> dw_val, dbeta, dalpha.
+__global__ __launch_bounds__(256) void bwd_reduce_kernel(const float* __restrict__ part, int n_slices,
+                                                         int64_t ST, int W, int R,
+                                                         float* __restrict__ dw_val,
+                                                         float* __restrict__ dr_val,
+                                                         float* __restrict__ dbeta,
+                                                         float* __restrict__ dalpha) {
+    const int NP = W + R + 2;
+    const int64_t total = ST * NP;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        float acc = 0.f;
+        for (int s = 0; s < n_slices; ++s) acc += part[(size_t)s * total + i];
+        const int64_t st = i / NP;
+        const int p = (int)(i % NP);
+        if (p < R)
+            dr_val[st * R + p] = acc;
+        else if (p < R + W)
+            dw_val[st * W + (p - R)] = acc;
+        else if (p == R + W)
+            dbeta[st] = acc;
+        else
+            dalpha[st] = acc;
+    }
+}
+
+template <typename VT, int SW, int PD, int K>
+hipError_t launch_bwd_k(const ScanBwdArgs& a, float* part, int n_slices, hipStream_t st) {
+    const BwdRec L = bwd_rec_layout(a.W, a.R);
+    constexpr int NS = bstage_slots<PD>();
+    const int lds_per_wave = NS * L.bytes + NS * SW * (int)sizeof(VT) +
+                             PD * (a.R + a.W) * SW * 4 + PD * a.W * SW * 4;
+    const int S = a.B * a.H;
+    if (lds_per_wave > LDS_LIMIT) return hipErrorInvalidConfiguration;
+    const int wpb = std::min(std::min(MAX_WPB, n_slices), LDS_LIMIT / lds_per_wave);
+    dim3 grid((n_slices + wpb - 1) / wpb, S);
+    const size_t sm = (size_t)lds_per_wave * wpb;
+    auto kfn = scan_bwd_kernel<VT, SW, PD, K>;
+    hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kfn, grid, dim3(wpb * SDM_WAVE), sm, st, a.ws + SDM_WS_HEADER,
+                       static_cast<const VT*>(a.v), a.mem, a.saved, a.dy, a.G, a.dv_out, part, a.T,
+                       a.dv, a.W, a.R, a.N, n_slices, S, lds_per_wave);
+    return hipGetLastError();
+}
+
+template <typename VT, int SW, int PD>
+hipError_t launch_bwd_kk(const ScanBwdArgs& a, float* part, int n_slices, hipStream_t st) {
+    constexpr int RG = SDM_WAVE / (SW / 4);
+    const int need = (max(a.W, a.R) + RG - 1) / RG;
+    if (need <= 1) return launch_bwd_k<VT, SW, PD, 1>(a, part, n_slices, st);
+    if (need <= 2) return launch_bwd_k<VT, SW, PD, 2>(a, part, n_slices, st);
+    return launch_bwd_k<VT, SW, PD, 4>(a, part, n_slices, st);
+}
+
+constexpr int BSW = 16, BPD = 4;
+
+size_t bwd_part_offset(int B, int H, int T, int W, int R) {
+    const size_t recb = (size_t)B * H * T * bwd_rec_layout(W, R).bytes;
+    return SDM_WS_HEADER + ((recb + 255) & ~(size_t)255);
+}
+
+}  // namespace
+
+size_t sdm_bwd_ws_bytes(int B, int H, int T, int W, int R, int dv) {
+    const int n_slices = (dv + BSW - 1) / BSW;
+    const size_t ST = (size_t)B * H * T;
+    size_t bytes = bwd_part_offset(B, H, T, W, R) + (size_t)n_slices * ST * (W + R + 2) * sizeof(float);
+    bytes = (bytes + 255) & ~(size_t)255;
+    bytes += ST * (size_t)(W + R) * sizeof(float);   // weight gradients when the caller wants none
+    return bytes;
+}
+
+hipError_t sdm_launch_scan_bwd(const ScanBwdArgs& a, hipStream_t st) {
+    const int S = a.B * a.H;
+    {
+        SdmProfScope ps(SDM_K_BWD_PREP, st);
+        dim3 grid((a.T + PT - 1) / PT, S);
+        const size_t sm = (size_t)(PT + BPD - 1) * (a.W + a.R) * sizeof(int);
+        hipLaunchKernelGGL(bwd_prep_kernel<BPD>, grid, dim3(256), sm, st, a.w_idx, a.w_val, a.r_idx,
+                           a.r_val, a.alpha, a.beta, a.in_dtype, a.T, a.W, a.R, a.N,
+                           a.ws + SDM_WS_HEADER, reinterpret_cast<unsigned int*>(a.ws));
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    const int n_slices = (a.dv + BSW - 1) / BSW;
+    float* part = reinterpret_cast<float*>(a.ws + bwd_part_offset(a.B, a.H, a.T, a.W, a.R));
+    hipError_t e;
+    {
+        SdmProfScope ps(SDM_K_BWD_SCAN, st);
+        e = a.in_dtype == SDM_DT_BF16 ? launch_bwd_kk<bf16_t, BSW, BPD>(a, part, n_slices, st)
+                                      : launch_bwd_kk<float, BSW, BPD>(a, part, n_slices, st);
+    }
+    if (e != hipSuccess) return e;
+    SdmProfScope ps(SDM_K_BWD_REDUCE, st);
+    const int64_t ST = (int64_t)S * a.T;
+    const int64_t total = ST * (a.W + a.R + 2);
+    const unsigned nb = (unsigned)std::min<int64_t>((total + 255) / 256, 65536);
+    hipLaunchKernelGGL(bwd_reduce_kernel, dim3(nb), dim3(256), 0, st, part, n_slices, ST, a.W, a.R,
+                       a.dw_val, a.dr_val, a.dbeta, a.dalpha);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- memory init
+namespace {
+__global__ __launch_bounds__(256) void mem_init_kernel(float4* __restrict__ dst,
+                                                       const float4* __restrict__ m0,
+                                                       int64_t per_head4, int H, int64_t total4) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total4;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        if (m0) {
+            const int64_t hh = (i / per_head4) % H;
+            dst[i] = m0[hh * per_head4 + i % per_head4];
+        } else {
+            dst[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    }
+}
+__global__ __launch_bounds__(256) void copy_kernel(float4* __restrict__ dst, const float4* __restrict__ src,
+                                                   int64_t n4) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4;
+         i += (int64_t)gridDim.x * blockDim.x)
+        dst[i] = src[i];
+}
+}  // namespace
+
+hipError_t sdm_launch_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int dv,
+                               hipStream_t st) {
+    const int64_t per_head4 = N * dv / 4;
+    const int64_t total4 = per_head4 * B * H;
+    if (total4 == 0) return hipSuccess;
+    const unsigned nb = (unsigned)std::min<int64_t>((total4 + 255) / 256, 8192);
+    hipLaunchKernelGGL(mem_init_kernel, dim3(nb), dim3(256), 0, st, reinterpret_cast<float4*>(dst),
+                       reinterpret_cast<const float4*>(m0), per_head4, H, total4);
+    return hipGetLastError();
+}
+
+namespace {
+__global__ void zero_words_kernel(unsigned int* p, int n) {
+    if ((int)threadIdx.x < n) p[threadIdx.x] = 0u;
+}
+}  // namespace
+
+hipError_t sdm_launch_zero_words(void* p, int n, hipStream_t st) {
+    hipLaunchKernelGGL(zero_words_kernel, dim3(1), dim3(64), 0, st, static_cast<unsigned int*>(p), n);
+    return hipGetLastError();
+}
+
+hipError_t sdm_launch_copy(float* dst, const float* src, size_t n, hipStream_t st) {
+    const int64_t n4 = (int64_t)(n / 4);
+    if (n4 == 0) return hipSuccess;
+    const unsigned nb = (unsigned)std::min<int64_t>((n4 + 255) / 256, 8192);
+    hipLaunchKernelGGL(copy_kernel, dim3(nb), dim3(256), 0, st, reinterpret_cast<float4*>(dst),
+                       reinterpret_cast<const float4*>(src), n4);
+    return hipGetLastError();
+}

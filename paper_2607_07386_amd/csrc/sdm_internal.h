@@ -1,0 +1,120 @@
+// Host-side launchers shared between the kernel files and the C ABI layer.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#define SDM_DT_F32 0
+#define SDM_DT_BF16 1
+
+// Per-token record of the forward scan (written by the prep kernel, staged in
+// LDS by the scan): slots and weights of both sides, forwarding links, gates.
+struct FwdRec {
+    int W, R;
+    int off_wval, off_rslot, off_rval, off_link, off_ab, bytes;
+};
+
+__host__ __device__ inline FwdRec fwd_rec_layout(int W, int R) {
+    FwdRec r;
+    r.W = W;
+    r.R = R;
+    r.off_wval = 4 * W;
+    r.off_rslot = 8 * W;
+    r.off_rval = 8 * W + 4 * R;
+    r.off_link = 8 * W + 8 * R;
+    r.off_ab = (r.off_link + 2 * (W + R) + 3) & ~3;
+    r.bytes = (r.off_ab + 8 + 15) & ~15;
+    return r;
+}
+
+// Backward record: slots/weights as forward, plus links for the rows the
+// reverse step reads (M[j_m], G[j_m], G[i_n]).
+struct BwdRec {
+    int W, R;
+    int off_wval, off_rslot, off_rval, off_lm, off_lgr, off_lgw, off_ab, bytes;
+};
+
+__host__ __device__ inline BwdRec bwd_rec_layout(int W, int R) {
+    BwdRec r;
+    r.W = W;
+    r.R = R;
+    r.off_wval = 4 * W;
+    r.off_rslot = 8 * W;
+    r.off_rval = 8 * W + 4 * R;
+    r.off_lm = 8 * W + 8 * R;          // int16 [R]: source of M_t[j_m]
+    r.off_lgr = r.off_lm + 2 * R;      // int16 [R]: source of G[j_m]
+    r.off_lgw = r.off_lgr + 2 * R;     // int16 [W]: source of G[i_n]
+    r.off_ab = (r.off_lgw + 2 * W + 3) & ~3;
+    r.bytes = (r.off_ab + 8 + 15) & ~15;
+    return r;
+}
+
+// Workspace header: device-side error flag(s) at offset 0.
+#define SDM_WS_HEADER 256
+
+hipError_t sdm_launch_address(const void* x, int x_dtype, const void* cb, int B, int H, int T,
+                              int dk, int s, int k, int32_t* idx, float* val, float* score,
+                              hipStream_t st);
+hipError_t sdm_launch_address_bwd(const void* cb, int cb_dtype, int B, int H, int T, int dk, int s,
+                                  int k, const int32_t* idx, const float* val, const float* dval,
+                                  float* dx, hipStream_t st);
+
+struct ScanFwdArgs {
+    const int32_t* w_idx;
+    const float* w_val;
+    const int32_t* r_idx;
+    const float* r_val;
+    const void* v;
+    const void* alpha;
+    const void* beta;
+    int in_dtype;
+    float* mem;
+    int B, H, T, dv, W, R;
+    int64_t N;
+    float* y;
+    float* saved;
+    unsigned char* ws;   // workspace base (header + records)
+};
+hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st);
+size_t sdm_fwd_ws_bytes(int B, int H, int T, int W, int R);
+
+struct ScanBwdArgs {
+    const int32_t* w_idx;
+    const float* w_val;
+    const int32_t* r_idx;
+    const float* r_val;
+    const void* v;
+    const void* alpha;
+    const void* beta;
+    int in_dtype;
+    float* mem;
+    const float* saved;
+    const float* dy;
+    int chunk;
+    int B, H, T, dv, W, R;
+    int64_t N;
+    float* dv_out;
+    float* dalpha;
+    float* dbeta;
+    float* G;         // dmem0 buffer, holds dM_T on entry
+    float* dw_val;    // [B,H,T,W] (workspace if the caller passed NULL)
+    float* dr_val;    // [B,H,T,R]
+    unsigned char* ws;
+};
+hipError_t sdm_launch_scan_bwd(const ScanBwdArgs& a, hipStream_t st);
+size_t sdm_bwd_ws_bytes(int B, int H, int T, int W, int R, int dv);
+
+hipError_t sdm_launch_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int dv,
+                               hipStream_t st);
+hipError_t sdm_launch_copy(float* dst, const float* src, size_t n, hipStream_t st);
+hipError_t sdm_launch_zero_words(void* p, int n, hipStream_t st);
+
+// Event bracketing of kernel launches (active only while profiling is enabled).
+void sdm_prof_begin(int kernel, hipStream_t st);
+void sdm_prof_end(int kernel, hipStream_t st);
+struct SdmProfScope {
+    int k;
+    hipStream_t st;
+    SdmProfScope(int kk, hipStream_t s) : k(kk), st(s) { sdm_prof_begin(k, st); }
+    ~SdmProfScope() { sdm_prof_end(k, st); }
+};

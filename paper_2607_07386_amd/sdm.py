@@ -1,0 +1,233 @@
+"""Python binding of libsdm.so: argument marshalling only.
+
+Every step of the SDM path runs in the HIP kernels behind the C ABI declared
+in ``include/sdm.h``; this module checks tensor placement/dtypes, allocates
+outputs and workspaces with torch (device memory), and passes raw pointers and
+the current HIP stream.  There is no fallback: if the library is missing or a
+call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsdm.so")
+HEADER = os.path.join(os.path.dirname(_HERE), "include", "sdm.h")
+
+SDM_F32, SDM_BF16 = 0, 1
+_STATUS = {0: "SDM_OK", -1: "SDM_ERR_INVALID_ARG", -2: "SDM_ERR_UNSUPPORTED",
+           -3: "SDM_ERR_WORKSPACE", -4: "SDM_ERR_HIP", -5: "SDM_ERR_DEVICE_CHECK"}
+
+
+class SdmError(RuntimeError):
+    def __init__(self, fn, status, msg):
+        super().__init__(f"{fn} failed: {_STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libsdm.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} not found: build it with "
+                              "`python -m paper_2607_07386_amd.build` (hipcc, gfx950)")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I, I64, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t
+        L.sdm_address.argtypes = [P, I, P, I, I, I, I, I64, I, P, P, P, P]
+        L.sdm_scan_fwd.argtypes = [P, P, I, P, P, I, P, P, P, I, P, I, I, I, I, I64, P, P, SZ, P, SZ, P]
+        L.sdm_scan_bwd.argtypes = [P, P, I, I, P, P, I, P, P, I, P, P, P, I, P, P, SZ, P, P, I,
+                                   I, I, I, I, I64, P, P, P, P, P, P, P, P, P, SZ, P]
+        L.sdm_mem_init.argtypes = [P, P, I, I, I64, I, P]
+        L.sdm_scan_fwd_workspace_bytes.argtypes = [I, I, I, I, I]
+        L.sdm_scan_saved_bytes.argtypes = [I, I, I, I, I]
+        L.sdm_scan_bwd_workspace_bytes.argtypes = [I, I, I, I, I, I]
+        for f in ("sdm_scan_fwd_workspace_bytes", "sdm_scan_saved_bytes", "sdm_scan_bwd_workspace_bytes"):
+            getattr(L, f).restype = SZ
+        L.sdm_check_device_errors.argtypes = [P, P]
+        L.sdm_profile_enable.argtypes = [I]
+        L.sdm_profile_read.argtypes = [I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
+        L.sdm_status_string.argtypes = [I]
+        L.sdm_status_string.restype = ctypes.c_char_p
+        L.sdm_last_error.restype = ctypes.c_char_p
+        L.sdm_version.restype = ctypes.c_char_p
+        for f in ("sdm_address", "sdm_scan_fwd", "sdm_scan_bwd", "sdm_mem_init", "sdm_check_device_errors",
+                  "sdm_profile_enable", "sdm_profile_read"):
+            getattr(L, f).restype = I
+        _lib = L
+    return _lib
+
+
+def header_symbols() -> list[str]:
+    """Names of the functions include/sdm.h declares."""
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(sdm_[a-z_0-9]+)\s*\(", txt)))
+
+
+def _check(fn: str, rc: int):
+    if rc != 0:
+        raise SdmError(fn, rc, lib().sdm_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return SDM_F32
+    if t.dtype == torch.bfloat16:
+        return SDM_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _dev(*ts):
+    dev = None
+    for t in ts:
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError("all tensors must be on the GPU")
+        if not t.is_contiguous():
+            raise ValueError("all tensors must be contiguous")
+        dev = dev or t.device
+        if t.device != dev:
+            raise ValueError("all tensors must be on the same device")
+    return dev
+
+
+def _ws(nbytes: int, device) -> torch.Tensor:
+    # torch's caching allocator returns 256-byte (or better) aligned blocks
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def address(x: torch.Tensor, codebook: torch.Tensor | None, N: int, topk: int,
+            want_score: bool = False):
+    """Product-key addressing of one side.  x [B,H,T,d_k]; codebook [H,2,sqrtN,d_k/2]
+    (same dtype) or None for direct mode.  Returns (idx int32, val fp32[, score])."""
+    dev = _dev(x, codebook)
+    B, H, T, dk = x.shape
+    idx = torch.empty((B, H, T, topk), dtype=torch.int32, device=dev)
+    val = torch.empty((B, H, T, topk), dtype=torch.float32, device=dev)
+    score = torch.empty_like(val) if want_score else None
+    if codebook is not None and codebook.dtype != x.dtype:
+        raise TypeError("codebook dtype must match x")
+    rc = lib().sdm_address(_ptr(x), _dtype_code(x), _ptr(codebook), B, H, T, dk, N, topk,
+                           _ptr(idx), _ptr(val), _ptr(score), _stream(dev))
+    _check("sdm_address", rc)
+    return (idx, val, score) if want_score else (idx, val)
+
+
+def fwd_workspace(B, H, T, W, R, device) -> torch.Tensor:
+    return _ws(lib().sdm_scan_fwd_workspace_bytes(B, H, T, W, R), device)
+
+
+def saved_buffer(B, H, T, W, d_v, device) -> torch.Tensor:
+    return torch.empty((B, H, T, W, d_v), dtype=torch.float32, device=device)
+
+
+def scan_fwd(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, saved=None, workspace=None, y=None):
+    """Sparse gated-delta scan, in place on mem (M_0 -> M_T).  Returns y [B,H,T,d_v] fp32."""
+    dev = _dev(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, saved, y)
+    B, H, T, dv = v.shape
+    W, R = w_idx.shape[-1], r_idx.shape[-1]
+    N = mem.shape[-2]
+    if not (v.dtype == alpha.dtype == beta.dtype):
+        raise TypeError("v, alpha, beta must share a dtype")
+    if mem.dtype != torch.float32:
+        raise TypeError("mem must be fp32")
+    if y is None:
+        y = torch.empty((B, H, T, dv), dtype=torch.float32, device=dev)
+    if workspace is None:
+        workspace = fwd_workspace(B, H, T, W, R, dev)
+    sb = saved.numel() * 4 if saved is not None else 0
+    rc = lib().sdm_scan_fwd(_ptr(w_idx), _ptr(w_val), W, _ptr(r_idx), _ptr(r_val), R, _ptr(v),
+                            _ptr(alpha), _ptr(beta), _dtype_code(v), _ptr(mem), B, H, T, dv, N,
+                            _ptr(y), _ptr(saved), sb, _ptr(workspace), workspace.numel(),
+                            _stream(dev))
+    _check("sdm_scan_fwd", rc)
+    return y
+
+
+def bwd_workspace(B, H, T, W, R, d_v, device) -> torch.Tensor:
+    return _ws(lib().sdm_scan_bwd_workspace_bytes(B, H, T, W, R, d_v), device)
+
+
+def scan_bwd(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, saved, dy, dmem_T=None,
+             cb_q=None, cb_k=None, d_k: int | None = None, chunk: int = 64, want_dqk: bool = True,
+             workspace=None, dmem0=None):
+    """Backward of scan_fwd (+ addressing).  mem: M_T in, M_0 out.  Returns a dict of
+    gradients: dv, dalpha, dbeta, dmem0, dw_val, dr_val and (if want_dqk) dq, dk."""
+    dev = _dev(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, saved, dy, dmem_T, cb_q, cb_k)
+    B, H, T, dv_ = v.shape
+    W, R = w_idx.shape[-1], r_idx.shape[-1]
+    N = mem.shape[-2]
+    f32 = dict(dtype=torch.float32, device=dev)
+    out = dict(dv=torch.empty((B, H, T, dv_), **f32), dalpha=torch.empty((B, H, T), **f32),
+               dbeta=torch.empty((B, H, T), **f32),
+               dmem0=dmem0 if dmem0 is not None else torch.empty((B, H, N, dv_), **f32),
+               dw_val=torch.empty((B, H, T, W), **f32), dr_val=torch.empty((B, H, T, R), **f32))
+    dq = dk = None
+    cb_dtype = SDM_F32
+    if want_dqk:
+        if d_k is None:
+            raise ValueError("d_k is required for addressing gradients")
+        dq = torch.empty((B, H, T, d_k), **f32)
+        dk = torch.empty((B, H, T, d_k), **f32)
+        cb = cb_q if cb_q is not None else cb_k
+        cb_dtype = _dtype_code(cb) if cb is not None else SDM_F32
+    if workspace is None:
+        workspace = bwd_workspace(B, H, T, W, R, dv_, dev)
+    rc = lib().sdm_scan_bwd(_ptr(cb_q), _ptr(cb_k), cb_dtype, int(d_k or 0), _ptr(w_idx),
+                            _ptr(w_val), W, _ptr(r_idx), _ptr(r_val), R, _ptr(v), _ptr(alpha),
+                            _ptr(beta), _dtype_code(v), _ptr(mem), _ptr(saved), saved.numel() * 4,
+                            _ptr(dy), _ptr(dmem_T), chunk, B, H, T, dv_, N, _ptr(dq), _ptr(dk),
+                            _ptr(out["dv"]), _ptr(out["dalpha"]), _ptr(out["dbeta"]),
+                            _ptr(out["dmem0"]), _ptr(out["dw_val"]), _ptr(out["dr_val"]),
+                            _ptr(workspace), workspace.numel(), _stream(dev))
+    _check("sdm_scan_bwd", rc)
+    if want_dqk:
+        out["dq"], out["dk"] = dq, dk
+    return out
+
+
+def mem_init(dst: torch.Tensor, m0: torch.Tensor | None):
+    """dst [B,H,N,d_v] = m0 [H,N,d_v] broadcast over B (or zero when m0 is None)."""
+    dev = _dev(dst, m0)
+    B, H, N, dv = dst.shape
+    rc = lib().sdm_mem_init(_ptr(dst), _ptr(m0), B, H, N, dv, _stream(dev))
+    _check("sdm_mem_init", rc)
+    return dst
+
+
+def check_device_errors(workspace: torch.Tensor):
+    rc = lib().sdm_check_device_errors(_ptr(workspace), _stream(workspace.device))
+    _check("sdm_check_device_errors", rc)
+
+
+KERNELS = {"address": 0, "fwd_prep": 1, "fwd_scan": 2, "bwd_prep": 3, "bwd_scan": 4, "bwd_reduce": 5,
+           "address_bwd": 6, "mem_init": 7}
+
+
+def profile_enable(on: bool = True):
+    """Start (or stop) HIP-event timing of every kernel the library launches; clears totals."""
+    _check("sdm_profile_enable", lib().sdm_profile_enable(int(on)))
+
+
+def profile_read(kernel: str):
+    """(total_ms, launches) of one kernel kind since profile_enable(True)."""
+    ms = ctypes.c_double(0.0)
+    n = ctypes.c_int64(0)
+    _check("sdm_profile_read", lib().sdm_profile_read(KERNELS[kernel], ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value

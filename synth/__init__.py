@@ -27,6 +27,7 @@ regenerated alone for sampled checks):
 from __future__ import annotations
 
 import math
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field, replace
 from typing import Iterable, Sequence
 
@@ -98,8 +99,12 @@ def _rng(w: Workload, tensor: int, b: int, h: int) -> np.random.Generator:
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round fp32 to bf16 (nearest, ties to even); returns uint16 bit patterns."""
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    rounding = ((u >> 16) & 1) + np.uint32(0x7FFF)
-    return ((u + rounding) >> 16).astype(np.uint16)
+    r = np.right_shift(u, np.uint32(16))
+    np.bitwise_and(r, np.uint32(1), out=r)
+    np.add(r, np.uint32(0x7FFF), out=r)
+    np.add(r, u, out=r)
+    np.right_shift(r, np.uint32(16), out=r)
+    return r.astype(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
@@ -107,20 +112,33 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
 
 
 class Stored:
-    """An input tensor in its storage dtype plus its exact value."""
+    """An input tensor in its storage dtype plus its exact value.
 
-    def __init__(self, arr64: np.ndarray, dtype: str):
-        self.dtype = dtype
-        f32 = arr64.astype(np.float32)
-        if dtype == "bf16":
-            self.bits = f32_to_bf16_bits(f32)
-            self.f32 = bf16_bits_to_f32(self.bits).reshape(arr64.shape)
-            self.bits = self.bits.reshape(arr64.shape)
-        elif dtype == "f32":
-            self.bits = None
-            self.f32 = f32
-        else:
+    ``f32`` holds the exact value of every element (bf16 values widen to fp32
+    exactly); ``bits`` holds the bf16 bit patterns for bf16 storage."""
+
+    def __init__(self, shape, dtype: str):
+        if dtype not in ("f32", "bf16"):
             raise ValueError(dtype)
+        self.dtype = dtype
+        self.f32 = np.empty(shape, np.float32)
+        self.bits = np.empty(shape, np.uint16) if dtype == "bf16" else None
+
+    @classmethod
+    def from_f64(cls, arr64: np.ndarray, dtype: str) -> "Stored":
+        st = cls(arr64.shape, dtype)
+        st.put(slice(None), arr64)
+        return st
+
+    def put(self, index, arr64: np.ndarray):
+        """Round fp64 values to the storage dtype and store them at ``index``."""
+        f32 = np.asarray(arr64, dtype=np.float32)
+        if self.dtype == "bf16":
+            bits = f32_to_bf16_bits(f32).reshape(f32.shape)
+            self.bits[index] = bits
+            self.f32[index] = bf16_bits_to_f32(bits).reshape(f32.shape)
+        else:
+            self.f32[index] = f32
 
     @property
     def f64(self) -> np.ndarray:
@@ -157,12 +175,12 @@ def m0_head(w: Workload, h: int) -> np.ndarray:
     return (g.standard_normal((w.N, w.d_v), dtype=np.float32) * np.float32(w.m0_std))
 
 
-def stream_inputs(w: Workload, b: int, h: int) -> dict:
+def stream_inputs(w: Workload, b: int, h: int, centres: np.ndarray | None = None) -> dict:
     """fp64 draws for one (b, h) stream: q, k [T,d_k], v [T,d_v], alpha, beta [T]."""
     T = w.T
     q = _normalise(_rng(w, _Q, b, h).standard_normal((T, w.d_k)))
     if w.clustered_keys:
-        cen = centres_head(w, h)
+        cen = centres if centres is not None else centres_head(w, h)
         ga = _rng(w, _ASSIGN, b, h)
         assign = ga.integers(0, w.n_clusters, size=T)
         k = _normalise(cen[assign] + w.cluster_sigma * _rng(w, _K, b, h).standard_normal((T, w.d_k)))
@@ -183,11 +201,13 @@ class Inputs:
 
     Arrays are laid out [B, H, T, ...] for the full workload.  With
     ``streams=[(b, h), ...]`` they are laid out [S, 1, T, ...]: each sampled
-    stream becomes its own batch row with one head, and ``heads[s]`` says
-    which head's codebook / initial memory it uses.
+    stream becomes its own batch row with one head.  ``heads[s]`` is the head
+    of flat stream s (its codebook and initial memory) in either layout.
+    Streams are drawn in parallel threads; each from its own generator, so
+    the values do not depend on the thread count.
     """
 
-    def __init__(self, w: Workload, streams: Sequence[tuple] | None = None, need_m0: bool = True):
+    def __init__(self, w: Workload, streams: Sequence[tuple] | None = None, threads: int = 8):
         self.w = w
         if streams is None:
             self.streams = [(b, h) for b in range(w.B) for h in range(w.H)]
@@ -195,34 +215,40 @@ class Inputs:
         else:
             self.streams = list(streams)
             self.shape_bh = (len(self.streams), 1)
-        S = len(self.streams)
-        T = w.T
-        q = np.empty((S, T, w.d_k), np.float64)
-        k = np.empty_like(q)
-        v = np.empty((S, T, w.d_v), np.float64)
-        al = np.empty((S, T), np.float64)
-        be = np.empty((S, T), np.float64)
-        for s, (b, h) in enumerate(self.streams):
-            d = stream_inputs(w, b, h)
-            q[s], k[s], v[s], al[s], be[s] = d["q"], d["k"], d["v"], d["alpha"], d["beta"]
-        bh = self.shape_bh
-        self.q = Stored(q.reshape(bh + (T, w.d_k)), w.dtype)
-        self.k = Stored(k.reshape(bh + (T, w.d_k)), w.dtype)
-        self.v = Stored(v.reshape(bh + (T, w.d_v)), w.dtype)
-        self.alpha = Stored(al.reshape(bh + (T,)), w.dtype)
-        self.beta = Stored(be.reshape(bh + (T,)), w.dtype)
-        heads = sorted({h for _, h in self.streams}) if streams is not None else list(range(w.H))
+        S, T = len(self.streams), w.T
         self.heads = [h for _, h in self.streams]
+        self.q = Stored((S, T, w.d_k), w.dtype)
+        self.k = Stored((S, T, w.d_k), w.dtype)
+        self.v = Stored((S, T, w.d_v), w.dtype)
+        self.alpha = Stored((S, T), w.dtype)
+        self.beta = Stored((S, T), w.dtype)
+        self._centres = {}
+        if w.clustered_keys:
+            for h in sorted(set(self.heads)):
+                self._centres[h] = centres_head(w, h)
+
+        def one(s):
+            b, h = self.streams[s]
+            d = stream_inputs(w, b, h, centres=self._centres.get(h))
+            for name in ("q", "k", "v", "alpha", "beta"):
+                getattr(self, name).put(s, d[name])
+
+        if S:
+            with ThreadPoolExecutor(max(1, min(threads, S))) as ex:
+                list(ex.map(one, range(S)))
+        bh = self.shape_bh
+        for name, last in (("q", (T, w.d_k)), ("k", (T, w.d_k)), ("v", (T, w.d_v)),
+                           ("alpha", (T,)), ("beta", (T,))):
+            st = getattr(self, name)
+            st.f32 = st.f32.reshape(bh + last)
+            if st.bits is not None:
+                st.bits = st.bits.reshape(bh + last)
         if w.codebook:
-            cbs = {h: codebook_head(w, h) for h in heads}
-            if streams is None:
-                cb = np.stack([cbs[h] for h in range(w.H)])
-            else:
-                cb = np.stack([cbs[h] for h in self.heads])
-            self.codebook = Stored(cb, w.dtype)          # [H or S, 2, sqrtN, d_k/2]
+            heads = list(range(w.H)) if streams is None else self.heads
+            cbs = {h: codebook_head(w, h) for h in set(heads)}
+            self.codebook = Stored.from_f64(np.stack([cbs[h] for h in heads]), w.dtype)
         else:
             self.codebook = None
-        self._need_m0 = need_m0
         self._m0_cache = {}
 
     # initial memory ------------------------------------------------------

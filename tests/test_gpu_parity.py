@@ -1,0 +1,382 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Bar: slot ids bit-exact except near-ties (a GPU-chosen slot outside the
+oracle's set must score within 1e-6 of the oracle's k-th best score; such
+flips are counted and reported); y, M_T and gradients within max relative
+error 1e-4 (fp32 inputs) or 2e-2 (bf16 inputs, fp32 state).  The scan is
+compared on the GPU's own slot ids and weights, so an addressing near-tie
+never leaks into the scan comparison.  Rows no token writes must come back
+bit-identical, and the backward must restore M_0 bit for bit.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from paper_2607_07386_amd import sdm
+from tests.gpu_util import (DEV, compare_address, gpu_forward, rel_err, to_dev, tol_for)
+
+pytestmark = pytest.mark.gpu
+
+REPORT = os.environ.get("SDM_REPORT", "")
+
+
+def report(name, **kw):
+    line = json.dumps(dict(test=name, **kw), default=float)
+    print(line, flush=True)
+    if REPORT:
+        with open(REPORT, "a") as f:
+            f.write(line + "\n")
+
+
+def np_(t):
+    return t.detach().cpu().numpy()
+
+
+def oracle_address_rows(w, inp, x_st, streams):
+    """Oracle addressing of the given (flat) streams, decided in fp32 like the kernel."""
+    x = x_st.f64.reshape((-1, w.T, w.d_k))[streams][:, None]
+    if inp.codebook is not None:
+        cbh = inp.codebook.f64
+        heads = [inp.heads[s] for s in streams]
+        out = [oracle.address(x[i:i + 1], cbh[heads[i]][None], w.N, w.topk, decide_f32=True)
+               for i in range(len(streams))]
+        return [np.concatenate([o[j] for o in out]) for j in range(3)], [cbh[h] for h in heads]
+    return oracle.address(x, None, w.N, w.topk, decide_f32=True), [None] * len(streams)
+
+
+def check_addressing(w, inp, g, streams):
+    stats = {}
+    for side, x_st, gi, gv in (("read", inp.q, g["r_idx"], g["r_val"]), ("write", inp.k, g["w_idx"], g["w_val"])):
+        (oi, ov, osc), cbs = oracle_address_rows(w, inp, x_st, streams)
+        gidx = np_(gi).reshape(-1, w.T, w.topk)[streams].reshape(-1, w.topk)
+        gval = np_(gv).reshape(-1, w.T, w.topk)[streams].reshape(-1, w.topk)
+        x64 = x_st.f64.reshape(-1, w.T, w.d_k)[streams].reshape(-1, w.d_k)
+        st = compare_address(gidx, gval, oi.reshape(-1, w.topk), ov.reshape(-1, w.topk),
+                             osc.reshape(-1, w.topk), x64, lambda r: cbs[r // w.T], w.sqrtN)
+        stats[side] = st
+    return stats
+
+
+def oracle_scan_rows(w, inp, g, streams, m0_of_stream, save=False):
+    """The oracle's scan of the given streams, fed the GPU's slot ids and weights."""
+    S = len(streams)
+
+    def take(t, last):
+        return np_(t).reshape((-1, w.T) + last)[streams]
+
+    wi, wv = take(g["w_idx"], (w.topk,)), take(g["w_val"], (w.topk,))
+    ri, rv = take(g["r_idx"], (w.topk,)), take(g["r_val"], (w.topk,))
+    v = inp.v.f64.reshape(-1, w.T, w.d_v)[streams]
+    al = inp.alpha.f64.reshape(-1, w.T)[streams]
+    be = inp.beta.f64.reshape(-1, w.T)[streams]
+    mem = np.zeros((S, w.N, w.d_v), np.float64)
+    for i, s in enumerate(streams):
+        m0 = m0_of_stream(s)
+        if m0 is not None:
+            mem[i] = m0
+    m_init = mem.copy()
+    res = oracle.scan_fwd(wi, wv, ri, rv, v, al, be, mem, save=save)
+    return dict(wi=wi, wv=wv, ri=ri, rv=rv, v=v, al=al, be=be, m_init=m_init, mem=mem,
+                y=res[0] if save else res, saved=res[1] if save else None)
+
+
+def check_scan(w, g, o, streams, name):
+    tol = tol_for(w)
+    y = np_(g["y"]).reshape(-1, w.T, w.d_v)[streams]
+    memg = np_(g["mem"]).reshape(-1, w.N, w.d_v)[streams]
+    ey, em = rel_err(y, o["y"]), rel_err(memg, o["mem"])
+    # rows no token writes: bit-identical to M_0
+    untouched_ok = True
+    for i in range(len(streams)):
+        written = np.zeros(w.N, bool)
+        written[o["wi"][i].ravel()] = True
+        untouched_ok &= np.array_equal(memg[i][~written], o["m_init"][i][~written].astype(np.float32))
+    report(name, y_rel_err=ey, mem_rel_err=em, tol=tol, untouched_bit_exact=bool(untouched_ok))
+    assert ey <= tol and em <= tol, (ey, em)
+    assert untouched_ok
+
+
+def m0_fn(w, inp):
+    if w.m0 == "zero":
+        return lambda s: None
+    return lambda s: inp.m0_head(inp.heads[s]).astype(np.float64)
+
+
+# --------------------------------------------------------------- small cases
+SMALL = {
+    "c0-tiny-f32": synth.WORKLOADS[0],
+    "bf16-mfma-ragged": synth.Workload("t", B=1, H=2, T=203, d_k=128, d_v=128, N=4096, topk=32, seed=11),
+    "f32-direct-dv40": synth.Workload("t", B=2, H=1, T=97, d_k=32, d_v=40, N=256, topk=8, dtype="f32",
+                                      seed=12, codebook=False),
+    "bf16-direct": synth.Workload("t", B=1, H=3, T=70, d_k=64, d_v=32, N=1024, topk=16, seed=13, codebook=False),
+    "bf16-s24-k24-dk48-dv36": synth.Workload("t", B=1, H=2, T=150, d_k=48, d_v=36, N=576, topk=24, seed=14),
+    "bf16-fma-dk20": synth.Workload("t", B=1, H=1, T=90, d_k=20, d_v=16, N=400, topk=5, seed=15),
+    "f32-k1": synth.Workload("t", B=1, H=2, T=65, d_k=16, d_v=8, N=100, topk=1, dtype="f32", seed=16),
+    "bf16-k64-s128": synth.Workload("t", B=1, H=1, T=64, d_k=64, d_v=64, N=16384, topk=64, seed=17),
+    "bf16-hazard-N64": synth.Workload("t", B=2, H=2, T=500, d_k=32, d_v=48, N=64, topk=8, seed=18),
+    "f32-hazard-N16-k4": synth.Workload("t", B=1, H=1, T=333, d_k=8, d_v=4, N=16, topk=4, dtype="f32", seed=19),
+    "bf16-T1": synth.Workload("t", B=2, H=2, T=1, d_k=32, d_v=32, N=256, topk=8, seed=20),
+    "bf16-m0-shared": synth.Workload("t", B=3, H=2, T=120, d_k=32, d_v=32, N=1024, topk=8, seed=21, m0="shared"),
+    "bf16-clustered": synth.Workload("t", B=1, H=2, T=400, d_k=64, d_v=32, N=4096, topk=16, seed=22,
+                                     clustered_keys=True, n_clusters=8),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_forward_small(name):
+    w = SMALL[name]
+    inp = synth.Inputs(w)
+    g = gpu_forward(w, inp)
+    S = w.B * w.H
+    streams = list(range(S))
+    st = check_addressing(w, inp, g, streams)
+    report(name + "/address", **{f"{k}_{kk}": vv for k, v in st.items() for kk, vv in v.items()})
+    o = oracle_scan_rows(w, inp, g, streams, m0_fn(w, inp))
+    check_scan(w, g, o, streams, name + "/scan")
+
+
+def test_empty_sequence_is_noop():
+    w = synth.Workload("t", B=1, H=1, T=0, d_k=32, d_v=32, N=256, topk=8)
+    dev = DEV
+    z = torch.zeros((1, 1, 0, 32), dtype=torch.bfloat16, device=dev)
+    idx, val = sdm.address(z, None, 256, 8)
+    assert idx.numel() == 0
+    mem = torch.randn((1, 1, 256, 32), device=dev)
+    ref = mem.clone()
+    e_i = torch.zeros((1, 1, 0, 8), dtype=torch.int32, device=dev)
+    e_v = torch.zeros((1, 1, 0, 8), dtype=torch.float32, device=dev)
+    g = torch.zeros((1, 1, 0), dtype=torch.bfloat16, device=dev)
+    y = sdm.scan_fwd(e_i, e_v, e_i, e_v, z, g, g, mem)
+    torch.cuda.synchronize()
+    assert y.numel() == 0 and torch.equal(mem, ref)
+
+
+# ------------------------------------------------- scan on hand-made index lists
+def _scan_case(S, T, N, W, R, dv, idx_fn, seed, dtype=torch.float32):
+    rng = np.random.default_rng(seed)
+    wi = np.zeros((S, T, W), np.int32)
+    ri = np.zeros((S, T, R), np.int32)
+    for s in range(S):
+        for t in range(T):
+            wi[s, t], ri[s, t] = idx_fn(rng, s, t, wi[s])
+    wv = rng.random((S, T, W)).astype(np.float32)
+    rv = rng.standard_normal((S, T, R)).astype(np.float32)
+    v = rng.standard_normal((S, T, dv)).astype(np.float32)
+    al = rng.uniform(0.05, 1.0, (S, T)).astype(np.float32)
+    be = rng.uniform(0.0, 1.0, (S, T)).astype(np.float32)
+    m0 = rng.standard_normal((S, N, dv)).astype(np.float32)
+    if dtype == torch.bfloat16:
+        v, al, be = (synth.bf16_bits_to_f32(synth.f32_to_bf16_bits(a)).reshape(a.shape) for a in (v, al, be))
+    t_ = lambda a: torch.from_numpy(a).to(DEV)
+    mem = t_(m0).reshape(S, 1, N, dv).contiguous()
+    y = sdm.scan_fwd(t_(wi)[:, None], t_(wv)[:, None], t_(ri)[:, None], t_(rv)[:, None],
+                     t_(v)[:, None].to(dtype), t_(al)[:, None].to(dtype), t_(be)[:, None].to(dtype), mem)
+    torch.cuda.synchronize()
+    memo = m0.astype(np.float64)
+    yo = oracle.scan_fwd(wi, wv, ri, rv, v, al, be, memo)
+    return np_(y)[:, 0], np_(mem)[:, 0], yo, memo
+
+
+HAZARDS = {
+    # every token writes slot 0 (plus random others) and reads it back
+    "slot0-every-token": lambda rng, s, t, prev: (
+        np.concatenate([[0], rng.choice(np.arange(1, 40), 5, replace=False)]).astype(np.int32),
+        np.concatenate([[0], rng.choice(np.arange(1, 40), 3, replace=False)]).astype(np.int32)),
+    # read set = previous token's write set (RAW across consecutive tokens)
+    "read-prev-writes": lambda rng, s, t, prev: (
+        rng.choice(24, 6, replace=False).astype(np.int32),
+        (prev[t - 1] if t > 0 else rng.choice(24, 6, replace=False)).astype(np.int32)),
+    # reads include this token's own writes, unsorted lists
+    "read-own-writes-unsorted": lambda rng, s, t, prev: (
+        (lambda a: (a, np.concatenate([a[:3], rng.choice(np.setdiff1d(np.arange(30), a), 3, replace=False)])))(
+            rng.choice(30, 6, replace=False).astype(np.int32))),
+    # write sets cycling with period 3 (re-touch at distance 3, inside the window)
+    "period-3": lambda rng, s, t, prev: (
+        (np.arange(6) + 6 * (t % 3)).astype(np.int32), (np.arange(6) + 6 * ((t + 1) % 3)).astype(np.int32)),
+    # period 9: re-touch just beyond an 8-token prefetch window
+    "period-9": lambda rng, s, t, prev: (
+        (np.arange(4) + 4 * (t % 9)).astype(np.int32), (np.arange(6) + 4 * ((t + 5) % 9)).astype(np.int32)),
+}
+
+
+@pytest.mark.parametrize("name", list(HAZARDS))
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_scan_hazards(name, dtype):
+    fn = HAZARDS[name]
+    W = len(fn(np.random.default_rng(0), 0, 0, np.zeros((1, 8), np.int32))[0])
+    R = len(fn(np.random.default_rng(0), 0, 0, np.zeros((1, 8), np.int32))[1])
+    y, mem, yo, memo = _scan_case(3, 211, 48, W, R, 20, fn, seed=5, dtype=dtype)
+    ey, em = rel_err(y, yo), rel_err(mem, memo)
+    report(f"hazard/{name}/{dtype}", y_rel_err=ey, mem_rel_err=em)
+    assert ey < 1e-4 and em < 1e-4
+
+
+def test_gated_deltanet_reduction_on_gpu():
+    """N = d_qk, every slot selected with the raw dense key/query as weights."""
+    rng = np.random.default_rng(9)
+    T, dqk, dv = 120, 16, 16
+    K = rng.standard_normal((T, dqk)).astype(np.float32) * 0.25
+    Q = rng.standard_normal((T, dqk)).astype(np.float32)
+    V = rng.standard_normal((T, dv)).astype(np.float32)
+    al = rng.uniform(0.5, 1.0, T).astype(np.float32)
+    be = rng.uniform(0.0, 1.0, T).astype(np.float32)
+    ids = np.tile(np.arange(dqk, dtype=np.int32), (T, 1))
+    t_ = lambda a: torch.from_numpy(np.ascontiguousarray(a))[None, None].to(DEV)
+    mem = torch.zeros((1, 1, dqk, dv), device=DEV)
+    y = sdm.scan_fwd(t_(ids), t_(K), t_(ids), t_(Q), t_(V), t_(al), t_(be), mem)
+    torch.cuda.synchronize()
+    S = np.zeros((dqk, dv))
+    ys = []
+    for t in range(T):
+        S = al[t] * S + be[t] * np.outer(K[t], V[t] - al[t] * S.T @ K[t])
+        ys.append(S.T @ Q[t])
+    assert rel_err(np_(y)[0, 0], np.array(ys)) < 1e-4
+    assert rel_err(np_(mem)[0, 0], S) < 1e-4
+
+
+def test_state_carry_bit_exact():
+    w = SMALL["bf16-hazard-N64"]
+    inp = synth.Inputs(w)
+    g = gpu_forward(w, inp)
+    T1 = 237
+    mem = torch.zeros_like(g["mem"])
+    ys = []
+    for sl in (slice(0, T1), slice(T1, w.T)):
+        part = lambda t: t[:, :, sl].contiguous()
+        ys.append(sdm.scan_fwd(part(g["w_idx"]), part(g["w_val"]), part(g["r_idx"]), part(g["r_val"]),
+                               part(g["v"]), part(g["alpha"]), part(g["beta"]), mem))
+    torch.cuda.synchronize()
+    assert torch.equal(torch.cat(ys, 2), g["y"])
+    assert torch.equal(mem, g["mem"])
+
+
+def test_out_of_range_slot_is_clamped_and_reported():
+    S, T, N, W, dv = 1, 20, 32, 4, 8
+    wi = torch.randint(0, N, (S, 1, T, W), dtype=torch.int32, device=DEV)
+    wi[0, 0, 5, 2] = N + 7          # out of range: clamped on the device, flagged
+    wv = torch.rand((S, 1, T, W), device=DEV)
+    v = torch.randn((S, 1, T, dv), device=DEV)
+    g = torch.rand((S, 1, T), device=DEV)
+    mem = torch.zeros((S, 1, N, dv), device=DEV)
+    ws = sdm.fwd_workspace(S, 1, T, W, W, DEV)
+    sdm.scan_fwd(wi, wv, wi.clamp(max=N - 1).contiguous(), wv, v, g, g, mem, workspace=ws)
+    with pytest.raises(sdm.SdmError) as e:
+        sdm.check_device_errors(ws)
+    assert e.value.status == -5
+    sdm.check_device_errors(ws)     # cleared
+
+
+# --------------------------------------------------------------- backward
+BWD = {
+    "bf16-small": synth.Workload("t", B=1, H=2, T=150, d_k=64, d_v=48, N=1024, topk=8, seed=31, train=True),
+    "f32-direct-hazard": synth.Workload("t", B=2, H=1, T=120, d_k=16, d_v=8, N=64, topk=6, dtype="f32",
+                                        seed=32, codebook=False, train=True),
+    "bf16-m0-k32": synth.Workload("t", B=1, H=2, T=70, d_k=128, d_v=128, N=4096, topk=32, seed=33,
+                                  m0="shared", train=True),
+}
+
+
+def run_backward_case(w, inp, streams, chunk=64):
+    g = gpu_forward(w, inp, save=True)
+    dy = torch.from_numpy(inp.dy()).to(DEV)
+    gr = sdm.scan_bwd(g["w_idx"], g["w_val"], g["r_idx"], g["r_val"], g["v"], g["alpha"], g["beta"],
+                      g["mem"], g["saved"], dy, cb_q=g["cb"], cb_k=g["cb"], d_k=w.d_k, chunk=chunk)
+    torch.cuda.synchronize()
+    o = oracle_scan_rows(w, inp, g, streams, m0_fn(w, inp), save=True)
+    dy64 = np_(dy).reshape(-1, w.T, w.d_v)[streams].astype(np.float64)
+    memT = o["mem"].copy()
+    og = oracle.scan_bwd(o["wi"], o["wv"], o["ri"], o["rv"], o["v"], o["al"], o["be"], memT, o["saved"], dy64)
+    assert np.array_equal(memT, o["m_init"])
+    cb = inp.codebook.f64 if inp.codebook is not None else None
+    out = {}
+    for name, key, last in (("dv", "dv", (w.d_v,)), ("dalpha", "dalpha", ()), ("dbeta", "dbeta", ()),
+                            ("dw_val", "dw_val", (w.topk,)), ("dr_val", "dr_val", (w.topk,))):
+        gg = np_(gr[key]).reshape((-1, w.T) + last)[streams]
+        out[name] = rel_err(gg, og[name])
+    gd = np_(gr["dmem0"]).reshape(-1, w.N, w.d_v)[streams]
+    out["dmem0"] = rel_err(gd, og["dmem0"])
+    # addressing gradients of the sampled streams, from the oracle's weight gradients
+    for side, idx, val, dval, key in (("dq", o["ri"], o["rv"], og["dr_val"], "dq"),
+                                      ("dk", o["wi"], o["wv"], og["dw_val"], "dk")):
+        ref = np.concatenate([
+            oracle.address_bwd(None if cb is None else cb[inp.heads[s]][None], idx[i:i + 1, None],
+                               val[i:i + 1, None], dval[i:i + 1, None], w.N, w.d_k)
+            for i, s in enumerate(streams)])[:, 0]
+        gg = np_(gr[key]).reshape(-1, w.T, w.d_k)[streams]
+        out[side] = rel_err(gg, ref)
+    restored = np_(g["mem"]).reshape(-1, w.N, w.d_v)[streams]
+    out["mem_restored_bit_exact"] = bool(np.array_equal(restored, o["m_init"].astype(np.float32)))
+    return out, gr
+
+
+@pytest.mark.parametrize("name", list(BWD))
+def test_backward_small(name):
+    w = BWD[name]
+    inp = synth.Inputs(w)
+    streams = list(range(w.B * w.H))
+    errs, _ = run_backward_case(w, inp, streams)
+    report(name + "/bwd", **errs)
+    tol = tol_for(w)
+    for k, e in errs.items():
+        if k != "mem_restored_bit_exact":
+            assert e <= tol, (k, e)
+    assert errs["mem_restored_bit_exact"]
+
+
+def test_backward_chunk_invariance():
+    w = BWD["bf16-small"]
+    inp = synth.Inputs(w)
+    outs = []
+    for chunk in (1, 16, 64, w.T):
+        _, gr = run_backward_case(w, inp, [0], chunk=chunk)
+        outs.append({k: np_(v) for k, v in gr.items()})
+    for o in outs[1:]:
+        for k in o:
+            assert np.array_equal(o[k], outs[0][k]), k
+
+
+# ------------------------------------------------- full-size workloads, sampled streams
+def _full(cfg, streams_of):
+    w = synth.WORKLOADS[cfg]
+    inp = synth.Inputs(w)
+    g = gpu_forward(w, inp)
+    S = w.B * w.H
+    streams = streams_of(S)
+    st = check_addressing(w, inp, g, streams)
+    report(f"c{cfg}/address", **{f"{k}_{kk}": vv for k, v in st.items() for kk, vv in v.items()})
+    # distinct slots touched, for context
+    o = oracle_scan_rows(w, inp, g, streams, m0_fn(w, inp))
+    check_scan(w, g, o, streams, f"c{cfg}/scan")
+
+
+@pytest.mark.slow
+def test_full_c1():
+    _full(1, lambda S: [0, S // 2 + 3, S - 1])
+
+
+@pytest.mark.slow
+def test_full_c2():
+    _full(2, lambda S: [5])
+
+
+@pytest.mark.slow
+def test_full_c3():
+    _full(3, lambda S: [0, S - 1])
+
+
+@pytest.mark.slow
+def test_full_c4_training():
+    w = synth.WORKLOADS[4]
+    inp = synth.Inputs(w)
+    S = w.B * w.H
+    errs, _ = run_backward_case(w, inp, [1, S - 2])
+    report("c4/bwd", **errs)
+    for k, e in errs.items():
+        if k != "mem_restored_bit_exact":
+            assert e <= tol_for(w), (k, e)
+    assert errs["mem_restored_bit_exact"]
