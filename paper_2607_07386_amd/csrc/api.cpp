@@ -222,6 +222,8 @@ int sdm_scan_fwd(const int32_t* w_idx, const float* w_val, int W, const int32_t*
             return fail(SDM_ERR_WORKSPACE, "saved buffer too small: %zu < %zu", saved_bytes,
                         sdm_scan_saved_bytes(B, H, T, W, d_v));
     }
+    if (!sdm_fwd_plan_ok(W, R, d_v, in_dtype))
+        return fail(SDM_ERR_UNSUPPORTED, "no forward launch plan for W=%d R=%d d_v=%d", W, R, d_v);
     const size_t need = sdm_fwd_ws_bytes(B, H, T, W, R);
     if (!workspace || !aligned(workspace, 256))
         return fail(SDM_ERR_INVALID_ARG, "workspace must be a 256-byte aligned pointer");
@@ -268,6 +270,8 @@ int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, cons
         if (dk && !cb_k && d_k != 2 * s) return fail(SDM_ERR_INVALID_ARG, "direct mode needs d_k == 2*sqrt(N)");
         if ((cb_q || cb_k) && (d_k % 2 || d_k < 2)) return fail(SDM_ERR_INVALID_ARG, "codebook mode needs an even d_k");
     }
+    if (!sdm_bwd_plan_ok(W, R, d_v, in_dtype))
+        return fail(SDM_ERR_UNSUPPORTED, "no backward launch plan for W=%d R=%d d_v=%d", W, R, d_v);
     const size_t need = sdm_bwd_ws_bytes(B, H, T, W, R, d_v);
     if (!workspace || !aligned(workspace, 256))
         return fail(SDM_ERR_INVALID_ARG, "workspace must be a 256-byte aligned pointer");

@@ -141,8 +141,8 @@ __host__ __device__ constexpr int bstage_slots() {
 // Staging of the records (and v slices) of the G tokens [u1 - G + 1, u1] (clamped at 0),
 // the order the backward visits them in.  Loads are unconditional; indices past
 // the valid range are clamped and the surplus is never stored.
-template <typename VT, int SW>
-__device__ __forceinline__ void bstage_load(u4v (&st)[4], u2v& stv, const unsigned char* srec,
+template <typename VT, int SW, int NR>
+__device__ __forceinline__ void bstage_load(u4v (&st)[NR], u2v& stv, const unsigned char* srec,
                                             const VT* sv, int u1, int dv, int slice, int rec_bytes,
                                             int lane) {
     constexpr int VB = SW * (int)sizeof(VT);
@@ -153,24 +153,24 @@ __device__ __forceinline__ void bstage_load(u4v (&st)[4], u2v& stv, const unsign
     const u4v* src = reinterpret_cast<const u4v*>(srec + (size_t)u0 * rec_bytes);
     const int last = cnt * rec_bytes / 16 - 1;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) st[r] = src[min(r * SDM_WAVE + lane, last)];
+    for (int r = 0; r < NR; ++r) st[r] = src[min(r * SDM_WAVE + lane, last)];
     const int tk = min(lane / ppt, cnt - 1);
     const int pc = min(lane % ppt, (dv - slice * SW) * (int)sizeof(VT) / 8 - 1);
     stv = *reinterpret_cast<const u2v*>(
         reinterpret_cast<const unsigned char*>(sv + (size_t)(u0 + tk) * dv) + pc * 8);
 }
 
-template <typename VT, int SW, int NS>
-__device__ __forceinline__ void bstage_store(const u4v (&st)[4], u2v stv, unsigned char* rring,
+template <typename VT, int SW, int NS, int NR>
+__device__ __forceinline__ void bstage_store(const u4v (&st)[NR], u2v stv, unsigned char* rring,
                                              unsigned char* vring, int u1, int rec_bytes, int lane) {
     constexpr int VB = SW * (int)sizeof(VT);
     constexpr int ppt = VB / 8;
     if (u1 < 0) return;
     const int u0 = max(0, u1 - G + 1);
     const int cnt = u1 - u0 + 1;
-    const int nchunk = cnt * rec_bytes / 16;
+    const int nchunk = cnt * rec_bytes / 16;   // <= NR * 64 (checked by the host plan)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < NR; ++r) {
         const int c = r * SDM_WAVE + lane;
         if (c < nchunk) {
             const int tk = (c * 16) / rec_bytes;   // records are whole 16-byte chunks
@@ -318,7 +318,7 @@ __device__ __forceinline__ void bwd_token(const BwdCtx& c, const BwdBuf<K>& b, i
 }
 
 // Partial scalars per (slice, stream, t): [R] rbar, [W] kbar, dbeta, dalpha.
-template <typename VT, int SW, int PD, int K>
+template <typename VT, int SW, int PD, int K, int NR>
 __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
     const unsigned char* __restrict__ recs, const VT* __restrict__ v, float* __restrict__ mem,
     const float* __restrict__ saved, const float* __restrict__ dy, float* __restrict__ Gtab,
@@ -366,7 +366,7 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
     const unsigned char* srec = recs + (size_t)stream * T * c.L.bytes;
     const VT* sv = v + (size_t)stream * T * dv + slice * SW;
 
-    u4v st[4];
+    u4v st[NR];
     u2v stv;
     BwdBuf<K> buf[PD];
 
@@ -374,10 +374,10 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
     // ending at T-1-i for i % G == 0.
     const int T1 = T - 1;
     for (int i0 = 0; i0 < LEAD - G; i0 += G) {
-        bstage_load<VT, SW>(st, stv, srec, sv, T1 - i0, dv, slice, c.L.bytes, lane);
-        bstage_store<VT, SW, NS>(st, stv, rring, vring, T1 - i0, c.L.bytes, lane);
+        bstage_load<VT, SW, NR>(st, stv, srec, sv, T1 - i0, dv, slice, c.L.bytes, lane);
+        bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, T1 - i0, c.L.bytes, lane);
     }
-    bstage_load<VT, SW>(st, stv, srec, sv, T1 - (LEAD - G), dv, slice, c.L.bytes, lane);
+    bstage_load<VT, SW, NR>(st, stv, srec, sv, T1 - (LEAD - G), dv, slice, c.L.bytes, lane);
 #pragma unroll
     for (int j = 0; j < PD; ++j) bissue_rows<K, RG, NS>(buf[j], c, max(T1 - j, 0));
 
@@ -387,8 +387,8 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
         for (int j = 0; j < PD; ++j) {
             const int t = T1 - (i0 + j);
             if (j % G == 0) {
-                bstage_store<VT, SW, NS>(st, stv, rring, vring, t - (LEAD - G), c.L.bytes, lane);
-                bstage_load<VT, SW>(st, stv, srec, sv, t - LEAD, dv, slice, c.L.bytes, lane);
+                bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, t - (LEAD - G), c.L.bytes, lane);
+                bstage_load<VT, SW, NR>(st, stv, srec, sv, t - LEAD, dv, slice, c.L.bytes, lane);
             }
             bwd_token<VT, SW, PD, K, NS>(c, buf[j], t, lane);
             bissue_rows<K, RG, NS>(buf[j], c, max(t - PD, 0));
@@ -427,36 +427,54 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(const float* __restrict
     }
 }
 
-template <typename VT, int SW, int PD, int K>
-hipError_t launch_bwd_k(const ScanBwdArgs& a, float* part, int n_slices, hipStream_t st) {
-    const BwdRec L = bwd_rec_layout(a.W, a.R);
-    constexpr int NS = bstage_slots<PD>();
-    const int lds_per_wave = NS * L.bytes + NS * SW * (int)sizeof(VT) +
-                             PD * (a.R + a.W) * SW * 4 + PD * a.W * SW * 4;
+constexpr int BSW = 16, BPD = 4;
+
+// Staging registers per lane for a block of G backward records (at most
+// 8 (W + R) + 4 R + 2 W + 8 bytes each) of a shape with max(W, R) <= 16 K.
+constexpr int bnr_for_k(int K) { return K == 1 ? 2 : (K == 2 ? 3 : 6); }
+
+struct BwdPlan {
+    int K, NR, lds_per_wave, wpb, n_slices;
+};
+
+bool bwd_plan(int W, int R, int dv, int in_dtype, BwdPlan* p) {
+    constexpr int RG = SDM_WAVE / (BSW / 4);
+    const int need = (std::max(W, R) + RG - 1) / RG;
+    if (need > 4) return false;
+    p->K = need <= 1 ? 1 : (need <= 2 ? 2 : 4);
+    p->NR = bnr_for_k(p->K);
+    const BwdRec L = bwd_rec_layout(W, R);
+    if (G * L.bytes > p->NR * SDM_WAVE * 16) return false;
+    const int vbytes = in_dtype == SDM_DT_BF16 ? 2 : 4;
+    constexpr int NS = bstage_slots<BPD>();
+    p->lds_per_wave = NS * L.bytes + NS * BSW * vbytes + BPD * (R + W) * BSW * 4 + BPD * W * BSW * 4;
+    if (p->lds_per_wave > LDS_LIMIT) return false;
+    p->n_slices = (dv + BSW - 1) / BSW;
+    p->wpb = std::min(std::min(MAX_WPB, p->n_slices), LDS_LIMIT / p->lds_per_wave);
+    return true;
+}
+
+template <typename VT, int K>
+hipError_t launch_bwd_k(const ScanBwdArgs& a, const BwdPlan& p, float* part, hipStream_t st) {
+    constexpr int NR = bnr_for_k(K);
     const int S = a.B * a.H;
-    if (lds_per_wave > LDS_LIMIT) return hipErrorInvalidConfiguration;
-    const int wpb = std::min(std::min(MAX_WPB, n_slices), LDS_LIMIT / lds_per_wave);
-    dim3 grid((n_slices + wpb - 1) / wpb, S);
-    const size_t sm = (size_t)lds_per_wave * wpb;
-    auto kfn = scan_bwd_kernel<VT, SW, PD, K>;
+    dim3 grid((p.n_slices + p.wpb - 1) / p.wpb, S);
+    const size_t sm = (size_t)p.lds_per_wave * p.wpb;
+    auto kfn = scan_bwd_kernel<VT, BSW, BPD, K, NR>;
     hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kfn, grid, dim3(wpb * SDM_WAVE), sm, st, a.ws + SDM_WS_HEADER,
+    hipLaunchKernelGGL(kfn, grid, dim3(p.wpb * SDM_WAVE), sm, st, a.ws + SDM_WS_HEADER,
                        static_cast<const VT*>(a.v), a.mem, a.saved, a.dy, a.G, a.dv_out, part, a.T,
-                       a.dv, a.W, a.R, a.N, n_slices, S, lds_per_wave);
+                       a.dv, a.W, a.R, a.N, p.n_slices, S, p.lds_per_wave);
     return hipGetLastError();
 }
 
-template <typename VT, int SW, int PD>
-hipError_t launch_bwd_kk(const ScanBwdArgs& a, float* part, int n_slices, hipStream_t st) {
-    constexpr int RG = SDM_WAVE / (SW / 4);
-    const int need = (max(a.W, a.R) + RG - 1) / RG;
-    if (need <= 1) return launch_bwd_k<VT, SW, PD, 1>(a, part, n_slices, st);
-    if (need <= 2) return launch_bwd_k<VT, SW, PD, 2>(a, part, n_slices, st);
-    return launch_bwd_k<VT, SW, PD, 4>(a, part, n_slices, st);
+template <typename VT>
+hipError_t launch_bwd_kk(const ScanBwdArgs& a, const BwdPlan& p, float* part, hipStream_t st) {
+    if (p.K == 1) return launch_bwd_k<VT, 1>(a, p, part, st);
+    if (p.K == 2) return launch_bwd_k<VT, 2>(a, p, part, st);
+    return launch_bwd_k<VT, 4>(a, p, part, st);
 }
-
-constexpr int BSW = 16, BPD = 4;
 
 size_t bwd_part_offset(int B, int H, int T, int W, int R) {
     const size_t recb = (size_t)B * H * T * bwd_rec_layout(W, R).bytes;
@@ -474,7 +492,14 @@ size_t sdm_bwd_ws_bytes(int B, int H, int T, int W, int R, int dv) {
     return bytes;
 }
 
+bool sdm_bwd_plan_ok(int W, int R, int dv, int in_dtype) {
+    BwdPlan p;
+    return bwd_plan(W, R, dv, in_dtype, &p);
+}
+
 hipError_t sdm_launch_scan_bwd(const ScanBwdArgs& a, hipStream_t st) {
+    BwdPlan plan;
+    if (!bwd_plan(a.W, a.R, a.dv, a.in_dtype, &plan)) return hipErrorInvalidConfiguration;
     const int S = a.B * a.H;
     {
         SdmProfScope ps(SDM_K_BWD_PREP, st);
@@ -486,13 +511,13 @@ hipError_t sdm_launch_scan_bwd(const ScanBwdArgs& a, hipStream_t st) {
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    const int n_slices = (a.dv + BSW - 1) / BSW;
+    const int n_slices = plan.n_slices;
     float* part = reinterpret_cast<float*>(a.ws + bwd_part_offset(a.B, a.H, a.T, a.W, a.R));
     hipError_t e;
     {
         SdmProfScope ps(SDM_K_BWD_SCAN, st);
-        e = a.in_dtype == SDM_DT_BF16 ? launch_bwd_kk<bf16_t, BSW, BPD>(a, part, n_slices, st)
-                                      : launch_bwd_kk<float, BSW, BPD>(a, part, n_slices, st);
+        e = a.in_dtype == SDM_DT_BF16 ? launch_bwd_kk<bf16_t>(a, plan, part, st)
+                                      : launch_bwd_kk<float>(a, plan, part, st);
     }
     if (e != hipSuccess) return e;
     SdmProfScope ps(SDM_K_BWD_REDUCE, st);

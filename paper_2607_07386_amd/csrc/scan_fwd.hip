@@ -126,8 +126,8 @@ __host__ __device__ constexpr int stage_slots() {
 // Staging of the G records (and v slices) of tokens [u0, u0 + G): global -> registers.
 // Every lane always loads: indices past the end are clamped to valid data (the
 // surplus is never read), so the loads carry no control flow.
-template <typename VT, int SW>
-__device__ __forceinline__ void stage_load(u4v (&st)[4], u2v& stv, const unsigned char* srec,
+template <typename VT, int SW, int NR>
+__device__ __forceinline__ void stage_load(u4v (&st)[NR], u2v& stv, const unsigned char* srec,
                                            const VT* sv, int u0, int T, int dv, int slice,
                                            int rec_bytes, int lane) {
     constexpr int VB = SW * (int)sizeof(VT);
@@ -137,7 +137,7 @@ __device__ __forceinline__ void stage_load(u4v (&st)[4], u2v& stv, const unsigne
     const u4v* src = reinterpret_cast<const u4v*>(srec + (size_t)ub * rec_bytes);
     const int last = cnt * rec_bytes / 16 - 1;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) st[r] = src[min(r * SDM_WAVE + lane, last)];
+    for (int r = 0; r < NR; ++r) st[r] = src[min(r * SDM_WAVE + lane, last)];
     const int tk = min(lane / ppt, cnt - 1);
     const int pc = min(lane % ppt, (dv - slice * SW) * (int)sizeof(VT) / 8 - 1);
     stv = *reinterpret_cast<const u2v*>(
@@ -145,15 +145,15 @@ __device__ __forceinline__ void stage_load(u4v (&st)[4], u2v& stv, const unsigne
 }
 
 // Registers -> LDS rings (slot = token mod NS; a block never wraps: u0 % G == 0).
-template <typename VT, int SW, int NS>
-__device__ __forceinline__ void stage_store(const u4v (&st)[4], u2v stv, unsigned char* rring,
+template <typename VT, int SW, int NS, int NR>
+__device__ __forceinline__ void stage_store(const u4v (&st)[NR], u2v stv, unsigned char* rring,
                                             unsigned char* vring, int u0, int rec_bytes, int lane) {
     constexpr int VB = SW * (int)sizeof(VT);
     constexpr int ppt = VB / 8;
     u4v* dst = reinterpret_cast<u4v*>(rring + (u0 & (NS - 1)) * rec_bytes);
-    const int nchunk = G * rec_bytes / 16;
+    const int nchunk = G * rec_bytes / 16;   // <= NR * 64 (checked by the host plan)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < NR; ++r) {
         const int c = r * SDM_WAVE + lane;
         if (c < nchunk) dst[c] = st[r];
     }
@@ -254,7 +254,7 @@ __device__ __forceinline__ void fwd_token(const FwdCtx<VT, SW, PD, K, SAVE>& c, 
     if (c.rg == 0 && c.colok) st4(c.ystream + (size_t)t * c.dv, yp);
 }
 
-template <typename VT, int SW, int PD, int K, bool SAVE>
+template <typename VT, int SW, int PD, int K, int NR, bool SAVE>
 __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_fwd_kernel(
     const unsigned char* __restrict__ recs, const VT* __restrict__ v, float* __restrict__ mem,
     float* __restrict__ y, float* __restrict__ saved, int T, int dv, int W, int R, int64_t N,
@@ -297,17 +297,17 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_fwd_kernel(
     const unsigned char* srec = recs + (size_t)stream * T * c.L.bytes;
     const VT* sv = v + (size_t)stream * T * dv + slice * SW;
 
-    u4v st[4];
+    u4v st[NR];
     u2v stv;
     v4f Pw[PD][K], Pr[PD][K];
 
     // ---- prologue: records of tokens [0, LEAD-G) in LDS, the next block in
     //      registers, rows of tokens [0, PD) in flight ----
     for (int u0 = 0; u0 < LEAD - G; u0 += G) {
-        stage_load<VT, SW>(st, stv, srec, sv, u0, T, dv, slice, c.L.bytes, lane);
-        stage_store<VT, SW, NS>(st, stv, rring, vring, u0, c.L.bytes, lane);
+        stage_load<VT, SW, NR>(st, stv, srec, sv, u0, T, dv, slice, c.L.bytes, lane);
+        stage_store<VT, SW, NS, NR>(st, stv, rring, vring, u0, c.L.bytes, lane);
     }
-    stage_load<VT, SW>(st, stv, srec, sv, LEAD - G, T, dv, slice, c.L.bytes, lane);
+    stage_load<VT, SW, NR>(st, stv, srec, sv, LEAD - G, T, dv, slice, c.L.bytes, lane);
 #pragma unroll
     for (int j = 0; j < PD; ++j) issue_rows<K, RG, NS>(Pw[j], Pr[j], rring, c.L, c.tab, min(j, T - 1), dv, c.rg);
 
@@ -318,8 +318,8 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_fwd_kernel(
         for (int j = 0; j < PD; ++j) {
             const int t = t0 + j;
             if (j % G == 0) {
-                stage_store<VT, SW, NS>(st, stv, rring, vring, t + LEAD - G, c.L.bytes, lane);
-                stage_load<VT, SW>(st, stv, srec, sv, t + LEAD, T, dv, slice, c.L.bytes, lane);
+                stage_store<VT, SW, NS, NR>(st, stv, rring, vring, t + LEAD - G, c.L.bytes, lane);
+                stage_load<VT, SW, NR>(st, stv, srec, sv, t + LEAD, T, dv, slice, c.L.bytes, lane);
             }
             fwd_token<VT, SW, PD, K, SAVE, NS>(c, Pw[j], Pr[j], t);
             issue_rows<K, RG, NS>(Pw[j], Pr[j], rring, c.L, c.tab, min(t + PD, T - 1), dv, c.rg);
@@ -333,33 +333,54 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_fwd_kernel(
     }
 }
 
-template <typename VT, int SW, int PD, int K, bool SAVE>
-hipError_t launch_fwd_k(const ScanFwdArgs& a, hipStream_t st) {
-    const FwdRec L = fwd_rec_layout(a.W, a.R);
-    constexpr int NS = stage_slots<PD>();
-    const int lds_per_wave = NS * L.bytes + NS * SW * (int)sizeof(VT) + PD * a.W * SW * 4;
-    const int n_slices = (a.dv + SW - 1) / SW;
+constexpr int FWD_SW = 16, FWD_PD = 8;
+
+// Staging registers per lane for a block of G records: enough for every
+// record of a shape with max(W, R) <= 16 K (10 (W + R) + 8 bytes, 16-aligned).
+constexpr int nr_for_k(int K) { return K == 1 ? 2 : (K == 2 ? 3 : 6); }
+
+struct FwdPlan {
+    int K, NR, lds_per_wave, wpb, n_slices;
+};
+
+// Launch geometry of the forward scan; false if the shape cannot be run.
+bool fwd_plan(int W, int R, int dv, int in_dtype, FwdPlan* p) {
+    constexpr int RG = SDM_WAVE / (FWD_SW / 4);
+    const int need = (std::max(W, R) + RG - 1) / RG;
+    if (need > 4) return false;
+    p->K = need <= 1 ? 1 : (need <= 2 ? 2 : 4);
+    p->NR = nr_for_k(p->K);
+    const FwdRec L = fwd_rec_layout(W, R);
+    if (G * L.bytes > p->NR * SDM_WAVE * 16) return false;
+    const int vbytes = in_dtype == SDM_DT_BF16 ? 2 : 4;
+    constexpr int NS = stage_slots<FWD_PD>();
+    p->lds_per_wave = NS * L.bytes + NS * FWD_SW * vbytes + FWD_PD * W * FWD_SW * 4;
+    if (p->lds_per_wave > LDS_LIMIT) return false;
+    p->n_slices = (dv + FWD_SW - 1) / FWD_SW;
+    p->wpb = std::min(std::min(MAX_WPB, p->n_slices), LDS_LIMIT / p->lds_per_wave);
+    return true;
+}
+
+template <typename VT, int K, bool SAVE>
+hipError_t launch_fwd_k(const ScanFwdArgs& a, const FwdPlan& p, hipStream_t st) {
+    constexpr int NR = nr_for_k(K);
     const int S = a.B * a.H;
-    if (lds_per_wave > LDS_LIMIT) return hipErrorInvalidConfiguration;
-    const int wpb = std::min(std::min(MAX_WPB, n_slices), LDS_LIMIT / lds_per_wave);
-    dim3 grid((n_slices + wpb - 1) / wpb, S);
-    const size_t sm = (size_t)lds_per_wave * wpb;
-    auto kfn = scan_fwd_kernel<VT, SW, PD, K, SAVE>;
+    dim3 grid((p.n_slices + p.wpb - 1) / p.wpb, S);
+    const size_t sm = (size_t)p.lds_per_wave * p.wpb;
+    auto kfn = scan_fwd_kernel<VT, FWD_SW, FWD_PD, K, NR, SAVE>;
     hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kfn, grid, dim3(wpb * SDM_WAVE), sm, st,
+    hipLaunchKernelGGL(kfn, grid, dim3(p.wpb * SDM_WAVE), sm, st,
                        a.ws + SDM_WS_HEADER, static_cast<const VT*>(a.v), a.mem, a.y, a.saved, a.T,
-                       a.dv, a.W, a.R, a.N, n_slices, lds_per_wave);
+                       a.dv, a.W, a.R, a.N, p.n_slices, p.lds_per_wave);
     return hipGetLastError();
 }
 
-template <typename VT, int SW, int PD, bool SAVE>
-hipError_t launch_fwd_kk(const ScanFwdArgs& a, hipStream_t st) {
-    constexpr int RG = SDM_WAVE / (SW / 4);
-    const int need = (max(a.W, a.R) + RG - 1) / RG;
-    if (need <= 1) return launch_fwd_k<VT, SW, PD, 1, SAVE>(a, st);
-    if (need <= 2) return launch_fwd_k<VT, SW, PD, 2, SAVE>(a, st);
-    return launch_fwd_k<VT, SW, PD, 4, SAVE>(a, st);
+template <typename VT, bool SAVE>
+hipError_t launch_fwd_kk(const ScanFwdArgs& a, const FwdPlan& p, hipStream_t st) {
+    if (p.K == 1) return launch_fwd_k<VT, 1, SAVE>(a, p, st);
+    if (p.K == 2) return launch_fwd_k<VT, 2, SAVE>(a, p, st);
+    return launch_fwd_k<VT, 4, SAVE>(a, p, st);
 }
 
 template <int PD>
@@ -379,17 +400,23 @@ size_t sdm_fwd_ws_bytes(int B, int H, int T, int W, int R) {
     return SDM_WS_HEADER + (size_t)B * H * T * fwd_rec_layout(W, R).bytes;
 }
 
+bool sdm_fwd_plan_ok(int W, int R, int dv, int in_dtype) {
+    FwdPlan p;
+    return fwd_plan(W, R, dv, in_dtype, &p);
+}
+
 hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st) {
-    constexpr int SW = 16, PD = 8;
+    FwdPlan p;
+    if (!fwd_plan(a.W, a.R, a.dv, a.in_dtype, &p)) return hipErrorInvalidConfiguration;
     hipError_t e;
     {
         SdmProfScope ps(SDM_K_FWD_PREP, st);
-        e = launch_prep<PD>(a, st);
+        e = launch_prep<FWD_PD>(a, st);
     }
     if (e != hipSuccess) return e;
     const bool save = a.saved != nullptr;
     SdmProfScope ps(SDM_K_FWD_SCAN, st);
     if (a.in_dtype == SDM_DT_BF16)
-        return save ? launch_fwd_kk<bf16_t, SW, PD, true>(a, st) : launch_fwd_kk<bf16_t, SW, PD, false>(a, st);
-    return save ? launch_fwd_kk<float, SW, PD, true>(a, st) : launch_fwd_kk<float, SW, PD, false>(a, st);
+        return save ? launch_fwd_kk<bf16_t, true>(a, p, st) : launch_fwd_kk<bf16_t, false>(a, p, st);
+    return save ? launch_fwd_kk<float, true>(a, p, st) : launch_fwd_kk<float, false>(a, p, st);
 }

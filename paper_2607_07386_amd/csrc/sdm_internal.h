@@ -76,6 +76,8 @@ struct ScanFwdArgs {
     unsigned char* ws;   // workspace base (header + records)
 };
 hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st);
+// true if the forward scan has a launch plan for this shape (registers, LDS)
+bool sdm_fwd_plan_ok(int W, int R, int dv, int in_dtype);
 size_t sdm_fwd_ws_bytes(int B, int H, int T, int W, int R);
 
 struct ScanBwdArgs {
@@ -102,6 +104,7 @@ struct ScanBwdArgs {
     unsigned char* ws;
 };
 hipError_t sdm_launch_scan_bwd(const ScanBwdArgs& a, hipStream_t st);
+bool sdm_bwd_plan_ok(int W, int R, int dv, int in_dtype);
 size_t sdm_bwd_ws_bytes(int B, int H, int T, int W, int R, int dv);
 
 hipError_t sdm_launch_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int dv,

@@ -130,3 +130,15 @@ def test_undo_log_matches_paper_memory_figures():
     assert abs(undo / 1e9 - g["paper_gb"]["undo"]) < 0.1
     assert round(per_chunk_states / 1e9, 2) == g["derived_gb"]["checkpoints"]
     assert round(undo / 1e9, 2) == g["derived_gb"]["undo"]
+
+
+def test_every_supported_shape_has_a_launch_plan():
+    """Every W, R <= 64 and d_v the header allows gets a scan plan whose staged
+    per-token records fit the staging registers and LDS: validation gets past
+    the plan and stops at the (deliberately) too-small workspace."""
+    for W in range(1, 65):
+        for R in (1, 7, 16, 17, 31, 32, 33, 48, 63, 64):
+            for dv, dt in ((4, 0), (36, 1), (128, 1), (960, 0), (4096, 1)):
+                assert fwd(W=W, R=R, dv=dv, dt=dt, wsb=0) == -3, (W, R, dv, dt)
+                assert bwd(W=W, R=R, dv=dv, dt=dt, wsb=0, cbq=None, cbk=None, dq=None, dkk=None) == -3, \
+                    (W, R, dv, dt)
