@@ -54,7 +54,10 @@ int check_scan_common(const int32_t* w_idx, const float* w_val, int W, const int
     if (d_v > 4096) return fail(SDM_ERR_UNSUPPORTED, "d_v must be <= 4096");
     if (N < 1 || N > (int64_t)1 << 31) return fail(SDM_ERR_INVALID_ARG, "N must be in [1, 2^31]");
     if (!valid_dtype(in_dtype)) return fail(SDM_ERR_INVALID_ARG, "in_dtype must be SDM_F32 or SDM_BF16");
-    if (!w_idx || !w_val || !r_idx || !r_val || !v || !alpha || !beta || !mem)
+    // arrays of zero size may come as NULL (empty tensors have no storage)
+    const bool tok = (int64_t)B * H * T > 0;
+    if ((tok && (!w_idx || !w_val || !r_idx || !r_val || !v || !alpha || !beta)) ||
+        ((int64_t)B * H > 0 && !mem))
         return fail(SDM_ERR_INVALID_ARG, "null input pointer");
     if (!aligned(w_idx, 16) || !aligned(w_val, 16) || !aligned(r_idx, 16) || !aligned(r_val, 16) ||
         !aligned(v, 16) || !aligned(alpha, 4) || !aligned(beta, 4) || !aligned(mem, 16))
@@ -178,10 +181,10 @@ int sdm_address(const void* x, int x_dtype, const void* codebook, int B, int H, 
     } else if (d_k != 2 * s) {
         return fail(SDM_ERR_INVALID_ARG, "direct mode needs d_k == 2*sqrt(N)");
     }
+    if ((int64_t)B * H * T == 0) return SDM_OK;   // nothing is read or written
     if (!x || !idx || !val) return fail(SDM_ERR_INVALID_ARG, "null pointer");
     if (!aligned(x, 16) || !aligned(idx, 4) || !aligned(val, 4) || (score && !aligned(score, 4)))
         return fail(SDM_ERR_INVALID_ARG, "misaligned pointer");
-    if ((int64_t)B * H * T == 0) return SDM_OK;
     hipError_t e;
     {
         SdmProfScope ps(SDM_K_ADDRESS, (hipStream_t)stream);
@@ -215,6 +218,7 @@ int sdm_scan_fwd(const int32_t* w_idx, const float* w_val, int W, const int32_t*
     int rc = check_scan_common(w_idx, w_val, W, r_idx, r_val, R, v, alpha, beta, in_dtype, mem, B,
                                H, T, d_v, N);
     if (rc != SDM_OK) return rc;
+    if ((int64_t)B * H * T == 0) return SDM_OK;   // nothing is read or written
     if (!y || !aligned(y, 16)) return fail(SDM_ERR_INVALID_ARG, "y must be a 16-byte aligned pointer");
     if (saved) {
         if (!aligned(saved, 16)) return fail(SDM_ERR_INVALID_ARG, "misaligned saved buffer");
@@ -231,7 +235,6 @@ int sdm_scan_fwd(const int32_t* w_idx, const float* w_val, int W, const int32_t*
     hipStream_t st = (hipStream_t)stream;
     hipError_t e = sdm_launch_zero_words(workspace, 4, st);
     if (e != hipSuccess) return hip_fail(e, "sdm_scan_fwd flag reset");
-    if ((int64_t)B * H * T == 0) return SDM_OK;
     ScanFwdArgs a;
     a.w_idx = w_idx; a.w_val = w_val; a.r_idx = r_idx; a.r_val = r_val;
     a.v = v; a.alpha = alpha; a.beta = beta; a.in_dtype = in_dtype;
@@ -254,7 +257,8 @@ int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, cons
                                H, T, d_v, N);
     if (rc != SDM_OK) return rc;
     if (chunk < 1) return fail(SDM_ERR_INVALID_ARG, "chunk must be >= 1");
-    if (!saved || !dy || !dv || !dalpha || !dbeta || !dmem0)
+    const bool tok = (int64_t)B * H * T > 0;
+    if ((tok && (!saved || !dy || !dv || !dalpha || !dbeta)) || ((int64_t)B * H > 0 && !dmem0))
         return fail(SDM_ERR_INVALID_ARG, "null pointer (saved, dy, dv, dalpha, dbeta, dmem0 are required)");
     if (!aligned(saved, 16) || !aligned(dy, 16) || !aligned(dv, 16) || !aligned(dmem0, 16) ||
         (dmem_T && !aligned(dmem_T, 16)))
