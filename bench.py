@@ -92,6 +92,9 @@ def main():
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     ap.add_argument("--only", choices=["fwd", "train"], default=None,
                     help="run one leg only (profiling runs)")
+    ap.add_argument("--calib", action="store_true",
+                    help="first run one plain 512 MiB copy (sdm_mem_init from a [16, 65536, 128] fp32 "
+                         "source): the reference dispatch for scaling HBM counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
@@ -114,6 +117,15 @@ def main():
     stream = torch.cuda.current_stream()
     out = {"metric": METRIC}
     w = synth.WORKLOADS[1]
+
+    if args.calib:
+        src = torch.ones((16, 65536, 128), dtype=torch.float32, device=dev)
+        dst = torch.empty((1, 16, 65536, 128), dtype=torch.float32, device=dev)
+        torch.cuda.synchronize()
+        sdm.mem_init(dst, src)
+        torch.cuda.synchronize()
+        out["calib_copy_bytes"] = src.numel() * 4
+        del src, dst
 
     # ------------------------------------------------------------ forward
     if args.only in (None, "fwd"):

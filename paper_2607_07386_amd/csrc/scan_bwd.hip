@@ -25,109 +25,6 @@ namespace {
 constexpr int G = 4;
 constexpr int MAX_WPB = 4;
 constexpr int LDS_LIMIT = 160 * 1024;
-constexpr int PT = 64;
-
-template <int PD>
-__global__ __launch_bounds__(256) void bwd_prep_kernel(const int32_t* __restrict__ w_idx,
-                                                       const float* __restrict__ w_val,
-                                                       const int32_t* __restrict__ r_idx,
-                                                       const float* __restrict__ r_val,
-                                                       const void* __restrict__ alpha,
-                                                       const void* __restrict__ beta, int in_dtype,
-                                                       int T, int W, int R, int64_t N,
-                                                       unsigned char* __restrict__ recs,
-                                                       unsigned int* __restrict__ err) {
-    extern __shared__ int sl[];   // [(PT + PD - 1)][W + R] clamped slots, write then read
-    const BwdRec L = bwd_rec_layout(W, R);
-    const int stream = blockIdx.y;
-    const int t0 = blockIdx.x * PT;
-    const int ntok = min(PT, T - t0);
-    const int nrow = W + R;
-    const int span = min(PT + PD - 1, T - t0);   // tokens t0 .. t0+span-1 (later tokens included)
-    const size_t sbase = (size_t)stream * T;
-    unsigned int bad = 0;
-    for (int i = threadIdx.x; i < span * nrow; i += blockDim.x) {
-        const int t = t0 + i / nrow, r = i % nrow;
-        int s = r < W ? w_idx[(sbase + t) * W + r] : r_idx[(sbase + t) * R + (r - W)];
-        if (s < 0 || s >= N) {
-            bad = 1;
-            s = 0;
-        }
-        sl[i] = s;
-    }
-    __syncthreads();
-    for (int i = threadIdx.x; i < ntok * nrow; i += blockDim.x) {
-        const int tl = i / nrow, r = i % nrow;
-        const int t = t0 + tl;
-        unsigned char* rec = recs + (sbase + t) * L.bytes;
-        const int slot = sl[i];
-        if (r < W) {
-            reinterpret_cast<int*>(rec)[r] = slot;
-            reinterpret_cast<float*>(rec + L.off_wval)[r] = w_val[(sbase + t) * W + r];
-        } else {
-            reinterpret_cast<int*>(rec + L.off_rslot)[r - W] = slot;
-            reinterpret_cast<float*>(rec + L.off_rval)[r - W] = r_val[(sbase + t) * R + (r - W)];
-        }
-        // G source: latest (smallest d) later token touching the slot; within a
-        // token the write adjoint (entry R + n) supersedes the read adjoint (entry m).
-        short lg = -1;
-        if (r < W) {   // d = 0: this token's read adjoint already updated G[slot]
-            const int* rl = sl + tl * nrow + W;
-            for (int m = 0; m < R; ++m)
-                if (rl[m] == slot) {
-                    lg = (short)m;
-                    break;
-                }
-        }
-        for (int d = 1; d < PD && lg < 0; ++d) {
-            if (t + d >= T) break;
-            const int* wl = sl + (tl + d) * nrow;
-            for (int n = 0; n < W; ++n)
-                if (wl[n] == slot) {
-                    lg = (short)((d << 8) | (R + n));
-                    break;
-                }
-            if (lg >= 0) break;
-            for (int m = 0; m < R; ++m)
-                if (wl[W + m] == slot) {
-                    lg = (short)((d << 8) | m);
-                    break;
-                }
-        }
-        if (r < W) {
-            reinterpret_cast<short*>(rec + L.off_lgw)[r] = lg;
-        } else {
-            reinterpret_cast<short*>(rec + L.off_lgr)[r - W] = lg;
-            // M source for a read row: the earliest later token that undid a write to it
-            short lm = -1;
-            for (int d = 1; d < PD && lm < 0; ++d) {
-                if (t + d >= T) break;
-                const int* wl = sl + (tl + d) * nrow;
-                for (int n = 0; n < W; ++n)
-                    if (wl[n] == slot) {
-                        lm = (short)((d << 8) | n);
-                        break;
-                    }
-            }
-            reinterpret_cast<short*>(rec + L.off_lm)[r - W] = lm;
-        }
-    }
-    for (int tl = threadIdx.x; tl < ntok; tl += blockDim.x) {
-        const size_t o = sbase + t0 + tl;
-        float al, be;
-        if (in_dtype == SDM_DT_BF16) {
-            al = to_f32(static_cast<const bf16_t*>(alpha)[o]);
-            be = to_f32(static_cast<const bf16_t*>(beta)[o]);
-        } else {
-            al = static_cast<const float*>(alpha)[o];
-            be = static_cast<const float*>(beta)[o];
-        }
-        unsigned char* rec = recs + o * L.bytes;
-        reinterpret_cast<float*>(rec + L.off_ab)[0] = al;
-        reinterpret_cast<float*>(rec + L.off_ab)[1] = be;
-    }
-    if (bad) atomicOr(err, 1u);
-}
 
 template <int PD>
 __host__ __device__ constexpr int bstage_lead() {
@@ -427,7 +324,7 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(const float* __restrict
     }
 }
 
-constexpr int BSW = 16, BPD = 4;
+constexpr int BSW = 16, BPD = SDM_BWD_PD;
 
 // Staging registers per lane for a block of G backward records (at most
 // 8 (W + R) + 4 R + 2 W + 8 bytes each) of a shape with max(W, R) <= 16 K.
@@ -503,12 +400,7 @@ hipError_t sdm_launch_scan_bwd(const ScanBwdArgs& a, hipStream_t st) {
     const int S = a.B * a.H;
     {
         SdmProfScope ps(SDM_K_BWD_PREP, st);
-        dim3 grid((a.T + PT - 1) / PT, S);
-        const size_t sm = (size_t)(PT + BPD - 1) * (a.W + a.R) * sizeof(int);
-        hipLaunchKernelGGL(bwd_prep_kernel<BPD>, grid, dim3(256), sm, st, a.w_idx, a.w_val, a.r_idx,
-                           a.r_val, a.alpha, a.beta, a.in_dtype, a.T, a.W, a.R, a.N,
-                           a.ws + SDM_WS_HEADER, reinterpret_cast<unsigned int*>(a.ws));
-        hipError_t e = hipGetLastError();
+        hipError_t e = sdm_launch_bwd_prep<BPD>(a, st);
         if (e != hipSuccess) return e;
     }
     const int n_slices = plan.n_slices;

@@ -28,91 +28,6 @@ namespace {
 constexpr int G = 4;            // tokens per staging block
 constexpr int MAX_WPB = 4;      // waves (column slices) per workgroup, at most
 constexpr int LDS_LIMIT = 160 * 1024;
-constexpr int PT = 64;          // tokens per prep workgroup
-
-template <int PD>
-__global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict__ w_idx,
-                                                       const float* __restrict__ w_val,
-                                                       const int32_t* __restrict__ r_idx,
-                                                       const float* __restrict__ r_val,
-                                                       const void* __restrict__ alpha,
-                                                       const void* __restrict__ beta, int in_dtype,
-                                                       int T, int W, int R, int64_t N,
-                                                       unsigned char* __restrict__ recs,
-                                                       unsigned int* __restrict__ err) {
-    extern __shared__ int wl[];   // [(PT + PD - 1)][W] clamped write slots
-    const FwdRec L = fwd_rec_layout(W, R);
-    const int stream = blockIdx.y;
-    const int t0 = blockIdx.x * PT;
-    const int tb = t0 - (PD - 1);
-    const int ntok = min(PT, T - t0);
-    const size_t sbase = (size_t)stream * T;
-    unsigned int bad = 0;
-    for (int i = threadIdx.x; i < (ntok + PD - 1) * W; i += blockDim.x) {
-        const int t = tb + i / W;
-        int s = -1;
-        if (t >= 0) {
-            s = w_idx[(sbase + t) * W + i % W];
-            if (s < 0 || s >= N) {
-                bad = 1;
-                s = 0;
-            }
-        }
-        wl[i] = s;
-    }
-    __syncthreads();
-    const int nrow = W + R;
-    for (int i = threadIdx.x; i < ntok * nrow; i += blockDim.x) {
-        const int tl = i / nrow, r = i % nrow;
-        const int t = t0 + tl;
-        unsigned char* rec = recs + (sbase + t) * L.bytes;
-        int slot, dmin;
-        float wgt;
-        if (r < W) {
-            slot = wl[(tl + PD - 1) * W + r];
-            wgt = w_val[(sbase + t) * W + r];
-            dmin = 1;
-            reinterpret_cast<int*>(rec)[r] = slot;
-            reinterpret_cast<float*>(rec + L.off_wval)[r] = wgt;
-        } else {
-            slot = r_idx[(sbase + t) * R + (r - W)];
-            if (slot < 0 || slot >= N) {
-                bad = 1;
-                slot = 0;
-            }
-            wgt = r_val[(sbase + t) * R + (r - W)];
-            dmin = 0;
-            reinterpret_cast<int*>(rec + L.off_rslot)[r - W] = slot;
-            reinterpret_cast<float*>(rec + L.off_rval)[r - W] = wgt;
-        }
-        short link = -1;
-        for (int d = dmin; d < PD && link < 0; ++d) {
-            if (t - d < 0) break;
-            const int* lst = wl + (tl + PD - 1 - d) * W;
-            for (int n = 0; n < W; ++n)
-                if (lst[n] == slot) {
-                    link = (short)((d << 8) | n);
-                    break;
-                }
-        }
-        reinterpret_cast<short*>(rec + L.off_link)[r] = link;
-    }
-    for (int tl = threadIdx.x; tl < ntok; tl += blockDim.x) {
-        const size_t o = sbase + t0 + tl;
-        float al, be;
-        if (in_dtype == SDM_DT_BF16) {
-            al = to_f32(static_cast<const bf16_t*>(alpha)[o]);
-            be = to_f32(static_cast<const bf16_t*>(beta)[o]);
-        } else {
-            al = static_cast<const float*>(alpha)[o];
-            be = static_cast<const float*>(beta)[o];
-        }
-        unsigned char* rec = recs + o * L.bytes;
-        reinterpret_cast<float*>(rec + L.off_ab)[0] = al;
-        reinterpret_cast<float*>(rec + L.off_ab)[1] = be;
-    }
-    if (bad) atomicOr(err, 1u);
-}
 
 template <int PD>
 __host__ __device__ constexpr int stage_lead() {   // L: records of token u are staged by step u-PD
@@ -333,7 +248,7 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_fwd_kernel(
     }
 }
 
-constexpr int FWD_SW = 16, FWD_PD = 8;
+constexpr int FWD_SW = 16, FWD_PD = SDM_FWD_PD;
 
 // Staging registers per lane for a block of G records: enough for every
 // record of a shape with max(W, R) <= 16 K (10 (W + R) + 8 bytes, 16-aligned).
@@ -383,17 +298,6 @@ hipError_t launch_fwd_kk(const ScanFwdArgs& a, const FwdPlan& p, hipStream_t st)
     return launch_fwd_k<VT, 4, SAVE>(a, p, st);
 }
 
-template <int PD>
-hipError_t launch_prep(const ScanFwdArgs& a, hipStream_t st) {
-    const int S = a.B * a.H;
-    dim3 grid((a.T + PT - 1) / PT, S);
-    const size_t sm = (size_t)(PT + PD - 1) * a.W * sizeof(int);
-    hipLaunchKernelGGL(fwd_prep_kernel<PD>, grid, dim3(256), sm, st, a.w_idx, a.w_val, a.r_idx,
-                       a.r_val, a.alpha, a.beta, a.in_dtype, a.T, a.W, a.R, a.N,
-                       a.ws + SDM_WS_HEADER, reinterpret_cast<unsigned int*>(a.ws));
-    return hipGetLastError();
-}
-
 }  // namespace
 
 size_t sdm_fwd_ws_bytes(int B, int H, int T, int W, int R) {
@@ -411,7 +315,7 @@ hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st) {
     hipError_t e;
     {
         SdmProfScope ps(SDM_K_FWD_PREP, st);
-        e = launch_prep<FWD_PD>(a, st);
+        e = sdm_launch_fwd_prep<FWD_PD>(a, st);
     }
     if (e != hipSuccess) return e;
     const bool save = a.saved != nullptr;

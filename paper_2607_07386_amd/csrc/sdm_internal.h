@@ -7,6 +7,11 @@
 #define SDM_DT_F32 0
 #define SDM_DT_BF16 1
 
+// Prefetch depth (tokens in flight per wave) of the forward and backward scans;
+// the prep kernels compute read-after-write links for exactly this window.
+#define SDM_FWD_PD 8
+#define SDM_BWD_PD 4
+
 // Per-token record of the forward scan (written by the prep kernel, staged in
 // LDS by the scan): slots and weights of both sides, forwarding links, gates.
 struct FwdRec {
@@ -80,6 +85,9 @@ hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st);
 bool sdm_fwd_plan_ok(int W, int R, int dv, int in_dtype);
 size_t sdm_fwd_ws_bytes(int B, int H, int T, int W, int R);
 
+template <int PD>
+hipError_t sdm_launch_fwd_prep(const ScanFwdArgs& a, hipStream_t st);
+
 struct ScanBwdArgs {
     const int32_t* w_idx;
     const float* w_val;
@@ -104,6 +112,8 @@ struct ScanBwdArgs {
     unsigned char* ws;
 };
 hipError_t sdm_launch_scan_bwd(const ScanBwdArgs& a, hipStream_t st);
+template <int PD>
+hipError_t sdm_launch_bwd_prep(const ScanBwdArgs& a, hipStream_t st);
 bool sdm_bwd_plan_ok(int W, int R, int dv, int in_dtype);
 size_t sdm_bwd_ws_bytes(int B, int H, int T, int W, int R, int dv);
 
