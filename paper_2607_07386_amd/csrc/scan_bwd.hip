@@ -141,14 +141,14 @@ __device__ __forceinline__ void bwd_token(const BwdCtx& c, const BwdBuf<K>& b, i
         const bool rok = m < c.R;
         const int mm = rok ? m : 0;
         const int l1 = lm[mm];
-        const int i1 = l1 >= 0 ? (((t + (l1 >> 8)) & (PD - 1)) * c.W + (l1 & 255)) : 0;
+        const int i1 = l1 >= 0 ? (((t + (l1 >> 8)) & (PD - 1)) * c.W + min(l1 & 255, c.W - 1)) : 0;
         const v4f Mv = v4sel(l1 >= 0, ld4(c.pring + i1 * SW + c.cq * 4), b.Mr[k]);
         float rb = c.colok ? v4dot(yb, Mv) : 0.f;
 #pragma unroll
         for (int q = 1; q < CQ; q <<= 1) rb += __shfl_xor(rb, q, SDM_WAVE);
         if (rok && c.cq == 0) prow[m] = rb;
         const int l2 = lgr[mm];
-        const int i2 = l2 >= 0 ? (((t + (l2 >> 8)) & (PD - 1)) * RW + (l2 & 255)) : 0;
+        const int i2 = l2 >= 0 ? (((t + (l2 >> 8)) & (PD - 1)) * RW + min(l2 & 255, RW - 1)) : 0;
         v4f g = v4sel(l2 >= 0, ld4(c.gring + i2 * SW + c.cq * 4), b.Gr[k]);
         const float rho = rok ? reinterpret_cast<const float*>(rec + L.off_rval)[mm] : 0.f;
         g = v4fma(rho, yb, g);
@@ -167,7 +167,7 @@ __device__ __forceinline__ void bwd_token(const BwdCtx& c, const BwdBuf<K>& b, i
         const bool rok = n < c.W;
         const int nn = rok ? n : 0;
         const int l = lgw[nn];
-        const int ig = l >= 0 ? (((t + (l >> 8)) & (PD - 1)) * RW + (l & 255)) : 0;
+        const int ig = l >= 0 ? (((t + (l >> 8)) & (PD - 1)) * RW + min(l & 255, RW - 1)) : 0;
         gn[k] = v4sel(rok, v4sel(l >= 0, ld4(c.gring + ig * SW + c.cq * 4), b.Gw[k]), v4zero());
         D[k] = v4sel(rok, al * b.Ps[k], v4zero());
         kap[k] = rok ? reinterpret_cast<const float*>(rec + L.off_wval)[nn] : 0.f;

@@ -128,7 +128,7 @@ __device__ __forceinline__ void fwd_token(const FwdCtx<VT, SW, PD, K, SAVE>& c, 
         const bool rok = n < c.W;
         const int nn = rok ? n : 0;
         const int l = lk[nn];
-        const int fidx = l >= 0 ? (((t - (l >> 8)) & (PD - 1)) * c.W + (l & 255)) : 0;
+        const int fidx = l >= 0 ? (((t - (l >> 8)) & (PD - 1)) * c.W + min(l & 255, c.W - 1)) : 0;
         const v4f f = ld4(c.fring + fidx * SW + c.cq * 4);
         v4f P = v4sel(l >= 0, f, Pw[k]);
         P = v4sel(rok, P, v4zero());
@@ -158,7 +158,7 @@ __device__ __forceinline__ void fwd_token(const FwdCtx<VT, SW, PD, K, SAVE>& c, 
         const bool rok = m < c.R;
         const int mm = rok ? m : 0;
         const int l = lk[c.W + mm];
-        const int fidx = l >= 0 ? (((t - (l >> 8)) & (PD - 1)) * c.W + (l & 255)) : 0;
+        const int fidx = l >= 0 ? (((t - (l >> 8)) & (PD - 1)) * c.W + min(l & 255, c.W - 1)) : 0;
         const v4f f = ld4(c.fring + fidx * SW + c.cq * 4);
         const v4f P = v4sel(l >= 0, f, Pr[k]);
         const float rho = rok ? reinterpret_cast<const float*>(rec + L.off_rval)[mm] : 0.f;

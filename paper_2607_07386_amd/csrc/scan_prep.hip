@@ -109,7 +109,7 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
     }
     for (int i = threadIdx.x; i < ntok * R; i += blockDim.x)
         rl[i] = clamp_slot(r_idx[(sbase + t0) * R + i], N, bad);
-    for (int i = threadIdx.x; i < ntok * nrow; i += blockDim.x) lk[i] = INT_MAX;
+    for (int i = threadIdx.x; i < PT * nrow; i += blockDim.x) lk[i] = INT_MAX;
     __syncthreads();
     for (int i = threadIdx.x; i < nw + ntok; i += blockDim.x) {
         if (i < nw)
@@ -211,7 +211,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const int32_t* __restrict
         wl[i] = clamp_slot(w_idx[(sbase + t0) * W + i], N, bad);
     for (int i = threadIdx.x; i < span * R; i += blockDim.x)
         rl[i] = clamp_slot(r_idx[(sbase + t0) * R + i], N, bad);
-    for (int i = threadIdx.x; i < ntok * (2 * R + W); i += blockDim.x) km[i] = INT_MAX;
+    for (int i = threadIdx.x; i < PT * (2 * R + W); i += blockDim.x) km[i] = INT_MAX;   // km, kgr, kgw
     __syncthreads();
     for (int i = threadIdx.x; i < 2 * span; i += blockDim.x) {
         if (i < span)

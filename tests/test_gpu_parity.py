@@ -380,3 +380,112 @@ def test_full_c4_training():
         if k != "mem_restored_bit_exact":
             assert e <= tol_for(w), (k, e)
     assert errs["mem_restored_bit_exact"]
+
+
+# ------------------------------------------------- prep records (read-after-write links)
+FWD_PD, BWD_PD = 8, 4
+
+
+def _rec_fwd(W, R):
+    off_link = 8 * W + 8 * R
+    off_ab = (off_link + 2 * (W + R) + 3) & ~3
+    return off_link, off_ab, (off_ab + 8 + 15) & ~15
+
+
+def _rec_bwd(W, R):
+    off_lm = 8 * W + 8 * R
+    off_ab = (off_lm + 2 * (2 * R + W) + 3) & ~3
+    return off_lm, off_ab, (off_ab + 8 + 15) & ~15
+
+
+def _links_fwd(wi, ri, PD):
+    T, W = wi.shape
+    R = ri.shape[1]
+    out = np.full((T, W + R), -1, np.int64)
+    for t in range(T):
+        for r in range(W + R):
+            slot = wi[t, r] if r < W else ri[t, r - W]
+            for d in range(1 if r < W else 0, PD):
+                if t - d < 0:
+                    break
+                hit = np.nonzero(wi[t - d] == slot)[0]
+                if hit.size:
+                    out[t, r] = (d << 8) | hit[0]
+                    break
+    return out
+
+
+def _links_bwd(wi, ri, PD):
+    T, W = wi.shape
+    R = ri.shape[1]
+    lm = np.full((T, R), -1, np.int64)
+    lgr = np.full((T, R), -1, np.int64)
+    lgw = np.full((T, W), -1, np.int64)
+
+    def g_source(t, slot, allow_self):
+        if allow_self:
+            hit = np.nonzero(ri[t] == slot)[0]
+            if hit.size:
+                return int(hit[0])
+        for d in range(1, PD):
+            if t + d >= T:
+                break
+            hw = np.nonzero(wi[t + d] == slot)[0]
+            if hw.size:
+                return (d << 8) | (R + int(hw[0]))
+            hr = np.nonzero(ri[t + d] == slot)[0]
+            if hr.size:
+                return (d << 8) | int(hr[0])
+        return -1
+
+    for t in range(T):
+        for m in range(R):
+            slot = ri[t, m]
+            for d in range(1, PD):
+                if t + d >= T:
+                    break
+                hw = np.nonzero(wi[t + d] == slot)[0]
+                if hw.size:
+                    lm[t, m] = (d << 8) | int(hw[0])
+                    break
+            lgr[t, m] = g_source(t, slot, False)
+        for n in range(W):
+            lgw[t, n] = g_source(t, wi[t, n], True)
+    return np.concatenate([lm, lgr, lgw], 1)
+
+
+@pytest.mark.parametrize("sorted_lists", [True, False])
+def test_prep_links_match_bruteforce(sorted_lists):
+    """Links in the staged per-token records equal a brute-force search, for the
+    forward and the backward window, across workgroup boundaries (T = 150 is
+    64 + 64 + 22 tokens) and for unsorted slot lists."""
+    rng = np.random.default_rng(77)
+    S, T, N, W, R, dv = 2, 150, 24, 5, 4, 8
+    wi = np.stack([np.stack([rng.choice(N, W, replace=False) for _ in range(T)]) for _ in range(S)]).astype(np.int32)
+    ri = np.stack([np.stack([rng.choice(N, R, replace=False) for _ in range(T)]) for _ in range(S)]).astype(np.int32)
+    if sorted_lists:
+        wi, ri = np.sort(wi, -1), np.sort(ri, -1)
+    t_ = lambda a: torch.from_numpy(np.ascontiguousarray(a))[:, None].to(DEV)
+    wv = t_(rng.random((S, T, W)).astype(np.float32))
+    rv = t_(rng.random((S, T, R)).astype(np.float32))
+    v = t_(rng.standard_normal((S, T, dv)).astype(np.float32))
+    g = t_(rng.random((S, T)).astype(np.float32))
+    mem = torch.zeros((S, 1, N, dv), device=DEV)
+    ws = sdm.fwd_workspace(S, 1, T, W, R, DEV)
+    saved = sdm.saved_buffer(S, 1, T, W, dv, DEV)
+    sdm.scan_fwd(t_(wi), wv, t_(ri), rv, v, g, g, mem, saved=saved, workspace=ws)
+    torch.cuda.synchronize()
+    off_link, _, rec = _rec_fwd(W, R)
+    raw = np_(ws)[256:256 + S * T * rec].reshape(S, T, rec)
+    got = raw[:, :, off_link:off_link + 2 * (W + R)].copy().view(np.int16).astype(np.int64)
+    for s in range(S):
+        np.testing.assert_array_equal(got[s], _links_fwd(wi[s], ri[s], FWD_PD))
+    bws = sdm.bwd_workspace(S, 1, T, W, R, dv, DEV)
+    sdm.scan_bwd(t_(wi), wv, t_(ri), rv, v, g, g, mem, saved, torch.zeros_like(v), workspace=bws,
+                 want_dqk=False)
+    torch.cuda.synchronize()
+    off_lm, _, rec = _rec_bwd(W, R)
+    raw = np_(bws)[256:256 + S * T * rec].reshape(S, T, rec)
+    got = raw[:, :, off_lm:off_lm + 2 * (2 * R + W)].copy().view(np.int16).astype(np.int64)
+    for s in range(S):
+        np.testing.assert_array_equal(got[s], _links_bwd(wi[s], ri[s], BWD_PD))
