@@ -6,12 +6,16 @@
 //  A. sub-key scores of the tile into LDS: bf16 codebooks on the matrix
 //     cores (v_mfma_f32_16x16x32_bf16: 16 tokens x 16 sub-keys x 32 deep),
 //     fp32 codebooks with plain FMAs, direct mode by copying x.
-//  B. per token (one wave): top-k of each half under (score desc, id asc)
-//     by bisection of the k-th largest order-preserving key with wave
-//     ballots, then the shortlist ranked by the same order.
+//  B. per token (one wave): top-k of each half under (score desc, id asc).
+//     Keys are 64-bit (order-preserving score bits, inverted id), so the
+//     order is total and ties go to the lower id.  The k-th largest of the
+//     64 per-lane maxima is a lower bound that at least k keys reach; the
+//     keys at or above it (about 40 for k = 32) are bitonic-sorted across the
+//     wave, which yields the ranked shortlist.  More than 64 survivors (or
+//     k > 32) take an exact bisection of the k-th key with wave ballots.
 //  C. candidates (i, j) of the two ranked shortlists with (i+1)(j+1) <= k
-//     (every other pair has >= k pairs ranked above it), bisection again,
-//     ties to the lower flat id, then sort by id and softmax.
+//     (every other pair has >= k pairs ranked above it), selected the same
+//     way, then sorted by slot id and softmax-normalised.
 #include "sdm_common.h"
 #include "sdm_internal.h"
 
@@ -89,10 +93,106 @@ __device__ void compact(const bool (&sel)[E], const float (&sc)[E], const int (&
     }
 }
 
+// Composite order key: larger key = higher score, or equal score and lower id.
+__device__ __forceinline__ uint64_t ckey(float score, uint32_t id) {
+    return ((uint64_t)ord_key(score) << 32) | (uint32_t)(~id);
+}
+__device__ __forceinline__ float ckey_score(uint64_t k) { return key_to_float((uint32_t)(k >> 32)); }
+__device__ __forceinline__ int ckey_id(uint64_t k) { return (int)(~(uint32_t)k); }
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
+    const uint32_t lo = __shfl_xor((uint32_t)v, m, SDM_WAVE);
+    const uint32_t hi = __shfl_xor((uint32_t)(v >> 32), m, SDM_WAVE);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Bitonic sort of one key per lane across the wave, descending (lane 0 holds
+// the largest).  Equal keys never swap, so padding keys stay padding.
+__device__ __forceinline__ uint64_t wave_sort_desc_u64(uint64_t key) {
+    const int lane = lane_id();
+#pragma unroll
+    for (int kk = 2; kk <= SDM_WAVE; kk <<= 1) {
+#pragma unroll
+        for (int j = kk >> 1; j > 0; j >>= 1) {
+            const uint64_t o = shfl_xor_u64(key, j);
+            const bool keep_max = ((lane & j) == 0) == ((lane & kk) == 0);
+            key = keep_max ? (o > key ? o : key) : (o < key ? o : key);
+        }
+    }
+    return key;
+}
+__device__ __forceinline__ uint32_t wave_sort_desc_u32(uint32_t key) {
+    const int lane = lane_id();
+#pragma unroll
+    for (int kk = 2; kk <= SDM_WAVE; kk <<= 1) {
+#pragma unroll
+        for (int j = kk >> 1; j > 0; j >>= 1) {
+            const uint32_t o = __shfl_xor(key, j, SDM_WAVE);
+            const bool keep_max = ((lane & j) == 0) == ((lane & kk) == 0);
+            key = keep_max ? max(o, key) : min(o, key);
+        }
+    }
+    return key;
+}
+// Ascending sort of keys with a payload riding along.
+__device__ __forceinline__ void wave_sort_asc_u32(uint32_t& key, float& pay) {
+    const int lane = lane_id();
+#pragma unroll
+    for (int kk = 2; kk <= SDM_WAVE; kk <<= 1) {
+#pragma unroll
+        for (int j = kk >> 1; j > 0; j >>= 1) {
+            const uint32_t o = __shfl_xor(key, j, SDM_WAVE);
+            const float op = __shfl_xor(pay, j, SDM_WAVE);
+            const bool keep_min = ((lane & j) == 0) == ((lane & kk) == 0);
+            const bool take = keep_min ? (o < key) : (o > key);
+            key = take ? o : key;
+            pay = take ? op : pay;
+        }
+    }
+}
+
+// Exact top-k (k <= 32 for the fast path) of E keys per lane, returned sorted
+// descending with lane i holding rank i (lanes >= k: padding).  The k-th
+// largest per-lane maximum bounds the answer from below (at least k keys reach
+// it), so only the keys at or above it are sorted; returns false when more
+// than 64 survive, and the caller then takes the bisection path.
+template <int E>
+__device__ __forceinline__ bool topk_sorted(const uint64_t (&key)[E], int ne, int k, uint64_t* buf,
+                                            uint64_t& top) {
+    const int lane = lane_id();
+    if (E == 1 || ne == 1) {
+        top = wave_sort_desc_u64(key[0]);
+        return true;
+    }
+    uint64_t m = key[0];
+#pragma unroll
+    for (int e = 1; e < E; ++e)
+        if (e < ne) m = key[e] > m ? key[e] : m;
+    const uint32_t srt = wave_sort_desc_u32((uint32_t)(m >> 32));
+    const uint32_t tau = __shfl(srt, k - 1, SDM_WAVE);
+    int base = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        if (e < ne) {
+            const bool c = key[e] != 0ull && (uint32_t)(key[e] >> 32) >= tau;
+            const unsigned long long msk = __ballot(c);
+            const int p = base + mbcnt64(msk);
+            if (c && p < SDM_WAVE) buf[p] = key[e];
+            base += popc64(msk);
+        }
+    }
+    if (base > SDM_WAVE) return false;
+    wait_lds();
+    __builtin_amdgcn_wave_barrier();
+    const uint64_t v = lane < base ? buf[lane] : 0ull;
+    top = wave_sort_desc_u64(v);
+    return true;
+}
+
 // Stage-1 selection of one half: top-k of s sub-scores, ranked (score desc,
 // id asc) into out[0 .. k).
 template <int E>
-__device__ void half_topk(const float* sc_row, int s, int k, Entry* scratch, Entry* out) {
+__device__ void half_topk_bisect(const float* sc_row, int s, int k, Entry* scratch, Entry* out) {
     const int lane = lane_id();
     uint32_t key[E];
     float sc[E];
@@ -123,6 +223,29 @@ __device__ void half_topk(const float* sc_row, int s, int k, Entry* scratch, Ent
     wait_lds();
 }
 
+// Stage-1 selection of one half: top-k of s sub-scores, ranked (score desc,
+// id asc) into out[0 .. k).
+template <int E>
+__device__ void half_topk(const float* sc_row, int s, int k, Entry* scratch, uint64_t* kbuf, Entry* out) {
+    const int lane = lane_id();
+    if (k <= 32) {
+        uint64_t key[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int g = e * SDM_WAVE + lane;
+            key[e] = g < s ? ckey(sc_row[g], (uint32_t)g) : 0ull;
+        }
+        uint64_t top;
+        if (topk_sorted<E>(key, E, k, kbuf, top)) {
+            if (lane < k) out[lane] = Entry{ckey_score(top), ckey_id(top)};
+            wait_lds();
+            __builtin_amdgcn_wave_barrier();
+            return;
+        }
+    }
+    half_topk_bisect<E>(sc_row, s, k, scratch, out);
+}
+
 template <typename XT, int MODE, int E>   // MODE 0: direct, 1: codebook FMA, 2: codebook MFMA (bf16)
 __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restrict__ x,
                                                             const XT* __restrict__ cb, int H, int T,
@@ -133,7 +256,8 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
     extern __shared__ __align__(16) unsigned char smem[];
     float* scores = reinterpret_cast<float*>(smem);                          // [ATILE][2*s]
     Entry* scratch = reinterpret_cast<Entry*>(scores + (size_t)ATILE * 2 * s);  // [AWAVES][3][MAXK]
-    uint32_t* pairs = reinterpret_cast<uint32_t*>(scratch + AWAVES * 3 * MAXK);  // [ncand]
+    uint64_t* kbufs = reinterpret_cast<uint64_t*>(scratch + AWAVES * 3 * MAXK);  // [AWAVES][64]
+    uint32_t* pairs = reinterpret_cast<uint32_t*>(kbufs + AWAVES * SDM_WAVE);      // [ncand]
     __shared__ int s_ncand;
 
     const int stream = blockIdx.y;
@@ -212,55 +336,72 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
 
     // ---- B, C: one wave per token --------------------------------------
     const int ncand = s_ncand;
+    const int ne2 = (ncand + SDM_WAVE - 1) / SDM_WAVE;
     Entry* scr = scratch + wave * 3 * MAXK;
     Entry* listA = scr + MAXK;
     Entry* listB = scr + 2 * MAXK;
+    uint64_t* kbuf = kbufs + wave * SDM_WAVE;
     for (int tt = wave; tt < ATILE; tt += AWAVES) {
         const int t = t0 + tt;
         if (t >= T) break;
         const float* row = scores + (size_t)tt * 2 * s;
-        half_topk<E>(row, s, k, scr, listA);
-        half_topk<E>(row + s, s, k, scr, listB);
+        half_topk<E>(row, s, k, scr, kbuf, listA);
+        half_topk<E>(row + s, s, k, scr, kbuf, listB);
 
-        uint32_t key[MAXCAND_E];
-        float sc[MAXCAND_E];
-        int id[MAXCAND_E];
-        bool sel[MAXCAND_E];
+        // stage 2 over the pruned pairs of the two ranked shortlists
+        uint64_t ck[MAXCAND_E];
 #pragma unroll
         for (int e = 0; e < MAXCAND_E; ++e) {
             const int c = e * SDM_WAVE + lane;
-            if (c < ncand) {
+            ck[e] = 0ull;
+            if (e < ne2 && c < ncand) {
                 const uint32_t pr = pairs[c];
                 const Entry a = listA[pr >> 16], b = listB[pr & 0xffffu];
-                sc[e] = a.score + b.score;
-                key[e] = ord_key(sc[e]);
-                id[e] = a.id * s + b.id;
-            } else {
-                sc[e] = 0.f;
-                key[e] = 0u;
-                id[e] = 0x7fffffff;
+                ck[e] = ckey(a.score + b.score, (uint32_t)(a.id * s + b.id));
             }
         }
-        select_topk<MAXCAND_E>(key, id, k, sel);
-        compact<MAXCAND_E>(sel, sc, id, scr);
-        wait_lds();
         float my_sc = -INFINITY;
-        int my_id = 0, rank = 0;
-        if (lane < k) {
-            my_sc = scr[lane].score;
-            my_id = scr[lane].id;
-            for (int j = 0; j < k; ++j) rank += scr[j].id < my_id;
+        uint32_t my_id = 0xffffffffu;
+        uint64_t top;
+        if (k <= 32 && topk_sorted<MAXCAND_E>(ck, ne2, k, kbuf, top)) {
+            if (lane < k) {
+                my_sc = ckey_score(top);
+                my_id = (uint32_t)ckey_id(top);
+            }
+        } else {
+            uint32_t key[MAXCAND_E];
+            float sc[MAXCAND_E];
+            int id[MAXCAND_E];
+            bool sel[MAXCAND_E];
+#pragma unroll
+            for (int e = 0; e < MAXCAND_E; ++e) {
+                const bool ok = ck[e] != 0ull;
+                sc[e] = ok ? ckey_score(ck[e]) : 0.f;
+                key[e] = ok ? (uint32_t)(ck[e] >> 32) : 0u;
+                id[e] = ok ? ckey_id(ck[e]) : 0x7fffffff;
+            }
+            select_topk<MAXCAND_E>(key, id, k, sel);
+            compact<MAXCAND_E>(sel, sc, id, scr);
+            wait_lds();
+            __builtin_amdgcn_wave_barrier();
+            if (lane < k) {
+                my_sc = scr[lane].score;
+                my_id = (uint32_t)scr[lane].id;
+            }
         }
-        const float mx = wave_max(my_sc);
+        // selected slots in ascending id order (App. A.2), then their softmax (Sec. 4)
+        wave_sort_asc_u32(my_id, my_sc);
+        const float mx = wave_max(lane < k ? my_sc : -INFINITY);
         const float ex = lane < k ? expf(my_sc - mx) : 0.f;
         const float z = wave_sum(ex);
         if (lane < k) {
-            const size_t o = ((size_t)stream * T + t) * k + rank;
-            idx[o] = my_id;
+            const size_t o = ((size_t)stream * T + t) * k + lane;
+            idx[o] = (int32_t)my_id;
             val[o] = ex / z;
             if (score) score[o] = my_sc;
         }
         wait_lds();
+        __builtin_amdgcn_wave_barrier();
     }
 }
 
@@ -317,7 +458,7 @@ hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, 
     const int E = (s + SDM_WAVE - 1) / SDM_WAVE;
     dim3 grid((T + ATILE - 1) / ATILE, B * H);
     const size_t sm = (size_t)ATILE * 2 * s * sizeof(float) + AWAVES * 3 * MAXK * sizeof(Entry) +
-                      320 * sizeof(uint32_t);
+                      AWAVES * SDM_WAVE * sizeof(uint64_t) + 320 * sizeof(uint32_t);
     const XT* xp = static_cast<const XT*>(x);
     const XT* cp = static_cast<const XT*>(cb);
 #define SDM_ADDR_CASE(EE)                                                                       \
