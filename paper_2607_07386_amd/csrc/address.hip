@@ -101,54 +101,54 @@ __device__ __forceinline__ float ckey_score(uint64_t k) { return key_to_float((u
 __device__ __forceinline__ int ckey_id(uint64_t k) { return (int)(~(uint32_t)k); }
 
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
-    const uint32_t lo = __shfl_xor((uint32_t)v, m, SDM_WAVE);
-    const uint32_t hi = __shfl_xor((uint32_t)(v >> 32), m, SDM_WAVE);
+    const uint32_t lo = xor_lane_u32((uint32_t)v, m);
+    const uint32_t hi = xor_lane_u32((uint32_t)(v >> 32), m);
     return ((uint64_t)hi << 32) | lo;
 }
 
-// Bitonic sort of one key per lane across the wave, descending (lane 0 holds
-// the largest).  Equal keys never swap, so padding keys stay padding.
+// Bitonic sorts of one key per lane across the wave.  Stage (KK, J) compares
+// lanes i and i ^ J inside blocks of KK; every distance is a template
+// argument, so each exchange is a DPP or permlane move.  Equal keys never
+// swap, so padding keys stay padding.
+template <int KK, int J>
+__device__ __forceinline__ uint64_t bitonic_desc_u64(uint64_t key, int lane) {
+    const uint64_t o = ((uint64_t)xor_lane<J>((uint32_t)(key >> 32)) << 32) | xor_lane<J>((uint32_t)key);
+    const bool keep_max = ((lane & J) == 0) == ((lane & KK) == 0);
+    key = keep_max ? (o > key ? o : key) : (o < key ? o : key);
+    if constexpr (J > 1) return bitonic_desc_u64<KK, J / 2>(key, lane);
+    else if constexpr (KK < SDM_WAVE) return bitonic_desc_u64<KK * 2, KK>(key, lane);
+    else return key;
+}
+template <int KK, int J>
+__device__ __forceinline__ uint32_t bitonic_desc_u32(uint32_t key, int lane) {
+    const uint32_t o = xor_lane<J>(key);
+    const bool keep_max = ((lane & J) == 0) == ((lane & KK) == 0);
+    key = keep_max ? max(o, key) : min(o, key);
+    if constexpr (J > 1) return bitonic_desc_u32<KK, J / 2>(key, lane);
+    else if constexpr (KK < SDM_WAVE) return bitonic_desc_u32<KK * 2, KK>(key, lane);
+    else return key;
+}
+template <int KK, int J>
+__device__ __forceinline__ void bitonic_asc_u32_pay(uint32_t& key, float& pay, int lane) {
+    const uint32_t o = xor_lane<J>(key);
+    const float op = xor_lane_ff<J>(pay);
+    const bool keep_min = ((lane & J) == 0) == ((lane & KK) == 0);
+    const bool take = keep_min ? (o < key) : (o > key);
+    key = take ? o : key;
+    pay = take ? op : pay;
+    if constexpr (J > 1) bitonic_asc_u32_pay<KK, J / 2>(key, pay, lane);
+    else if constexpr (KK < SDM_WAVE) bitonic_asc_u32_pay<KK * 2, KK>(key, pay, lane);
+}
+// Descending: lane 0 holds the largest key.
 __device__ __forceinline__ uint64_t wave_sort_desc_u64(uint64_t key) {
-    const int lane = lane_id();
-#pragma unroll
-    for (int kk = 2; kk <= SDM_WAVE; kk <<= 1) {
-#pragma unroll
-        for (int j = kk >> 1; j > 0; j >>= 1) {
-            const uint64_t o = shfl_xor_u64(key, j);
-            const bool keep_max = ((lane & j) == 0) == ((lane & kk) == 0);
-            key = keep_max ? (o > key ? o : key) : (o < key ? o : key);
-        }
-    }
-    return key;
+    return bitonic_desc_u64<2, 1>(key, lane_id());
 }
 __device__ __forceinline__ uint32_t wave_sort_desc_u32(uint32_t key) {
-    const int lane = lane_id();
-#pragma unroll
-    for (int kk = 2; kk <= SDM_WAVE; kk <<= 1) {
-#pragma unroll
-        for (int j = kk >> 1; j > 0; j >>= 1) {
-            const uint32_t o = __shfl_xor(key, j, SDM_WAVE);
-            const bool keep_max = ((lane & j) == 0) == ((lane & kk) == 0);
-            key = keep_max ? max(o, key) : min(o, key);
-        }
-    }
-    return key;
+    return bitonic_desc_u32<2, 1>(key, lane_id());
 }
-// Ascending sort of keys with a payload riding along.
+// Ascending, with a payload riding along.
 __device__ __forceinline__ void wave_sort_asc_u32(uint32_t& key, float& pay) {
-    const int lane = lane_id();
-#pragma unroll
-    for (int kk = 2; kk <= SDM_WAVE; kk <<= 1) {
-#pragma unroll
-        for (int j = kk >> 1; j > 0; j >>= 1) {
-            const uint32_t o = __shfl_xor(key, j, SDM_WAVE);
-            const float op = __shfl_xor(pay, j, SDM_WAVE);
-            const bool keep_min = ((lane & j) == 0) == ((lane & kk) == 0);
-            const bool take = keep_min ? (o < key) : (o > key);
-            key = take ? o : key;
-            pay = take ? op : pay;
-        }
-    }
+    bitonic_asc_u32_pay<2, 1>(key, pay, lane_id());
 }
 
 // Exact top-k (k <= 32 for the fast path) of E keys per lane, returned sorted

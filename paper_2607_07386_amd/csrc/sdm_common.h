@@ -46,7 +46,44 @@ __device__ __forceinline__ int mbcnt64(unsigned long long m) {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
-__device__ __forceinline__ float shfl_xor_f(float v, int m) { return __shfl_xor(v, m, SDM_WAVE); }
+// Value of lane (this lane ^ M) without going through LDS: DPP row/quad
+// permutes for M <= 8, the gfx950 permlane swaps for 16 and 32.
+template <int M>
+__device__ __forceinline__ uint32_t xor_lane(uint32_t v) {
+    if constexpr (M == 1) {
+        return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+    } else if constexpr (M == 2) {
+        return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+    } else if constexpr (M == 4) {
+        const int h = __builtin_amdgcn_mov_dpp((int)v, 0x141, 0xF, 0xF, false);     // row_half_mirror: i ^ 7
+        return (uint32_t)__builtin_amdgcn_mov_dpp(h, 0x1B, 0xF, 0xF, false);        // quad_perm [3,2,1,0]: ^ 3
+    } else if constexpr (M == 8) {
+        return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xF, 0xF, false);  // row_ror:8
+    } else if constexpr (M == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        return ((lane_id() >> 4) & 1) ? r[0] : r[1];
+    } else {
+        static_assert(M == 32, "xor distance must be a power of two below 64");
+        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        return lane_id() >= 32 ? r[0] : r[1];
+    }
+}
+// Same for a distance known only after unrolling (folds to one case).
+__device__ __forceinline__ uint32_t xor_lane_u32(uint32_t v, int m) {
+    switch (m) {
+        case 1: return xor_lane<1>(v);
+        case 2: return xor_lane<2>(v);
+        case 4: return xor_lane<4>(v);
+        case 8: return xor_lane<8>(v);
+        case 16: return xor_lane<16>(v);
+        case 32: return xor_lane<32>(v);
+        default: return (uint32_t)__shfl_xor((int)v, m, SDM_WAVE);
+    }
+}
+__device__ __forceinline__ float xor_lane_f(float v, int m) {
+    return __uint_as_float(xor_lane_u32(__float_as_uint(v), m));
+}
+__device__ __forceinline__ float shfl_xor_f(float v, int m) { return xor_lane_f(v, m); }
 
 __device__ __forceinline__ float4 shfl_xor_f4(float4 v, int m) {
     return make_float4(__shfl_xor(v.x, m, SDM_WAVE), __shfl_xor(v.y, m, SDM_WAVE),
@@ -71,20 +108,28 @@ __device__ __forceinline__ float f4dot(float4 a, float4 b) {
 }
 __device__ __forceinline__ float4 f4zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
 
+template <int M>
+__device__ __forceinline__ float xor_lane_ff(float v) {
+    return __uint_as_float(xor_lane<M>(__float_as_uint(v)));
+}
+// Butterfly reductions over the wave (every lane receives the result).
+template <int M = 32>
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, SDM_WAVE);
-    return v;
+    v += xor_lane_ff<M>(v);
+    if constexpr (M > 1) return wave_sum<M / 2>(v);
+    else return v;
 }
+template <int M = 32>
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, SDM_WAVE));
-    return v;
+    v = fmaxf(v, xor_lane_ff<M>(v));
+    if constexpr (M > 1) return wave_max<M / 2>(v);
+    else return v;
 }
+template <int M = 32>
 __device__ __forceinline__ int wave_min_i(int v) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) v = min(v, __shfl_xor(v, m, SDM_WAVE));
-    return v;
+    v = min(v, (int)xor_lane<M>((uint32_t)v));
+    if constexpr (M > 1) return wave_min_i<M / 2>(v);
+    else return v;
 }
 
 // Clang vector of 4 floats: elementwise arithmetic, kept in registers.
