@@ -145,7 +145,7 @@ __device__ __forceinline__ void bwd_token(const BwdCtx& c, const BwdBuf<K>& b, i
         const v4f Mv = v4sel(l1 >= 0, ld4(c.pring + i1 * SW + c.cq * 4), b.Mr[k]);
         float rb = c.colok ? v4dot(yb, Mv) : 0.f;
 #pragma unroll
-        for (int q = 1; q < CQ; q <<= 1) rb += __shfl_xor(rb, q, SDM_WAVE);
+        for (int q = 1; q < CQ; q <<= 1) rb += xor_lane_f(rb, q);
         if (rok && c.cq == 0) prow[m] = rb;
         const int l2 = lgr[mm];
         const int i2 = l2 >= 0 ? (((t + (l2 >> 8)) & (PD - 1)) * RW + min(l2 & 255, RW - 1)) : 0;
@@ -191,7 +191,7 @@ __device__ __forceinline__ void bwd_token(const BwdCtx& c, const BwdBuf<K>& b, i
         if (n < c.W) {
             float kb = c.colok ? (v4dot(gn[k], e) - be * v4dot(ebp, D[k])) : 0.f;
 #pragma unroll
-            for (int q = 1; q < CQ; q <<= 1) kb += __shfl_xor(kb, q, SDM_WAVE);
+            for (int q = 1; q < CQ; q <<= 1) kb += xor_lane_f(kb, q);
             if (c.cq == 0) prow[c.R + n] = kb;
             const v4f Db = v4fma(-be * kap[k], ebp, gn[k]);
             if (c.colok) ab += v4dot(Db, b.Ps[k]);
@@ -206,7 +206,7 @@ __device__ __forceinline__ void bwd_token(const BwdCtx& c, const BwdBuf<K>& b, i
         }
     }
 #pragma unroll
-    for (int q = 1; q < CQ; q <<= 1) bb += __shfl_xor(bb, q, SDM_WAVE);
+    for (int q = 1; q < CQ; q <<= 1) bb += xor_lane_f(bb, q);
     ab = wave_sum(ab);
     if (lane == 0) {
         prow[RW] = bb;

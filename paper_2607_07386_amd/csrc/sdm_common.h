@@ -163,10 +163,10 @@ __device__ __forceinline__ float v4dot(v4f a, v4f b) {
 }
 __device__ __forceinline__ v4f v4shfl_xor(v4f v, int m) {
     v4f r;
-    r.x = __shfl_xor(v.x, m, SDM_WAVE);
-    r.y = __shfl_xor(v.y, m, SDM_WAVE);
-    r.z = __shfl_xor(v.z, m, SDM_WAVE);
-    r.w = __shfl_xor(v.w, m, SDM_WAVE);
+    r.x = xor_lane_f(v.x, m);
+    r.y = xor_lane_f(v.y, m);
+    r.z = xor_lane_f(v.z, m);
+    r.w = xor_lane_f(v.w, m);
     return r;
 }
 __device__ __forceinline__ v4f v4sel(bool c, v4f a, v4f b) {
