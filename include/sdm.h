@@ -171,6 +171,19 @@ size_t sdm_scan_bwd_workspace_bytes(int B, int H, int T, int W, int R, int d_v);
 int sdm_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int d_v, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Scan geometry.  Every column of the state is an independent recurrence
+ * (Eq. 3-5 mix rows only within a column), so the scans give each wave a slice
+ * of columns of one (b, h) stream.  sdm_set_scan_slice_width(sw):
+ *   0   automatic (default): 16 columns per wave when B*H*ceil(d_v/16) waves
+ *       cover every SIMD of the device, else 8 (twice as many waves);
+ *   8, 16  force that width.
+ * Process-wide; applies to launches that start after the call.  Results of
+ * the two widths agree to the rounding of the sums over rows.  Any other
+ * value returns SDM_ERR_INVALID_ARG and keeps the setting.
+ * ---------------------------------------------------------------------- */
+int sdm_set_scan_slice_width(int sw);
+
+/* ------------------------------------------------------------------------
  * Per-kernel timing with HIP events, off by default.  While enabled, every
  * kernel the library launches is bracketed by two HIP events recorded on the
  * stream it is launched on; sdm_profile_read() waits for the recorded events

@@ -6,11 +6,32 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <atomic>
 #include <mutex>
 #include <vector>
 
-#include "../../include/sdm.h"
+#include "sdm.h"
 #include "sdm_internal.h"
+
+namespace {
+std::atomic<int> g_slice_width{0};
+}
+
+int sdm_scan_slice_width() { return g_slice_width.load(std::memory_order_relaxed); }
+
+int sdm_device_simds() {
+    constexpr int MAXDEV = 64;
+    static int cache[MAXDEV] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAXDEV) return 1024;
+    if (cache[dev] == 0) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+            cus = 256;
+        cache[dev] = 4 * cus;
+    }
+    return cache[dev];
+}
 
 namespace {
 
@@ -110,6 +131,14 @@ void sdm_prof_end(int k, hipStream_t st) {
 }
 
 extern "C" {
+
+int sdm_set_scan_slice_width(int sw) {
+    g_err[0] = 0;
+    if (sw != 0 && sw != 8 && sw != 16)
+        return fail(SDM_ERR_INVALID_ARG, "sdm_set_scan_slice_width: width must be 0 (automatic), 8 or 16, got %d", sw);
+    g_slice_width.store(sw, std::memory_order_relaxed);
+    return SDM_OK;
+}
 
 int sdm_profile_enable(int on) {
     ProfState& p = prof();

@@ -18,7 +18,7 @@
 
 #include "sdm_common.h"
 #include "sdm_internal.h"
-#include "../../include/sdm.h"
+#include "sdm.h"
 
 namespace {
 
@@ -324,40 +324,57 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(const float* __restrict
     }
 }
 
-constexpr int BSW = 16, BPD = SDM_BWD_PD;
+constexpr int BPD = SDM_BWD_PD;
+constexpr int BSW_MIN = 8;   // narrowest slice: sizes the per-slice partials
 
-// Staging registers per lane for a block of G backward records (at most
-// 8 (W + R) + 4 R + 2 W + 8 bytes each) of a shape with max(W, R) <= 16 K.
-constexpr int bnr_for_k(int K) { return K == 1 ? 2 : (K == 2 ? 3 : 6); }
+// Staging registers per lane (16 bytes each) for a block of G records: a
+// record of a shape with max(W, R) <= K RG takes at most 22 K RG + 8 bytes
+// rounded up to 16.
+template <int SW>
+constexpr int bnr_for_k(int K) {
+    constexpr int RG = SDM_WAVE / (SW / 4);
+    return (G * ((22 * K * RG + 8 + 15) / 16 * 16) + SDM_WAVE * 16 - 1) / (SDM_WAVE * 16);
+}
 
 struct BwdPlan {
-    int K, NR, lds_per_wave, wpb, n_slices;
+    int SW, K, NR, lds_per_wave, wpb, n_slices;
 };
 
-bool bwd_plan(int W, int R, int dv, int in_dtype, BwdPlan* p) {
-    constexpr int RG = SDM_WAVE / (BSW / 4);
+template <int SW>
+bool bwd_plan_sw(int W, int R, int dv, int in_dtype, BwdPlan* p) {
+    constexpr int RG = SDM_WAVE / (SW / 4);
     const int need = (std::max(W, R) + RG - 1) / RG;
-    if (need > 4) return false;
+    if (need > (SW == 16 ? 4 : 2)) return false;
+    p->SW = SW;
     p->K = need <= 1 ? 1 : (need <= 2 ? 2 : 4);
-    p->NR = bnr_for_k(p->K);
+    p->NR = bnr_for_k<SW>(p->K);
     const BwdRec L = bwd_rec_layout(W, R);
     if (G * L.bytes > p->NR * SDM_WAVE * 16) return false;
     const int vbytes = in_dtype == SDM_DT_BF16 ? 2 : 4;
     constexpr int NS = bstage_slots<BPD>();
-    p->lds_per_wave = NS * L.bytes + NS * BSW * vbytes + BPD * (R + W) * BSW * 4 + BPD * W * BSW * 4;
+    p->lds_per_wave = NS * L.bytes + NS * SW * vbytes + BPD * (R + W) * SW * 4 + BPD * W * SW * 4;
     if (p->lds_per_wave > LDS_LIMIT) return false;
-    p->n_slices = (dv + BSW - 1) / BSW;
+    p->n_slices = (dv + SW - 1) / SW;
     p->wpb = std::min(std::min(MAX_WPB, p->n_slices), LDS_LIMIT / p->lds_per_wave);
     return true;
 }
 
-template <typename VT, int K>
+// 16 columns per wave when that already gives every SIMD a wave, else 8,
+// unless a width is forced.
+bool bwd_plan(int S, int W, int R, int dv, int in_dtype, BwdPlan* p) {
+    const int forced = sdm_scan_slice_width();
+    if (forced == 16 || (forced == 0 && (int64_t)S * ((dv + 15) / 16) >= sdm_device_simds()))
+        return bwd_plan_sw<16>(W, R, dv, in_dtype, p);
+    return bwd_plan_sw<BSW_MIN>(W, R, dv, in_dtype, p);
+}
+
+template <typename VT, int SW, int K>
 hipError_t launch_bwd_k(const ScanBwdArgs& a, const BwdPlan& p, float* part, hipStream_t st) {
-    constexpr int NR = bnr_for_k(K);
+    constexpr int NR = bnr_for_k<SW>(K);
     const int S = a.B * a.H;
     dim3 grid((p.n_slices + p.wpb - 1) / p.wpb, S);
     const size_t sm = (size_t)p.lds_per_wave * p.wpb;
-    auto kfn = scan_bwd_kernel<VT, BSW, BPD, K, NR>;
+    auto kfn = scan_bwd_kernel<VT, SW, BPD, K, NR>;
     hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kfn, grid, dim3(p.wpb * SDM_WAVE), sm, st, a.ws + SDM_WS_HEADER,
@@ -368,9 +385,13 @@ hipError_t launch_bwd_k(const ScanBwdArgs& a, const BwdPlan& p, float* part, hip
 
 template <typename VT>
 hipError_t launch_bwd_kk(const ScanBwdArgs& a, const BwdPlan& p, float* part, hipStream_t st) {
-    if (p.K == 1) return launch_bwd_k<VT, 1>(a, p, part, st);
-    if (p.K == 2) return launch_bwd_k<VT, 2>(a, p, part, st);
-    return launch_bwd_k<VT, 4>(a, p, part, st);
+    if (p.SW == 8) {
+        if (p.K == 1) return launch_bwd_k<VT, 8, 1>(a, p, part, st);
+        return launch_bwd_k<VT, 8, 2>(a, p, part, st);
+    }
+    if (p.K == 1) return launch_bwd_k<VT, 16, 1>(a, p, part, st);
+    if (p.K == 2) return launch_bwd_k<VT, 16, 2>(a, p, part, st);
+    return launch_bwd_k<VT, 16, 4>(a, p, part, st);
 }
 
 size_t bwd_part_offset(int B, int H, int T, int W, int R) {
@@ -381,7 +402,7 @@ size_t bwd_part_offset(int B, int H, int T, int W, int R) {
 }  // namespace
 
 size_t sdm_bwd_ws_bytes(int B, int H, int T, int W, int R, int dv) {
-    const int n_slices = (dv + BSW - 1) / BSW;
+    const int n_slices = (dv + BSW_MIN - 1) / BSW_MIN;   // the most slices any plan uses
     const size_t ST = (size_t)B * H * T;
     size_t bytes = bwd_part_offset(B, H, T, W, R) + (size_t)n_slices * ST * (W + R + 2) * sizeof(float);
     bytes = (bytes + 255) & ~(size_t)255;
@@ -391,13 +412,13 @@ size_t sdm_bwd_ws_bytes(int B, int H, int T, int W, int R, int dv) {
 
 bool sdm_bwd_plan_ok(int W, int R, int dv, int in_dtype) {
     BwdPlan p;
-    return bwd_plan(W, R, dv, in_dtype, &p);
+    return bwd_plan_sw<16>(W, R, dv, in_dtype, &p) && bwd_plan_sw<BSW_MIN>(W, R, dv, in_dtype, &p);
 }
 
 hipError_t sdm_launch_scan_bwd(const ScanBwdArgs& a, hipStream_t st) {
     BwdPlan plan;
-    if (!bwd_plan(a.W, a.R, a.dv, a.in_dtype, &plan)) return hipErrorInvalidConfiguration;
     const int S = a.B * a.H;
+    if (!bwd_plan(S, a.W, a.R, a.dv, a.in_dtype, &plan)) return hipErrorInvalidConfiguration;
     {
         SdmProfScope ps(SDM_K_BWD_PREP, st);
         hipError_t e = sdm_launch_bwd_prep<BPD>(a, st);

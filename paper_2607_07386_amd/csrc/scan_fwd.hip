@@ -21,7 +21,7 @@
 
 #include "sdm_common.h"
 #include "sdm_internal.h"
-#include "../../include/sdm.h"
+#include "sdm.h"
 
 namespace {
 
@@ -248,41 +248,58 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_fwd_kernel(
     }
 }
 
-constexpr int FWD_SW = 16, FWD_PD = SDM_FWD_PD;
+constexpr int FWD_PD = SDM_FWD_PD;
 
-// Staging registers per lane for a block of G records: enough for every
-// record of a shape with max(W, R) <= 16 K (10 (W + R) + 8 bytes, 16-aligned).
-constexpr int nr_for_k(int K) { return K == 1 ? 2 : (K == 2 ? 3 : 6); }
+// Staging registers per lane (16 bytes each) for a block of G records: enough
+// for every record of a shape with max(W, R) <= K RG, whose record takes at
+// most 20 K RG + 8 bytes rounded up to 16.
+template <int SW>
+constexpr int nr_for_k(int K) {
+    constexpr int RG = SDM_WAVE / (SW / 4);
+    return (G * ((20 * K * RG + 8 + 15) / 16 * 16) + SDM_WAVE * 16 - 1) / (SDM_WAVE * 16);
+}
 
 struct FwdPlan {
-    int K, NR, lds_per_wave, wpb, n_slices;
+    int SW, K, NR, lds_per_wave, wpb, n_slices;
 };
 
-// Launch geometry of the forward scan; false if the shape cannot be run.
-bool fwd_plan(int W, int R, int dv, int in_dtype, FwdPlan* p) {
-    constexpr int RG = SDM_WAVE / (FWD_SW / 4);
+// Launch geometry of the forward scan with SW columns per wave; false if the
+// shape cannot be run.
+template <int SW>
+bool fwd_plan_sw(int W, int R, int dv, int in_dtype, FwdPlan* p) {
+    constexpr int RG = SDM_WAVE / (SW / 4);
     const int need = (std::max(W, R) + RG - 1) / RG;
-    if (need > 4) return false;
+    if (need > (SW == 16 ? 4 : 2)) return false;
+    p->SW = SW;
     p->K = need <= 1 ? 1 : (need <= 2 ? 2 : 4);
-    p->NR = nr_for_k(p->K);
+    p->NR = nr_for_k<SW>(p->K);
     const FwdRec L = fwd_rec_layout(W, R);
     if (G * L.bytes > p->NR * SDM_WAVE * 16) return false;
     const int vbytes = in_dtype == SDM_DT_BF16 ? 2 : 4;
     constexpr int NS = stage_slots<FWD_PD>();
-    p->lds_per_wave = NS * L.bytes + NS * FWD_SW * vbytes + FWD_PD * W * FWD_SW * 4;
+    p->lds_per_wave = NS * L.bytes + NS * SW * vbytes + FWD_PD * W * SW * 4;
     if (p->lds_per_wave > LDS_LIMIT) return false;
-    p->n_slices = (dv + FWD_SW - 1) / FWD_SW;
+    p->n_slices = (dv + SW - 1) / SW;
     p->wpb = std::min(std::min(MAX_WPB, p->n_slices), LDS_LIMIT / p->lds_per_wave);
     return true;
 }
 
-template <typename VT, int K, bool SAVE>
+// 16 columns per wave when that already gives every SIMD a wave, else 8
+// (twice the waves, half the columns each), unless a width is forced.
+bool fwd_plan(int S, int W, int R, int dv, int in_dtype, FwdPlan* p) {
+    const int forced = sdm_scan_slice_width();
+    if (forced == 16 || (forced == 0 && (int64_t)S * ((dv + 15) / 16) >= sdm_device_simds()))
+        return fwd_plan_sw<16>(W, R, dv, in_dtype, p);
+    return fwd_plan_sw<8>(W, R, dv, in_dtype, p);
+}
+
+template <typename VT, int SW, int K, bool SAVE>
 hipError_t launch_fwd_k(const ScanFwdArgs& a, const FwdPlan& p, hipStream_t st) {
-    constexpr int NR = nr_for_k(K);
+    constexpr int NR = nr_for_k<SW>(K);
     const int S = a.B * a.H;
     dim3 grid((p.n_slices + p.wpb - 1) / p.wpb, S);
     const size_t sm = (size_t)p.lds_per_wave * p.wpb;
-    auto kfn = scan_fwd_kernel<VT, FWD_SW, FWD_PD, K, NR, SAVE>;
+    auto kfn = scan_fwd_kernel<VT, SW, FWD_PD, K, NR, SAVE>;
     hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kfn, grid, dim3(p.wpb * SDM_WAVE), sm, st,
@@ -293,9 +310,13 @@ hipError_t launch_fwd_k(const ScanFwdArgs& a, const FwdPlan& p, hipStream_t st) 
 
 template <typename VT, bool SAVE>
 hipError_t launch_fwd_kk(const ScanFwdArgs& a, const FwdPlan& p, hipStream_t st) {
-    if (p.K == 1) return launch_fwd_k<VT, 1, SAVE>(a, p, st);
-    if (p.K == 2) return launch_fwd_k<VT, 2, SAVE>(a, p, st);
-    return launch_fwd_k<VT, 4, SAVE>(a, p, st);
+    if (p.SW == 8) {
+        if (p.K == 1) return launch_fwd_k<VT, 8, 1, SAVE>(a, p, st);
+        return launch_fwd_k<VT, 8, 2, SAVE>(a, p, st);
+    }
+    if (p.K == 1) return launch_fwd_k<VT, 16, 1, SAVE>(a, p, st);
+    if (p.K == 2) return launch_fwd_k<VT, 16, 2, SAVE>(a, p, st);
+    return launch_fwd_k<VT, 16, 4, SAVE>(a, p, st);
 }
 
 }  // namespace
@@ -305,13 +326,13 @@ size_t sdm_fwd_ws_bytes(int B, int H, int T, int W, int R) {
 }
 
 bool sdm_fwd_plan_ok(int W, int R, int dv, int in_dtype) {
-    FwdPlan p;
-    return fwd_plan(W, R, dv, in_dtype, &p);
+    FwdPlan p;   // the 16-column plan fits whenever the 8-column one does
+    return fwd_plan_sw<16>(W, R, dv, in_dtype, &p) && fwd_plan_sw<8>(W, R, dv, in_dtype, &p);
 }
 
 hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st) {
     FwdPlan p;
-    if (!fwd_plan(a.W, a.R, a.dv, a.in_dtype, &p)) return hipErrorInvalidConfiguration;
+    if (!fwd_plan(a.B * a.H, a.W, a.R, a.dv, a.in_dtype, &p)) return hipErrorInvalidConfiguration;
     hipError_t e;
     {
         SdmProfScope ps(SDM_K_FWD_PREP, st);

@@ -8,12 +8,13 @@
 // prefetch window: the link (d << 8 | entry) names that token (d tokens
 // away) and its ring entry; -1 means the row is read from HBM.
 //
-// One thread per (token, row) walks the candidate tokens nearest first and
-// stops at the first that holds the slot.  Each token's slot list carries a
-// 1024-bit filter in LDS, so a candidate costs one bit test and only a set
-// bit (a hit, or about W/1024 false positives) costs an exact search; slot
-// lists need not be sorted.  Records are then written out word by word,
-// coalesced.
+// One thread per (token, row) searches the slot lists of the candidate tokens
+// in the window.  Addressing returns every list in ascending slot order, so a
+// search is a fixed-length branch-free binary search (ceil(log2 W) LDS reads,
+// the same for every lane); a list that is not strictly increasing is
+// searched linearly instead (first occurrence).  Candidates are visited
+// farthest first and a hit overwrites, so the nearest one wins without a
+// data-dependent exit.  Records are then written out word by word, coalesced.
 #include "sdm_common.h"
 #include "sdm_internal.h"
 
@@ -40,15 +41,28 @@ __device__ __forceinline__ void load_gates(const void* alpha, const void* beta, 
     }
 }
 
-// 1024-bit slot filter per token list: a clear bit proves the slot is absent,
-// a set bit is confirmed by an exact search of the list.
-constexpr int FWORDS = 32;
-__device__ __forceinline__ int fhash(int slot) { return (slot ^ (slot >> 10) ^ (slot >> 20)) & 1023; }
-__device__ __forceinline__ bool ftest(const uint32_t* bm, int h) { return (bm[h >> 5] >> (h & 31)) & 1u; }
-__device__ __forceinline__ int find(const int* lst, int n, int slot) {
+// Position of slot in lst[0, n), or -1.  srt: lst is strictly increasing.
+__device__ __forceinline__ int find_slot(const int* lst, int n, bool srt, int slot) {
+    if (srt) {
+        int lo = 0;
+        for (int len = n; len > 1;) {
+            const int half = len >> 1;
+            lo = lst[lo + half] <= slot ? lo + half : lo;
+            len -= half;
+        }
+        return lst[lo] == slot ? lo : -1;
+    }
     for (int i = 0; i < n; ++i)
         if (lst[i] == slot) return i;
     return -1;
+}
+
+// srt[l] = 1 when list l of the n lists [nl][len] in lst is strictly increasing.
+__device__ __forceinline__ void mark_sorted(const int* lst, int nl, int len, int* srt) {
+    for (int i = threadIdx.x; i < nl; i += blockDim.x) srt[i] = 1;
+    __syncthreads();
+    for (int i = threadIdx.x; i < nl * len; i += blockDim.x)
+        if (i % len != 0 && lst[i] <= lst[i - 1]) srt[i / len] = 0;
 }
 
 // ---------------------------------------------------------------- forward
@@ -75,42 +89,32 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
     const int nrow = W + R;
     int* wl = sm;                                        // [PT+PD-1][W]
     int* rl = wl + (PT + PD - 1) * W;                    // [PT][R]
-    short* lk = reinterpret_cast<short*>(rl + PT * R);   // [PT][W + R] links
-    uint32_t* bm = reinterpret_cast<uint32_t*>(lk + ((PT * nrow + 1) & ~1));  // [PT+PD-1][FWORDS]
+    int* wsrt = rl + PT * R;                             // [PT+PD-1]
+    short* lk = reinterpret_cast<short*>(wsrt + PT + PD - 1);   // [PT][W + R] links
     const size_t sbase = (size_t)stream * T;
     unsigned int bad = 0u;
 
-    for (int i = threadIdx.x; i < (PT + PD - 1) * FWORDS; i += blockDim.x) bm[i] = 0u;
-    __syncthreads();
     for (int i = threadIdx.x; i < nw * W; i += blockDim.x) {
         const int t = tb + i / W;
-        const int slot = t >= 0 ? clamp_slot(w_idx[(sbase + t) * W + i % W], N, bad) : -1;
-        wl[i] = slot;
-        if (slot >= 0) {
-            const int h = fhash(slot);
-            atomicOr(&bm[(i / W) * FWORDS + (h >> 5)], 1u << (h & 31));
-        }
+        wl[i] = t >= 0 ? clamp_slot(w_idx[(sbase + t) * W + i % W], N, bad) : -1;
     }
     for (int i = threadIdx.x; i < ntok * R; i += blockDim.x)
         rl[i] = clamp_slot(r_idx[(sbase + t0) * R + i], N, bad);
+    __syncthreads();
+    mark_sorted(wl, nw, W, wsrt);
     __syncthreads();
 
     for (int i = threadIdx.x; i < ntok * nrow; i += blockDim.x) {
         const int tl = i / nrow, r = i % nrow;
         const bool wrow = r < W;
         const int slot = wrow ? wl[(tl + PD - 1) * W + r] : rl[tl * R + (r - W)];
-        const int h = fhash(slot);
+        const int dlo = wrow ? 1 : 0;           // a read row may hit its own token
+        const int dhi = min(PD - 1, t0 + tl);   // no writer before token 0
         short link = -1;
-        for (int d = wrow ? 1 : 0; d < PD; ++d) {
-            if (t0 + tl - d < 0) break;
-            const int u = tl + PD - 1 - d;   // write list of token t - d
-            if (ftest(bm + u * FWORDS, h)) {
-                const int n = find(wl + u * W, W, slot);
-                if (n >= 0) {
-                    link = (short)((d << 8) | n);
-                    break;
-                }
-            }
+        for (int d = dhi; d >= dlo; --d) {
+            const int u = tl + PD - 1 - d;       // write list of token t - d
+            const int n = find_slot(wl + u * W, W, wsrt[u] != 0, slot);
+            if (n >= 0) link = (short)((d << 8) | n);
         }
         lk[i] = link;
     }
@@ -174,26 +178,19 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const int32_t* __restrict
     const int nlink = 2 * R + W;
     int* wl = sm;                                          // [PT+PD-1][W]
     int* rl = wl + (PT + PD - 1) * W;                      // [PT+PD-1][R]
-    short* lk = reinterpret_cast<short*>(rl + (PT + PD - 1) * R);   // [PT][2R + W]: lm, lgr, lgw
-    uint32_t* wbm = reinterpret_cast<uint32_t*>(lk + ((PT * nlink + 1) & ~1));  // [PT+PD-1][FWORDS]
-    uint32_t* rbm = wbm + (PT + PD - 1) * FWORDS;
+    int* wsrt = rl + (PT + PD - 1) * R;                    // [PT+PD-1]
+    int* rsrt = wsrt + PT + PD - 1;                        // [PT+PD-1]
+    short* lk = reinterpret_cast<short*>(rsrt + PT + PD - 1);   // [PT][2R + W]: lm, lgr, lgw
     const size_t sbase = (size_t)stream * T;
     unsigned int bad = 0u;
 
-    for (int i = threadIdx.x; i < 2 * (PT + PD - 1) * FWORDS; i += blockDim.x) wbm[i] = 0u;
+    for (int i = threadIdx.x; i < span * W; i += blockDim.x)
+        wl[i] = clamp_slot(w_idx[(sbase + t0) * W + i], N, bad);
+    for (int i = threadIdx.x; i < span * R; i += blockDim.x)
+        rl[i] = clamp_slot(r_idx[(sbase + t0) * R + i], N, bad);
     __syncthreads();
-    for (int i = threadIdx.x; i < span * W; i += blockDim.x) {
-        const int slot = clamp_slot(w_idx[(sbase + t0) * W + i], N, bad);
-        wl[i] = slot;
-        const int h = fhash(slot);
-        atomicOr(&wbm[(i / W) * FWORDS + (h >> 5)], 1u << (h & 31));
-    }
-    for (int i = threadIdx.x; i < span * R; i += blockDim.x) {
-        const int slot = clamp_slot(r_idx[(sbase + t0) * R + i], N, bad);
-        rl[i] = slot;
-        const int h = fhash(slot);
-        atomicOr(&rbm[(i / R) * FWORDS + (h >> 5)], 1u << (h & 31));
-    }
+    mark_sorted(wl, span, W, wsrt);
+    mark_sorted(rl, span, R, rsrt);
     __syncthreads();
 
     const int nrow = W + R;
@@ -201,26 +198,21 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const int32_t* __restrict
         const int tl = i / nrow, r = i % nrow;
         const bool wrow = r < W;
         const int slot = wrow ? wl[tl * W + r] : rl[tl * R + (r - W)];
-        const int h = fhash(slot);
         short lg = -1, lm = -1;
-        if (wrow && ftest(rbm + tl * FWORDS, h)) {   // this token's read adjoint
-            const int m = find(rl + tl * R, R, slot);
-            if (m >= 0) lg = (short)m;
-        }
-        for (int d = 1; d < PD && (lg < 0 || (!wrow && lm < 0)); ++d) {
+        for (int d = min(PD - 1, span - 1 - tl); d >= 1; --d) {   // farthest first, nearest wins
             const int u = tl + d;
-            if (u >= span) break;
-            int n = -1;
-            if (ftest(wbm + u * FWORDS, h)) n = find(wl + u * W, W, slot);
+            const int n = find_slot(wl + u * W, W, wsrt[u] != 0, slot);
+            const int m = find_slot(rl + u * R, R, rsrt[u] != 0, slot);
             if (n >= 0) {
-                if (lg < 0) lg = (short)((d << 8) | (R + n));
-                if (!wrow && lm < 0) lm = (short)((d << 8) | n);
-            } else if (lg < 0 && ftest(rbm + u * FWORDS, h)) {
-                const int m = find(rl + u * R, R, slot);
-                if (m >= 0) lg = (short)((d << 8) | m);
+                lg = (short)((d << 8) | (R + n));
+                lm = (short)((d << 8) | n);
+            } else if (m >= 0) {
+                lg = (short)((d << 8) | m);
             }
         }
         if (wrow) {
+            const int m = find_slot(rl + tl * R, R, rsrt[tl] != 0, slot);   // this token's read adjoint
+            if (m >= 0) lg = (short)m;
             lk[tl * nlink + 2 * R + r] = lg;
         } else {
             lk[tl * nlink + (r - W)] = lm;
@@ -260,15 +252,13 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const int32_t* __restrict
 
 template <int PD>
 size_t fwd_prep_lds(int W, int R) {
-    return sizeof(int) * ((size_t)(PT + PD - 1) * W + (size_t)PT * R) +
-           sizeof(short) * (((size_t)PT * (W + R) + 1) & ~(size_t)1) +
-           sizeof(uint32_t) * (size_t)(PT + PD - 1) * FWORDS;
+    return sizeof(int) * ((size_t)(PT + PD - 1) * (W + 1) + (size_t)PT * R) +
+           sizeof(short) * (size_t)PT * (W + R);
 }
 template <int PD>
 size_t bwd_prep_lds(int W, int R) {
-    return sizeof(int) * (size_t)(PT + PD - 1) * (W + R) +
-           sizeof(short) * (((size_t)PT * (2 * R + W) + 1) & ~(size_t)1) +
-           sizeof(uint32_t) * 2 * (size_t)(PT + PD - 1) * FWORDS;
+    return sizeof(int) * (size_t)(PT + PD - 1) * (W + R + 2) +
+           sizeof(short) * (size_t)PT * (2 * R + W);
 }
 
 }  // namespace

@@ -81,6 +81,10 @@ struct ScanFwdArgs {
     unsigned char* ws;   // workspace base (header + records)
 };
 hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st);
+// SIMDs (4 per compute unit) of the current device; 1024 if it cannot be queried.
+int sdm_device_simds();
+// Forced scan slice width (8 or 16), or 0 for the automatic choice.
+int sdm_scan_slice_width();
 // true if the forward scan has a launch plan for this shape (registers, LDS)
 bool sdm_fwd_plan_ok(int W, int R, int dv, int in_dtype);
 size_t sdm_fwd_ws_bytes(int B, int H, int T, int W, int R);

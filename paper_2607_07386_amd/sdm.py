@@ -53,6 +53,7 @@ def lib() -> ctypes.CDLL:
             getattr(L, f).restype = SZ
         L.sdm_check_device_errors.argtypes = [P, P]
         L.sdm_profile_enable.argtypes = [I]
+        L.sdm_set_scan_slice_width.argtypes = [I]
         L.sdm_profile_read.argtypes = [I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
         L.sdm_status_string.argtypes = [I]
         L.sdm_status_string.restype = ctypes.c_char_p
@@ -218,6 +219,11 @@ def check_device_errors(workspace: torch.Tensor):
 
 KERNELS = {"address": 0, "fwd_prep": 1, "fwd_scan": 2, "bwd_prep": 3, "bwd_scan": 4, "bwd_reduce": 5,
            "address_bwd": 6, "mem_init": 7}
+
+
+def set_scan_slice_width(sw: int):
+    """Columns per scan wave: 0 automatic, or force 8 / 16 (process-wide)."""
+    _check("sdm_set_scan_slice_width", lib().sdm_set_scan_slice_width(int(sw)))
 
 
 def profile_enable(on: bool = True):

@@ -105,6 +105,14 @@ def test_scan_bwd_validation(kw, code):
     assert L.sdm_last_error()
 
 
+def test_slice_width_setting():
+    for sw in (8, 16, 0):
+        assert L.sdm_set_scan_slice_width(sw) == 0
+    for sw in (-1, 4, 12, 32):
+        assert L.sdm_set_scan_slice_width(sw) == -1
+        assert b"width" in L.sdm_last_error()
+
+
 def test_mem_init_validation():
     assert L.sdm_mem_init(None, None, 1, 1, 16, 4, None) == -1
     assert L.sdm_mem_init(A, None, 1, 1, 16, 6, None) == -1

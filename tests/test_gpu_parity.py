@@ -107,6 +107,14 @@ def m0_fn(w, inp):
     return lambda s: inp.m0_head(inp.heads[s]).astype(np.float64)
 
 
+@pytest.fixture(params=[8, 16], ids=["sw8", "sw16"])
+def slice_width(request):
+    """Runs a test with each scan slice width forced, then restores the automatic choice."""
+    sdm.set_scan_slice_width(request.param)
+    yield request.param
+    sdm.set_scan_slice_width(0)
+
+
 # --------------------------------------------------------------- small cases
 SMALL = {
     "c0-tiny-f32": synth.WORKLOADS[0],
@@ -128,7 +136,7 @@ SMALL = {
 
 
 @pytest.mark.parametrize("name", list(SMALL))
-def test_forward_small(name):
+def test_forward_small(name, slice_width):
     w = SMALL[name]
     inp = synth.Inputs(w)
     g = gpu_forward(w, inp)
@@ -137,7 +145,7 @@ def test_forward_small(name):
     st = check_addressing(w, inp, g, streams)
     report(name + "/address", **{f"{k}_{kk}": vv for k, v in st.items() for kk, vv in v.items()})
     o = oracle_scan_rows(w, inp, g, streams, m0_fn(w, inp))
-    check_scan(w, g, o, streams, name + "/scan")
+    check_scan(w, g, o, streams, f"{name}/sw{slice_width}/scan")
 
 
 def test_empty_sequence_is_noop():
@@ -206,13 +214,13 @@ HAZARDS = {
 
 @pytest.mark.parametrize("name", list(HAZARDS))
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-def test_scan_hazards(name, dtype):
+def test_scan_hazards(name, dtype, slice_width):
     fn = HAZARDS[name]
     W = len(fn(np.random.default_rng(0), 0, 0, np.zeros((1, 8), np.int32))[0])
     R = len(fn(np.random.default_rng(0), 0, 0, np.zeros((1, 8), np.int32))[1])
     y, mem, yo, memo = _scan_case(3, 211, 48, W, R, 20, fn, seed=5, dtype=dtype)
     ey, em = rel_err(y, yo), rel_err(mem, memo)
-    report(f"hazard/{name}/{dtype}", y_rel_err=ey, mem_rel_err=em)
+    report(f"hazard/{name}/{dtype}/sw{slice_width}", y_rel_err=ey, mem_rel_err=em)
     assert ey < 1e-4 and em < 1e-4
 
 
@@ -315,12 +323,12 @@ def run_backward_case(w, inp, streams, chunk=64):
 
 
 @pytest.mark.parametrize("name", list(BWD))
-def test_backward_small(name):
+def test_backward_small(name, slice_width):
     w = BWD[name]
     inp = synth.Inputs(w)
     streams = list(range(w.B * w.H))
     errs, _ = run_backward_case(w, inp, streams)
-    report(name + "/bwd", **errs)
+    report(f"{name}/sw{slice_width}/bwd", **errs)
     tol = tol_for(w)
     for k, e in errs.items():
         if k != "mem_restored_bit_exact":
