@@ -246,6 +246,200 @@ __device__ void half_topk(const float* sc_row, int s, int k, Entry* scratch, uin
     half_topk_bisect<E>(sc_row, s, k, scratch, out);
 }
 
+// ---- fast path (k <= 32, s <= 256) ------------------------------------
+// Descending bitonic sort of one 64-bit key per lane, held as (hi, lo).  One
+// 64-bit compare per stage decides for both partners: the lane keeping the
+// larger key takes the other's when it is larger, the other lane when it is
+// not (keys are distinct except empty ones, which are equal and interchangeable).
+template <int KK, int J, int NMAX>
+__device__ __forceinline__ void bsort_desc64(uint32_t& hi, uint32_t& lo, int lane) {
+    const uint32_t oh = xor_lane<J>(hi), ol = xor_lane<J>(lo);
+    const bool gt = ((uint64_t)oh << 32 | ol) > ((uint64_t)hi << 32 | lo);
+    const bool keep_max = lane_in<~(lanes_with_bit<J>() ^ lanes_with_bit<KK>())>();
+    const bool take = gt == keep_max;
+    hi = take ? oh : hi;
+    lo = take ? ol : lo;
+    if constexpr (J > 1) bsort_desc64<KK, J / 2, NMAX>(hi, lo, lane);
+    else if constexpr (KK < NMAX) bsort_desc64<KK * 2, KK, NMAX>(hi, lo, lane);
+}
+// Ascending bitonic sort of one key per lane with a payload, within blocks of NMAX lanes.
+template <int KK, int J, int NMAX>
+__device__ __forceinline__ void bsort_asc_pay(uint32_t& key, float& pay, int lane) {
+    const uint32_t o = xor_lane<J>(key);
+    const float op = xor_lane_ff<J>(pay);
+    const bool lt = o < key;
+    const bool keep_min = lane_in<~(lanes_with_bit<J>() ^ lanes_with_bit<KK>())>();
+    const bool take = lt == keep_min;
+    key = take ? o : key;
+    pay = take ? op : pay;
+    if constexpr (J > 1) bsort_asc_pay<KK, J / 2, NMAX>(key, pay, lane);
+    else if constexpr (KK < NMAX) bsort_asc_pay<KK * 2, KK, NMAX>(key, pay, lane);
+}
+
+// Top-k (k <= 32) of E scores per lane (ids gid; -inf pads) under the order
+// (score desc, id asc): returned sorted descending as 64-bit keys
+// (order key of the score, inverted id), rank r in lane r.  The k-th largest
+// per-lane maximum, found by bisection on order keys with wave ballots, is
+// reached by at least k scores; only those are sorted.  Returns false
+// (uniformly) when more than 64 reach it.
+template <int E>
+__device__ __forceinline__ bool fast_topk(const float (&sc)[E], const uint32_t (&gid)[E], int k,
+                                          uint2* kbuf, uint32_t& th, uint32_t& tl) {
+    const int lane = lane_id();
+    float mf = sc[0];
+#pragma unroll
+    for (int e = 1; e < E; ++e) mf = fmaxf(mf, sc[e]);
+    const uint32_t m = ord_key(mf);
+    // The bound only has to be at or below the k-th largest lane maximum, so
+    // the bisection stops after the sign, the exponent and 11 mantissa bits:
+    // it may admit the few extra scores within 2^-11 (relative) below it.
+    uint32_t tau = 0u;
+#pragma unroll
+    for (int bit = 31; bit >= 12; --bit) {
+        const uint32_t c = tau | (1u << bit);
+        if (popc64(__ballot(m >= c)) >= k) tau = c;
+    }
+    const float tf = key_to_float(tau);   // scores >= tf are exactly the keys >= tau
+    int base = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const bool c = sc[e] >= tf;
+        const unsigned long long msk = __ballot(c);
+        const int p = base + mbcnt64(msk);
+        if (c && p < SDM_WAVE) kbuf[p] = make_uint2(__float_as_uint(sc[e]), gid[e]);
+        base += popc64(msk);
+    }
+    if (base > SDM_WAVE || base < k) return false;   // (< k only for non-finite scores)
+    __builtin_amdgcn_wave_barrier();
+    const uint2 v = kbuf[min(lane, SDM_WAVE - 1)];
+    const bool ok = lane < base;
+    th = ok ? ord_key(__uint_as_float(v.x)) : 0u;
+    tl = ~v.y;
+    bsort_desc64<2, 1, SDM_WAVE>(th, tl, lane);
+    return true;
+}
+
+// One token, k <= 32 and s <= SP = 64 E: stage 1 on both halves (rows padded
+// to SP with -inf), stage 2 over the pruned pairs (pi, pj: this lane's pair
+// ranks; pairs past the count point at a -inf list entry), id sort and
+// softmax, outputs written.  Returns false when a selection overflowed (the
+// caller then runs the general path for this token).
+template <int E>
+__device__ __forceinline__ bool token_fast(const float* row, int s, int k, const uint32_t (&pi)[3],
+                                           const uint32_t (&pj)[3], Entry* listA, Entry* listB,
+                                           uint2* kbuf, int32_t* idx_out, float* val_out,
+                                           float* score_out) {
+    constexpr int SP = E * SDM_WAVE;
+    const int lane = lane_id();
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+        float sc[E];
+        uint32_t gid[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            sc[e] = row[half * SP + e * SDM_WAVE + lane];
+            gid[e] = e * SDM_WAVE + lane;
+        }
+        uint32_t th, tl;
+        if (!fast_topk<E>(sc, gid, k, kbuf, th, tl)) return false;
+        Entry* out = half ? listB : listA;
+        if (lane < k) out[lane] = Entry{key_to_float(th), (int)~tl};
+    }
+    __builtin_amdgcn_wave_barrier();
+    float sc[3];
+    uint32_t gid[3];
+#pragma unroll
+    for (int e = 0; e < 3; ++e) {
+        const Entry a = listA[pi[e]], b = listB[pj[e]];
+        sc[e] = a.score + b.score;
+        gid[e] = (uint32_t)(a.id * s + b.id);
+    }
+    uint32_t th, tl;
+    if (!fast_topk<3>(sc, gid, k, kbuf, th, tl)) return false;
+    // lanes < k hold the selection, best first: lane 0 has the maximum score
+    const bool mine = lane < k;
+    uint32_t my_id = mine ? ~tl : 0xffffffffu;
+    float my_sc = mine ? key_to_float(th) : -INFINITY;
+    const float mx = __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(my_sc)));
+    // slots in ascending id order (App. A.2), then softmax (Sec. 4)
+    bsort_asc_pay<2, 1, 32>(my_id, my_sc, lane);
+    const float ex = expf(my_sc - mx);
+    const float z = wave_sum<16>(ex);
+    if (lane < k) {
+        idx_out[lane] = (int32_t)my_id;
+        val_out[lane] = ex / z;
+        if (score_out) score_out[lane] = my_sc;
+    }
+    return true;
+}
+
+// One token on the general path (any k, overflowing selections): stage 1 on
+// both halves, stage 2 over the pruned pairs, id sort and softmax.  Kept out
+// of line: it is the cold path of the common shapes.
+template <int E>
+__device__ __noinline__ void token_general(const float* row, int s, int sp, int k, int ncand, const uint32_t* pairs,
+                                           Entry* scr, Entry* listA, Entry* listB, uint64_t* kbuf,
+                                           int32_t* idx_out, float* val_out, float* score_out) {
+    const int lane = lane_id();
+    const int ne2 = (ncand + SDM_WAVE - 1) / SDM_WAVE;
+    half_topk<E>(row, s, k, scr, kbuf, listA);
+    half_topk<E>(row + sp, s, k, scr, kbuf, listB);
+
+    // stage 2 over the pruned pairs of the two ranked shortlists
+    uint64_t ck[MAXCAND_E];
+#pragma unroll
+    for (int e = 0; e < MAXCAND_E; ++e) {
+        const int c = e * SDM_WAVE + lane;
+        ck[e] = 0ull;
+        if (e < ne2 && c < ncand) {
+            const uint32_t pr = pairs[c];
+            const Entry a = listA[pr >> 16], b = listB[pr & 0xffffu];
+            ck[e] = ckey(a.score + b.score, (uint32_t)(a.id * s + b.id));
+        }
+    }
+    float my_sc = -INFINITY;
+    uint32_t my_id = 0xffffffffu;
+    uint64_t top;
+    if (k <= 32 && topk_sorted<MAXCAND_E>(ck, ne2, k, kbuf, top)) {
+        if (lane < k) {
+            my_sc = ckey_score(top);
+            my_id = (uint32_t)ckey_id(top);
+        }
+    } else {
+        uint32_t key[MAXCAND_E];
+        float sc[MAXCAND_E];
+        int id[MAXCAND_E];
+        bool sel[MAXCAND_E];
+#pragma unroll
+        for (int e = 0; e < MAXCAND_E; ++e) {
+            const bool ok = ck[e] != 0ull;
+            sc[e] = ok ? ckey_score(ck[e]) : 0.f;
+            key[e] = ok ? (uint32_t)(ck[e] >> 32) : 0u;
+            id[e] = ok ? ckey_id(ck[e]) : 0x7fffffff;
+        }
+        select_topk<MAXCAND_E>(key, id, k, sel);
+        compact<MAXCAND_E>(sel, sc, id, scr);
+        wait_lds();
+        __builtin_amdgcn_wave_barrier();
+        if (lane < k) {
+            my_sc = scr[lane].score;
+            my_id = (uint32_t)scr[lane].id;
+        }
+    }
+    // selected slots in ascending id order (App. A.2), then their softmax (Sec. 4)
+    wave_sort_asc_u32(my_id, my_sc);
+    const float mx = wave_max(lane < k ? my_sc : -INFINITY);
+    const float ex = lane < k ? expf(my_sc - mx) : 0.f;
+    const float z = wave_sum(ex);
+    if (lane < k) {
+        idx_out[lane] = (int32_t)my_id;
+        val_out[lane] = ex / z;
+        if (score_out) score_out[lane] = my_sc;
+    }
+    wait_lds();
+    __builtin_amdgcn_wave_barrier();
+}
+
 template <typename XT, int MODE, int E>   // MODE 0: direct, 1: codebook FMA, 2: codebook MFMA (bf16)
 __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restrict__ x,
                                                             const XT* __restrict__ cb, int H, int T,
@@ -254,8 +448,8 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
                                                             float* __restrict__ val,
                                                             float* __restrict__ score) {
     extern __shared__ __align__(16) unsigned char smem[];
-    float* scores = reinterpret_cast<float*>(smem);                          // [ATILE][2*s]
-    Entry* scratch = reinterpret_cast<Entry*>(scores + (size_t)ATILE * 2 * s);  // [AWAVES][3][MAXK]
+    float* scores = reinterpret_cast<float*>(smem);                          // [ATILE][2][64 E]
+    Entry* scratch = reinterpret_cast<Entry*>(scores + (size_t)ATILE * 2 * E * SDM_WAVE);  // [AWAVES][3][MAXK]
     uint64_t* kbufs = reinterpret_cast<uint64_t*>(scratch + AWAVES * 3 * MAXK);  // [AWAVES][64]
     uint32_t* pairs = reinterpret_cast<uint32_t*>(kbufs + AWAVES * SDM_WAVE);      // [ncand]
     __shared__ int s_ncand;
@@ -278,26 +472,27 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
     }
 
     // ---- A: sub-scores of the 16-token tile -------------------------------
+    // Row of a token: [2][SP], half h's sub-key j at h*SP + j; j in [s, SP) holds -inf.
+    constexpr int SP = E * SDM_WAVE;
     if constexpr (MODE == 0) {
-        for (int i = tid; i < ATILE * 2 * s; i += blockDim.x) {
-            const int tt = i / (2 * s), j = i % (2 * s);
+        for (int i = tid; i < ATILE * 2 * SP; i += blockDim.x) {
+            const int tt = i / (2 * SP), half = (i / SP) & 1, j = i % SP;
             const int t = t0 + tt;
-            scores[i] = t < T ? to_f32(xs[(size_t)t * dk + j]) : 0.f;
+            scores[i] = j >= s ? -INFINITY : (t < T ? to_f32(xs[(size_t)t * dk + half * s + j]) : 0.f);
         }
     } else if constexpr (MODE == 1) {
         const int dh = dk / 2;
         const XT* cbh = cb + (size_t)h * 2 * s * dh;
-        for (int i = tid; i < ATILE * 2 * s; i += blockDim.x) {
-            const int tt = i / (2 * s), hj = i % (2 * s);
-            const int half = hj / s, j = hj % s;
+        for (int i = tid; i < ATILE * 2 * SP; i += blockDim.x) {
+            const int tt = i / (2 * SP), half = (i / SP) & 1, j = i % SP;
             const int t = t0 + tt;
             float acc = 0.f;
-            if (t < T) {
+            if (j < s && t < T) {
                 const XT* xr = xs + (size_t)t * dk + half * dh;
                 const XT* cr = cbh + ((size_t)half * s + j) * dh;
                 for (int c = 0; c < dh; ++c) acc = fmaf(to_f32(xr[c]), to_f32(cr[c]), acc);
             }
-            scores[i] = acc;
+            scores[i] = j < s ? acc : -INFINITY;
         }
     } else {
         // MFMA 16x16x32: A[i][kk] = x[t0+i][half*dh + kk], B[kk][j] = cb[half][j0+j][kk].
@@ -328,78 +523,52 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
             }
             if (j < s) {
 #pragma unroll
-                for (int v = 0; v < 4; ++v) scores[(size_t)(4 * q + v) * 2 * s + half * s + j] = acc[v];
+                for (int v = 0; v < 4; ++v) scores[(size_t)(4 * q + v) * 2 * SP + half * SP + j] = acc[v];
             }
+        }
+        if (s < SP) {
+            const int pad = SP - s;
+            for (int i = tid; i < ATILE * 2 * pad; i += blockDim.x)
+                scores[(i / pad) * SP + s + i % pad] = -INFINITY;
         }
     }
     __syncthreads();
 
     // ---- B, C: one wave per token --------------------------------------
     const int ncand = s_ncand;
-    const int ne2 = (ncand + SDM_WAVE - 1) / SDM_WAVE;
     Entry* scr = scratch + wave * 3 * MAXK;
     Entry* listA = scr + MAXK;
     Entry* listB = scr + 2 * MAXK;
     uint64_t* kbuf = kbufs + wave * SDM_WAVE;
+    // fast path: k <= 32, so at most 130 pruned pairs (3 per lane); list
+    // entries past k hold -inf and pairs past the count point at entry 63
+    const bool fast = E <= 4 && k <= 32 && k <= s;
+    uint32_t pi[3], pj[3];
+#pragma unroll
+    for (int e = 0; e < 3; ++e) {
+        const int c = e * SDM_WAVE + lane;
+        const uint32_t pr = c < ncand ? pairs[min(c, ncand - 1)] : ((MAXK - 1u) << 16 | (MAXK - 1u));
+        pi[e] = pr >> 16;
+        pj[e] = pr & 0xffffu;
+    }
+    if (lane >= k) {
+        listA[lane] = Entry{-INFINITY, 0};
+        listB[lane] = Entry{-INFINITY, 0};
+    }
     for (int tt = wave; tt < ATILE; tt += AWAVES) {
         const int t = t0 + tt;
         if (t >= T) break;
-        const float* row = scores + (size_t)tt * 2 * s;
-        half_topk<E>(row, s, k, scr, kbuf, listA);
-        half_topk<E>(row + s, s, k, scr, kbuf, listB);
-
-        // stage 2 over the pruned pairs of the two ranked shortlists
-        uint64_t ck[MAXCAND_E];
-#pragma unroll
-        for (int e = 0; e < MAXCAND_E; ++e) {
-            const int c = e * SDM_WAVE + lane;
-            ck[e] = 0ull;
-            if (e < ne2 && c < ncand) {
-                const uint32_t pr = pairs[c];
-                const Entry a = listA[pr >> 16], b = listB[pr & 0xffffu];
-                ck[e] = ckey(a.score + b.score, (uint32_t)(a.id * s + b.id));
+        const float* row = scores + (size_t)tt * 2 * SP;
+        if constexpr (E <= 4) {
+            if (fast) {
+                const size_t o = ((size_t)stream * T + t) * k;
+                if (token_fast<E>(row, s, k, pi, pj, listA, listB, reinterpret_cast<uint2*>(kbuf),
+                                  idx + o, val + o, score ? score + o : nullptr))
+                    continue;
             }
         }
-        float my_sc = -INFINITY;
-        uint32_t my_id = 0xffffffffu;
-        uint64_t top;
-        if (k <= 32 && topk_sorted<MAXCAND_E>(ck, ne2, k, kbuf, top)) {
-            if (lane < k) {
-                my_sc = ckey_score(top);
-                my_id = (uint32_t)ckey_id(top);
-            }
-        } else {
-            uint32_t key[MAXCAND_E];
-            float sc[MAXCAND_E];
-            int id[MAXCAND_E];
-            bool sel[MAXCAND_E];
-#pragma unroll
-            for (int e = 0; e < MAXCAND_E; ++e) {
-                const bool ok = ck[e] != 0ull;
-                sc[e] = ok ? ckey_score(ck[e]) : 0.f;
-                key[e] = ok ? (uint32_t)(ck[e] >> 32) : 0u;
-                id[e] = ok ? ckey_id(ck[e]) : 0x7fffffff;
-            }
-            select_topk<MAXCAND_E>(key, id, k, sel);
-            compact<MAXCAND_E>(sel, sc, id, scr);
-            wait_lds();
-            __builtin_amdgcn_wave_barrier();
-            if (lane < k) {
-                my_sc = scr[lane].score;
-                my_id = (uint32_t)scr[lane].id;
-            }
-        }
-        // selected slots in ascending id order (App. A.2), then their softmax (Sec. 4)
-        wave_sort_asc_u32(my_id, my_sc);
-        const float mx = wave_max(lane < k ? my_sc : -INFINITY);
-        const float ex = lane < k ? expf(my_sc - mx) : 0.f;
-        const float z = wave_sum(ex);
-        if (lane < k) {
-            const size_t o = ((size_t)stream * T + t) * k + lane;
-            idx[o] = (int32_t)my_id;
-            val[o] = ex / z;
-            if (score) score[o] = my_sc;
-        }
+        token_general<E>(row, s, SP, k, ncand, pairs, scr, listA, listB, kbuf, idx + ((size_t)stream * T + t) * k,
+                         val + ((size_t)stream * T + t) * k, score ? score + ((size_t)stream * T + t) * k : nullptr);
         wait_lds();
         __builtin_amdgcn_wave_barrier();
     }
@@ -452,17 +621,22 @@ __global__ __launch_bounds__(256) void address_bwd_kernel(const XT* __restrict__
     }
 }
 
+// LDS of a tile: padded score rows, per-wave lists and sort buffer, pair table.
+constexpr size_t address_lds_bytes(int E) {
+    return (size_t)ATILE * 2 * E * SDM_WAVE * sizeof(float) + AWAVES * 3 * MAXK * sizeof(Entry) +
+           AWAVES * SDM_WAVE * sizeof(uint64_t) + 320 * sizeof(uint32_t);
+}
+
 template <typename XT, int MODE>
 hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, int dk, int s,
                             int k, int32_t* idx, float* val, float* score, hipStream_t st) {
     const int E = (s + SDM_WAVE - 1) / SDM_WAVE;
     dim3 grid((T + ATILE - 1) / ATILE, B * H);
-    const size_t sm = (size_t)ATILE * 2 * s * sizeof(float) + AWAVES * 3 * MAXK * sizeof(Entry) +
-                      AWAVES * SDM_WAVE * sizeof(uint64_t) + 320 * sizeof(uint32_t);
     const XT* xp = static_cast<const XT*>(x);
     const XT* cp = static_cast<const XT*>(cb);
 #define SDM_ADDR_CASE(EE)                                                                       \
     {                                                                                           \
+        const size_t sm = address_lds_bytes(EE);                                                \
         auto kfn = address_kernel<XT, MODE, EE>;                                                \
         hipError_t e = hipFuncSetAttribute((const void*)kfn,                                    \
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm); \

@@ -46,6 +46,21 @@ __device__ __forceinline__ int mbcnt64(unsigned long long m) {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
+// Wave mask of the lanes whose index has bit M set (M a power of two; 0 for
+// M >= 64), and the same as a per-lane condition: the mask is a constant, so
+// the condition costs no vector instruction.
+template <int M>
+__host__ __device__ constexpr unsigned long long lanes_with_bit() {
+    unsigned long long m = 0ull;
+    for (int l = 0; l < 64; ++l)
+        if (l & M) m |= 1ull << l;
+    return m;
+}
+template <unsigned long long MASK>
+__device__ __forceinline__ bool lane_in() {
+    return __builtin_amdgcn_inverse_ballot_w64(MASK);
+}
+
 // Value of lane (this lane ^ M) without going through LDS: DPP row/quad
 // permutes for M <= 8, the gfx950 permlane swaps for 16 and 32.
 template <int M>
@@ -61,11 +76,11 @@ __device__ __forceinline__ uint32_t xor_lane(uint32_t v) {
         return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xF, 0xF, false);  // row_ror:8
     } else if constexpr (M == 16) {
         const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
-        return ((lane_id() >> 4) & 1) ? r[0] : r[1];
+        return lane_in<lanes_with_bit<16>()>() ? r[0] : r[1];
     } else {
         static_assert(M == 32, "xor distance must be a power of two below 64");
         const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-        return lane_id() >= 32 ? r[0] : r[1];
+        return lane_in<lanes_with_bit<32>()>() ? r[0] : r[1];
     }
 }
 // Same for a distance known only after unrolling (folds to one case).
