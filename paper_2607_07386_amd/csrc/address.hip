@@ -24,12 +24,40 @@ namespace {
 constexpr int ATILE = 16;     // tokens per workgroup
 constexpr int AWAVES = 4;
 constexpr int MAXK = 64;
-constexpr int MAXCAND_E = 5;  // ceil(303 / 64): pruned candidates for k <= 64
+constexpr int MAXKS = 8;      // 32-deep MFMA steps per half: d_k / 2 <= 256
+constexpr int MAXCAND_E = 5;  // ceil(280 / 64): pruned candidates for k <= 64
 
 struct Entry {
     float score;
     int id;
 };
+
+// Pruned stage-2 pairs for every k <= MAXK: ranks (i, j) with (i+1)(j+1) <= k,
+// i ascending then j ascending, packed as i << 8 | j.
+constexpr int pair_count_total() {
+    int t = 0;
+    for (int k = 1; k <= MAXK; ++k)
+        for (int i = 1; i <= k; ++i) t += k / i;
+    return t;
+}
+struct PairTable {
+    uint16_t off[MAXK + 1];   // first pair of k
+    uint16_t n[MAXK + 1];     // number of pairs of k
+    uint16_t e[pair_count_total()];
+};
+constexpr PairTable make_pair_table() {
+    PairTable p{};
+    int o = 0;
+    for (int k = 1; k <= MAXK; ++k) {
+        p.off[k] = (uint16_t)o;
+        for (int i = 0; i < k; ++i)
+            for (int j = 0; j < k / (i + 1); ++j) p.e[o++] = (uint16_t)(i << 8 | j);
+        p.n[k] = (uint16_t)(o - p.off[k]);
+    }
+    return p;
+}
+__constant__ const PairTable c_pairs = make_pair_table();
+static_assert(make_pair_table().n[32] <= 3 * 64 && make_pair_table().n[MAXK] <= MAXCAND_E * 64, "pair counts");
 
 // k-th largest key: the largest tau with #{key >= tau} >= k.
 template <int E>
@@ -276,23 +304,21 @@ __device__ __forceinline__ void bsort_asc_pay(uint32_t& key, float& pay, int lan
     else if constexpr (KK < NMAX) bsort_asc_pay<KK * 2, KK, NMAX>(key, pay, lane);
 }
 
-// Top-k (k <= 32) of E scores per lane (ids gid; -inf pads) under the order
-// (score desc, id asc): returned sorted descending as 64-bit keys
-// (order key of the score, inverted id), rank r in lane r.  The k-th largest
-// per-lane maximum, found by bisection on order keys with wave ballots, is
-// reached by at least k scores; only those are sorted.  Returns false
-// (uniformly) when more than 64 reach it.
+// Candidates for the top-k (k <= 32) of E scores per lane (ids gid; -inf
+// pads): the k-th largest per-lane maximum, found by bisection on order keys
+// with wave ballots, is reached by at least k scores, and those are gathered
+// into lanes 0 .. n-1 as (score bits, id).  The bound only has to be at or
+// below that maximum, so the bisection stops after the sign, the exponent and
+// 11 mantissa bits (admitting the few scores within 2^-11 relative below it).
+// Returns false (uniformly) unless k <= n <= 64.
 template <int E>
-__device__ __forceinline__ bool fast_topk(const float (&sc)[E], const uint32_t (&gid)[E], int k,
-                                          uint2* kbuf, uint32_t& th, uint32_t& tl) {
+__device__ __forceinline__ bool gather_candidates(const float (&sc)[E], const uint32_t (&gid)[E], int k,
+                                                  uint2* kbuf, uint2& mine, int& n) {
     const int lane = lane_id();
     float mf = sc[0];
 #pragma unroll
     for (int e = 1; e < E; ++e) mf = fmaxf(mf, sc[e]);
     const uint32_t m = ord_key(mf);
-    // The bound only has to be at or below the k-th largest lane maximum, so
-    // the bisection stops after the sign, the exponent and 11 mantissa bits:
-    // it may admit the few extra scores within 2^-11 (relative) below it.
     uint32_t tau = 0u;
 #pragma unroll
     for (int bit = 31; bit >= 12; --bit) {
@@ -309,11 +335,24 @@ __device__ __forceinline__ bool fast_topk(const float (&sc)[E], const uint32_t (
         if (c && p < SDM_WAVE) kbuf[p] = make_uint2(__float_as_uint(sc[e]), gid[e]);
         base += popc64(msk);
     }
+    n = base;
     if (base > SDM_WAVE || base < k) return false;   // (< k only for non-finite scores)
     __builtin_amdgcn_wave_barrier();
-    const uint2 v = kbuf[min(lane, SDM_WAVE - 1)];
-    const bool ok = lane < base;
-    th = ok ? ord_key(__uint_as_float(v.x)) : 0u;
+    mine = kbuf[min(lane, SDM_WAVE - 1)];
+    return true;
+}
+
+// Ranked top-k (k <= 32) of E scores per lane under (score desc, id asc):
+// 64-bit keys (order key of the score, inverted id) sorted descending, rank r
+// in lane r.  False when the candidates overflow.
+template <int E>
+__device__ __forceinline__ bool fast_topk(const float (&sc)[E], const uint32_t (&gid)[E], int k,
+                                          uint2* kbuf, uint32_t& th, uint32_t& tl) {
+    const int lane = lane_id();
+    uint2 v;
+    int n;
+    if (!gather_candidates<E>(sc, gid, k, kbuf, v, n)) return false;
+    th = lane < n ? ord_key(__uint_as_float(v.x)) : 0u;
     tl = ~v.y;
     bsort_desc64<2, 1, SDM_WAVE>(th, tl, lane);
     return true;
@@ -354,13 +393,28 @@ __device__ __forceinline__ bool token_fast(const float* row, int s, int k, const
         sc[e] = a.score + b.score;
         gid[e] = (uint32_t)(a.id * s + b.id);
     }
-    uint32_t th, tl;
-    if (!fast_topk<3>(sc, gid, k, kbuf, th, tl)) return false;
-    // lanes < k hold the selection, best first: lane 0 has the maximum score
+    uint2 v;
+    int n;
+    if (!gather_candidates<3>(sc, gid, k, kbuf, v, n)) return false;
+    // exact k-th largest candidate score by bisection; a tie across the k-th
+    // place (to be broken by id) takes the general path
+    const uint32_t key = lane < n ? ord_key(__uint_as_float(v.x)) : 0u;
+    uint32_t tau = 0u;
+#pragma unroll
+    for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t c = tau | (1u << bit);
+        if (popc64(__ballot(key >= c)) >= k) tau = c;
+    }
+    const bool sel = key >= tau;
+    const unsigned long long selm = __ballot(sel);
+    if (popc64(selm) != k) return false;
+    if (sel) kbuf[mbcnt64(selm)] = v;
+    __builtin_amdgcn_wave_barrier();
+    const uint2 w = kbuf[min(lane, SDM_WAVE - 1)];
     const bool mine = lane < k;
-    uint32_t my_id = mine ? ~tl : 0xffffffffu;
-    float my_sc = mine ? key_to_float(th) : -INFINITY;
-    const float mx = __uint_as_float(__builtin_amdgcn_readfirstlane(__float_as_uint(my_sc)));
+    uint32_t my_id = mine ? w.y : 0xffffffffu;
+    float my_sc = mine ? __uint_as_float(w.x) : -INFINITY;
+    const float mx = wave_max<16>(my_sc);
     // slots in ascending id order (App. A.2), then softmax (Sec. 4)
     bsort_asc_pay<2, 1, 32>(my_id, my_sc, lane);
     const float ex = expf(my_sc - mx);
@@ -377,7 +431,7 @@ __device__ __forceinline__ bool token_fast(const float* row, int s, int k, const
 // both halves, stage 2 over the pruned pairs, id sort and softmax.  Kept out
 // of line: it is the cold path of the common shapes.
 template <int E>
-__device__ __noinline__ void token_general(const float* row, int s, int sp, int k, int ncand, const uint32_t* pairs,
+__device__ __noinline__ void token_general(const float* row, int s, int sp, int k, int ncand, const uint16_t* pairs,
                                            Entry* scr, Entry* listA, Entry* listB, uint64_t* kbuf,
                                            int32_t* idx_out, float* val_out, float* score_out) {
     const int lane = lane_id();
@@ -393,7 +447,7 @@ __device__ __noinline__ void token_general(const float* row, int s, int sp, int 
         ck[e] = 0ull;
         if (e < ne2 && c < ncand) {
             const uint32_t pr = pairs[c];
-            const Entry a = listA[pr >> 16], b = listB[pr & 0xffffu];
+            const Entry a = listA[pr >> 8], b = listB[pr & 0xffu];
             ck[e] = ckey(a.score + b.score, (uint32_t)(a.id * s + b.id));
         }
     }
@@ -451,8 +505,6 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
     float* scores = reinterpret_cast<float*>(smem);                          // [ATILE][2][64 E]
     Entry* scratch = reinterpret_cast<Entry*>(scores + (size_t)ATILE * 2 * E * SDM_WAVE);  // [AWAVES][3][MAXK]
     uint64_t* kbufs = reinterpret_cast<uint64_t*>(scratch + AWAVES * 3 * MAXK);  // [AWAVES][64]
-    uint32_t* pairs = reinterpret_cast<uint32_t*>(kbufs + AWAVES * SDM_WAVE);      // [ncand]
-    __shared__ int s_ncand;
 
     const int stream = blockIdx.y;
     const int h = stream % H;
@@ -462,14 +514,8 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
     const int lane = lane_id();
     const XT* xs = x + ((size_t)stream * T) * dk;
 
-    // pair table of the pruned stage-2 candidates
-    if (tid < k) {
-        int off = 0;
-        for (int i = 0; i < tid; ++i) off += k / (i + 1);
-        const int cnt = k / (tid + 1);
-        for (int j = 0; j < cnt; ++j) pairs[off + j] = ((uint32_t)tid << 16) | (uint32_t)j;
-        if (tid == k - 1) s_ncand = off + cnt;
-    }
+    const uint16_t* pairs = c_pairs.e + c_pairs.off[k];
+    const int ncand = c_pairs.n[k];
 
     // ---- A: sub-scores of the 16-token tile -------------------------------
     // Row of a token: [2][SP], half h's sub-key j at h*SP + j; j in [s, SP) holds -inf.
@@ -501,29 +547,37 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
         const int dh = dk / 2;
         const XT* cbh = cb + (size_t)h * 2 * s * dh;
         const int ntile = (s + 15) / 16;
+        const int nks = (dh + 31) / 32;   // 32-deep steps (at most MAXKS)
         const int r16 = lane % 16, q = lane / 16;
         const int t = t0 + r16;
-        for (int job = wave; job < 2 * ntile; job += AWAVES) {
-            const int half = job / ntile;
-            const int j0 = (job % ntile) * 16;
-            const int j = j0 + r16;
-            sdm_f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-            for (int kk = 0; kk < dh; kk += 32) {
-                const int kc = kk + 8 * q;
-                sdm_bf16x8 a, b;
-                if (t < T && kc < dh)
-                    a = *reinterpret_cast<const sdm_bf16x8*>(xs + (size_t)t * dk + half * dh + kc);
-                else
-                    a = sdm_bf16x8{};
-                if (j < s && kc < dh)
-                    b = *reinterpret_cast<const sdm_bf16x8*>(cbh + ((size_t)half * s + j) * dh + kc);
-                else
-                    b = sdm_bf16x8{};
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
-            }
-            if (j < s) {
+        for (int half = 0; half < 2; ++half) {
+            // operand A (this lane's token row, k-slices 8q .. 8q+7 of each step) serves
+            // every sub-key tile of the half
+            sdm_bf16x8 a[MAXKS];
 #pragma unroll
-                for (int v = 0; v < 4; ++v) scores[(size_t)(4 * q + v) * 2 * SP + half * SP + j] = acc[v];
+            for (int ks = 0; ks < MAXKS; ++ks) {
+                const int kc = ks * 32 + 8 * q;
+                a[ks] = sdm_bf16x8{};
+                if (ks < nks && t < T && kc < dh)
+                    a[ks] = *reinterpret_cast<const sdm_bf16x8*>(xs + (size_t)t * dk + half * dh + kc);
+            }
+            for (int jt = wave; jt < ntile; jt += AWAVES) {
+                const int j = jt * 16 + r16;
+                const XT* crow = cbh + ((size_t)half * s + min(j, s - 1)) * dh;
+                sdm_f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < MAXKS; ++ks) {
+                    if (ks < nks) {
+                        const int kc = ks * 32 + 8 * q;
+                        sdm_bf16x8 b = sdm_bf16x8{};
+                        if (j < s && kc < dh) b = *reinterpret_cast<const sdm_bf16x8*>(crow + kc);
+                        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks], b, acc, 0, 0, 0);
+                    }
+                }
+                if (j < s) {
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) scores[(size_t)(4 * q + v) * 2 * SP + half * SP + j] = acc[v];
+                }
             }
         }
         if (s < SP) {
@@ -535,7 +589,6 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
     __syncthreads();
 
     // ---- B, C: one wave per token --------------------------------------
-    const int ncand = s_ncand;
     Entry* scr = scratch + wave * 3 * MAXK;
     Entry* listA = scr + MAXK;
     Entry* listB = scr + 2 * MAXK;
@@ -547,9 +600,9 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
 #pragma unroll
     for (int e = 0; e < 3; ++e) {
         const int c = e * SDM_WAVE + lane;
-        const uint32_t pr = c < ncand ? pairs[min(c, ncand - 1)] : ((MAXK - 1u) << 16 | (MAXK - 1u));
-        pi[e] = pr >> 16;
-        pj[e] = pr & 0xffffu;
+        const uint32_t pr = c < ncand ? pairs[min(c, ncand - 1)] : ((MAXK - 1u) << 8 | (MAXK - 1u));
+        pi[e] = pr >> 8;
+        pj[e] = pr & 0xffu;
     }
     if (lane >= k) {
         listA[lane] = Entry{-INFINITY, 0};
@@ -621,10 +674,10 @@ __global__ __launch_bounds__(256) void address_bwd_kernel(const XT* __restrict__
     }
 }
 
-// LDS of a tile: padded score rows, per-wave lists and sort buffer, pair table.
+// LDS of a tile: padded score rows, per-wave lists and sort buffer.
 constexpr size_t address_lds_bytes(int E) {
     return (size_t)ATILE * 2 * E * SDM_WAVE * sizeof(float) + AWAVES * 3 * MAXK * sizeof(Entry) +
-           AWAVES * SDM_WAVE * sizeof(uint64_t) + 320 * sizeof(uint32_t);
+           AWAVES * SDM_WAVE * sizeof(uint64_t);
 }
 
 template <typename XT, int MODE>
