@@ -34,14 +34,43 @@ sys.path.insert(0, ROOT)
 METRIC = "SDM layer tokens/sec (fwd, fwd+bwd) at 1 GPU; achieved HBM GB/s vs peak"
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fwd_scan_c1.json")
-SCAN_SRC = os.path.join(ROOT, "paper_2607_07386_amd", "csrc", "scan_fwd.hip")
+# sources of the forward scan kernel: the traffic file holds their hash
+SCAN_SRCS = [os.path.join(ROOT, "paper_2607_07386_amd", "csrc", f)
+             for f in ("scan_fwd.hip", "sdm_common.h", "sdm_internal.h")]
+
+
+def scan_src_hash():
+    h = hashlib.sha256()
+    for f in SCAN_SRCS:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
 
 
 def fwd_scan_bytes_per_token_head(W, R, d_v, in_bytes):
-    """Bytes the forward scan must move per (token, head): W rows gathered and
-    W scattered, R rows gathered (fp32 rows of d_v), the value vector in, the
-    output vector out."""
-    return (2 * W + R) * d_v * 4 + d_v * in_bytes + d_v * 4
+    """Bytes the forward scan must move per (token, head), every row counted as
+    the eager recurrence touches it: W rows gathered and W scattered, R rows
+    gathered (fp32 rows of d_v), v, alpha and beta in, the slot ids and weights
+    of both sides in, y out."""
+    return (2 * W + R) * d_v * 4 + d_v * in_bytes + 2 * in_bytes + (W + R) * 8 + d_v * 4
+
+
+def unique_row_bytes(w_idx, r_idx, d_v, in_bytes, window=64):
+    """Stricter count: within each window of 64 tokens of a stream, every
+    distinct slot is loaded once (read or written) and every distinct written
+    slot stored once; the per-token vectors as above."""
+    import numpy as np
+    S, T, W = w_idx.shape
+    R = r_idx.shape[2]
+    nw = T // window
+    wi = w_idx[:, :nw * window].reshape(S, nw, window * W)
+    both = np.concatenate([wi, r_idx[:, :nw * window].reshape(S, nw, window * R)], axis=2)
+
+    def distinct(a):
+        a = np.sort(a, axis=2)
+        return int((a[:, :, 1:] != a[:, :, :-1]).sum() + a.shape[0] * a.shape[1])
+    rows = distinct(both) + distinct(wi)
+    tokens = S * nw * window
+    return rows * d_v * 4 + tokens * (d_v * in_bytes + 2 * in_bytes + (W + R) * 8 + d_v * 4), tokens
 
 
 def log(msg):
@@ -167,11 +196,15 @@ def main():
         unit_bytes = fwd_scan_bytes_per_token_head(w.topk, w.topk, w.d_v, 2)
         launch_bytes = unit_bytes * B * H * T
         achieved = launch_bytes / (scan_ms * 1e-3) / 1e9
+        # stricter count from the ids of the last step (host copy, outside the timed region)
+        r_last, w_last = bufs["last"]
+        uniq_bytes, uniq_tokens = unique_row_bytes(
+            w_last.reshape(B * H, T, -1).cpu().numpy(), r_last.reshape(B * H, T, -1).cpu().numpy(), w.d_v, 2)
+        uniq_launch = uniq_bytes * (B * H * T) / uniq_tokens
         traffic = None
         if os.path.exists(TRAFFIC_FILE):
             tr = json.load(open(TRAFFIC_FILE))
-            src_hash = hashlib.sha256(open(SCAN_SRC, "rb").read()).hexdigest()
-            if tr.get("scan_fwd_sha256") == src_hash:
+            if tr.get("scan_sources_sha256") == scan_src_hash():
                 traffic = tr.get("hbm_bytes_per_launch")
         out.update({
             "value": round(tokens / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
@@ -186,7 +219,9 @@ def main():
             "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                          "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                          "kernel": "scan_fwd_kernel", "algorithmic_bytes_per_token_head": unit_bytes,
-                         "algorithmic_bytes_per_launch": launch_bytes, "kernel_ms": round(scan_ms, 4)},
+                         "algorithmic_bytes_per_launch": launch_bytes, "kernel_ms": round(scan_ms, 4),
+                         "unique_row_bytes_per_launch": round(uniq_launch),
+                         "frac_unique_rows": round(uniq_launch / (scan_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
         })
         if not args.no_cpu_baseline:
             log("cpu baseline (oracle)")
