@@ -121,6 +121,8 @@ def main():
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     ap.add_argument("--only", choices=["fwd", "train"], default=None,
                     help="run one leg only (profiling runs)")
+    ap.add_argument("--chunk", type=int, default=0,
+                    help="tokens per pipeline stage of the forward step (0: the library's choice)")
     ap.add_argument("--calib", action="store_true",
                     help="first run one plain 512 MiB copy (sdm_mem_init from a [16, 65536, 128] fp32 "
                          "source): the reference dispatch for scaling HBM counters")
@@ -167,13 +169,19 @@ def main():
         sdm.mem_init(mem, None)
         ws = sdm.fwd_workspace(B, H, T, w.topk, w.topk, dev)
         y = torch.empty((B, H, T, w.d_v), dtype=torch.float32, device=dev)
-        bufs = {}
+        outs = {n: torch.empty((B, H, T, w.topk), dtype=dt, device=dev)
+                for n, dt in (("r_idx", torch.int32), ("r_val", torch.float32),
+                              ("w_idx", torch.int32), ("w_val", torch.float32))}
 
         def step():
+            # addressing of both sides and the scan in one call, pipelined over chunks of tokens
+            sdm.forward(q, k, cb, cb, v, al, be, mem, w.N, w.topk, workspace=ws, y=y, out=outs,
+                        chunk=args.chunk)
+
+        def step_sequential():
             r_idx, r_val = sdm.address(q, cb, w.N, w.topk)
             w_idx, w_val = sdm.address(k, cb, w.N, w.topk)
             sdm.scan_fwd(w_idx, w_val, r_idx, r_val, v, al, be, mem, workspace=ws, y=y)
-            bufs["last"] = (r_idx, w_idx)
 
         log("warmup")
         for _ in range(args.warmup):
@@ -191,16 +199,25 @@ def main():
         ms = e0.elapsed_time(e1) / args.steps
         kern = {name: sdm.profile_read(name) for name in ("address", "fwd_prep", "fwd_scan")}
         sdm.profile_enable(False)
+        # reference: the same work as three separate calls on one stream (not the reported value)
+        e0.record(stream)
+        for _ in range(3):
+            step_sequential()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms_seq = e0.elapsed_time(e1) / 3
         tokens = B * T
-        scan_ms = kern["fwd_scan"][0] / max(kern["fwd_scan"][1], 1)
+        scan_launches = max(kern["fwd_scan"][1], 1)
+        scan_ms = kern["fwd_scan"][0] / scan_launches
         unit_bytes = fwd_scan_bytes_per_token_head(w.topk, w.topk, w.d_v, 2)
-        launch_bytes = unit_bytes * B * H * T
+        tokens_per_launch = B * H * T * args.steps / scan_launches
+        launch_bytes = round(unit_bytes * tokens_per_launch)
         achieved = launch_bytes / (scan_ms * 1e-3) / 1e9
         # stricter count from the ids of the last step (host copy, outside the timed region)
-        r_last, w_last = bufs["last"]
+        r_last, w_last = outs["r_idx"], outs["w_idx"]
         uniq_bytes, uniq_tokens = unique_row_bytes(
             w_last.reshape(B * H, T, -1).cpu().numpy(), r_last.reshape(B * H, T, -1).cpu().numpy(), w.d_v, 2)
-        uniq_launch = uniq_bytes * (B * H * T) / uniq_tokens
+        uniq_launch = uniq_bytes * tokens_per_launch / uniq_tokens
         traffic = None
         if os.path.exists(TRAFFIC_FILE):
             tr = json.load(open(TRAFFIC_FILE))
@@ -214,7 +231,10 @@ def main():
             "config": {"workload": "1.4B-shaped SDM layer forward: B=8 H=16 T=4096 d_k=d_v=128 "
                                    "N=65536 top-32 reads/writes, bf16 q/k/v/gates, fp32 memory",
                        "global_batch": B, "seq_len": T, "heads": H, "slots_per_head": w.N,
-                       "topk": w.topk, "inputs": "bf16", "state": "f32", "parallelism": "none (1 GPU)"},
+                       "topk": w.topk, "inputs": "bf16", "state": "f32", "parallelism": "none (1 GPU)",
+                       "pipeline": f"sdm_forward: addressing of chunk c+1 overlaps the scan of chunk c, "
+                                   f"{round(args.steps * T / scan_launches)}-token chunks"},
+            "ms_per_step_sequential": round(ms_seq, 4),
             "kernels_ms": {n: round(v[0] / max(v[1], 1), 4) for n, v in kern.items()},
             "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                          "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
@@ -226,7 +246,7 @@ def main():
         if not args.no_cpu_baseline:
             log("cpu baseline (oracle)")
             out["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_streams, min(args.cpu_tokens, w.T))
-        del q, k, v, al, be, cb, mem, ws, y, bufs
+        del q, k, v, al, be, cb, mem, ws, y, outs
         torch.cuda.empty_cache()
 
     # ------------------------------------------------------------ training step

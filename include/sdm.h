@@ -110,6 +110,39 @@ int sdm_scan_fwd(const int32_t* w_idx, const float* w_val, int W,
                  float* y, float* saved, size_t saved_bytes,
                  void* workspace, size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------------------------------
+ * sdm_forward — the whole forward of the layer's memory (Sec. 3.1 steps 1-3):
+ * sdm_address on q (read side, codebook cb_q) and on k (write side, cb_k),
+ * then sdm_scan_fwd with W = R = topk, with the same results bit for bit.
+ * The addressing of a chunk of `chunk` tokens overlaps the scan of the
+ * previous chunk: chunk c's addressing and records run on a library-owned
+ * second stream of the device (created on first use, default priority,
+ * synchronised with `stream` through events), its scan on `stream`.  When the
+ * call returns, all of its work is ordered before later work on `stream`.
+ *   q, k          [B, H, T, d_k] in x_dtype.
+ *   cb_q, cb_k    codebooks as for sdm_address (may be the same pointer or
+ *                 both NULL for direct mode).
+ *   r_idx, r_val  out [B, H, T, topk]: read slots and weights.
+ *   w_idx, w_val  out [B, H, T, topk]: write slots and weights.
+ *   v, alpha, beta, in_dtype, mem, y, saved, saved_bytes, workspace, ws_bytes:
+ *                 as for sdm_scan_fwd (workspace of
+ *                 sdm_scan_fwd_workspace_bytes(B, H, T, topk, topk)).
+ *   chunk         tokens per pipeline stage, rounded up to a multiple of 64
+ *                 and to at most 64 stages; 0 picks T/4 for T >= 2048 and a
+ *                 single stage otherwise.
+ * Outputs must not alias inputs or each other.  Validation as for the three
+ * calls; on a HIP launch error part of the work may already be enqueued.
+ * Concurrent calls on one device share its second stream, so they serialise
+ * their addressing.
+ * ---------------------------------------------------------------------- */
+int sdm_forward(const void* q, const void* k, int x_dtype,
+                const void* cb_q, const void* cb_k, int d_k, int topk,
+                const void* v, const void* alpha, const void* beta, int in_dtype,
+                float* mem, int B, int H, int T, int d_v, int64_t N,
+                int32_t* r_idx, float* r_val, int32_t* w_idx, float* w_val,
+                float* y, float* saved, size_t saved_bytes, int chunk,
+                void* workspace, size_t ws_bytes, void* stream);
+
 size_t sdm_scan_fwd_workspace_bytes(int B, int H, int T, int W, int R);
 size_t sdm_scan_saved_bytes(int B, int H, int T, int W, int d_v);
 

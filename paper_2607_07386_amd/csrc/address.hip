@@ -497,7 +497,7 @@ __device__ __noinline__ void token_general(const float* row, int s, int sp, int 
 template <typename XT, int MODE, int E>   // MODE 0: direct, 1: codebook FMA, 2: codebook MFMA (bf16)
 __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restrict__ x,
                                                             const XT* __restrict__ cb, int H, int T,
-                                                            int dk, int s, int k,
+                                                            int tb, int te, int dk, int s, int k,
                                                             int32_t* __restrict__ idx,
                                                             float* __restrict__ val,
                                                             float* __restrict__ score) {
@@ -508,7 +508,7 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
 
     const int stream = blockIdx.y;
     const int h = stream % H;
-    const int t0 = blockIdx.x * ATILE;
+    const int t0 = tb + blockIdx.x * ATILE;   // tile of tokens [t0, t0 + ATILE) within [tb, te)
     const int tid = threadIdx.x;
     const int wave = tid / SDM_WAVE;
     const int lane = lane_id();
@@ -524,7 +524,7 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
         for (int i = tid; i < ATILE * 2 * SP; i += blockDim.x) {
             const int tt = i / (2 * SP), half = (i / SP) & 1, j = i % SP;
             const int t = t0 + tt;
-            scores[i] = j >= s ? -INFINITY : (t < T ? to_f32(xs[(size_t)t * dk + half * s + j]) : 0.f);
+            scores[i] = j >= s ? -INFINITY : (t < te ? to_f32(xs[(size_t)t * dk + half * s + j]) : 0.f);
         }
     } else if constexpr (MODE == 1) {
         const int dh = dk / 2;
@@ -533,7 +533,7 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
             const int tt = i / (2 * SP), half = (i / SP) & 1, j = i % SP;
             const int t = t0 + tt;
             float acc = 0.f;
-            if (j < s && t < T) {
+            if (j < s && t < te) {
                 const XT* xr = xs + (size_t)t * dk + half * dh;
                 const XT* cr = cbh + ((size_t)half * s + j) * dh;
                 for (int c = 0; c < dh; ++c) acc = fmaf(to_f32(xr[c]), to_f32(cr[c]), acc);
@@ -558,7 +558,7 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
             for (int ks = 0; ks < MAXKS; ++ks) {
                 const int kc = ks * 32 + 8 * q;
                 a[ks] = sdm_bf16x8{};
-                if (ks < nks && t < T && kc < dh)
+                if (ks < nks && t < te && kc < dh)
                     a[ks] = *reinterpret_cast<const sdm_bf16x8*>(xs + (size_t)t * dk + half * dh + kc);
             }
             for (int jt = wave; jt < ntile; jt += AWAVES) {
@@ -610,7 +610,7 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
     }
     for (int tt = wave; tt < ATILE; tt += AWAVES) {
         const int t = t0 + tt;
-        if (t >= T) break;
+        if (t >= te) break;
         const float* row = scores + (size_t)tt * 2 * SP;
         if constexpr (E <= 4) {
             if (fast) {
@@ -681,10 +681,10 @@ constexpr size_t address_lds_bytes(int E) {
 }
 
 template <typename XT, int MODE>
-hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, int dk, int s,
-                            int k, int32_t* idx, float* val, float* score, hipStream_t st) {
+hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, int tb, int tn, int dk,
+                            int s, int k, int32_t* idx, float* val, float* score, hipStream_t st) {
     const int E = (s + SDM_WAVE - 1) / SDM_WAVE;
-    dim3 grid((T + ATILE - 1) / ATILE, B * H);
+    dim3 grid((tn + ATILE - 1) / ATILE, B * H);
     const XT* xp = static_cast<const XT*>(x);
     const XT* cp = static_cast<const XT*>(cb);
 #define SDM_ADDR_CASE(EE)                                                                       \
@@ -694,8 +694,8 @@ hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, 
         hipError_t e = hipFuncSetAttribute((const void*)kfn,                                    \
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm); \
         if (e != hipSuccess) return e;                                                          \
-        hipLaunchKernelGGL(kfn, grid, dim3(ATILE * 16), sm, st, xp, cp, H, T, dk, s, k, idx,    \
-                           val, score);                                                         \
+        hipLaunchKernelGGL(kfn, grid, dim3(ATILE * 16), sm, st, xp, cp, H, T, tb, tb + tn, dk, s, k,\
+                           idx, val, score);                                                    \
         return hipGetLastError();                                                               \
     }
     if (E <= 1) SDM_ADDR_CASE(1)
@@ -709,16 +709,17 @@ hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, 
 }  // namespace
 
 hipError_t sdm_launch_address(const void* x, int x_dtype, const void* cb, int B, int H, int T,
-                              int dk, int s, int k, int32_t* idx, float* val, float* score,
-                              hipStream_t st) {
+                              int tb, int tn, int dk, int s, int k, int32_t* idx, float* val,
+                              float* score, hipStream_t st) {
+    if (tn <= 0) return hipSuccess;
     if (x_dtype == SDM_DT_BF16) {
-        if (!cb) return launch_address_e<bf16_t, 0>(x, cb, B, H, T, dk, s, k, idx, val, score, st);
+        if (!cb) return launch_address_e<bf16_t, 0>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st);
         if ((dk / 2) % 8 == 0)
-            return launch_address_e<bf16_t, 2>(x, cb, B, H, T, dk, s, k, idx, val, score, st);
-        return launch_address_e<bf16_t, 1>(x, cb, B, H, T, dk, s, k, idx, val, score, st);
+            return launch_address_e<bf16_t, 2>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st);
+        return launch_address_e<bf16_t, 1>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st);
     }
-    if (!cb) return launch_address_e<float, 0>(x, cb, B, H, T, dk, s, k, idx, val, score, st);
-    return launch_address_e<float, 1>(x, cb, B, H, T, dk, s, k, idx, val, score, st);
+    if (!cb) return launch_address_e<float, 0>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st);
+    return launch_address_e<float, 1>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st);
 }
 
 hipError_t sdm_launch_address_bwd(const void* cb, int cb_dtype, int B, int H, int T, int dk, int s,

@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <algorithm>
 #include <atomic>
 #include <mutex>
 #include <vector>
@@ -130,6 +131,73 @@ void sdm_prof_end(int k, hipStream_t st) {
     if (e && hipEventRecord(e, st) == hipSuccess) p.done[k].push_back({b, e});
 }
 
+namespace {
+
+// Validation shared by sdm_address and sdm_forward; *s_out = sqrt(N).
+int check_address(const void* x, int x_dtype, const void* codebook, int B, int H, int T, int d_k,
+                  int64_t N, int topk, const int32_t* idx, const float* val, const float* score,
+                  int* s_out) {
+    if (B < 0 || H < 0 || T < 0) return fail(SDM_ERR_INVALID_ARG, "B, H, T must be >= 0");
+    if ((int64_t)B * H > kMaxStreams) return fail(SDM_ERR_UNSUPPORTED, "B*H must be <= %d", kMaxStreams);
+    if (!valid_dtype(x_dtype)) return fail(SDM_ERR_INVALID_ARG, "x_dtype must be SDM_F32 or SDM_BF16");
+    const int s = isqrt64(N);
+    if (s < 0) return fail(SDM_ERR_INVALID_ARG, "N=%lld is not a perfect square", (long long)N);
+    if (s > 1024) return fail(SDM_ERR_UNSUPPORTED, "sqrt(N) must be <= 1024");
+    if (topk < 1 || topk > s) return fail(SDM_ERR_INVALID_ARG, "topk must be in [1, sqrt(N)]");
+    if (topk > 64) return fail(SDM_ERR_UNSUPPORTED, "topk must be <= 64");
+    if (d_k < 1) return fail(SDM_ERR_INVALID_ARG, "d_k must be >= 1");
+    if (codebook) {
+        if (d_k % 2) return fail(SDM_ERR_INVALID_ARG, "codebook mode needs an even d_k");
+        if (d_k / 2 > 256) return fail(SDM_ERR_UNSUPPORTED, "codebook mode needs d_k/2 <= 256");
+        if (!aligned(codebook, 16)) return fail(SDM_ERR_INVALID_ARG, "misaligned codebook");
+    } else if (d_k != 2 * s) {
+        return fail(SDM_ERR_INVALID_ARG, "direct mode needs d_k == 2*sqrt(N)");
+    }
+    *s_out = s;
+    if ((int64_t)B * H * T == 0) return SDM_OK;   // nothing is read or written
+    if (!x || !idx || !val) return fail(SDM_ERR_INVALID_ARG, "null pointer");
+    if (!aligned(x, 16) || !aligned(idx, 4) || !aligned(val, 4) || (score && !aligned(score, 4)))
+        return fail(SDM_ERR_INVALID_ARG, "misaligned pointer");
+    return SDM_OK;
+}
+
+// Outputs, plan and workspace of a forward scan (after check_scan_common, T > 0).
+int check_scan_fwd_rest(int W, int R, int in_dtype, int B, int H, int T, int d_v, const float* y,
+                        const float* saved, size_t saved_bytes, const void* workspace, size_t ws_bytes) {
+    if (!y || !aligned(y, 16)) return fail(SDM_ERR_INVALID_ARG, "y must be a 16-byte aligned pointer");
+    if (saved) {
+        if (!aligned(saved, 16)) return fail(SDM_ERR_INVALID_ARG, "misaligned saved buffer");
+        if (saved_bytes < sdm_scan_saved_bytes(B, H, T, W, d_v))
+            return fail(SDM_ERR_WORKSPACE, "saved buffer too small: %zu < %zu", saved_bytes,
+                        sdm_scan_saved_bytes(B, H, T, W, d_v));
+    }
+    if (!sdm_fwd_plan_ok(W, R, d_v, in_dtype))
+        return fail(SDM_ERR_UNSUPPORTED, "no forward launch plan for W=%d R=%d d_v=%d", W, R, d_v);
+    const size_t need = sdm_fwd_ws_bytes(B, H, T, W, R);
+    if (!workspace || !aligned(workspace, 256))
+        return fail(SDM_ERR_INVALID_ARG, "workspace must be a 256-byte aligned pointer");
+    if (ws_bytes < need) return fail(SDM_ERR_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, need);
+    return SDM_OK;
+}
+
+}  // namespace
+
+// ---- state of the fused forward's pipeline ----
+namespace {
+constexpr int kMaxChunks = 64;
+constexpr int kMaxDevices = 64;
+struct SidePipe {
+    std::mutex mu;
+    hipStream_t side[kMaxDevices] = {};
+    std::vector<hipEvent_t> ev[kMaxDevices];
+};
+SidePipe& side_pipe() {
+    static SidePipe p;
+    return p;
+}
+int round_up(int x, int m) { return (x + m - 1) / m * m; }
+}  // namespace
+
 extern "C" {
 
 int sdm_set_scan_slice_width(int sw) {
@@ -191,33 +259,17 @@ const char* sdm_status_string(int status) {
     }
 }
 
+
 int sdm_address(const void* x, int x_dtype, const void* codebook, int B, int H, int T, int d_k,
                 int64_t N, int topk, int32_t* idx, float* val, float* score, void* stream) {
     g_err[0] = 0;
-    if (B < 0 || H < 0 || T < 0) return fail(SDM_ERR_INVALID_ARG, "B, H, T must be >= 0");
-    if ((int64_t)B * H > kMaxStreams) return fail(SDM_ERR_UNSUPPORTED, "B*H must be <= %d", kMaxStreams);
-    if (!valid_dtype(x_dtype)) return fail(SDM_ERR_INVALID_ARG, "x_dtype must be SDM_F32 or SDM_BF16");
-    const int s = isqrt64(N);
-    if (s < 0) return fail(SDM_ERR_INVALID_ARG, "N=%lld is not a perfect square", (long long)N);
-    if (s > 1024) return fail(SDM_ERR_UNSUPPORTED, "sqrt(N) must be <= 1024");
-    if (topk < 1 || topk > s) return fail(SDM_ERR_INVALID_ARG, "topk must be in [1, sqrt(N)]");
-    if (topk > 64) return fail(SDM_ERR_UNSUPPORTED, "topk must be <= 64");
-    if (d_k < 1) return fail(SDM_ERR_INVALID_ARG, "d_k must be >= 1");
-    if (codebook) {
-        if (d_k % 2) return fail(SDM_ERR_INVALID_ARG, "codebook mode needs an even d_k");
-        if (d_k / 2 > 256) return fail(SDM_ERR_UNSUPPORTED, "codebook mode needs d_k/2 <= 256");
-        if (!aligned(codebook, 16)) return fail(SDM_ERR_INVALID_ARG, "misaligned codebook");
-    } else if (d_k != 2 * s) {
-        return fail(SDM_ERR_INVALID_ARG, "direct mode needs d_k == 2*sqrt(N)");
-    }
-    if ((int64_t)B * H * T == 0) return SDM_OK;   // nothing is read or written
-    if (!x || !idx || !val) return fail(SDM_ERR_INVALID_ARG, "null pointer");
-    if (!aligned(x, 16) || !aligned(idx, 4) || !aligned(val, 4) || (score && !aligned(score, 4)))
-        return fail(SDM_ERR_INVALID_ARG, "misaligned pointer");
+    int s = 0;
+    const int rc = check_address(x, x_dtype, codebook, B, H, T, d_k, N, topk, idx, val, score, &s);
+    if (rc != SDM_OK || (int64_t)B * H * T == 0) return rc;
     hipError_t e;
     {
         SdmProfScope ps(SDM_K_ADDRESS, (hipStream_t)stream);
-        e = sdm_launch_address(x, x_dtype, codebook, B, H, T, d_k, s, topk, idx, val, score,
+        e = sdm_launch_address(x, x_dtype, codebook, B, H, T, 0, T, d_k, s, topk, idx, val, score,
                                (hipStream_t)stream);
     }
     if (e != hipSuccess) return hip_fail(e, "sdm_address launch");
@@ -248,19 +300,8 @@ int sdm_scan_fwd(const int32_t* w_idx, const float* w_val, int W, const int32_t*
                                H, T, d_v, N);
     if (rc != SDM_OK) return rc;
     if ((int64_t)B * H * T == 0) return SDM_OK;   // nothing is read or written
-    if (!y || !aligned(y, 16)) return fail(SDM_ERR_INVALID_ARG, "y must be a 16-byte aligned pointer");
-    if (saved) {
-        if (!aligned(saved, 16)) return fail(SDM_ERR_INVALID_ARG, "misaligned saved buffer");
-        if (saved_bytes < sdm_scan_saved_bytes(B, H, T, W, d_v))
-            return fail(SDM_ERR_WORKSPACE, "saved buffer too small: %zu < %zu", saved_bytes,
-                        sdm_scan_saved_bytes(B, H, T, W, d_v));
-    }
-    if (!sdm_fwd_plan_ok(W, R, d_v, in_dtype))
-        return fail(SDM_ERR_UNSUPPORTED, "no forward launch plan for W=%d R=%d d_v=%d", W, R, d_v);
-    const size_t need = sdm_fwd_ws_bytes(B, H, T, W, R);
-    if (!workspace || !aligned(workspace, 256))
-        return fail(SDM_ERR_INVALID_ARG, "workspace must be a 256-byte aligned pointer");
-    if (ws_bytes < need) return fail(SDM_ERR_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, need);
+    rc = check_scan_fwd_rest(W, R, in_dtype, B, H, T, d_v, y, saved, saved_bytes, workspace, ws_bytes);
+    if (rc != SDM_OK) return rc;
     hipStream_t st = (hipStream_t)stream;
     hipError_t e = sdm_launch_zero_words(workspace, 4, st);
     if (e != hipSuccess) return hip_fail(e, "sdm_scan_fwd flag reset");
@@ -269,8 +310,109 @@ int sdm_scan_fwd(const int32_t* w_idx, const float* w_val, int W, const int32_t*
     a.v = v; a.alpha = alpha; a.beta = beta; a.in_dtype = in_dtype;
     a.mem = mem; a.B = B; a.H = H; a.T = T; a.dv = d_v; a.W = W; a.R = R; a.N = N;
     a.y = y; a.saved = saved; a.ws = static_cast<unsigned char*>(workspace);
+    a.tb = 0; a.te = T;
     e = sdm_launch_scan_fwd(a, st);
     if (e != hipSuccess) return hip_fail(e, "sdm_scan_fwd launch");
+    return SDM_OK;
+}
+
+// ---- fused forward: addressing pipelined with the scan over chunks of tokens ----
+
+int sdm_forward(const void* q, const void* k, int x_dtype, const void* cb_q, const void* cb_k, int d_k,
+                int topk, const void* v, const void* alpha, const void* beta, int in_dtype, float* mem,
+                int B, int H, int T, int d_v, int64_t N, int32_t* r_idx, float* r_val, int32_t* w_idx,
+                float* w_val, float* y, float* saved, size_t saved_bytes, int chunk, void* workspace,
+                size_t ws_bytes, void* stream) {
+    g_err[0] = 0;
+    int s = 0;
+    int rc = check_address(q, x_dtype, cb_q, B, H, T, d_k, N, topk, r_idx, r_val, nullptr, &s);
+    if (rc != SDM_OK) return rc;
+    rc = check_address(k, x_dtype, cb_k, B, H, T, d_k, N, topk, w_idx, w_val, nullptr, &s);
+    if (rc != SDM_OK) return rc;
+    rc = check_scan_common(w_idx, w_val, topk, r_idx, r_val, topk, v, alpha, beta, in_dtype, mem, B, H,
+                           T, d_v, N);
+    if (rc != SDM_OK) return rc;
+    if (chunk < 0) return fail(SDM_ERR_INVALID_ARG, "chunk must be >= 0");
+    if ((int64_t)B * H * T == 0) return SDM_OK;
+    rc = check_scan_fwd_rest(topk, topk, in_dtype, B, H, T, d_v, y, saved, saved_bytes, workspace,
+                             ws_bytes);
+    if (rc != SDM_OK) return rc;
+
+    // pipeline stage length: a multiple of 64 tokens, at most kMaxChunks stages
+    int len = chunk > 0 ? round_up(chunk, 64) : (T >= 2048 ? round_up((T + 3) / 4, 64) : T);
+    len = std::max(len, round_up((T + kMaxChunks - 1) / kMaxChunks, 64));
+    const int nchunks = (T + len - 1) / len;
+
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e = sdm_launch_zero_words(workspace, 4, st);
+    if (e != hipSuccess) return hip_fail(e, "sdm_forward flag reset");
+    ScanFwdArgs a;
+    a.w_idx = w_idx; a.w_val = w_val; a.r_idx = r_idx; a.r_val = r_val;
+    a.v = v; a.alpha = alpha; a.beta = beta; a.in_dtype = in_dtype;
+    a.mem = mem; a.B = B; a.H = H; a.T = T; a.dv = d_v; a.W = topk; a.R = topk; a.N = N;
+    a.y = y; a.saved = saved; a.ws = static_cast<unsigned char*>(workspace);
+
+    auto stage_front = [&](int tb, int te, hipStream_t sx) -> hipError_t {
+        hipError_t ee;
+        {
+            SdmProfScope ps(SDM_K_ADDRESS, sx);
+            ee = sdm_launch_address(q, x_dtype, cb_q, B, H, T, tb, te - tb, d_k, s, topk, r_idx, r_val,
+                                    nullptr, sx);
+        }
+        if (ee != hipSuccess) return ee;
+        {
+            SdmProfScope ps(SDM_K_ADDRESS, sx);
+            ee = sdm_launch_address(k, x_dtype, cb_k, B, H, T, tb, te - tb, d_k, s, topk, w_idx, w_val,
+                                    nullptr, sx);
+        }
+        if (ee != hipSuccess) return ee;
+        ScanFwdArgs ac = a;
+        ac.tb = tb;
+        ac.te = te;
+        return sdm_launch_fwd_prep_range(ac, sx);
+    };
+
+    if (nchunks == 1) {
+        e = stage_front(0, T, st);
+        if (e == hipSuccess) {
+            a.tb = 0;
+            a.te = T;
+            e = sdm_launch_fwd_scan_range(a, st);
+        }
+        return e == hipSuccess ? SDM_OK : hip_fail(e, "sdm_forward launch");
+    }
+
+    int dev = 0;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return hip_fail(e, "sdm_forward hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(SDM_ERR_UNSUPPORTED, "device index %d", dev);
+    SidePipe& sp = side_pipe();
+    std::lock_guard<std::mutex> lk(sp.mu);
+    if (!sp.side[dev]) {
+        if ((e = hipStreamCreateWithFlags(&sp.side[dev], hipStreamNonBlocking)) != hipSuccess) {
+            sp.side[dev] = nullptr;
+            return hip_fail(e, "sdm_forward side stream");
+        }
+    }
+    std::vector<hipEvent_t>& ev = sp.ev[dev];
+    while ((int)ev.size() < nchunks + 1) {
+        hipEvent_t x;
+        if ((e = hipEventCreateWithFlags(&x, hipEventDisableTiming)) != hipSuccess)
+            return hip_fail(e, "sdm_forward event");
+        ev.push_back(x);
+    }
+    hipStream_t side = sp.side[dev];
+    // the side stream starts after the caller's earlier work; chunk c's scan waits for its front
+    if ((e = hipEventRecord(ev[0], st)) != hipSuccess) return hip_fail(e, "sdm_forward record");
+    if ((e = hipStreamWaitEvent(side, ev[0], 0)) != hipSuccess) return hip_fail(e, "sdm_forward wait");
+    for (int c = 0; c < nchunks; ++c) {
+        const int tb = c * len, te = std::min(T, tb + len);
+        if ((e = stage_front(tb, te, side)) != hipSuccess) return hip_fail(e, "sdm_forward launch");
+        if ((e = hipEventRecord(ev[c + 1], side)) != hipSuccess) return hip_fail(e, "sdm_forward record");
+        if ((e = hipStreamWaitEvent(st, ev[c + 1], 0)) != hipSuccess) return hip_fail(e, "sdm_forward wait");
+        a.tb = tb;
+        a.te = te;
+        if ((e = sdm_launch_fwd_scan_range(a, st)) != hipSuccess) return hip_fail(e, "sdm_forward launch");
+    }
     return SDM_OK;
 }
 

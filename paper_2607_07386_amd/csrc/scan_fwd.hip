@@ -39,16 +39,16 @@ __host__ __device__ constexpr int stage_slots() {
 }
 
 // Staging of the G records (and v slices) of tokens [u0, u0 + G): global -> registers.
-// Every lane always loads: indices past the end are clamped to valid data (the
+// Every lane always loads: indices at or past te are clamped to valid data (the
 // surplus is never read), so the loads carry no control flow.
 template <typename VT, int SW, int NR>
 __device__ __forceinline__ void stage_load(u4v (&st)[NR], u2v& stv, const unsigned char* srec,
-                                           const VT* sv, int u0, int T, int dv, int slice,
+                                           const VT* sv, int u0, int te, int dv, int slice,
                                            int rec_bytes, int lane) {
     constexpr int VB = SW * (int)sizeof(VT);
     constexpr int ppt = VB / 8;   // 8-byte pieces per token
-    const int ub = min(u0, T - 1);
-    const int cnt = min(G, T - ub);
+    const int ub = min(u0, te - 1);
+    const int cnt = min(G, te - ub);
     const u4v* src = reinterpret_cast<const u4v*>(srec + (size_t)ub * rec_bytes);
     const int last = cnt * rec_bytes / 16 - 1;
 #pragma unroll
@@ -172,8 +172,9 @@ __device__ __forceinline__ void fwd_token(const FwdCtx<VT, SW, PD, K, SAVE>& c, 
 template <typename VT, int SW, int PD, int K, int NR, bool SAVE>
 __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_fwd_kernel(
     const unsigned char* __restrict__ recs, const VT* __restrict__ v, float* __restrict__ mem,
-    float* __restrict__ y, float* __restrict__ saved, int T, int dv, int W, int R, int64_t N,
-    int n_slices, int lds_per_wave) {
+    float* __restrict__ y, float* __restrict__ saved, int T, int tb, int te, int dv, int W, int R,
+    int64_t N, int n_slices, int lds_per_wave) {
+    // tokens [tb, te) of each stream (tb a multiple of PD); layout strides use T
     constexpr int CQ = SW / 4;           // lanes per row slice (16 bytes each)
     constexpr int RG = SDM_WAVE / CQ;    // rows per load instruction
     constexpr int LEAD = stage_lead<PD>();
@@ -216,35 +217,36 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_fwd_kernel(
     u2v stv;
     v4f Pw[PD][K], Pr[PD][K];
 
-    // ---- prologue: records of tokens [0, LEAD-G) in LDS, the next block in
-    //      registers, rows of tokens [0, PD) in flight ----
-    for (int u0 = 0; u0 < LEAD - G; u0 += G) {
-        stage_load<VT, SW, NR>(st, stv, srec, sv, u0, T, dv, slice, c.L.bytes, lane);
+    // ---- prologue: records of tokens [tb, tb+LEAD-G) in LDS, the next block in
+    //      registers, rows of tokens [tb, tb+PD) in flight ----
+    for (int u0 = tb; u0 < tb + LEAD - G; u0 += G) {
+        stage_load<VT, SW, NR>(st, stv, srec, sv, u0, te, dv, slice, c.L.bytes, lane);
         stage_store<VT, SW, NS, NR>(st, stv, rring, vring, u0, c.L.bytes, lane);
     }
-    stage_load<VT, SW, NR>(st, stv, srec, sv, LEAD - G, T, dv, slice, c.L.bytes, lane);
+    stage_load<VT, SW, NR>(st, stv, srec, sv, tb + LEAD - G, te, dv, slice, c.L.bytes, lane);
 #pragma unroll
-    for (int j = 0; j < PD; ++j) issue_rows<K, RG, NS>(Pw[j], Pr[j], rring, c.L, c.tab, min(j, T - 1), dv, c.rg);
+    for (int j = 0; j < PD; ++j)
+        issue_rows<K, RG, NS>(Pw[j], Pr[j], rring, c.L, c.tab, min(tb + j, te - 1), dv, c.rg);
 
     // ---- main loop over whole blocks of PD tokens; buffer j holds token t0 + j ----
-    const int Tfull = T - T % PD;
-    for (int t0 = 0; t0 < Tfull; t0 += PD) {
+    const int Tfull = te - (te - tb) % PD;
+    for (int t0 = tb; t0 < Tfull; t0 += PD) {
 #pragma unroll
         for (int j = 0; j < PD; ++j) {
             const int t = t0 + j;
             if (j % G == 0) {
                 stage_store<VT, SW, NS, NR>(st, stv, rring, vring, t + LEAD - G, c.L.bytes, lane);
-                stage_load<VT, SW, NR>(st, stv, srec, sv, t + LEAD, T, dv, slice, c.L.bytes, lane);
+                stage_load<VT, SW, NR>(st, stv, srec, sv, t + LEAD, te, dv, slice, c.L.bytes, lane);
             }
             fwd_token<VT, SW, PD, K, SAVE, NS>(c, Pw[j], Pr[j], t);
-            issue_rows<K, RG, NS>(Pw[j], Pr[j], rring, c.L, c.tab, min(t + PD, T - 1), dv, c.rg);
+            issue_rows<K, RG, NS>(Pw[j], Pr[j], rring, c.L, c.tab, min(t + PD, te - 1), dv, c.rg);
         }
     }
     // ---- tail: fewer than PD tokens, all rows already in flight ----
 #pragma unroll
     for (int j = 0; j < PD; ++j) {
         const int t = Tfull + j;
-        if (t < T) fwd_token<VT, SW, PD, K, SAVE, NS>(c, Pw[j], Pr[j], t);
+        if (t < te) fwd_token<VT, SW, PD, K, SAVE, NS>(c, Pw[j], Pr[j], t);
     }
 }
 
@@ -304,7 +306,7 @@ hipError_t launch_fwd_k(const ScanFwdArgs& a, const FwdPlan& p, hipStream_t st) 
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kfn, grid, dim3(p.wpb * SDM_WAVE), sm, st,
                        a.ws + SDM_WS_HEADER, static_cast<const VT*>(a.v), a.mem, a.y, a.saved, a.T,
-                       a.dv, a.W, a.R, a.N, p.n_slices, p.lds_per_wave);
+                       a.tb, a.te, a.dv, a.W, a.R, a.N, p.n_slices, p.lds_per_wave);
     return hipGetLastError();
 }
 
@@ -330,18 +332,23 @@ bool sdm_fwd_plan_ok(int W, int R, int dv, int in_dtype) {
     return fwd_plan_sw<16>(W, R, dv, in_dtype, &p) && fwd_plan_sw<8>(W, R, dv, in_dtype, &p);
 }
 
-hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st) {
+hipError_t sdm_launch_fwd_prep_range(const ScanFwdArgs& a, hipStream_t st) {
+    SdmProfScope ps(SDM_K_FWD_PREP, st);
+    return sdm_launch_fwd_prep<FWD_PD>(a, st);
+}
+
+hipError_t sdm_launch_fwd_scan_range(const ScanFwdArgs& a, hipStream_t st) {
     FwdPlan p;
     if (!fwd_plan(a.B * a.H, a.W, a.R, a.dv, a.in_dtype, &p)) return hipErrorInvalidConfiguration;
-    hipError_t e;
-    {
-        SdmProfScope ps(SDM_K_FWD_PREP, st);
-        e = sdm_launch_fwd_prep<FWD_PD>(a, st);
-    }
-    if (e != hipSuccess) return e;
     const bool save = a.saved != nullptr;
     SdmProfScope ps(SDM_K_FWD_SCAN, st);
     if (a.in_dtype == SDM_DT_BF16)
         return save ? launch_fwd_kk<bf16_t, true>(a, p, st) : launch_fwd_kk<bf16_t, false>(a, p, st);
     return save ? launch_fwd_kk<float, true>(a, p, st) : launch_fwd_kk<float, false>(a, p, st);
+}
+
+hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st) {
+    hipError_t e = sdm_launch_fwd_prep_range(a, st);
+    if (e != hipSuccess) return e;
+    return sdm_launch_fwd_scan_range(a, st);
 }

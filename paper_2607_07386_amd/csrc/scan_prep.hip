@@ -68,7 +68,9 @@ __device__ __forceinline__ void mark_sorted(const int* lst, int nl, int len, int
 // ---------------------------------------------------------------- forward
 // Token t, write row n: latest writer t-d, 1 <= d < PD, of the same slot.
 // Token t, read row m: latest writer t-d, 0 <= d < PD (d = 0: t itself).
-// Entry = position of the slot in that writer's write list.
+// Entry = position of the slot in that writer's write list.  Records are made
+// for tokens [ta, te) of each stream; writers before ta are not linked (a scan
+// started at ta finds their rows in HBM).
 template <int PD>
 __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict__ w_idx,
                                                        const float* __restrict__ w_val,
@@ -76,15 +78,15 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
                                                        const float* __restrict__ r_val,
                                                        const void* __restrict__ alpha,
                                                        const void* __restrict__ beta, int in_dtype,
-                                                       int T, int W, int R, int64_t N,
+                                                       int T, int ta, int te, int W, int R, int64_t N,
                                                        unsigned char* __restrict__ recs,
                                                        unsigned int* __restrict__ err) {
     extern __shared__ int sm[];
     const FwdRec L = fwd_rec_layout(W, R);
     const int stream = blockIdx.y;
-    const int t0 = blockIdx.x * PT;
+    const int t0 = ta + blockIdx.x * PT;
     const int tb = t0 - (PD - 1);           // first token whose write list is needed
-    const int ntok = min(PT, T - t0);
+    const int ntok = min(PT, te - t0);
     const int nw = ntok + PD - 1;           // write lists held
     const int nrow = W + R;
     int* wl = sm;                                        // [PT+PD-1][W]
@@ -96,7 +98,7 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
 
     for (int i = threadIdx.x; i < nw * W; i += blockDim.x) {
         const int t = tb + i / W;
-        wl[i] = t >= 0 ? clamp_slot(w_idx[(sbase + t) * W + i % W], N, bad) : -1;
+        wl[i] = t >= ta ? clamp_slot(w_idx[(sbase + t) * W + i % W], N, bad) : -1;
     }
     for (int i = threadIdx.x; i < ntok * R; i += blockDim.x)
         rl[i] = clamp_slot(r_idx[(sbase + t0) * R + i], N, bad);
@@ -109,7 +111,7 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
         const bool wrow = r < W;
         const int slot = wrow ? wl[(tl + PD - 1) * W + r] : rl[tl * R + (r - W)];
         const int dlo = wrow ? 1 : 0;           // a read row may hit its own token
-        const int dhi = min(PD - 1, t0 + tl);   // no writer before token 0
+        const int dhi = min(PD - 1, t0 + tl - ta);   // no writer before token ta
         short link = -1;
         for (int d = dhi; d >= dlo; --d) {
             const int u = tl + PD - 1 - d;       // write list of token t - d
@@ -266,13 +268,13 @@ size_t bwd_prep_lds(int W, int R) {
 template <int PD>
 hipError_t sdm_launch_fwd_prep(const ScanFwdArgs& a, hipStream_t st) {
     const int S = a.B * a.H;
-    dim3 grid((a.T + PT - 1) / PT, S);
+    dim3 grid((a.te - a.tb + PT - 1) / PT, S);
     const size_t sm = fwd_prep_lds<PD>(a.W, a.R);
     auto kfn = fwd_prep_kernel<PD>;
     hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kfn, grid, dim3(256), sm, st, a.w_idx, a.w_val, a.r_idx, a.r_val, a.alpha,
-                       a.beta, a.in_dtype, a.T, a.W, a.R, a.N, a.ws + SDM_WS_HEADER,
+                       a.beta, a.in_dtype, a.T, a.tb, a.te, a.W, a.R, a.N, a.ws + SDM_WS_HEADER,
                        reinterpret_cast<unsigned int*>(a.ws));
     return hipGetLastError();
 }

@@ -57,9 +57,10 @@ __host__ __device__ inline BwdRec bwd_rec_layout(int W, int R) {
 // Workspace header: device-side error flag(s) at offset 0.
 #define SDM_WS_HEADER 256
 
+// Tokens [tb, tb + tn) of every stream (layout strides use T).
 hipError_t sdm_launch_address(const void* x, int x_dtype, const void* cb, int B, int H, int T,
-                              int dk, int s, int k, int32_t* idx, float* val, float* score,
-                              hipStream_t st);
+                              int tb, int tn, int dk, int s, int k, int32_t* idx, float* val,
+                              float* score, hipStream_t st);
 hipError_t sdm_launch_address_bwd(const void* cb, int cb_dtype, int B, int H, int T, int dk, int s,
                                   int k, const int32_t* idx, const float* val, const float* dval,
                                   float* dx, hipStream_t st);
@@ -79,8 +80,12 @@ struct ScanFwdArgs {
     float* y;
     float* saved;
     unsigned char* ws;   // workspace base (header + records)
+    int tb = 0, te = 0;  // tokens processed: [tb, te) (layout strides use T); tb % 8 == 0
 };
-hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st);
+hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st);   // prep + scan
+// the two halves separately (records of [tb, te), then the scan of [tb, te))
+hipError_t sdm_launch_fwd_prep_range(const ScanFwdArgs& a, hipStream_t st);
+hipError_t sdm_launch_fwd_scan_range(const ScanFwdArgs& a, hipStream_t st);
 // SIMDs (4 per compute unit) of the current device; 1024 if it cannot be queried.
 int sdm_device_simds();
 // Forced scan slice width (8 or 16), or 0 for the automatic choice.

@@ -46,6 +46,8 @@ def lib() -> ctypes.CDLL:
         L.sdm_scan_bwd.argtypes = [P, P, I, I, P, P, I, P, P, I, P, P, P, I, P, P, SZ, P, P, I,
                                    I, I, I, I, I64, P, P, P, P, P, P, P, P, P, SZ, P]
         L.sdm_mem_init.argtypes = [P, P, I, I, I64, I, P]
+        L.sdm_forward.argtypes = [P, P, I, P, P, I, I, P, P, P, I, P, I, I, I, I, I64, P, P, P, P, P, P,
+                                  SZ, I, P, SZ, P]
         L.sdm_scan_fwd_workspace_bytes.argtypes = [I, I, I, I, I]
         L.sdm_scan_saved_bytes.argtypes = [I, I, I, I, I]
         L.sdm_scan_bwd_workspace_bytes.argtypes = [I, I, I, I, I, I]
@@ -159,6 +161,43 @@ def scan_fwd(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, saved=None, worksp
                             _stream(dev))
     _check("sdm_scan_fwd", rc)
     return y
+
+
+def forward(q, k, cb_q, cb_k, v, alpha, beta, mem, N: int, topk: int, saved=None, workspace=None,
+            y=None, out=None, chunk: int = 0):
+    """The layer's memory forward in one call: addressing of q (read side) and k (write side)
+    pipelined with the scan over chunks of tokens; in place on mem.  Returns a dict with y,
+    r_idx, r_val, w_idx, w_val.  out: optional dict of preallocated outputs of those names."""
+    dev = _dev(q, k, cb_q, cb_k, v, alpha, beta, mem, saved, y)
+    B, H, T, dk = q.shape
+    dv = v.shape[-1]
+    if k.shape != q.shape or k.dtype != q.dtype:
+        raise TypeError("q and k must share shape and dtype")
+    for cb in (cb_q, cb_k):
+        if cb is not None and cb.dtype != q.dtype:
+            raise TypeError("codebook dtype must match q and k")
+    if not (v.dtype == alpha.dtype == beta.dtype):
+        raise TypeError("v, alpha, beta must share a dtype")
+    if mem.dtype != torch.float32:
+        raise TypeError("mem must be fp32")
+    o = dict(out or {})
+    shp = (B, H, T, topk)
+    for name, dt in (("r_idx", torch.int32), ("w_idx", torch.int32), ("r_val", torch.float32),
+                     ("w_val", torch.float32)):
+        if name not in o:
+            o[name] = torch.empty(shp, dtype=dt, device=dev)
+    o["y"] = y if y is not None else o.get("y", torch.empty((B, H, T, dv), dtype=torch.float32, device=dev))
+    _dev(*o.values())
+    if workspace is None:
+        workspace = fwd_workspace(B, H, T, topk, topk, dev)
+    sb = saved.numel() * 4 if saved is not None else 0
+    rc = lib().sdm_forward(_ptr(q), _ptr(k), _dtype_code(q), _ptr(cb_q), _ptr(cb_k), dk, topk, _ptr(v),
+                           _ptr(alpha), _ptr(beta), _dtype_code(v), _ptr(mem), B, H, T, dv, N,
+                           _ptr(o["r_idx"]), _ptr(o["r_val"]), _ptr(o["w_idx"]), _ptr(o["w_val"]),
+                           _ptr(o["y"]), _ptr(saved), sb, int(chunk), _ptr(workspace), workspace.numel(),
+                           _stream(dev))
+    _check("sdm_forward", rc)
+    return o
 
 
 def bwd_workspace(B, H, T, W, R, d_v, device) -> torch.Tensor:

@@ -18,3 +18,12 @@ def oracle_mod():
     import oracle
     oracle.build(force=False)
     return oracle
+
+
+@pytest.fixture(params=[8, 16], ids=["sw8", "sw16"])
+def slice_width(request):
+    """Runs a GPU test with each scan slice width forced, then restores the automatic choice."""
+    from paper_2607_07386_amd import sdm
+    sdm.set_scan_slice_width(request.param)
+    yield request.param
+    sdm.set_scan_slice_width(0)

@@ -150,3 +150,22 @@ def test_every_supported_shape_has_a_launch_plan():
                 assert fwd(W=W, R=R, dv=dv, dt=dt, wsb=0) == -3, (W, R, dv, dt)
                 assert bwd(W=W, R=R, dv=dv, dt=dt, wsb=0, cbq=None, cbk=None, dq=None, dkk=None) == -3, \
                     (W, R, dv, dt)
+
+
+def test_forward_validation():
+    """sdm_forward validates like the three calls it fuses, plus its chunk argument."""
+    def fw(**kw):
+        a = dict(q=A, k=A, xdt=1, cbq=B_, cbk=B_, dk=128, topk=32, v=A, al=A, be=A, dt=1, mem=A, B=1,
+                 H=1, T=8, dv=128, N=65536, ri=A, rv=A, wi=A, wv=A, y=A, saved=None, sb=0, chunk=0, ws=A,
+                 wsb=1 << 30)
+        a.update(kw)
+        return L.sdm_forward(a["q"], a["k"], a["xdt"], a["cbq"], a["cbk"], a["dk"], a["topk"], a["v"],
+                             a["al"], a["be"], a["dt"], a["mem"], a["B"], a["H"], a["T"], a["dv"], a["N"],
+                             a["ri"], a["rv"], a["wi"], a["wv"], a["y"], a["saved"], a["sb"], a["chunk"],
+                             a["ws"], a["wsb"], None)
+    for kw, code in ((dict(chunk=-1), -1), (dict(N=65535), -1), (dict(topk=65), -2), (dict(k=None), -1),
+                     (dict(ri=A + 4), -1), (dict(dv=6), -1), (dict(wsb=100), -3), (dict(y=None), -1),
+                     (dict(cbk=A + 2), -1), (dict(xdt=5), -1)):
+        assert fw(**kw) == code, kw
+        assert L.sdm_last_error()
+    assert fw(T=0) == 0

@@ -107,14 +107,6 @@ def m0_fn(w, inp):
     return lambda s: inp.m0_head(inp.heads[s]).astype(np.float64)
 
 
-@pytest.fixture(params=[8, 16], ids=["sw8", "sw16"])
-def slice_width(request):
-    """Runs a test with each scan slice width forced, then restores the automatic choice."""
-    sdm.set_scan_slice_width(request.param)
-    yield request.param
-    sdm.set_scan_slice_width(0)
-
-
 # --------------------------------------------------------------- small cases
 SMALL = {
     "c0-tiny-f32": synth.WORKLOADS[0],
