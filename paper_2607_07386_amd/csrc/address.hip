@@ -628,8 +628,11 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
 }
 
 // Backward of the weights through softmax and the sub-key scores: one wave
-// per token, lanes over the d_k outputs.
-template <typename XT, bool CODEBOOK>
+// per token.  Lane n < k first forms g_n = w_n (wbar_n - sum_m w_m wbar_m) and
+// the sub-key ids of slot n; then, for n = 0 .. k-1 (read across the wave),
+// each lane adds g_n times its NC columns of the two sub-key rows.  The
+// codebook rows are read coalesced, several n in flight.
+template <typename XT, bool CODEBOOK, int NC>
 __global__ __launch_bounds__(256) void address_bwd_kernel(const XT* __restrict__ cb, int H, int T,
                                                           int dk, int s, int k,
                                                           const int32_t* __restrict__ idx,
@@ -640,37 +643,62 @@ __global__ __launch_bounds__(256) void address_bwd_kernel(const XT* __restrict__
     const int64_t r = (int64_t)blockIdx.x * (blockDim.x / SDM_WAVE) + threadIdx.x / SDM_WAVE;
     if (r >= ntok) return;
     const int h = (int)((r / T) % H);
-    const int32_t* I = idx + r * k;
-    const float* w = val + r * k;
-    const float* wb = dval + r * k;
-    float p = 0.f;
-    for (int n = lane; n < k; n += SDM_WAVE) p = fmaf(w[n], wb[n], p);
-    const float dot = wave_sum(p);
+    const bool has = lane < k;
+    const float w = has ? val[r * k + lane] : 0.f;
+    const float wb = has ? dval[r * k + lane] : 0.f;
+    const int id = has ? min(max(idx[r * k + lane], 0), s * s - 1) : 0;   // never read outside
+    const float dot = wave_sum(w * wb);
+    const float g = w * (wb - dot);
+    const int sub0 = id / s, sub1 = id - sub0 * s;
     float* out = dx + r * dk;
+    float acc[NC];
+#pragma unroll
+    for (int i = 0; i < NC; ++i) acc[i] = 0.f;
     if constexpr (CODEBOOK) {
         const int dh = dk / 2;
         const XT* cbh = cb + (size_t)h * 2 * s * dh;
-        for (int c = lane; c < dk; c += SDM_WAVE) {
-            const int half = c / dh, cc = c % dh;
-            float acc = 0.f;
-            for (int n = 0; n < k; ++n) {
-                const float g = w[n] * (wb[n] - dot);
-                const int id = min(max(I[n], 0), s * s - 1);   // never read outside the codebook
-                const int sub = half ? (id % s) : (id / s);
-                acc = fmaf(g, to_f32(cbh[((size_t)half * s + sub) * dh + cc]), acc);
+        int base[NC];   // offset of this lane's column i in sub-key row 0 of its half
+        bool hi[NC];
+#pragma unroll
+        for (int i = 0; i < NC; ++i) {
+            const int c = min(lane + SDM_WAVE * i, dk - 1);
+            hi[i] = c >= dh;
+            base[i] = hi[i] ? s * dh + (c - dh) : c;
+        }
+        // slots past k carry g = 0 and sub-key 0: whole groups of 8, no remainder
+        for (int n0 = 0; n0 < k; n0 += 8) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int n = n0 + u;
+                const float gn = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g), n));
+                const int a0 = __builtin_amdgcn_readlane(sub0, n), a1 = __builtin_amdgcn_readlane(sub1, n);
+#pragma unroll
+                for (int i = 0; i < NC; ++i)
+                    acc[i] = fmaf(gn, to_f32(cbh[base[i] + (hi[i] ? a1 : a0) * dh]), acc[i]);
             }
-            out[c] = acc;
         }
     } else {
-        for (int c = lane; c < dk; c += SDM_WAVE) {
-            const int half = c / s, j = c % s;
-            float acc = 0.f;
-            for (int n = 0; n < k; ++n) {
-                const int sub = half ? (I[n] % s) : (I[n] / s);
-                if (sub == j) acc += w[n] * (wb[n] - dot);
-            }
-            out[c] = acc;
+        // direct mode: column c = half * s + j receives g_n when sub-key half(n) == j
+        int j[NC];
+        bool hi[NC];
+#pragma unroll
+        for (int i = 0; i < NC; ++i) {
+            const int c = lane + SDM_WAVE * i;
+            hi[i] = c >= s;
+            j[i] = hi[i] ? c - s : c;
         }
+        for (int n = 0; n < k; ++n) {
+            const float gn = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g), n));
+            const int a0 = __builtin_amdgcn_readlane(sub0, n), a1 = __builtin_amdgcn_readlane(sub1, n);
+#pragma unroll
+            for (int i = 0; i < NC; ++i)
+                if ((hi[i] ? a1 : a0) == j[i]) acc[i] += gn;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+        const int c = lane + SDM_WAVE * i;
+        if (c < dk) out[c] = acc[i];
     }
 }
 
@@ -722,26 +750,44 @@ hipError_t sdm_launch_address(const void* x, int x_dtype, const void* cb, int B,
     return launch_address_e<float, 1>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st);
 }
 
+namespace {
+
+template <typename XT, int NC>
+void launch_address_bwd_nc(const void* cb, int B, int H, int T, int dk, int s, int k,
+                           const int32_t* idx, const float* val, const float* dval, float* dx,
+                           int64_t ntok, hipStream_t st) {
+    dim3 grid((unsigned)((ntok + 3) / 4));
+    if (cb)
+        hipLaunchKernelGGL((address_bwd_kernel<XT, true, NC>), grid, dim3(256), 0, st,
+                           static_cast<const XT*>(cb), H, T, dk, s, k, idx, val, dval, dx, ntok);
+    else
+        hipLaunchKernelGGL((address_bwd_kernel<XT, false, NC>), grid, dim3(256), 0, st,
+                           static_cast<const XT*>(cb), H, T, dk, s, k, idx, val, dval, dx, ntok);
+}
+
+template <typename XT>
+void launch_address_bwd_t(const void* cb, int B, int H, int T, int dk, int s, int k,
+                          const int32_t* idx, const float* val, const float* dval, float* dx,
+                          int64_t ntok, hipStream_t st) {
+    // columns per lane: d_k <= 512 in codebook mode, d_k = 2 sqrt(N) <= 2048 in direct mode
+    if (dk <= 64) launch_address_bwd_nc<XT, 1>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
+    else if (dk <= 128) launch_address_bwd_nc<XT, 2>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
+    else if (dk <= 256) launch_address_bwd_nc<XT, 4>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
+    else if (dk <= 512) launch_address_bwd_nc<XT, 8>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
+    else if (dk <= 1024) launch_address_bwd_nc<XT, 16>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
+    else launch_address_bwd_nc<XT, 32>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
+}
+
+}  // namespace
+
 hipError_t sdm_launch_address_bwd(const void* cb, int cb_dtype, int B, int H, int T, int dk, int s,
                                   int k, const int32_t* idx, const float* val, const float* dval,
                                   float* dx, hipStream_t st) {
     const int64_t ntok = (int64_t)B * H * T;
     if (ntok == 0) return hipSuccess;
-    dim3 grid((unsigned)((ntok + 3) / 4));
-    if (cb_dtype == SDM_DT_BF16) {
-        if (cb)
-            hipLaunchKernelGGL((address_bwd_kernel<bf16_t, true>), grid, dim3(256), 0, st,
-                               static_cast<const bf16_t*>(cb), H, T, dk, s, k, idx, val, dval, dx, ntok);
-        else
-            hipLaunchKernelGGL((address_bwd_kernel<bf16_t, false>), grid, dim3(256), 0, st,
-                               static_cast<const bf16_t*>(cb), H, T, dk, s, k, idx, val, dval, dx, ntok);
-    } else {
-        if (cb)
-            hipLaunchKernelGGL((address_bwd_kernel<float, true>), grid, dim3(256), 0, st,
-                               static_cast<const float*>(cb), H, T, dk, s, k, idx, val, dval, dx, ntok);
-        else
-            hipLaunchKernelGGL((address_bwd_kernel<float, false>), grid, dim3(256), 0, st,
-                               static_cast<const float*>(cb), H, T, dk, s, k, idx, val, dval, dx, ntok);
-    }
+    if (cb_dtype == SDM_DT_BF16)
+        launch_address_bwd_t<bf16_t>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
+    else
+        launch_address_bwd_t<float>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
     return hipGetLastError();
 }

@@ -444,24 +444,44 @@ hipError_t sdm_launch_scan_bwd(const ScanBwdArgs& a, hipStream_t st) {
 
 // ---------------------------------------------------------------- memory init
 namespace {
+// M0 broadcast over B (m0 = [H][per_head4] float4s) or a zero fill; each thread
+// writes 4 float4s (one per 256-thread stride) per pass of the grid.
 __global__ __launch_bounds__(256) void mem_init_kernel(float4* __restrict__ dst,
                                                        const float4* __restrict__ m0,
                                                        int64_t per_head4, int H, int64_t total4) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total4;
-         i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x * 4;
+    for (int64_t i0 = ((int64_t)blockIdx.x * blockDim.x) * 4 + threadIdx.x; i0 < total4; i0 += stride) {
         if (m0) {
-            const int64_t hh = (i / per_head4) % H;
-            dst[i] = m0[hh * per_head4 + i % per_head4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int64_t i = i0 + (int64_t)u * blockDim.x;
+                if (i < total4) dst[i] = m0[((i / per_head4) % H) * per_head4 + i % per_head4];
+            }
         } else {
-            dst[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int64_t i = i0 + (int64_t)u * blockDim.x;
+                if (i < total4) dst[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+            }
         }
     }
 }
 __global__ __launch_bounds__(256) void copy_kernel(float4* __restrict__ dst, const float4* __restrict__ src,
                                                    int64_t n4) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4;
-         i += (int64_t)gridDim.x * blockDim.x)
-        dst[i] = src[i];
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x * 4;
+    for (int64_t i0 = ((int64_t)blockIdx.x * blockDim.x) * 4 + threadIdx.x; i0 < n4; i0 += stride) {
+        float4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int64_t i = i0 + (int64_t)u * blockDim.x;
+            if (i < n4) v[u] = src[i];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int64_t i = i0 + (int64_t)u * blockDim.x;
+            if (i < n4) dst[i] = v[u];
+        }
+    }
 }
 }  // namespace
 
