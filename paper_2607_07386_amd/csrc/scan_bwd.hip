@@ -231,9 +231,11 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
 
     const int lane = lane_id();
     const int wave = threadIdx.x / SDM_WAVE;
-    const int slice = blockIdx.x * (blockDim.x / SDM_WAVE) + wave;
+    const int wpb = blockDim.x / SDM_WAVE;
+    int group, stream;
+    scan_wg_coords<true>((n_slices + wpb - 1) / wpb, group, stream);
+    const int slice = group * wpb + wave;
     if (slice >= n_slices) return;
-    const int stream = blockIdx.y;
 
     BwdCtx c;
     c.L = bwd_rec_layout(W, R);
@@ -372,7 +374,7 @@ template <typename VT, int SW, int K>
 hipError_t launch_bwd_k(const ScanBwdArgs& a, const BwdPlan& p, float* part, hipStream_t st) {
     constexpr int NR = bnr_for_k<SW>(K);
     const int S = a.B * a.H;
-    dim3 grid((p.n_slices + p.wpb - 1) / p.wpb, S);
+    dim3 grid((p.n_slices + p.wpb - 1) / p.wpb * S);   // XCD-aware order: scan_wg_coords<true>
     const size_t sm = (size_t)p.lds_per_wave * p.wpb;
     auto kfn = scan_bwd_kernel<VT, SW, BPD, K, NR>;
     hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);

@@ -185,9 +185,11 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_fwd_kernel(
 
     const int lane = lane_id();
     const int wave = threadIdx.x / SDM_WAVE;
-    const int slice = blockIdx.x * (blockDim.x / SDM_WAVE) + wave;
+    const int wpb = blockDim.x / SDM_WAVE;
+    int group, stream;
+    scan_wg_coords<false>((n_slices + wpb - 1) / wpb, group, stream);
+    const int slice = group * wpb + wave;
     if (slice >= n_slices) return;
-    const int stream = blockIdx.y;
 
     FwdCtx<VT, SW, PD, K, SAVE> c;
     c.L = fwd_rec_layout(W, R);
@@ -299,7 +301,7 @@ template <typename VT, int SW, int K, bool SAVE>
 hipError_t launch_fwd_k(const ScanFwdArgs& a, const FwdPlan& p, hipStream_t st) {
     constexpr int NR = nr_for_k<SW>(K);
     const int S = a.B * a.H;
-    dim3 grid((p.n_slices + p.wpb - 1) / p.wpb, S);
+    dim3 grid((p.n_slices + p.wpb - 1) / p.wpb * S);   // order: scan_wg_coords
     const size_t sm = (size_t)p.lds_per_wave * p.wpb;
     auto kfn = scan_fwd_kernel<VT, SW, FWD_PD, K, NR, SAVE>;
     hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
