@@ -128,8 +128,9 @@ int sdm_scan_fwd(const int32_t* w_idx, const float* w_val, int W,
  *                 as for sdm_scan_fwd (workspace of
  *                 sdm_scan_fwd_workspace_bytes(B, H, T, topk, topk)).
  *   chunk         tokens per pipeline stage, rounded up to a multiple of 64
- *                 and to at most 64 stages; 0 picks T/4 for T >= 2048 and a
- *                 single stage otherwise.
+ *                 and to at most 64 stages; the first stage is a quarter of
+ *                 that (its addressing has nothing to overlap).  0 picks T/4
+ *                 for T >= 2048 and a single stage otherwise.
  * Outputs must not alias inputs or each other.  Validation as for the three
  * calls; on a HIP launch error part of the work may already be enqueued.
  * Concurrent calls on one device share its second stream, so they serialise

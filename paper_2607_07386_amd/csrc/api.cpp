@@ -338,10 +338,17 @@ int sdm_forward(const void* q, const void* k, int x_dtype, const void* cb_q, con
                              ws_bytes);
     if (rc != SDM_OK) return rc;
 
-    // pipeline stage length: a multiple of 64 tokens, at most kMaxChunks stages
-    int len = chunk > 0 ? round_up(chunk, 64) : (T >= 2048 ? round_up((T + 3) / 4, 64) : T);
-    len = std::max(len, round_up((T + kMaxChunks - 1) / kMaxChunks, 64));
-    const int nchunks = (T + len - 1) / len;
+    // pipeline stages: a short first stage (a quarter of the stage length; its
+    // addressing cannot overlap anything), then stages of len tokens; all
+    // multiples of 64 tokens, at most kMaxChunks of them
+    int len = T, first = T, nchunks = 1;
+    if (chunk > 0 || T >= 2048) {
+        len = chunk > 0 ? round_up(chunk, 64) : round_up((T + 3) / 4, 64);
+        len = std::max(len, round_up((T + kMaxChunks - 2) / (kMaxChunks - 1), 64));
+        first = std::min(T, round_up(std::max(len / 4, 64), 64));
+        nchunks = first >= T ? 1 : 1 + (T - first + len - 1) / len;
+    }
+    auto stage_begin = [&](int c) { return c == 0 ? 0 : std::min(T, first + (c - 1) * len); };
 
     hipStream_t st = (hipStream_t)stream;
     hipError_t e = sdm_launch_zero_words(workspace, 4, st);
@@ -405,7 +412,7 @@ int sdm_forward(const void* q, const void* k, int x_dtype, const void* cb_q, con
     if ((e = hipEventRecord(ev[0], st)) != hipSuccess) return hip_fail(e, "sdm_forward record");
     if ((e = hipStreamWaitEvent(side, ev[0], 0)) != hipSuccess) return hip_fail(e, "sdm_forward wait");
     for (int c = 0; c < nchunks; ++c) {
-        const int tb = c * len, te = std::min(T, tb + len);
+        const int tb = stage_begin(c), te = stage_begin(c + 1) > tb ? stage_begin(c + 1) : T;
         if ((e = stage_front(tb, te, side)) != hipSuccess) return hip_fail(e, "sdm_forward launch");
         if ((e = hipEventRecord(ev[c + 1], side)) != hipSuccess) return hip_fail(e, "sdm_forward record");
         if ((e = hipStreamWaitEvent(st, ev[c + 1], 0)) != hipSuccess) return hip_fail(e, "sdm_forward wait");
