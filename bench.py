@@ -119,8 +119,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-streams", type=int, default=16)
     ap.add_argument("--cpu-tokens", type=int, default=4096)
-    ap.add_argument("--only", choices=["fwd", "train"], default=None,
+    ap.add_argument("--only", choices=["fwd", "train", "init", "decode"], default=None,
                     help="run one leg only (profiling runs)")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the memory-initialisation and decode legs")
     ap.add_argument("--chunk", type=int, default=0,
                     help="tokens per pipeline stage of the forward step (0: the library's choice)")
     ap.add_argument("--calib", action="store_true",
@@ -191,12 +193,16 @@ def main():
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         log(f"timing {args.steps} steps")
         torch.cuda.synchronize()
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
         e0.record(stream)
-        for _ in range(args.steps):
+        evs[0].record(stream)
+        for i in range(args.steps):
             step()
+            evs[i + 1].record(stream)
         e1.record(stream)
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / args.steps
+        per_step = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
         kern = {name: sdm.profile_read(name) for name in ("address", "fwd_prep", "fwd_scan")}
         sdm.profile_enable(False)
         # reference: the same work as three separate calls on one stream (not the reported value)
@@ -234,6 +240,8 @@ def main():
                        "topk": w.topk, "inputs": "bf16", "state": "f32", "parallelism": "none (1 GPU)",
                        "pipeline": f"sdm_forward: addressing of chunk c+1 overlaps the scan of chunk c, "
                                    f"{round(args.steps * T / scan_launches)}-token chunks"},
+            "ms_per_step_median": round(per_step[len(per_step) // 2], 4),
+            "ms_per_step_min": round(per_step[0], 4),
             "ms_per_step_sequential": round(ms_seq, 4),
             "kernels_ms": {n: round(v[0] / max(v[1], 1), 4) for n, v in kern.items()},
             "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
@@ -298,6 +306,65 @@ def main():
                         "(dq, dk, dv, dalpha, dbeta, dM0)",
             "kernels_ms": {n: round(v[0] / max(v[1], 1), 4) for n, v in kern.items()},
         }
+    extra = not args.no_extra
+    # ------------------------------------------------------------ memory initialisation (a9)
+    if (extra and args.only is None) or args.only == "init":
+        w3 = synth.WORKLOADS[3]
+        log("timing the learned-M0 broadcast of the learned-M0 workload")
+        m0 = torch.zeros((w3.H, w3.N, w3.d_v), dtype=torch.float32, device=dev)
+        dst = torch.empty((w3.B, w3.H, w3.N, w3.d_v), dtype=torch.float32, device=dev)
+        sdm.mem_init(dst, m0)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(3):
+            sdm.mem_init(dst, m0)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ims = e0.elapsed_time(e1) / 3
+        moved = dst.numel() * 4 + m0.numel() * 4
+        out["mem_init"] = {
+            "workload": f"M0 [H={w3.H}, N={w3.N}, d_v={w3.d_v}] fp32 broadcast to B={w3.B} sequences",
+            "ms": round(ims, 4), "bytes_written": dst.numel() * 4, "bytes_read_unique": m0.numel() * 4,
+            "GB_s": round(moved / (ims * 1e-3) / 1e9, 1)}
+        del m0, dst
+        torch.cuda.empty_cache()
+
+    # ------------------------------------------------------------ decode steps (T = 1)
+    if (extra and args.only is None) or args.only == "decode":
+        wd = synth.Workload("decode", B=16, H=16, T=1, d_k=128, d_v=128, N=65536, topk=32, seed=5)
+        log("timing single-token decode steps")
+        ind = synth.Inputs(wd)
+        q, k, v = to_dev(ind.q), to_dev(ind.k), to_dev(ind.v)
+        al, be, cb = to_dev(ind.alpha), to_dev(ind.beta), to_dev(ind.codebook)
+        mem = torch.zeros((wd.B, wd.H, wd.N, wd.d_v), dtype=torch.float32, device=dev)
+        ws = sdm.fwd_workspace(wd.B, wd.H, 1, wd.topk, wd.topk, dev)
+        y = torch.empty((wd.B, wd.H, 1, wd.d_v), dtype=torch.float32, device=dev)
+        douts = {n: torch.empty((wd.B, wd.H, 1, wd.topk), dtype=dt, device=dev)
+                 for n, dt in (("r_idx", torch.int32), ("r_val", torch.float32),
+                               ("w_idx", torch.int32), ("w_val", torch.float32))}
+
+        def dstep():
+            sdm.forward(q, k, cb, cb, v, al, be, mem, wd.N, wd.topk, workspace=ws, y=y, out=douts)
+
+        for _ in range(5):
+            dstep()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        nd = 100
+        e0.record(stream)
+        for _ in range(nd):
+            dstep()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        dms = e0.elapsed_time(e1) / nd
+        out["decode"] = {
+            "workload": f"one token per step for B={wd.B} sequences, H={wd.H}, N={wd.N}, d={wd.d_v}, "
+                        f"top-{wd.topk}; memory resident; one sdm_forward call per step",
+            "us_per_step": round(dms * 1e3, 2), "tokens_per_s": round(wd.B / (dms * 1e-3), 1)}
+        del q, k, v, al, be, cb, mem, ws, y, douts
+        torch.cuda.empty_cache()
+
     print(json.dumps(out), flush=True)
 
 

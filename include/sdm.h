@@ -201,6 +201,7 @@ size_t sdm_scan_bwd_workspace_bytes(int B, int H, int T, int W, int R, int d_v);
  *   dst[b, h] = m0[h] for every b   (m0 != NULL)
  *   dst = 0                         (m0 == NULL)
  *   dst  out [B, H, N, d_v] fp32;  m0  [H, N, d_v] fp32 or NULL.
+ * d_v % 4 == 0, B*H <= 65535, pointers 16-B aligned.
  * ---------------------------------------------------------------------- */
 int sdm_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int d_v, void* stream);
 

@@ -503,6 +503,7 @@ int sdm_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int d_v, 
     g_err[0] = 0;
     if (B < 0 || H < 0 || N < 0 || d_v < 0) return fail(SDM_ERR_INVALID_ARG, "negative size");
     if (d_v % 4) return fail(SDM_ERR_INVALID_ARG, "d_v must be a multiple of 4");
+    if ((int64_t)B * H > kMaxStreams) return fail(SDM_ERR_UNSUPPORTED, "B*H must be <= %d", kMaxStreams);
     if (!dst || !aligned(dst, 16) || (m0 && !aligned(m0, 16)))
         return fail(SDM_ERR_INVALID_ARG, "null or misaligned pointer");
     hipError_t e;

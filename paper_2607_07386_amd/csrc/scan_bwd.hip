@@ -446,24 +446,40 @@ hipError_t sdm_launch_scan_bwd(const ScanBwdArgs& a, hipStream_t st) {
 
 // ---------------------------------------------------------------- memory init
 namespace {
-// M0 broadcast over B (m0 = [H][per_head4] float4s) or a zero fill; each thread
-// writes 4 float4s (one per 256-thread stride) per pass of the grid.
+// M0 broadcast over B (m0 = [H][per_head4] float4s) or a zero fill.  Block row
+// y is one head h (broadcast: every element is read once and written to all B
+// tables) or one (b, h) table (zero fill); each thread handles 4 float4s (one
+// per 256-thread stride) per pass.
 __global__ __launch_bounds__(256) void mem_init_kernel(float4* __restrict__ dst,
                                                        const float4* __restrict__ m0,
-                                                       int64_t per_head4, int H, int64_t total4) {
+                                                       int64_t per_head4, int B, int H) {
+    const int row = blockIdx.y;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x * 4;
-    for (int64_t i0 = ((int64_t)blockIdx.x * blockDim.x) * 4 + threadIdx.x; i0 < total4; i0 += stride) {
-        if (m0) {
+    if (m0) {
+        const float4* src = m0 + (size_t)row * per_head4;
+        for (int64_t i0 = ((int64_t)blockIdx.x * blockDim.x) * 4 + threadIdx.x; i0 < per_head4; i0 += stride) {
+            float4 v[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int64_t i = i0 + (int64_t)u * blockDim.x;
-                if (i < total4) dst[i] = m0[((i / per_head4) % H) * per_head4 + i % per_head4];
+                if (i < per_head4) v[u] = src[i];
             }
-        } else {
+            for (int b = 0; b < B; ++b) {
+                float4* d = dst + ((size_t)b * H + row) * per_head4;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int64_t i = i0 + (int64_t)u * blockDim.x;
+                    if (i < per_head4) d[i] = v[u];
+                }
+            }
+        }
+    } else {
+        float4* d = dst + (size_t)row * per_head4;
+        for (int64_t i0 = ((int64_t)blockIdx.x * blockDim.x) * 4 + threadIdx.x; i0 < per_head4; i0 += stride) {
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int64_t i = i0 + (int64_t)u * blockDim.x;
-                if (i < total4) dst[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (i < per_head4) d[i] = make_float4(0.f, 0.f, 0.f, 0.f);
             }
         }
     }
@@ -490,11 +506,13 @@ __global__ __launch_bounds__(256) void copy_kernel(float4* __restrict__ dst, con
 hipError_t sdm_launch_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int dv,
                                hipStream_t st) {
     const int64_t per_head4 = N * dv / 4;
-    const int64_t total4 = per_head4 * B * H;
-    if (total4 == 0) return hipSuccess;
-    const unsigned nb = (unsigned)std::min<int64_t>((total4 + 255) / 256, 8192);
-    hipLaunchKernelGGL(mem_init_kernel, dim3(nb), dim3(256), 0, st, reinterpret_cast<float4*>(dst),
-                       reinterpret_cast<const float4*>(m0), per_head4, H, total4);
+    const int64_t rows = m0 ? (int64_t)H : (int64_t)B * H;   // heads, or (b, h) tables
+    if (per_head4 == 0 || rows == 0 || B == 0) return hipSuccess;
+    // about 8192 blocks in all, at least one per row
+    const int64_t per_row = std::max<int64_t>(1, std::min<int64_t>((per_head4 + 1023) / 1024,
+                                                                   (8192 + rows - 1) / rows));
+    hipLaunchKernelGGL(mem_init_kernel, dim3((unsigned)per_row, (unsigned)rows), dim3(256), 0, st,
+                       reinterpret_cast<float4*>(dst), reinterpret_cast<const float4*>(m0), per_head4, B, H);
     return hipGetLastError();
 }
 

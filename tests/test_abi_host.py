@@ -117,6 +117,7 @@ def test_mem_init_validation():
     assert L.sdm_mem_init(None, None, 1, 1, 16, 4, None) == -1
     assert L.sdm_mem_init(A, None, 1, 1, 16, 6, None) == -1
     assert L.sdm_mem_init(A + 4, None, 1, 1, 16, 4, None) == -1
+    assert L.sdm_mem_init(A, None, 65536, 2, 16, 4, None) == -2
 
 
 def test_sizes():

@@ -124,6 +124,10 @@ SMALL = {
     "bf16-m0-shared": synth.Workload("t", B=3, H=2, T=120, d_k=32, d_v=32, N=1024, topk=8, seed=21, m0="shared"),
     "bf16-clustered": synth.Workload("t", B=1, H=2, T=400, d_k=64, d_v=32, N=4096, topk=16, seed=22,
                                      clustered_keys=True, n_clusters=8),
+    # the paper's 1.4B layer (Table 1): H = 2, sqrt(N) = 240 (not a power of two), d_v = 960,
+    # W = R = 64, direct-mode addressing (d_k = 2 sqrt(N))
+    "paper-1.4b-layer": synth.Workload("t", B=1, H=2, T=130, d_k=480, d_v=960, N=57600, topk=64,
+                                       seed=23, codebook=False),
 }
 
 
@@ -278,6 +282,8 @@ BWD = {
                                         seed=32, codebook=False, train=True),
     "bf16-m0-k32": synth.Workload("t", B=1, H=2, T=70, d_k=128, d_v=128, N=4096, topk=32, seed=33,
                                   m0="shared", train=True),
+    "paper-1.4b-layer": synth.Workload("t", B=1, H=2, T=40, d_k=480, d_v=960, N=57600, topk=64,
+                                       seed=34, codebook=False, m0="shared", train=True),
 }
 
 
