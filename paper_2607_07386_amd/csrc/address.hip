@@ -217,64 +217,6 @@ __device__ __forceinline__ bool topk_sorted(const uint64_t (&key)[E], int ne, in
     return true;
 }
 
-// Stage-1 selection of one half: top-k of s sub-scores, ranked (score desc,
-// id asc) into out[0 .. k).
-template <int E>
-__device__ void half_topk_bisect(const float* sc_row, int s, int k, Entry* scratch, Entry* out) {
-    const int lane = lane_id();
-    uint32_t key[E];
-    float sc[E];
-    int id[E];
-    bool sel[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const int g = e * SDM_WAVE + lane;
-        const bool ok = g < s;
-        sc[e] = ok ? sc_row[g] : 0.f;
-        key[e] = ok ? ord_key(sc[e]) : 0u;
-        id[e] = ok ? g : 0x7fffffff;
-    }
-    select_topk<E>(key, id, k, sel);
-    compact<E>(sel, sc, id, scratch);
-    wait_lds();
-    if (lane < k) {
-        const Entry me = scratch[lane];
-        const uint32_t mk = ord_key(me.score);
-        int rank = 0;
-        for (int j = 0; j < k; ++j) {
-            const Entry o = scratch[j];
-            const uint32_t ok = ord_key(o.score);
-            rank += (ok > mk) || (ok == mk && o.id < me.id);
-        }
-        out[rank] = me;
-    }
-    wait_lds();
-}
-
-// Stage-1 selection of one half: top-k of s sub-scores, ranked (score desc,
-// id asc) into out[0 .. k).
-template <int E>
-__device__ void half_topk(const float* sc_row, int s, int k, Entry* scratch, uint64_t* kbuf, Entry* out) {
-    const int lane = lane_id();
-    if (k <= 32) {
-        uint64_t key[E];
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-            const int g = e * SDM_WAVE + lane;
-            key[e] = g < s ? ckey(sc_row[g], (uint32_t)g) : 0ull;
-        }
-        uint64_t top;
-        if (topk_sorted<E>(key, E, k, kbuf, top)) {
-            if (lane < k) out[lane] = Entry{ckey_score(top), ckey_id(top)};
-            wait_lds();
-            __builtin_amdgcn_wave_barrier();
-            return;
-        }
-    }
-    half_topk_bisect<E>(sc_row, s, k, scratch, out);
-}
-
-// ---- fast path (k <= 32, s <= 256) ------------------------------------
 // Descending bitonic sort of one 64-bit key per lane, held as (hi, lo).  One
 // 64-bit compare per stage decides for both partners: the lane keeping the
 // larger key takes the other's when it is larger, the other lane when it is
@@ -304,6 +246,60 @@ __device__ __forceinline__ void bsort_asc_pay(uint32_t& key, float& pay, int lan
     else if constexpr (KK < NMAX) bsort_asc_pay<KK * 2, KK, NMAX>(key, pay, lane);
 }
 
+// Stage-1 selection of one half: top-k of s sub-scores, ranked (score desc,
+// id asc) into out[0 .. k).
+template <int E>
+__device__ void half_topk_bisect(const float* sc_row, int s, int k, Entry* scratch, Entry* out) {
+    const int lane = lane_id();
+    uint32_t key[E];
+    float sc[E];
+    int id[E];
+    bool sel[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int g = e * SDM_WAVE + lane;
+        const bool ok = g < s;
+        sc[e] = ok ? sc_row[g] : 0.f;
+        key[e] = ok ? ord_key(sc[e]) : 0u;
+        id[e] = ok ? g : 0x7fffffff;
+    }
+    select_topk<E>(key, id, k, sel);
+    compact<E>(sel, sc, id, scratch);
+    wait_lds();
+    __builtin_amdgcn_wave_barrier();
+    // rank the k selected (k <= 64) with one bitonic sort of (score key, inverted id)
+    const Entry me = scratch[min(lane, k - 1)];
+    uint32_t th = lane < k ? ord_key(me.score) : 0u;
+    uint32_t tl = ~(uint32_t)me.id;
+    bsort_desc64<2, 1, SDM_WAVE>(th, tl, lane);
+    if (lane < k) out[lane] = Entry{key_to_float(th), (int)~tl};
+    wait_lds();
+}
+
+// Stage-1 selection of one half: top-k of s sub-scores, ranked (score desc,
+// id asc) into out[0 .. k).
+template <int E>
+__device__ void half_topk(const float* sc_row, int s, int k, Entry* scratch, uint64_t* kbuf, Entry* out) {
+    const int lane = lane_id();
+    if (k <= 32) {
+        uint64_t key[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int g = e * SDM_WAVE + lane;
+            key[e] = g < s ? ckey(sc_row[g], (uint32_t)g) : 0ull;
+        }
+        uint64_t top;
+        if (topk_sorted<E>(key, E, k, kbuf, top)) {
+            if (lane < k) out[lane] = Entry{ckey_score(top), ckey_id(top)};
+            wait_lds();
+            __builtin_amdgcn_wave_barrier();
+            return;
+        }
+    }
+    half_topk_bisect<E>(sc_row, s, k, scratch, out);
+}
+
+// ---- fast path (k <= 32, s <= 256) ------------------------------------
 // Candidates for the top-k (k <= 32) of E scores per lane (ids gid; -inf
 // pads): the k-th largest per-lane maximum, found by bisection on order keys
 // with wave ballots, is reached by at least k scores, and those are gathered
