@@ -4,14 +4,18 @@
 One step = one pass of the layer's sparse path over one batch of synthetic
 input of the 1.4B-shaped workload (B=8, H=16, T=4096, d_k=d_v=128,
 N=65536 slots per head, top-32 reads and writes, bf16 inputs, fp32 memory):
-addressing of the read queries and of the write keys, then the forward scan.
-The memory table stays resident in HBM and carries from one step to the next
-(the state-carry property: each step is a further 4096 tokens of every
-stream; the work per step does not depend on the table's contents).
+addressing of the read queries and of the write keys, then the forward scan,
+as one sdm_forward call (addressing of the next chunk of tokens overlaps the
+scan of the current one; steps do not overlap each other).  The same work as
+three separate calls is timed too (`ms_per_step_sequential`).  The memory
+table stays resident in HBM and carries from one step to the next (the
+state-carry property: each step is a further 4096 tokens of every stream; the
+work per step does not depend on the table's contents).
 
-A second measurement times the training step (forward with the undo log +
-backward with addressing gradients) on the training workload (B=4, H=16,
-T=4096), reported under "train".
+Further legs: the training step (forward with the undo log + backward with
+addressing gradients) on the training workload (B=4, H=16, T=4096) under
+"train"; the learned-M0 broadcast of the learned-M0 workload under
+"mem_init"; single-token decode steps under "decode".
 
 Printed: one JSON line.  `value` is forward tokens/s (B*T positions, all
 heads) over the timed steps; `roofline` gives the forward scan kernel's
