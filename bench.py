@@ -125,6 +125,8 @@ def main():
     ap.add_argument("--cpu-tokens", type=int, default=4096)
     ap.add_argument("--only", choices=["fwd", "train", "init", "decode"], default=None,
                     help="run one leg only (profiling runs)")
+    ap.add_argument("--no-sequential", action="store_true",
+                    help="skip the reference timing of the forward step as three separate calls")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the memory-initialisation and decode legs")
     ap.add_argument("--chunk", type=int, default=0,
@@ -210,12 +212,18 @@ def main():
         kern = {name: sdm.profile_read(name) for name in ("address", "fwd_prep", "fwd_scan")}
         sdm.profile_enable(False)
         # reference: the same work as three separate calls on one stream (not the reported value)
-        e0.record(stream)
-        for _ in range(3):
-            step_sequential()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ms_seq = e0.elapsed_time(e1) / 3
+        ms_seq = seq_scan_ms = None
+        if not args.no_sequential:
+            sdm.profile_enable(True)
+            e0.record(stream)
+            for _ in range(3):
+                step_sequential()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms_seq = round(e0.elapsed_time(e1) / 3, 4)
+            t_scan, n_scan = sdm.profile_read("fwd_scan")
+            sdm.profile_enable(False)
+            seq_scan_ms = t_scan / max(n_scan, 1)
         tokens = B * T
         scan_launches = max(kern["fwd_scan"][1], 1)
         scan_ms = kern["fwd_scan"][0] / scan_launches
@@ -246,14 +254,19 @@ def main():
                                    f"{round(args.steps * T / scan_launches)}-token chunks"},
             "ms_per_step_median": round(per_step[len(per_step) // 2], 4),
             "ms_per_step_min": round(per_step[0], 4),
-            "ms_per_step_sequential": round(ms_seq, 4),
+            "ms_per_step_sequential": ms_seq,
             "kernels_ms": {n: round(v[0] / max(v[1], 1), 4) for n, v in kern.items()},
             "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                          "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                          "kernel": "scan_fwd_kernel", "algorithmic_bytes_per_token_head": unit_bytes,
                          "algorithmic_bytes_per_launch": launch_bytes, "kernel_ms": round(scan_ms, 4),
                          "unique_row_bytes_per_launch": round(uniq_launch),
-                         "frac_unique_rows": round(uniq_launch / (scan_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+                         "frac_unique_rows": round(uniq_launch / (scan_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                         # the same kernel over all 4096 tokens with nothing running beside it
+                         # (the sequential reference above)
+                         "standalone_kernel_ms": None if seq_scan_ms is None else round(seq_scan_ms, 4),
+                         "frac_standalone": None if seq_scan_ms is None else round(
+                             unit_bytes * B * H * T / (seq_scan_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
         })
         if not args.no_cpu_baseline:
             log("cpu baseline (oracle)")
