@@ -20,6 +20,9 @@ CASES = {
     "f32-direct-N64": synth.Workload("t", B=1, H=3, T=333, d_k=16, d_v=8, N=64, topk=8, dtype="f32",
                                      seed=42, codebook=False),
     "bf16-k32": synth.Workload("t", B=1, H=2, T=520, d_k=128, d_v=128, N=4096, topk=32, seed=43),
+    # 128 streams: an overlapped stage has more 16-token tiles than the capped addressing grid
+    # has workgroups, so workgroups take several tiles
+    "bf16-128-streams": synth.Workload("t", B=8, H=16, T=320, d_k=64, d_v=32, N=1024, topk=8, seed=44),
 }
 
 
