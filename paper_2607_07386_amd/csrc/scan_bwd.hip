@@ -300,6 +300,263 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
     }
 }
 
+// ---------------------------------------------------------------------------
+// Line-cooperative variant (8-column slices, W = R = 32, d_v a multiple of 32).
+//
+// The four waves of a workgroup are four consecutive 8-column slices of one
+// stream, i.e. 32 columns: one 128-byte line of every table row.  With each
+// wave moving only its own 32 bytes of a row, the 16 slices of a stream touch
+// the 4 lines of a row at different times, and the memory system then serves
+// the scattered rows at about 3.9 TB/s; moving whole lines it serves the same
+// bytes at about 5 TB/s.  So global table loads and stores go through LDS:
+// each wave loads (and stores) 8 of the 32 rows of a token as whole lines,
+// and the pieces a wave computes on are exchanged through LDS, with two
+// workgroup barriers per token.  The recurrence itself (links, rings, per-token
+// arithmetic) is the same as in scan_bwd_kernel, per wave and per slice.
+//
+// Per token t (B1, B2 are workgroup barriers):
+//   S1  this wave's line rows of token t (loaded earlier) -> LDS row buffer
+//   B1
+//   S2  each wave reads its pieces, runs the token, writes its output pieces
+//       (G rows read, G rows written, undo M rows) to the LDS staging buffer
+//   B2
+//   S3  each wave stores 8 staged rows of each output as whole lines
+//   S4  line loads of token t - PD + 1
+// A load issued in S4 sees the stores of tokens >= t + 1 (every wave stored
+// those before B1), and the tokens t .. t - PD + 2 that it does not see are
+// exactly the PD - 1 tokens the prep kernel links to the LDS rings, as in
+// the per-wave kernel (whose loads for t - PD follow token t's stores).
+// A read row whose slot the same token also writes must end with the write
+// adjoint: the write pass marks such rows (a d = 0 link into the read part)
+// and S3 skips their read-adjoint store.
+constexpr int LW = 4;          // waves (slices) per workgroup
+constexpr int LROWB = 160;     // LDS bytes per staged row: 128 + 32 of padding, so that
+                               // the per-slice piece reads (stride of one row) hit distinct banks
+constexpr int LROWS = 32;      // rows per token (W = R)
+constexpr int LFLAGS = LROWS + SDM_WAVE;   // read-row marks, then one dummy entry per lane
+constexpr int line_shared_bytes() { return (4 + 3) * LROWS * LROWB + LFLAGS * 4; }
+
+struct LineBuf {
+    v4f Mr, Gr, Gw, Ps;   // line layout: row 8 w + lane / 8, columns 4 (lane % 8) of the 32
+    v4f Dy;               // piece layout: this lane's 4 columns of dy
+};
+
+__device__ __forceinline__ v4f lds4(const unsigned char* base, int a, int r, int q) {
+    return *reinterpret_cast<const v4f*>(base + (a * LROWS + r) * LROWB + q * 16);
+}
+__device__ __forceinline__ void lds4_st(unsigned char* base, int a, int r, int q, v4f v) {
+    *reinterpret_cast<v4f*>(base + (a * LROWS + r) * LROWB + q * 16) = v;
+}
+
+// One token on the pieces (row rg, columns 4 cq.. of slice w) read from the
+// row buffer; outputs to the staging buffer and the per-wave rings.
+template <typename VT, int PD, int NS>
+__device__ __forceinline__ void bwd_token_line(const BwdCtx& c, const unsigned char* lb, unsigned char* sb,
+                                               int* flags, v4f yb, int t, int w, int lane) {
+    constexpr int SW = 8;
+    constexpr int VB = SW * (int)sizeof(VT);
+    const BwdRec& L = c.L;
+    const int RW = 2 * LROWS;
+    const int m = c.rg;                 // read row and write row of this lane (W = R = 32)
+    const int q = 2 * w + c.cq;         // this lane's column quad within the line
+    const unsigned char* rec = c.rring + (t & (NS - 1)) * L.bytes;
+    const float al = reinterpret_cast<const float*>(rec + L.off_ab)[0];
+    const float be = reinterpret_cast<const float*>(rec + L.off_ab)[1];
+    float* prow = c.spart + (size_t)t * (RW + 2);
+    float* gring_t = c.gring + (size_t)((t & (PD - 1)) * RW) * SW + c.cq * 4;
+
+    // ---- read adjoint: rbar_m = <dy, M_t[j_m]>, G[j_m] += rho_m dy ----
+    const int l1 = reinterpret_cast<const short*>(rec + L.off_lm)[m];
+    const int i1 = l1 >= 0 ? (((t + (l1 >> 8)) & (PD - 1)) * LROWS + min(l1 & 255, LROWS - 1)) : 0;
+    const v4f Mv = v4sel(l1 >= 0, ld4(c.pring + i1 * SW + c.cq * 4), lds4(lb, 0, m, q));
+    float rb = v4dot(yb, Mv);
+    rb += xor_lane_f(rb, 1);
+    if (c.cq == 0) prow[m] = rb;
+    const int l2 = reinterpret_cast<const short*>(rec + L.off_lgr)[m];
+    const int i2 = l2 >= 0 ? (((t + (l2 >> 8)) & (PD - 1)) * RW + min(l2 & 255, RW - 1)) : 0;
+    v4f g = v4sel(l2 >= 0, ld4(c.gring + i2 * SW + c.cq * 4), lds4(lb, 1, m, q));
+    g = v4fma(reinterpret_cast<const float*>(rec + L.off_rval)[m], yb, g);
+    st4(gring_t + m * SW, g);
+    lds4_st(sb, 0, m, q, g);
+
+    // ---- write adjoint ----
+    const int lw = reinterpret_cast<const short*>(rec + L.off_lgw)[m];
+    const int ig = lw >= 0 ? (((t + (lw >> 8)) & (PD - 1)) * RW + min(lw & 255, RW - 1)) : 0;
+    const v4f gn = v4sel(lw >= 0, ld4(c.gring + ig * SW + c.cq * 4), lds4(lb, 2, m, q));
+    const v4f Ps = lds4(lb, 3, m, q);
+    const v4f D = al * Ps;
+    const float kap = reinterpret_cast<const float*>(rec + L.off_wval)[m];
+    v4f up = kap * D, ebp = kap * gn;
+#pragma unroll
+    for (int s = 2; s < SDM_WAVE; s <<= 1) {
+        up += v4shfl_xor(up, s);
+        ebp += v4shfl_xor(ebp, s);
+    }
+    const v4f vv = ld4v(reinterpret_cast<const VT*>(c.vring + (t & (NS - 1)) * VB) + c.cq * 4);
+    const v4f vmu = vv - up;
+    const v4f e = be * vmu;
+    if (c.rg == 0) st4(c.sdv + (size_t)t * c.dv, be * ebp);
+    float bb = v4dot(ebp, vmu);
+    float kb = v4dot(gn, e) - be * v4dot(ebp, D);
+    kb += xor_lane_f(kb, 1);
+    if (c.cq == 0) prow[LROWS + m] = kb;
+    const v4f Db = v4fma(-be * kap, ebp, gn);
+    float ab = v4dot(Db, Ps);
+    const v4f gnew = al * Db;
+    st4(gring_t + (LROWS + m) * SW, gnew);
+    st4(c.pring + ((t & (PD - 1)) * LROWS + m) * SW + c.cq * 4, Ps);
+    lds4_st(sb, 1, m, q, gnew);
+    lds4_st(sb, 2, m, q, Ps);
+    // a d = 0 link into the read part: this token also reads the slot it writes
+    const bool same = lw >= 0 && (lw >> 8) == 0 && (lw & 255) < LROWS;
+    flags[same ? (lw & 255) : LROWS + lane] = t;
+    bb += xor_lane_f(bb, 1);
+    ab = wave_sum(ab);
+    if (lane == 0) {
+        prow[RW] = bb;
+        prow[RW + 1] = ab;
+    }
+}
+
+// Slot ids (this lane's line row) of token u's read row and written row.
+__device__ __forceinline__ int2 line_slots(const BwdCtx& c, int u, int rl, int NS) {
+    const unsigned char* rec = c.rring + (u & (NS - 1)) * c.L.bytes;
+    return make_int2(reinterpret_cast<const int*>(rec + c.L.off_rslot)[rl], reinterpret_cast<const int*>(rec)[rl]);
+}
+
+struct LinePtrs {
+    float* mt;          // memory table of the stream, at this lane's line columns
+    float* gt;          // adjoint table, same
+    const float* sv;    // saved rows of the stream, same
+    int rl;             // this lane's line row (0..31)
+    int lq;             // this lane's column quad within the line
+};
+
+__device__ __forceinline__ void line_issue(LineBuf& b, const BwdCtx& c, const LinePtrs& p, int2 sl, int u) {
+    b.Mr = ld4(p.mt + (size_t)sl.x * c.dv);
+    b.Gr = ld4(p.gt + (size_t)sl.x * c.dv);
+    b.Gw = ld4(p.gt + (size_t)sl.y * c.dv);
+    b.Ps = ld4(p.sv + ((size_t)u * LROWS + p.rl) * c.dv);
+    b.Dy = ld4(c.sdy + (size_t)u * c.dv);
+}
+
+template <typename VT, int PD, int NS>
+__device__ __forceinline__ void line_step(const BwdCtx& c, const LinePtrs& p, unsigned char* lb,
+                                          unsigned char* sb, int* flags, const LineBuf& cur, LineBuf& nxt,
+                                          int t, int w, int lane, bool issue) {
+    const int u = max(t - PD + 1, 0);
+    const int2 st_sl = line_slots(c, t, p.rl, NS);
+    const int2 ld_sl = line_slots(c, u, p.rl, NS);
+    lds4_st(lb, 0, p.rl, p.lq, cur.Mr);
+    lds4_st(lb, 1, p.rl, p.lq, cur.Gr);
+    lds4_st(lb, 2, p.rl, p.lq, cur.Gw);
+    lds4_st(lb, 3, p.rl, p.lq, cur.Ps);
+    __syncthreads();
+    bwd_token_line<VT, PD, NS>(c, lb, sb, flags, cur.Dy, t, w, lane);
+    __syncthreads();
+    if (flags[p.rl] != t) st4(p.gt + (size_t)st_sl.x * c.dv, lds4(sb, 0, p.rl, p.lq));
+    st4(p.gt + (size_t)st_sl.y * c.dv, lds4(sb, 1, p.rl, p.lq));
+    st4(p.mt + (size_t)st_sl.y * c.dv, lds4(sb, 2, p.rl, p.lq));
+    if (issue) line_issue(nxt, c, p, ld_sl, u);
+}
+
+template <typename VT, int PD, int NR>
+__global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
+    const unsigned char* __restrict__ recs, const VT* __restrict__ v, float* __restrict__ mem,
+    const float* __restrict__ saved, const float* __restrict__ dy, float* __restrict__ Gtab,
+    float* __restrict__ dv_out, float* __restrict__ part, int T, int dv, int64_t N, int n_slices, int S,
+    int lds_per_wave) {
+    constexpr int SW = 8;
+    constexpr int LEAD = bstage_lead<PD>();
+    constexpr int NS = bstage_slots<PD>();
+    constexpr int VB = SW * (int)sizeof(VT);
+    static_assert(PD % G == 0, "prefetch depth must be a multiple of the staging block");
+    static_assert(NS >= LEAD && NS >= PD, "record ring too small");
+
+    const int lane = lane_id();
+    const int w = threadIdx.x / SDM_WAVE;
+    int group, stream;
+    scan_wg_coords<true>(n_slices / LW, group, stream);
+    const int slice = group * LW + w;   // n_slices is a multiple of LW: every wave exists
+
+    BwdCtx c;
+    c.L = bwd_rec_layout(LROWS, LROWS);
+    c.dv = dv;
+    c.W = LROWS;
+    c.R = LROWS;
+    c.rg = lane / 2;
+    c.cq = lane % 2;
+    c.colok = true;
+    const int col = slice * SW + c.cq * 4;
+
+    extern __shared__ __align__(16) unsigned char smem[];
+    unsigned char* rring = smem + (size_t)w * lds_per_wave;
+    unsigned char* vring = rring + NS * c.L.bytes;
+    c.rring = rring;
+    c.vring = vring;
+    c.gring = reinterpret_cast<float*>(vring + NS * VB);
+    c.pring = c.gring + PD * 2 * LROWS * SW;
+    c.mtab = mem + (size_t)stream * N * dv + col;
+    c.gtab = Gtab + (size_t)stream * N * dv + col;
+    c.ssaved = saved + (size_t)stream * T * LROWS * dv + col;
+    c.sdy = dy + (size_t)stream * T * dv + col;
+    c.sdv = dv_out + (size_t)stream * T * dv + col;
+    c.spart = part + ((size_t)slice * S + stream) * T * (2 * LROWS + 2);
+    unsigned char* lb = smem + (size_t)LW * lds_per_wave;
+    unsigned char* sb = lb + 4 * LROWS * LROWB;
+    int* flags = reinterpret_cast<int*>(sb + 3 * LROWS * LROWB);
+
+    LinePtrs p;
+    p.rl = 8 * w + lane / 8;
+    p.lq = lane % 8;
+    const size_t lcol = (size_t)group * 32 + p.lq * 4;
+    p.mt = mem + (size_t)stream * N * dv + lcol;
+    p.gt = Gtab + (size_t)stream * N * dv + lcol;
+    p.sv = saved + (size_t)stream * T * LROWS * dv + lcol;
+
+    if (w == 0)
+        for (int i = lane; i < LFLAGS; i += SDM_WAVE) flags[i] = -1;
+
+    const unsigned char* srec = recs + (size_t)stream * T * c.L.bytes;
+    const VT* sv = v + (size_t)stream * T * dv + slice * SW;
+    u4v st[NR];
+    u2v stv;
+    LineBuf buf[PD];
+
+    const int T1 = T - 1;
+    for (int i0 = 0; i0 < LEAD - G; i0 += G) {
+        bstage_load<VT, SW, NR>(st, stv, srec, sv, T1 - i0, dv, slice, c.L.bytes, lane);
+        bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, T1 - i0, c.L.bytes, lane);
+    }
+    bstage_load<VT, SW, NR>(st, stv, srec, sv, T1 - (LEAD - G), dv, slice, c.L.bytes, lane);
+#pragma unroll
+    for (int j = 0; j < PD - 1; ++j) {
+        const int u = max(T1 - j, 0);
+        line_issue(buf[j], c, p, line_slots(c, u, p.rl, NS), u);
+    }
+    __syncthreads();   // flags initialised
+
+    // Token t = T-1-i uses buf[i % PD]; step i loads token t - PD + 1 into
+    // buf[(i + PD - 1) % PD], the buffer token t + 1 used.
+    const int Tfull = T - T % PD;
+    for (int i0 = 0; i0 < Tfull; i0 += PD) {
+#pragma unroll
+        for (int j = 0; j < PD; ++j) {
+            const int t = T1 - (i0 + j);
+            if (j % G == 0) {
+                bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, t - (LEAD - G), c.L.bytes, lane);
+                bstage_load<VT, SW, NR>(st, stv, srec, sv, t - LEAD, dv, slice, c.L.bytes, lane);
+            }
+            line_step<VT, PD, NS>(c, p, lb, sb, flags, buf[j], buf[(j + PD - 1) % PD], t, w, lane, true);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < PD; ++j) {
+        const int i = Tfull + j;
+        if (i < T) line_step<VT, PD, NS>(c, p, lb, sb, flags, buf[j], buf[(j + PD - 1) % PD], T1 - i, w, lane, false);
+    }
+}
+
 // Sum the per-slice partial scalars: rbar -> dr_val, kbar -> dw_val, dbeta, dalpha.
 __global__ __launch_bounds__(256) void bwd_reduce_kernel(const float* __restrict__ part, int n_slices,
                                                          int64_t ST, int W, int R,
@@ -370,12 +627,31 @@ bool bwd_plan(int S, int W, int R, int dv, int in_dtype, BwdPlan* p) {
     return bwd_plan_sw<BSW_MIN>(W, R, dv, in_dtype, p);
 }
 
+// The line-cooperative kernel's shape: 8-column slices, W = R = 32, d_v a
+// multiple of 32 (whole lines per workgroup), and its LDS within the limit.
+bool line_io_ok(const ScanBwdArgs& a, const BwdPlan& p) {
+    return sdm_bwd_line_enabled() && p.SW == 8 && p.K == 1 && a.W == LROWS && a.R == LROWS && a.dv % 32 == 0 &&
+           p.n_slices % LW == 0 && (size_t)p.lds_per_wave * LW + line_shared_bytes() <= (size_t)LDS_LIMIT;
+}
+
 template <typename VT, int SW, int K>
 hipError_t launch_bwd_k(const ScanBwdArgs& a, const BwdPlan& p, float* part, hipStream_t st) {
     constexpr int NR = bnr_for_k<SW>(K);
     const int S = a.B * a.H;
     dim3 grid((p.n_slices + p.wpb - 1) / p.wpb * S);   // XCD-aware order: scan_wg_coords<true>
     const size_t sm = (size_t)p.lds_per_wave * p.wpb;
+    if constexpr (SW == 8 && K == 1) {
+        if (line_io_ok(a, p)) {
+            auto kl = scan_bwd_line_kernel<VT, BPD, NR>;
+            const size_t sml = (size_t)p.lds_per_wave * LW + line_shared_bytes();
+            hipError_t e = hipFuncSetAttribute((const void*)kl, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sml);
+            if (e != hipSuccess) return e;
+            hipLaunchKernelGGL(kl, dim3(p.n_slices / LW * S), dim3(LW * SDM_WAVE), sml, st, a.ws + SDM_WS_HEADER,
+                               static_cast<const VT*>(a.v), a.mem, a.saved, a.dy, a.G, a.dv_out, part, a.T,
+                               a.dv, a.N, p.n_slices, S, p.lds_per_wave);
+            return hipGetLastError();
+        }
+    }
     auto kfn = scan_bwd_kernel<VT, SW, BPD, K, NR>;
     hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
     if (e != hipSuccess) return e;

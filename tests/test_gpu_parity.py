@@ -346,6 +346,47 @@ def test_backward_chunk_invariance():
             assert np.array_equal(o[k], outs[0][k]), k
 
 
+# Line-cooperative backward kernel (8-column slices, W = R = 32, d_v a multiple of 32):
+# against the oracle, and against the per-wave kernel (same arithmetic per slice; the
+# compiler may contract a product into an fma differently, so to 1e-5, not bit for bit).  N = 1024 with 32
+# slots per side makes a token's read and write sets share a slot in most tokens and
+# rows recur within the prefetch window; T = 3 is shorter than the load lead.
+LINE = {
+    "bf16-line-ragged": synth.Workload("t", B=1, H=2, T=203, d_k=64, d_v=64, N=1024, topk=32, seed=41,
+                                       train=True),
+    "f32-line-direct": synth.Workload("t", B=2, H=1, T=66, d_k=64, d_v=32, N=1024, topk=32, dtype="f32",
+                                      seed=42, codebook=False, train=True),
+    "bf16-line-T3": synth.Workload("t", B=1, H=1, T=3, d_k=32, d_v=96, N=1024, topk=32, seed=43,
+                                   m0="shared", train=True),
+}
+
+
+@pytest.mark.parametrize("name", list(LINE))
+def test_backward_line_io(name):
+    w = LINE[name]
+    inp = synth.Inputs(w)
+    streams = list(range(w.B * w.H))
+    sdm.set_scan_slice_width(8)
+    try:
+        errs, g_line = run_backward_case(w, inp, streams)
+        sdm.set_bwd_line_io(False)
+        g = gpu_forward(w, inp, save=True)
+        dy = torch.from_numpy(inp.dy()).to(DEV)
+        g_wave = sdm.scan_bwd(g["w_idx"], g["w_val"], g["r_idx"], g["r_val"], g["v"], g["alpha"], g["beta"],
+                              g["mem"], g["saved"], dy, cb_q=g["cb"], cb_k=g["cb"], d_k=w.d_k, chunk=64)
+        torch.cuda.synchronize()
+    finally:
+        sdm.set_bwd_line_io(True)
+        sdm.set_scan_slice_width(0)
+    report(f"{name}/bwd-line", **errs)
+    for k, e in errs.items():
+        if k != "mem_restored_bit_exact":
+            assert e <= tol_for(w), (k, e)
+    assert errs["mem_restored_bit_exact"]
+    for k in g_line:
+        assert rel_err(np_(g_line[k]), np_(g_wave[k]).astype(np.float64)) <= 1e-5, k
+
+
 # ------------------------------------------------- full-size workloads, sampled streams
 def _full(cfg, streams_of):
     w = synth.WORKLOADS[cfg]
