@@ -18,6 +18,7 @@
 
 #include "sdm_common.h"
 #include "sdm_internal.h"
+#include "sdm_reduce.h"
 #include "sdm.h"
 
 namespace {
@@ -317,18 +318,18 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
 // Per token t (B1, B2 are workgroup barriers):
 //   S1  this wave's line rows of token t (loaded earlier) -> LDS row buffer
 //   B1
-//   S2  each wave reads its pieces, runs the token, writes its output pieces
+//   S2  line loads of token t - PD + 1
+//   S3  each wave reads its pieces, runs the token, writes its output pieces
 //       (G rows read, G rows written, undo M rows) to the LDS staging buffer
 //   B2
-//   S3  each wave stores 8 staged rows of each output as whole lines
-//   S4  line loads of token t - PD + 1
-// A load issued in S4 sees the stores of tokens >= t + 1 (every wave stored
+//   S4  each wave stores 8 staged rows of each output as whole lines
+// A load issued in S2 sees the stores of tokens >= t + 1 (every wave stored
 // those before B1), and the tokens t .. t - PD + 2 that it does not see are
 // exactly the PD - 1 tokens the prep kernel links to the LDS rings, as in
 // the per-wave kernel (whose loads for t - PD follow token t's stores).
 // A read row whose slot the same token also writes must end with the write
 // adjoint: the write pass marks such rows (a d = 0 link into the read part)
-// and S3 skips their read-adjoint store.
+// and S4 skips their read-adjoint store.
 constexpr int LW = 4;          // waves (slices) per workgroup
 constexpr int LROWB = 160;     // LDS bytes per staged row: 128 + 32 of padding, so that
                                // the per-slice piece reads (stride of one row) hit distinct banks
@@ -348,73 +349,80 @@ __device__ __forceinline__ void lds4_st(unsigned char* base, int a, int r, int q
     *reinterpret_cast<v4f*>(base + (a * LROWS + r) * LROWB + q * 16) = v;
 }
 
+// Record fields of one token for this lane's row, read before the token's
+// first barrier so that their LDS latency overlaps the barrier wait.
+struct LineTok {
+    float al, be, rho, kap;
+    int l1, l2, lw;   // links of M_t[j_m], G[j_m], G[i_n]
+    v4f vv;
+};
+
+template <typename VT, int NS>
+__device__ __forceinline__ void line_read_tok(LineTok& x, const BwdCtx& c, int t) {
+    constexpr int VB = 8 * (int)sizeof(VT);
+    const BwdRec& L = c.L;
+    const unsigned char* rec = c.rring + (t & (NS - 1)) * L.bytes;
+    const int m = c.rg;
+    x.al = reinterpret_cast<const float*>(rec + L.off_ab)[0];
+    x.be = reinterpret_cast<const float*>(rec + L.off_ab)[1];
+    x.rho = reinterpret_cast<const float*>(rec + L.off_rval)[m];
+    x.kap = reinterpret_cast<const float*>(rec + L.off_wval)[m];
+    x.l1 = reinterpret_cast<const short*>(rec + L.off_lm)[m];
+    x.l2 = reinterpret_cast<const short*>(rec + L.off_lgr)[m];
+    x.lw = reinterpret_cast<const short*>(rec + L.off_lgw)[m];
+    x.vv = ld4v(reinterpret_cast<const VT*>(c.vring + (t & (NS - 1)) * VB) + c.cq * 4);
+}
+
 // One token on the pieces (row rg, columns 4 cq.. of slice w) read from the
 // row buffer; outputs to the staging buffer and the per-wave rings.
-template <typename VT, int PD, int NS>
+template <int PD>
 __device__ __forceinline__ void bwd_token_line(const BwdCtx& c, const unsigned char* lb, unsigned char* sb,
-                                               int* flags, v4f yb, int t, int w, int lane) {
+                                               int* flags, const LineTok& x, v4f yb, int t, int w, int lane) {
+    using namespace sdm_reduce;
     constexpr int SW = 8;
-    constexpr int VB = SW * (int)sizeof(VT);
-    const BwdRec& L = c.L;
     const int RW = 2 * LROWS;
     const int m = c.rg;                 // read row and write row of this lane (W = R = 32)
     const int q = 2 * w + c.cq;         // this lane's column quad within the line
-    const unsigned char* rec = c.rring + (t & (NS - 1)) * L.bytes;
-    const float al = reinterpret_cast<const float*>(rec + L.off_ab)[0];
-    const float be = reinterpret_cast<const float*>(rec + L.off_ab)[1];
     float* prow = c.spart + (size_t)t * (RW + 2);
     float* gring_t = c.gring + (size_t)((t & (PD - 1)) * RW) * SW + c.cq * 4;
 
     // ---- read adjoint: rbar_m = <dy, M_t[j_m]>, G[j_m] += rho_m dy ----
-    const int l1 = reinterpret_cast<const short*>(rec + L.off_lm)[m];
-    const int i1 = l1 >= 0 ? (((t + (l1 >> 8)) & (PD - 1)) * LROWS + min(l1 & 255, LROWS - 1)) : 0;
-    const v4f Mv = v4sel(l1 >= 0, ld4(c.pring + i1 * SW + c.cq * 4), lds4(lb, 0, m, q));
-    float rb = v4dot(yb, Mv);
-    rb += xor_lane_f(rb, 1);
-    if (c.cq == 0) prow[m] = rb;
-    const int l2 = reinterpret_cast<const short*>(rec + L.off_lgr)[m];
-    const int i2 = l2 >= 0 ? (((t + (l2 >> 8)) & (PD - 1)) * RW + min(l2 & 255, RW - 1)) : 0;
-    v4f g = v4sel(l2 >= 0, ld4(c.gring + i2 * SW + c.cq * 4), lds4(lb, 1, m, q));
-    g = v4fma(reinterpret_cast<const float*>(rec + L.off_rval)[m], yb, g);
+    const int i1 = x.l1 >= 0 ? (((t + (x.l1 >> 8)) & (PD - 1)) * LROWS + min(x.l1 & 255, LROWS - 1)) : 0;
+    const v4f Mv = v4sel(x.l1 >= 0, ld4(c.pring + i1 * SW + c.cq * 4), lds4(lb, 0, m, q));
+    const float rb = add_xor<1>(v4dot(yb, Mv));
+    const int i2 = x.l2 >= 0 ? (((t + (x.l2 >> 8)) & (PD - 1)) * RW + min(x.l2 & 255, RW - 1)) : 0;
+    v4f g = v4sel(x.l2 >= 0, ld4(c.gring + i2 * SW + c.cq * 4), lds4(lb, 1, m, q));
+    g = v4fma(x.rho, yb, g);
     st4(gring_t + m * SW, g);
     lds4_st(sb, 0, m, q, g);
 
     // ---- write adjoint ----
-    const int lw = reinterpret_cast<const short*>(rec + L.off_lgw)[m];
-    const int ig = lw >= 0 ? (((t + (lw >> 8)) & (PD - 1)) * RW + min(lw & 255, RW - 1)) : 0;
-    const v4f gn = v4sel(lw >= 0, ld4(c.gring + ig * SW + c.cq * 4), lds4(lb, 2, m, q));
+    const int ig = x.lw >= 0 ? (((t + (x.lw >> 8)) & (PD - 1)) * RW + min(x.lw & 255, RW - 1)) : 0;
+    const v4f gn = v4sel(x.lw >= 0, ld4(c.gring + ig * SW + c.cq * 4), lds4(lb, 2, m, q));
     const v4f Ps = lds4(lb, 3, m, q);
-    const v4f D = al * Ps;
-    const float kap = reinterpret_cast<const float*>(rec + L.off_wval)[m];
-    v4f up = kap * D, ebp = kap * gn;
-#pragma unroll
-    for (int s = 2; s < SDM_WAVE; s <<= 1) {
-        up += v4shfl_xor(up, s);
-        ebp += v4shfl_xor(ebp, s);
-    }
-    const v4f vv = ld4v(reinterpret_cast<const VT*>(c.vring + (t & (NS - 1)) * VB) + c.cq * 4);
-    const v4f vmu = vv - up;
-    const v4f e = be * vmu;
-    if (c.rg == 0) st4(c.sdv + (size_t)t * c.dv, be * ebp);
-    float bb = v4dot(ebp, vmu);
-    float kb = v4dot(gn, e) - be * v4dot(ebp, D);
-    kb += xor_lane_f(kb, 1);
-    if (c.cq == 0) prow[LROWS + m] = kb;
-    const v4f Db = v4fma(-be * kap, ebp, gn);
-    float ab = v4dot(Db, Ps);
-    const v4f gnew = al * Db;
+    const v4f D = x.al * Ps;
+    v4f up = x.kap * D, ebp = x.kap * gn;
+    rows_allreduce8<2>(up, ebp);
+    const v4f vmu = x.vv - up;
+    const v4f e = x.be * vmu;
+    const float bb = add_xor<1>(v4dot(ebp, vmu));
+    const float kb = add_xor<1>(v4dot(gn, e) - x.be * v4dot(ebp, D));
+    const v4f Db = v4fma(-x.be * x.kap, ebp, gn);
+    const float ab = wave_sum(v4dot(Db, Ps));
+    const v4f gnew = x.al * Db;
     st4(gring_t + (LROWS + m) * SW, gnew);
     st4(c.pring + ((t & (PD - 1)) * LROWS + m) * SW + c.cq * 4, Ps);
     lds4_st(sb, 1, m, q, gnew);
     lds4_st(sb, 2, m, q, Ps);
     // a d = 0 link into the read part: this token also reads the slot it writes
-    const bool same = lw >= 0 && (lw >> 8) == 0 && (lw & 255) < LROWS;
-    flags[same ? (lw & 255) : LROWS + lane] = t;
-    bb += xor_lane_f(bb, 1);
-    ab = wave_sum(ab);
-    if (lane == 0) {
-        prow[RW] = bb;
-        prow[RW + 1] = ab;
+    const bool same = x.lw >= 0 && (x.lw >> 8) == 0 && (x.lw & 255) < LROWS;
+    flags[same ? (x.lw & 255) : LROWS + lane] = t;
+    // partial sums of this slice: the two lanes of row m hold rbar_m and kbar_m
+    // (each lane stores one); row 0 also stores dv of the token, dbeta and dalpha
+    prow[c.cq * LROWS + m] = c.cq ? kb : rb;
+    if (lane < 2) {
+        st4(c.sdv + (size_t)t * c.dv, x.be * ebp);
+        prow[RW + lane] = lane ? ab : bb;
     }
 }
 
@@ -445,6 +453,8 @@ __device__ __forceinline__ void line_step(const BwdCtx& c, const LinePtrs& p, un
                                           unsigned char* sb, int* flags, const LineBuf& cur, LineBuf& nxt,
                                           int t, int w, int lane, bool issue) {
     const int u = max(t - PD + 1, 0);
+    LineTok x;
+    line_read_tok<VT, NS>(x, c, t);
     const int2 st_sl = line_slots(c, t, p.rl, NS);
     const int2 ld_sl = line_slots(c, u, p.rl, NS);
     lds4_st(lb, 0, p.rl, p.lq, cur.Mr);
@@ -452,12 +462,13 @@ __device__ __forceinline__ void line_step(const BwdCtx& c, const LinePtrs& p, un
     lds4_st(lb, 2, p.rl, p.lq, cur.Gw);
     lds4_st(lb, 3, p.rl, p.lq, cur.Ps);
     __syncthreads();
-    bwd_token_line<VT, PD, NS>(c, lb, sb, flags, cur.Dy, t, w, lane);
+    // every wave stored token t + 1 before the barrier: the loads may go now
+    if (issue) line_issue(nxt, c, p, ld_sl, u);
+    bwd_token_line<PD>(c, lb, sb, flags, x, cur.Dy, t, w, lane);
     __syncthreads();
     if (flags[p.rl] != t) st4(p.gt + (size_t)st_sl.x * c.dv, lds4(sb, 0, p.rl, p.lq));
     st4(p.gt + (size_t)st_sl.y * c.dv, lds4(sb, 1, p.rl, p.lq));
     st4(p.mt + (size_t)st_sl.y * c.dv, lds4(sb, 2, p.rl, p.lq));
-    if (issue) line_issue(nxt, c, p, ld_sl, u);
 }
 
 template <typename VT, int PD, int NR>
