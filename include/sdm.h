@@ -219,18 +219,21 @@ int sdm_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int d_v, 
 int sdm_set_scan_slice_width(int sw);
 
 /* ------------------------------------------------------------------------
- * Backward table I/O.  With 8-column slices, W = R = 32 and d_v a multiple
- * of 32, the backward scan by default runs its four-wave line-cooperative
- * kernel: the waves of four adjacent slices (one 128-byte line of every table
- * row) move table rows between HBM and LDS as whole lines and exchange their
- * pieces in LDS.  sdm_set_bwd_line_io(0) always uses the per-wave kernel
- * (each wave moves its own 32-byte pieces), 1 restores the default.  The two
- * do the same per-slice arithmetic; results agree to rounding (the compiler
- * may fuse a product into an fma in one and not the other).
- * Process-wide; applies to launches that start after the call.  Any other
- * value returns SDM_ERR_INVALID_ARG and keeps the setting.
+ * Table I/O of the scans.  By default each scan runs a four-wave
+ * line-cooperative kernel where the shape allows it: the waves of four
+ * adjacent column slices (4 x 8 or 4 x 16 columns: one or two 128-byte lines
+ * of every table row) move table rows between HBM and LDS as whole lines and
+ * exchange their pieces in LDS.  Forward: W = R = 32 and d_v a multiple of 4
+ * times the slice width; backward: 8-column slices, W = R = 32 and d_v a
+ * multiple of 32.  sdm_set_scan_line_io(0) always uses the per-wave kernels
+ * (each wave moves its own pieces of the rows), 1 restores the default.  The
+ * two do the same arithmetic per slice; results agree to rounding (the sums
+ * over rows are taken in a different order, and the compiler may fuse a
+ * product into an fma in one and not the other).  Process-wide; applies to
+ * launches that start after the call.  Any other value returns
+ * SDM_ERR_INVALID_ARG and keeps the setting.
  * ---------------------------------------------------------------------- */
-int sdm_set_bwd_line_io(int on);
+int sdm_set_scan_line_io(int on);
 
 /* ------------------------------------------------------------------------
  * Per-kernel timing with HIP events, off by default.  While enabled, every

@@ -16,11 +16,11 @@
 
 namespace {
 std::atomic<int> g_slice_width{0};
-std::atomic<int> g_bwd_line{1};
+std::atomic<int> g_line_io{1};
 }
 
 int sdm_scan_slice_width() { return g_slice_width.load(std::memory_order_relaxed); }
-bool sdm_bwd_line_enabled() { return g_bwd_line.load(std::memory_order_relaxed) != 0; }
+bool sdm_line_io_enabled() { return g_line_io.load(std::memory_order_relaxed) != 0; }
 
 int sdm_device_simds() {
     constexpr int MAXDEV = 64;
@@ -210,11 +210,11 @@ int sdm_set_scan_slice_width(int sw) {
     return SDM_OK;
 }
 
-int sdm_set_bwd_line_io(int on) {
+int sdm_set_scan_line_io(int on) {
     g_err[0] = 0;
     if (on != 0 && on != 1)
-        return fail(SDM_ERR_INVALID_ARG, "sdm_set_bwd_line_io: expected 0 or 1, got %d", on);
-    g_bwd_line.store(on, std::memory_order_relaxed);
+        return fail(SDM_ERR_INVALID_ARG, "sdm_set_scan_line_io: expected 0 or 1, got %d", on);
+    g_line_io.store(on, std::memory_order_relaxed);
     return SDM_OK;
 }
 

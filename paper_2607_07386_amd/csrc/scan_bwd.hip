@@ -641,7 +641,7 @@ bool bwd_plan(int S, int W, int R, int dv, int in_dtype, BwdPlan* p) {
 // The line-cooperative kernel's shape: 8-column slices, W = R = 32, d_v a
 // multiple of 32 (whole lines per workgroup), and its LDS within the limit.
 bool line_io_ok(const ScanBwdArgs& a, const BwdPlan& p) {
-    return sdm_bwd_line_enabled() && p.SW == 8 && p.K == 1 && a.W == LROWS && a.R == LROWS && a.dv % 32 == 0 &&
+    return sdm_line_io_enabled() && p.SW == 8 && p.K == 1 && a.W == LROWS && a.R == LROWS && a.dv % 32 == 0 &&
            p.n_slices % LW == 0 && (size_t)p.lds_per_wave * LW + line_shared_bytes() <= (size_t)LDS_LIMIT;
 }
 

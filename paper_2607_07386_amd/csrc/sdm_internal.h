@@ -90,8 +90,8 @@ hipError_t sdm_launch_fwd_scan_range(const ScanFwdArgs& a, hipStream_t st);
 int sdm_device_simds();
 // Forced scan slice width (8 or 16), or 0 for the automatic choice.
 int sdm_scan_slice_width();
-// Whether the backward may use its line-cooperative kernel (default: yes).
-bool sdm_bwd_line_enabled();
+// Whether the scans may use their line-cooperative kernels (default: yes).
+bool sdm_line_io_enabled();
 // true if the forward scan has a launch plan for this shape (registers, LDS)
 bool sdm_fwd_plan_ok(int W, int R, int dv, int in_dtype);
 size_t sdm_fwd_ws_bytes(int B, int H, int T, int W, int R);

@@ -99,4 +99,17 @@ __device__ __forceinline__ void rows_allreduce8(v4f& a, v4f& b) {
     b = v4f{o0[2], o1[2], o0[3], o1[3]};
 }
 
+// Same for the four floats of one v4f (16 VALU instructions at CQ = 2).
+template <int CQ>
+__device__ __forceinline__ void rows_allreduce4(v4f& a) {
+    static_assert(CQ >= 1 && CQ <= 8 && (CQ & (CQ - 1)) == 0, "class count must divide a row");
+    const float y0 = detail::swap32_sum(a.x, a.z);   // halves [x | z]
+    const float y1 = detail::swap32_sum(a.y, a.w);   // halves [y | w]
+    float z = detail::swap16_sum(y0, y1);            // rows [x y z w]
+    z = row_sum_from<CQ>(z);
+    float o[4];
+    detail::rows_gather4(z, o);
+    a = v4f{o[0], o[1], o[2], o[3]};
+}
+
 }  // namespace sdm_reduce

@@ -56,7 +56,7 @@ def lib() -> ctypes.CDLL:
         L.sdm_check_device_errors.argtypes = [P, P]
         L.sdm_profile_enable.argtypes = [I]
         L.sdm_set_scan_slice_width.argtypes = [I]
-        L.sdm_set_bwd_line_io.argtypes = [I]
+        L.sdm_set_scan_line_io.argtypes = [I]
         L.sdm_profile_read.argtypes = [I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
         L.sdm_status_string.argtypes = [I]
         L.sdm_status_string.restype = ctypes.c_char_p
@@ -266,9 +266,9 @@ def set_scan_slice_width(sw: int):
     _check("sdm_set_scan_slice_width", lib().sdm_set_scan_slice_width(int(sw)))
 
 
-def set_bwd_line_io(on: bool):
-    """Backward scan: line-cooperative table I/O where the shape allows (default) or per-wave pieces."""
-    _check("sdm_set_bwd_line_io", lib().sdm_set_bwd_line_io(int(bool(on))))
+def set_scan_line_io(on: bool):
+    """Scans: line-cooperative table I/O where the shape allows (default) or per-wave pieces (process-wide)."""
+    _check("sdm_set_scan_line_io", lib().sdm_set_scan_line_io(int(bool(on))))
 
 
 def profile_enable(on: bool = True):

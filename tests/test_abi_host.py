@@ -113,13 +113,13 @@ def test_slice_width_setting():
         assert b"width" in L.sdm_last_error()
 
 
-def test_bwd_line_io_setting():
+def test_scan_line_io_setting():
     for on in (0, 1):
-        assert L.sdm_set_bwd_line_io(on) == 0
+        assert L.sdm_set_scan_line_io(on) == 0
     for on in (-1, 2, 8):
-        assert L.sdm_set_bwd_line_io(on) == -1
+        assert L.sdm_set_scan_line_io(on) == -1
         assert b"expected 0 or 1" in L.sdm_last_error()
-    assert L.sdm_set_bwd_line_io(1) == 0
+    assert L.sdm_set_scan_line_io(1) == 0
 
 
 def test_mem_init_validation():

@@ -144,6 +144,38 @@ def test_forward_small(name, slice_width):
     check_scan(w, g, o, streams, f"{name}/sw{slice_width}/scan")
 
 
+# Line-cooperative forward kernel (W = R = 32, d_v a multiple of 4 x slice width):
+# against the oracle, and against the per-wave kernel (to 1e-5: the sums over rows
+# are taken in another order), with and without the undo log.  N = 1024 with 32
+# slots makes rows recur within the prefetch window and tokens read what they write.
+FLINE = {
+    "bf16-fline-ragged": synth.Workload("t", B=1, H=2, T=203, d_k=64, d_v=128, N=1024, topk=32, seed=51),
+    "f32-fline-direct": synth.Workload("t", B=2, H=1, T=61, d_k=64, d_v=64, N=1024, topk=32, dtype="f32",
+                                       seed=52, codebook=False),
+    "bf16-fline-T5-m0": synth.Workload("t", B=2, H=1, T=5, d_k=32, d_v=64, N=1024, topk=32, seed=53,
+                                       m0="shared"),
+}
+
+
+@pytest.mark.parametrize("save", [False, True])
+@pytest.mark.parametrize("name", list(FLINE))
+def test_forward_line_io(name, save, slice_width):
+    w = FLINE[name]
+    inp = synth.Inputs(w)
+    streams = list(range(w.B * w.H))
+    g = gpu_forward(w, inp, save=save)
+    o = oracle_scan_rows(w, inp, g, streams, m0_fn(w, inp))
+    check_scan(w, g, o, streams, f"{name}/sw{slice_width}/save{int(save)}/fline")
+    sdm.set_scan_line_io(False)
+    try:
+        gw = gpu_forward(w, inp, save=save)
+    finally:
+        sdm.set_scan_line_io(True)
+    keys = ("y", "mem") + (("saved",) if save else ())
+    for k in keys:
+        assert rel_err(np_(g[k]), np_(gw[k]).astype(np.float64)) <= 1e-5, k
+
+
 def test_empty_sequence_is_noop():
     w = synth.Workload("t", B=1, H=1, T=0, d_k=32, d_v=32, N=256, topk=8)
     dev = DEV
@@ -369,14 +401,14 @@ def test_backward_line_io(name):
     sdm.set_scan_slice_width(8)
     try:
         errs, g_line = run_backward_case(w, inp, streams)
-        sdm.set_bwd_line_io(False)
+        sdm.set_scan_line_io(False)
         g = gpu_forward(w, inp, save=True)
         dy = torch.from_numpy(inp.dy()).to(DEV)
         g_wave = sdm.scan_bwd(g["w_idx"], g["w_val"], g["r_idx"], g["r_val"], g["v"], g["alpha"], g["beta"],
                               g["mem"], g["saved"], dy, cb_q=g["cb"], cb_k=g["cb"], d_k=w.d_k, chunk=64)
         torch.cuda.synchronize()
     finally:
-        sdm.set_bwd_line_io(True)
+        sdm.set_scan_line_io(True)
         sdm.set_scan_slice_width(0)
     report(f"{name}/bwd-line", **errs)
     for k, e in errs.items():
