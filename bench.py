@@ -40,7 +40,10 @@ HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fwd_scan_c1.json")
 # sources of the forward scan kernel: the traffic file holds their hash
 SCAN_SRCS = [os.path.join(ROOT, "paper_2607_07386_amd", "csrc", f)
-             for f in ("scan_fwd.hip", "sdm_common.h", "sdm_internal.h")]
+             for f in ("scan_fwd.hip", "sdm_common.h", "sdm_internal.h", "sdm_reduce.h")]
+# the forward scan kernel this workload runs (W = R = 32, d_v a multiple of 64:
+# the line-cooperative kernel, the library's default)
+SCAN_KERNEL = "scan_fwd_line_kernel"
 
 
 def scan_src_hash():
@@ -258,7 +261,7 @@ def main():
             "kernels_ms": {n: round(v[0] / max(v[1], 1), 4) for n, v in kern.items()},
             "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                          "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                         "kernel": "scan_fwd_kernel", "algorithmic_bytes_per_token_head": unit_bytes,
+                         "kernel": SCAN_KERNEL, "algorithmic_bytes_per_token_head": unit_bytes,
                          "algorithmic_bytes_per_launch": launch_bytes, "kernel_ms": round(scan_ms, 4),
                          "unique_row_bytes_per_launch": round(uniq_launch),
                          "frac_unique_rows": round(uniq_launch / (scan_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),

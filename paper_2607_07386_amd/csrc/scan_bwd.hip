@@ -335,7 +335,8 @@ constexpr int LROWB = 160;     // LDS bytes per staged row: 128 + 32 of padding,
                                // the per-slice piece reads (stride of one row) hit distinct banks
 constexpr int LROWS = 32;      // rows per token (W = R)
 constexpr int LFLAGS = LROWS + SDM_WAVE;   // read-row marks, then one dummy entry per lane
-constexpr int line_shared_bytes() { return (4 + 3) * LROWS * LROWB + LFLAGS * 4; }
+constexpr int LPART = 2 * LROWS + 2;       // per-token partial sums: rbar[32], kbar[32], dbeta, dalpha
+constexpr int line_shared_bytes() { return (4 + 3) * LROWS * LROWB + LFLAGS * 4 + LW * LPART * 4; }
 
 struct LineBuf {
     v4f Mr, Gr, Gw, Ps;   // line layout: row 8 w + lane / 8, columns 4 (lane % 8) of the 32
@@ -377,13 +378,14 @@ __device__ __forceinline__ void line_read_tok(LineTok& x, const BwdCtx& c, int t
 // row buffer; outputs to the staging buffer and the per-wave rings.
 template <int PD>
 __device__ __forceinline__ void bwd_token_line(const BwdCtx& c, const unsigned char* lb, unsigned char* sb,
-                                               int* flags, const LineTok& x, v4f yb, int t, int w, int lane) {
+                                               int* flags, float* psum, const LineTok& x, v4f yb, int t, int w,
+                                               int lane) {
     using namespace sdm_reduce;
     constexpr int SW = 8;
     const int RW = 2 * LROWS;
     const int m = c.rg;                 // read row and write row of this lane (W = R = 32)
     const int q = 2 * w + c.cq;         // this lane's column quad within the line
-    float* prow = c.spart + (size_t)t * (RW + 2);
+    float* prow = psum + w * LPART;   // this slice's partial sums of the token (LDS)
     float* gring_t = c.gring + (size_t)((t & (PD - 1)) * RW) * SW + c.cq * 4;
 
     // ---- read adjoint: rbar_m = <dy, M_t[j_m]>, G[j_m] += rho_m dy ----
@@ -418,7 +420,8 @@ __device__ __forceinline__ void bwd_token_line(const BwdCtx& c, const unsigned c
     const bool same = x.lw >= 0 && (x.lw >> 8) == 0 && (x.lw & 255) < LROWS;
     flags[same ? (x.lw & 255) : LROWS + lane] = t;
     // partial sums of this slice: the two lanes of row m hold rbar_m and kbar_m
-    // (each lane stores one); row 0 also stores dv of the token, dbeta and dalpha
+    // (each lane writes one); row 0 also writes dbeta and dalpha, and stores
+    // this slice's dv of the token
     prow[c.cq * LROWS + m] = c.cq ? kb : rb;
     if (lane < 2) {
         st4(c.sdv + (size_t)t * c.dv, x.be * ebp);
@@ -450,8 +453,8 @@ __device__ __forceinline__ void line_issue(LineBuf& b, const BwdCtx& c, const Li
 
 template <typename VT, int PD, int NS>
 __device__ __forceinline__ void line_step(const BwdCtx& c, const LinePtrs& p, unsigned char* lb,
-                                          unsigned char* sb, int* flags, const LineBuf& cur, LineBuf& nxt,
-                                          int t, int w, int lane, bool issue) {
+                                          unsigned char* sb, int* flags, float* psum, const LineBuf& cur,
+                                          LineBuf& nxt, int t, int w, int lane, bool issue) {
     const int u = max(t - PD + 1, 0);
     LineTok x;
     line_read_tok<VT, NS>(x, c, t);
@@ -464,8 +467,13 @@ __device__ __forceinline__ void line_step(const BwdCtx& c, const LinePtrs& p, un
     __syncthreads();
     // every wave stored token t + 1 before the barrier: the loads may go now
     if (issue) line_issue(nxt, c, p, ld_sl, u);
-    bwd_token_line<PD>(c, lb, sb, flags, x, cur.Dy, t, w, lane);
+    bwd_token_line<PD>(c, lb, sb, flags, psum, x, cur.Dy, t, w, lane);
     __syncthreads();
+    // the workgroup's partial sums of the token: wave w adds entries 17 w .. 17 w + 16
+    // of the four slices and stores them
+    const int pi = 17 * w + lane;
+    if (lane < 17 && pi < LPART)
+        c.spart[(size_t)t * LPART + pi] = ((psum[pi] + psum[LPART + pi]) + psum[2 * LPART + pi]) + psum[3 * LPART + pi];
     if (flags[p.rl] != t) st4(p.gt + (size_t)st_sl.x * c.dv, lds4(sb, 0, p.rl, p.lq));
     st4(p.gt + (size_t)st_sl.y * c.dv, lds4(sb, 1, p.rl, p.lq));
     st4(p.mt + (size_t)st_sl.y * c.dv, lds4(sb, 2, p.rl, p.lq));
@@ -512,10 +520,11 @@ __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
     c.ssaved = saved + (size_t)stream * T * LROWS * dv + col;
     c.sdy = dy + (size_t)stream * T * dv + col;
     c.sdv = dv_out + (size_t)stream * T * dv + col;
-    c.spart = part + ((size_t)slice * S + stream) * T * (2 * LROWS + 2);
+    c.spart = part + ((size_t)group * S + stream) * T * LPART;   // per workgroup (4 slices)
     unsigned char* lb = smem + (size_t)LW * lds_per_wave;
     unsigned char* sb = lb + 4 * LROWS * LROWB;
     int* flags = reinterpret_cast<int*>(sb + 3 * LROWS * LROWB);
+    float* psum = reinterpret_cast<float*>(flags + LFLAGS);
 
     LinePtrs p;
     p.rl = 8 * w + lane / 8;
@@ -558,18 +567,19 @@ __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
                 bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, t - (LEAD - G), c.L.bytes, lane);
                 bstage_load<VT, SW, NR>(st, stv, srec, sv, t - LEAD, dv, slice, c.L.bytes, lane);
             }
-            line_step<VT, PD, NS>(c, p, lb, sb, flags, buf[j], buf[(j + PD - 1) % PD], t, w, lane, true);
+            line_step<VT, PD, NS>(c, p, lb, sb, flags, psum, buf[j], buf[(j + PD - 1) % PD], t, w, lane, true);
         }
     }
 #pragma unroll
     for (int j = 0; j < PD; ++j) {
         const int i = Tfull + j;
-        if (i < T) line_step<VT, PD, NS>(c, p, lb, sb, flags, buf[j], buf[(j + PD - 1) % PD], T1 - i, w, lane, false);
+        if (i < T) line_step<VT, PD, NS>(c, p, lb, sb, flags, psum, buf[j], buf[(j + PD - 1) % PD], T1 - i, w, lane, false);
     }
 }
 
-// Sum the per-slice partial scalars: rbar -> dr_val, kbar -> dw_val, dbeta, dalpha.
-__global__ __launch_bounds__(256) void bwd_reduce_kernel(const float* __restrict__ part, int n_slices,
+// Sum the partial scalars (one set per slice, or per workgroup of slices for the
+// line-cooperative kernel): rbar -> dr_val, kbar -> dw_val, dbeta, dalpha.
+__global__ __launch_bounds__(256) void bwd_reduce_kernel(const float* __restrict__ part, int n_parts,
                                                          int64_t ST, int W, int R,
                                                          float* __restrict__ dw_val,
                                                          float* __restrict__ dr_val,
@@ -580,7 +590,7 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(const float* __restrict
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
          i += (int64_t)gridDim.x * blockDim.x) {
         float acc = 0.f;
-        for (int s = 0; s < n_slices; ++s) acc += part[(size_t)s * total + i];
+        for (int s = 0; s < n_parts; ++s) acc += part[(size_t)s * total + i];
         const int64_t st = i / NP;
         const int p = (int)(i % NP);
         if (p < R)
@@ -645,14 +655,16 @@ bool line_io_ok(const ScanBwdArgs& a, const BwdPlan& p) {
            p.n_slices % LW == 0 && (size_t)p.lds_per_wave * LW + line_shared_bytes() <= (size_t)LDS_LIMIT;
 }
 
+// line: run the line-cooperative kernel (line_io_ok held); its partial sums
+// are per workgroup of LW slices.
 template <typename VT, int SW, int K>
-hipError_t launch_bwd_k(const ScanBwdArgs& a, const BwdPlan& p, float* part, hipStream_t st) {
+hipError_t launch_bwd_k(const ScanBwdArgs& a, const BwdPlan& p, bool line, float* part, hipStream_t st) {
     constexpr int NR = bnr_for_k<SW>(K);
     const int S = a.B * a.H;
     dim3 grid((p.n_slices + p.wpb - 1) / p.wpb * S);   // XCD-aware order: scan_wg_coords<true>
     const size_t sm = (size_t)p.lds_per_wave * p.wpb;
     if constexpr (SW == 8 && K == 1) {
-        if (line_io_ok(a, p)) {
+        if (line) {
             auto kl = scan_bwd_line_kernel<VT, BPD, NR>;
             const size_t sml = (size_t)p.lds_per_wave * LW + line_shared_bytes();
             hipError_t e = hipFuncSetAttribute((const void*)kl, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sml);
@@ -673,14 +685,14 @@ hipError_t launch_bwd_k(const ScanBwdArgs& a, const BwdPlan& p, float* part, hip
 }
 
 template <typename VT>
-hipError_t launch_bwd_kk(const ScanBwdArgs& a, const BwdPlan& p, float* part, hipStream_t st) {
+hipError_t launch_bwd_kk(const ScanBwdArgs& a, const BwdPlan& p, bool line, float* part, hipStream_t st) {
     if (p.SW == 8) {
-        if (p.K == 1) return launch_bwd_k<VT, 8, 1>(a, p, part, st);
-        return launch_bwd_k<VT, 8, 2>(a, p, part, st);
+        if (p.K == 1) return launch_bwd_k<VT, 8, 1>(a, p, line, part, st);
+        return launch_bwd_k<VT, 8, 2>(a, p, false, part, st);
     }
-    if (p.K == 1) return launch_bwd_k<VT, 16, 1>(a, p, part, st);
-    if (p.K == 2) return launch_bwd_k<VT, 16, 2>(a, p, part, st);
-    return launch_bwd_k<VT, 16, 4>(a, p, part, st);
+    if (p.K == 1) return launch_bwd_k<VT, 16, 1>(a, p, false, part, st);
+    if (p.K == 2) return launch_bwd_k<VT, 16, 2>(a, p, false, part, st);
+    return launch_bwd_k<VT, 16, 4>(a, p, false, part, st);
 }
 
 size_t bwd_part_offset(int B, int H, int T, int W, int R) {
@@ -713,20 +725,21 @@ hipError_t sdm_launch_scan_bwd(const ScanBwdArgs& a, hipStream_t st) {
         hipError_t e = sdm_launch_bwd_prep<BPD>(a, st);
         if (e != hipSuccess) return e;
     }
-    const int n_slices = plan.n_slices;
+    const bool line = line_io_ok(a, plan);
+    const int n_parts = line ? plan.n_slices / LW : plan.n_slices;   // partial sums per (stream, token)
     float* part = reinterpret_cast<float*>(a.ws + bwd_part_offset(a.B, a.H, a.T, a.W, a.R));
     hipError_t e;
     {
         SdmProfScope ps(SDM_K_BWD_SCAN, st);
-        e = a.in_dtype == SDM_DT_BF16 ? launch_bwd_kk<bf16_t>(a, plan, part, st)
-                                      : launch_bwd_kk<float>(a, plan, part, st);
+        e = a.in_dtype == SDM_DT_BF16 ? launch_bwd_kk<bf16_t>(a, plan, line, part, st)
+                                      : launch_bwd_kk<float>(a, plan, line, part, st);
     }
     if (e != hipSuccess) return e;
     SdmProfScope ps(SDM_K_BWD_REDUCE, st);
     const int64_t ST = (int64_t)S * a.T;
     const int64_t total = ST * (a.W + a.R + 2);
     const unsigned nb = (unsigned)std::min<int64_t>((total + 255) / 256, 65536);
-    hipLaunchKernelGGL(bwd_reduce_kernel, dim3(nb), dim3(256), 0, st, part, n_slices, ST, a.W, a.R,
+    hipLaunchKernelGGL(bwd_reduce_kernel, dim3(nb), dim3(256), 0, st, part, n_parts, ST, a.W, a.R,
                        a.dw_val, a.dr_val, a.dbeta, a.dalpha);
     return hipGetLastError();
 }
