@@ -182,7 +182,9 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_fwd_kernel(
     constexpr int NS = stage_slots<PD>();
     constexpr int VB = SW * (int)sizeof(VT);
     static_assert(PD % G == 0, "prefetch depth must be a multiple of the staging block");
-    static_assert(NS > LEAD && NS > PD, "record ring too small");
+    // the block staged at step t (tokens t+LEAD-G .. t+LEAD-1) reuses only slots of
+    // tokens already done, while tokens t .. t+LEAD-G-1 stay: NS >= LEAD suffices
+    static_assert(NS >= LEAD && NS >= PD, "record ring too small");
 
     const int lane = lane_id();
     const int wave = threadIdx.x / SDM_WAVE;
@@ -444,7 +446,9 @@ __global__ __launch_bounds__(FLW * SDM_WAVE) void scan_fwd_line_kernel(
     constexpr int NS = stage_slots<PD>();
     constexpr int VB = SW * (int)sizeof(VT);
     static_assert(PD % G == 0, "prefetch depth must be a multiple of the staging block");
-    static_assert(NS > LEAD && NS > PD, "record ring too small");
+    // the block staged at step t (tokens t+LEAD-G .. t+LEAD-1) reuses only slots of
+    // tokens already done, while tokens t .. t+LEAD-G-1 stay: NS >= LEAD suffices
+    static_assert(NS >= LEAD && NS >= PD, "record ring too small");
     static_assert(FLine<SW>::NLI * FLine<SW>::LRI == 8, "8 rows per wave");
 
     const int lane = lane_id();

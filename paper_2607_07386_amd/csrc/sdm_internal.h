@@ -9,7 +9,7 @@
 
 // Prefetch depth (tokens in flight per wave) of the forward and backward scans;
 // the prep kernels compute read-after-write links for exactly this window.
-#define SDM_FWD_PD 8
+#define SDM_FWD_PD 4
 #define SDM_BWD_PD 4
 
 // Per-token record of the forward scan (written by the prep kernel, staged in

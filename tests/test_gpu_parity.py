@@ -462,7 +462,7 @@ def test_full_c4_training():
 
 
 # ------------------------------------------------- prep records (read-after-write links)
-FWD_PD, BWD_PD = 8, 4
+FWD_PD, BWD_PD = 4, 4
 
 
 def _rec_fwd(W, R):
