@@ -186,6 +186,7 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_fwd_kernel(
     // tokens already done, while tokens t .. t+LEAD-G-1 stay: NS >= LEAD suffices
     static_assert(NS >= LEAD && NS >= PD, "record ring too small");
 
+    __builtin_amdgcn_s_setprio(3);   // as in scan_fwd_line_kernel
     const int lane = lane_id();
     const int wave = threadIdx.x / SDM_WAVE;
     const int wpb = blockDim.x / SDM_WAVE;
@@ -451,6 +452,10 @@ __global__ __launch_bounds__(FLW * SDM_WAVE) void scan_fwd_line_kernel(
     static_assert(NS >= LEAD && NS >= PD, "record ring too small");
     static_assert(FLine<SW>::NLI * FLine<SW>::LRI == 8, "8 rows per wave");
 
+    // In the pipelined forward the next stage's addressing and records share the
+    // CUs; the scan waves are latency-bound and go first at each issue slot
+    // (wave priority, not a queue priority), the others fill the gaps.
+    __builtin_amdgcn_s_setprio(3);
     const int lane = lane_id();
     const int w = threadIdx.x / SDM_WAVE;
     int group, stream;
