@@ -546,6 +546,46 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
         const int nks = (dh + 31) / 32;   // 32-deep steps (at most MAXKS)
         const int r16 = lane % 16, q = lane / 16;
         const int t = t0 + r16;
+        if (E <= 4 && nks <= 2) {
+            // dh <= 64, s <= 256: this wave's tiles of a half (at most E) need 2 E
+            // codebook operands; all are loaded before the first MFMA, so the half
+            // pays one load latency instead of one per tile.
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                sdm_bf16x8 a[2], b[E][2];
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) {
+                    const int kc = ks * 32 + 8 * q;
+                    a[ks] = sdm_bf16x8{};
+                    if (ks < nks && t < te && kc < dh)
+                        a[ks] = *reinterpret_cast<const sdm_bf16x8*>(xs + (size_t)t * dk + half * dh + kc);
+                }
+#pragma unroll
+                for (int i = 0; i < E; ++i) {
+                    const int j = (wave + AWAVES * i) * 16 + r16;
+                    const XT* crow = cbh + ((size_t)half * s + min(j, s - 1)) * dh;
+#pragma unroll
+                    for (int ks = 0; ks < 2; ++ks) {
+                        const int kc = ks * 32 + 8 * q;
+                        b[i][ks] = sdm_bf16x8{};
+                        if (ks < nks && j < s && kc < dh)
+                            b[i][ks] = *reinterpret_cast<const sdm_bf16x8*>(crow + kc);
+                    }
+                }
+#pragma unroll
+                for (int i = 0; i < E; ++i) {
+                    const int j = (wave + AWAVES * i) * 16 + r16;
+                    sdm_f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0], b[i][0], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1], b[i][1], acc, 0, 0, 0);
+                    if (j < s) {
+#pragma unroll
+                        for (int v = 0; v < 4; ++v)
+                            scores[(size_t)(4 * q + v) * 2 * SP + half * SP + j] = acc[v];
+                    }
+                }
+            }
+        } else
         for (int half = 0; half < 2; ++half) {
             // operand A (this lane's token row, k-slices 8q .. 8q+7 of each step) serves
             // every sub-key tile of the half
