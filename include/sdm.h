@@ -173,7 +173,16 @@ size_t sdm_scan_saved_bytes(int B, int H, int T, int W, int d_v);
  *   dy            [B, H, T, d_v] fp32: gradient of y.
  *   dmem_T        optional [B, H, N, d_v] fp32 gradient of M_T (NULL = 0).
  *                 May alias dmem0.
- *   chunk         tokens per backward chunk (> 0); results do not depend on it.
+ *   chunk         (> 0) sets the pipeline stages of the backward: from the end
+ *                 of the sequence, a stage of a quarter of L, then stages of
+ *                 L = max(chunk, T/4) tokens (multiples of 64, at most about 64
+ *                 stages); chunk >= T runs one stage.  Each stage's scan runs
+ *                 on `stream`; the records of the next stage and the weight
+ *                 and addressing gradients of the previous one run meanwhile on
+ *                 the library's second stream (the one sdm_forward uses, with
+ *                 the same event ordering: when the call returns, all of its
+ *                 work is ordered before later work on `stream`).  Results do
+ *                 not depend on chunk, bit for bit.
  *   dq, dk        optional out [B, H, T, d_k] fp32 (NULL = not computed).
  *   dv            out [B, H, T, d_v] fp32.
  *   dalpha, dbeta out [B, H, T] fp32.

@@ -674,10 +674,13 @@ __global__ __launch_bounds__(256) void address_bwd_kernel(const XT* __restrict__
                                                           const int32_t* __restrict__ idx,
                                                           const float* __restrict__ val,
                                                           const float* __restrict__ dval,
-                                                          float* __restrict__ dx, int64_t ntok) {
+                                                          float* __restrict__ dx, int tb, int tn,
+                                                          int64_t ntok) {
+    // token-sides (stream, t) for t in [tb, tb + tn): ntok = streams * tn
     const int lane = lane_id();
-    const int64_t r = (int64_t)blockIdx.x * (blockDim.x / SDM_WAVE) + threadIdx.x / SDM_WAVE;
-    if (r >= ntok) return;
+    const int64_t lr = (int64_t)blockIdx.x * (blockDim.x / SDM_WAVE) + threadIdx.x / SDM_WAVE;
+    if (lr >= ntok) return;
+    const int64_t r = (lr / tn) * T + tb + lr % tn;
     const int h = (int)((r / T) % H);
     const bool has = lane < k;
     const float w = has ? val[r * k + lane] : 0.f;
@@ -789,41 +792,43 @@ hipError_t sdm_launch_address(const void* x, int x_dtype, const void* cb, int B,
 namespace {
 
 template <typename XT, int NC>
-void launch_address_bwd_nc(const void* cb, int B, int H, int T, int dk, int s, int k,
+void launch_address_bwd_nc(const void* cb, int H, int T, int tb, int tn, int dk, int s, int k,
                            const int32_t* idx, const float* val, const float* dval, float* dx,
                            int64_t ntok, hipStream_t st) {
     dim3 grid((unsigned)((ntok + 3) / 4));
     if (cb)
         hipLaunchKernelGGL((address_bwd_kernel<XT, true, NC>), grid, dim3(256), 0, st,
-                           static_cast<const XT*>(cb), H, T, dk, s, k, idx, val, dval, dx, ntok);
+                           static_cast<const XT*>(cb), H, T, dk, s, k, idx, val, dval, dx, tb, tn, ntok);
     else
         hipLaunchKernelGGL((address_bwd_kernel<XT, false, NC>), grid, dim3(256), 0, st,
-                           static_cast<const XT*>(cb), H, T, dk, s, k, idx, val, dval, dx, ntok);
+                           static_cast<const XT*>(cb), H, T, dk, s, k, idx, val, dval, dx, tb, tn, ntok);
 }
 
 template <typename XT>
-void launch_address_bwd_t(const void* cb, int B, int H, int T, int dk, int s, int k,
+void launch_address_bwd_t(const void* cb, int H, int T, int tb, int tn, int dk, int s, int k,
                           const int32_t* idx, const float* val, const float* dval, float* dx,
                           int64_t ntok, hipStream_t st) {
     // columns per lane: d_k <= 512 in codebook mode, d_k = 2 sqrt(N) <= 2048 in direct mode
-    if (dk <= 64) launch_address_bwd_nc<XT, 1>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
-    else if (dk <= 128) launch_address_bwd_nc<XT, 2>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
-    else if (dk <= 256) launch_address_bwd_nc<XT, 4>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
-    else if (dk <= 512) launch_address_bwd_nc<XT, 8>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
-    else if (dk <= 1024) launch_address_bwd_nc<XT, 16>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
-    else launch_address_bwd_nc<XT, 32>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
+#define SDM_ABWD(NC) launch_address_bwd_nc<XT, NC>(cb, H, T, tb, tn, dk, s, k, idx, val, dval, dx, ntok, st)
+    if (dk <= 64) SDM_ABWD(1);
+    else if (dk <= 128) SDM_ABWD(2);
+    else if (dk <= 256) SDM_ABWD(4);
+    else if (dk <= 512) SDM_ABWD(8);
+    else if (dk <= 1024) SDM_ABWD(16);
+    else SDM_ABWD(32);
+#undef SDM_ABWD
 }
 
 }  // namespace
 
-hipError_t sdm_launch_address_bwd(const void* cb, int cb_dtype, int B, int H, int T, int dk, int s,
-                                  int k, const int32_t* idx, const float* val, const float* dval,
+hipError_t sdm_launch_address_bwd(const void* cb, int cb_dtype, int B, int H, int T, int tb, int tn, int dk,
+                                  int s, int k, const int32_t* idx, const float* val, const float* dval,
                                   float* dx, hipStream_t st) {
-    const int64_t ntok = (int64_t)B * H * T;
+    const int64_t ntok = (int64_t)B * H * tn;
     if (ntok == 0) return hipSuccess;
     if (cb_dtype == SDM_DT_BF16)
-        launch_address_bwd_t<bf16_t>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
+        launch_address_bwd_t<bf16_t>(cb, H, T, tb, tn, dk, s, k, idx, val, dval, dx, ntok, st);
     else
-        launch_address_bwd_t<float>(cb, B, H, T, dk, s, k, idx, val, dval, dx, ntok, st);
+        launch_address_bwd_t<float>(cb, H, T, tb, tn, dk, s, k, idx, val, dval, dx, ntok, st);
     return hipGetLastError();
 }

@@ -197,6 +197,30 @@ SidePipe& side_pipe() {
     static SidePipe p;
     return p;
 }
+// The current device's second stream (created on first use, default priority)
+// and at least nev events; the caller holds sp.mu while it enqueues.
+hipError_t side_get(SidePipe& sp, int nev, hipStream_t* side, std::vector<hipEvent_t>** ev, int* dev_out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    if (!sp.side[dev]) {
+        if ((e = hipStreamCreateWithFlags(&sp.side[dev], hipStreamNonBlocking)) != hipSuccess) {
+            sp.side[dev] = nullptr;
+            return e;
+        }
+    }
+    std::vector<hipEvent_t>& v = sp.ev[dev];
+    while ((int)v.size() < nev) {
+        hipEvent_t x;
+        if ((e = hipEventCreateWithFlags(&x, hipEventDisableTiming)) != hipSuccess) return e;
+        v.push_back(x);
+    }
+    *side = sp.side[dev];
+    *ev = &v;
+    *dev_out = dev;
+    return hipSuccess;
+}
 int round_up(int x, int m) { return (x + m - 1) / m * m; }
 }  // namespace
 
@@ -399,25 +423,13 @@ int sdm_forward(const void* q, const void* k, int x_dtype, const void* cb_q, con
         return e == hipSuccess ? SDM_OK : hip_fail(e, "sdm_forward launch");
     }
 
-    int dev = 0;
-    if ((e = hipGetDevice(&dev)) != hipSuccess) return hip_fail(e, "sdm_forward hipGetDevice");
-    if (dev < 0 || dev >= kMaxDevices) return fail(SDM_ERR_UNSUPPORTED, "device index %d", dev);
     SidePipe& sp = side_pipe();
     std::lock_guard<std::mutex> lk(sp.mu);
-    if (!sp.side[dev]) {
-        if ((e = hipStreamCreateWithFlags(&sp.side[dev], hipStreamNonBlocking)) != hipSuccess) {
-            sp.side[dev] = nullptr;
-            return hip_fail(e, "sdm_forward side stream");
-        }
-    }
-    std::vector<hipEvent_t>& ev = sp.ev[dev];
-    while ((int)ev.size() < nchunks + 1) {
-        hipEvent_t x;
-        if ((e = hipEventCreateWithFlags(&x, hipEventDisableTiming)) != hipSuccess)
-            return hip_fail(e, "sdm_forward event");
-        ev.push_back(x);
-    }
-    hipStream_t side = sp.side[dev];
+    hipStream_t side = nullptr;
+    std::vector<hipEvent_t>* evp = nullptr;
+    int dev = 0;
+    if ((e = side_get(sp, nchunks + 1, &side, &evp, &dev)) != hipSuccess) return hip_fail(e, "sdm_forward side stream");
+    std::vector<hipEvent_t>& ev = *evp;
     // the side stream starts after the caller's earlier work; chunk c's scan waits for its front
     if ((e = hipEventRecord(ev[0], st)) != hipSuccess) return hip_fail(e, "sdm_forward record");
     if ((e = hipStreamWaitEvent(side, ev[0], 0)) != hipSuccess) return hip_fail(e, "sdm_forward wait");
@@ -494,18 +506,86 @@ int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, cons
     a.dw_val = dw_val ? dw_val : spare;
     a.dr_val = dr_val ? dr_val : spare + ST * W;
     a.ws = ws;
-    e = sdm_launch_scan_bwd(a, st);
-    if (e != hipSuccess) return hip_fail(e, "sdm_scan_bwd launch");
-    if (dq) {
-        SdmProfScope ps(SDM_K_ADDRESS_BWD, st);
-        e = sdm_launch_address_bwd(cb_q, cb_dtype, B, H, T, d_k, s, R, r_idx, r_val, a.dr_val, dq, st);
-        if (e != hipSuccess) return hip_fail(e, "sdm_scan_bwd dq");
+    a.line = sdm_bwd_line_io(a) ? 1 : 0;   // one decision for every stage and the reduce
+
+    // Stages of tokens from the end of the sequence down: a short first stage,
+    // then stages of len = max(chunk, T/4) tokens (multiples of 64, at most
+    // about kMaxChunks of them); chunk >= T runs one stage.  Stage c's scan
+    // runs on `stream`; its records, and the sums and addressing gradients of
+    // the stage before, run on the library's second stream meanwhile.
+    int len = T, first = T;
+    if (chunk < T) {
+        len = round_up(std::max(chunk, (T + 3) / 4), 64);
+        len = std::max(len, round_up((T + kMaxChunks - 2) / (kMaxChunks - 1), 64));
+        first = std::min(T, round_up(std::max(len / 4, 64), 64));
     }
-    if (dk) {
-        SdmProfScope ps(SDM_K_ADDRESS_BWD, st);
-        e = sdm_launch_address_bwd(cb_k, cb_dtype, B, H, T, d_k, s, W, w_idx, w_val, a.dw_val, dk, st);
-        if (e != hipSuccess) return hip_fail(e, "sdm_scan_bwd dk");
+    const int nchunks = first >= T ? 1 : 1 + (T - first + len - 1) / len;
+    auto stage_end = [&](int c) { return c == 0 ? T : std::max(0, T - first - (c - 1) * len); };
+    auto ranged = [&](int c) {
+        ScanBwdArgs ac = a;
+        ac.te = stage_end(c);
+        ac.tb = stage_end(c + 1);
+        return ac;
+    };
+    auto post = [&](const ScanBwdArgs& ac, hipStream_t sx) -> hipError_t {
+        hipError_t ee = sdm_launch_bwd_reduce_range(ac, sx);
+        if (ee != hipSuccess) return ee;
+        if (dq) {
+            SdmProfScope ps(SDM_K_ADDRESS_BWD, sx);
+            ee = sdm_launch_address_bwd(cb_q, cb_dtype, B, H, T, ac.tb, ac.te - ac.tb, d_k, s, R, r_idx, r_val,
+                                        a.dr_val, dq, sx);
+            if (ee != hipSuccess) return ee;
+        }
+        if (dk) {
+            SdmProfScope ps(SDM_K_ADDRESS_BWD, sx);
+            ee = sdm_launch_address_bwd(cb_k, cb_dtype, B, H, T, ac.tb, ac.te - ac.tb, d_k, s, W, w_idx, w_val,
+                                        a.dw_val, dk, sx);
+        }
+        return ee;
+    };
+    if (nchunks == 1) {
+        ScanBwdArgs ac = ranged(0);
+        if ((e = sdm_launch_bwd_prep_range(ac, st)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd launch");
+        if ((e = sdm_launch_bwd_scan_range(ac, st)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd launch");
+        if ((e = post(ac, st)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd launch");
+        return SDM_OK;
     }
+    SidePipe& sp = side_pipe();
+    std::lock_guard<std::mutex> lk(sp.mu);
+    hipStream_t side = nullptr;
+    std::vector<hipEvent_t>* evp = nullptr;
+    int dev = 0;
+    // events: [0] start, [1 + c] records of stage c ready, [1 + nchunks + c] scan of stage c done, last: side done
+    if ((e = side_get(sp, 2 * nchunks + 2, &side, &evp, &dev)) != hipSuccess)
+        return hip_fail(e, "sdm_scan_bwd side stream");
+    std::vector<hipEvent_t>& ev = *evp;
+    hipEvent_t ev_start = ev[0], ev_end = ev[2 * nchunks + 1];
+    auto ev_prep = [&](int c) { return ev[1 + c]; };
+    auto ev_scan = [&](int c) { return ev[1 + nchunks + c]; };
+    // the flag reset above (and the caller's earlier work) precede the side stream
+    if ((e = hipEventRecord(ev_start, st)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd record");
+    if ((e = hipStreamWaitEvent(side, ev_start, 0)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd wait");
+    // side: prep 0, prep 1, then for each c: [scan c done] post c, prep c + 2
+    for (int c = 0; c < std::min(2, nchunks); ++c) {
+        if ((e = sdm_launch_bwd_prep_range(ranged(c), side)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd launch");
+        if ((e = hipEventRecord(ev_prep(c), side)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd record");
+    }
+    for (int c = 0; c < nchunks; ++c) {
+        const ScanBwdArgs ac = ranged(c);
+        if ((e = hipStreamWaitEvent(st, ev_prep(c), 0)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd wait");
+        if ((e = sdm_launch_bwd_scan_range(ac, st)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd launch");
+        if ((e = hipEventRecord(ev_scan(c), st)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd record");
+        if ((e = hipStreamWaitEvent(side, ev_scan(c), 0)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd wait");
+        if ((e = post(ac, side)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd launch");
+        if (c + 2 < nchunks) {
+            if ((e = sdm_launch_bwd_prep_range(ranged(c + 2), side)) != hipSuccess)
+                return hip_fail(e, "sdm_scan_bwd launch");
+            if ((e = hipEventRecord(ev_prep(c + 2), side)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd record");
+        }
+    }
+    // everything the call enqueued is ordered before later work on `stream`
+    if ((e = hipEventRecord(ev_end, side)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd record");
+    if ((e = hipStreamWaitEvent(st, ev_end, 0)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd wait");
     return SDM_OK;
 }
 

@@ -36,17 +36,17 @@ __host__ __device__ constexpr int bstage_slots() {
     return bstage_lead<PD>() <= 8 ? 8 : (bstage_lead<PD>() <= 16 ? 16 : 32);
 }
 
-// Staging of the records (and v slices) of the G tokens [u1 - G + 1, u1] (clamped at 0),
-// the order the backward visits them in.  Loads are unconditional; indices past
-// the valid range are clamped and the surplus is never stored.
+// Staging of the records (and v slices) of the G tokens [u1 - G + 1, u1] (clamped at lo,
+// the first token of the range), the order the backward visits them in.  Loads are
+// unconditional; indices past the valid range are clamped and the surplus is never stored.
 template <typename VT, int SW, int NR>
 __device__ __forceinline__ void bstage_load(u4v (&st)[NR], u2v& stv, const unsigned char* srec,
-                                            const VT* sv, int u1, int dv, int slice, int rec_bytes,
+                                            const VT* sv, int u1, int lo, int dv, int slice, int rec_bytes,
                                             int lane) {
     constexpr int VB = SW * (int)sizeof(VT);
     constexpr int ppt = VB / 8;
-    const int ub1 = max(u1, 0);
-    const int u0 = max(0, ub1 - G + 1);
+    const int ub1 = max(u1, lo);
+    const int u0 = max(lo, ub1 - G + 1);
     const int cnt = ub1 - u0 + 1;
     const u4v* src = reinterpret_cast<const u4v*>(srec + (size_t)u0 * rec_bytes);
     const int last = cnt * rec_bytes / 16 - 1;
@@ -60,11 +60,11 @@ __device__ __forceinline__ void bstage_load(u4v (&st)[NR], u2v& stv, const unsig
 
 template <typename VT, int SW, int NS, int NR>
 __device__ __forceinline__ void bstage_store(const u4v (&st)[NR], u2v stv, unsigned char* rring,
-                                             unsigned char* vring, int u1, int rec_bytes, int lane) {
+                                             unsigned char* vring, int u1, int lo, int rec_bytes, int lane) {
     constexpr int VB = SW * (int)sizeof(VT);
     constexpr int ppt = VB / 8;
-    if (u1 < 0) return;
-    const int u0 = max(0, u1 - G + 1);
+    if (u1 < lo) return;
+    const int u0 = max(lo, u1 - G + 1);
     const int cnt = u1 - u0 + 1;
     const int nchunk = cnt * rec_bytes / 16;   // <= NR * 64 (checked by the host plan)
 #pragma unroll
@@ -220,8 +220,9 @@ template <typename VT, int SW, int PD, int K, int NR>
 __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
     const unsigned char* __restrict__ recs, const VT* __restrict__ v, float* __restrict__ mem,
     const float* __restrict__ saved, const float* __restrict__ dy, float* __restrict__ Gtab,
-    float* __restrict__ dv_out, float* __restrict__ part, int T, int dv, int W, int R, int64_t N,
-    int n_slices, int S, int lds_per_wave) {
+    float* __restrict__ dv_out, float* __restrict__ part, int T, int tb, int te, int dv, int W, int R,
+    int64_t N, int n_slices, int S, int lds_per_wave) {
+    // tokens te-1 down to tb of each stream (layout strides use T)
     constexpr int CQ = SW / 4;
     constexpr int RG = SDM_WAVE / CQ;
     constexpr int LEAD = bstage_lead<PD>();
@@ -270,34 +271,35 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
     u2v stv;
     BwdBuf<K> buf[PD];
 
-    // Step i processes token t = T-1-i.  Staging blocks are the G tokens
-    // ending at T-1-i for i % G == 0.
-    const int T1 = T - 1;
+    // Step i processes token t = te-1-i.  Staging blocks are the G tokens
+    // ending at te-1-i for i % G == 0.
+    const int T1 = te - 1;
     for (int i0 = 0; i0 < LEAD - G; i0 += G) {
-        bstage_load<VT, SW, NR>(st, stv, srec, sv, T1 - i0, dv, slice, c.L.bytes, lane);
-        bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, T1 - i0, c.L.bytes, lane);
+        bstage_load<VT, SW, NR>(st, stv, srec, sv, T1 - i0, tb, dv, slice, c.L.bytes, lane);
+        bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, T1 - i0, tb, c.L.bytes, lane);
     }
-    bstage_load<VT, SW, NR>(st, stv, srec, sv, T1 - (LEAD - G), dv, slice, c.L.bytes, lane);
+    bstage_load<VT, SW, NR>(st, stv, srec, sv, T1 - (LEAD - G), tb, dv, slice, c.L.bytes, lane);
 #pragma unroll
-    for (int j = 0; j < PD; ++j) bissue_rows<K, RG, NS>(buf[j], c, max(T1 - j, 0));
+    for (int j = 0; j < PD; ++j) bissue_rows<K, RG, NS>(buf[j], c, max(T1 - j, tb));
 
-    const int Tfull = T - T % PD;
-    for (int i0 = 0; i0 < Tfull; i0 += PD) {
+    const int n = te - tb;
+    const int nfull = n - n % PD;
+    for (int i0 = 0; i0 < nfull; i0 += PD) {
 #pragma unroll
         for (int j = 0; j < PD; ++j) {
             const int t = T1 - (i0 + j);
             if (j % G == 0) {
-                bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, t - (LEAD - G), c.L.bytes, lane);
-                bstage_load<VT, SW, NR>(st, stv, srec, sv, t - LEAD, dv, slice, c.L.bytes, lane);
+                bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, t - (LEAD - G), tb, c.L.bytes, lane);
+                bstage_load<VT, SW, NR>(st, stv, srec, sv, t - LEAD, tb, dv, slice, c.L.bytes, lane);
             }
             bwd_token<VT, SW, PD, K, NS>(c, buf[j], t, lane);
-            bissue_rows<K, RG, NS>(buf[j], c, max(t - PD, 0));
+            bissue_rows<K, RG, NS>(buf[j], c, max(t - PD, tb));
         }
     }
 #pragma unroll
     for (int j = 0; j < PD; ++j) {
-        const int i = Tfull + j;
-        if (i < T) bwd_token<VT, SW, PD, K, NS>(c, buf[j], T1 - i, lane);
+        const int i = nfull + j;
+        if (i < n) bwd_token<VT, SW, PD, K, NS>(c, buf[j], T1 - i, lane);
     }
 }
 
@@ -454,8 +456,8 @@ __device__ __forceinline__ void line_issue(LineBuf& b, const BwdCtx& c, const Li
 template <typename VT, int PD, int NS>
 __device__ __forceinline__ void line_step(const BwdCtx& c, const LinePtrs& p, unsigned char* lb,
                                           unsigned char* sb, int* flags, float* psum, const LineBuf& cur,
-                                          LineBuf& nxt, int t, int w, int lane, bool issue) {
-    const int u = max(t - PD + 1, 0);
+                                          LineBuf& nxt, int t, int tb, int w, int lane, bool issue) {
+    const int u = max(t - PD + 1, tb);
     LineTok x;
     line_read_tok<VT, NS>(x, c, t);
     const int2 st_sl = line_slots(c, t, p.rl, NS);
@@ -483,8 +485,9 @@ template <typename VT, int PD, int NR>
 __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
     const unsigned char* __restrict__ recs, const VT* __restrict__ v, float* __restrict__ mem,
     const float* __restrict__ saved, const float* __restrict__ dy, float* __restrict__ Gtab,
-    float* __restrict__ dv_out, float* __restrict__ part, int T, int dv, int64_t N, int n_slices, int S,
-    int lds_per_wave) {
+    float* __restrict__ dv_out, float* __restrict__ part, int T, int tb, int te, int dv, int64_t N,
+    int n_slices, int S, int lds_per_wave) {
+    // tokens te-1 down to tb of each stream (layout strides use T)
     constexpr int SW = 8;
     constexpr int LEAD = bstage_lead<PD>();
     constexpr int NS = bstage_slots<PD>();
@@ -543,56 +546,60 @@ __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
     u2v stv;
     LineBuf buf[PD];
 
-    const int T1 = T - 1;
+    const int T1 = te - 1;
     for (int i0 = 0; i0 < LEAD - G; i0 += G) {
-        bstage_load<VT, SW, NR>(st, stv, srec, sv, T1 - i0, dv, slice, c.L.bytes, lane);
-        bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, T1 - i0, c.L.bytes, lane);
+        bstage_load<VT, SW, NR>(st, stv, srec, sv, T1 - i0, tb, dv, slice, c.L.bytes, lane);
+        bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, T1 - i0, tb, c.L.bytes, lane);
     }
-    bstage_load<VT, SW, NR>(st, stv, srec, sv, T1 - (LEAD - G), dv, slice, c.L.bytes, lane);
+    bstage_load<VT, SW, NR>(st, stv, srec, sv, T1 - (LEAD - G), tb, dv, slice, c.L.bytes, lane);
 #pragma unroll
     for (int j = 0; j < PD - 1; ++j) {
-        const int u = max(T1 - j, 0);
+        const int u = max(T1 - j, tb);
         line_issue(buf[j], c, p, line_slots(c, u, p.rl, NS), u);
     }
     __syncthreads();   // flags initialised
 
-    // Token t = T-1-i uses buf[i % PD]; step i loads token t - PD + 1 into
+    // Token t = te-1-i uses buf[i % PD]; step i loads token t - PD + 1 into
     // buf[(i + PD - 1) % PD], the buffer token t + 1 used.
-    const int Tfull = T - T % PD;
-    for (int i0 = 0; i0 < Tfull; i0 += PD) {
+    const int n = te - tb;
+    const int nfull = n - n % PD;
+    for (int i0 = 0; i0 < nfull; i0 += PD) {
 #pragma unroll
         for (int j = 0; j < PD; ++j) {
             const int t = T1 - (i0 + j);
             if (j % G == 0) {
-                bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, t - (LEAD - G), c.L.bytes, lane);
-                bstage_load<VT, SW, NR>(st, stv, srec, sv, t - LEAD, dv, slice, c.L.bytes, lane);
+                bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, t - (LEAD - G), tb, c.L.bytes, lane);
+                bstage_load<VT, SW, NR>(st, stv, srec, sv, t - LEAD, tb, dv, slice, c.L.bytes, lane);
             }
-            line_step<VT, PD, NS>(c, p, lb, sb, flags, psum, buf[j], buf[(j + PD - 1) % PD], t, w, lane, true);
+            line_step<VT, PD, NS>(c, p, lb, sb, flags, psum, buf[j], buf[(j + PD - 1) % PD], t, tb, w, lane, true);
         }
     }
 #pragma unroll
     for (int j = 0; j < PD; ++j) {
-        const int i = Tfull + j;
-        if (i < T) line_step<VT, PD, NS>(c, p, lb, sb, flags, psum, buf[j], buf[(j + PD - 1) % PD], T1 - i, w, lane, false);
+        const int i = nfull + j;
+        if (i < n) line_step<VT, PD, NS>(c, p, lb, sb, flags, psum, buf[j], buf[(j + PD - 1) % PD], T1 - i, tb, w, lane, false);
     }
 }
 
 // Sum the partial scalars (one set per slice, or per workgroup of slices for the
-// line-cooperative kernel): rbar -> dr_val, kbar -> dw_val, dbeta, dalpha.
-__global__ __launch_bounds__(256) void bwd_reduce_kernel(const float* __restrict__ part, int n_parts,
-                                                         int64_t ST, int W, int R,
+// line-cooperative kernel) of tokens [tb, tb + n) of every stream: rbar -> dr_val,
+// kbar -> dw_val, dbeta, dalpha.
+__global__ __launch_bounds__(256) void bwd_reduce_kernel(const float* __restrict__ part, int n_parts, int S,
+                                                         int T, int tb, int n, int W, int R,
                                                          float* __restrict__ dw_val,
                                                          float* __restrict__ dr_val,
                                                          float* __restrict__ dbeta,
                                                          float* __restrict__ dalpha) {
     const int NP = W + R + 2;
-    const int64_t total = ST * NP;
+    const int64_t ST = (int64_t)S * T;
+    const int64_t total = (int64_t)S * n * NP;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
          i += (int64_t)gridDim.x * blockDim.x) {
-        float acc = 0.f;
-        for (int s = 0; s < n_parts; ++s) acc += part[(size_t)s * total + i];
-        const int64_t st = i / NP;
+        const int64_t sr = i / NP;
         const int p = (int)(i % NP);
+        const int64_t st = (sr / n) * T + tb + sr % n;
+        float acc = 0.f;
+        for (int sl = 0; sl < n_parts; ++sl) acc += part[((size_t)sl * ST + st) * NP + p];
         if (p < R)
             dr_val[st * R + p] = acc;
         else if (p < R + W)
@@ -650,9 +657,16 @@ bool bwd_plan(int S, int W, int R, int dv, int in_dtype, BwdPlan* p) {
 
 // The line-cooperative kernel's shape: 8-column slices, W = R = 32, d_v a
 // multiple of 32 (whole lines per workgroup), and its LDS within the limit.
-bool line_io_ok(const ScanBwdArgs& a, const BwdPlan& p) {
-    return sdm_line_io_enabled() && p.SW == 8 && p.K == 1 && a.W == LROWS && a.R == LROWS && a.dv % 32 == 0 &&
-           p.n_slices % LW == 0 && (size_t)p.lds_per_wave * LW + line_shared_bytes() <= (size_t)LDS_LIMIT;
+bool line_shape_ok(const ScanBwdArgs& a, const BwdPlan& p) {
+    return p.SW == 8 && p.K == 1 && a.W == LROWS && a.R == LROWS && a.dv % 32 == 0 && p.n_slices % LW == 0 &&
+           (size_t)p.lds_per_wave * LW + line_shared_bytes() <= (size_t)LDS_LIMIT;
+}
+bool line_io_ok(const ScanBwdArgs& a, const BwdPlan& p) { return sdm_line_io_enabled() && line_shape_ok(a, p); }
+// a.line >= 0: the caller's decision (one per call, so that every range and the
+// reduce agree), which must fit the shape
+bool use_line(const ScanBwdArgs& a, const BwdPlan& p, bool* ok) {
+    *ok = a.line <= 0 || line_shape_ok(a, p);
+    return a.line >= 0 ? (a.line != 0 && *ok) : line_io_ok(a, p);
 }
 
 // line: run the line-cooperative kernel (line_io_ok held); its partial sums
@@ -671,7 +685,7 @@ hipError_t launch_bwd_k(const ScanBwdArgs& a, const BwdPlan& p, bool line, float
             if (e != hipSuccess) return e;
             hipLaunchKernelGGL(kl, dim3(p.n_slices / LW * S), dim3(LW * SDM_WAVE), sml, st, a.ws + SDM_WS_HEADER,
                                static_cast<const VT*>(a.v), a.mem, a.saved, a.dy, a.G, a.dv_out, part, a.T,
-                               a.dv, a.N, p.n_slices, S, p.lds_per_wave);
+                               a.tb, a.te, a.dv, a.N, p.n_slices, S, p.lds_per_wave);
             return hipGetLastError();
         }
     }
@@ -680,7 +694,7 @@ hipError_t launch_bwd_k(const ScanBwdArgs& a, const BwdPlan& p, bool line, float
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kfn, grid, dim3(p.wpb * SDM_WAVE), sm, st, a.ws + SDM_WS_HEADER,
                        static_cast<const VT*>(a.v), a.mem, a.saved, a.dy, a.G, a.dv_out, part, a.T,
-                       a.dv, a.W, a.R, a.N, p.n_slices, S, p.lds_per_wave);
+                       a.tb, a.te, a.dv, a.W, a.R, a.N, p.n_slices, S, p.lds_per_wave);
     return hipGetLastError();
 }
 
@@ -716,30 +730,42 @@ bool sdm_bwd_plan_ok(int W, int R, int dv, int in_dtype) {
     return bwd_plan_sw<16>(W, R, dv, in_dtype, &p) && bwd_plan_sw<BSW_MIN>(W, R, dv, in_dtype, &p);
 }
 
-hipError_t sdm_launch_scan_bwd(const ScanBwdArgs& a, hipStream_t st) {
+bool sdm_bwd_line_io(const ScanBwdArgs& a) {
     BwdPlan plan;
-    const int S = a.B * a.H;
-    if (!bwd_plan(S, a.W, a.R, a.dv, a.in_dtype, &plan)) return hipErrorInvalidConfiguration;
-    {
-        SdmProfScope ps(SDM_K_BWD_PREP, st);
-        hipError_t e = sdm_launch_bwd_prep<BPD>(a, st);
-        if (e != hipSuccess) return e;
-    }
-    const bool line = line_io_ok(a, plan);
-    const int n_parts = line ? plan.n_slices / LW : plan.n_slices;   // partial sums per (stream, token)
+    return bwd_plan(a.B * a.H, a.W, a.R, a.dv, a.in_dtype, &plan) && line_io_ok(a, plan);
+}
+
+hipError_t sdm_launch_bwd_prep_range(const ScanBwdArgs& a, hipStream_t st) {
+    SdmProfScope ps(SDM_K_BWD_PREP, st);
+    return sdm_launch_bwd_prep<BPD>(a, st);
+}
+
+hipError_t sdm_launch_bwd_scan_range(const ScanBwdArgs& a, hipStream_t st) {
+    BwdPlan plan;
+    if (!bwd_plan(a.B * a.H, a.W, a.R, a.dv, a.in_dtype, &plan)) return hipErrorInvalidConfiguration;
+    bool ok;
+    const bool line = use_line(a, plan, &ok);
+    if (!ok) return hipErrorInvalidConfiguration;
     float* part = reinterpret_cast<float*>(a.ws + bwd_part_offset(a.B, a.H, a.T, a.W, a.R));
-    hipError_t e;
-    {
-        SdmProfScope ps(SDM_K_BWD_SCAN, st);
-        e = a.in_dtype == SDM_DT_BF16 ? launch_bwd_kk<bf16_t>(a, plan, line, part, st)
-                                      : launch_bwd_kk<float>(a, plan, line, part, st);
-    }
-    if (e != hipSuccess) return e;
+    SdmProfScope ps(SDM_K_BWD_SCAN, st);
+    return a.in_dtype == SDM_DT_BF16 ? launch_bwd_kk<bf16_t>(a, plan, line, part, st)
+                                     : launch_bwd_kk<float>(a, plan, line, part, st);
+}
+
+hipError_t sdm_launch_bwd_reduce_range(const ScanBwdArgs& a, hipStream_t st) {
+    BwdPlan plan;
+    if (!bwd_plan(a.B * a.H, a.W, a.R, a.dv, a.in_dtype, &plan)) return hipErrorInvalidConfiguration;
+    bool ok;
+    const bool line = use_line(a, plan, &ok);
+    if (!ok) return hipErrorInvalidConfiguration;
+    const int n_parts = line ? plan.n_slices / LW : plan.n_slices;   // partial sums per (stream, token)
+    const float* part = reinterpret_cast<const float*>(a.ws + bwd_part_offset(a.B, a.H, a.T, a.W, a.R));
+    const int S = a.B * a.H, n = a.te - a.tb;
+    if (S == 0 || n <= 0) return hipSuccess;
     SdmProfScope ps(SDM_K_BWD_REDUCE, st);
-    const int64_t ST = (int64_t)S * a.T;
-    const int64_t total = ST * (a.W + a.R + 2);
+    const int64_t total = (int64_t)S * n * (a.W + a.R + 2);
     const unsigned nb = (unsigned)std::min<int64_t>((total + 255) / 256, 65536);
-    hipLaunchKernelGGL(bwd_reduce_kernel, dim3(nb), dim3(256), 0, st, part, n_parts, ST, a.W, a.R,
+    hipLaunchKernelGGL(bwd_reduce_kernel, dim3(nb), dim3(256), 0, st, part, n_parts, S, a.T, a.tb, n, a.W, a.R,
                        a.dw_val, a.dr_val, a.dbeta, a.dalpha);
     return hipGetLastError();
 }

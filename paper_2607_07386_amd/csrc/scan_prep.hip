@@ -168,15 +168,17 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const int32_t* __restrict
                                                        const float* __restrict__ r_val,
                                                        const void* __restrict__ alpha,
                                                        const void* __restrict__ beta, int in_dtype,
-                                                       int T, int W, int R, int64_t N,
+                                                       int T, int tb, int te, int W, int R, int64_t N,
                                                        unsigned char* __restrict__ recs,
                                                        unsigned int* __restrict__ err) {
+    // records of tokens [tb, te); links only to tokens below te (the backward
+    // of later tokens, in an earlier call, left its rows in HBM)
     extern __shared__ int sm[];
     const BwdRec L = bwd_rec_layout(W, R);
     const int stream = blockIdx.y;
-    const int t0 = blockIdx.x * PT;
-    const int ntok = min(PT, T - t0);
-    const int span = min(PT + PD - 1, T - t0);   // tokens t0 .. t0+span-1 (later ones included)
+    const int t0 = tb + blockIdx.x * PT;
+    const int ntok = min(PT, te - t0);
+    const int span = min(PT + PD - 1, te - t0);   // tokens t0 .. t0+span-1 (later ones included)
     const int nlink = 2 * R + W;
     int* wl = sm;                                          // [PT+PD-1][W]
     int* rl = wl + (PT + PD - 1) * W;                      // [PT+PD-1][R]
@@ -282,13 +284,13 @@ hipError_t sdm_launch_fwd_prep(const ScanFwdArgs& a, hipStream_t st) {
 template <int PD>
 hipError_t sdm_launch_bwd_prep(const ScanBwdArgs& a, hipStream_t st) {
     const int S = a.B * a.H;
-    dim3 grid((a.T + PT - 1) / PT, S);
+    dim3 grid((a.te - a.tb + PT - 1) / PT, S);
     const size_t sm = bwd_prep_lds<PD>(a.W, a.R);
     auto kfn = bwd_prep_kernel<PD>;
     hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kfn, grid, dim3(256), sm, st, a.w_idx, a.w_val, a.r_idx, a.r_val, a.alpha,
-                       a.beta, a.in_dtype, a.T, a.W, a.R, a.N, a.ws + SDM_WS_HEADER,
+                       a.beta, a.in_dtype, a.T, a.tb, a.te, a.W, a.R, a.N, a.ws + SDM_WS_HEADER,
                        reinterpret_cast<unsigned int*>(a.ws));
     return hipGetLastError();
 }

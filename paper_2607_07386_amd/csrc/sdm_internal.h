@@ -61,8 +61,9 @@ __host__ __device__ inline BwdRec bwd_rec_layout(int W, int R) {
 hipError_t sdm_launch_address(const void* x, int x_dtype, const void* cb, int B, int H, int T,
                               int tb, int tn, int dk, int s, int k, int32_t* idx, float* val,
                               float* score, hipStream_t st);
-hipError_t sdm_launch_address_bwd(const void* cb, int cb_dtype, int B, int H, int T, int dk, int s,
-                                  int k, const int32_t* idx, const float* val, const float* dval,
+// token-sides (b, h, t) for t in [tb, tb + tn)
+hipError_t sdm_launch_address_bwd(const void* cb, int cb_dtype, int B, int H, int T, int tb, int tn, int dk,
+                                  int s, int k, const int32_t* idx, const float* val, const float* dval,
                                   float* dx, hipStream_t st);
 
 struct ScanFwdArgs {
@@ -80,7 +81,7 @@ struct ScanFwdArgs {
     float* y;
     float* saved;
     unsigned char* ws;   // workspace base (header + records)
-    int tb = 0, te = 0;  // tokens processed: [tb, te) (layout strides use T); tb % 8 == 0
+    int tb = 0, te = 0;  // tokens processed: [tb, te) (layout strides use T); tb a multiple of SDM_FWD_PD
 };
 hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st);   // prep + scan
 // the two halves separately (records of [tb, te), then the scan of [tb, te))
@@ -121,8 +122,17 @@ struct ScanBwdArgs {
     float* dw_val;    // [B,H,T,W] (workspace if the caller passed NULL)
     float* dr_val;    // [B,H,T,R]
     unsigned char* ws;
+    int tb = 0, te = 0;  // tokens processed, te-1 down to tb (layout strides use T)
+    int line = -1;       // line-cooperative kernel: 1 / 0, or -1 to decide from the shape
 };
-hipError_t sdm_launch_scan_bwd(const ScanBwdArgs& a, hipStream_t st);
+// Backward of tokens a.te-1 down to a.tb, in three steps: records (with links
+// inside the range), the scan, the sum of the partial scalars.  Ranges are run
+// from the end of the sequence down; tables carry the state between them.
+hipError_t sdm_launch_bwd_prep_range(const ScanBwdArgs& a, hipStream_t st);
+hipError_t sdm_launch_bwd_scan_range(const ScanBwdArgs& a, hipStream_t st);
+hipError_t sdm_launch_bwd_reduce_range(const ScanBwdArgs& a, hipStream_t st);
+// whether the backward of this shape runs the line-cooperative kernel now
+bool sdm_bwd_line_io(const ScanBwdArgs& a);
 template <int PD>
 hipError_t sdm_launch_bwd_prep(const ScanBwdArgs& a, hipStream_t st);
 bool sdm_bwd_plan_ok(int W, int R, int dv, int in_dtype);

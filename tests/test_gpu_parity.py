@@ -366,8 +366,11 @@ def test_backward_small(name, slice_width):
     assert errs["mem_restored_bit_exact"]
 
 
-def test_backward_chunk_invariance():
-    w = BWD["bf16-small"]
+@pytest.mark.parametrize("name", ["bf16-small", "bf16-line-ragged"])
+def test_backward_chunk_invariance(name):
+    """chunk sets the backward's pipeline stages (chunk >= T: one stage); results
+    are the same bit for bit (per-wave kernel, and the line-cooperative one)."""
+    w = BWD.get(name) or LINE[name]
     inp = synth.Inputs(w)
     outs = []
     for chunk in (1, 16, 64, w.T):
@@ -494,9 +497,13 @@ def _links_fwd(wi, ri, PD):
     return out
 
 
-def _links_bwd(wi, ri, PD):
+def _links_bwd(wi, ri, PD, stage_end=None):
+    """stage_end[t]: end (exclusive) of the backward stage holding token t; links
+    never reach tokens at or past it (default: one stage)."""
     T, W = wi.shape
     R = ri.shape[1]
+    if stage_end is None:
+        stage_end = np.full(T, T)
     lm = np.full((T, R), -1, np.int64)
     lgr = np.full((T, R), -1, np.int64)
     lgw = np.full((T, W), -1, np.int64)
@@ -507,7 +514,7 @@ def _links_bwd(wi, ri, PD):
             if hit.size:
                 return int(hit[0])
         for d in range(1, PD):
-            if t + d >= T:
+            if t + d >= stage_end[t]:
                 break
             hw = np.nonzero(wi[t + d] == slot)[0]
             if hw.size:
@@ -521,7 +528,7 @@ def _links_bwd(wi, ri, PD):
         for m in range(R):
             slot = ri[t, m]
             for d in range(1, PD):
-                if t + d >= T:
+                if t + d >= stage_end[t]:
                     break
                 hw = np.nonzero(wi[t + d] == slot)[0]
                 if hw.size:
@@ -537,7 +544,9 @@ def _links_bwd(wi, ri, PD):
 def test_prep_links_match_bruteforce(sorted_lists):
     """Links in the staged per-token records equal a brute-force search, for the
     forward and the backward window, across workgroup boundaries (T = 150 is
-    64 + 64 + 22 tokens) and for unsorted slot lists."""
+    64 + 64 + 22 tokens) and for unsorted slot lists.  The backward runs once as
+    one stage (chunk = T) and once in its pipeline stages (chunk 64: tokens
+    [86, 150), [22, 86), [0, 22)), whose links stop at the stage's end."""
     rng = np.random.default_rng(77)
     S, T, N, W, R, dv = 2, 150, 24, 5, 4, 8
     wi = np.stack([np.stack([rng.choice(N, W, replace=False) for _ in range(T)]) for _ in range(S)]).astype(np.int32)
@@ -560,11 +569,14 @@ def test_prep_links_match_bruteforce(sorted_lists):
     for s in range(S):
         np.testing.assert_array_equal(got[s], _links_fwd(wi[s], ri[s], FWD_PD))
     bws = sdm.bwd_workspace(S, 1, T, W, R, dv, DEV)
-    sdm.scan_bwd(t_(wi), wv, t_(ri), rv, v, g, g, mem, saved, torch.zeros_like(v), workspace=bws,
-                 want_dqk=False)
-    torch.cuda.synchronize()
     off_lm, _, rec = _rec_bwd(W, R)
-    raw = np_(bws)[256:256 + S * T * rec].reshape(S, T, rec)
-    got = raw[:, :, off_lm:off_lm + 2 * (2 * R + W)].copy().view(np.int16).astype(np.int64)
-    for s in range(S):
-        np.testing.assert_array_equal(got[s], _links_bwd(wi[s], ri[s], BWD_PD))
+    staged_end = np.repeat([22, 86, 150], [22, 64, 64])
+    for chunk, ends in ((T, None), (64, staged_end)):
+        mem_c = mem.clone()
+        sdm.scan_bwd(t_(wi), wv, t_(ri), rv, v, g, g, mem_c, saved, torch.zeros_like(v), workspace=bws,
+                     want_dqk=False, chunk=chunk)
+        torch.cuda.synchronize()
+        raw = np_(bws)[256:256 + S * T * rec].reshape(S, T, rec)
+        got = raw[:, :, off_lm:off_lm + 2 * (2 * R + W)].copy().view(np.int16).astype(np.int64)
+        for s in range(S):
+            np.testing.assert_array_equal(got[s], _links_bwd(wi[s], ri[s], BWD_PD, ends))
