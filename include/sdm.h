@@ -173,10 +173,11 @@ size_t sdm_scan_saved_bytes(int B, int H, int T, int W, int d_v);
  *   dy            [B, H, T, d_v] fp32: gradient of y.
  *   dmem_T        optional [B, H, N, d_v] fp32 gradient of M_T (NULL = 0).
  *                 May alias dmem0.
- *   chunk         (> 0) sets the pipeline stages of the backward: from the end
- *                 of the sequence, a stage of a quarter of L, then stages of
- *                 L = max(chunk, T/4) tokens (multiples of 64, at most about 64
- *                 stages); chunk >= T runs one stage.  Each stage's scan runs
+ *   chunk         (> 0) sets the pipeline stages of the backward: with
+ *                 L = max(chunk, T/4) rounded up to 64 (and at least T/63), the
+ *                 first stage (the end of the sequence) and the last are a
+ *                 quarter of L, the tokens between them even stages of at most
+ *                 L (multiples of 64); chunk >= T runs one stage.  Each stage's scan runs
  *                 on `stream`; the records of the next stage and the weight
  *                 and addressing gradients of the previous one run meanwhile on
  *                 the library's second stream (the one sdm_forward uses, with

@@ -519,8 +519,22 @@ int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, cons
         len = std::max(len, round_up((T + kMaxChunks - 2) / (kMaxChunks - 1), 64));
         first = std::min(T, round_up(std::max(len / 4, 64), 64));
     }
-    const int nchunks = first >= T ? 1 : 1 + (T - first + len - 1) / len;
-    auto stage_end = [&](int c) { return c == 0 ? T : std::max(0, T - first - (c - 1) * len); };
+    // first and last stages short (nothing overlaps the first stage's records or
+    // the last stage's gradient tails); the tokens between them in even stages of
+    // at most len (multiples of 64)
+    int nmid = 0, mid = 0, last = 0;
+    if (first < T) {
+        last = std::min(first, T - first);
+        const int rest = T - first - last;
+        nmid = rest > 0 ? (rest + len - 1) / len : 0;
+        mid = nmid > 0 ? round_up((rest + nmid - 1) / nmid, 64) : 0;
+    }
+    const int nchunks = first >= T ? 1 : 1 + nmid + 1;
+    auto stage_end = [&](int c) {
+        if (c == 0) return T;
+        if (c <= nmid + 1) return std::max(last, T - first - (c - 1) * mid);
+        return 0;
+    };
     auto ranged = [&](int c) {
         ScanBwdArgs ac = a;
         ac.te = stage_end(c);

@@ -546,7 +546,7 @@ def test_prep_links_match_bruteforce(sorted_lists):
     forward and the backward window, across workgroup boundaries (T = 150 is
     64 + 64 + 22 tokens) and for unsorted slot lists.  The backward runs once as
     one stage (chunk = T) and once in its pipeline stages (chunk 64: tokens
-    [86, 150), [22, 86), [0, 22)), whose links stop at the stage's end."""
+    [86, 150), [64, 86), [0, 64)), whose links stop at the stage's end."""
     rng = np.random.default_rng(77)
     S, T, N, W, R, dv = 2, 150, 24, 5, 4, 8
     wi = np.stack([np.stack([rng.choice(N, W, replace=False) for _ in range(T)]) for _ in range(S)]).astype(np.int32)
@@ -570,7 +570,7 @@ def test_prep_links_match_bruteforce(sorted_lists):
         np.testing.assert_array_equal(got[s], _links_fwd(wi[s], ri[s], FWD_PD))
     bws = sdm.bwd_workspace(S, 1, T, W, R, dv, DEV)
     off_lm, _, rec = _rec_bwd(W, R)
-    staged_end = np.repeat([22, 86, 150], [22, 64, 64])
+    staged_end = np.repeat([64, 86, 150], [64, 22, 64])
     for chunk, ends in ((T, None), (64, staged_end)):
         mem_c = mem.clone()
         sdm.scan_bwd(t_(wi), wv, t_(ri), rv, v, g, g, mem_c, saved, torch.zeros_like(v), workspace=bws,
