@@ -21,7 +21,13 @@
 
 namespace {
 
-constexpr int ATILE = 16;     // tokens per workgroup
+constexpr int ATILE = 16;     // tokens per workgroup (the MFMA tile's rows), sqrt(N) <= 256
+// Tokens per workgroup for E = ceil(sqrt(N) / 64): the scores of a tile take
+// 2 AT 64 E floats of LDS, so larger sqrt(N) takes fewer tokens per workgroup
+// (rows of the 16-row MFMA tile past AT are zero) to keep several workgroups
+// on a CU: 32 KB at E = 4, 8, 16.
+template <int E>
+__host__ __device__ constexpr int atile() { return E <= 4 ? ATILE : (E <= 8 ? 8 : 4); }
 constexpr int AWAVES = 4;
 constexpr int MAXK = 64;
 constexpr int MAXKS = 8;      // 32-deep MFMA steps per half: d_k / 2 <= 256
@@ -491,20 +497,21 @@ __device__ __noinline__ void token_general(const float* row, int s, int sp, int 
 }
 
 template <typename XT, int MODE, int E>   // MODE 0: direct, 1: codebook FMA, 2: codebook MFMA (bf16)
-__global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restrict__ x,
+__global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __restrict__ x,
                                                             const XT* __restrict__ cb, int H, int T,
                                                             int tb, int te, int dk, int s, int k,
                                                             int32_t* __restrict__ idx,
                                                             float* __restrict__ val,
                                                             float* __restrict__ score) {
     extern __shared__ __align__(16) unsigned char smem[];
-    float* scores = reinterpret_cast<float*>(smem);                          // [ATILE][2][64 E]
-    Entry* scratch = reinterpret_cast<Entry*>(scores + (size_t)ATILE * 2 * E * SDM_WAVE);  // [AWAVES][3][MAXK]
+    constexpr int AT = atile<E>();
+    float* scores = reinterpret_cast<float*>(smem);                          // [AT][2][64 E]
+    Entry* scratch = reinterpret_cast<Entry*>(scores + (size_t)AT * 2 * E * SDM_WAVE);  // [AWAVES][3][MAXK]
     uint64_t* kbufs = reinterpret_cast<uint64_t*>(scratch + AWAVES * 3 * MAXK);  // [AWAVES][64]
 
     const int stream = blockIdx.y;
     const int h = stream % H;
-    const int t0 = tb + blockIdx.x * ATILE;   // tile of tokens [t0, t0 + ATILE) within [tb, te)
+    const int t0 = tb + blockIdx.x * AT;   // tile of tokens [t0, t0 + AT) within [tb, te)
     const int tid = threadIdx.x;
     const int wave = tid / SDM_WAVE;
     const int lane = lane_id();
@@ -517,7 +524,7 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
     // Row of a token: [2][SP], half h's sub-key j at h*SP + j; j in [s, SP) holds -inf.
     constexpr int SP = E * SDM_WAVE;
     if constexpr (MODE == 0) {
-        for (int i = tid; i < ATILE * 2 * SP; i += blockDim.x) {
+        for (int i = tid; i < AT * 2 * SP; i += blockDim.x) {
             const int tt = i / (2 * SP), half = (i / SP) & 1, j = i % SP;
             const int t = t0 + tt;
             scores[i] = j >= s ? -INFINITY : (t < te ? to_f32(xs[(size_t)t * dk + half * s + j]) : 0.f);
@@ -525,7 +532,7 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
     } else if constexpr (MODE == 1) {
         const int dh = dk / 2;
         const XT* cbh = cb + (size_t)h * 2 * s * dh;
-        for (int i = tid; i < ATILE * 2 * SP; i += blockDim.x) {
+        for (int i = tid; i < AT * 2 * SP; i += blockDim.x) {
             const int tt = i / (2 * SP), half = (i / SP) & 1, j = i % SP;
             const int t = t0 + tt;
             float acc = 0.f;
@@ -546,6 +553,7 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
         const int nks = (dh + 31) / 32;   // 32-deep steps (at most MAXKS)
         const int r16 = lane % 16, q = lane / 16;
         const int t = t0 + r16;
+        const bool trow = r16 < AT && t < te;   // this lane's token row exists
         if (E <= 4 && nks <= 2) {
             // dh <= 64, s <= 256: this wave's tiles of a half (at most E) need 2 E
             // codebook operands; all are loaded before the first MFMA, so the half
@@ -557,7 +565,7 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
                 for (int ks = 0; ks < 2; ++ks) {
                     const int kc = ks * 32 + 8 * q;
                     a[ks] = sdm_bf16x8{};
-                    if (ks < nks && t < te && kc < dh)
+                    if (ks < nks && trow && kc < dh)
                         a[ks] = *reinterpret_cast<const sdm_bf16x8*>(xs + (size_t)t * dk + half * dh + kc);
                 }
 #pragma unroll
@@ -594,7 +602,7 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
             for (int ks = 0; ks < MAXKS; ++ks) {
                 const int kc = ks * 32 + 8 * q;
                 a[ks] = sdm_bf16x8{};
-                if (ks < nks && t < te && kc < dh)
+                if (ks < nks && trow && kc < dh)
                     a[ks] = *reinterpret_cast<const sdm_bf16x8*>(xs + (size_t)t * dk + half * dh + kc);
             }
             for (int jt = wave; jt < ntile; jt += AWAVES) {
@@ -612,13 +620,14 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
                 }
                 if (j < s) {
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) scores[(size_t)(4 * q + v) * 2 * SP + half * SP + j] = acc[v];
+                    for (int v = 0; v < 4; ++v)
+                        if (4 * q + v < AT) scores[(size_t)(4 * q + v) * 2 * SP + half * SP + j] = acc[v];
                 }
             }
         }
         if (s < SP) {
             const int pad = SP - s;
-            for (int i = tid; i < ATILE * 2 * pad; i += blockDim.x)
+            for (int i = tid; i < AT * 2 * pad; i += blockDim.x)
                 scores[(i / pad) * SP + s + i % pad] = -INFINITY;
         }
     }
@@ -644,7 +653,7 @@ __global__ __launch_bounds__(ATILE * 16) void address_kernel(const XT* __restric
         listA[lane] = Entry{-INFINITY, 0};
         listB[lane] = Entry{-INFINITY, 0};
     }
-    for (int tt = wave; tt < ATILE; tt += AWAVES) {
+    for (int tt = wave; tt < AT; tt += AWAVES) {
         const int t = t0 + tt;
         if (t >= te) break;
         const float* row = scores + (size_t)tt * 2 * SP;
@@ -742,8 +751,8 @@ __global__ __launch_bounds__(256) void address_bwd_kernel(const XT* __restrict__
 }
 
 // LDS of a tile: padded score rows, per-wave lists and sort buffer.
-constexpr size_t address_lds_bytes(int E) {
-    return (size_t)ATILE * 2 * E * SDM_WAVE * sizeof(float) + AWAVES * 3 * MAXK * sizeof(Entry) +
+constexpr size_t address_lds_bytes(int E, int AT) {
+    return (size_t)AT * 2 * E * SDM_WAVE * sizeof(float) + AWAVES * 3 * MAXK * sizeof(Entry) +
            AWAVES * SDM_WAVE * sizeof(uint64_t);
 }
 
@@ -751,18 +760,18 @@ template <typename XT, int MODE>
 hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, int tb, int tn, int dk,
                             int s, int k, int32_t* idx, float* val, float* score, hipStream_t st) {
     const int E = (s + SDM_WAVE - 1) / SDM_WAVE;
-    dim3 grid((tn + ATILE - 1) / ATILE, B * H);
     const XT* xp = static_cast<const XT*>(x);
     const XT* cp = static_cast<const XT*>(cb);
 #define SDM_ADDR_CASE(EE)                                                                       \
     {                                                                                           \
-        const size_t sm = address_lds_bytes(EE);                                                \
+        constexpr int AT = atile<EE>();                                                         \
+        const size_t sm = address_lds_bytes(EE, AT);                                            \
         auto kfn = address_kernel<XT, MODE, EE>;                                                \
         hipError_t e = hipFuncSetAttribute((const void*)kfn,                                    \
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm); \
         if (e != hipSuccess) return e;                                                          \
-        hipLaunchKernelGGL(kfn, grid, dim3(ATILE * 16), sm, st, xp, cp, H, T, tb, tb + tn, dk, s, k,\
-                           idx, val, score);                                                    \
+        hipLaunchKernelGGL(kfn, dim3((tn + AT - 1) / AT, B * H), dim3(AWAVES * SDM_WAVE), sm, st, xp, cp, \
+                           H, T, tb, tb + tn, dk, s, k, idx, val, score);                      \
         return hipGetLastError();                                                               \
     }
     if (E <= 1) SDM_ADDR_CASE(1)

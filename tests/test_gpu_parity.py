@@ -118,6 +118,9 @@ SMALL = {
     "bf16-fma-dk20": synth.Workload("t", B=1, H=1, T=90, d_k=20, d_v=16, N=400, topk=5, seed=15),
     "f32-k1": synth.Workload("t", B=1, H=2, T=65, d_k=16, d_v=8, N=100, topk=1, dtype="f32", seed=16),
     "bf16-k64-s128": synth.Workload("t", B=1, H=1, T=64, d_k=64, d_v=64, N=16384, topk=64, seed=17),
+    # sqrt(N) = 512 and 1024: 8- and 4-token addressing workgroups (T not a multiple of either)
+    "bf16-s512": synth.Workload("t", B=1, H=2, T=43, d_k=64, d_v=32, N=262144, topk=32, seed=24),
+    "bf16-s1024": synth.Workload("t", B=1, H=1, T=26, d_k=128, d_v=16, N=1048576, topk=32, seed=25),
     "bf16-hazard-N64": synth.Workload("t", B=2, H=2, T=500, d_k=32, d_v=48, N=64, topk=8, seed=18),
     "f32-hazard-N16-k4": synth.Workload("t", B=1, H=1, T=333, d_k=8, d_v=4, N=16, topk=4, dtype="f32", seed=19),
     "bf16-T1": synth.Workload("t", B=2, H=2, T=1, d_k=32, d_v=32, N=256, topk=8, seed=20),
