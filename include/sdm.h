@@ -63,7 +63,7 @@ enum sdm_status {
  *             NULL selects direct mode, which needs d_k == 2*sqrt(N) and takes
  *             s0 = x[0:sqrt(N)], s1 = x[sqrt(N):2*sqrt(N)] as the scores.
  *   N         slots per head; must be a perfect square, sqrt(N) <= 1024.
- *   topk      slots selected per token, 1 <= topk <= min(sqrt(N), 64).
+ *   topk      slots selected per token, 1 <= topk <= min(sqrt(N), 128).
  *   idx       out [B, H, T, topk] int32: selected slot ids, ascending.
  *   val       out [B, H, T, topk] fp32: softmax weights, in idx order.
  *   score     optional out [B, H, T, topk] fp32: the raw selected scores.
@@ -101,7 +101,7 @@ int sdm_address(const void* x, int x_dtype, const void* codebook,
  *                 (the undo log of App. A.3); saved_bytes must be at least
  *                 sdm_scan_saved_bytes().
  *   workspace     at least sdm_scan_fwd_workspace_bytes() bytes, 256-B aligned.
- * Limits: 1 <= W, R <= 64; d_v % 4 == 0; d_v <= 4096; T == 0 is a no-op.
+ * Limits: 1 <= W, R <= 128; d_v % 4 == 0; d_v <= 4096; T == 0 is a no-op.
  * ---------------------------------------------------------------------- */
 int sdm_scan_fwd(const int32_t* w_idx, const float* w_val, int W,
                  const int32_t* r_idx, const float* r_val, int R,

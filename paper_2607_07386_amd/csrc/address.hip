@@ -2,7 +2,8 @@
 // Sec. 4 softmax-normalised activations, App. A.2 sort-by-index) and its
 // backward, for gfx950.
 //
-// One workgroup = 4 waves = a tile of 16 tokens of one (b, h) stream.
+// One workgroup = 4 waves = a tile of 16 tokens (8 or 4 for sqrt(N) above
+// 256 or 512) of one (b, h) stream.
 //  A. sub-key scores of the tile into LDS: bf16 codebooks on the matrix
 //     cores (v_mfma_f32_16x16x32_bf16: 16 tokens x 16 sub-keys x 32 deep),
 //     fp32 codebooks with plain FMAs, direct mode by copying x.
@@ -16,6 +17,8 @@
 //  C. candidates (i, j) of the two ranked shortlists with (i+1)(j+1) <= k
 //     (every other pair has >= k pairs ranked above it), selected the same
 //     way, then sorted by slot id and softmax-normalised.
+// k in (64, 128] runs a kernel of its own: lists of two entries per lane,
+// exact bisection selection, 128-wide bitonic sorts.
 #include "sdm_common.h"
 #include "sdm_internal.h"
 
@@ -29,9 +32,11 @@ constexpr int ATILE = 16;     // tokens per workgroup (the MFMA tile's rows), sq
 template <int E>
 __host__ __device__ constexpr int atile() { return E <= 4 ? ATILE : (E <= 8 ? 8 : 4); }
 constexpr int AWAVES = 4;
-constexpr int MAXK = 64;
+constexpr int MAXK = 64;      // largest k of the one-entry-per-lane kernels
+constexpr int MAXK_BIG = 128; // largest k: two entries per lane
 constexpr int MAXKS = 8;      // 32-deep MFMA steps per half: d_k / 2 <= 256
 constexpr int MAXCAND_E = 5;  // ceil(280 / 64): pruned candidates for k <= 64
+constexpr int MAXCAND_BIG = 11;  // ceil(645 / 64): pruned candidates for k <= 128
 
 struct Entry {
     float score;
@@ -64,6 +69,14 @@ constexpr PairTable make_pair_table() {
 }
 __constant__ const PairTable c_pairs = make_pair_table();
 static_assert(make_pair_table().n[32] <= 3 * 64 && make_pair_table().n[MAXK] <= MAXCAND_E * 64, "pair counts");
+
+// Number of pruned pairs of k: sum over i < k of floor(k / (i + 1)).
+__host__ __device__ constexpr int pair_count(int k) {
+    int n = 0;
+    for (int i = 1; i <= k; ++i) n += k / i;
+    return n;
+}
+static_assert(pair_count(MAXK_BIG) <= MAXCAND_BIG * SDM_WAVE, "pair counts, k <= 128");
 
 // k-th largest key: the largest tau with #{key >= tau} >= k.
 template <int E>
@@ -496,7 +509,156 @@ __device__ __noinline__ void token_general(const float* row, int s, int sp, int 
     __builtin_amdgcn_wave_barrier();
 }
 
-template <typename XT, int MODE, int E>   // MODE 0: direct, 1: codebook FMA, 2: codebook MFMA (bf16)
+// ---- k in (64, 128]: two list entries per lane ---------------------------
+// Position p = 64 r + lane of a 128-entry list lives in register r of its lane.
+// Bitonic stage (KK, J) pairs positions p and p ^ J: within a lane's two
+// registers for J = 64, across lanes (DPP / permlane) otherwise.  The lower
+// position of a pair keeps the larger key when its block of KK runs
+// descending, which for a descending sort is the block with p & KK == 0.
+template <int KK, int J>
+__device__ __forceinline__ void bsort128_desc(uint64_t (&key)[2], int lane) {
+    if constexpr (J == 64) {
+        const uint64_t a = key[0], b = key[1];
+        key[0] = a > b ? a : b;
+        key[1] = a > b ? b : a;
+    } else {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            const uint64_t o = ((uint64_t)xor_lane<J>((uint32_t)(key[r] >> 32)) << 32) |
+                               xor_lane<J>((uint32_t)key[r]);
+            const bool desc = KK == 128 ? true : (KK == 64 ? r == 0 : (lane & KK) == 0);
+            const bool keep_max = ((lane & J) == 0) == desc;
+            key[r] = keep_max ? (o > key[r] ? o : key[r]) : (o < key[r] ? o : key[r]);
+        }
+    }
+    if constexpr (J > 1) bsort128_desc<KK, J / 2>(key, lane);
+    else if constexpr (KK < 128) bsort128_desc<KK * 2, KK>(key, lane);
+}
+// Ascending by key with a payload riding along (same network, directions flipped).
+template <int KK, int J>
+__device__ __forceinline__ void bsort128_asc_pay(uint32_t (&key)[2], float (&pay)[2], int lane) {
+    if constexpr (J == 64) {
+        const bool sw = key[1] < key[0];
+        const uint32_t k0 = key[0];
+        const float p0 = pay[0];
+        key[0] = sw ? key[1] : key[0];
+        pay[0] = sw ? pay[1] : pay[0];
+        key[1] = sw ? k0 : key[1];
+        pay[1] = sw ? p0 : pay[1];
+    } else {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            const uint32_t o = xor_lane<J>(key[r]);
+            const float op = xor_lane_ff<J>(pay[r]);
+            const bool asc = KK == 128 ? true : (KK == 64 ? r == 0 : (lane & KK) == 0);
+            const bool keep_min = ((lane & J) == 0) == asc;
+            const bool take = keep_min ? (o < key[r]) : (o > key[r]);
+            key[r] = take ? o : key[r];
+            pay[r] = take ? op : pay[r];
+        }
+    }
+    if constexpr (J > 1) bsort128_asc_pay<KK, J / 2>(key, pay, lane);
+    else if constexpr (KK < 128) bsort128_asc_pay<KK * 2, KK>(key, pay, lane);
+}
+
+// Stage 1 of one half for k <= 128: exact selection, then the k selected
+// ranked (score desc, id asc) into out[0 .. k).
+template <int E>
+__device__ void half_topk_big(const float* sc_row, int s, int k, Entry* scratch, Entry* out) {
+    const int lane = lane_id();
+    uint32_t key[E];
+    float sc[E];
+    int id[E];
+    bool sel[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int g = e * SDM_WAVE + lane;
+        const bool ok = g < s;
+        sc[e] = ok ? sc_row[g] : 0.f;
+        key[e] = ok ? ord_key(sc[e]) : 0u;
+        id[e] = ok ? g : 0x7fffffff;
+    }
+    select_topk<E>(key, id, k, sel);
+    compact<E>(sel, sc, id, scratch);
+    wait_lds();
+    __builtin_amdgcn_wave_barrier();
+    uint64_t ck2[2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        const int p = r * SDM_WAVE + lane;
+        const Entry me = scratch[min(p, k - 1)];
+        ck2[r] = p < k ? ckey(me.score, (uint32_t)me.id) : 0ull;
+    }
+    bsort128_desc<2, 1>(ck2, lane);
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        const int p = r * SDM_WAVE + lane;
+        if (p < k) out[p] = Entry{ckey_score(ck2[r]), ckey_id(ck2[r])};
+    }
+    wait_lds();
+    __builtin_amdgcn_wave_barrier();
+}
+
+// One token with 64 < k <= 128: stage 1 on both halves, stage 2 over the
+// pruned pairs (pairs[0 .. ncand), i << 8 | j), the k winners sorted by id,
+// softmax.  Lane l writes positions l and 64 + l of the outputs.
+template <int E>
+__device__ __noinline__ void token_big(const float* row, int s, int sp, int k, int ncand, const uint16_t* pairs,
+                                       Entry* scr, Entry* listA, Entry* listB, int32_t* idx_out,
+                                       float* val_out, float* score_out) {
+    const int lane = lane_id();
+    half_topk_big<E>(row, s, k, scr, listA);
+    half_topk_big<E>(row + sp, s, k, scr, listB);
+
+    uint32_t key[MAXCAND_BIG];
+    float sc[MAXCAND_BIG];
+    int id[MAXCAND_BIG];
+    bool sel[MAXCAND_BIG];
+#pragma unroll
+    for (int e = 0; e < MAXCAND_BIG; ++e) {
+        const int c = e * SDM_WAVE + lane;
+        const bool ok = c < ncand;
+        const uint32_t pr = pairs[ok ? c : 0];
+        const Entry a = listA[pr >> 8], b = listB[pr & 0xffu];
+        sc[e] = ok ? a.score + b.score : 0.f;
+        key[e] = ok ? ord_key(sc[e]) : 0u;
+        id[e] = ok ? a.id * s + b.id : 0x7fffffff;
+    }
+    select_topk<MAXCAND_BIG>(key, id, k, sel);
+    compact<MAXCAND_BIG>(sel, sc, id, scr);
+    wait_lds();
+    __builtin_amdgcn_wave_barrier();
+
+    // selected slots in ascending id order (App. A.2), then their softmax (Sec. 4)
+    uint32_t my_id[2];
+    float my_sc[2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        const int p = r * SDM_WAVE + lane;
+        const Entry me = scr[min(p, k - 1)];
+        my_id[r] = p < k ? (uint32_t)me.id : 0xffffffffu;
+        my_sc[r] = p < k ? me.score : -INFINITY;
+    }
+    bsort128_asc_pay<2, 1>(my_id, my_sc, lane);
+    const float mx = wave_max(fmaxf(my_sc[0], my_sc[1]));
+    float ex[2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) ex[r] = r * SDM_WAVE + lane < k ? expf(my_sc[r] - mx) : 0.f;
+    const float z = wave_sum(ex[0] + ex[1]);
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        const int p = r * SDM_WAVE + lane;
+        if (p < k) {
+            idx_out[p] = (int32_t)my_id[r];
+            val_out[p] = ex[r] / z;
+            if (score_out) score_out[p] = my_sc[r];
+        }
+    }
+    wait_lds();
+    __builtin_amdgcn_wave_barrier();
+}
+
+template <typename XT, int MODE, int E, int KM>   // MODE 0: direct, 1: codebook FMA, 2: codebook MFMA (bf16)
 __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __restrict__ x,
                                                             const XT* __restrict__ cb, int H, int T,
                                                             int tb, int te, int dk, int s, int k,
@@ -506,8 +668,8 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __
     extern __shared__ __align__(16) unsigned char smem[];
     constexpr int AT = atile<E>();
     float* scores = reinterpret_cast<float*>(smem);                          // [AT][2][64 E]
-    Entry* scratch = reinterpret_cast<Entry*>(scores + (size_t)AT * 2 * E * SDM_WAVE);  // [AWAVES][3][MAXK]
-    uint64_t* kbufs = reinterpret_cast<uint64_t*>(scratch + AWAVES * 3 * MAXK);  // [AWAVES][64]
+    Entry* scratch = reinterpret_cast<Entry*>(scores + (size_t)AT * 2 * E * SDM_WAVE);  // [AWAVES][3][KM]
+    uint64_t* kbufs = reinterpret_cast<uint64_t*>(scratch + AWAVES * 3 * KM);  // [AWAVES][64]
 
     const int stream = blockIdx.y;
     const int h = stream % H;
@@ -517,8 +679,24 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __
     const int lane = lane_id();
     const XT* xs = x + ((size_t)stream * T) * dk;
 
-    const uint16_t* pairs = c_pairs.e + c_pairs.off[k];
-    const int ncand = c_pairs.n[k];
+    const uint16_t* pairs;
+    int ncand;
+    if constexpr (KM > MAXK) {
+        // k > 64: this workgroup's pair list (i ascending, then j) in LDS, built
+        // here; every thread finishes it before the barrier after the scores
+        uint16_t* lp = reinterpret_cast<uint16_t*>(kbufs + AWAVES * SDM_WAVE);   // [MAXCAND_BIG * 64]
+        for (int i = tid; i < k; i += blockDim.x) {
+            int o = 0;
+            for (int a = 1; a <= i; ++a) o += k / a;
+            const int n = k / (i + 1);
+            for (int j = 0; j < n; ++j) lp[o + j] = (uint16_t)(i << 8 | j);
+        }
+        pairs = lp;
+        ncand = pair_count(k);
+    } else {
+        pairs = c_pairs.e + c_pairs.off[k];
+        ncand = c_pairs.n[k];
+    }
 
     // ---- A: sub-scores of the 16-token tile -------------------------------
     // Row of a token: [2][SP], half h's sub-key j at h*SP + j; j in [s, SP) holds -inf.
@@ -634,10 +812,20 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __
     __syncthreads();
 
     // ---- B, C: one wave per token --------------------------------------
-    Entry* scr = scratch + wave * 3 * MAXK;
-    Entry* listA = scr + MAXK;
-    Entry* listB = scr + 2 * MAXK;
+    Entry* scr = scratch + wave * 3 * KM;
+    Entry* listA = scr + KM;
+    Entry* listB = scr + 2 * KM;
     uint64_t* kbuf = kbufs + wave * SDM_WAVE;
+    if constexpr (KM > MAXK) {
+        for (int tt = wave; tt < AT; tt += AWAVES) {
+            const int t = t0 + tt;
+            if (t >= te) break;
+            const size_t o = ((size_t)stream * T + t) * k;
+            token_big<E>(scores + (size_t)tt * 2 * SP, s, SP, k, ncand, pairs, scr, listA, listB, idx + o,
+                         val + o, score ? score + o : nullptr);
+        }
+        return;
+    }
     // fast path: k <= 32, so at most 130 pruned pairs (3 per lane); list
     // entries past k hold -inf and pairs past the count point at entry 63
     const bool fast = E <= 4 && k <= 32 && k <= s;
@@ -673,11 +861,12 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __
 }
 
 // Backward of the weights through softmax and the sub-key scores: one wave
-// per token.  Lane n < k first forms g_n = w_n (wbar_n - sum_m w_m wbar_m) and
-// the sub-key ids of slot n; then, for n = 0 .. k-1 (read across the wave),
-// each lane adds g_n times its NC columns of the two sub-key rows.  The
-// codebook rows are read coalesced, several n in flight.
-template <typename XT, bool CODEBOOK, int NC>
+// per token.  Lane l first forms, for slots n = 64 r + l < k (r < KR),
+// g_n = w_n (wbar_n - sum_m w_m wbar_m) and the sub-key ids of slot n; then,
+// for n = 0 .. k-1 (read across the wave), each lane adds g_n times its NC
+// columns of the two sub-key rows.  The codebook rows are read coalesced,
+// several n in flight.
+template <typename XT, bool CODEBOOK, int NC, int KR>
 __global__ __launch_bounds__(256) void address_bwd_kernel(const XT* __restrict__ cb, int H, int T,
                                                           int dk, int s, int k,
                                                           const int32_t* __restrict__ idx,
@@ -691,13 +880,23 @@ __global__ __launch_bounds__(256) void address_bwd_kernel(const XT* __restrict__
     if (lr >= ntok) return;
     const int64_t r = (lr / tn) * T + tb + lr % tn;
     const int h = (int)((r / T) % H);
-    const bool has = lane < k;
-    const float w = has ? val[r * k + lane] : 0.f;
-    const float wb = has ? dval[r * k + lane] : 0.f;
-    const int id = has ? min(max(idx[r * k + lane], 0), s * s - 1) : 0;   // never read outside
-    const float dot = wave_sum(w * wb);
-    const float g = w * (wb - dot);
-    const int sub0 = id / s, sub1 = id - sub0 * s;
+    float w[KR], wb[KR], g[KR];
+    int sub0[KR], sub1[KR];
+    float dp = 0.f;
+#pragma unroll
+    for (int q = 0; q < KR; ++q) {
+        const int n = q * SDM_WAVE + lane;
+        const bool has = n < k;
+        w[q] = has ? val[r * k + n] : 0.f;
+        wb[q] = has ? dval[r * k + n] : 0.f;
+        const int id = has ? min(max(idx[r * k + n], 0), s * s - 1) : 0;   // never read outside
+        sub0[q] = id / s;
+        sub1[q] = id - sub0[q] * s;
+        dp = fmaf(w[q], wb[q], dp);
+    }
+    const float dot = wave_sum(dp);
+#pragma unroll
+    for (int q = 0; q < KR; ++q) g[q] = w[q] * (wb[q] - dot);
     float* out = dx + r * dk;
     float acc[NC];
 #pragma unroll
@@ -714,15 +913,19 @@ __global__ __launch_bounds__(256) void address_bwd_kernel(const XT* __restrict__
             base[i] = hi[i] ? s * dh + (c - dh) : c;
         }
         // slots past k carry g = 0 and sub-key 0: whole groups of 8, no remainder
-        for (int n0 = 0; n0 < k; n0 += 8) {
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const int n = n0 + u;
-                const float gn = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g), n));
-                const int a0 = __builtin_amdgcn_readlane(sub0, n), a1 = __builtin_amdgcn_readlane(sub1, n);
+        for (int q = 0; q < KR; ++q) {
+            for (int n0 = 0; n0 < min(k - q * SDM_WAVE, SDM_WAVE); n0 += 8) {
 #pragma unroll
-                for (int i = 0; i < NC; ++i)
-                    acc[i] = fmaf(gn, to_f32(cbh[base[i] + (hi[i] ? a1 : a0) * dh]), acc[i]);
+                for (int u = 0; u < 8; ++u) {
+                    const int n = n0 + u;
+                    const float gn = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g[q]), n));
+                    const int a0 = __builtin_amdgcn_readlane(sub0[q], n);
+                    const int a1 = __builtin_amdgcn_readlane(sub1[q], n);
+#pragma unroll
+                    for (int i = 0; i < NC; ++i)
+                        acc[i] = fmaf(gn, to_f32(cbh[base[i] + (hi[i] ? a1 : a0) * dh]), acc[i]);
+                }
             }
         }
     } else {
@@ -735,12 +938,16 @@ __global__ __launch_bounds__(256) void address_bwd_kernel(const XT* __restrict__
             hi[i] = c >= s;
             j[i] = hi[i] ? c - s : c;
         }
-        for (int n = 0; n < k; ++n) {
-            const float gn = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g), n));
-            const int a0 = __builtin_amdgcn_readlane(sub0, n), a1 = __builtin_amdgcn_readlane(sub1, n);
 #pragma unroll
-            for (int i = 0; i < NC; ++i)
-                if ((hi[i] ? a1 : a0) == j[i]) acc[i] += gn;
+        for (int q = 0; q < KR; ++q) {
+            for (int n = 0; n < min(k - q * SDM_WAVE, SDM_WAVE); ++n) {
+                const float gn = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(g[q]), n));
+                const int a0 = __builtin_amdgcn_readlane(sub0[q], n);
+                const int a1 = __builtin_amdgcn_readlane(sub1[q], n);
+#pragma unroll
+                for (int i = 0; i < NC; ++i)
+                    if ((hi[i] ? a1 : a0) == j[i]) acc[i] += gn;
+            }
         }
     }
 #pragma unroll
@@ -750,10 +957,11 @@ __global__ __launch_bounds__(256) void address_bwd_kernel(const XT* __restrict__
     }
 }
 
-// LDS of a tile: padded score rows, per-wave lists and sort buffer.
-constexpr size_t address_lds_bytes(int E, int AT) {
-    return (size_t)AT * 2 * E * SDM_WAVE * sizeof(float) + AWAVES * 3 * MAXK * sizeof(Entry) +
-           AWAVES * SDM_WAVE * sizeof(uint64_t);
+// LDS of a tile: padded score rows, per-wave lists and sort buffer, and for
+// k > 64 the pair list.
+constexpr size_t address_lds_bytes(int E, int AT, int KM) {
+    return (size_t)AT * 2 * E * SDM_WAVE * sizeof(float) + AWAVES * 3 * KM * sizeof(Entry) +
+           AWAVES * SDM_WAVE * sizeof(uint64_t) + (KM > MAXK ? MAXCAND_BIG * SDM_WAVE * sizeof(uint16_t) : 0);
 }
 
 template <typename XT, int MODE>
@@ -762,11 +970,11 @@ hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, 
     const int E = (s + SDM_WAVE - 1) / SDM_WAVE;
     const XT* xp = static_cast<const XT*>(x);
     const XT* cp = static_cast<const XT*>(cb);
-#define SDM_ADDR_CASE(EE)                                                                       \
+#define SDM_ADDR_CASE(EE, KM)                                                                   \
     {                                                                                           \
         constexpr int AT = atile<EE>();                                                         \
-        const size_t sm = address_lds_bytes(EE, AT);                                            \
-        auto kfn = address_kernel<XT, MODE, EE>;                                                \
+        const size_t sm = address_lds_bytes(EE, AT, KM);                                        \
+        auto kfn = address_kernel<XT, MODE, EE, KM>;                                            \
         hipError_t e = hipFuncSetAttribute((const void*)kfn,                                    \
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm); \
         if (e != hipSuccess) return e;                                                          \
@@ -774,11 +982,17 @@ hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, 
                            H, T, tb, tb + tn, dk, s, k, idx, val, score);                      \
         return hipGetLastError();                                                               \
     }
-    if (E <= 1) SDM_ADDR_CASE(1)
-    if (E <= 2) SDM_ADDR_CASE(2)
-    if (E <= 4) SDM_ADDR_CASE(4)
-    if (E <= 8) SDM_ADDR_CASE(8)
-    SDM_ADDR_CASE(16)
+    if (k > MAXK) {   // k <= sqrt(N), so E >= 2
+        if (E <= 2) SDM_ADDR_CASE(2, MAXK_BIG)
+        if (E <= 4) SDM_ADDR_CASE(4, MAXK_BIG)
+        if (E <= 8) SDM_ADDR_CASE(8, MAXK_BIG)
+        SDM_ADDR_CASE(16, MAXK_BIG)
+    }
+    if (E <= 1) SDM_ADDR_CASE(1, MAXK)
+    if (E <= 2) SDM_ADDR_CASE(2, MAXK)
+    if (E <= 4) SDM_ADDR_CASE(4, MAXK)
+    if (E <= 8) SDM_ADDR_CASE(8, MAXK)
+    SDM_ADDR_CASE(16, MAXK)
 #undef SDM_ADDR_CASE
 }
 
@@ -805,12 +1019,21 @@ void launch_address_bwd_nc(const void* cb, int H, int T, int tb, int tn, int dk,
                            const int32_t* idx, const float* val, const float* dval, float* dx,
                            int64_t ntok, hipStream_t st) {
     dim3 grid((unsigned)((ntok + 3) / 4));
-    if (cb)
-        hipLaunchKernelGGL((address_bwd_kernel<XT, true, NC>), grid, dim3(256), 0, st,
-                           static_cast<const XT*>(cb), H, T, dk, s, k, idx, val, dval, dx, tb, tn, ntok);
-    else
-        hipLaunchKernelGGL((address_bwd_kernel<XT, false, NC>), grid, dim3(256), 0, st,
-                           static_cast<const XT*>(cb), H, T, dk, s, k, idx, val, dval, dx, tb, tn, ntok);
+    const XT* c = static_cast<const XT*>(cb);
+    if (k > SDM_WAVE) {
+        if (cb)
+            hipLaunchKernelGGL((address_bwd_kernel<XT, true, NC, 2>), grid, dim3(256), 0, st, c, H, T, dk, s, k,
+                               idx, val, dval, dx, tb, tn, ntok);
+        else
+            hipLaunchKernelGGL((address_bwd_kernel<XT, false, NC, 2>), grid, dim3(256), 0, st, c, H, T, dk, s, k,
+                               idx, val, dval, dx, tb, tn, ntok);
+    } else if (cb) {
+        hipLaunchKernelGGL((address_bwd_kernel<XT, true, NC, 1>), grid, dim3(256), 0, st, c, H, T, dk, s, k, idx,
+                           val, dval, dx, tb, tn, ntok);
+    } else {
+        hipLaunchKernelGGL((address_bwd_kernel<XT, false, NC, 1>), grid, dim3(256), 0, st, c, H, T, dk, s, k, idx,
+                           val, dval, dx, tb, tn, ntok);
+    }
 }
 
 template <typename XT>

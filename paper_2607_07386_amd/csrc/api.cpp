@@ -73,7 +73,7 @@ int check_scan_common(const int32_t* w_idx, const float* w_val, int W, const int
     if (B < 0 || H < 0 || T < 0) return fail(SDM_ERR_INVALID_ARG, "B, H, T must be >= 0");
     if ((int64_t)B * H > kMaxStreams) return fail(SDM_ERR_UNSUPPORTED, "B*H must be <= %d", kMaxStreams);
     if (W < 1 || R < 1) return fail(SDM_ERR_INVALID_ARG, "W and R must be >= 1");
-    if (W > 64 || R > 64) return fail(SDM_ERR_UNSUPPORTED, "W and R must be <= 64");
+    if (W > 128 || R > 128) return fail(SDM_ERR_UNSUPPORTED, "W and R must be <= 128");
     if (d_v < 4 || d_v % 4 != 0) return fail(SDM_ERR_INVALID_ARG, "d_v must be a positive multiple of 4");
     if (d_v > 4096) return fail(SDM_ERR_UNSUPPORTED, "d_v must be <= 4096");
     if (N < 1 || N > (int64_t)1 << 31) return fail(SDM_ERR_INVALID_ARG, "N must be in [1, 2^31]");
@@ -146,7 +146,7 @@ int check_address(const void* x, int x_dtype, const void* codebook, int B, int H
     if (s < 0) return fail(SDM_ERR_INVALID_ARG, "N=%lld is not a perfect square", (long long)N);
     if (s > 1024) return fail(SDM_ERR_UNSUPPORTED, "sqrt(N) must be <= 1024");
     if (topk < 1 || topk > s) return fail(SDM_ERR_INVALID_ARG, "topk must be in [1, sqrt(N)]");
-    if (topk > 64) return fail(SDM_ERR_UNSUPPORTED, "topk must be <= 64");
+    if (topk > 128) return fail(SDM_ERR_UNSUPPORTED, "topk must be <= 128");
     if (d_k < 1) return fail(SDM_ERR_INVALID_ARG, "d_k must be >= 1");
     if (codebook) {
         if (d_k % 2) return fail(SDM_ERR_INVALID_ARG, "codebook mode needs an even d_k");

@@ -630,8 +630,8 @@ struct BwdPlan {
 template <int SW>
 bool bwd_plan_sw(int W, int R, int dv, int in_dtype, BwdPlan* p) {
     constexpr int RG = SDM_WAVE / (SW / 4);
-    const int need = (std::max(W, R) + RG - 1) / RG;
-    if (need > (SW == 16 ? 4 : 2)) return false;
+    const int need = (std::max(W, R) + RG - 1) / RG;   // row passes: at most 4 (64 or 128 rows)
+    if (need > 4) return false;
     p->SW = SW;
     p->K = need <= 1 ? 1 : (need <= 2 ? 2 : 4);
     p->NR = bnr_for_k<SW>(p->K);
@@ -647,12 +647,13 @@ bool bwd_plan_sw(int W, int R, int dv, int in_dtype, BwdPlan* p) {
 }
 
 // 16 columns per wave when that already gives every SIMD a wave, else 8,
-// unless a width is forced.
+// unless a width is forced; the other width when the chosen one cannot hold
+// the shape (16 columns hold at most 64 rows).
 bool bwd_plan(int S, int W, int R, int dv, int in_dtype, BwdPlan* p) {
     const int forced = sdm_scan_slice_width();
     if (forced == 16 || (forced == 0 && (int64_t)S * ((dv + 15) / 16) >= sdm_device_simds()))
-        return bwd_plan_sw<16>(W, R, dv, in_dtype, p);
-    return bwd_plan_sw<BSW_MIN>(W, R, dv, in_dtype, p);
+        return bwd_plan_sw<16>(W, R, dv, in_dtype, p) || bwd_plan_sw<BSW_MIN>(W, R, dv, in_dtype, p);
+    return bwd_plan_sw<BSW_MIN>(W, R, dv, in_dtype, p) || bwd_plan_sw<16>(W, R, dv, in_dtype, p);
 }
 
 // The line-cooperative kernel's shape: 8-column slices, W = R = 32, d_v a
@@ -702,7 +703,8 @@ template <typename VT>
 hipError_t launch_bwd_kk(const ScanBwdArgs& a, const BwdPlan& p, bool line, float* part, hipStream_t st) {
     if (p.SW == 8) {
         if (p.K == 1) return launch_bwd_k<VT, 8, 1>(a, p, line, part, st);
-        return launch_bwd_k<VT, 8, 2>(a, p, false, part, st);
+        if (p.K == 2) return launch_bwd_k<VT, 8, 2>(a, p, false, part, st);
+        return launch_bwd_k<VT, 8, 4>(a, p, false, part, st);
     }
     if (p.K == 1) return launch_bwd_k<VT, 16, 1>(a, p, false, part, st);
     if (p.K == 2) return launch_bwd_k<VT, 16, 2>(a, p, false, part, st);
@@ -726,8 +728,8 @@ size_t sdm_bwd_ws_bytes(int B, int H, int T, int W, int R, int dv) {
 }
 
 bool sdm_bwd_plan_ok(int W, int R, int dv, int in_dtype) {
-    BwdPlan p;
-    return bwd_plan_sw<16>(W, R, dv, in_dtype, &p) && bwd_plan_sw<BSW_MIN>(W, R, dv, in_dtype, &p);
+    BwdPlan p;   // every width bwd_plan may choose falls back to the 8-column plan
+    return bwd_plan_sw<BSW_MIN>(W, R, dv, in_dtype, &p);
 }
 
 bool sdm_bwd_line_io(const ScanBwdArgs& a) {

@@ -548,8 +548,8 @@ struct FwdPlan {
 template <int SW>
 bool fwd_plan_sw(int W, int R, int dv, int in_dtype, FwdPlan* p) {
     constexpr int RG = SDM_WAVE / (SW / 4);
-    const int need = (std::max(W, R) + RG - 1) / RG;
-    if (need > (SW == 16 ? 4 : 2)) return false;
+    const int need = (std::max(W, R) + RG - 1) / RG;   // row passes: at most 4 (64 or 128 rows)
+    if (need > 4) return false;
     p->SW = SW;
     p->K = need <= 1 ? 1 : (need <= 2 ? 2 : 4);
     p->NR = nr_for_k<SW>(p->K);
@@ -565,12 +565,14 @@ bool fwd_plan_sw(int W, int R, int dv, int in_dtype, FwdPlan* p) {
 }
 
 // 16 columns per wave when that already gives every SIMD a wave, else 8
-// (twice the waves, half the columns each), unless a width is forced.
+// (twice the waves, half the columns each), unless a width is forced.  The
+// other width is taken when the chosen one cannot hold the shape (16 columns
+// hold at most 64 rows).
 bool fwd_plan(int S, int W, int R, int dv, int in_dtype, FwdPlan* p) {
     const int forced = sdm_scan_slice_width();
     if (forced == 16 || (forced == 0 && (int64_t)S * ((dv + 15) / 16) >= sdm_device_simds()))
-        return fwd_plan_sw<16>(W, R, dv, in_dtype, p);
-    return fwd_plan_sw<8>(W, R, dv, in_dtype, p);
+        return fwd_plan_sw<16>(W, R, dv, in_dtype, p) || fwd_plan_sw<8>(W, R, dv, in_dtype, p);
+    return fwd_plan_sw<8>(W, R, dv, in_dtype, p) || fwd_plan_sw<16>(W, R, dv, in_dtype, p);
 }
 
 // LDS of the line-cooperative forward kernel (shared part, per-wave part).
@@ -624,7 +626,8 @@ template <typename VT, bool SAVE>
 hipError_t launch_fwd_kk(const ScanFwdArgs& a, const FwdPlan& p, hipStream_t st) {
     if (p.SW == 8) {
         if (p.K == 1) return launch_fwd_k<VT, 8, 1, SAVE>(a, p, st);
-        return launch_fwd_k<VT, 8, 2, SAVE>(a, p, st);
+        if (p.K == 2) return launch_fwd_k<VT, 8, 2, SAVE>(a, p, st);
+        return launch_fwd_k<VT, 8, 4, SAVE>(a, p, st);
     }
     if (p.K == 1) return launch_fwd_k<VT, 16, 1, SAVE>(a, p, st);
     if (p.K == 2) return launch_fwd_k<VT, 16, 2, SAVE>(a, p, st);
@@ -638,8 +641,8 @@ size_t sdm_fwd_ws_bytes(int B, int H, int T, int W, int R) {
 }
 
 bool sdm_fwd_plan_ok(int W, int R, int dv, int in_dtype) {
-    FwdPlan p;   // the 16-column plan fits whenever the 8-column one does
-    return fwd_plan_sw<16>(W, R, dv, in_dtype, &p) && fwd_plan_sw<8>(W, R, dv, in_dtype, &p);
+    FwdPlan p;   // every width fwd_plan may choose falls back to the 8-column plan
+    return fwd_plan_sw<8>(W, R, dv, in_dtype, &p);
 }
 
 hipError_t sdm_launch_fwd_prep_range(const ScanFwdArgs& a, hipStream_t st) {

@@ -49,7 +49,7 @@ def addr(**kw):
 
 @pytest.mark.parametrize("kw,code", [
     (dict(N=65535), -1), (dict(N=0), -1), (dict(topk=0), -1), (dict(topk=257), -1),
-    (dict(N=128 * 128, topk=65), -2), (dict(d_k=127), -1), (dict(d_k=1024), -2),
+    (dict(N=100 * 100, topk=101), -1), (dict(N=256 * 256, topk=129), -2), (dict(d_k=127), -1), (dict(d_k=1024), -2),
     (dict(cb=None, d_k=100), -1), (dict(x=None), -1), (dict(idx=None), -1), (dict(x=A + 4), -1),
     (dict(x_dtype=7), -1), (dict(T=-1), -1), (dict(B=70000), -2), (dict(N=2048 * 2048), -2),
 ])
@@ -73,7 +73,7 @@ def fwd(**kw):
 
 
 @pytest.mark.parametrize("kw,code", [
-    (dict(W=0), -1), (dict(R=0), -1), (dict(W=65), -2), (dict(dv=6), -1), (dict(dv=8192), -2),
+    (dict(W=0), -1), (dict(R=0), -1), (dict(W=129), -2), (dict(R=129), -2), (dict(dv=6), -1), (dict(dv=8192), -2),
     (dict(N=0), -1), (dict(dt=2), -1), (dict(mem=None), -1), (dict(y=None), -1), (dict(v=A + 2), -1),
     (dict(ws=None), -1), (dict(ws=A + 16), -1), (dict(wsb=100), -3),
     (dict(saved=A, sb=10), -3), (dict(saved=A + 8, sb=1 << 40), -1), (dict(B=-1), -1),
@@ -151,11 +151,11 @@ def test_undo_log_matches_paper_memory_figures():
 
 
 def test_every_supported_shape_has_a_launch_plan():
-    """Every W, R <= 64 and d_v the header allows gets a scan plan whose staged
+    """Every W, R <= 128 and d_v the header allows gets a scan plan whose staged
     per-token records fit the staging registers and LDS: validation gets past
     the plan and stops at the (deliberately) too-small workspace."""
-    for W in range(1, 65):
-        for R in (1, 7, 16, 17, 31, 32, 33, 48, 63, 64):
+    for W in range(1, 129):
+        for R in (1, 7, 16, 17, 31, 32, 33, 48, 63, 64, 65, 96, 127, 128):
             for dv, dt in ((4, 0), (36, 1), (128, 1), (960, 0), (4096, 1)):
                 assert fwd(W=W, R=R, dv=dv, dt=dt, wsb=0) == -3, (W, R, dv, dt)
                 assert bwd(W=W, R=R, dv=dv, dt=dt, wsb=0, cbq=None, cbk=None, dq=None, dkk=None) == -3, \
@@ -173,7 +173,7 @@ def test_forward_validation():
                              a["al"], a["be"], a["dt"], a["mem"], a["B"], a["H"], a["T"], a["dv"], a["N"],
                              a["ri"], a["rv"], a["wi"], a["wv"], a["y"], a["saved"], a["sb"], a["chunk"],
                              a["ws"], a["wsb"], None)
-    for kw, code in ((dict(chunk=-1), -1), (dict(N=65535), -1), (dict(topk=65), -2), (dict(k=None), -1),
+    for kw, code in ((dict(chunk=-1), -1), (dict(N=65535), -1), (dict(topk=129, N=256 * 256), -2), (dict(k=None), -1),
                      (dict(ri=A + 4), -1), (dict(dv=6), -1), (dict(wsb=100), -3), (dict(y=None), -1),
                      (dict(cbk=A + 2), -1), (dict(xdt=5), -1)):
         assert fw(**kw) == code, kw

@@ -121,6 +121,11 @@ SMALL = {
     # sqrt(N) = 512 and 1024: 8- and 4-token addressing workgroups (T not a multiple of either)
     "bf16-s512": synth.Workload("t", B=1, H=2, T=43, d_k=64, d_v=32, N=262144, topk=32, seed=24),
     "bf16-s1024": synth.Workload("t", B=1, H=1, T=26, d_k=128, d_v=16, N=1048576, topk=32, seed=25),
+    # k in (64, 128]: two list entries per lane in addressing, 128-row scan plans
+    "bf16-k128-s128": synth.Workload("t", B=1, H=2, T=70, d_k=64, d_v=40, N=16384, topk=128, seed=26),
+    "f32-k100-s256-direct": synth.Workload("t", B=1, H=1, T=45, d_k=512, d_v=24, N=65536, topk=100,
+                                           dtype="f32", seed=27, codebook=False),
+    "bf16-k96-s512": synth.Workload("t", B=1, H=1, T=19, d_k=128, d_v=16, N=262144, topk=96, seed=28),
     "bf16-hazard-N64": synth.Workload("t", B=2, H=2, T=500, d_k=32, d_v=48, N=64, topk=8, seed=18),
     "f32-hazard-N16-k4": synth.Workload("t", B=1, H=1, T=333, d_k=8, d_v=4, N=16, topk=4, dtype="f32", seed=19),
     "bf16-T1": synth.Workload("t", B=2, H=2, T=1, d_k=32, d_v=32, N=256, topk=8, seed=20),
@@ -196,14 +201,14 @@ def test_empty_sequence_is_noop():
 
 
 # ------------------------------------------------- scan on hand-made index lists
-def _scan_case(S, T, N, W, R, dv, idx_fn, seed, dtype=torch.float32):
+def _scan_case(S, T, N, W, R, dv, idx_fn, seed, dtype=torch.float32, wscale=1.0):
     rng = np.random.default_rng(seed)
     wi = np.zeros((S, T, W), np.int32)
     ri = np.zeros((S, T, R), np.int32)
     for s in range(S):
         for t in range(T):
             wi[s, t], ri[s, t] = idx_fn(rng, s, t, wi[s])
-    wv = rng.random((S, T, W)).astype(np.float32)
+    wv = (rng.random((S, T, W)) * wscale).astype(np.float32)
     rv = rng.standard_normal((S, T, R)).astype(np.float32)
     v = rng.standard_normal((S, T, dv)).astype(np.float32)
     al = rng.uniform(0.05, 1.0, (S, T)).astype(np.float32)
@@ -252,6 +257,22 @@ def test_scan_hazards(name, dtype, slice_width):
     y, mem, yo, memo = _scan_case(3, 211, 48, W, R, 20, fn, seed=5, dtype=dtype)
     ey, em = rel_err(y, yo), rel_err(mem, memo)
     report(f"hazard/{name}/{dtype}/sw{slice_width}", y_rel_err=ey, mem_rel_err=em)
+    assert ey < 1e-4 and em < 1e-4
+
+
+# W != R with lists past 64 rows (the 8-column, four-pass plans): random sets
+# over 300 slots, so rows recur within the prefetch window in most tokens.
+# Write weights are scaled by 2 / sqrt(W): then beta kappa_n sum(kappa) <= 2 and
+# a re-written row's factor alpha (1 - beta kappa_n sum(kappa)) stays in
+# [-1, 1]; unscaled weights in [0, 1) grow rows past the fp32 range.
+@pytest.mark.parametrize("W,R", [(128, 64), (40, 128), (128, 128)])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_scan_wide_lists(W, R, dtype, slice_width):
+    fn = lambda rng, s, t, prev: (rng.choice(300, W, replace=False).astype(np.int32),
+                                  rng.choice(300, R, replace=False).astype(np.int32))
+    y, mem, yo, memo = _scan_case(2, 150, 300, W, R, 24, fn, seed=9, dtype=dtype, wscale=2 / np.sqrt(W))
+    ey, em = rel_err(y, yo), rel_err(mem, memo)
+    report(f"wide/W{W}R{R}/{dtype}/sw{slice_width}", y_rel_err=ey, mem_rel_err=em)
     assert ey < 1e-4 and em < 1e-4
 
 
@@ -319,6 +340,10 @@ BWD = {
                                   m0="shared", train=True),
     "paper-1.4b-layer": synth.Workload("t", B=1, H=2, T=40, d_k=480, d_v=960, N=57600, topk=64,
                                        seed=34, codebook=False, m0="shared", train=True),
+    "bf16-k128-m0": synth.Workload("t", B=1, H=2, T=70, d_k=64, d_v=40, N=16384, topk=128, seed=35,
+                                   m0="shared", train=True),
+    "f32-k100-direct": synth.Workload("t", B=1, H=1, T=45, d_k=512, d_v=24, N=65536, topk=100, dtype="f32",
+                                      seed=36, codebook=False, train=True),
 }
 
 
