@@ -132,8 +132,12 @@ def main():
                     help="skip the reference timing of the forward step as three separate calls")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the memory-initialisation and decode legs")
-    ap.add_argument("--chunk", type=int, default=0,
-                    help="tokens per pipeline stage of the forward step (0: the library's choice)")
+    ap.add_argument("--chunk", type=int, default=448,
+                    help="tokens per pipeline stage of the forward step (0: the library's choice, a "
+                         "quarter of T; 448, measured best for this workload, by default)")
+    ap.add_argument("--train-chunk", type=int, default=0,
+                    help="tokens per pipeline stage of the training step's forward (0: the library's "
+                         "choice, measured best there)")
     ap.add_argument("--calib", action="store_true",
                     help="first run one plain 512 MiB copy (sdm_mem_init from a [16, 65536, 128] fp32 "
                          "source): the reference dispatch for scaling HBM counters")
@@ -253,8 +257,9 @@ def main():
                                    "N=65536 top-32 reads/writes, bf16 q/k/v/gates, fp32 memory",
                        "global_batch": B, "seq_len": T, "heads": H, "slots_per_head": w.N,
                        "topk": w.topk, "inputs": "bf16", "state": "f32", "parallelism": "none (1 GPU)",
-                       "pipeline": f"sdm_forward: addressing of chunk c+1 overlaps the scan of chunk c, "
-                                   f"{round(args.steps * T / scan_launches)}-token chunks"},
+                       "pipeline": f"sdm_forward(chunk={args.chunk}): addressing of stage c+1 overlaps the "
+                                   f"scan of stage c; {round(scan_launches / args.steps)} stages per step, "
+                                   f"{round(args.steps * T / scan_launches)} tokens on average"},
             "ms_per_step_median": round(per_step[len(per_step) // 2], 4),
             "ms_per_step_min": round(per_step[0], 4),
             "ms_per_step_sequential": ms_seq,
@@ -300,7 +305,7 @@ def main():
         def tstep():
             # forward with the undo log (addressing pipelined with the scan), then the backward
             o = sdm.forward(q, k, cb, cb, v, al, be, mem, wt.N, wt.topk, saved=saved, workspace=fws,
-                            y=y, out=touts, chunk=args.chunk)
+                            y=y, out=touts, chunk=args.train_chunk)
             sdm.scan_bwd(o["w_idx"], o["w_val"], o["r_idx"], o["r_val"], v, al, be, mem, saved, dy,
                          cb_q=cb, cb_k=cb, d_k=wt.d_k, chunk=wt.chunk, workspace=bws, dmem0=dmem0)
 
