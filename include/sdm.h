@@ -219,8 +219,9 @@ int sdm_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int d_v, 
  * Scan geometry.  Every column of the state is an independent recurrence
  * (Eq. 3-5 mix rows only within a column), so the scans give each wave a slice
  * of columns of one (b, h) stream.  sdm_set_scan_slice_width(sw):
- *   0   automatic (default): 16 columns per wave when B*H*ceil(d_v/16) waves
- *       cover every SIMD of the device, else 8 (twice as many waves);
+ *   0   automatic (default): 8 columns per wave, unless B*H*ceil(d_v/8)
+ *       waves would put 1.5 or more on every SIMD of the device: then 16 (half
+ *       as many waves); 8 as well where 16 columns cannot hold W or R (> 64);
  *   8, 16  force that width.
  * Process-wide; applies to launches that start after the call.  Results of
  * the two widths agree to the rounding of the sums over rows.  Any other

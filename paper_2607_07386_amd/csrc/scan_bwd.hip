@@ -646,12 +646,13 @@ bool bwd_plan_sw(int W, int R, int dv, int in_dtype, BwdPlan* p) {
     return true;
 }
 
-// 16 columns per wave when that already gives every SIMD a wave, else 8,
-// unless a width is forced; the other width when the chosen one cannot hold
-// the shape (16 columns hold at most 64 rows).
+// 8 columns per wave, unless that would put 1.5 or more waves on every SIMD:
+// then 16, unless a width is forced (the reason is the forward's); the other
+// width when the chosen one cannot hold the shape (16 columns hold at most 64
+// rows).
 bool bwd_plan(int S, int W, int R, int dv, int in_dtype, BwdPlan* p) {
     const int forced = sdm_scan_slice_width();
-    if (forced == 16 || (forced == 0 && (int64_t)S * ((dv + 15) / 16) >= sdm_device_simds()))
+    if (forced == 16 || (forced == 0 && 2 * (int64_t)S * ((dv + 7) / 8) >= 3 * (int64_t)sdm_device_simds()))
         return bwd_plan_sw<16>(W, R, dv, in_dtype, p) || bwd_plan_sw<BSW_MIN>(W, R, dv, in_dtype, p);
     return bwd_plan_sw<BSW_MIN>(W, R, dv, in_dtype, p) || bwd_plan_sw<16>(W, R, dv, in_dtype, p);
 }

@@ -564,13 +564,16 @@ bool fwd_plan_sw(int W, int R, int dv, int in_dtype, FwdPlan* p) {
     return true;
 }
 
-// 16 columns per wave when that already gives every SIMD a wave, else 8
-// (twice the waves, half the columns each), unless a width is forced.  The
-// other width is taken when the chosen one cannot hold the shape (16 columns
-// hold at most 64 rows).
+// 8 columns per wave, unless that would put 1.5 or more waves on every SIMD:
+// then 16 (half the waves, twice the columns each), unless a width is forced.
+// At two 8-column waves per SIMD the rows in flight outgrow the L2 and four
+// waves sharing each 128-byte line fetch it more than once: measured, the
+// per-wave scan at 1920 such waves fetched three times its bytes and ran at
+// half the speed of 960 16-column waves.  The other width is taken when the
+// chosen one cannot hold the shape (16 columns hold at most 64 rows).
 bool fwd_plan(int S, int W, int R, int dv, int in_dtype, FwdPlan* p) {
     const int forced = sdm_scan_slice_width();
-    if (forced == 16 || (forced == 0 && (int64_t)S * ((dv + 15) / 16) >= sdm_device_simds()))
+    if (forced == 16 || (forced == 0 && 2 * (int64_t)S * ((dv + 7) / 8) >= 3 * (int64_t)sdm_device_simds()))
         return fwd_plan_sw<16>(W, R, dv, in_dtype, p) || fwd_plan_sw<8>(W, R, dv, in_dtype, p);
     return fwd_plan_sw<8>(W, R, dv, in_dtype, p) || fwd_plan_sw<16>(W, R, dv, in_dtype, p);
 }
