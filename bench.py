@@ -387,13 +387,13 @@ def main():
         dms = e0.elapsed_time(e1) / nd
         out["decode"] = {
             "workload": f"one token per step for B={wd.B} sequences, H={wd.H}, N={wd.N}, d={wd.d_v}, "
-                        f"top-{wd.topk}; memory resident; one sdm_forward call per step",
+                        f"top-{wd.topk}; memory resident; one sdm_forward call per step (T = 1: one fused launch)",
             "us_per_step": round(dms * 1e3, 2), "tokens_per_s": round(wd.B / (dms * 1e-3), 1)}
         del q, k, v, al, be, cb, mem, ws, y, douts
         torch.cuda.empty_cache()
 
     # ------------------------------------------------------------ the paper's 1.4B layer
-    if args.only == "paper" or (args.only is None and not args.no_extra):
+    if (extra and args.only is None) or args.only == "paper":
         # Table 1's 1.4B layer: H = 2, N = 240^2 slots of d_v = 960, top-64 reads and
         # writes, direct-mode addressing (d_k = 2 sqrt(N)); 8 sequences of 4096 tokens
         wp = synth.Workload("paper-1.4b-layer", B=8, H=2, T=4096, d_k=480, d_v=960, N=57600, topk=64,

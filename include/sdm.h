@@ -131,6 +131,12 @@ int sdm_scan_fwd(const int32_t* w_idx, const float* w_val, int W,
  *                 and to at most 64 stages; the first stage is a quarter of
  *                 that (its addressing has nothing to overlap).  0 picks T/4
  *                 for T >= 2048 and a single stage otherwise.
+ * One token (T = 1, the decode step) without an undo log, both codebooks
+ * given or both NULL: a single launch on `stream` does the addressing of both
+ * sides and the scan step, one workgroup per (b, h) stream.  Slots and
+ * weights are those of sdm_address bit for bit; y and mem agree with
+ * sdm_scan_fwd to the rounding of the sums over rows (taken in another
+ * order); `chunk` is ignored.
  * Outputs must not alias inputs or each other.  Validation as for the three
  * calls; on a HIP launch error part of the work may already be enqueued.
  * Concurrent calls on one device share its second stream, so they serialise
@@ -258,7 +264,7 @@ int sdm_set_scan_line_io(int on);
 enum sdm_kernel {
     SDM_K_ADDRESS = 0, SDM_K_FWD_PREP = 1, SDM_K_FWD_SCAN = 2, SDM_K_BWD_PREP = 3,
     SDM_K_BWD_SCAN = 4, SDM_K_BWD_REDUCE = 5, SDM_K_ADDRESS_BWD = 6, SDM_K_MEM_INIT = 7,
-    SDM_K_COUNT = 8
+    SDM_K_DECODE = 8, SDM_K_COUNT = 9
 };
 int sdm_profile_enable(int on);
 int sdm_profile_read(int kernel, double* total_ms, int64_t* launches);

@@ -19,6 +19,8 @@
 //     way, then sorted by slot id and softmax-normalised.
 // k in (64, 128] runs a kernel of its own: lists of two entries per lane,
 // exact bisection selection, 128-wide bitonic sorts.
+#include <algorithm>
+
 #include "sdm_common.h"
 #include "sdm_internal.h"
 
@@ -658,34 +660,13 @@ __device__ __noinline__ void token_big(const float* row, int s, int sp, int k, i
     __builtin_amdgcn_wave_barrier();
 }
 
-template <typename XT, int MODE, int E, int KM>   // MODE 0: direct, 1: codebook FMA, 2: codebook MFMA (bf16)
-__global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __restrict__ x,
-                                                            const XT* __restrict__ cb, int H, int T,
-                                                            int tb, int te, int dk, int s, int k,
-                                                            int32_t* __restrict__ idx,
-                                                            float* __restrict__ val,
-                                                            float* __restrict__ score) {
-    extern __shared__ __align__(16) unsigned char smem[];
-    constexpr int AT = atile<E>();
-    float* scores = reinterpret_cast<float*>(smem);                          // [AT][2][64 E]
-    Entry* scratch = reinterpret_cast<Entry*>(scores + (size_t)AT * 2 * E * SDM_WAVE);  // [AWAVES][3][KM]
-    uint64_t* kbufs = reinterpret_cast<uint64_t*>(scratch + AWAVES * 3 * KM);  // [AWAVES][64]
-
-    const int stream = blockIdx.y;
-    const int h = stream % H;
-    const int t0 = tb + blockIdx.x * AT;   // tile of tokens [t0, t0 + AT) within [tb, te)
-    const int tid = threadIdx.x;
-    const int wave = tid / SDM_WAVE;
-    const int lane = lane_id();
-    const XT* xs = x + ((size_t)stream * T) * dk;
-
-    const uint16_t* pairs;
-    int ncand;
+// Pruned stage-2 pairs of k (i << 8 | j, i ascending then j): the constant
+// table for k <= 64; for k > 64 the workgroup builds them in lp (LDS), visible
+// after its next barrier.
+template <int KM>
+__device__ __forceinline__ void tile_pairs(int k, uint16_t* lp, const uint16_t*& pairs, int& ncand) {
     if constexpr (KM > MAXK) {
-        // k > 64: this workgroup's pair list (i ascending, then j) in LDS, built
-        // here; every thread finishes it before the barrier after the scores
-        uint16_t* lp = reinterpret_cast<uint16_t*>(kbufs + AWAVES * SDM_WAVE);   // [MAXCAND_BIG * 64]
-        for (int i = tid; i < k; i += blockDim.x) {
+        for (int i = threadIdx.x; i < k; i += blockDim.x) {
             int o = 0;
             for (int a = 1; a <= i; ++a) o += k / a;
             const int n = k / (i + 1);
@@ -697,24 +678,33 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __
         pairs = c_pairs.e + c_pairs.off[k];
         ncand = c_pairs.n[k];
     }
+}
 
-    // ---- A: sub-scores of the 16-token tile -------------------------------
-    // Row of a token: [2][SP], half h's sub-key j at h*SP + j; j in [s, SP) holds -inf.
+// Phase A: sub-key scores of tokens t0 .. t0 + nt - 1 (nt <= AT) of one
+// stream (xs: its x, token stride dk; cbh: its head's codebook [2][s][dk/2],
+// unused in direct mode) into score rows 0 .. nt-1: row [2][SP], half h's
+// sub-key j at h SP + j, j in [s, SP) -inf.  Rows past nt are not written.
+template <typename XT, int MODE, int E>
+__device__ __forceinline__ void tile_scores(const XT* __restrict__ xs, const XT* __restrict__ cbh, int t0, int nt,
+                                            int dk, int s, float* scores) {
     constexpr int SP = E * SDM_WAVE;
+    const int tid = threadIdx.x;
+    const int wave = tid / SDM_WAVE;
+    const int lane = lane_id();
+    // Row of a token: [2][SP], half h's sub-key j at h*SP + j; j in [s, SP) holds -inf.
     if constexpr (MODE == 0) {
-        for (int i = tid; i < AT * 2 * SP; i += blockDim.x) {
+        for (int i = tid; i < nt * 2 * SP; i += blockDim.x) {
             const int tt = i / (2 * SP), half = (i / SP) & 1, j = i % SP;
             const int t = t0 + tt;
-            scores[i] = j >= s ? -INFINITY : (t < te ? to_f32(xs[(size_t)t * dk + half * s + j]) : 0.f);
+            scores[i] = j >= s ? -INFINITY : to_f32(xs[(size_t)t * dk + half * s + j]);
         }
     } else if constexpr (MODE == 1) {
         const int dh = dk / 2;
-        const XT* cbh = cb + (size_t)h * 2 * s * dh;
-        for (int i = tid; i < AT * 2 * SP; i += blockDim.x) {
+        for (int i = tid; i < nt * 2 * SP; i += blockDim.x) {
             const int tt = i / (2 * SP), half = (i / SP) & 1, j = i % SP;
             const int t = t0 + tt;
             float acc = 0.f;
-            if (j < s && t < te) {
+            if (j < s) {
                 const XT* xr = xs + (size_t)t * dk + half * dh;
                 const XT* cr = cbh + ((size_t)half * s + j) * dh;
                 for (int c = 0; c < dh; ++c) acc = fmaf(to_f32(xr[c]), to_f32(cr[c]), acc);
@@ -726,12 +716,11 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __
         // Lane l supplies row/col (l % 16) and k-slice 8*(l/16) .. +7 of each 32-deep step;
         // result acc[v] is D[4*(l/16) + v][l % 16].
         const int dh = dk / 2;
-        const XT* cbh = cb + (size_t)h * 2 * s * dh;
         const int ntile = (s + 15) / 16;
         const int nks = (dh + 31) / 32;   // 32-deep steps (at most MAXKS)
         const int r16 = lane % 16, q = lane / 16;
         const int t = t0 + r16;
-        const bool trow = r16 < AT && t < te;   // this lane's token row exists
+        const bool trow = r16 < nt;   // this lane's token row exists
         if (E <= 4 && nks <= 2) {
             // dh <= 64, s <= 256: this wave's tiles of a half (at most E) need 2 E
             // codebook operands; all are loaded before the first MFMA, so the half
@@ -767,7 +756,7 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __
                     if (j < s) {
 #pragma unroll
                         for (int v = 0; v < 4; ++v)
-                            scores[(size_t)(4 * q + v) * 2 * SP + half * SP + j] = acc[v];
+                            if (4 * q + v < nt) scores[(size_t)(4 * q + v) * 2 * SP + half * SP + j] = acc[v];
                     }
                 }
             }
@@ -799,19 +788,98 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __
                 if (j < s) {
 #pragma unroll
                     for (int v = 0; v < 4; ++v)
-                        if (4 * q + v < AT) scores[(size_t)(4 * q + v) * 2 * SP + half * SP + j] = acc[v];
+                        if (4 * q + v < nt) scores[(size_t)(4 * q + v) * 2 * SP + half * SP + j] = acc[v];
                 }
             }
         }
         if (s < SP) {
             const int pad = SP - s;
-            for (int i = tid; i < AT * 2 * pad; i += blockDim.x)
+            for (int i = tid; i < nt * 2 * pad; i += blockDim.x)
                 scores[(i / pad) * SP + s + i % pad] = -INFINITY;
         }
     }
+}
+
+// Per-wave state of phases B, C: scratch lists and sort buffer, and for the
+// fast path (k <= 32: at most 130 pruned pairs, 3 per lane) the pair ranks;
+// list entries past k hold -inf and pairs past the count point at entry 63.
+struct SelWave {
+    Entry* scr;
+    Entry* listA;
+    Entry* listB;
+    uint64_t* kbuf;
+    uint32_t pi[3], pj[3];
+};
+template <int KM>
+__device__ __forceinline__ void select_init(SelWave& w, Entry* scratch, uint64_t* kbufs, int wave, int k,
+                                            int ncand, const uint16_t* pairs) {
+    const int lane = lane_id();
+    w.scr = scratch + wave * 3 * KM;
+    w.listA = w.scr + KM;
+    w.listB = w.scr + 2 * KM;
+    w.kbuf = kbufs + wave * SDM_WAVE;
+    if constexpr (KM <= MAXK) {
+#pragma unroll
+        for (int e = 0; e < 3; ++e) {
+            const int c = e * SDM_WAVE + lane;
+            const uint32_t pr = c < ncand ? pairs[min(c, ncand - 1)] : ((MAXK - 1u) << 8 | (MAXK - 1u));
+            w.pi[e] = pr >> 8;
+            w.pj[e] = pr & 0xffu;
+        }
+        if (lane >= k) {
+            w.listA[lane] = Entry{-INFINITY, 0};
+            w.listB[lane] = Entry{-INFINITY, 0};
+        }
+    }
+}
+
+// Phases B, C of one token (score row `row`) on this wave: ranked top-k of
+// each half, stage 2, id sort, softmax; k values to io, vo (and so).
+template <int E, int KM>
+__device__ __forceinline__ void select_token(SelWave& w, const float* row, int s, int k, int ncand,
+                                             const uint16_t* pairs, int32_t* io, float* vo, float* so) {
+    constexpr int SP = E * SDM_WAVE;
+    if constexpr (KM > MAXK) {
+        token_big<E>(row, s, SP, k, ncand, pairs, w.scr, w.listA, w.listB, io, vo, so);
+    } else {
+        if constexpr (E <= 4) {
+            if (k <= 32 && k <= s &&
+                token_fast<E>(row, s, k, w.pi, w.pj, w.listA, w.listB, reinterpret_cast<uint2*>(w.kbuf), io, vo,
+                              so))
+                return;
+        }
+        token_general<E>(row, s, SP, k, ncand, pairs, w.scr, w.listA, w.listB, w.kbuf, io, vo, so);
+        wait_lds();
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
+// The tokens [t0, min(t0 + AT, te)) of stream `stream` (AT = atile<E>()), by
+// the AWAVES waves of a workgroup, in the LDS smem (address_lds_bytes): one
+// wave per token in phases B, C.  MODE 0: direct, 1: codebook FMA, 2:
+// codebook MFMA (bf16).
+template <typename XT, int MODE, int E, int KM>
+__device__ __forceinline__ void address_tile(const XT* __restrict__ x, const XT* __restrict__ cb, int H, int T,
+                                             int stream, int t0, int te, int dk, int s, int k,
+                                             int32_t* __restrict__ idx, float* __restrict__ val,
+                                             float* __restrict__ score, unsigned char* smem) {
+    constexpr int AT = atile<E>();
+    constexpr int SP = E * SDM_WAVE;
+    float* scores = reinterpret_cast<float*>(smem);                          // [AT][2][64 E]
+    Entry* scratch = reinterpret_cast<Entry*>(scores + (size_t)AT * 2 * SP);  // [AWAVES][3][KM]
+    uint64_t* kbufs = reinterpret_cast<uint64_t*>(scratch + AWAVES * 3 * KM);  // [AWAVES][64]
+    const int wave = threadIdx.x / SDM_WAVE;
+    const uint16_t* pairs;
+    int ncand;
+    tile_pairs<KM>(k, reinterpret_cast<uint16_t*>(kbufs + AWAVES * SDM_WAVE), pairs, ncand);
+    const XT* cbh = MODE == 0 ? cb : cb + (size_t)(stream % H) * 2 * s * (dk / 2);
+    tile_scores<XT, MODE, E>(x + (size_t)stream * T * dk, cbh, t0, min(AT, te - t0), dk, s, scores);
     __syncthreads();
 
-    // ---- B, C: one wave per token --------------------------------------
+    // ---- B, C: one wave per token (as select_init / select_token, written
+    //      out here: the same code through those helpers spills scalar
+    //      registers in this loop)
+    const int lane = lane_id();
     Entry* scr = scratch + wave * 3 * KM;
     Entry* listA = scr + KM;
     Entry* listB = scr + 2 * KM;
@@ -826,8 +894,6 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __
         }
         return;
     }
-    // fast path: k <= 32, so at most 130 pruned pairs (3 per lane); list
-    // entries past k hold -inf and pairs past the count point at entry 63
     const bool fast = E <= 4 && k <= 32 && k <= s;
     uint32_t pi[3], pj[3];
 #pragma unroll
@@ -858,6 +924,172 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __
         wait_lds();
         __builtin_amdgcn_wave_barrier();
     }
+}
+
+// Grid (tiles of AT tokens of [tb, te), streams).
+template <typename XT, int MODE, int E, int KM>
+__global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __restrict__ x,
+                                                                    const XT* __restrict__ cb, int H, int T,
+                                                                    int tb, int te, int dk, int s, int k,
+                                                                    int32_t* __restrict__ idx,
+                                                                    float* __restrict__ val,
+                                                                    float* __restrict__ score) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    address_tile<XT, MODE, E, KM>(x, cb, H, T, blockIdx.y, tb + blockIdx.x * atile<E>(), te, dk, s, k, idx, val,
+                                  score, smem);
+}
+
+// ---- one token per stream (decode) ----------------------------------------
+// One workgroup per (b, h) stream does the whole layer step for its single
+// token: addressing of the read query and of the write key (their scores as
+// two rows of one tile, then the two selections on two waves at once), then
+// Sec. 3.1 steps 2-3 on every column (Eqs. sdm-decay,
+// sdm-write in the read-back form, sdm-read after the write):
+//   P_n = M[i_n]; D_n = alpha P_n; u = sum_n kappa_n D_n; e = beta (v - u);
+//   M[i_n] = D_n + kappa_n e; y = sum_m rho_m M[j_m].
+// Threads are DEC_RG row groups x 32 column quads, over the columns in chunks
+// of DEC_COLS.  Read rows are loaded with the write rows, before the write; a
+// read row that this token also writes takes the written value instead (the
+// write list is ascending, App. A.2, so its position is a binary search).
+// Every other read row is one this token leaves unchanged.
+constexpr int DEC_RG = 8;                       // row groups
+constexpr int DEC_COLS = 128;                   // columns per chunk: 32 quads
+constexpr int DEC_ROWS = MAXK_BIG / DEC_RG;     // rows per thread, at most
+
+__device__ __forceinline__ float load_scalar(const void* p, int in_dtype, size_t i) {
+    return in_dtype == SDM_DT_BF16 ? to_f32(static_cast<const bf16_t*>(p)[i]) : static_cast<const float*>(p)[i];
+}
+__device__ __forceinline__ v4f load_quad(const void* p, int in_dtype, size_t i) {
+    return in_dtype == SDM_DT_BF16 ? ld4v(static_cast<const bf16_t*>(p) + i) : ld4v(static_cast<const float*>(p) + i);
+}
+
+template <typename XT, int MODE, int E, int KM>
+__global__ __launch_bounds__(AWAVES * SDM_WAVE) void decode_kernel(
+    const XT* __restrict__ q, const XT* __restrict__ kx, const XT* __restrict__ cb_q, const XT* __restrict__ cb_k,
+    int H, int dk, int s, int topk, const void* __restrict__ v, const void* __restrict__ alpha,
+    const void* __restrict__ beta, int in_dtype, float* __restrict__ mem, int64_t N, int dv,
+    int32_t* __restrict__ r_idx, float* __restrict__ r_val, int32_t* __restrict__ w_idx,
+    float* __restrict__ w_val, float* __restrict__ y, unsigned int* __restrict__ flags) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int stream = blockIdx.x;
+    if (stream == 0 && threadIdx.x < 4) flags[threadIdx.x] = 0u;   // the call's device-error words
+    {
+        // both sides at once: score rows 0 (read query) and 1 (write key), then
+        // phases B, C of the two on waves 0 and 1
+        constexpr int AT = atile<E>();
+        constexpr int SP = E * SDM_WAVE;
+        float* scores = reinterpret_cast<float*>(smem);
+        Entry* scratch = reinterpret_cast<Entry*>(scores + (size_t)AT * 2 * SP);
+        uint64_t* kbufs = reinterpret_cast<uint64_t*>(scratch + AWAVES * 3 * KM);
+        const uint16_t* pairs;
+        int ncand;
+        tile_pairs<KM>(topk, reinterpret_cast<uint16_t*>(kbufs + AWAVES * SDM_WAVE), pairs, ncand);
+        const size_t hc = (size_t)(stream % H) * 2 * s * (dk / 2);
+        tile_scores<XT, MODE, E>(q + (size_t)stream * dk, MODE == 0 ? cb_q : cb_q + hc, 0, 1, dk, s, scores);
+        tile_scores<XT, MODE, E>(kx + (size_t)stream * dk, MODE == 0 ? cb_k : cb_k + hc, 0, 1, dk, s,
+                                 scores + 2 * SP);
+        __syncthreads();
+        const int wave = threadIdx.x / SDM_WAVE;
+        if (wave < 2) {
+            SelWave w;
+            select_init<KM>(w, scratch, kbufs, wave, topk, ncand, pairs);
+            const size_t o = (size_t)stream * topk;
+            if (wave == 0)
+                select_token<E, KM>(w, scores, s, topk, ncand, pairs, r_idx + o, r_val + o, nullptr);
+            else
+                select_token<E, KM>(w, scores + 2 * SP, s, topk, ncand, pairs, w_idx + o, w_val + o, nullptr);
+        }
+    }
+    __syncthreads();   // the slot lists in global memory are complete and visible to the workgroup
+
+    const int W = topk, R = topk;
+    const int tid = threadIdx.x, rg = tid / 32, cq = tid % 32;
+    const int32_t* wi = w_idx + (size_t)stream * W;
+    const int32_t* ri = r_idx + (size_t)stream * R;
+    const float* wv = w_val + (size_t)stream * W;
+    const float* rv = r_val + (size_t)stream * R;
+    int* lw = reinterpret_cast<int*>(smem);                          // [MAXK_BIG] write slots
+    float* red = reinterpret_cast<float*>(lw + MAXK_BIG);            // [DEC_RG][DEC_COLS] partial sums
+    float* nrow = red + DEC_RG * DEC_COLS;                           // [W][DEC_COLS] written rows
+    for (int i = tid; i < W; i += blockDim.x) lw[i] = wi[i];
+    __syncthreads();
+
+    int wslot[DEC_ROWS], rslot[DEC_ROWS], link[DEC_ROWS];
+    float kap[DEC_ROWS], rho[DEC_ROWS];
+#pragma unroll
+    for (int j = 0; j < DEC_ROWS; ++j) {
+        const int n = rg + DEC_RG * j;
+        wslot[j] = n < W ? min(max(wi[n], 0), (int)(N - 1)) : 0;
+        kap[j] = n < W ? wv[n] : 0.f;
+        rslot[j] = n < R ? min(max(ri[n], 0), (int)(N - 1)) : 0;
+        rho[j] = n < R ? rv[n] : 0.f;
+        link[j] = -1;
+        if (n < R) {   // position of the read slot in the ascending write list
+            int lo = 0;
+            for (int len = W; len > 1;) {
+                const int half = len >> 1;
+                lo = lw[lo + half] <= rslot[j] ? lo + half : lo;
+                len -= half;
+            }
+            link[j] = lw[lo] == rslot[j] ? lo : -1;
+        }
+    }
+    const float al = load_scalar(alpha, in_dtype, stream), be = load_scalar(beta, in_dtype, stream);
+    float* tab = mem + (size_t)stream * N * dv;
+
+    for (int c0 = 0; c0 < dv; c0 += DEC_COLS) {
+        const int col = c0 + cq * 4;
+        const bool colok = col < dv;      // d_v is a multiple of 4: whole quads
+        const int cl = colok ? col : dv - 4;
+        v4f P[DEC_ROWS], Q[DEC_ROWS];
+#pragma unroll
+        for (int j = 0; j < DEC_ROWS; ++j) {
+            const int n = rg + DEC_RG * j;
+            if (n < W) P[j] = ld4(tab + (size_t)wslot[j] * dv + cl);
+            if (n < R) Q[j] = ld4(tab + (size_t)rslot[j] * dv + cl);
+        }
+        v4f up = v4zero();
+#pragma unroll
+        for (int j = 0; j < DEC_ROWS; ++j)
+            if (rg + DEC_RG * j < W) up = v4fma(kap[j], al * P[j], up);
+        st4(red + rg * DEC_COLS + cq * 4, up);
+        __syncthreads();
+        v4f u = v4zero();
+#pragma unroll
+        for (int g = 0; g < DEC_RG; ++g) u += ld4(red + g * DEC_COLS + cq * 4);
+        const v4f e = be * (load_quad(v, in_dtype, (size_t)stream * dv + cl) - u);
+#pragma unroll
+        for (int j = 0; j < DEC_ROWS; ++j) {
+            const int n = rg + DEC_RG * j;
+            if (n < W) {
+                const v4f nw = v4fma(kap[j], e, al * P[j]);
+                st4(nrow + n * DEC_COLS + cq * 4, nw);
+                if (colok) st4(tab + (size_t)wslot[j] * dv + col, nw);
+            }
+        }
+        __syncthreads();   // written rows in LDS; every thread has read red
+        v4f yp = v4zero();
+#pragma unroll
+        for (int j = 0; j < DEC_ROWS; ++j) {
+            if (rg + DEC_RG * j < R) {
+                const v4f mv = link[j] >= 0 ? ld4(nrow + link[j] * DEC_COLS + cq * 4) : Q[j];
+                yp = v4fma(rho[j], mv, yp);
+            }
+        }
+        st4(red + rg * DEC_COLS + cq * 4, yp);
+        __syncthreads();
+        if (rg == 0 && colok) {
+            v4f yy = v4zero();
+#pragma unroll
+            for (int g = 0; g < DEC_RG; ++g) yy += ld4(red + g * DEC_COLS + cq * 4);
+            st4(y + (size_t)stream * dv + col, yy);
+        }
+        __syncthreads();   // red and nrow are reused by the next chunk
+    }
+}
+
+constexpr size_t decode_scan_lds_bytes(int W) {
+    return (size_t)(MAXK_BIG + DEC_RG * DEC_COLS + (size_t)W * DEC_COLS) * sizeof(float);
 }
 
 // Backward of the weights through softmax and the sub-key scores: one wave
@@ -1063,4 +1295,63 @@ hipError_t sdm_launch_address_bwd(const void* cb, int cb_dtype, int B, int H, in
     else
         launch_address_bwd_t<float>(cb, H, T, tb, tn, dk, s, k, idx, val, dval, dx, ntok, st);
     return hipGetLastError();
+}
+
+namespace {
+template <typename XT, int MODE>
+hipError_t launch_decode_m(const void* q, const void* k, const void* cb_q, const void* cb_k, int B, int H,
+                           int dk, int s, int topk, const void* v, const void* alpha, const void* beta,
+                           int in_dtype, float* mem, int64_t N, int dv, int32_t* r_idx, float* r_val,
+                           int32_t* w_idx, float* w_val, float* y, unsigned int* flags, hipStream_t st) {
+    const int E = (s + SDM_WAVE - 1) / SDM_WAVE;
+    const XT* qp = static_cast<const XT*>(q);
+    const XT* kp = static_cast<const XT*>(k);
+    const XT* cq = static_cast<const XT*>(cb_q);
+    const XT* ck = static_cast<const XT*>(cb_k);
+#define SDM_DEC_CASE(EE, KM)                                                                              \
+    {                                                                                                     \
+        const size_t sm = std::max(address_lds_bytes(EE, atile<EE>(), KM), decode_scan_lds_bytes(topk)); \
+        auto kfn = decode_kernel<XT, MODE, EE, KM>;                                                       \
+        hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize,  \
+                                           (int)sm);                                                      \
+        if (e != hipSuccess) return e;                                                                    \
+        hipLaunchKernelGGL(kfn, dim3(B * H), dim3(AWAVES * SDM_WAVE), sm, st, qp, kp, cq, ck, H, dk, s,   \
+                           topk, v, alpha, beta, in_dtype, mem, N, dv, r_idx, r_val, w_idx, w_val, y, flags); \
+        return hipGetLastError();                                                                         \
+    }
+    if (topk > MAXK) {   // topk <= sqrt(N), so E >= 2
+        if (E <= 2) SDM_DEC_CASE(2, MAXK_BIG)
+        if (E <= 4) SDM_DEC_CASE(4, MAXK_BIG)
+        if (E <= 8) SDM_DEC_CASE(8, MAXK_BIG)
+        SDM_DEC_CASE(16, MAXK_BIG)
+    }
+    if (E <= 1) SDM_DEC_CASE(1, MAXK)
+    if (E <= 2) SDM_DEC_CASE(2, MAXK)
+    if (E <= 4) SDM_DEC_CASE(4, MAXK)
+    if (E <= 8) SDM_DEC_CASE(8, MAXK)
+    SDM_DEC_CASE(16, MAXK)
+#undef SDM_DEC_CASE
+}
+}  // namespace
+
+hipError_t sdm_launch_decode(const void* q, const void* k, int x_dtype, const void* cb_q, const void* cb_k, int B,
+                             int H, int dk, int s, int topk, const void* v, const void* alpha, const void* beta,
+                             int in_dtype, float* mem, int64_t N, int dv, int32_t* r_idx, float* r_val,
+                             int32_t* w_idx, float* w_val, float* y, unsigned int* flags, hipStream_t st) {
+    if (B * H == 0) return hipSuccess;
+    if (x_dtype == SDM_DT_BF16) {
+        if (!cb_q)
+            return launch_decode_m<bf16_t, 0>(q, k, cb_q, cb_k, B, H, dk, s, topk, v, alpha, beta, in_dtype, mem,
+                                              N, dv, r_idx, r_val, w_idx, w_val, y, flags, st);
+        if ((dk / 2) % 8 == 0)
+            return launch_decode_m<bf16_t, 2>(q, k, cb_q, cb_k, B, H, dk, s, topk, v, alpha, beta, in_dtype, mem,
+                                              N, dv, r_idx, r_val, w_idx, w_val, y, flags, st);
+        return launch_decode_m<bf16_t, 1>(q, k, cb_q, cb_k, B, H, dk, s, topk, v, alpha, beta, in_dtype, mem, N,
+                                          dv, r_idx, r_val, w_idx, w_val, y, flags, st);
+    }
+    if (!cb_q)
+        return launch_decode_m<float, 0>(q, k, cb_q, cb_k, B, H, dk, s, topk, v, alpha, beta, in_dtype, mem, N,
+                                         dv, r_idx, r_val, w_idx, w_val, y, flags, st);
+    return launch_decode_m<float, 1>(q, k, cb_q, cb_k, B, H, dk, s, topk, v, alpha, beta, in_dtype, mem, N, dv,
+                                     r_idx, r_val, w_idx, w_val, y, flags, st);
 }

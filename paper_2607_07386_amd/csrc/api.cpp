@@ -372,6 +372,17 @@ int sdm_forward(const void* q, const void* k, int x_dtype, const void* cb_q, con
                              ws_bytes);
     if (rc != SDM_OK) return rc;
 
+    hipStream_t st = (hipStream_t)stream;
+    // one token without an undo log, both sides in the same addressing mode:
+    // addressing and the scan step in one launch
+    if (T == 1 && !saved && (cb_q == nullptr) == (cb_k == nullptr)) {
+        SdmProfScope ps(SDM_K_DECODE, st);
+        hipError_t e = sdm_launch_decode(q, k, x_dtype, cb_q, cb_k, B, H, d_k, s, topk, v, alpha, beta, in_dtype,
+                                         mem, N, d_v, r_idx, r_val, w_idx, w_val, y,
+                                         static_cast<unsigned int*>(workspace), st);
+        return e == hipSuccess ? SDM_OK : hip_fail(e, "sdm_forward single-token launch");
+    }
+
     // pipeline stages: a short first stage (a quarter of the stage length; its
     // addressing cannot overlap anything), then stages of len tokens; all
     // multiples of 64 tokens, at most kMaxChunks of them
@@ -384,7 +395,6 @@ int sdm_forward(const void* q, const void* k, int x_dtype, const void* cb_q, con
     }
     auto stage_begin = [&](int c) { return c == 0 ? 0 : std::min(T, first + (c - 1) * len); };
 
-    hipStream_t st = (hipStream_t)stream;
     hipError_t e = sdm_launch_zero_words(workspace, 4, st);
     if (e != hipSuccess) return hip_fail(e, "sdm_forward flag reset");
     ScanFwdArgs a;

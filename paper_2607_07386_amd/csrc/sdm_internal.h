@@ -62,6 +62,13 @@ hipError_t sdm_launch_address(const void* x, int x_dtype, const void* cb, int B,
                               int tb, int tn, int dk, int s, int k, int32_t* idx, float* val,
                               float* score, hipStream_t st);
 // token-sides (b, h, t) for t in [tb, tb + tn)
+// One token per stream (T = 1, no undo log): addressing of both sides and the
+// scan step in one launch, one workgroup per stream.  cb_q and cb_k are both
+// codebooks or both NULL (direct mode).
+hipError_t sdm_launch_decode(const void* q, const void* k, int x_dtype, const void* cb_q, const void* cb_k, int B,
+                             int H, int dk, int s, int topk, const void* v, const void* alpha, const void* beta,
+                             int in_dtype, float* mem, int64_t N, int dv, int32_t* r_idx, float* r_val,
+                             int32_t* w_idx, float* w_val, float* y, unsigned int* flags, hipStream_t st);
 hipError_t sdm_launch_address_bwd(const void* cb, int cb_dtype, int B, int H, int T, int tb, int tn, int dk,
                                   int s, int k, const int32_t* idx, const float* val, const float* dval,
                                   float* dx, hipStream_t st);

@@ -258,7 +258,7 @@ def check_device_errors(workspace: torch.Tensor):
 
 
 KERNELS = {"address": 0, "fwd_prep": 1, "fwd_scan": 2, "bwd_prep": 3, "bwd_scan": 4, "bwd_reduce": 5,
-           "address_bwd": 6, "mem_init": 7}
+           "address_bwd": 6, "mem_init": 7, "decode": 8}
 
 
 def set_scan_slice_width(sw: int):
