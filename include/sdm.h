@@ -267,6 +267,10 @@ enum sdm_kernel {
     SDM_K_DECODE = 8, SDM_K_COUNT = 9
 };
 int sdm_profile_enable(int on);
+/* Which kernel kinds the events bracket while profiling is enabled: bit k for
+ * enum sdm_kernel k (all by default).  Fewer events disturb a pipelined call
+ * less.  Bits past SDM_K_COUNT return SDM_ERR_INVALID_ARG. */
+int sdm_profile_select(unsigned int mask);
 int sdm_profile_read(int kernel, double* total_ms, int64_t* launches);
 
 /* ------------------------------------------------------------------------

@@ -93,6 +93,7 @@ int check_scan_common(const int32_t* w_idx, const float* w_val, int W, const int
 struct ProfState {
     std::mutex mu;
     bool on = false;
+    unsigned int mask = (1u << SDM_K_COUNT) - 1;   // kernel kinds timed while on
     std::vector<hipEvent_t> pool;                 // free events
     std::vector<std::pair<hipEvent_t, hipEvent_t>> done[SDM_K_COUNT];
     hipEvent_t open_ev[SDM_K_COUNT] = {};
@@ -116,7 +117,7 @@ hipEvent_t take_event(ProfState& p) {
 
 void sdm_prof_begin(int k, hipStream_t st) {
     ProfState& p = prof();
-    if (!p.on) return;
+    if (!p.on || !(p.mask >> k & 1u)) return;
     std::lock_guard<std::mutex> g(p.mu);
     hipEvent_t e = take_event(p);
     if (e && hipEventRecord(e, st) == hipSuccess) p.open_ev[k] = e;
@@ -124,7 +125,7 @@ void sdm_prof_begin(int k, hipStream_t st) {
 
 void sdm_prof_end(int k, hipStream_t st) {
     ProfState& p = prof();
-    if (!p.on) return;
+    if (!p.on || !(p.mask >> k & 1u)) return;
     std::lock_guard<std::mutex> g(p.mu);
     hipEvent_t b = p.open_ev[k];
     p.open_ev[k] = nullptr;
@@ -254,6 +255,15 @@ int sdm_profile_enable(int on) {
         p.done[k].clear();
     }
     p.on = on != 0;
+    return SDM_OK;
+}
+
+int sdm_profile_select(unsigned int mask) {
+    g_err[0] = 0;
+    if (mask >> SDM_K_COUNT) return fail(SDM_ERR_INVALID_ARG, "sdm_profile_select: unknown kernel kinds in 0x%x", mask);
+    ProfState& p = prof();
+    std::lock_guard<std::mutex> g(p.mu);
+    p.mask = mask;
     return SDM_OK;
 }
 

@@ -55,6 +55,7 @@ def lib() -> ctypes.CDLL:
             getattr(L, f).restype = SZ
         L.sdm_check_device_errors.argtypes = [P, P]
         L.sdm_profile_enable.argtypes = [I]
+        L.sdm_profile_select.argtypes = [ctypes.c_uint]
         L.sdm_set_scan_slice_width.argtypes = [I]
         L.sdm_set_scan_line_io.argtypes = [I]
         L.sdm_profile_read.argtypes = [I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
@@ -63,7 +64,7 @@ def lib() -> ctypes.CDLL:
         L.sdm_last_error.restype = ctypes.c_char_p
         L.sdm_version.restype = ctypes.c_char_p
         for f in ("sdm_address", "sdm_scan_fwd", "sdm_scan_bwd", "sdm_mem_init", "sdm_check_device_errors",
-                  "sdm_profile_enable", "sdm_profile_read"):
+                  "sdm_profile_enable", "sdm_profile_select", "sdm_profile_read"):
             getattr(L, f).restype = I
         _lib = L
     return _lib
@@ -274,6 +275,12 @@ def set_scan_line_io(on: bool):
 def profile_enable(on: bool = True):
     """Start (or stop) HIP-event timing of every kernel the library launches; clears totals."""
     _check("sdm_profile_enable", lib().sdm_profile_enable(int(on)))
+
+
+def profile_select(kernels=None):
+    """Time only these kernel kinds (names of KERNELS) while profiling is on; None: all."""
+    mask = (1 << len(KERNELS)) - 1 if kernels is None else sum(1 << KERNELS[k] for k in kernels)
+    _check("sdm_profile_select", lib().sdm_profile_select(mask))
 
 
 def profile_read(kernel: str):

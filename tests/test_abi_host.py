@@ -122,6 +122,14 @@ def test_scan_line_io_setting():
     assert L.sdm_set_scan_line_io(1) == 0
 
 
+def test_profile_select():
+    assert L.sdm_profile_select(1 << 2) == 0
+    assert L.sdm_profile_select((1 << 9) - 1) == 0
+    assert L.sdm_profile_select(1 << 9) == -1
+    assert b"unknown kernel kinds" in L.sdm_last_error()
+    assert L.sdm_profile_select((1 << 9) - 1) == 0
+
+
 def test_mem_init_validation():
     assert L.sdm_mem_init(None, None, 1, 1, 16, 4, None) == -1
     assert L.sdm_mem_init(A, None, 1, 1, 16, 6, None) == -1
