@@ -227,7 +227,9 @@ int sdm_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int d_v, 
  * of columns of one (b, h) stream.  sdm_set_scan_slice_width(sw):
  *   0   automatic (default): 8 columns per wave, unless B*H*ceil(d_v/8)
  *       waves would put 1.5 or more on every SIMD of the device: then 16 (half
- *       as many waves); 8 as well where 16 columns cannot hold W or R (> 64);
+ *       as many waves); 8 as well where 16 columns cannot hold W or R (> 64),
+ *       and for the forward's line-cooperative kernel at W = R = 64 (whose
+ *       16-column form holds most of a CU's LDS);
  *   8, 16  force that width.
  * Process-wide; applies to launches that start after the call.  Results of
  * the two widths agree to the rounding of the sums over rows.  Any other

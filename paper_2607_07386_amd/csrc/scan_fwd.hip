@@ -257,14 +257,14 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_fwd_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Line-cooperative variant (W = R = 32, d_v a multiple of 4 SW).
+// Line-cooperative variant (W = R = FR, 32 or 64; d_v a multiple of 4 SW).
 //
 // The four waves of a workgroup are four adjacent SW-column slices of one
 // stream (4 SW columns: a 128-byte line of every table row at SW = 8, two at
 // SW = 16).  Moving only its own SW columns of each row, a wave touches a
 // line in pieces at times of its own and the rows are served more slowly
 // than when whole lines move together, so table rows go through LDS: each
-// wave loads and stores 8 of a token's 32 rows over all 4 SW columns, and the
+// wave loads and stores FR / 4 of a token's FR rows over all 4 SW columns, and the
 // waves exchange their pieces in LDS, with two workgroup barriers per token.
 // The recurrence (links, the written-row ring, the per-token arithmetic) is
 // that of scan_fwd_kernel, per wave and slice.
@@ -276,36 +276,35 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_fwd_kernel(
 //   S3  each wave computes its pieces; written rows (and, when saving, the
 //       pre-write rows) -> LDS staging buffer; y of its columns -> HBM
 //   B2
-//   S4  each wave stores 8 staged rows as whole lines
+//   S4  each wave stores FR / 4 staged rows as whole lines
 // A load issued in S2 sees the stores of tokens <= t - 1 (every wave stored
 // those before B1); the tokens t .. t + PD - 2 it cannot see are the PD - 1
 // writers the prep kernel links to the ring, as for the per-wave kernel.
 // One ring of records serves the four waves (they read the same records),
 // which keeps LDS low enough for an addressing workgroup to share the CU.
 constexpr int FLW = 4;       // waves (slices) per workgroup
-constexpr int FROWS = 32;    // W = R
 template <int SW>
 __host__ __device__ constexpr int frow_bytes() { return 20 * SW; }   // 16 SW of line + 4 SW of padding
-template <int SW>
+template <int SW, int FR>
 constexpr int fline_shared_bytes(bool save, int ns, int rec_bytes) {
-    return ns * rec_bytes + (2 + (save ? 2 : 1)) * FROWS * frow_bytes<SW>();
+    return ns * rec_bytes + (2 + (save ? 2 : 1)) * FR * frow_bytes<SW>();
 }
 
-template <int SW>
+template <int SW, int FR>
 __device__ __forceinline__ v4f fl_ld(const unsigned char* base, int a, int r, int q) {
-    return *reinterpret_cast<const v4f*>(base + (a * FROWS + r) * frow_bytes<SW>() + q * 16);
+    return *reinterpret_cast<const v4f*>(base + (a * FR + r) * frow_bytes<SW>() + q * 16);
 }
-template <int SW>
+template <int SW, int FR>
 __device__ __forceinline__ void fl_st(unsigned char* base, int a, int r, int q, v4f v) {
-    *reinterpret_cast<v4f*>(base + (a * FROWS + r) * frow_bytes<SW>() + q * 16) = v;
+    *reinterpret_cast<v4f*>(base + (a * FR + r) * frow_bytes<SW>() + q * 16) = v;
 }
 
-// Rows per wave in line layout: instruction i covers rows 8 w + LRI i + lane / LQ.
-template <int SW>
+// Rows per wave in line layout: instruction i covers rows (FR / 4) w + LRI i + lane / LQ.
+template <int SW, int FR>
 struct FLine {
     static constexpr int LQ = SW;            // 16-byte quads per staged row (4 SW columns)
     static constexpr int LRI = SDM_WAVE / LQ;
-    static constexpr int NLI = 8 / LRI;
+    static constexpr int NLI = FR / FLW / LRI;
     v4f Pw[NLI], Pr[NLI];
 };
 
@@ -317,9 +316,10 @@ struct FLinePtrs {
 };
 
 // Staging of G records, shared by the workgroup: wave w moves 16-byte chunks
-// w 64 + lane (one per lane covers G records up to 4 KB); v slices per wave.
-template <typename VT, int SW>
-__device__ __forceinline__ void fl_stage_load(u4v& st, u2v& stv, const unsigned char* srec, const VT* sv,
+// w 64 + lane + 256 j, j < NC (NC chunks per lane cover G records up to NC 4
+// KB); v slices per wave.
+template <typename VT, int SW, int NC>
+__device__ __forceinline__ void fl_stage_load(u4v (&st)[NC], u2v& stv, const unsigned char* srec, const VT* sv,
                                               int u0, int te, int dv, int slice, int rec_bytes, int w,
                                               int lane) {
     constexpr int VB = SW * (int)sizeof(VT);
@@ -327,43 +327,48 @@ __device__ __forceinline__ void fl_stage_load(u4v& st, u2v& stv, const unsigned 
     const int ub = min(u0, te - 1);
     const int cnt = min(G, te - ub);
     const u4v* src = reinterpret_cast<const u4v*>(srec + (size_t)ub * rec_bytes);
-    st = src[min(w * SDM_WAVE + lane, cnt * rec_bytes / 16 - 1)];
+#pragma unroll
+    for (int j = 0; j < NC; ++j)
+        st[j] = src[min(w * SDM_WAVE + lane + j * FLW * SDM_WAVE, cnt * rec_bytes / 16 - 1)];
     const int tk = min(lane / ppt, cnt - 1);
     const int pc = min(lane % ppt, (dv - slice * SW) * (int)sizeof(VT) / 8 - 1);
     stv = *reinterpret_cast<const u2v*>(
         reinterpret_cast<const unsigned char*>(sv + (size_t)(ub + tk) * dv) + pc * 8);
 }
-template <typename VT, int SW, int NS>
-__device__ __forceinline__ void fl_stage_store(u4v st, u2v stv, unsigned char* rring, unsigned char* vring,
-                                               int u0, int rec_bytes, int w, int lane) {
+template <typename VT, int SW, int NS, int NC>
+__device__ __forceinline__ void fl_stage_store(const u4v (&st)[NC], u2v stv, unsigned char* rring,
+                                               unsigned char* vring, int u0, int rec_bytes, int w, int lane) {
     constexpr int VB = SW * (int)sizeof(VT);
     constexpr int ppt = VB / 8;
-    const int c = w * SDM_WAVE + lane;
-    if (c < G * rec_bytes / 16) reinterpret_cast<u4v*>(rring + (u0 & (NS - 1)) * rec_bytes)[c] = st;
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+        const int c = w * SDM_WAVE + lane + j * FLW * SDM_WAVE;
+        if (c < G * rec_bytes / 16) reinterpret_cast<u4v*>(rring + (u0 & (NS - 1)) * rec_bytes)[c] = st[j];
+    }
     const int tk = lane / ppt, pc = lane % ppt;
     if (tk < G) *reinterpret_cast<u2v*>(vring + ((u0 + tk) & (NS - 1)) * VB + pc * 8) = stv;
 }
 
-template <int SW, int NS>
-__device__ __forceinline__ void fl_issue(FLine<SW>& b, const unsigned char* rring, const FwdRec& L,
+template <int SW, int NS, int FR>
+__device__ __forceinline__ void fl_issue(FLine<SW, FR>& b, const unsigned char* rring, const FwdRec& L,
                                          const FLinePtrs<SW>& p, int u, int dv) {
     const unsigned char* rec = rring + (u & (NS - 1)) * L.bytes;
 #pragma unroll
-    for (int i = 0; i < FLine<SW>::NLI; ++i) {
-        const int r = p.r0 + FLine<SW>::LRI * i;
+    for (int i = 0; i < FLine<SW, FR>::NLI; ++i) {
+        const int r = p.r0 + FLine<SW, FR>::LRI * i;
         b.Pw[i] = ld4(p.tab + (size_t)reinterpret_cast<const int*>(rec)[r] * dv);
         b.Pr[i] = ld4(p.tab + (size_t)reinterpret_cast<const int*>(rec + L.off_rslot)[r] * dv);
     }
 }
 
 // One token on this wave's pieces (rows rg + RG k, columns 4 cq.. of slice w).
-template <typename VT, int SW, int PD, bool SAVE, int NS>
+template <typename VT, int SW, int PD, bool SAVE, int NS, int FR>
 __device__ __forceinline__ void fwd_token_line(const FwdCtx<VT, SW, PD, 2, SAVE>& c, const unsigned char* lb,
                                                unsigned char* sb, int t, int w) {
     using namespace sdm_reduce;
     constexpr int CQ = SW / 4;
     constexpr int RG = SDM_WAVE / CQ;
-    constexpr int K = FROWS / RG;
+    constexpr int K = FR / RG;
     constexpr int VB = SW * (int)sizeof(VT);
     const FwdRec& L = c.L;
     const int q = w * CQ + c.cq;
@@ -379,10 +384,10 @@ __device__ __forceinline__ void fwd_token_line(const FwdCtx<VT, SW, PD, 2, SAVE>
     for (int k = 0; k < K; ++k) {
         const int n = c.rg + RG * k;
         const int l = lk[n];
-        const int fidx = l >= 0 ? (((t - (l >> 8)) & (PD - 1)) * FROWS + min(l & 255, FROWS - 1)) : 0;
-        const v4f P = v4sel(l >= 0, ld4(c.fring + fidx * SW + c.cq * 4), fl_ld<SW>(lb, 0, n, q));
+        const int fidx = l >= 0 ? (((t - (l >> 8)) & (PD - 1)) * FR + min(l & 255, FR - 1)) : 0;
+        const v4f P = v4sel(l >= 0, ld4(c.fring + fidx * SW + c.cq * 4), fl_ld<SW, FR>(lb, 0, n, q));
         kap[k] = reinterpret_cast<const float*>(rec + L.off_wval)[n];
-        if (SAVE) fl_st<SW>(sb, 1, n, q, P);
+        if (SAVE) fl_st<SW, FR>(sb, 1, n, q, P);
         D[k] = al * P;
         up = v4fma(kap[k], D[k], up);
     }
@@ -393,27 +398,27 @@ __device__ __forceinline__ void fwd_token_line(const FwdCtx<VT, SW, PD, 2, SAVE>
     for (int k = 0; k < K; ++k) {
         const int n = c.rg + RG * k;
         const v4f nw = v4fma(kap[k], e, D[k]);
-        st4(c.fring + ((t & (PD - 1)) * FROWS + n) * SW + c.cq * 4, nw);
-        fl_st<SW>(sb, 0, n, q, nw);
+        st4(c.fring + ((t & (PD - 1)) * FR + n) * SW + c.cq * 4, nw);
+        fl_st<SW, FR>(sb, 0, n, q, nw);
     }
     v4f yp = v4zero();
 #pragma unroll
     for (int k = 0; k < K; ++k) {
         const int m = c.rg + RG * k;
-        const int l = lk[FROWS + m];
-        const int fidx = l >= 0 ? (((t - (l >> 8)) & (PD - 1)) * FROWS + min(l & 255, FROWS - 1)) : 0;
-        const v4f P = v4sel(l >= 0, ld4(c.fring + fidx * SW + c.cq * 4), fl_ld<SW>(lb, 1, m, q));
+        const int l = lk[FR + m];
+        const int fidx = l >= 0 ? (((t - (l >> 8)) & (PD - 1)) * FR + min(l & 255, FR - 1)) : 0;
+        const v4f P = v4sel(l >= 0, ld4(c.fring + fidx * SW + c.cq * 4), fl_ld<SW, FR>(lb, 1, m, q));
         yp = v4fma(reinterpret_cast<const float*>(rec + L.off_rval)[m], P, yp);
     }
     rows_allreduce4<CQ>(yp);
     if (c.rg == 0) st4(c.ystream + (size_t)t * c.dv, yp);
 }
 
-template <typename VT, int SW, int PD, bool SAVE, int NS>
+template <typename VT, int SW, int PD, bool SAVE, int NS, int FR>
 __device__ __forceinline__ void fl_step(const FwdCtx<VT, SW, PD, 2, SAVE>& c, const FLinePtrs<SW>& p,
-                                        unsigned char* lb, unsigned char* sb, const FLine<SW>& cur,
-                                        FLine<SW>& nxt, int t, int te, int w, bool issue) {
-    constexpr int NLI = FLine<SW>::NLI, LRI = FLine<SW>::LRI;
+                                        unsigned char* lb, unsigned char* sb, const FLine<SW, FR>& cur,
+                                        FLine<SW, FR>& nxt, int t, int te, int w, bool issue) {
+    constexpr int NLI = FLine<SW, FR>::NLI, LRI = FLine<SW, FR>::LRI;
     const FwdRec& L = c.L;
     int wslot[NLI];
     const unsigned char* rec = c.rring + (t & (NS - 1)) * L.bytes;
@@ -421,23 +426,23 @@ __device__ __forceinline__ void fl_step(const FwdCtx<VT, SW, PD, 2, SAVE>& c, co
     for (int i = 0; i < NLI; ++i) wslot[i] = reinterpret_cast<const int*>(rec)[p.r0 + LRI * i];
 #pragma unroll
     for (int i = 0; i < NLI; ++i) {
-        fl_st<SW>(lb, 0, p.r0 + LRI * i, p.lq, cur.Pw[i]);
-        fl_st<SW>(lb, 1, p.r0 + LRI * i, p.lq, cur.Pr[i]);
+        fl_st<SW, FR>(lb, 0, p.r0 + LRI * i, p.lq, cur.Pw[i]);
+        fl_st<SW, FR>(lb, 1, p.r0 + LRI * i, p.lq, cur.Pr[i]);
     }
     __syncthreads();
     // every wave stored token t - 1 before the barrier: the loads may go now
-    if (issue) fl_issue<SW, NS>(nxt, c.rring, L, p, min(t + PD - 1, te - 1), c.dv);
-    fwd_token_line<VT, SW, PD, SAVE, NS>(c, lb, sb, t, w);
+    if (issue) fl_issue<SW, NS, FR>(nxt, c.rring, L, p, min(t + PD - 1, te - 1), c.dv);
+    fwd_token_line<VT, SW, PD, SAVE, NS, FR>(c, lb, sb, t, w);
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < NLI; ++i) {
         const int r = p.r0 + LRI * i;
-        st4(p.tab + (size_t)wslot[i] * c.dv, fl_ld<SW>(sb, 0, r, p.lq));
-        if (SAVE) st4(p.sv + ((size_t)t * FROWS + r) * c.dv, fl_ld<SW>(sb, 1, r, p.lq));
+        st4(p.tab + (size_t)wslot[i] * c.dv, fl_ld<SW, FR>(sb, 0, r, p.lq));
+        if (SAVE) st4(p.sv + ((size_t)t * FR + r) * c.dv, fl_ld<SW, FR>(sb, 1, r, p.lq));
     }
 }
 
-template <typename VT, int SW, int PD, bool SAVE>
+template <typename VT, int SW, int PD, bool SAVE, int FR>
 __global__ __launch_bounds__(FLW * SDM_WAVE) void scan_fwd_line_kernel(
     const unsigned char* __restrict__ recs, const VT* __restrict__ v, float* __restrict__ mem,
     float* __restrict__ y, float* __restrict__ saved, int T, int tb, int te, int dv, int64_t N,
@@ -450,7 +455,9 @@ __global__ __launch_bounds__(FLW * SDM_WAVE) void scan_fwd_line_kernel(
     // the block staged at step t (tokens t+LEAD-G .. t+LEAD-1) reuses only slots of
     // tokens already done, while tokens t .. t+LEAD-G-1 stay: NS >= LEAD suffices
     static_assert(NS >= LEAD && NS >= PD, "record ring too small");
-    static_assert(FLine<SW>::NLI * FLine<SW>::LRI == 8, "8 rows per wave");
+    static_assert(FLine<SW, FR>::NLI * FLine<SW, FR>::LRI * FLW == FR, "FR / 4 rows per wave");
+    // records of G tokens in NC 16-byte chunks per lane of the workgroup
+    constexpr int NC = (G * ((20 * FR + 8 + 15) / 16 * 16) + FLW * SDM_WAVE * 16 - 1) / (FLW * SDM_WAVE * 16);
 
     // In the pipelined forward the next stage's addressing and records share the
     // CUs; the scan waves are latency-bound and go first at each issue slot
@@ -463,10 +470,10 @@ __global__ __launch_bounds__(FLW * SDM_WAVE) void scan_fwd_line_kernel(
     const int slice = group * FLW + w;   // n_slices is a multiple of FLW: every wave exists
 
     FwdCtx<VT, SW, PD, 2, SAVE> c;
-    c.L = fwd_rec_layout(FROWS, FROWS);
+    c.L = fwd_rec_layout(FR, FR);
     c.dv = dv;
-    c.W = FROWS;
-    c.R = FROWS;
+    c.W = FR;
+    c.R = FR;
     c.rg = lane / CQ;
     c.cq = lane % CQ;
     c.colok = true;
@@ -475,8 +482,8 @@ __global__ __launch_bounds__(FLW * SDM_WAVE) void scan_fwd_line_kernel(
     extern __shared__ __align__(16) unsigned char smem[];
     unsigned char* rring = smem;                                   // NS records, shared
     unsigned char* lb = rring + NS * c.L.bytes;                    // [2][32] rows
-    unsigned char* sb = lb + 2 * FROWS * frow_bytes<SW>();         // [1 or 2][32] rows
-    unsigned char* own = sb + (SAVE ? 2 : 1) * FROWS * frow_bytes<SW>() + (size_t)w * per_wave_lds;
+    unsigned char* sb = lb + 2 * FR * frow_bytes<SW>();         // [1 or 2][FR] rows
+    unsigned char* own = sb + (SAVE ? 2 : 1) * FR * frow_bytes<SW>() + (size_t)w * per_wave_lds;
     unsigned char* vring = own;                                    // NS v slices of this wave
     c.rring = rring;
     c.vring = vring;
@@ -486,26 +493,26 @@ __global__ __launch_bounds__(FLW * SDM_WAVE) void scan_fwd_line_kernel(
     c.sstream = nullptr;
 
     FLinePtrs<SW> p;
-    p.r0 = 8 * w + lane / FLine<SW>::LQ;
-    p.lq = lane % FLine<SW>::LQ;
+    p.r0 = FR / FLW * w + lane / FLine<SW, FR>::LQ;
+    p.lq = lane % FLine<SW, FR>::LQ;
     const size_t lcol = (size_t)group * FLW * SW + p.lq * 4;
     p.tab = mem + (size_t)stream * N * dv + lcol;
-    p.sv = SAVE ? saved + (size_t)stream * T * FROWS * dv + lcol : nullptr;
+    p.sv = SAVE ? saved + (size_t)stream * T * FR * dv + lcol : nullptr;
 
     const unsigned char* srec = recs + (size_t)stream * T * c.L.bytes;
     const VT* sv = v + (size_t)stream * T * dv + slice * SW;
-    u4v st;
+    u4v st[NC];
     u2v stv;
-    FLine<SW> buf[PD];
+    FLine<SW, FR> buf[PD];
 
     for (int u0 = tb; u0 < tb + LEAD - G; u0 += G) {
-        fl_stage_load<VT, SW>(st, stv, srec, sv, u0, te, dv, slice, c.L.bytes, w, lane);
-        fl_stage_store<VT, SW, NS>(st, stv, rring, vring, u0, c.L.bytes, w, lane);
+        fl_stage_load<VT, SW, NC>(st, stv, srec, sv, u0, te, dv, slice, c.L.bytes, w, lane);
+        fl_stage_store<VT, SW, NS, NC>(st, stv, rring, vring, u0, c.L.bytes, w, lane);
     }
-    fl_stage_load<VT, SW>(st, stv, srec, sv, tb + LEAD - G, te, dv, slice, c.L.bytes, w, lane);
+    fl_stage_load<VT, SW, NC>(st, stv, srec, sv, tb + LEAD - G, te, dv, slice, c.L.bytes, w, lane);
     __syncthreads();   // records of the first tokens from every wave
 #pragma unroll
-    for (int j = 0; j < PD - 1; ++j) fl_issue<SW, NS>(buf[j], rring, c.L, p, min(tb + j, te - 1), dv);
+    for (int j = 0; j < PD - 1; ++j) fl_issue<SW, NS, FR>(buf[j], rring, c.L, p, min(tb + j, te - 1), dv);
 
     // Token t = t0 + j uses buf[j]; its step loads token t + PD - 1 into
     // buf[(j + PD - 1) % PD], the buffer token t - 1 used.
@@ -515,16 +522,16 @@ __global__ __launch_bounds__(FLW * SDM_WAVE) void scan_fwd_line_kernel(
         for (int j = 0; j < PD; ++j) {
             const int t = t0 + j;
             if (j % G == 0) {
-                fl_stage_store<VT, SW, NS>(st, stv, rring, vring, t + LEAD - G, c.L.bytes, w, lane);
-                fl_stage_load<VT, SW>(st, stv, srec, sv, t + LEAD, te, dv, slice, c.L.bytes, w, lane);
+                fl_stage_store<VT, SW, NS, NC>(st, stv, rring, vring, t + LEAD - G, c.L.bytes, w, lane);
+                fl_stage_load<VT, SW, NC>(st, stv, srec, sv, t + LEAD, te, dv, slice, c.L.bytes, w, lane);
             }
-            fl_step<VT, SW, PD, SAVE, NS>(c, p, lb, sb, buf[j], buf[(j + PD - 1) % PD], t, te, w, true);
+            fl_step<VT, SW, PD, SAVE, NS, FR>(c, p, lb, sb, buf[j], buf[(j + PD - 1) % PD], t, te, w, true);
         }
     }
 #pragma unroll
     for (int j = 0; j < PD; ++j) {
         const int t = Tfull + j;
-        if (t < te) fl_step<VT, SW, PD, SAVE, NS>(c, p, lb, sb, buf[j], buf[(j + PD - 1) % PD], t, te, w, false);
+        if (t < te) fl_step<VT, SW, PD, SAVE, NS, FR>(c, p, lb, sb, buf[j], buf[(j + PD - 1) % PD], t, te, w, false);
     }
 }
 
@@ -571,32 +578,40 @@ bool fwd_plan_sw(int W, int R, int dv, int in_dtype, FwdPlan* p) {
 // per-wave scan at 1920 such waves fetched three times its bytes and ran at
 // half the speed of 960 16-column waves.  The other width is taken when the
 // chosen one cannot hold the shape (16 columns hold at most 64 rows).
+//
+// Except, when the width is automatic, for the line-cooperative kernel at
+// W = R = 64: at 16 columns it holds 137-155 KB of a CU's 160 KB of LDS, so the
+// addressing that sdm_forward runs beside the scan is left the CUs without a
+// scan workgroup.  The 8-column line kernel takes half that LDS and moves whole
+// lines, so the many-waves penalty above does not apply: at 16 streams with
+// d_v = 960 it measured 10.3 ms per forward step against 10.7 ms (13.1 against
+// 14.1 with the undo log).
 bool fwd_plan(int S, int W, int R, int dv, int in_dtype, FwdPlan* p) {
     const int forced = sdm_scan_slice_width();
-    if (forced == 16 || (forced == 0 && 2 * (int64_t)S * ((dv + 7) / 8) >= 3 * (int64_t)sdm_device_simds()))
+    const bool line64 = W == 64 && R == 64 && sdm_line_io_enabled() && dv % (FLW * 8) == 0;
+    if (forced == 16 ||
+        (forced == 0 && !line64 && 2 * (int64_t)S * ((dv + 7) / 8) >= 3 * (int64_t)sdm_device_simds()))
         return fwd_plan_sw<16>(W, R, dv, in_dtype, p) || fwd_plan_sw<8>(W, R, dv, in_dtype, p);
     return fwd_plan_sw<8>(W, R, dv, in_dtype, p) || fwd_plan_sw<16>(W, R, dv, in_dtype, p);
 }
 
 // LDS of the line-cooperative forward kernel (shared part, per-wave part).
-template <int SW>
+template <int SW, int FR>
 size_t fline_lds(bool save, int in_dtype, size_t* per_wave) {
     constexpr int NS = stage_slots<FWD_PD>();
     const int vbytes = in_dtype == SDM_DT_BF16 ? 2 : 4;
-    *per_wave = (size_t)NS * SW * vbytes + (size_t)FWD_PD * FROWS * SW * 4;
-    return (size_t)fline_shared_bytes<SW>(save, NS, fwd_rec_layout(FROWS, FROWS).bytes) + FLW * *per_wave;
+    *per_wave = (size_t)NS * SW * vbytes + (size_t)FWD_PD * FR * SW * 4;
+    return (size_t)fline_shared_bytes<SW, FR>(save, NS, fwd_rec_layout(FR, FR).bytes) + FLW * *per_wave;
 }
 
-// The line-cooperative kernel's shape: W = R = 32 (K = 32 / RG), d_v a
-// multiple of 4 SW (whole workgroups), the shared record block within one
-// chunk per lane, and its LDS within the limit.
-template <int SW, int K>
+// The line-cooperative kernel's shape: W = R = FR, d_v a multiple of 4 SW
+// (whole workgroups), and its LDS within the limit (at 64 rows, 16 columns
+// and the undo log: 155 KB).
+template <int SW, int FR>
 bool fline_ok(const ScanFwdArgs& a, const FwdPlan& p, bool save, size_t* lds, size_t* per_wave) {
-    constexpr int RG = SDM_WAVE / (SW / 4);
-    if (!sdm_line_io_enabled() || K * RG != FROWS || a.W != FROWS || a.R != FROWS || a.dv % (FLW * SW) != 0 ||
-        p.n_slices % FLW != 0 || G * fwd_rec_layout(FROWS, FROWS).bytes > FLW * SDM_WAVE * 16)
+    if (!sdm_line_io_enabled() || a.W != FR || a.R != FR || a.dv % (FLW * SW) != 0 || p.n_slices % FLW != 0)
         return false;
-    *lds = fline_lds<SW>(save, a.in_dtype, per_wave);
+    *lds = fline_lds<SW, FR>(save, a.in_dtype, per_wave);
     return *lds <= (size_t)LDS_LIMIT;
 }
 
@@ -605,14 +620,18 @@ hipError_t launch_fwd_k(const ScanFwdArgs& a, const FwdPlan& p, hipStream_t st) 
     constexpr int NR = nr_for_k<SW>(K);
     const int S = a.B * a.H;
     size_t lds = 0, per_wave = 0;
-    if (fline_ok<SW, K>(a, p, SAVE, &lds, &per_wave)) {
-        auto kl = scan_fwd_line_kernel<VT, SW, FWD_PD, SAVE>;
-        hipError_t e = hipFuncSetAttribute((const void*)kl, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(kl, dim3(p.n_slices / FLW * S), dim3(FLW * SDM_WAVE), lds, st,
-                           a.ws + SDM_WS_HEADER, static_cast<const VT*>(a.v), a.mem, a.y, a.saved, a.T, a.tb,
-                           a.te, a.dv, a.N, p.n_slices, (int)per_wave);
-        return hipGetLastError();
+    constexpr int FR = K * (SDM_WAVE / (SW / 4));   // rows the plan's K passes hold
+    if constexpr (FR == 32 || FR == 64) {
+        if (fline_ok<SW, FR>(a, p, SAVE, &lds, &per_wave)) {
+            auto kl = scan_fwd_line_kernel<VT, SW, FWD_PD, SAVE, FR>;
+            hipError_t e =
+                hipFuncSetAttribute((const void*)kl, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            if (e != hipSuccess) return e;
+            hipLaunchKernelGGL(kl, dim3(p.n_slices / FLW * S), dim3(FLW * SDM_WAVE), lds, st,
+                               a.ws + SDM_WS_HEADER, static_cast<const VT*>(a.v), a.mem, a.y, a.saved, a.T,
+                               a.tb, a.te, a.dv, a.N, p.n_slices, (int)per_wave);
+            return hipGetLastError();
+        }
     }
     dim3 grid((p.n_slices + p.wpb - 1) / p.wpb * S);   // order: scan_wg_coords
     const size_t sm = (size_t)p.lds_per_wave * p.wpb;

@@ -152,7 +152,7 @@ def test_forward_small(name, slice_width):
     check_scan(w, g, o, streams, f"{name}/sw{slice_width}/scan")
 
 
-# Line-cooperative forward kernel (W = R = 32, d_v a multiple of 4 x slice width):
+# Line-cooperative forward kernel (W = R = 32 or 64, d_v a multiple of 4 x slice width):
 # against the oracle, and against the per-wave kernel (to 1e-5: the sums over rows
 # are taken in another order), with and without the undo log.  N = 1024 with 32
 # slots makes rows recur within the prefetch window and tokens read what they write.
@@ -162,6 +162,10 @@ FLINE = {
                                        seed=52, codebook=False),
     "bf16-fline-T5-m0": synth.Workload("t", B=2, H=1, T=5, d_k=32, d_v=64, N=1024, topk=32, seed=53,
                                        m0="shared"),
+    # W = R = 64: each wave moves 16 of a token's 64 rows; two record chunks per lane
+    "bf16-fline64-ragged": synth.Workload("t", B=1, H=2, T=150, d_k=64, d_v=128, N=4096, topk=64, seed=54),
+    "f32-fline64-direct": synth.Workload("t", B=1, H=2, T=70, d_k=128, d_v=64, N=4096, topk=64, dtype="f32",
+                                         seed=55, codebook=False, m0="shared"),
 }
 
 
