@@ -145,7 +145,8 @@ def main():
                          "source): the reference dispatch for scaling HBM counters")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+        print(json.dumps({"error": "the SDM path is measured on one GPU only (the streams shard with no exchange "
+                                   "in the forward; no multi-GPU path is built); --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
 
