@@ -34,6 +34,9 @@ CASES = {
                                        codebook=False, m0="shared"),
     # k in (64, 128]: two list entries per lane
     "bf16-k128": synth.Workload("t", B=1, H=3, T=3, d_k=64, d_v=40, N=16384, topk=128, seed=65, m0="shared"),
+    # the smallest shapes: one slot per side, one column quad, sqrt(N) = 10
+    "f32-k1-dv4": synth.Workload("t", B=3, H=1, T=4, d_k=16, d_v=4, N=100, topk=1, dtype="f32", seed=66,
+                                 m0="shared"),
 }
 
 
