@@ -39,6 +39,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "SDM layer tokens/sec (fwd, fwd+bwd) at 1 GPU; achieved HBM GB/s vs peak"
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 matrix-core peak of the MI355X
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fwd_scan_c1.json")
 # sources of the forward scan kernel: the traffic file holds their hash
 SCAN_SRCS = [os.path.join(ROOT, "paper_2607_07386_amd", "csrc", f)
@@ -80,6 +81,19 @@ def unique_row_bytes(w_idx, r_idx, d_v, in_bytes, window=64):
     rows = distinct(both) + distinct(wi)
     tokens = S * nw * window
     return rows * d_v * 4 + tokens * (d_v * in_bytes + 2 * in_bytes + (W + R) * 8 + d_v * 4), tokens
+
+
+def scoring_mfma(w, call_ms):
+    """The addressing's sub-key scoring against the bf16 matrix-core peak: per
+    call (one side, every token-head) 2 sqrt(N) d_k flops per token-head (both
+    halves, sqrt(N) sub-keys of d_k / 2), over the address kernel's time alone."""
+    flops = 2 * w.sqrtN * w.d_k * w.B * w.H * w.T
+    tf = flops / (call_ms * 1e-3) / 1e12
+    return {"bound": "mfma", "kernel": "address_kernel", "flops_per_call": flops, "call_ms": round(call_ms, 4),
+            "achieved": round(tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 5),
+            "note": "the kernel's time is mostly top-k selection on the vector ALUs; scoring alone is a "
+                    "small part of it"}
 
 
 def log(msg):
@@ -128,7 +142,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-streams", type=int, default=16)
     ap.add_argument("--cpu-tokens", type=int, default=4096)
-    ap.add_argument("--only", choices=["fwd", "train", "init", "decode", "paper"], default=None,
+    ap.add_argument("--only", choices=["fwd", "train", "init", "decode", "paper", "address"], default=None,
                     help="run one leg only (profiling runs)")
     ap.add_argument("--no-sequential", action="store_true",
                     help="skip the reference timing of the forward step as three separate calls")
@@ -242,8 +256,10 @@ def main():
             torch.cuda.synchronize()
             ms_seq = round(e0.elapsed_time(e1) / 3, 4)
             t_scan, n_scan = sdm.profile_read("fwd_scan")
+            t_addr, n_addr = sdm.profile_read("address")
             sdm.profile_enable(False)
             seq_scan_ms = t_scan / max(n_scan, 1)
+            out["scoring"] = scoring_mfma(w, t_addr / max(n_addr, 1))
         tokens = B * T
         scan_launches = max(kern["fwd_scan"][1], 1)
         scan_ms = kern["fwd_scan"][0] / scan_launches
@@ -402,6 +418,26 @@ def main():
             "us_per_step": round(dms * 1e3, 2), "tokens_per_s": round(wd.B / (dms * 1e-3), 1)}
         del q, k, v, al, be, cb, mem, ws, y, douts
         torch.cuda.empty_cache()
+
+    # ------------------------------------------------------------ addressing alone
+    if args.only == "address":
+        # both sides' addressing of the forward workload, one call after the other
+        log("addressing: generating inputs")
+        ia = synth.Inputs(w)
+        q, k, cb = to_dev(ia.q), to_dev(ia.k), to_dev(ia.codebook)
+        for _ in range(args.warmup):
+            sdm.address(q, cb, w.N, w.topk)
+            sdm.address(k, cb, w.N, w.topk)
+        torch.cuda.synchronize()
+        sdm.profile_enable(True)
+        for _ in range(args.steps):
+            sdm.address(q, cb, w.N, w.topk)
+            sdm.address(k, cb, w.N, w.topk)
+        torch.cuda.synchronize()
+        t_addr, n_addr = sdm.profile_read("address")
+        sdm.profile_enable(False)
+        out["scoring"] = scoring_mfma(w, t_addr / max(n_addr, 1))
+        del q, k, cb
 
     # ------------------------------------------------------------ the paper's 1.4B layer
     if (extra and args.only is None) or args.only == "paper":
