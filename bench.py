@@ -127,8 +127,17 @@ def cpu_baseline(w, inp, n_streams, T_sample):
     cat = lambda xs: np.concatenate(xs)[:, 0]
     oracle.scan_fwd(cat(wi), cat(wv), cat(ri), cat(rv), v, al, be, mem)
     dt = time.perf_counter() - t0
-    return dict(value=n_streams * T / w.H / dt, unit="tokens/s", cores=oracle.max_threads(),
-                kind="oracle", wall_s=round(dt, 3),
+    # one stream on one thread: the oracle's serial cost per stream
+    cores = oracle.max_threads()
+    oracle.set_threads(1)
+    t1 = time.perf_counter()
+    a = oracle.address(x_q[:1], cb[inp.heads[0]][None], w.N, w.topk)
+    b = oracle.address(x_k[:1], cb[inp.heads[0]][None], w.N, w.topk)
+    oracle.scan_fwd(b[0][:, 0], b[1][:, 0], a[0][:, 0], a[1][:, 0], v[:1], al[:1], be[:1], np.zeros((1, w.N, w.d_v)))
+    dt1 = time.perf_counter() - t1
+    oracle.set_threads(cores)
+    return dict(value=n_streams * T / w.H / dt, unit="tokens/s", cores=cores,
+                kind="oracle", wall_s=round(dt, 3), one_stream_one_thread_s=round(dt1, 3),
                 sample=f"{n_streams} of {w.B * w.H} (b,h) streams x {T} tokens of the same workload; "
                        f"address(q)+address(k)+forward scan, fp64; tokens/s = streams*T/H/wall")
 

@@ -56,6 +56,8 @@ def _load():
             lib.orc_scan_bwd.argtypes = [I, I, I, L, I, I, P, P, P, P, P, P, P, P, P, P, P,
                                          P, P, P, P, P]
             lib.orc_address_bwd.argtypes = [P, I, I, I, I, L, I, P, P, P, P]
+            lib.orc_set_threads.argtypes = [I]
+            lib.orc_set_threads.restype = None
             for f in ("orc_address", "orc_address_brute", "orc_scan_fwd", "orc_scan_bwd",
                       "orc_address_bwd", "orc_max_threads"):
                 getattr(lib, f).restype = ctypes.c_int
@@ -77,6 +79,11 @@ def _i32(a):
 
 def max_threads() -> int:
     return _load().orc_max_threads()
+
+
+def set_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops from now on (for timing)."""
+    _load().orc_set_threads(int(n))
 
 
 def address(x, codebook, N: int, topk: int, decide_f32: bool = True, brute: bool = False):

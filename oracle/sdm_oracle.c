@@ -400,3 +400,12 @@ int orc_max_threads(void) {
     return 1;
 #endif
 }
+
+/* Threads of the parallel loops that follow (n >= 1); timing only. */
+void orc_set_threads(int n) {
+#ifdef _OPENMP
+    omp_set_num_threads(n < 1 ? 1 : n);
+#else
+    (void)n;
+#endif
+}
