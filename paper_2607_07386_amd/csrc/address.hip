@@ -721,13 +721,15 @@ __device__ __forceinline__ void tile_scores(const XT* __restrict__ xs, const XT*
         const int r16 = lane % 16, q = lane / 16;
         const int t = t0 + r16;
         const bool trow = r16 < nt;   // this lane's token row exists
-        if (E <= 4 && nks <= 2) {
-            // dh <= 64, s <= 256: this wave's tiles of a half (at most E) need 2 E
-            // codebook operands; all are loaded before the first MFMA, so the half
-            // pays one load latency instead of one per tile.
+        if (nks <= 2) {
+            // dh <= 64: this wave's tiles of a half (E of them) need 2 E codebook
+            // operands; they are loaded EG tiles at a time, all of a group before
+            // its first MFMA, so a group pays one load latency instead of one per
+            // tile (every tile at once for s <= 256, E <= 4)
+            constexpr int EG = E < 4 ? E : 4;
 #pragma unroll
             for (int half = 0; half < 2; ++half) {
-                sdm_bf16x8 a[2], b[E][2];
+                sdm_bf16x8 a[2];
 #pragma unroll
                 for (int ks = 0; ks < 2; ++ks) {
                     const int kc = ks * 32 + 8 * q;
@@ -736,27 +738,31 @@ __device__ __forceinline__ void tile_scores(const XT* __restrict__ xs, const XT*
                         a[ks] = *reinterpret_cast<const sdm_bf16x8*>(xs + (size_t)t * dk + half * dh + kc);
                 }
 #pragma unroll
-                for (int i = 0; i < E; ++i) {
-                    const int j = (wave + AWAVES * i) * 16 + r16;
-                    const XT* crow = cbh + ((size_t)half * s + min(j, s - 1)) * dh;
+                for (int i0 = 0; i0 < E; i0 += EG) {
+                    sdm_bf16x8 b[EG][2];
 #pragma unroll
-                    for (int ks = 0; ks < 2; ++ks) {
-                        const int kc = ks * 32 + 8 * q;
-                        b[i][ks] = sdm_bf16x8{};
-                        if (ks < nks && j < s && kc < dh)
-                            b[i][ks] = *reinterpret_cast<const sdm_bf16x8*>(crow + kc);
+                    for (int i = 0; i < EG; ++i) {
+                        const int j = (wave + AWAVES * (i0 + i)) * 16 + r16;
+                        const XT* crow = cbh + ((size_t)half * s + min(j, s - 1)) * dh;
+#pragma unroll
+                        for (int ks = 0; ks < 2; ++ks) {
+                            const int kc = ks * 32 + 8 * q;
+                            b[i][ks] = sdm_bf16x8{};
+                            if (ks < nks && j < s && kc < dh)
+                                b[i][ks] = *reinterpret_cast<const sdm_bf16x8*>(crow + kc);
+                        }
                     }
-                }
 #pragma unroll
-                for (int i = 0; i < E; ++i) {
-                    const int j = (wave + AWAVES * i) * 16 + r16;
-                    sdm_f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0], b[i][0], acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1], b[i][1], acc, 0, 0, 0);
-                    if (j < s) {
+                    for (int i = 0; i < EG; ++i) {
+                        const int j = (wave + AWAVES * (i0 + i)) * 16 + r16;
+                        sdm_f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+                        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0], b[i][0], acc, 0, 0, 0);
+                        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1], b[i][1], acc, 0, 0, 0);
+                        if (j < s) {
 #pragma unroll
-                        for (int v = 0; v < 4; ++v)
-                            if (4 * q + v < nt) scores[(size_t)(4 * q + v) * 2 * SP + half * SP + j] = acc[v];
+                            for (int v = 0; v < 4; ++v)
+                                if (4 * q + v < nt) scores[(size_t)(4 * q + v) * 2 * SP + half * SP + j] = acc[v];
+                        }
                     }
                 }
             }
