@@ -33,6 +33,16 @@ constexpr int ATILE = 16;     // tokens per workgroup (the MFMA tile's rows), sq
 // on a CU: 32 KB at E = 4, 8, 16.
 template <int E>
 __host__ __device__ constexpr int atile() { return E <= 4 ? ATILE : (E <= 8 ? 8 : 4); }
+// For sqrt(N) > 512 and k <= 64 the tile scores one half at a time, so the
+// same 32 KB of scores hold 8 tokens instead of 4 and each workgroup reads the
+// head's codebook (256 KB at sqrt(N) = 1024) for twice as many tokens.  Stage
+// 1 of a half leaves each token's ranked shortlist in LDS; stage 2 reads both.
+// (At sqrt(N) = 512 the same layout, 16 tokens in 56 KB, halved the
+// workgroups per CU and measured slower.)
+template <int E, int KM>
+__host__ __device__ constexpr bool half_seq() { return E >= 16 && KM <= 64; }
+template <int E, int KM>
+__host__ __device__ constexpr int tile_tokens() { return half_seq<E, KM>() ? 8 : atile<E>(); }
 constexpr int AWAVES = 4;
 constexpr int MAXK = 64;      // largest k of the one-entry-per-lane kernels
 constexpr int MAXK_BIG = 128; // largest k: two entries per lane
@@ -444,18 +454,15 @@ __device__ __forceinline__ bool token_fast(const float* row, int s, int k, const
     return true;
 }
 
-// One token on the general path (any k, overflowing selections): stage 1 on
-// both halves, stage 2 over the pruned pairs, id sort and softmax.  Kept out
-// of line: it is the cold path of the common shapes.
-template <int E>
-__device__ __noinline__ void token_general(const float* row, int s, int sp, int k, int ncand, const uint16_t* pairs,
-                                           Entry* scr, Entry* listA, Entry* listB, uint64_t* kbuf,
-                                           int32_t* idx_out, float* val_out, float* score_out) {
+// Stage 2 of one token (k <= 64) on this wave, from the ranked shortlists of
+// the two halves: the pruned pairs, their top-k, id sort, softmax.  Out of
+// line: inlined into token_general it raised the address kernel's registers
+// from 104 to 148.
+__device__ __noinline__ void token_pairs(int s, int k, int ncand, const uint16_t* pairs, Entry* scr,
+                                            const Entry* listA, const Entry* listB, uint64_t* kbuf,
+                                            int32_t* idx_out, float* val_out, float* score_out) {
     const int lane = lane_id();
     const int ne2 = (ncand + SDM_WAVE - 1) / SDM_WAVE;
-    half_topk<E>(row, s, k, scr, kbuf, listA);
-    half_topk<E>(row + sp, s, k, scr, kbuf, listB);
-
     // stage 2 over the pruned pairs of the two ranked shortlists
     uint64_t ck[MAXCAND_E];
 #pragma unroll
@@ -509,6 +516,18 @@ __device__ __noinline__ void token_general(const float* row, int s, int sp, int 
     }
     wait_lds();
     __builtin_amdgcn_wave_barrier();
+}
+
+// One token on the general path (any k, overflowing selections): stage 1 on
+// both halves, stage 2 over the pruned pairs, id sort and softmax.  Kept out
+// of line: it is the cold path of the common shapes.
+template <int E>
+__device__ __noinline__ void token_general(const float* row, int s, int sp, int k, int ncand, const uint16_t* pairs,
+                                           Entry* scr, Entry* listA, Entry* listB, uint64_t* kbuf,
+                                           int32_t* idx_out, float* val_out, float* score_out) {
+    half_topk<E>(row, s, k, scr, kbuf, listA);
+    half_topk<E>(row + sp, s, k, scr, kbuf, listB);
+    token_pairs(s, k, ncand, pairs, scr, listA, listB, kbuf, idx_out, val_out, score_out);
 }
 
 // ---- k in (64, 128]: two list entries per lane ---------------------------
@@ -682,9 +701,10 @@ __device__ __forceinline__ void tile_pairs(int k, uint16_t* lp, const uint16_t*&
 
 // Phase A: sub-key scores of tokens t0 .. t0 + nt - 1 (nt <= AT) of one
 // stream (xs: its x, token stride dk; cbh: its head's codebook [2][s][dk/2],
-// unused in direct mode) into score rows 0 .. nt-1: row [2][SP], half h's
-// sub-key j at h SP + j, j in [s, SP) -inf.  Rows past nt are not written.
-template <typename XT, int MODE, int E>
+// unused in direct mode) into score rows 0 .. nt-1: row [NH][SP] for halves
+// HB .. HB + NH - 1 (both by default), half h's sub-key j at (h - HB) SP + j,
+// j in [s, SP) -inf.  Rows past nt are not written.
+template <typename XT, int MODE, int E, int HB = 0, int NH = 2>
 __device__ __forceinline__ void tile_scores(const XT* __restrict__ xs, const XT* __restrict__ cbh, int t0, int nt,
                                             int dk, int s, float* scores) {
     constexpr int SP = E * SDM_WAVE;
@@ -693,15 +713,15 @@ __device__ __forceinline__ void tile_scores(const XT* __restrict__ xs, const XT*
     const int lane = lane_id();
     // Row of a token: [2][SP], half h's sub-key j at h*SP + j; j in [s, SP) holds -inf.
     if constexpr (MODE == 0) {
-        for (int i = tid; i < nt * 2 * SP; i += blockDim.x) {
-            const int tt = i / (2 * SP), half = (i / SP) & 1, j = i % SP;
+        for (int i = tid; i < nt * NH * SP; i += blockDim.x) {
+            const int tt = i / (NH * SP), half = HB + (i / SP) % NH, j = i % SP;
             const int t = t0 + tt;
             scores[i] = j >= s ? -INFINITY : to_f32(xs[(size_t)t * dk + half * s + j]);
         }
     } else if constexpr (MODE == 1) {
         const int dh = dk / 2;
-        for (int i = tid; i < nt * 2 * SP; i += blockDim.x) {
-            const int tt = i / (2 * SP), half = (i / SP) & 1, j = i % SP;
+        for (int i = tid; i < nt * NH * SP; i += blockDim.x) {
+            const int tt = i / (NH * SP), half = HB + (i / SP) % NH, j = i % SP;
             const int t = t0 + tt;
             float acc = 0.f;
             if (j < s) {
@@ -728,7 +748,7 @@ __device__ __forceinline__ void tile_scores(const XT* __restrict__ xs, const XT*
             // tile (every tile at once for s <= 256, E <= 4)
             constexpr int EG = E < 4 ? E : 4;
 #pragma unroll
-            for (int half = 0; half < 2; ++half) {
+            for (int half = HB; half < HB + NH; ++half) {
                 sdm_bf16x8 a[2];
 #pragma unroll
                 for (int ks = 0; ks < 2; ++ks) {
@@ -761,13 +781,14 @@ __device__ __forceinline__ void tile_scores(const XT* __restrict__ xs, const XT*
                         if (j < s) {
 #pragma unroll
                             for (int v = 0; v < 4; ++v)
-                                if (4 * q + v < nt) scores[(size_t)(4 * q + v) * 2 * SP + half * SP + j] = acc[v];
+                                if (4 * q + v < nt)
+                                    scores[(size_t)(4 * q + v) * NH * SP + (half - HB) * SP + j] = acc[v];
                         }
                     }
                 }
             }
         } else
-        for (int half = 0; half < 2; ++half) {
+        for (int half = HB; half < HB + NH; ++half) {
             // operand A (this lane's token row, k-slices 8q .. 8q+7 of each step) serves
             // every sub-key tile of the half
             sdm_bf16x8 a[MAXKS];
@@ -794,13 +815,13 @@ __device__ __forceinline__ void tile_scores(const XT* __restrict__ xs, const XT*
                 if (j < s) {
 #pragma unroll
                     for (int v = 0; v < 4; ++v)
-                        if (4 * q + v < nt) scores[(size_t)(4 * q + v) * 2 * SP + half * SP + j] = acc[v];
+                        if (4 * q + v < nt) scores[(size_t)(4 * q + v) * NH * SP + (half - HB) * SP + j] = acc[v];
                 }
             }
         }
         if (s < SP) {
             const int pad = SP - s;
-            for (int i = tid; i < nt * 2 * pad; i += blockDim.x)
+            for (int i = tid; i < nt * NH * pad; i += blockDim.x)
                 scores[(i / pad) * SP + s + i % pad] = -INFINITY;
         }
     }
@@ -932,7 +953,50 @@ __device__ __forceinline__ void address_tile(const XT* __restrict__ x, const XT*
     }
 }
 
-// Grid (tiles of AT tokens of [tb, te), streams).
+// The tokens [t0, min(t0 + AH, te)) of stream `stream` (AH = tile_tokens),
+// one half at a time (half_seq shapes): scores of one half for every token of
+// the tile, stage 1 of each token into its shortlist, then stage 2 of each.
+template <typename XT, int MODE, int E, int KM>
+__device__ __forceinline__ void address_tile_halves(const XT* __restrict__ x, const XT* __restrict__ cb, int H,
+                                                    int T, int stream, int t0, int te, int dk, int s, int k,
+                                                    int32_t* __restrict__ idx, float* __restrict__ val,
+                                                    float* __restrict__ score, unsigned char* smem) {
+    constexpr int AH = tile_tokens<E, KM>();
+    constexpr int SP = E * SDM_WAVE;
+    float* scores = reinterpret_cast<float*>(smem);                           // [AH][SP], one half
+    Entry* shortl = reinterpret_cast<Entry*>(scores + (size_t)AH * SP);       // [AH][2][KM]
+    Entry* scratch = shortl + (size_t)AH * 2 * KM;                            // [AWAVES][3][KM]
+    uint64_t* kbufs = reinterpret_cast<uint64_t*>(scratch + AWAVES * 3 * KM);  // [AWAVES][64]
+    const int wave = threadIdx.x / SDM_WAVE;
+    const uint16_t* pairs;
+    int ncand;
+    tile_pairs<KM>(k, nullptr, pairs, ncand);   // k <= 64: the constant table
+    const XT* xs = x + (size_t)stream * T * dk;
+    const XT* cbh = MODE == 0 ? cb : cb + (size_t)(stream % H) * 2 * s * (dk / 2);
+    const int nt = min(AH, te - t0);
+    Entry* scr = scratch + wave * 3 * KM;
+    uint64_t* kbuf = kbufs + wave * SDM_WAVE;
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+        if (half == 0)
+            tile_scores<XT, MODE, E, 0, 1>(xs, cbh, t0, nt, dk, s, scores);
+        else
+            tile_scores<XT, MODE, E, 1, 1>(xs, cbh, t0, nt, dk, s, scores);
+        __syncthreads();
+        for (int tt = wave; tt < nt; tt += AWAVES)
+            half_topk<E>(scores + (size_t)tt * SP, s, k, scr, kbuf, shortl + ((size_t)tt * 2 + half) * KM);
+        __syncthreads();   // the next half overwrites the scores
+    }
+    for (int tt = wave; tt < nt; tt += AWAVES) {
+        const size_t o = ((size_t)stream * T + t0 + tt) * k;
+        token_pairs(s, k, ncand, pairs, scr, shortl + (size_t)tt * 2 * KM, shortl + ((size_t)tt * 2 + 1) * KM, kbuf,
+                    idx + o, val + o, score ? score + o : nullptr);
+        wait_lds();
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
+// Grid (tiles of tile_tokens tokens of [tb, te), streams).
 template <typename XT, int MODE, int E, int KM>
 __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __restrict__ x,
                                                                     const XT* __restrict__ cb, int H, int T,
@@ -941,8 +1005,12 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __
                                                                     float* __restrict__ val,
                                                                     float* __restrict__ score) {
     extern __shared__ __align__(16) unsigned char smem[];
-    address_tile<XT, MODE, E, KM>(x, cb, H, T, blockIdx.y, tb + blockIdx.x * atile<E>(), te, dk, s, k, idx, val,
-                                  score, smem);
+    if constexpr (half_seq<E, KM>())
+        address_tile_halves<XT, MODE, E, KM>(x, cb, H, T, blockIdx.y, tb + blockIdx.x * tile_tokens<E, KM>(), te, dk,
+                                             s, k, idx, val, score, smem);
+    else
+        address_tile<XT, MODE, E, KM>(x, cb, H, T, blockIdx.y, tb + blockIdx.x * atile<E>(), te, dk, s, k, idx, val,
+                                      score, smem);
 }
 
 // ---- one token per stream (decode) ----------------------------------------
@@ -1201,6 +1269,17 @@ constexpr size_t address_lds_bytes(int E, int AT, int KM) {
     return (size_t)AT * 2 * E * SDM_WAVE * sizeof(float) + AWAVES * 3 * KM * sizeof(Entry) +
            AWAVES * SDM_WAVE * sizeof(uint64_t) + (KM > MAXK ? MAXCAND_BIG * SDM_WAVE * sizeof(uint16_t) : 0);
 }
+// The same for address_kernel's tile (one half of scores and the shortlists
+// for half_seq shapes).
+template <int E, int KM>
+constexpr size_t tile_lds_bytes() {
+    constexpr int AT = tile_tokens<E, KM>();
+    if constexpr (half_seq<E, KM>())
+        return (size_t)AT * E * SDM_WAVE * sizeof(float) + (size_t)AT * 2 * KM * sizeof(Entry) +
+               AWAVES * 3 * KM * sizeof(Entry) + AWAVES * SDM_WAVE * sizeof(uint64_t);
+    else
+        return address_lds_bytes(E, AT, KM);
+}
 
 template <typename XT, int MODE>
 hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, int tb, int tn, int dk,
@@ -1210,8 +1289,8 @@ hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, 
     const XT* cp = static_cast<const XT*>(cb);
 #define SDM_ADDR_CASE(EE, KM)                                                                   \
     {                                                                                           \
-        constexpr int AT = atile<EE>();                                                         \
-        const size_t sm = address_lds_bytes(EE, AT, KM);                                        \
+        constexpr int AT = tile_tokens<EE, KM>();                                               \
+        const size_t sm = tile_lds_bytes<EE, KM>();                                             \
         auto kfn = address_kernel<XT, MODE, EE, KM>;                                            \
         hipError_t e = hipFuncSetAttribute((const void*)kfn,                                    \
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm); \
