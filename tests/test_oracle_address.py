@@ -82,6 +82,21 @@ def test_two_stage_equals_brute_force(oracle_mod, decide_f32):
             np.testing.assert_array_equal(u, w)
 
 
+@pytest.mark.parametrize("s,k,codebook", [(40, 40, True), (72, 65, False), (128, 100, True), (128, 128, False)])
+def test_large_k_matches_exhaustive_numpy_and_brute_force(oracle_mod, s, k, codebook):
+    """k up to 128 (the largest k of the boundary), including k = sqrt(N): the
+    two-stage selection against an exhaustive numpy sort of all N scores and
+    against the oracle's own brute force."""
+    rng = np.random.default_rng(11 + s + k)
+    x, cb = _rand_case(rng, 1, 1, 3, s, codebook=codebook)
+    idx, val, score = oracle_mod.address(x, cb, s * s, k)
+    np.testing.assert_array_equal(idx, _numpy_topk(_numpy_scores(x, cb, s), k))
+    b = oracle_mod.address(x, cb, s * s, k, brute=True)
+    for u, w in zip((idx, val, score), b):
+        np.testing.assert_array_equal(u, w)
+    np.testing.assert_allclose(val.sum(-1), 1.0, rtol=0, atol=1e-12)
+
+
 def test_exact_ties_take_lower_slot_id(oracle_mod):
     """Direct mode, s = 4.  Sub-scores s0 = [.5,.5,.1,.5], s1 = [.25,.25,0,.25]:
     nine slots tie at the maximum 0.75; the three with the lowest ids are
