@@ -503,17 +503,19 @@ int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, cons
     hipStream_t st = (hipStream_t)stream;
     hipError_t e = sdm_launch_zero_words(workspace, 4, st);
     if (e != hipSuccess) return hip_fail(e, "sdm_scan_bwd flag reset");
-    // adjoint of the memory starts as dL/dM_T
+    // adjoint of the memory starts as dL/dM_T (on `stream`, before the first scan;
+    // the records do not need it, so the pipelined path overlaps the two)
     const size_t memel = (size_t)B * H * N * d_v;
-    {
+    auto init_adjoint = [&]() -> hipError_t {
         SdmProfScope ps(SDM_K_MEM_INIT, st);
-        if (dmem_T == nullptr)
-            e = sdm_launch_mem_init(dmem0, nullptr, B, H, N, d_v, st);
-        else if (dmem_T != dmem0)
-            e = sdm_launch_copy(dmem0, dmem_T, memel, st);
+        if (dmem_T == nullptr) return sdm_launch_mem_init(dmem0, nullptr, B, H, N, d_v, st);
+        if (dmem_T != dmem0) return sdm_launch_copy(dmem0, dmem_T, memel, st);
+        return hipSuccess;
+    };
+    if ((int64_t)B * H * T == 0) {
+        if ((e = init_adjoint()) != hipSuccess) return hip_fail(e, "sdm_scan_bwd adjoint init");
+        return SDM_OK;
     }
-    if (e != hipSuccess) return hip_fail(e, "sdm_scan_bwd adjoint init");
-    if ((int64_t)B * H * T == 0) return SDM_OK;
     unsigned char* ws = static_cast<unsigned char*>(workspace);
     const size_t ST = (size_t)B * H * T;
     float* spare = reinterpret_cast<float*>(ws + need - ST * (W + R) * sizeof(float));
@@ -579,6 +581,7 @@ int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, cons
     };
     if (nchunks == 1) {
         ScanBwdArgs ac = ranged(0);
+        if ((e = init_adjoint()) != hipSuccess) return hip_fail(e, "sdm_scan_bwd adjoint init");
         if ((e = sdm_launch_bwd_prep_range(ac, st)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd launch");
         if ((e = sdm_launch_bwd_scan_range(ac, st)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd launch");
         if ((e = post(ac, st)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd launch");
@@ -596,9 +599,11 @@ int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, cons
     hipEvent_t ev_start = ev[0], ev_end = ev[2 * nchunks + 1];
     auto ev_prep = [&](int c) { return ev[1 + c]; };
     auto ev_scan = [&](int c) { return ev[1 + nchunks + c]; };
-    // the flag reset above (and the caller's earlier work) precede the side stream
+    // the flag reset above (and the caller's earlier work) precede the side stream;
+    // the adjoint init follows on `stream`, beside the first stages' records
     if ((e = hipEventRecord(ev_start, st)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd record");
     if ((e = hipStreamWaitEvent(side, ev_start, 0)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd wait");
+    if ((e = init_adjoint()) != hipSuccess) return hip_fail(e, "sdm_scan_bwd adjoint init");
     // side: prep 0, prep 1, then for each c: [scan c done] post c, prep c + 2
     for (int c = 0; c < std::min(2, nchunks); ++c) {
         if ((e = sdm_launch_bwd_prep_range(ranged(c), side)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd launch");
