@@ -228,7 +228,8 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
     constexpr int LEAD = bstage_lead<PD>();
     constexpr int NS = bstage_slots<PD>();
     constexpr int VB = SW * (int)sizeof(VT);
-    static_assert(PD % G == 0, "prefetch depth must be a multiple of the staging block");
+    // staging blocks of G tokens every G steps; the prefetch depth divides or is a multiple of G
+    static_assert(PD % G == 0 || G % PD == 0, "prefetch depth and staging block");
     static_assert(NS >= LEAD && NS >= PD, "record ring too small");
 
     const int lane = lane_id();
@@ -288,7 +289,7 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
 #pragma unroll
         for (int j = 0; j < PD; ++j) {
             const int t = T1 - (i0 + j);
-            if (j % G == 0) {
+            if ((i0 + j) % G == 0) {
                 bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, t - (LEAD - G), tb, c.L.bytes, lane);
                 bstage_load<VT, SW, NR>(st, stv, srec, sv, t - LEAD, tb, dv, slice, c.L.bytes, lane);
             }
@@ -613,6 +614,11 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(const float* __restrict
 
 constexpr int BPD = SDM_BWD_PD;
 constexpr int BSW_MIN = 8;   // narrowest slice: sizes the per-slice partials
+// Prefetch depth of the per-wave kernel with K row passes: BPD tokens, or 2 at
+// K = 4 (64 rows at 16 columns, 128 at 8), where BPD tokens of prefetched rows
+// (4 x 17 float4 per lane) outgrow the registers.  The records' links follow
+// the same depth.
+constexpr int bpd_for_k(int K) { return K >= 4 ? 2 : BPD; }
 
 // Staging registers per lane (16 bytes each) for a block of G records: a
 // record of a shape with max(W, R) <= K RG takes at most 22 K RG + 8 bytes
@@ -624,7 +630,7 @@ constexpr int bnr_for_k(int K) {
 }
 
 struct BwdPlan {
-    int SW, K, NR, lds_per_wave, wpb, n_slices;
+    int SW, K, NR, lds_per_wave, wpb, n_slices, PD;
 };
 
 template <int SW>
@@ -635,11 +641,13 @@ bool bwd_plan_sw(int W, int R, int dv, int in_dtype, BwdPlan* p) {
     p->SW = SW;
     p->K = need <= 1 ? 1 : (need <= 2 ? 2 : 4);
     p->NR = bnr_for_k<SW>(p->K);
+    p->PD = bpd_for_k(p->K);
     const BwdRec L = bwd_rec_layout(W, R);
     if (G * L.bytes > p->NR * SDM_WAVE * 16) return false;
     const int vbytes = in_dtype == SDM_DT_BF16 ? 2 : 4;
+    static_assert(bstage_slots<2>() == bstage_slots<BPD>(), "one record ring size for both depths");
     constexpr int NS = bstage_slots<BPD>();
-    p->lds_per_wave = NS * L.bytes + NS * SW * vbytes + BPD * (R + W) * SW * 4 + BPD * W * SW * 4;
+    p->lds_per_wave = NS * L.bytes + NS * SW * vbytes + p->PD * (R + W) * SW * 4 + p->PD * W * SW * 4;
     if (p->lds_per_wave > LDS_LIMIT) return false;
     p->n_slices = (dv + SW - 1) / SW;
     p->wpb = std::min(std::min(MAX_WPB, p->n_slices), LDS_LIMIT / p->lds_per_wave);
@@ -691,7 +699,7 @@ hipError_t launch_bwd_k(const ScanBwdArgs& a, const BwdPlan& p, bool line, float
             return hipGetLastError();
         }
     }
-    auto kfn = scan_bwd_kernel<VT, SW, BPD, K, NR>;
+    auto kfn = scan_bwd_kernel<VT, SW, bpd_for_k(K), K, NR>;
     hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kfn, grid, dim3(p.wpb * SDM_WAVE), sm, st, a.ws + SDM_WS_HEADER,
@@ -739,8 +747,10 @@ bool sdm_bwd_line_io(const ScanBwdArgs& a) {
 }
 
 hipError_t sdm_launch_bwd_prep_range(const ScanBwdArgs& a, hipStream_t st) {
+    BwdPlan plan;   // the links' window is the scan's prefetch depth
+    if (!bwd_plan(a.B * a.H, a.W, a.R, a.dv, a.in_dtype, &plan)) return hipErrorInvalidConfiguration;
     SdmProfScope ps(SDM_K_BWD_PREP, st);
-    return sdm_launch_bwd_prep<BPD>(a, st);
+    return plan.PD == 2 ? sdm_launch_bwd_prep<2>(a, st) : sdm_launch_bwd_prep<BPD>(a, st);
 }
 
 hipError_t sdm_launch_bwd_scan_range(const ScanBwdArgs& a, hipStream_t st) {

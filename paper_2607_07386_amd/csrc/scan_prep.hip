@@ -297,3 +297,4 @@ hipError_t sdm_launch_bwd_prep(const ScanBwdArgs& a, hipStream_t st) {
 
 template hipError_t sdm_launch_fwd_prep<SDM_FWD_PD>(const ScanFwdArgs&, hipStream_t);
 template hipError_t sdm_launch_bwd_prep<SDM_BWD_PD>(const ScanBwdArgs&, hipStream_t);
+template hipError_t sdm_launch_bwd_prep<2>(const ScanBwdArgs&, hipStream_t);

@@ -280,6 +280,40 @@ def test_scan_wide_lists(W, R, dtype, slice_width):
     assert ey < 1e-4 and em < 1e-4
 
 
+# Backward with lists of 64 and 128 rows (the per-wave kernel's four-pass
+# shapes, which prefetch two tokens ahead instead of four): random sets over
+# 150 slots, so most rows recur within the prefetch window.  Scan level, fp32,
+# against the oracle's reverse pass; the memory must come back bit for bit.
+@pytest.mark.parametrize("W,R", [(64, 64), (128, 96)])
+def test_backward_wide_lists(W, R, slice_width):
+    S, T, N, dv = 2, 70, 150, 24
+    rng = np.random.default_rng(13 + W)
+    wi = np.stack([np.stack([np.sort(rng.choice(N, W, replace=False)) for _ in range(T)]) for _ in range(S)])
+    ri = np.stack([np.stack([np.sort(rng.choice(N, R, replace=False)) for _ in range(T)]) for _ in range(S)])
+    wi, ri = wi.astype(np.int32), ri.astype(np.int32)
+    wv = (rng.random((S, T, W)) * 2 / np.sqrt(W)).astype(np.float32)
+    rv = rng.standard_normal((S, T, R)).astype(np.float32)
+    v = rng.standard_normal((S, T, dv)).astype(np.float32)
+    al = rng.uniform(0.05, 1.0, (S, T)).astype(np.float32)
+    be = rng.uniform(0.0, 1.0, (S, T)).astype(np.float32)
+    m0 = rng.standard_normal((S, N, dv)).astype(np.float32)
+    dy = rng.standard_normal((S, T, dv)).astype(np.float32)
+    t_ = lambda a: torch.from_numpy(a).to(DEV)[:, None].contiguous()
+    mem = torch.from_numpy(m0).to(DEV)[:, None].contiguous()
+    saved = sdm.saved_buffer(S, 1, T, W, dv, DEV)
+    sdm.scan_fwd(t_(wi), t_(wv), t_(ri), t_(rv), t_(v), t_(al), t_(be), mem, saved=saved)
+    g = sdm.scan_bwd(t_(wi), t_(wv), t_(ri), t_(rv), t_(v), t_(al), t_(be), mem, saved, t_(dy), want_dqk=False)
+    torch.cuda.synchronize()
+    memo = m0.astype(np.float64)
+    _, P = oracle.scan_fwd(wi, wv, ri, rv, v, al, be, memo, save=True)
+    og = oracle.scan_bwd(wi, wv, ri, rv, v, al, be, memo, P, dy.astype(np.float64))
+    errs = {k: rel_err(np_(g[k])[:, 0], og[k]) for k in ("dv", "dalpha", "dbeta", "dw_val", "dr_val", "dmem0")}
+    report(f"bwd-wide/W{W}R{R}/sw{slice_width}", **errs)
+    for k, e in errs.items():
+        assert e <= 1e-4, (k, e)
+    assert np.array_equal(np_(mem)[:, 0], m0), "the undo did not restore M_0 bit for bit"
+
+
 def test_gated_deltanet_reduction_on_gpu():
     """N = d_qk, every slot selected with the raw dense key/query as weights."""
     rng = np.random.default_rng(9)
