@@ -136,6 +136,10 @@ SMALL = {
     # W = R = 64, direct-mode addressing (d_k = 2 sqrt(N))
     "paper-1.4b-layer": synth.Workload("t", B=1, H=2, T=130, d_k=480, d_v=960, N=57600, topk=64,
                                        seed=23, codebook=False),
+    # the paper's 8B layer: sqrt(N) = 480, d_v = 1920, W = R = 64, direct mode (one stream; its
+    # table is 1.8 GB)
+    "paper-8b-layer": synth.Workload("t", B=1, H=1, T=24, d_k=960, d_v=1920, N=230400, topk=64,
+                                     seed=29, codebook=False),
 }
 
 
@@ -380,6 +384,8 @@ BWD = {
                                        seed=34, codebook=False, m0="shared", train=True),
     "bf16-k128-m0": synth.Workload("t", B=1, H=2, T=70, d_k=64, d_v=40, N=16384, topk=128, seed=35,
                                    m0="shared", train=True),
+    "paper-8b-layer": synth.Workload("t", B=1, H=1, T=12, d_k=960, d_v=1920, N=230400, topk=64,
+                                     seed=37, codebook=False, train=True),
     "f32-k100-direct": synth.Workload("t", B=1, H=1, T=45, d_k=512, d_v=24, N=65536, topk=100, dtype="f32",
                                       seed=36, codebook=False, train=True),
 }
