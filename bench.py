@@ -16,8 +16,8 @@ Further legs: the training step (forward with the undo log + backward with
 addressing gradients) on the training workload (B=4, H=16, T=4096) under
 "train"; the learned-M0 broadcast of the learned-M0 workload under
 "mem_init"; single-token decode steps under "decode"; the paper's own 1.4B
-layer shape (H=2, sqrt(N)=240, d_v=960, W=R=64, direct-mode addressing;
-forward and training steps) under "paper_layer".
+and 8B layer shapes (H=2, sqrt(N)=240 and 480, d_v=960 and 1920, W=R=64,
+direct-mode addressing; forward and training steps) under "paper_layer".
 
 Printed: one JSON line.  `value` is forward tokens/s (B*T positions, all
 heads) over the timed steps; `roofline` gives the forward scan kernel's
@@ -448,75 +448,89 @@ def main():
         out["scoring"] = scoring_mfma(w, t_addr / max(n_addr, 1))
         del q, k, cb
 
-    # ------------------------------------------------------------ the paper's 1.4B layer
+    # ------------------------------------------------------------ the paper's 1.4B and 8B layers
     if (extra and args.only is None) or args.only == "paper":
-        # Table 1's 1.4B layer: H = 2, N = 240^2 slots of d_v = 960, top-64 reads and
-        # writes, direct-mode addressing (d_k = 2 sqrt(N)); 8 sequences of 4096 tokens
-        wp = synth.Workload("paper-1.4b-layer", B=8, H=2, T=4096, d_k=480, d_v=960, N=57600, topk=64,
-                            seed=6, codebook=False)
-        log("paper layer: generating inputs")
-        ip = synth.Inputs(wp)
-        q, k, v = to_dev(ip.q), to_dev(ip.k), to_dev(ip.v)
-        al, be = to_dev(ip.alpha), to_dev(ip.beta)
-        B, H, T = wp.B, wp.H, wp.T
-        mem = torch.empty((B, H, wp.N, wp.d_v), dtype=torch.float32, device=dev)
-        sdm.mem_init(mem, None)
-        ws = sdm.fwd_workspace(B, H, T, wp.topk, wp.topk, dev)
-        y = torch.empty((B, H, T, wp.d_v), dtype=torch.float32, device=dev)
-        pouts = {n: torch.empty((B, H, T, wp.topk), dtype=dt, device=dev)
-                 for n, dt in (("r_idx", torch.int32), ("r_val", torch.float32),
-                               ("w_idx", torch.int32), ("w_val", torch.float32))}
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-
-        def timed(fn, n):
-            fn()
-            torch.cuda.synchronize()
-            sdm.profile_enable(True)
-            e0.record(stream)
-            for _ in range(n):
-                fn()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            kms = {name: round(sdm.profile_read(name)[0] / n, 4)
-                   for name in ("address", "fwd_prep", "fwd_scan", "bwd_prep", "bwd_scan", "bwd_reduce",
-                                "address_bwd", "mem_init")}
-            sdm.profile_enable(False)
-            return e0.elapsed_time(e1) / n, {kk: vv for kk, vv in kms.items() if vv > 0}
-
-        log("paper layer: timing forward steps")
-        pms, pk = timed(lambda: sdm.forward(q, k, None, None, v, al, be, mem, wp.N, wp.topk, workspace=ws,
-                                            y=y, out=pouts), 5)
-        fbytes = fwd_scan_bytes_per_token_head(wp.topk, wp.topk, wp.d_v, 2) * B * H * T
-        res = {"workload": f"the paper's 1.4B layer shape: B={B} H={H} T={T} N={wp.N} (sqrt 240) d_v={wp.d_v} "
-                           f"top-{wp.topk} reads/writes, direct-mode addressing d_k={wp.d_k}, bf16 inputs, "
-                           f"fp32 memory",
-               "fwd": {"ms_per_step": round(pms, 3), "tokens_per_s": round(B * T / (pms * 1e-3), 1),
-                       "kernels_ms": pk, "scan_algorithmic_bytes": fbytes,
-                       "scan_GB_s": round(fbytes / (pk["fwd_scan"] * 1e-3) / 1e9, 1)}}
-        log("paper layer: timing training steps")
-        saved = sdm.saved_buffer(B, H, T, wp.topk, wp.d_v, dev)
-        bws = sdm.bwd_workspace(B, H, T, wp.topk, wp.topk, wp.d_v, dev)
-        dmem0 = torch.empty((B, H, wp.N, wp.d_v), dtype=torch.float32, device=dev)
-        dy = torch.from_numpy(ip.dy()).to(dev)
-
-        def pstep_train():
-            o = sdm.forward(q, k, None, None, v, al, be, mem, wp.N, wp.topk, saved=saved, workspace=ws, y=y,
-                            out=pouts)
-            sdm.scan_bwd(o["w_idx"], o["w_val"], o["r_idx"], o["r_val"], v, al, be, mem, saved, dy,
-                         d_k=wp.d_k, chunk=64, workspace=bws, dmem0=dmem0)
-
-        tms, tk = timed(pstep_train, 3)
-        # backward rows: (4W + 3R) d_v fp32 (M_t and G reads, G and undo writes, saved P), plus
-        # dy and dv (fp32) and v (bf16) per token-head
-        bbytes = ((4 * wp.topk + 3 * wp.topk) * wp.d_v * 4 + wp.d_v * (4 + 4 + 2)) * B * H * T
-        res["train"] = {"ms_per_step": round(tms, 3), "tokens_per_s": round(B * T / (tms * 1e-3), 1),
-                        "kernels_ms": tk, "bwd_scan_algorithmic_bytes": bbytes,
-                        "bwd_scan_GB_s": round(bbytes / (tk["bwd_scan"] * 1e-3) / 1e9, 1)}
-        out["paper_layer"] = res
-        del q, k, v, al, be, mem, ws, y, pouts, saved, bws, dmem0, dy
-        torch.cuda.empty_cache()
+        # Table 1's layers, direct-mode addressing (d_k = 2 sqrt(N)), top-64 reads and writes,
+        # H = 2: the 1.4B layer has N = 240^2 slots of d_v = 960 (8 sequences of 4096 tokens),
+        # the 8B layer N = 480^2 slots of d_v = 1920 (4 sequences of 4096 tokens)
+        shapes = (("1.4b", 240, synth.Workload("paper-1.4b-layer", B=8, H=2, T=4096, d_k=480, d_v=960,
+                                               N=57600, topk=64, seed=6, codebook=False)),
+                  ("8b", 480, synth.Workload("paper-8b-layer", B=4, H=2, T=4096, d_k=960, d_v=1920,
+                                             N=230400, topk=64, seed=8, codebook=False)))
+        out["paper_layer"] = {}
+        for tag, root, wp in shapes:
+            out["paper_layer"][tag] = paper_layer(sdm, to_dev, wp, tag, root, stream, dev)
 
     print(json.dumps(out), flush=True)
+
+
+def paper_layer(sdm, to_dev, wp, tag, root, stream, dev):
+    """Forward and training steps of one of the paper's layer shapes; returns the timings."""
+    import torch
+
+    import synth
+
+    log(f"paper {tag} layer: generating inputs")
+    ip = synth.Inputs(wp)
+    q, k, v = to_dev(ip.q), to_dev(ip.k), to_dev(ip.v)
+    al, be = to_dev(ip.alpha), to_dev(ip.beta)
+    B, H, T = wp.B, wp.H, wp.T
+    mem = torch.empty((B, H, wp.N, wp.d_v), dtype=torch.float32, device=dev)
+    sdm.mem_init(mem, None)
+    ws = sdm.fwd_workspace(B, H, T, wp.topk, wp.topk, dev)
+    y = torch.empty((B, H, T, wp.d_v), dtype=torch.float32, device=dev)
+    pouts = {n: torch.empty((B, H, T, wp.topk), dtype=dt, device=dev)
+             for n, dt in (("r_idx", torch.int32), ("r_val", torch.float32),
+                           ("w_idx", torch.int32), ("w_val", torch.float32))}
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn, n):
+        fn()
+        torch.cuda.synchronize()
+        sdm.profile_enable(True)
+        e0.record(stream)
+        for _ in range(n):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        kms = {name: round(sdm.profile_read(name)[0] / n, 4)
+               for name in ("address", "fwd_prep", "fwd_scan", "bwd_prep", "bwd_scan", "bwd_reduce",
+                            "address_bwd", "mem_init")}
+        sdm.profile_enable(False)
+        return e0.elapsed_time(e1) / n, {kk: vv for kk, vv in kms.items() if vv > 0}
+
+    log(f"paper {tag} layer: timing forward steps")
+    pms, pk = timed(lambda: sdm.forward(q, k, None, None, v, al, be, mem, wp.N, wp.topk, workspace=ws,
+                                        y=y, out=pouts), 5)
+    fbytes = fwd_scan_bytes_per_token_head(wp.topk, wp.topk, wp.d_v, 2) * B * H * T
+    res = {"workload": f"the paper's {tag.upper()} layer shape: B={B} H={H} T={T} N={wp.N} (sqrt {root}) "
+                       f"d_v={wp.d_v} top-{wp.topk} reads/writes, direct-mode addressing d_k={wp.d_k}, "
+                       f"bf16 inputs, fp32 memory",
+           "fwd": {"ms_per_step": round(pms, 3), "tokens_per_s": round(B * T / (pms * 1e-3), 1),
+                   "kernels_ms": pk, "scan_algorithmic_bytes": fbytes,
+                   "scan_GB_s": round(fbytes / (pk["fwd_scan"] * 1e-3) / 1e9, 1)}}
+    log(f"paper {tag} layer: timing training steps")
+    saved = sdm.saved_buffer(B, H, T, wp.topk, wp.d_v, dev)
+    bws = sdm.bwd_workspace(B, H, T, wp.topk, wp.topk, wp.d_v, dev)
+    dmem0 = torch.empty((B, H, wp.N, wp.d_v), dtype=torch.float32, device=dev)
+    dy = torch.from_numpy(ip.dy()).to(dev)
+
+    def pstep_train():
+        o = sdm.forward(q, k, None, None, v, al, be, mem, wp.N, wp.topk, saved=saved, workspace=ws, y=y,
+                        out=pouts)
+        sdm.scan_bwd(o["w_idx"], o["w_val"], o["r_idx"], o["r_val"], v, al, be, mem, saved, dy,
+                     d_k=wp.d_k, chunk=64, workspace=bws, dmem0=dmem0)
+
+    tms, tk = timed(pstep_train, 3)
+    # backward rows: (4W + 3R) d_v fp32 (M_t and G reads, G and undo writes, saved P), plus
+    # dy and dv (fp32) and v (bf16) per token-head
+    bbytes = ((4 * wp.topk + 3 * wp.topk) * wp.d_v * 4 + wp.d_v * (4 + 4 + 2)) * B * H * T
+    res["train"] = {"ms_per_step": round(tms, 3), "tokens_per_s": round(B * T / (tms * 1e-3), 1),
+                    "kernels_ms": tk, "bwd_scan_algorithmic_bytes": bbytes,
+                    "bwd_scan_GB_s": round(bbytes / (tk["bwd_scan"] * 1e-3) / 1e9, 1)}
+    del q, k, v, al, be, mem, ws, y, pouts, saved, bws, dmem0, dy
+    torch.cuda.empty_cache()
+    return res
 
 
 if __name__ == "__main__":
