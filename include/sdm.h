@@ -154,6 +154,34 @@ size_t sdm_scan_fwd_workspace_bytes(int B, int H, int T, int W, int R);
 size_t sdm_scan_saved_bytes(int B, int H, int T, int W, int d_v);
 
 /* ------------------------------------------------------------------------
+ * sdm_scan_fwd_chunked — the recurrence of sdm_scan_fwd by the chunk-parallel
+ * form of App. A.1-A.2, for inference.  Tokens are taken 64 at a time.  Within
+ * a chunk starting from the table M0, with lambda_{t,i} the sum of log alpha_s
+ * over the chunk's tokens s <= t that write slot i, the innovations
+ * x_t = beta_t (v_t - u_t) solve the unit lower-triangular system
+ * (I + diag(beta) A) x = diag(beta) (V - retrieved) with the gated sparse inner
+ * products A of App. A.2 (Eq. sparse-ip); the reads are the decayed M0 rows plus
+ * a triangular product QK x; each slot written in the chunk is then stored
+ * once.  The first kernel (all chunks in parallel) builds per-chunk
+ * coefficients from the slot lists and gates alone; the second walks the
+ * chunks of each stream in order, one workgroup per 32 columns.  Results equal
+ * sdm_scan_fwd's up to the rounding of the reassociated sums and of the
+ * triangular solve.
+ *   Arguments as for sdm_scan_fwd, without the undo log; workspace of at least
+ *   sdm_scan_fwd_chunked_workspace_bytes() bytes (256-B aligned), which holds
+ *   about (8 C^2 + 8 C (W + R) + 16 C W) bytes per stream and chunk (C = 64).
+ * Limits: W, R <= 64 (SDM_ERR_UNSUPPORTED beyond); forget gates must be > 0
+ * (the decays are taken in log form): a gate <= 0 is treated as 1e-30 and
+ * flagged for sdm_check_device_errors, as are out-of-range slot ids (clamped).
+ * ---------------------------------------------------------------------- */
+int sdm_scan_fwd_chunked(const int32_t* w_idx, const float* w_val, int W,
+                         const int32_t* r_idx, const float* r_val, int R,
+                         const void* v, const void* alpha, const void* beta, int in_dtype,
+                         float* mem, int B, int H, int T, int d_v, int64_t N,
+                         float* y, void* workspace, size_t ws_bytes, void* stream);
+size_t sdm_scan_fwd_chunked_workspace_bytes(int B, int H, int T, int W, int R);
+
+/* ------------------------------------------------------------------------
  * sdm_scan_bwd — reverse mode of sdm_scan_fwd plus the addressing gradient.
  * Past memory states are recovered by undoing the in-place writes from the
  * saved pre-write rows (App. A.3); per token the forward intermediates
@@ -266,7 +294,7 @@ int sdm_set_scan_line_io(int on);
 enum sdm_kernel {
     SDM_K_ADDRESS = 0, SDM_K_FWD_PREP = 1, SDM_K_FWD_SCAN = 2, SDM_K_BWD_PREP = 3,
     SDM_K_BWD_SCAN = 4, SDM_K_BWD_REDUCE = 5, SDM_K_ADDRESS_BWD = 6, SDM_K_MEM_INIT = 7,
-    SDM_K_DECODE = 8, SDM_K_COUNT = 9
+    SDM_K_DECODE = 8, SDM_K_CHUNK_COEF = 9, SDM_K_CHUNK_SCAN = 10, SDM_K_COUNT = 11
 };
 int sdm_profile_enable(int on);
 /* Which kernel kinds the events bracket while profiling is enabled: bit k for
@@ -278,8 +306,9 @@ int sdm_profile_read(int kernel, double* total_ms, int64_t* launches);
 /* ------------------------------------------------------------------------
  * Diagnostics.
  *   sdm_check_device_errors  synchronises `stream`, then reports whether
- *       any scan since the last check clamped an out-of-range slot id
- *       (SDM_ERR_DEVICE_CHECK) and clears the flag held in `workspace`.
+ *       any scan since the last check clamped an out-of-range slot id, or
+ *       the chunked scan met a forget gate <= 0 (SDM_ERR_DEVICE_CHECK), and
+ *       clears the flag held in `workspace`.
  *   sdm_status_string        static text for a status code.
  *   sdm_last_error           thread-local text of the last failure.
  *   sdm_version              library version string.

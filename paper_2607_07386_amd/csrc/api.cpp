@@ -360,6 +360,50 @@ int sdm_scan_fwd(const int32_t* w_idx, const float* w_val, int W, const int32_t*
     return SDM_OK;
 }
 
+size_t sdm_scan_fwd_chunked_workspace_bytes(int B, int H, int T, int W, int R) {
+    if (B < 0 || H < 0 || T < 0 || W < 1 || R < 1) return 0;
+    return sdm_chunk_ws_bytes(B, H, T, W, R);
+}
+
+int sdm_scan_fwd_chunked(const int32_t* w_idx, const float* w_val, int W, const int32_t* r_idx,
+                         const float* r_val, int R, const void* v, const void* alpha, const void* beta,
+                         int in_dtype, float* mem, int B, int H, int T, int d_v, int64_t N, float* y,
+                         void* workspace, size_t ws_bytes, void* stream) {
+    g_err[0] = 0;
+    int rc = check_scan_common(w_idx, w_val, W, r_idx, r_val, R, v, alpha, beta, in_dtype, mem, B,
+                               H, T, d_v, N);
+    if (rc != SDM_OK) return rc;
+    if ((int64_t)B * H * T == 0) return SDM_OK;
+    if (!y || !aligned(y, 16)) return fail(SDM_ERR_INVALID_ARG, "y must be a 16-byte aligned pointer");
+    if (!sdm_chunk_shape_ok(W, R))
+        return fail(SDM_ERR_UNSUPPORTED, "the chunked scan takes W, R <= %d (got W=%d R=%d)",
+                    SDM_CHUNK_MAX_LIST, W, R);
+    const size_t need = sdm_chunk_ws_bytes(B, H, T, W, R);
+    if (!workspace || !aligned(workspace, 256))
+        return fail(SDM_ERR_INVALID_ARG, "workspace must be a 256-byte aligned pointer");
+    if (ws_bytes < need) return fail(SDM_ERR_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, need);
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e = sdm_launch_zero_words(workspace, 4, st);
+    if (e != hipSuccess) return hip_fail(e, "sdm_scan_fwd_chunked flag reset");
+    ScanFwdArgs a;
+    a.w_idx = w_idx; a.w_val = w_val; a.r_idx = r_idx; a.r_val = r_val;
+    a.v = v; a.alpha = alpha; a.beta = beta; a.in_dtype = in_dtype;
+    a.mem = mem; a.B = B; a.H = H; a.T = T; a.dv = d_v; a.W = W; a.R = R; a.N = N;
+    a.y = y; a.saved = nullptr; a.ws = static_cast<unsigned char*>(workspace);
+    a.tb = 0; a.te = T;
+    {
+        SdmProfScope ps(SDM_K_CHUNK_COEF, st);
+        e = sdm_launch_chunk_coef(a, st);
+    }
+    if (e != hipSuccess) return hip_fail(e, "sdm_scan_fwd_chunked coefficient launch");
+    {
+        SdmProfScope ps(SDM_K_CHUNK_SCAN, st);
+        e = sdm_launch_chunk_scan(a, st);
+    }
+    if (e != hipSuccess) return hip_fail(e, "sdm_scan_fwd_chunked scan launch");
+    return SDM_OK;
+}
+
 // ---- fused forward: addressing pipelined with the scan over chunks of tokens ----
 
 int sdm_forward(const void* q, const void* k, int x_dtype, const void* cb_q, const void* cb_k, int d_k,
@@ -656,7 +700,8 @@ int sdm_check_device_errors(void* workspace, void* stream) {
         e = sdm_launch_zero_words(workspace, 1, st);
         if (e == hipSuccess) e = hipStreamSynchronize(st);
         if (e != hipSuccess) return hip_fail(e, "sdm_check_device_errors clear");
-        return fail(SDM_ERR_DEVICE_CHECK, "a slot id outside [0, N) was clamped");
+        if (flag & 1u) return fail(SDM_ERR_DEVICE_CHECK, "a slot id outside [0, N) was clamped");
+        return fail(SDM_ERR_DEVICE_CHECK, "the chunked scan met a forget gate alpha <= 0");
     }
     return SDM_OK;
 }

@@ -1,0 +1,478 @@
+// Chunk-parallel schedule of the forward scan (App. A.1, A.2): the recurrence
+// of sdm_scan_fwd computed 64 tokens at a time.  Within a chunk starting from
+// the table M0, with lambda_{t,i} the sum of log alpha_s over the chunk's
+// tokens s <= t that write slot i (decay only on written rows), the decayed
+// innovations x_t = beta_t (v_t - u_t) solve
+//   (I + diag(beta) A) x = diag(beta) (V - retrieved),
+//   A[t][s]   = sum over slots i written by t and s < t of
+//               kappa_t(i) kappa_s(i) exp(lambda_{t,i} - lambda_{s,i}),
+//   retrieved_t = sum_n kappa_{t,n} exp(lambda_{t,i_n}) M0[i_n],
+// the reads are
+//   y_t = sum_m rho_{t,m} exp(lambda_{t,j_m}) M0[j_m] + sum_{s<=t} QK[t][s] x_s,
+//   QK[t][s]  = sum over slots j read by t and written by s of
+//               rho_t(j) kappa_s(j) exp(lambda_{t,j} - lambda_{s,j}),
+// and every slot written in the chunk ends at
+//   M[i] = exp(lambda_{C,i}) M0[i] + sum_s kappa_s(i) exp(lambda_{C,i} - lambda_{s,i}) x_s.
+//
+// Two kernels.  chunk_coef_kernel (one workgroup per stream and chunk, all
+// chunks at once) needs only the slot lists and gates: it sorts the chunk's
+// write entries by (slot, token), takes lambda as a running sum along each
+// slot's entries, accumulates A and QK from the pairs inside a slot's entries,
+// inverts the unit lower-triangular system into L = (I + diag(beta) A)^-1
+// diag(beta), and stores L, QK, the gather weights and the per-slot scatter
+// lists as one record per chunk.  chunk_scan_kernel (one workgroup per stream
+// and 32-column slice) walks the chunks in order: gathers of retrieved and of
+// the reads' first term from the chunk-start table, x = L (V - retrieved) and
+// y = inter + QK x from LDS, then one store of every written slot.
+#include "sdm_common.h"
+#include "sdm_internal.h"
+
+namespace {
+
+constexpr int CC = SDM_CHUNK;       // tokens per chunk
+constexpr int CT1 = 256;            // threads of the coefficient kernel
+constexpr int CT2 = 512;            // threads of the scan kernel: one (token, column quad) each
+constexpr int CCOLS = 32;           // columns per scan workgroup (one 128-byte line of a row)
+constexpr int LDP = CC + 1;         // padded row stride of L and QK in LDS
+constexpr int CK_LDS_LIMIT = 160 * 1024;
+static_assert(CT2 == CC * (CCOLS / 4), "one thread per (token, column quad) of a chunk");
+
+// Per-chunk record: nseg, then L and QK [C][C], the gather weights
+// exp(lambda) kappa [C][W] and exp(lambda) rho [C][R], then per written slot
+// (sorted by id) its first entry, id and decay exp(lambda_C), and per entry
+// (sorted by slot, then token) its token and scatter weight.
+struct ChunkRec {
+    int off_l, off_qk, off_cr, off_cy, off_sbeg, off_sslot, off_sdec, off_etok, off_ecoef, bytes;
+};
+
+__host__ __device__ inline ChunkRec chunk_rec_layout(int W, int R) {
+    ChunkRec r;
+    const int E = CC * W;
+    int o = 16;
+    r.off_l = o;     o += CC * CC * 4;
+    r.off_qk = o;    o += CC * CC * 4;
+    r.off_cr = o;    o += CC * W * 4;
+    r.off_cy = o;    o += CC * R * 4;
+    r.off_sbeg = o;  o += (E + 1) * 4;
+    o = (o + 15) & ~15;
+    r.off_sslot = o; o += E * 4;
+    r.off_sdec = o;  o += E * 4;
+    r.off_etok = o;  o += E * 4;
+    r.off_ecoef = o; o += E * 4;
+    r.bytes = (o + 255) & ~255;
+    return r;
+}
+
+inline int pow2_at_least(int x) {
+    int p = 64;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+inline size_t coef_lds_bytes(int W) {
+    const int P = pow2_at_least(CC * W);
+    return (size_t)P * 8 + (size_t)3 * CC * W * 4 + (size_t)3 * CC * CC * 4 + 2 * CC * 4 + (CT1 + 1) * 4;
+}
+
+__device__ __forceinline__ unsigned long long key_slot(unsigned long long k) { return k >> 16; }
+__device__ __forceinline__ int key_tok(unsigned long long k) { return (int)((k >> 8) & 255); }
+__device__ __forceinline__ int key_ent(unsigned long long k) { return (int)(k & 255); }
+
+template <typename VT>
+__global__ __launch_bounds__(CT1) void chunk_coef_kernel(
+    const int32_t* __restrict__ w_idx, const float* __restrict__ w_val, const int32_t* __restrict__ r_idx,
+    const float* __restrict__ r_val, const VT* __restrict__ alpha, const VT* __restrict__ beta, int T, int W,
+    int R, int64_t N, int nch, int P, unsigned char* __restrict__ recs, unsigned int* __restrict__ err) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const ChunkRec L = chunk_rec_layout(W, R);
+    const int tid = threadIdx.x;
+    const int s = blockIdx.x / nch, c = blockIdx.x - s * nch;
+    const int t0 = c * CC, n = min(CC, T - t0);
+    const int E = n * W;
+    const size_t tok0 = (size_t)s * T + t0;
+
+    unsigned long long* keys = reinterpret_cast<unsigned long long*>(smem);   // [P]
+    float* kap = reinterpret_cast<float*>(keys + P);    // [C*W] kappa at (t, n)
+    float* lamw = kap + CC * W;                          // [C*W] lambda at (t, n)
+    float* lams = lamw + CC * W;                         // [C*W] lambda in sorted order
+    float* A = lams + CC * W;                            // [C][C]
+    float* QK = A + CC * CC;                             // [C][C]
+    float* Lm = QK + CC * CC;                            // [C][C]
+    float* la = Lm + CC * CC;                            // [C] log alpha
+    float* bt = la + CC;                                 // [C] beta
+    int* cnt = reinterpret_cast<int*>(bt + CC);          // [CT1 + 1]
+
+    unsigned char* rec = recs + (size_t)blockIdx.x * L.bytes;
+    float* g_cr = reinterpret_cast<float*>(rec + L.off_cr);
+    float* g_cy = reinterpret_cast<float*>(rec + L.off_cy);
+    int* g_sbeg = reinterpret_cast<int*>(rec + L.off_sbeg);
+    int* g_sslot = reinterpret_cast<int*>(rec + L.off_sslot);
+    float* g_sdec = reinterpret_cast<float*>(rec + L.off_sdec);
+    int* g_etok = reinterpret_cast<int*>(rec + L.off_etok);
+    float* g_ecoef = reinterpret_cast<float*>(rec + L.off_ecoef);
+
+    unsigned int bad = 0;
+    // ---- write entries as sort keys (slot, token, entry); gates ----
+    for (int e = tid; e < P; e += CT1) {
+        unsigned long long key = ~0ull;
+        if (e < E) {
+            const int t = e / W, j = e - t * W;
+            int64_t id = w_idx[(tok0 + t) * W + j];
+            if (id < 0 || id >= N) {
+                bad |= 1u;
+                id = id < 0 ? 0 : N - 1;
+            }
+            key = ((unsigned long long)id << 16) | (unsigned long long)(t << 8) | (unsigned long long)j;
+            kap[e] = w_val[(tok0 + t) * W + j];
+        }
+        keys[e] = key;
+    }
+    for (int t = tid; t < CC; t += CT1) {
+        float a = 1.f, b = 0.f;
+        if (t < n) {
+            a = to_f32(alpha[tok0 + t]);
+            b = to_f32(beta[tok0 + t]);
+            if (!(a > 0.f)) bad |= 2u;   // the log form needs alpha > 0
+        }
+        la[t] = logf(fmaxf(a, 1e-30f));
+        bt[t] = b;
+    }
+    for (int i = tid; i < 3 * CC * CC; i += CT1) A[i] = 0.f;   // A, QK, L
+    __syncthreads();
+
+    // ---- bitonic sort of the keys, ascending ----
+    for (int k = 2; k <= P; k <<= 1)
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = tid; i < P; i += CT1) {
+                const int l = i ^ j;
+                if (l > i) {
+                    const unsigned long long x = keys[i], y = keys[l];
+                    if ((x > y) == ((i & k) == 0)) {
+                        keys[i] = y;
+                        keys[l] = x;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+
+    // ---- lambda: running sum of log alpha along each slot's entries (token order) ----
+    for (int e = tid; e < E; e += CT1) {
+        const unsigned long long ke = keys[e];
+        float sum = la[key_tok(ke)];
+        for (int f = e - 1; f >= 0 && key_slot(keys[f]) == key_slot(ke); --f) sum += la[key_tok(keys[f])];
+        lams[e] = sum;
+        lamw[key_tok(ke) * W + key_ent(ke)] = sum;
+    }
+    __syncthreads();
+
+    // ---- segments (one per distinct written slot), numbered in sorted order ----
+    const int ept = (E + CT1 - 1) / CT1;
+    const int e0 = min(E, tid * ept), e1 = min(E, e0 + ept);
+    int ns = 0;
+    for (int e = e0; e < e1; ++e) ns += (e == 0 || key_slot(keys[e]) != key_slot(keys[e - 1])) ? 1 : 0;
+    cnt[tid] = ns;
+    __syncthreads();
+    for (int d = 1; d < CT1; d <<= 1) {
+        const int v = cnt[tid] + (tid >= d ? cnt[tid - d] : 0);
+        __syncthreads();
+        cnt[tid] = v;
+        __syncthreads();
+    }
+    {
+        int g = cnt[tid] - ns;
+        for (int e = e0; e < e1; ++e) {
+            if (!(e == 0 || key_slot(keys[e]) != key_slot(keys[e - 1]))) continue;
+            int f = e;
+            while (f + 1 < E && key_slot(keys[f + 1]) == key_slot(keys[e])) ++f;
+            g_sbeg[g] = e;
+            g_sslot[g] = (int)key_slot(keys[e]);
+            g_sdec[g] = expf(lams[f]);
+            ++g;
+        }
+        if (tid == CT1 - 1) {
+            g_sbeg[cnt[CT1 - 1]] = E;
+            *reinterpret_cast<int*>(rec) = cnt[CT1 - 1];
+        }
+    }
+
+    // ---- per entry: scatter weight, and A from every earlier writer of the slot ----
+    for (int e = tid; e < E; e += CT1) {
+        const unsigned long long ke = keys[e];
+        const unsigned long long se = key_slot(ke);
+        int f = e;
+        while (f + 1 < E && key_slot(keys[f + 1]) == se) ++f;
+        const int t = key_tok(ke);
+        const float kt = kap[t * W + key_ent(ke)], le = lams[e];
+        g_etok[e] = t;
+        g_ecoef[e] = kt * expf(lams[f] - le);
+        for (int g = e - 1; g >= 0 && key_slot(keys[g]) == se; --g) {
+            const unsigned long long kg = keys[g];
+            atomicAdd(&A[t * CC + key_tok(kg)], kt * kap[key_tok(kg) * W + key_ent(kg)] * expf(le - lams[g]));
+        }
+    }
+    // ---- gather weights of the write side ----
+    for (int e = tid; e < E; e += CT1) g_cr[e] = kap[e] * expf(lamw[e]);
+    // ---- read side: lambda of the read slot after token t, gather weight, QK ----
+    for (int e = tid; e < n * R; e += CT1) {
+        const int t = e / R, m = e - t * R;
+        int64_t id = r_idx[(tok0 + t) * R + m];
+        if (id < 0 || id >= N) {
+            bad |= 1u;
+            id = id < 0 ? 0 : N - 1;
+        }
+        const float rho = r_val[(tok0 + t) * R + m];
+        int lo = 0, hi = E;
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (key_slot(keys[mid]) < (unsigned long long)id) lo = mid + 1;
+            else hi = mid;
+        }
+        int last = lo - 1;
+        while (last + 1 < E && key_slot(keys[last + 1]) == (unsigned long long)id && key_tok(keys[last + 1]) <= t)
+            ++last;
+        const float lr = last >= lo ? lams[last] : 0.f;
+        g_cy[t * R + m] = rho * expf(lr);
+        for (int f = lo; f <= last; ++f) {
+            const unsigned long long kf = keys[f];
+            atomicAdd(&QK[t * CC + key_tok(kf)], rho * kap[key_tok(kf) * W + key_ent(kf)] * expf(lr - lams[f]));
+        }
+    }
+    __syncthreads();
+
+    // ---- L = (I + diag(beta) A)^-1 diag(beta): one column per thread, forward substitution ----
+    if (tid < n) {
+        const int cc = tid;
+        Lm[cc * CC + cc] = bt[cc];
+        for (int t = cc + 1; t < n; ++t) {
+            float acc = 0.f;
+            for (int u = cc; u < t; ++u) acc += A[t * CC + u] * Lm[u * CC + cc];
+            Lm[t * CC + cc] = -bt[t] * acc;
+        }
+    }
+    __syncthreads();
+    {
+        float4* gl = reinterpret_cast<float4*>(rec + L.off_l);     // L then QK, contiguous
+        float4* gq = reinterpret_cast<float4*>(rec + L.off_qk);
+        const float4* sl = reinterpret_cast<const float4*>(Lm);
+        const float4* sq = reinterpret_cast<const float4*>(QK);
+        for (int i = tid; i < CC * CC / 4; i += CT1) {
+            gl[i] = sl[i];
+            gq[i] = sq[i];
+        }
+    }
+    if (bad) atomicOr(err, bad);
+}
+
+// LDS of the scan kernel beyond its static arrays: the chunk's slot ids and
+// gather weights, and (SEG) its scatter lists.
+inline size_t scan_dyn_lds(int W, int R, bool seg) {
+    const ChunkRec L = chunk_rec_layout(W, R);
+    size_t b = (size_t)CC * (W + R) * 8;
+    if (seg) b += (size_t)(L.off_ecoef + CC * W * 4 - L.off_sbeg);
+    return b;
+}
+
+constexpr int GB = 32;   // row gathers in flight per thread
+constexpr int SB = 16;   // scatter rows in flight per thread
+
+template <typename VT, bool SEG>
+__global__ __launch_bounds__(CT2) void chunk_scan_kernel(const int32_t* __restrict__ w_idx,
+                                                         const int32_t* __restrict__ r_idx, const VT* __restrict__ v,
+                                                         float* __restrict__ mem, float* __restrict__ y,
+                                                         const unsigned char* __restrict__ recs, int T, int W, int R,
+                                                         int64_t N, int dv, int nch, int nslice) {
+    __shared__ float Ls[CC * LDP];
+    __shared__ float Qs[CC * LDP];
+    __shared__ __align__(16) float Rr[CC * CCOLS];
+    __shared__ __align__(16) float Xs[CC * CCOLS];
+    extern __shared__ __align__(16) unsigned char dyn[];
+    const ChunkRec L = chunk_rec_layout(W, R);
+    const int WR = W + R;
+    int* sid = reinterpret_cast<int*>(dyn);                    // [C][W] write ids, then [C][R] read ids
+    float* scf = reinterpret_cast<float*>(sid + CC * WR);      // [C][W] then [C][R] gather weights
+    unsigned char* sseg = reinterpret_cast<unsigned char*>(scf + CC * WR);   // scatter lists (SEG)
+    const int seg_bytes = L.off_ecoef + CC * W * 4 - L.off_sbeg;
+
+    const int tid = threadIdx.x;
+    const int s = blockIdx.x / nslice, sl = blockIdx.x - s * nslice;
+    const int q = tid & 7;                  // column quad within the slice
+    const int tl = tid >> 3;                // token within the chunk
+    const int col = sl * CCOLS + q * 4;
+    const bool colok = col < dv;
+    float* ms = mem + (size_t)s * N * dv;
+
+    for (int c = 0; c < nch; ++c) {
+        const unsigned char* rec = recs + ((size_t)s * nch + c) * L.bytes;
+        const int t0 = c * CC, n = min(CC, T - t0);
+        const size_t tk0 = (size_t)s * T + t0;
+        // ---- stage the chunk's record and slot ids ----
+        {
+            const float4* gl = reinterpret_cast<const float4*>(rec + L.off_l);
+            const float4* gq = reinterpret_cast<const float4*>(rec + L.off_qk);
+            for (int i = tid; i < CC * CC / 4; i += CT2) {
+                const float4 a = gl[i], b = gq[i];
+                const int r = (4 * i) / CC, k = (4 * i) % CC;
+                Ls[r * LDP + k] = a.x; Ls[r * LDP + k + 1] = a.y; Ls[r * LDP + k + 2] = a.z; Ls[r * LDP + k + 3] = a.w;
+                Qs[r * LDP + k] = b.x; Qs[r * LDP + k + 1] = b.y; Qs[r * LDP + k + 2] = b.z; Qs[r * LDP + k + 3] = b.w;
+            }
+            // gather weights: [C][W] then [C][R], contiguous in the record
+            const float* gcf = reinterpret_cast<const float*>(rec + L.off_cr);
+            for (int i = tid; i < CC * WR; i += CT2) scf[i] = gcf[i];
+            for (int i = tid; i < n * W; i += CT2) {
+                int64_t id = w_idx[tk0 * W + i];
+                sid[i] = (int)(id < 0 ? 0 : (id >= N ? N - 1 : id));
+            }
+            for (int i = tid; i < n * R; i += CT2) {
+                int64_t id = r_idx[tk0 * R + i];
+                sid[CC * W + i] = (int)(id < 0 ? 0 : (id >= N ? N - 1 : id));
+            }
+            if (SEG) {
+                const float4* gs = reinterpret_cast<const float4*>(rec + L.off_sbeg);
+                float4* ls = reinterpret_cast<float4*>(sseg);
+                for (int i = tid; i < seg_bytes / 16; i += CT2) ls[i] = gs[i];
+            }
+        }
+        __syncthreads();
+        // ---- gathers from the chunk-start table, GB rows in flight ----
+        float4 inter = make_float4(0.f, 0.f, 0.f, 0.f);
+        float4 rr = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (tl < n && colok) {
+            float4 ret = make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int j0 = 0; j0 < WR; j0 += GB) {
+                float4 m[GB];
+#pragma unroll
+                for (int jj = 0; jj < GB; ++jj) {
+                    const int j = j0 + jj;
+                    // past the lists: row 0 (in bounds, unused)
+                    const int id = j < W ? sid[tl * W + j] : (j < WR ? sid[CC * W + tl * R + (j - W)] : 0);
+                    m[jj] = load4(ms + (size_t)id * dv + col);
+                }
+#pragma unroll
+                for (int jj = 0; jj < GB; ++jj) {
+                    const int j = j0 + jj;
+                    if (j < W) {
+                        const float w = scf[tl * W + j];
+                        ret.x += w * m[jj].x; ret.y += w * m[jj].y; ret.z += w * m[jj].z; ret.w += w * m[jj].w;
+                    } else if (j < WR) {
+                        const float w = scf[CC * W + tl * R + (j - W)];
+                        inter.x += w * m[jj].x; inter.y += w * m[jj].y; inter.z += w * m[jj].z; inter.w += w * m[jj].w;
+                    }
+                }
+            }
+            const float4 vv = load4(v + (tk0 + tl) * dv + col);
+            rr = make_float4(vv.x - ret.x, vv.y - ret.y, vv.z - ret.z, vv.w - ret.w);
+        }
+        *reinterpret_cast<float4*>(&Rr[tl * CCOLS + q * 4]) = rr;
+        __syncthreads();
+        // ---- x = L (V - retrieved) ----
+        {
+            float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int u = 0; u <= tl && u < n; ++u) {
+                const float l = Ls[tl * LDP + u];
+                const float4 r = *reinterpret_cast<const float4*>(&Rr[u * CCOLS + q * 4]);
+                acc.x += l * r.x; acc.y += l * r.y; acc.z += l * r.z; acc.w += l * r.w;
+            }
+            *reinterpret_cast<float4*>(&Xs[tl * CCOLS + q * 4]) = acc;
+        }
+        __syncthreads();
+        // ---- y = inter + QK x ----
+        if (tl < n && colok) {
+            float4 acc = inter;
+            for (int u = 0; u <= tl; ++u) {
+                const float w = Qs[tl * LDP + u];
+                const float4 x = *reinterpret_cast<const float4*>(&Xs[u * CCOLS + q * 4]);
+                acc.x += w * x.x; acc.y += w * x.y; acc.z += w * x.z; acc.w += w * x.w;
+            }
+            *reinterpret_cast<float4*>(y + (tk0 + tl) * dv + col) = acc;
+        }
+        // ---- one store per written slot: decayed chunk-start row plus its tokens' x ----
+        {
+            // the lists in LDS (SEG) or in the record
+            const unsigned char* sb = SEG ? sseg : rec + L.off_sbeg;
+            const int nseg = *reinterpret_cast<const int*>(rec);
+            const int* sbeg = reinterpret_cast<const int*>(sb);
+            const int* sslot = reinterpret_cast<const int*>(sb + (L.off_sslot - L.off_sbeg));
+            const float* sdec = reinterpret_cast<const float*>(sb + (L.off_sdec - L.off_sbeg));
+            const int* etok = reinterpret_cast<const int*>(sb + (L.off_etok - L.off_sbeg));
+            const float* ecoef = reinterpret_cast<const float*>(sb + (L.off_ecoef - L.off_sbeg));
+            if (colok) {
+                for (int g0 = tl; g0 < nseg; g0 += SB * (CT2 / 8)) {
+                    float4 m[SB];
+#pragma unroll
+                    for (int b = 0; b < SB; ++b) {
+                        const int g = g0 + b * (CT2 / 8);
+                        // past the last segment: reload segment g0's row (in bounds, unused)
+                        m[b] = load4(ms + (size_t)sslot[g < nseg ? g : g0] * dv + col);
+                    }
+#pragma unroll
+                    for (int b = 0; b < SB; ++b) {
+                        const int g = g0 + b * (CT2 / 8);
+                        if (g < nseg) {
+                            const float d = sdec[g];
+                            float4 acc = make_float4(d * m[b].x, d * m[b].y, d * m[b].z, d * m[b].w);
+                            const int fe = sbeg[g + 1];
+                            for (int f = sbeg[g]; f < fe; ++f) {
+                                const float w = ecoef[f];
+                                const float4 x = *reinterpret_cast<const float4*>(&Xs[etok[f] * CCOLS + q * 4]);
+                                acc.x += w * x.x; acc.y += w * x.y; acc.z += w * x.z; acc.w += w * x.w;
+                            }
+                            *reinterpret_cast<float4*>(ms + (size_t)sslot[g] * dv + col) = acc;
+                        }
+                    }
+                }
+            }
+        }
+        __syncthreads();
+    }
+}
+
+template <typename VT>
+hipError_t launch_chunk_coef(const ScanFwdArgs& a, hipStream_t st) {
+    const int S = a.B * a.H, nch = (a.T + CC - 1) / CC;
+    const int P = pow2_at_least(CC * a.W);
+    const size_t lds = coef_lds_bytes(a.W);
+    auto kl = chunk_coef_kernel<VT>;
+    hipError_t e = hipFuncSetAttribute((const void*)kl, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kl, dim3((unsigned)(S * nch)), dim3(CT1), lds, st, a.w_idx, a.w_val, a.r_idx, a.r_val,
+                       static_cast<const VT*>(a.alpha), static_cast<const VT*>(a.beta), a.T, a.W, a.R, a.N, nch, P,
+                       a.ws + SDM_WS_HEADER, reinterpret_cast<unsigned int*>(a.ws));
+    return hipGetLastError();
+}
+
+template <typename VT>
+hipError_t launch_chunk_scan(const ScanFwdArgs& a, hipStream_t st) {
+    const int S = a.B * a.H, nch = (a.T + CC - 1) / CC;
+    const int nslice = (a.dv + CCOLS - 1) / CCOLS;
+    constexpr size_t static_lds = (size_t)2 * CC * LDP * 4 + (size_t)2 * CC * CCOLS * 4;
+    const bool seg = static_lds + scan_dyn_lds(a.W, a.R, true) <= (size_t)CK_LDS_LIMIT;
+    const size_t lds = scan_dyn_lds(a.W, a.R, seg);
+    auto kl = seg ? chunk_scan_kernel<VT, true> : chunk_scan_kernel<VT, false>;
+    hipError_t e = hipFuncSetAttribute((const void*)kl, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kl, dim3((unsigned)(S * nslice)), dim3(CT2), lds, st, a.w_idx, a.r_idx,
+                       static_cast<const VT*>(a.v), a.mem, a.y, a.ws + SDM_WS_HEADER, a.T, a.W, a.R, a.N, a.dv,
+                       nch, nslice);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bool sdm_chunk_shape_ok(int W, int R) {
+    return W >= 1 && R >= 1 && W <= SDM_CHUNK_MAX_LIST && R <= SDM_CHUNK_MAX_LIST &&
+           coef_lds_bytes(W) <= (size_t)CK_LDS_LIMIT;
+}
+
+size_t sdm_chunk_ws_bytes(int B, int H, int T, int W, int R) {
+    const size_t nch = ((size_t)T + CC - 1) / CC;
+    return SDM_WS_HEADER + (size_t)B * H * nch * chunk_rec_layout(W, R).bytes;
+}
+
+hipError_t sdm_launch_chunk_coef(const ScanFwdArgs& a, hipStream_t st) {
+    return a.in_dtype == SDM_DT_BF16 ? launch_chunk_coef<bf16_t>(a, st) : launch_chunk_coef<float>(a, st);
+}
+
+hipError_t sdm_launch_chunk_scan(const ScanFwdArgs& a, hipStream_t st) {
+    return a.in_dtype == SDM_DT_BF16 ? launch_chunk_scan<bf16_t>(a, st) : launch_chunk_scan<float>(a, st);
+}

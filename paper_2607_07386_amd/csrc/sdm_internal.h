@@ -107,6 +107,16 @@ size_t sdm_fwd_ws_bytes(int B, int H, int T, int W, int R);
 template <int PD>
 hipError_t sdm_launch_fwd_prep(const ScanFwdArgs& a, hipStream_t st);
 
+// Chunk-parallel forward scan: tokens in chunks of SDM_CHUNK, W and R at most
+// SDM_CHUNK_MAX_LIST.  The coefficient kernel writes one record per (stream,
+// chunk) after the workspace header; the scan kernel reads them (a.saved unused).
+#define SDM_CHUNK 64
+#define SDM_CHUNK_MAX_LIST 64
+bool sdm_chunk_shape_ok(int W, int R);
+size_t sdm_chunk_ws_bytes(int B, int H, int T, int W, int R);
+hipError_t sdm_launch_chunk_coef(const ScanFwdArgs& a, hipStream_t st);
+hipError_t sdm_launch_chunk_scan(const ScanFwdArgs& a, hipStream_t st);
+
 struct ScanBwdArgs {
     const int32_t* w_idx;
     const float* w_val;

@@ -48,10 +48,13 @@ def lib() -> ctypes.CDLL:
         L.sdm_mem_init.argtypes = [P, P, I, I, I64, I, P]
         L.sdm_forward.argtypes = [P, P, I, P, P, I, I, P, P, P, I, P, I, I, I, I, I64, P, P, P, P, P, P,
                                   SZ, I, P, SZ, P]
+        L.sdm_scan_fwd_chunked.argtypes = [P, P, I, P, P, I, P, P, P, I, P, I, I, I, I, I64, P, P, SZ, P]
         L.sdm_scan_fwd_workspace_bytes.argtypes = [I, I, I, I, I]
+        L.sdm_scan_fwd_chunked_workspace_bytes.argtypes = [I, I, I, I, I]
         L.sdm_scan_saved_bytes.argtypes = [I, I, I, I, I]
         L.sdm_scan_bwd_workspace_bytes.argtypes = [I, I, I, I, I, I]
-        for f in ("sdm_scan_fwd_workspace_bytes", "sdm_scan_saved_bytes", "sdm_scan_bwd_workspace_bytes"):
+        for f in ("sdm_scan_fwd_workspace_bytes", "sdm_scan_saved_bytes", "sdm_scan_bwd_workspace_bytes",
+                  "sdm_scan_fwd_chunked_workspace_bytes"):
             getattr(L, f).restype = SZ
         L.sdm_check_device_errors.argtypes = [P, P]
         L.sdm_profile_enable.argtypes = [I]
@@ -63,7 +66,8 @@ def lib() -> ctypes.CDLL:
         L.sdm_status_string.restype = ctypes.c_char_p
         L.sdm_last_error.restype = ctypes.c_char_p
         L.sdm_version.restype = ctypes.c_char_p
-        for f in ("sdm_address", "sdm_scan_fwd", "sdm_scan_bwd", "sdm_mem_init", "sdm_check_device_errors",
+        for f in ("sdm_address", "sdm_scan_fwd", "sdm_scan_fwd_chunked", "sdm_scan_bwd", "sdm_mem_init",
+                  "sdm_check_device_errors",
                   "sdm_profile_enable", "sdm_profile_select", "sdm_profile_read"):
             getattr(L, f).restype = I
         _lib = L
@@ -165,6 +169,32 @@ def scan_fwd(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, saved=None, worksp
     return y
 
 
+def chunked_workspace(B, H, T, W, R, device) -> torch.Tensor:
+    return _ws(lib().sdm_scan_fwd_chunked_workspace_bytes(B, H, T, W, R), device)
+
+
+def scan_fwd_chunked(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, workspace=None, y=None):
+    """The same recurrence as scan_fwd by the chunk-parallel form (64-token chunks), in place on
+    mem.  Inference only (no undo log); W, R <= 64.  Returns y [B,H,T,d_v] fp32."""
+    dev = _dev(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, y)
+    B, H, T, dv = v.shape
+    W, R = w_idx.shape[-1], r_idx.shape[-1]
+    N = mem.shape[-2]
+    if not (v.dtype == alpha.dtype == beta.dtype):
+        raise TypeError("v, alpha, beta must share a dtype")
+    if mem.dtype != torch.float32:
+        raise TypeError("mem must be fp32")
+    if y is None:
+        y = torch.empty((B, H, T, dv), dtype=torch.float32, device=dev)
+    if workspace is None:
+        workspace = chunked_workspace(B, H, T, W, R, dev)
+    rc = lib().sdm_scan_fwd_chunked(_ptr(w_idx), _ptr(w_val), W, _ptr(r_idx), _ptr(r_val), R, _ptr(v),
+                                    _ptr(alpha), _ptr(beta), _dtype_code(v), _ptr(mem), B, H, T, dv, N,
+                                    _ptr(y), _ptr(workspace), workspace.numel(), _stream(dev))
+    _check("sdm_scan_fwd_chunked", rc)
+    return y
+
+
 def forward(q, k, cb_q, cb_k, v, alpha, beta, mem, N: int, topk: int, saved=None, workspace=None,
             y=None, out=None, chunk: int = 0):
     """The layer's memory forward in one call: addressing of q (read side) and k (write side)
@@ -259,7 +289,7 @@ def check_device_errors(workspace: torch.Tensor):
 
 
 KERNELS = {"address": 0, "fwd_prep": 1, "fwd_scan": 2, "bwd_prep": 3, "bwd_scan": 4, "bwd_reduce": 5,
-           "address_bwd": 6, "mem_init": 7, "decode": 8}
+           "address_bwd": 6, "mem_init": 7, "decode": 8, "chunk_coef": 9, "chunk_scan": 10}
 
 
 def set_scan_slice_width(sw: int):

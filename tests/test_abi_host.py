@@ -83,6 +83,38 @@ def test_scan_fwd_validation(kw, code):
     assert L.sdm_last_error()
 
 
+def fwd_chunked(**kw):
+    a = dict(wi=A, wv=A, W=32, ri=A, rv=A, R=32, v=A, al=A, be=A, dt=1, mem=A, B=1, H=1, T=8, dv=128,
+             N=65536, y=A, ws=A, wsb=1 << 30)
+    a.update(kw)
+    return L.sdm_scan_fwd_chunked(a["wi"], a["wv"], a["W"], a["ri"], a["rv"], a["R"], a["v"], a["al"],
+                                  a["be"], a["dt"], a["mem"], a["B"], a["H"], a["T"], a["dv"], a["N"], a["y"],
+                                  a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(W=0), -1), (dict(R=0), -1), (dict(W=65), -2), (dict(R=65), -2), (dict(W=129), -2), (dict(dv=6), -1),
+    (dict(N=0), -1), (dict(dt=2), -1), (dict(mem=None), -1), (dict(y=None), -1), (dict(y=A + 4), -1),
+    (dict(ws=None), -1), (dict(ws=A + 16), -1), (dict(wsb=100), -3), (dict(B=-1), -1),
+])
+def test_scan_fwd_chunked_validation(kw, code):
+    assert fwd_chunked(**kw) == code
+    assert L.sdm_last_error()
+
+
+def test_scan_fwd_chunked_empty_is_noop():
+    assert fwd_chunked(T=0, ws=None, y=None) == 0
+    assert fwd_chunked(B=0, ws=None, y=None) == 0
+
+
+def test_chunked_workspace_size():
+    # one record per (stream, 64-token chunk) after a 256-byte header
+    one = L.sdm_scan_fwd_chunked_workspace_bytes(1, 1, 64, 32, 32)
+    assert one > 256 and (one - 256) % 256 == 0
+    assert L.sdm_scan_fwd_chunked_workspace_bytes(2, 3, 65, 32, 32) == 256 + 12 * (one - 256)
+    assert L.sdm_scan_fwd_chunked_workspace_bytes(1, 1, 64, 0, 32) == 0
+
+
 def bwd(**kw):
     a = dict(cbq=A, cbk=A, cbdt=1, dk=128, wi=A, wv=A, W=32, ri=A, rv=A, R=32, v=A, al=A, be=A, dt=1,
              mem=A, saved=A, sb=1 << 40, dy=A, dmT=None, chunk=64, B=1, H=1, T=8, dv=128, N=65536,
@@ -124,10 +156,10 @@ def test_scan_line_io_setting():
 
 def test_profile_select():
     assert L.sdm_profile_select(1 << 2) == 0
-    assert L.sdm_profile_select((1 << 9) - 1) == 0
-    assert L.sdm_profile_select(1 << 9) == -1
+    assert L.sdm_profile_select((1 << 11) - 1) == 0
+    assert L.sdm_profile_select(1 << 11) == -1
     assert b"unknown kernel kinds" in L.sdm_last_error()
-    assert L.sdm_profile_select((1 << 9) - 1) == 0
+    assert L.sdm_profile_select((1 << 11) - 1) == 0
 
 
 def test_mem_init_validation():
