@@ -390,17 +390,51 @@ int sdm_scan_fwd_chunked(const int32_t* w_idx, const float* w_val, int W, const 
     a.v = v; a.alpha = alpha; a.beta = beta; a.in_dtype = in_dtype;
     a.mem = mem; a.B = B; a.H = H; a.T = T; a.dv = d_v; a.W = W; a.R = R; a.N = N;
     a.y = y; a.saved = nullptr; a.ws = static_cast<unsigned char*>(workspace);
-    a.tb = 0; a.te = T;
-    {
-        SdmProfScope ps(SDM_K_CHUNK_COEF, st);
-        e = sdm_launch_chunk_coef(a, st);
-    }
-    if (e != hipSuccess) return hip_fail(e, "sdm_scan_fwd_chunked coefficient launch");
-    {
+    // Chunk ranges: the coefficients of range r + 1 (all chunks independent)
+    // run on the second stream beside the scan of range r, which holds a
+    // workgroup per (stream, slice) only.
+    const int nch = (T + SDM_CHUNK - 1) / SDM_CHUNK;
+    const int nr = nch >= 32 ? 8 : 1;
+    auto range = [&](int r) {
+        ScanFwdArgs b = a;
+        b.tb = (int)((int64_t)nch * r / nr) * SDM_CHUNK;
+        b.te = std::min(T, (int)((int64_t)nch * (r + 1) / nr) * SDM_CHUNK);
+        return b;
+    };
+    auto coef = [&](const ScanFwdArgs& b, hipStream_t s) {
+        SdmProfScope ps(SDM_K_CHUNK_COEF, s);
+        return sdm_launch_chunk_coef(b, s);
+    };
+    auto scan = [&](const ScanFwdArgs& b) {
         SdmProfScope ps(SDM_K_CHUNK_SCAN, st);
-        e = sdm_launch_chunk_scan(a, st);
+        return sdm_launch_chunk_scan(b, st);
+    };
+    if (nr == 1) {
+        a.tb = 0; a.te = T;
+        if ((e = coef(a, st)) != hipSuccess) return hip_fail(e, "sdm_scan_fwd_chunked coefficient launch");
+        if ((e = scan(a)) != hipSuccess) return hip_fail(e, "sdm_scan_fwd_chunked scan launch");
+        return SDM_OK;
     }
-    if (e != hipSuccess) return hip_fail(e, "sdm_scan_fwd_chunked scan launch");
+    SidePipe& sp = side_pipe();
+    std::lock_guard<std::mutex> lk(sp.mu);
+    hipStream_t side;
+    std::vector<hipEvent_t>* evp;
+    int dev;
+    if ((e = side_get(sp, nr + 1, &side, &evp, &dev)) != hipSuccess) return hip_fail(e, "sdm_scan_fwd_chunked streams");
+    std::vector<hipEvent_t>& ev = *evp;
+    if ((e = hipEventRecord(ev[0], st)) != hipSuccess) return hip_fail(e, "sdm_scan_fwd_chunked record");
+    if ((e = hipStreamWaitEvent(side, ev[0], 0)) != hipSuccess) return hip_fail(e, "sdm_scan_fwd_chunked wait");
+    if ((e = coef(range(0), st)) != hipSuccess) return hip_fail(e, "sdm_scan_fwd_chunked coefficient launch");
+    for (int r = 0; r < nr; ++r) {
+        if (r + 1 < nr) {
+            if ((e = coef(range(r + 1), side)) != hipSuccess)
+                return hip_fail(e, "sdm_scan_fwd_chunked coefficient launch");
+            if ((e = hipEventRecord(ev[r + 1], side)) != hipSuccess) return hip_fail(e, "sdm_scan_fwd_chunked record");
+        }
+        if ((e = scan(range(r))) != hipSuccess) return hip_fail(e, "sdm_scan_fwd_chunked scan launch");
+        if (r + 1 < nr && (e = hipStreamWaitEvent(st, ev[r + 1], 0)) != hipSuccess)
+            return hip_fail(e, "sdm_scan_fwd_chunked wait");
+    }
     return SDM_OK;
 }
 

@@ -82,11 +82,13 @@ template <typename VT>
 __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
     const int32_t* __restrict__ w_idx, const float* __restrict__ w_val, const int32_t* __restrict__ r_idx,
     const float* __restrict__ r_val, const VT* __restrict__ alpha, const VT* __restrict__ beta, int T, int W,
-    int R, int64_t N, int nch, int P, unsigned char* __restrict__ recs, unsigned int* __restrict__ err) {
+    int R, int64_t N, int nch, int cb, int ncr, int P, unsigned char* __restrict__ recs,
+    unsigned int* __restrict__ err) {
+    // chunks [cb, cb + ncr) of every stream
     extern __shared__ __align__(16) unsigned char smem[];
     const ChunkRec L = chunk_rec_layout(W, R);
     const int tid = threadIdx.x;
-    const int s = blockIdx.x / nch, c = blockIdx.x - s * nch;
+    const int s = blockIdx.x / ncr, c = cb + (blockIdx.x - s * ncr);
     const int t0 = c * CC, n = min(CC, T - t0);
     const int E = n * W;
     const size_t tok0 = (size_t)s * T + t0;
@@ -102,7 +104,7 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
     float* bt = la + CC;                                 // [C] beta
     int* cnt = reinterpret_cast<int*>(bt + CC);          // [CT1 + 1]
 
-    unsigned char* rec = recs + (size_t)blockIdx.x * L.bytes;
+    unsigned char* rec = recs + ((size_t)s * nch + c) * L.bytes;
     float* g_cr = reinterpret_cast<float*>(rec + L.off_cr);
     float* g_cy = reinterpret_cast<float*>(rec + L.off_cy);
     int* g_sbeg = reinterpret_cast<int*>(rec + L.off_sbeg);
@@ -281,7 +283,8 @@ __global__ __launch_bounds__(CT2) void chunk_scan_kernel(const int32_t* __restri
                                                          const int32_t* __restrict__ r_idx, const VT* __restrict__ v,
                                                          float* __restrict__ mem, float* __restrict__ y,
                                                          const unsigned char* __restrict__ recs, int T, int W, int R,
-                                                         int64_t N, int dv, int nch, int nslice) {
+                                                         int64_t N, int dv, int nch, int cb, int ce, int nslice) {
+    // chunks [cb, ce) of the stream, in order
     __shared__ float Ls[CC * LDP];
     __shared__ float Qs[CC * LDP];
     __shared__ __align__(16) float Rr[CC * CCOLS];
@@ -302,7 +305,7 @@ __global__ __launch_bounds__(CT2) void chunk_scan_kernel(const int32_t* __restri
     const bool colok = col < dv;
     float* ms = mem + (size_t)s * N * dv;
 
-    for (int c = 0; c < nch; ++c) {
+    for (int c = cb; c < ce; ++c) {
         const unsigned char* rec = recs + ((size_t)s * nch + c) * L.bytes;
         const int t0 = c * CC, n = min(CC, T - t0);
         const size_t tk0 = (size_t)s * T + t0;
@@ -366,9 +369,12 @@ __global__ __launch_bounds__(CT2) void chunk_scan_kernel(const int32_t* __restri
         *reinterpret_cast<float4*>(&Rr[tl * CCOLS + q * 4]) = rr;
         __syncthreads();
         // ---- x = L (V - retrieved) ----
+        // (L and QK are zero above the diagonal and past the chunk's tokens, and
+        // Rr past them: the products run over all C columns, unrolled)
         {
             float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-            for (int u = 0; u <= tl && u < n; ++u) {
+#pragma unroll 16
+            for (int u = 0; u < CC; ++u) {
                 const float l = Ls[tl * LDP + u];
                 const float4 r = *reinterpret_cast<const float4*>(&Rr[u * CCOLS + q * 4]);
                 acc.x += l * r.x; acc.y += l * r.y; acc.z += l * r.z; acc.w += l * r.w;
@@ -379,7 +385,8 @@ __global__ __launch_bounds__(CT2) void chunk_scan_kernel(const int32_t* __restri
         // ---- y = inter + QK x ----
         if (tl < n && colok) {
             float4 acc = inter;
-            for (int u = 0; u <= tl; ++u) {
+#pragma unroll 16
+            for (int u = 0; u < CC; ++u) {
                 const float w = Qs[tl * LDP + u];
                 const float4 x = *reinterpret_cast<const float4*>(&Xs[u * CCOLS + q * 4]);
                 acc.x += w * x.x; acc.y += w * x.y; acc.z += w * x.z; acc.w += w * x.w;
@@ -405,19 +412,30 @@ __global__ __launch_bounds__(CT2) void chunk_scan_kernel(const int32_t* __restri
                         // past the last segment: reload segment g0's row (in bounds, unused)
                         m[b] = load4(ms + (size_t)sslot[g < nseg ? g : g0] * dv + col);
                     }
+                    // every segment has a first entry: the batch takes those together,
+                    // then any further entries of its segments
+                    int fb[SB];
+                    float4 acc[SB];
+#pragma unroll
+                    for (int b = 0; b < SB; ++b) {
+                        const int g = min(g0 + b * (CT2 / 8), nseg - 1);
+                        fb[b] = sbeg[g];
+                        const float d = sdec[g], w = ecoef[fb[b]];
+                        const float4 x = *reinterpret_cast<const float4*>(&Xs[etok[fb[b]] * CCOLS + q * 4]);
+                        acc[b] = make_float4(d * m[b].x + w * x.x, d * m[b].y + w * x.y, d * m[b].z + w * x.z,
+                                             d * m[b].w + w * x.w);
+                    }
 #pragma unroll
                     for (int b = 0; b < SB; ++b) {
                         const int g = g0 + b * (CT2 / 8);
                         if (g < nseg) {
-                            const float d = sdec[g];
-                            float4 acc = make_float4(d * m[b].x, d * m[b].y, d * m[b].z, d * m[b].w);
                             const int fe = sbeg[g + 1];
-                            for (int f = sbeg[g]; f < fe; ++f) {
+                            for (int f = fb[b] + 1; f < fe; ++f) {
                                 const float w = ecoef[f];
                                 const float4 x = *reinterpret_cast<const float4*>(&Xs[etok[f] * CCOLS + q * 4]);
-                                acc.x += w * x.x; acc.y += w * x.y; acc.z += w * x.z; acc.w += w * x.w;
+                                acc[b].x += w * x.x; acc[b].y += w * x.y; acc[b].z += w * x.z; acc[b].w += w * x.w;
                             }
-                            *reinterpret_cast<float4*>(ms + (size_t)sslot[g] * dv + col) = acc;
+                            *reinterpret_cast<float4*>(ms + (size_t)sslot[g] * dv + col) = acc[b];
                         }
                     }
                 }
@@ -430,13 +448,16 @@ __global__ __launch_bounds__(CT2) void chunk_scan_kernel(const int32_t* __restri
 template <typename VT>
 hipError_t launch_chunk_coef(const ScanFwdArgs& a, hipStream_t st) {
     const int S = a.B * a.H, nch = (a.T + CC - 1) / CC;
+    const int cb = a.tb / CC, ce = (a.te + CC - 1) / CC;
+    if (ce <= cb) return hipSuccess;
     const int P = pow2_at_least(CC * a.W);
     const size_t lds = coef_lds_bytes(a.W);
     auto kl = chunk_coef_kernel<VT>;
     hipError_t e = hipFuncSetAttribute((const void*)kl, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kl, dim3((unsigned)(S * nch)), dim3(CT1), lds, st, a.w_idx, a.w_val, a.r_idx, a.r_val,
-                       static_cast<const VT*>(a.alpha), static_cast<const VT*>(a.beta), a.T, a.W, a.R, a.N, nch, P,
+    hipLaunchKernelGGL(kl, dim3((unsigned)(S * (ce - cb))), dim3(CT1), lds, st, a.w_idx, a.w_val, a.r_idx, a.r_val,
+                       static_cast<const VT*>(a.alpha), static_cast<const VT*>(a.beta), a.T, a.W, a.R, a.N, nch, cb,
+                       ce - cb, P,
                        a.ws + SDM_WS_HEADER, reinterpret_cast<unsigned int*>(a.ws));
     return hipGetLastError();
 }
@@ -444,6 +465,8 @@ hipError_t launch_chunk_coef(const ScanFwdArgs& a, hipStream_t st) {
 template <typename VT>
 hipError_t launch_chunk_scan(const ScanFwdArgs& a, hipStream_t st) {
     const int S = a.B * a.H, nch = (a.T + CC - 1) / CC;
+    const int cb = a.tb / CC, ce = (a.te + CC - 1) / CC;
+    if (ce <= cb) return hipSuccess;
     const int nslice = (a.dv + CCOLS - 1) / CCOLS;
     constexpr size_t static_lds = (size_t)2 * CC * LDP * 4 + (size_t)2 * CC * CCOLS * 4;
     const bool seg = static_lds + scan_dyn_lds(a.W, a.R, true) <= (size_t)CK_LDS_LIMIT;
@@ -453,7 +476,7 @@ hipError_t launch_chunk_scan(const ScanFwdArgs& a, hipStream_t st) {
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kl, dim3((unsigned)(S * nslice)), dim3(CT2), lds, st, a.w_idx, a.r_idx,
                        static_cast<const VT*>(a.v), a.mem, a.y, a.ws + SDM_WS_HEADER, a.T, a.W, a.R, a.N, a.dv,
-                       nch, nslice);
+                       nch, cb, ce, nslice);
     return hipGetLastError();
 }
 

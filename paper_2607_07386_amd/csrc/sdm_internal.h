@@ -110,6 +110,7 @@ hipError_t sdm_launch_fwd_prep(const ScanFwdArgs& a, hipStream_t st);
 // Chunk-parallel forward scan: tokens in chunks of SDM_CHUNK, W and R at most
 // SDM_CHUNK_MAX_LIST.  The coefficient kernel writes one record per (stream,
 // chunk) after the workspace header; the scan kernel reads them (a.saved unused).
+// Both take the chunks of tokens [a.tb, a.te) (tb a multiple of SDM_CHUNK).
 #define SDM_CHUNK 64
 #define SDM_CHUNK_MAX_LIST 64
 bool sdm_chunk_shape_ok(int W, int R);

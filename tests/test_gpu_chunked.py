@@ -184,3 +184,17 @@ def test_chunked_empty_sequence_is_noop():
     y = sdm.scan_fwd_chunked(e_i, e_v, e_i, e_v, z, g, g, mem)
     torch.cuda.synchronize()
     assert y.numel() == 0 and torch.equal(mem, ref)
+
+
+def test_chunked_ranges_overlap_coefficients():
+    """33 chunks (2100 tokens, the last ragged): eight chunk ranges, the coefficients of each
+    later range on the library's second stream beside the scan of the range before it."""
+    W, R, fn = LISTS["read-own-writes-unsorted"]
+    sdm.profile_enable(True)
+    y, mem, yo, memo = _lists_case(2, 2100, 48, W, R, 20, fn, seed=11)
+    n_coef, n_scan = sdm.profile_read("chunk_coef")[1], sdm.profile_read("chunk_scan")[1]
+    sdm.profile_enable(False)
+    ey, em = rel_err(y, yo), rel_err(mem, memo)
+    print(f"chunked/ranges: y {ey:.2e} mem {em:.2e}", flush=True)
+    assert n_coef == 8 and n_scan == 8
+    assert ey < TOL and em < TOL
