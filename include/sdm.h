@@ -180,6 +180,11 @@ int sdm_scan_fwd_chunked(const int32_t* w_idx, const float* w_val, int W,
                          float* mem, int B, int H, int T, int d_v, int64_t N,
                          float* y, void* workspace, size_t ws_bytes, void* stream);
 size_t sdm_scan_fwd_chunked_workspace_bytes(int B, int H, int T, int W, int R);
+/* Columns per workgroup of sdm_scan_fwd_chunked's scan kernel: 32 (a 128-byte
+ * piece of every row), 16 (twice the workgroups), or 0 (default), which takes
+ * 32.  Process-wide; any other value returns SDM_ERR_INVALID_ARG and keeps the
+ * setting. */
+int sdm_set_chunk_scan_cols(int cols);
 
 /* ------------------------------------------------------------------------
  * sdm_scan_bwd — reverse mode of sdm_scan_fwd plus the addressing gradient.

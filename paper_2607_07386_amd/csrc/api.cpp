@@ -20,6 +20,8 @@ std::atomic<int> g_line_io{1};
 }
 
 int sdm_scan_slice_width() { return g_slice_width.load(std::memory_order_relaxed); }
+std::atomic<int> g_chunk_cols{0};
+int sdm_chunk_cols() { return g_chunk_cols.load(std::memory_order_relaxed); }
 bool sdm_line_io_enabled() { return g_line_io.load(std::memory_order_relaxed) != 0; }
 
 int sdm_device_simds() {
@@ -232,6 +234,14 @@ int sdm_set_scan_slice_width(int sw) {
     if (sw != 0 && sw != 8 && sw != 16)
         return fail(SDM_ERR_INVALID_ARG, "sdm_set_scan_slice_width: width must be 0 (automatic), 8 or 16, got %d", sw);
     g_slice_width.store(sw, std::memory_order_relaxed);
+    return SDM_OK;
+}
+
+int sdm_set_chunk_scan_cols(int cols) {
+    g_err[0] = 0;
+    if (cols != 0 && cols != 16 && cols != 32)
+        return fail(SDM_ERR_INVALID_ARG, "sdm_set_chunk_scan_cols: expected 0 (automatic), 16 or 32, got %d", cols);
+    g_chunk_cols.store(cols, std::memory_order_relaxed);
     return SDM_OK;
 }
 

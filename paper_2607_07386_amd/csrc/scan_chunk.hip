@@ -31,11 +31,12 @@ namespace {
 
 constexpr int CC = SDM_CHUNK;       // tokens per chunk
 constexpr int CT1 = 256;            // threads of the coefficient kernel
-constexpr int CT2 = 512;            // threads of the scan kernel: one (token, column quad) each
-constexpr int CCOLS = 32;           // columns per scan workgroup (one 128-byte line of a row)
+// The scan kernel takes COLS = 32 or 16 columns per workgroup (a 128- or
+// 64-byte piece of every row), with one thread per (token, column quad).
+template <int COLS>
+constexpr int scan_threads() { return CC * COLS / 4; }
 constexpr int LDP = CC + 1;         // padded row stride of L and QK in LDS
 constexpr int CK_LDS_LIMIT = 160 * 1024;
-static_assert(CT2 == CC * (CCOLS / 4), "one thread per (token, column quad) of a chunk");
 
 // Per-chunk record: nseg, then L and QK [C][C], the gather weights
 // exp(lambda) kappa [C][W] and exp(lambda) rho [C][R], then per written slot
@@ -277,14 +278,25 @@ inline size_t scan_dyn_lds(int W, int R, bool seg) {
 
 constexpr int GB = 32;   // row gathers in flight per thread
 constexpr int SB = 16;   // scatter rows in flight per thread
+// Scatter lists staged in LDS up to this many bytes (the largest that fits the
+// LDS limit beside the rest); longer lists are read from the record.
+constexpr int SEG_LDS_MAX = 80 * 1024;
 
-template <typename VT, bool SEG>
-__global__ __launch_bounds__(CT2) void chunk_scan_kernel(const int32_t* __restrict__ w_idx,
+template <typename VT, bool SEG, int COLS>
+__global__ __launch_bounds__(scan_threads<COLS>()) void chunk_scan_kernel(const int32_t* __restrict__ w_idx,
                                                          const int32_t* __restrict__ r_idx, const VT* __restrict__ v,
                                                          float* __restrict__ mem, float* __restrict__ y,
                                                          const unsigned char* __restrict__ recs, int T, int W, int R,
                                                          int64_t N, int dv, int nch, int cb, int ce, int nslice) {
     // chunks [cb, ce) of the stream, in order
+    constexpr int CT2 = scan_threads<COLS>();
+    constexpr int CCOLS = COLS;
+    constexpr int QPR = COLS / 4;    // column quads per row piece
+    // staging loads per thread: gather weights (float4), slot ids per side, scatter lists (float4)
+    constexpr int ST_CF = CC * 2 * SDM_CHUNK_MAX_LIST / 4 / CT2;
+    constexpr int ST_ID = CC * SDM_CHUNK_MAX_LIST / CT2;
+    constexpr int ST_SEG = SEG_LDS_MAX / 16 / CT2;
+    constexpr int SEG_RB = ST_SEG < 10 ? ST_SEG : 10;   // scatter-list float4s in registers per round
     __shared__ float Ls[CC * LDP];
     __shared__ float Qs[CC * LDP];
     __shared__ __align__(16) float Rr[CC * CCOLS];
@@ -299,8 +311,8 @@ __global__ __launch_bounds__(CT2) void chunk_scan_kernel(const int32_t* __restri
 
     const int tid = threadIdx.x;
     const int s = blockIdx.x / nslice, sl = blockIdx.x - s * nslice;
-    const int q = tid & 7;                  // column quad within the slice
-    const int tl = tid >> 3;                // token within the chunk
+    const int q = tid % QPR;                // column quad within the slice
+    const int tl = tid / QPR;               // token within the chunk
     const int col = sl * CCOLS + q * 4;
     const bool colok = col < dv;
     float* ms = mem + (size_t)s * N * dv;
@@ -309,31 +321,65 @@ __global__ __launch_bounds__(CT2) void chunk_scan_kernel(const int32_t* __restri
         const unsigned char* rec = recs + ((size_t)s * nch + c) * L.bytes;
         const int t0 = c * CC, n = min(CC, T - t0);
         const size_t tk0 = (size_t)s * T + t0;
-        // ---- stage the chunk's record and slot ids ----
+        // ---- stage the chunk's record and slot ids: every load first, then the LDS stores ----
         {
             const float4* gl = reinterpret_cast<const float4*>(rec + L.off_l);
             const float4* gq = reinterpret_cast<const float4*>(rec + L.off_qk);
-            for (int i = tid; i < CC * CC / 4; i += CT2) {
-                const float4 a = gl[i], b = gq[i];
-                const int r = (4 * i) / CC, k = (4 * i) % CC;
-                Ls[r * LDP + k] = a.x; Ls[r * LDP + k + 1] = a.y; Ls[r * LDP + k + 2] = a.z; Ls[r * LDP + k + 3] = a.w;
-                Qs[r * LDP + k] = b.x; Qs[r * LDP + k + 1] = b.y; Qs[r * LDP + k + 2] = b.z; Qs[r * LDP + k + 3] = b.w;
+            const float4* gcf = reinterpret_cast<const float4*>(rec + L.off_cr);   // [C][W] then [C][R]
+            const float4* gsg = reinterpret_cast<const float4*>(rec + L.off_sbeg);
+            const int ncf = CC * WR / 4, nsg = SEG ? seg_bytes / 16 : 0;
+            float4 la[CC * CC / 4 / CT2], qa[CC * CC / 4 / CT2], cf[ST_CF], sg[SEG_RB];
+            int iw[ST_ID], ir[ST_ID];
+#pragma unroll
+            for (int k = 0; k < CC * CC / 4 / CT2; ++k) {
+                la[k] = gl[tid + k * CT2];
+                qa[k] = gq[tid + k * CT2];
             }
-            // gather weights: [C][W] then [C][R], contiguous in the record
-            const float* gcf = reinterpret_cast<const float*>(rec + L.off_cr);
-            for (int i = tid; i < CC * WR; i += CT2) scf[i] = gcf[i];
-            for (int i = tid; i < n * W; i += CT2) {
-                int64_t id = w_idx[tk0 * W + i];
-                sid[i] = (int)(id < 0 ? 0 : (id >= N ? N - 1 : id));
+            // unconditional loads at clamped (valid) indices keep these arrays in
+            // registers; only the stores below are guarded
+#pragma unroll
+            for (int k = 0; k < ST_CF; ++k) cf[k] = gcf[min(tid + k * CT2, ncf - 1)];
+#pragma unroll
+            for (int k = 0; k < ST_ID; ++k) {
+                const int i = tid + k * CT2;
+                iw[k] = w_idx[tk0 * W + min(i, n * W - 1)];
+                ir[k] = r_idx[tk0 * R + min(i, n * R - 1)];
             }
-            for (int i = tid; i < n * R; i += CT2) {
-                int64_t id = r_idx[tk0 * R + i];
-                sid[CC * W + i] = (int)(id < 0 ? 0 : (id >= N ? N - 1 : id));
+            if constexpr (SEG) {
+#pragma unroll
+                for (int k = 0; k < SEG_RB; ++k) sg[k] = gsg[min(tid + k * CT2, nsg - 1)];
             }
-            if (SEG) {
-                const float4* gs = reinterpret_cast<const float4*>(rec + L.off_sbeg);
-                float4* ls = reinterpret_cast<float4*>(sseg);
-                for (int i = tid; i < seg_bytes / 16; i += CT2) ls[i] = gs[i];
+#pragma unroll
+            for (int k = 0; k < CC * CC / 4 / CT2; ++k) {
+                const int i = tid + k * CT2;
+                const int r = (4 * i) / CC, c4 = (4 * i) % CC;
+                float* lrow = Ls + r * LDP + c4;
+                float* qrow = Qs + r * LDP + c4;
+                lrow[0] = la[k].x; lrow[1] = la[k].y; lrow[2] = la[k].z; lrow[3] = la[k].w;
+                qrow[0] = qa[k].x; qrow[1] = qa[k].y; qrow[2] = qa[k].z; qrow[3] = qa[k].w;
+            }
+#pragma unroll
+            for (int k = 0; k < ST_CF; ++k)
+                if (tid + k * CT2 < ncf) reinterpret_cast<float4*>(scf)[tid + k * CT2] = cf[k];
+#pragma unroll
+            for (int k = 0; k < ST_ID; ++k) {
+                const int i = tid + k * CT2;
+                if (i < n * W) sid[i] = (int)(iw[k] < 0 ? 0 : (iw[k] >= N ? N - 1 : iw[k]));
+                if (i < n * R) sid[CC * W + i] = (int)(ir[k] < 0 ? 0 : (ir[k] >= N ? N - 1 : ir[k]));
+            }
+            if constexpr (SEG) {
+                // scatter lists: SEG_RB float4 per thread with the loads above,
+                // the rest in further rounds of SEG_RB
+#pragma unroll
+                for (int k = 0; k < SEG_RB; ++k)
+                    if (tid + k * CT2 < nsg) reinterpret_cast<float4*>(sseg)[tid + k * CT2] = sg[k];
+                for (int k0 = SEG_RB; k0 < ST_SEG; k0 += SEG_RB) {
+#pragma unroll
+                    for (int k = 0; k < SEG_RB; ++k) sg[k] = gsg[min(tid + (k0 + k) * CT2, nsg - 1)];
+#pragma unroll
+                    for (int k = 0; k < SEG_RB; ++k)
+                        if (tid + (k0 + k) * CT2 < nsg) reinterpret_cast<float4*>(sseg)[tid + (k0 + k) * CT2] = sg[k];
+                }
             }
         }
         __syncthreads();
@@ -404,11 +450,11 @@ __global__ __launch_bounds__(CT2) void chunk_scan_kernel(const int32_t* __restri
             const int* etok = reinterpret_cast<const int*>(sb + (L.off_etok - L.off_sbeg));
             const float* ecoef = reinterpret_cast<const float*>(sb + (L.off_ecoef - L.off_sbeg));
             if (colok) {
-                for (int g0 = tl; g0 < nseg; g0 += SB * (CT2 / 8)) {
+                for (int g0 = tl; g0 < nseg; g0 += SB * CC) {
                     float4 m[SB];
 #pragma unroll
                     for (int b = 0; b < SB; ++b) {
-                        const int g = g0 + b * (CT2 / 8);
+                        const int g = g0 + b * CC;
                         // past the last segment: reload segment g0's row (in bounds, unused)
                         m[b] = load4(ms + (size_t)sslot[g < nseg ? g : g0] * dv + col);
                     }
@@ -418,7 +464,7 @@ __global__ __launch_bounds__(CT2) void chunk_scan_kernel(const int32_t* __restri
                     float4 acc[SB];
 #pragma unroll
                     for (int b = 0; b < SB; ++b) {
-                        const int g = min(g0 + b * (CT2 / 8), nseg - 1);
+                        const int g = min(g0 + b * CC, nseg - 1);
                         fb[b] = sbeg[g];
                         const float d = sdec[g], w = ecoef[fb[b]];
                         const float4 x = *reinterpret_cast<const float4*>(&Xs[etok[fb[b]] * CCOLS + q * 4]);
@@ -427,10 +473,11 @@ __global__ __launch_bounds__(CT2) void chunk_scan_kernel(const int32_t* __restri
                     }
 #pragma unroll
                     for (int b = 0; b < SB; ++b) {
-                        const int g = g0 + b * (CT2 / 8);
+                        const int g = g0 + b * CC;
                         if (g < nseg) {
                             const int fe = sbeg[g + 1];
-                            for (int f = fb[b] + 1; f < fe; ++f) {
+                            int f = fb[b] + 1;
+                            for (; f < fe; ++f) {
                                 const float w = ecoef[f];
                                 const float4 x = *reinterpret_cast<const float4*>(&Xs[etok[f] * CCOLS + q * 4]);
                                 acc[b].x += w * x.x; acc[b].y += w * x.y; acc[b].z += w * x.z; acc[b].w += w * x.w;
@@ -462,22 +509,34 @@ hipError_t launch_chunk_coef(const ScanFwdArgs& a, hipStream_t st) {
     return hipGetLastError();
 }
 
-template <typename VT>
-hipError_t launch_chunk_scan(const ScanFwdArgs& a, hipStream_t st) {
+template <typename VT, int COLS>
+hipError_t launch_chunk_scan_cols(const ScanFwdArgs& a, hipStream_t st) {
     const int S = a.B * a.H, nch = (a.T + CC - 1) / CC;
     const int cb = a.tb / CC, ce = (a.te + CC - 1) / CC;
     if (ce <= cb) return hipSuccess;
-    const int nslice = (a.dv + CCOLS - 1) / CCOLS;
-    constexpr size_t static_lds = (size_t)2 * CC * LDP * 4 + (size_t)2 * CC * CCOLS * 4;
-    const bool seg = static_lds + scan_dyn_lds(a.W, a.R, true) <= (size_t)CK_LDS_LIMIT;
+    const int nslice = (a.dv + COLS - 1) / COLS;
+    constexpr size_t static_lds = (size_t)2 * CC * LDP * 4 + (size_t)2 * CC * COLS * 4;
+    const size_t seg_bytes = scan_dyn_lds(a.W, a.R, true) - scan_dyn_lds(a.W, a.R, false);
+    // (at 16 columns the staged lists push the kernel past its registers: they
+    // are read from the record there)
+    const bool seg = COLS == 32 && static_lds + scan_dyn_lds(a.W, a.R, true) <= (size_t)CK_LDS_LIMIT &&
+                     seg_bytes <= (size_t)SEG_LDS_MAX;
     const size_t lds = scan_dyn_lds(a.W, a.R, seg);
-    auto kl = seg ? chunk_scan_kernel<VT, true> : chunk_scan_kernel<VT, false>;
+    auto kl = seg ? chunk_scan_kernel<VT, true, COLS> : chunk_scan_kernel<VT, false, COLS>;
     hipError_t e = hipFuncSetAttribute((const void*)kl, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kl, dim3((unsigned)(S * nslice)), dim3(CT2), lds, st, a.w_idx, a.r_idx,
+    hipLaunchKernelGGL(kl, dim3((unsigned)(S * nslice)), dim3(scan_threads<COLS>()), lds, st, a.w_idx, a.r_idx,
                        static_cast<const VT*>(a.v), a.mem, a.y, a.ws + SDM_WS_HEADER, a.T, a.W, a.R, a.N, a.dv,
                        nch, cb, ce, nslice);
     return hipGetLastError();
+}
+
+// 32-column slices unless 16 are forced.  (At the long-context shape, 16
+// streams of 128 columns, 16-column slices double the workgroups and measured
+// slower: 41.0 against 35.2 ms.)
+template <typename VT>
+hipError_t launch_chunk_scan(const ScanFwdArgs& a, hipStream_t st) {
+    return sdm_chunk_cols() == 16 ? launch_chunk_scan_cols<VT, 16>(a, st) : launch_chunk_scan_cols<VT, 32>(a, st);
 }
 
 }  // namespace

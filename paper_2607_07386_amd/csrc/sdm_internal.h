@@ -114,6 +114,8 @@ hipError_t sdm_launch_fwd_prep(const ScanFwdArgs& a, hipStream_t st);
 #define SDM_CHUNK 64
 #define SDM_CHUNK_MAX_LIST 64
 bool sdm_chunk_shape_ok(int W, int R);
+// Forced columns per workgroup of the chunked scan (16 or 32), or 0 for automatic.
+int sdm_chunk_cols();
 size_t sdm_chunk_ws_bytes(int B, int H, int T, int W, int R);
 hipError_t sdm_launch_chunk_coef(const ScanFwdArgs& a, hipStream_t st);
 hipError_t sdm_launch_chunk_scan(const ScanFwdArgs& a, hipStream_t st);

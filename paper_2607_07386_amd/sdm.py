@@ -61,6 +61,7 @@ def lib() -> ctypes.CDLL:
         L.sdm_profile_select.argtypes = [ctypes.c_uint]
         L.sdm_set_scan_slice_width.argtypes = [I]
         L.sdm_set_scan_line_io.argtypes = [I]
+        L.sdm_set_chunk_scan_cols.argtypes = [I]
         L.sdm_profile_read.argtypes = [I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
         L.sdm_status_string.argtypes = [I]
         L.sdm_status_string.restype = ctypes.c_char_p
@@ -290,6 +291,11 @@ def check_device_errors(workspace: torch.Tensor):
 
 KERNELS = {"address": 0, "fwd_prep": 1, "fwd_scan": 2, "bwd_prep": 3, "bwd_scan": 4, "bwd_reduce": 5,
            "address_bwd": 6, "mem_init": 7, "decode": 8, "chunk_coef": 9, "chunk_scan": 10}
+
+
+def set_chunk_scan_cols(cols: int):
+    """Columns per workgroup of the chunked scan: 16, 32, or 0 for the default (32)."""
+    _check("sdm_set_chunk_scan_cols", lib().sdm_set_chunk_scan_cols(int(cols)))
 
 
 def set_scan_slice_width(sw: int):

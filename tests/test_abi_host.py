@@ -145,6 +145,14 @@ def test_slice_width_setting():
         assert b"width" in L.sdm_last_error()
 
 
+def test_chunk_scan_cols_setting():
+    for c in (16, 32, 0):
+        assert L.sdm_set_chunk_scan_cols(c) == 0
+    for c in (-1, 8, 24, 64):
+        assert L.sdm_set_chunk_scan_cols(c) == -1
+        assert b"expected 0" in L.sdm_last_error()
+
+
 def test_scan_line_io_setting():
     for on in (0, 1):
         assert L.sdm_set_scan_line_io(on) == 0

@@ -21,6 +21,14 @@ pytestmark = pytest.mark.gpu
 TOL = 1e-4
 
 
+@pytest.fixture(autouse=True, params=[16, 32], ids=["cols16", "cols32"])
+def chunk_cols(request):
+    """Every case at both scan-workgroup widths."""
+    sdm.set_chunk_scan_cols(request.param)
+    yield request.param
+    sdm.set_chunk_scan_cols(0)
+
+
 def np_(t):
     return t.detach().cpu().numpy()
 
