@@ -17,7 +17,9 @@ addressing gradients) on the training workload (B=4, H=16, T=4096) under
 "train"; the learned-M0 broadcast of the learned-M0 workload under
 "mem_init"; single-token decode steps under "decode"; the paper's own 1.4B
 and 8B layer shapes (H=2, sqrt(N)=240 and 480, d_v=960 and 1920, W=R=64,
-direct-mode addressing; forward and training steps) under "paper_layer".
+direct-mode addressing; forward and training steps) under "paper_layer"; the
+long-context scan (16 streams of 65536 tokens) by the sequential and the
+chunk-parallel schedules under "long_context".
 
 Printed: one JSON line.  `value` is forward tokens/s (B*T positions, all
 heads) over the timed steps; `roofline` gives the forward scan kernel's
@@ -151,7 +153,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-streams", type=int, default=16)
     ap.add_argument("--cpu-tokens", type=int, default=4096)
-    ap.add_argument("--only", choices=["fwd", "train", "init", "decode", "paper", "address"], default=None,
+    ap.add_argument("--only", choices=["fwd", "train", "init", "decode", "paper", "address", "long"], default=None,
                     help="run one leg only (profiling runs)")
     ap.add_argument("--no-sequential", action="store_true",
                     help="skip the reference timing of the forward step as three separate calls")
@@ -447,6 +449,52 @@ def main():
         sdm.profile_enable(False)
         out["scoring"] = scoring_mfma(w, t_addr / max(n_addr, 1))
         del q, k, cb
+
+    # ------------------------------------------------------------ long context: both scan schedules
+    if (extra and args.only is None) or args.only == "long":
+        wl = synth.WORKLOADS[2]
+        log("long context: generating inputs and addressing")
+        il = synth.Inputs(wl)
+        q, k, v = to_dev(il.q), to_dev(il.k), to_dev(il.v)
+        al, be, cb = to_dev(il.alpha), to_dev(il.beta), to_dev(il.codebook)
+        ri, rv = sdm.address(q, cb, wl.N, wl.topk)
+        wi, wv = sdm.address(k, cb, wl.N, wl.topk)
+        del q, k
+        mem = torch.zeros((wl.B, wl.H, wl.N, wl.d_v), dtype=torch.float32, device=dev)
+        yl = torch.empty((wl.B, wl.H, wl.T, wl.d_v), dtype=torch.float32, device=dev)
+        wsf = sdm.fwd_workspace(wl.B, wl.H, wl.T, wl.topk, wl.topk, dev)
+        wsc = sdm.chunked_workspace(wl.B, wl.H, wl.T, wl.topk, wl.topk, dev)
+        units = wl.B * wl.H * wl.T
+        lbytes = fwd_scan_bytes_per_token_head(wl.topk, wl.topk, wl.d_v, 2) * units
+        res = {"workload": f"long context: B={wl.B} H={wl.H} T={wl.T} N={wl.N} d_v={wl.d_v} top-{wl.topk}, "
+                           f"clustered keys; the scan alone on the workload's own slot lists",
+               "scan_algorithmic_bytes": lbytes}
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for name, fn, kinds in (
+                ("sequential", lambda: sdm.scan_fwd(wi, wv, ri, rv, v, al, be, mem, workspace=wsf, y=yl),
+                 ("fwd_prep", "fwd_scan")),
+                ("chunked", lambda: sdm.scan_fwd_chunked(wi, wv, ri, rv, v, al, be, mem, workspace=wsc, y=yl),
+                 ("chunk_coef", "chunk_scan"))):
+            log(f"long context: timing the {name} scan")
+            fn()
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(3):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / 3
+            sdm.profile_enable(True)
+            fn()
+            torch.cuda.synchronize()
+            kms = {kk: round(sdm.profile_read(kk)[0], 3) for kk in kinds}
+            sdm.profile_enable(False)
+            res[name] = {"ms": round(ms, 3), "tokens_per_s": round(wl.B * wl.T / (ms * 1e-3), 1),
+                         "GB_s": round(lbytes / (ms * 1e-3) / 1e9, 1), "kernels_ms": kms}
+        res["chunked_speedup"] = round(res["sequential"]["ms"] / res["chunked"]["ms"], 3)
+        out["long_context"] = res
+        del v, al, be, cb, ri, rv, wi, wv, mem, yl, wsf, wsc
+        torch.cuda.empty_cache()
 
     # ------------------------------------------------------------ the paper's 1.4B and 8B layers
     if (extra and args.only is None) or args.only == "paper":
