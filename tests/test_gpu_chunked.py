@@ -206,3 +206,33 @@ def test_chunked_ranges_overlap_coefficients():
     print(f"chunked/ranges: y {ey:.2e} mem {em:.2e}", flush=True)
     assert n_coef == 8 and n_scan == 8
     assert ey < TOL and em < TOL
+
+
+@pytest.mark.slow
+def test_chunked_full_long_context(chunk_cols):
+    """The long-context workload at full size (16 streams x 65536 tokens, clustered keys) in the
+    launch configuration the bench times (32 columns, 8 chunk ranges); one sampled stream against
+    the oracle fed the GPU's slot lists."""
+    if chunk_cols != 32:
+        pytest.skip("full size runs at the default width, the one the bench times")
+    w = synth.WORKLOADS[2]
+    inp = synth.Inputs(w)
+    q, k, v = to_dev(inp.q), to_dev(inp.k), to_dev(inp.v)
+    al, be, cb = to_dev(inp.alpha), to_dev(inp.beta), to_dev(inp.codebook)
+    r_idx, r_val = sdm.address(q, cb, w.N, w.topk)
+    w_idx, w_val = sdm.address(k, cb, w.N, w.topk)
+    del q, k
+    mem = torch.zeros((w.B, w.H, w.N, w.d_v), dtype=torch.float32, device=DEV)
+    ws = sdm.chunked_workspace(w.B, w.H, w.T, w.topk, w.topk, DEV)
+    y = sdm.scan_fwd_chunked(w_idx, w_val, r_idx, r_val, v, al, be, mem, workspace=ws)
+    sdm.check_device_errors(ws)
+    s = 5
+    take = lambda t, last: np_(t).reshape(-1, w.T, last)[s:s + 1]
+    memo = np.zeros((1, w.N, w.d_v), np.float64)
+    yo = oracle.scan_fwd(take(w_idx, w.topk), take(w_val, w.topk).astype(np.float64), take(r_idx, w.topk),
+                         take(r_val, w.topk).astype(np.float64), inp.v.f64.reshape(-1, w.T, w.d_v)[s:s + 1],
+                         inp.alpha.f64.reshape(-1, w.T)[s:s + 1], inp.beta.f64.reshape(-1, w.T)[s:s + 1], memo)
+    ey = rel_err(np_(y).reshape(-1, w.T, w.d_v)[s:s + 1], yo)
+    em = rel_err(np_(mem).reshape(-1, w.N, w.d_v)[s:s + 1], memo)
+    print(f"chunked/full-long-context stream {s}: y {ey:.2e} mem {em:.2e}", flush=True)
+    assert ey < TOL and em < TOL
