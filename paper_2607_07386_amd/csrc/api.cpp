@@ -405,10 +405,14 @@ int sdm_scan_fwd_chunked(const int32_t* w_idx, const float* w_val, int W, const 
     // workgroup per (stream, slice) only.
     const int nch = (T + SDM_CHUNK - 1) / SDM_CHUNK;
     const int nr = nch >= 32 ? 8 : 1;
+    // the first range is a quarter of the others: its coefficients overlap nothing
+    auto bound = [&](int r) {
+        return r == 0 ? 0 : r == nr ? nch : (int)((int64_t)nch * (4 * r - 3) / (4 * nr - 3));
+    };
     auto range = [&](int r) {
         ScanFwdArgs b = a;
-        b.tb = (int)((int64_t)nch * r / nr) * SDM_CHUNK;
-        b.te = std::min(T, (int)((int64_t)nch * (r + 1) / nr) * SDM_CHUNK);
+        b.tb = bound(r) * SDM_CHUNK;
+        b.te = std::min(T, bound(r + 1) * SDM_CHUNK);
         return b;
     };
     auto coef = [&](const ScanFwdArgs& b, hipStream_t s) {
