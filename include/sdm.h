@@ -164,7 +164,11 @@ size_t sdm_scan_saved_bytes(int B, int H, int T, int W, int d_v);
  * a triangular product QK x; each slot written in the chunk is then stored
  * once.  The first kernel (all chunks in parallel) builds per-chunk
  * coefficients from the slot lists and gates alone; the second walks the
- * chunks of each stream in order, one workgroup per 32 columns.  Results equal
+ * chunks of each stream in order, one workgroup per 32 columns (see
+ * sdm_set_chunk_scan_cols).  With 32 or more chunks both run over 8 chunk
+ * ranges, the coefficients of the next range on the library's second stream
+ * (as sdm_forward's) beside the scan of the current one; all work is ordered
+ * before later work on `stream` when the call returns.  Results equal
  * sdm_scan_fwd's up to the rounding of the reassociated sums and of the
  * triangular solve.
  *   Arguments as for sdm_scan_fwd, without the undo log; workspace of at least

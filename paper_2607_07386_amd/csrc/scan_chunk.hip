@@ -21,9 +21,11 @@
 // inverts the unit lower-triangular system into L = (I + diag(beta) A)^-1
 // diag(beta), and stores L, QK, the gather weights and the per-slot scatter
 // lists as one record per chunk.  chunk_scan_kernel (one workgroup per stream
-// and 32-column slice) walks the chunks in order: gathers of retrieved and of
-// the reads' first term from the chunk-start table, x = L (V - retrieved) and
-// y = inter + QK x from LDS, then one store of every written slot.
+// and 32-column slice, or 16 when forced) walks the chunks in order: gathers of
+// retrieved and of the reads' first term from the chunk-start table,
+// x = L (V - retrieved) and y = inter + QK x from LDS, then one store of every
+// written slot.  The host side runs both over chunk ranges so that the
+// coefficients of the next range overlap the scan of the current one.
 #include "sdm_common.h"
 #include "sdm_internal.h"
 
