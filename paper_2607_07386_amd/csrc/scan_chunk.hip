@@ -279,7 +279,7 @@ inline size_t scan_dyn_lds(int W, int R, bool seg) {
 }
 
 constexpr int GB = 32;   // row gathers in flight per thread
-constexpr int SB = 16;   // scatter rows in flight per thread
+constexpr int SB = 8;    // scatter rows in flight per thread
 // Scatter lists staged in LDS up to this many bytes (the largest that fits the
 // LDS limit beside the rest); longer lists are read from the record.
 constexpr int SEG_LDS_MAX = 80 * 1024;
