@@ -11,6 +11,10 @@ Function map (paper passages in the C source):
   scan_fwd       Sec. 3.1 steps 2-3, Eqs. (sdm-decay), (sdm-write), (sdm-read)
   scan_bwd       reverse mode with undo of the in-place writes (App. A.3)
   address_bwd    gradient of the softmax weights w.r.t. the projected vectors
+  gates          forget / input gates from their pre-activations (Sec. 3.1 step 2)
+  gates_bwd      their reverse mode, with the per-head sums for A and b_dt
+  norm_gate      RMS norm of each head's read vector times the output gate (Sec. 3.1 step 4)
+  norm_gate_bwd  its reverse mode
 """
 from __future__ import annotations
 
@@ -56,10 +60,16 @@ def _load():
             lib.orc_scan_bwd.argtypes = [I, I, I, L, I, I, P, P, P, P, P, P, P, P, P, P, P,
                                          P, P, P, P, P]
             lib.orc_address_bwd.argtypes = [P, I, I, I, I, L, I, P, P, P, P]
+            lib.orc_gates.argtypes = [I, I, I, P, P, P, P, P, P]
+            lib.orc_gates_bwd.argtypes = [I, I, I, P, P, P, P, P, P, P, P, P, P]
+            D = ctypes.c_double
+            lib.orc_norm_gate.argtypes = [L, I, P, P, P, D, I, P, P]
+            lib.orc_norm_gate_bwd.argtypes = [L, I, P, P, P, D, I, P, P, P, P]
             lib.orc_set_threads.argtypes = [I]
             lib.orc_set_threads.restype = None
             for f in ("orc_address", "orc_address_brute", "orc_scan_fwd", "orc_scan_bwd",
-                      "orc_address_bwd", "orc_max_threads"):
+                      "orc_address_bwd", "orc_gates", "orc_gates_bwd", "orc_norm_gate", "orc_norm_gate_bwd",
+                      "orc_max_threads"):
                 getattr(lib, f).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -152,6 +162,57 @@ def address_bwd(codebook, idx, val, dval, N: int, d_k: int):
     if rc != 0:
         raise ValueError("oracle address_bwd: invalid arguments")
     return dx
+
+
+def gates(a, b, A, b_dt):
+    """a, b [B,H,T] pre-activations; A, b_dt [H].  Returns alpha, beta [B,H,T]."""
+    a, b, A, bd = _f64(a), _f64(b), _f64(A), _f64(b_dt)
+    H = A.shape[0]
+    T = a.shape[-1]
+    S = a.size // T if T else int(np.prod(a.shape[:-1]))
+    al, be = np.empty(a.shape), np.empty(a.shape)
+    if _load().orc_gates(S, H, T, _p(a), _p(b), _p(A), _p(bd), _p(al), _p(be)) != 0:
+        raise ValueError("oracle gates: invalid arguments")
+    return al, be
+
+
+def gates_bwd(a, b, A, b_dt, dalpha, dbeta):
+    """Gradients of the gates: returns da, db [B,H,T] and dA, db_dt [H]."""
+    a, b, A, bd = _f64(a), _f64(b), _f64(A), _f64(b_dt)
+    dal, dbe = _f64(dalpha), _f64(dbeta)
+    H = A.shape[0]
+    T = a.shape[-1]
+    S = a.size // T if T else int(np.prod(a.shape[:-1]))
+    da, db = np.empty(a.shape), np.empty(a.shape)
+    dA, dbd = np.empty(H), np.empty(H)
+    if _load().orc_gates_bwd(S, H, T, _p(a), _p(b), _p(A), _p(bd), _p(dal), _p(dbe), _p(da), _p(db), _p(dA),
+                             _p(dbd)) != 0:
+        raise ValueError("oracle gates_bwd: invalid arguments")
+    return da, db, dA, dbd
+
+
+def norm_gate(y, g, gamma, eps: float, act: int):
+    """y, g [..., d_v]; gamma [d_v].  Returns o [..., d_v] and rstd [...]."""
+    y, g, gm = _f64(y), _f64(g), _f64(gamma)
+    dv = y.shape[-1]
+    rows = y.size // dv
+    o = np.empty(y.shape)
+    rstd = np.empty(y.shape[:-1])
+    if _load().orc_norm_gate(rows, dv, _p(y), _p(g), _p(gm), float(eps), int(act), _p(o), _p(rstd)) != 0:
+        raise ValueError("oracle norm_gate: invalid arguments")
+    return o, rstd
+
+
+def norm_gate_bwd(y, g, gamma, eps: float, act: int, dout):
+    """Returns dy, dg [..., d_v] and dgamma [d_v]."""
+    y, g, gm, do = _f64(y), _f64(g), _f64(gamma), _f64(dout)
+    dv = y.shape[-1]
+    rows = y.size // dv
+    dy, dg, dgm = np.empty(y.shape), np.empty(y.shape), np.empty(dv)
+    if _load().orc_norm_gate_bwd(rows, dv, _p(y), _p(g), _p(gm), float(eps), int(act), _p(do), _p(dy), _p(dg),
+                                 _p(dgm)) != 0:
+        raise ValueError("oracle norm_gate_bwd: invalid arguments")
+    return dy, dg, dgm
 
 
 def layer_forward(x_q, x_k, cb, v, alpha, beta, m0, N, topk, decide_f32=True, save=False):

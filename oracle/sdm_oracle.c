@@ -18,6 +18,10 @@
  *                Eq. (sdm-read) on the post-write memory M_t.
  *   Backward     reverse mode of the forward; past memory states are
  *                recovered by undoing the in-place writes (App. A.3).
+ *   Gates        Sec. 3.1 step 2: the forget gate from A, b_dt and its
+ *                projection, the input gate from its projection; reverse mode.
+ *   Epilogue     Sec. 3.1 step 4 and Fig. 2: RMS norm of each head's read
+ *                vector times the element-wise output gate; reverse mode.
  *
  * Readings where the paper is silent (listed with their reasons in the
  * design notes): codebook scoring when d_k != 2 sqrt(N); ties ordered by
@@ -390,6 +394,123 @@ int orc_address_bwd(const double* cb, int B, int H, int T, int dk, int64_t N, in
         }
         free(sb);
     }
+    return 0;
+}
+
+/* ------------------------------------------------------------ gates
+ * Sec. 3.1 step 2: the forget gate alpha_t = exp(-A softplus(W_a x_t + b_dt))
+ * and the input gate beta_t = sigma(W_b x_t), one of each per head and token.
+ * The projections W_a x_t and W_b x_t arrive as the pre-activations a and b
+ * [S, T] (S = B*H streams, head h = s mod H); A and b_dt are per head [H]
+ * (Sec. 4 initialises A in [0, 16] and b_dt from inverse softplus of
+ * [0.001, 0.1]). */
+static double softplus(double z) {
+    /* log(1 + e^z), written so that neither branch overflows */
+    return z > 0.0 ? z + log1p(exp(-z)) : log1p(exp(z));
+}
+
+static double sigmoid(double z) {
+    return z >= 0.0 ? 1.0 / (1.0 + exp(-z)) : exp(z) / (1.0 + exp(z));
+}
+
+int orc_gates(int S, int H, int T, const double* a, const double* b, const double* A, const double* b_dt,
+              double* alpha, double* beta) {
+    if (S < 0 || H < 1 || T < 0) return -1;
+    for (int64_t s = 0; s < S; ++s) {
+        const int h = (int)(s % H);
+        for (int t = 0; t < T; ++t) {
+            const int64_t i = s * T + t;
+            alpha[i] = exp(-A[h] * softplus(a[i] + b_dt[h]));
+            beta[i] = sigmoid(b[i]);
+        }
+    }
+    return 0;
+}
+
+/* Reverse mode of orc_gates.  With z = a + b_dt: d alpha / dz = -A alpha
+ * sigma(z) (softplus' = sigma), d alpha / dA = -softplus(z) alpha,
+ * d beta / db = beta (1 - beta).  dA and db_dt sum over every (b, t) of the
+ * head. */
+int orc_gates_bwd(int S, int H, int T, const double* a, const double* b, const double* A,
+                  const double* b_dt, const double* dalpha, const double* dbeta, double* da, double* db,
+                  double* dA, double* db_dt) {
+    if (S < 0 || H < 1 || T < 0) return -1;
+    for (int h = 0; h < H; ++h) dA[h] = db_dt[h] = 0.0;
+    for (int64_t s = 0; s < S; ++s) {
+        const int h = (int)(s % H);
+        for (int t = 0; t < T; ++t) {
+            const int64_t i = s * T + t;
+            const double z = a[i] + b_dt[h];
+            const double al = exp(-A[h] * softplus(z));
+            const double dz = dalpha[i] * (-A[h] * al * sigmoid(z));
+            da[i] = dz;
+            db_dt[h] += dz;
+            dA[h] += dalpha[i] * (-softplus(z) * al);
+            const double be = sigmoid(b[i]);
+            db[i] = dbeta[i] * be * (1.0 - be);
+        }
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------ output epilogue
+ * Sec. 3.1 step 4 ("Norm, Gating, and Head Mixing") and Fig. 2's
+ * g_t (.) Norm(y_t): per (b, h, t) row of d_v values,
+ *   rstd = 1 / sqrt(mean_c y[c]^2 + eps),  o[c] = y[c] rstd gamma[c] phi(g[c]),
+ * with gamma [d_v] the norm's scale (shared by heads) and phi the gate's
+ * activation: act = 0 identity (the text's element-wise gate), act = 1
+ * SiLU, phi(g) = g sigma(g).  W_o, which mixes the heads afterwards, is a
+ * plain GEMM and not part of this step. */
+static double gate_act(double g, int act) { return act ? g * sigmoid(g) : g; }
+
+static double gate_act_grad(double g, int act) {
+    if (!act) return 1.0;
+    const double sg = sigmoid(g);
+    return sg * (1.0 + g * (1.0 - sg));
+}
+
+int orc_norm_gate(int64_t rows, int dv, const double* y, const double* g, const double* gamma, double eps,
+                  int act, double* o, double* rstd) {
+    if (rows < 0 || dv < 1 || (act != 0 && act != 1)) return -1;
+    for (int64_t r = 0; r < rows; ++r) {
+        const double* yr = y + r * dv;
+        double ss = 0.0;
+        for (int c = 0; c < dv; ++c) ss += yr[c] * yr[c];
+        const double rs = 1.0 / sqrt(ss / dv + eps);
+        rstd[r] = rs;
+        for (int c = 0; c < dv; ++c) o[r * dv + c] = yr[c] * rs * gamma[c] * gate_act(g[r * dv + c], act);
+    }
+    return 0;
+}
+
+/* Reverse mode of orc_norm_gate, with n = y rstd:
+ *   dg = do gamma n phi'(g);  dn = do phi(g) gamma;  dgamma = sum over rows of do phi(g) n;
+ *   dy = rstd (dn - n mean_c(dn n)). */
+int orc_norm_gate_bwd(int64_t rows, int dv, const double* y, const double* g, const double* gamma, double eps,
+                      int act, const double* dout, double* dy, double* dg, double* dgamma) {
+    if (rows < 0 || dv < 1 || (act != 0 && act != 1)) return -1;
+    for (int c = 0; c < dv; ++c) dgamma[c] = 0.0;
+    double* dn = (double*)malloc(sizeof(double) * dv);
+    if (!dn) return -1;
+    for (int64_t r = 0; r < rows; ++r) {
+        const double* yr = y + r * dv;
+        double ss = 0.0;
+        for (int c = 0; c < dv; ++c) ss += yr[c] * yr[c];
+        const double rs = 1.0 / sqrt(ss / dv + eps);
+        double dot = 0.0;
+        for (int c = 0; c < dv; ++c) {
+            const int64_t i = r * dv + c;
+            const double n = yr[c] * rs;
+            const double ph = gate_act(g[i], act);
+            dg[i] = dout[i] * gamma[c] * n * gate_act_grad(g[i], act);
+            dgamma[c] += dout[i] * ph * n;
+            dn[c] = dout[i] * ph * gamma[c];
+            dot += dn[c] * n;
+        }
+        dot /= dv;
+        for (int c = 0; c < dv; ++c) dy[r * dv + c] = rs * (dn[c] - yr[c] * rs * dot);
+    }
+    free(dn);
     return 0;
 }
 
