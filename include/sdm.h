@@ -20,8 +20,23 @@
  *     any error nothing is launched, no output is touched, the call returns a
  *     negative status and sdm_last_error() (thread-local) describes it.  No
  *     entry point prints, throws or aborts.
- *   - Entry points are stateless and reentrant; calls on different streams
- *     may run concurrently if their buffers do not overlap.
+ *   - Process-wide state: three geometry switches (sdm_set_scan_slice_width,
+ *     sdm_set_scan_line_io, sdm_set_chunk_scan_cols) choose which scan kernel
+ *     a later launch runs and so the rounding order of its sums over rows;
+ *     the event profiler (sdm_profile_*); and, per device, a second stream
+ *     created on first use by the pipelined calls (sdm_forward with more than
+ *     one stage, sdm_scan_fwd_chunked with 32 or more chunks, sdm_scan_bwd
+ *     with more than one stage), whose enqueueing is serialised by a lock.
+ *     Apart from these, calls keep no state between them and are thread safe:
+ *     calls on different streams may run concurrently if their buffers do not
+ *     overlap (pipelined calls on one device then share its second stream).
+ *   - SDM_DEBUG=1 in the environment makes sdm_scan_fwd, sdm_scan_fwd_chunked
+ *     and sdm_scan_bwd check every token's slot lists on the device first (ids
+ *     in [0, N) and distinct within a list, the condition Sec. 3.1 step 2's
+ *     sets imply and the backward's replace step needs) and return
+ *     SDM_ERR_INVALID_ARG before any output is touched.  The check uses word 1
+ *     of the workspace and synchronises the stream; without it a repeated id
+ *     is undefined behaviour and an id out of range is clamped and flagged.
  *   - dtype codes: SDM_F32 (IEEE fp32) or SDM_BF16 (bfloat16).  Memory
  *     tables, outputs and gradients are always fp32.
  */
@@ -152,6 +167,7 @@ int sdm_forward(const void* q, const void* k, int x_dtype,
 
 size_t sdm_scan_fwd_workspace_bytes(int B, int H, int T, int W, int R);
 size_t sdm_scan_saved_bytes(int B, int H, int T, int W, int d_v);
+
 
 /* ------------------------------------------------------------------------
  * sdm_scan_fwd_chunked — the recurrence of sdm_scan_fwd by the chunk-parallel

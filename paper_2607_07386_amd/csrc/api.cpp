@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <algorithm>
 #include <atomic>
@@ -88,6 +89,29 @@ int check_scan_common(const int32_t* w_idx, const float* w_val, int W, const int
     if (!aligned(w_idx, 16) || !aligned(w_val, 16) || !aligned(r_idx, 16) || !aligned(r_val, 16) ||
         !aligned(v, 16) || !aligned(alpha, 4) || !aligned(beta, 4) || !aligned(mem, 16))
         return fail(SDM_ERR_INVALID_ARG, "misaligned pointer (16-byte alignment required)");
+    return SDM_OK;
+}
+
+// SDM_DEBUG=1 in the environment: the scans first check every token's slot
+// lists on the device (ids in [0, N), distinct within a list) and return
+// SDM_ERR_INVALID_ARG before touching any output.  The check synchronises the
+// stream and uses word 1 of the workspace header.
+bool debug_checks() {
+    const char* e = std::getenv("SDM_DEBUG");
+    return e && e[0] == '1' && e[1] == 0;
+}
+
+int debug_check_ids(const int32_t* w_idx, int W, const int32_t* r_idx, int R, int64_t ntok, int64_t N,
+                    void* workspace, hipStream_t st) {
+    unsigned int* flag = static_cast<unsigned int*>(workspace) + 1;
+    hipError_t e = sdm_launch_zero_words(workspace, 4, st);
+    if (e == hipSuccess) e = sdm_launch_check_ids(w_idx, W, r_idx, R, ntok, N, flag, st);
+    unsigned int h = 0;
+    if (e == hipSuccess) e = hipMemcpyAsync(&h, flag, sizeof(h), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, "SDM_DEBUG slot-list check");
+    if (h & 2u) return fail(SDM_ERR_INVALID_ARG, "SDM_DEBUG: a token's slot list repeats an id");
+    if (h & 1u) return fail(SDM_ERR_INVALID_ARG, "SDM_DEBUG: a slot id lies outside [0, N)");
     return SDM_OK;
 }
 
@@ -357,6 +381,9 @@ int sdm_scan_fwd(const int32_t* w_idx, const float* w_val, int W, const int32_t*
     rc = check_scan_fwd_rest(W, R, in_dtype, B, H, T, d_v, y, saved, saved_bytes, workspace, ws_bytes);
     if (rc != SDM_OK) return rc;
     hipStream_t st = (hipStream_t)stream;
+    if (debug_checks() &&
+        (rc = debug_check_ids(w_idx, W, r_idx, R, (int64_t)B * H * T, N, workspace, st)) != SDM_OK)
+        return rc;
     hipError_t e = sdm_launch_zero_words(workspace, 4, st);
     if (e != hipSuccess) return hip_fail(e, "sdm_scan_fwd flag reset");
     ScanFwdArgs a;
@@ -393,6 +420,9 @@ int sdm_scan_fwd_chunked(const int32_t* w_idx, const float* w_val, int W, const 
         return fail(SDM_ERR_INVALID_ARG, "workspace must be a 256-byte aligned pointer");
     if (ws_bytes < need) return fail(SDM_ERR_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, need);
     hipStream_t st = (hipStream_t)stream;
+    if (debug_checks() &&
+        (rc = debug_check_ids(w_idx, W, r_idx, R, (int64_t)B * H * T, N, workspace, st)) != SDM_OK)
+        return rc;
     hipError_t e = sdm_launch_zero_words(workspace, 4, st);
     if (e != hipSuccess) return hip_fail(e, "sdm_scan_fwd_chunked flag reset");
     ScanFwdArgs a;
@@ -452,13 +482,15 @@ int sdm_scan_fwd_chunked(const int32_t* w_idx, const float* w_val, int W, const 
     return SDM_OK;
 }
 
+}  // extern "C"
+
 // ---- fused forward: addressing pipelined with the scan over chunks of tokens ----
 
-int sdm_forward(const void* q, const void* k, int x_dtype, const void* cb_q, const void* cb_k, int d_k,
-                int topk, const void* v, const void* alpha, const void* beta, int in_dtype, float* mem,
-                int B, int H, int T, int d_v, int64_t N, int32_t* r_idx, float* r_val, int32_t* w_idx,
-                float* w_val, float* y, float* saved, size_t saved_bytes, int chunk, void* workspace,
-                size_t ws_bytes, void* stream) {
+int sdm_forward_impl(const void* q, const void* k, int x_dtype, const void* cb_q, const void* cb_k, int d_k,
+                     int topk, const void* v, const void* alpha, const void* beta, int in_dtype, float* mem,
+                     int B, int H, int T, int d_v, int64_t N, int32_t* r_idx, float* r_val, int32_t* w_idx,
+                     float* w_val, float* y, float* saved, size_t saved_bytes, int chunk, void* workspace,
+                     size_t ws_bytes, void* stream, bool pipelined) {
     g_err[0] = 0;
     int s = 0;
     int rc = check_address(q, x_dtype, cb_q, B, H, T, d_k, N, topk, r_idx, r_val, nullptr, &s);
@@ -489,7 +521,7 @@ int sdm_forward(const void* q, const void* k, int x_dtype, const void* cb_q, con
     // addressing cannot overlap anything), then stages of len tokens; all
     // multiples of 64 tokens, at most kMaxChunks of them
     int len = T, first = T, nchunks = 1;
-    if (chunk > 0 || T >= 2048) {
+    if (pipelined && (chunk > 0 || T >= 2048)) {
         len = chunk > 0 ? round_up(chunk, 64) : round_up((T + 3) / 4, 64);
         len = std::max(len, round_up((T + kMaxChunks - 2) / (kMaxChunks - 1), 64));
         first = std::min(T, round_up(std::max(len / 4, 64), 64));
@@ -557,6 +589,20 @@ int sdm_forward(const void* q, const void* k, int x_dtype, const void* cb_q, con
     return SDM_OK;
 }
 
+int sdm_set_error(int status, const char* msg) { return fail(status, "%s", msg); }
+
+extern "C" {
+
+int sdm_forward(const void* q, const void* k, int x_dtype, const void* cb_q, const void* cb_k, int d_k,
+                int topk, const void* v, const void* alpha, const void* beta, int in_dtype, float* mem,
+                int B, int H, int T, int d_v, int64_t N, int32_t* r_idx, float* r_val, int32_t* w_idx,
+                float* w_val, float* y, float* saved, size_t saved_bytes, int chunk, void* workspace,
+                size_t ws_bytes, void* stream) {
+    return sdm_forward_impl(q, k, x_dtype, cb_q, cb_k, d_k, topk, v, alpha, beta, in_dtype, mem, B, H, T, d_v,
+                            N, r_idx, r_val, w_idx, w_val, y, saved, saved_bytes, chunk, workspace, ws_bytes,
+                            stream, true);
+}
+
 int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, const int32_t* w_idx,
                  const float* w_val, int W, const int32_t* r_idx, const float* r_val, int R,
                  const void* v, const void* alpha, const void* beta, int in_dtype, float* mem,
@@ -593,6 +639,9 @@ int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, cons
         return fail(SDM_ERR_INVALID_ARG, "workspace must be a 256-byte aligned pointer");
     if (ws_bytes < need) return fail(SDM_ERR_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, need);
     hipStream_t st = (hipStream_t)stream;
+    if (debug_checks() && (int64_t)B * H * T > 0 &&
+        (rc = debug_check_ids(w_idx, W, r_idx, R, (int64_t)B * H * T, N, workspace, st)) != SDM_OK)
+        return rc;
     hipError_t e = sdm_launch_zero_words(workspace, 4, st);
     if (e != hipSuccess) return hip_fail(e, "sdm_scan_bwd flag reset");
     // adjoint of the memory starts as dL/dM_T (on `stream`, before the first scan;

@@ -295,6 +295,39 @@ hipError_t sdm_launch_bwd_prep(const ScanBwdArgs& a, hipStream_t st) {
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- debug id check
+// One thread per (token, side): flags bit 0 if a slot id lies outside [0, N),
+// bit 1 if an id repeats within the token's list (the backward's replace step
+// G[i_n] = alpha Dbar_n needs distinct write ids).  Debug builds of a call
+// only: O(K^2) compares per list.
+namespace {
+__global__ __launch_bounds__(256) void check_ids_kernel(const int32_t* __restrict__ w_idx, int W,
+                                                        const int32_t* __restrict__ r_idx, int R,
+                                                        int64_t ntok, int64_t N, unsigned int* __restrict__ flag) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= 2 * ntok) return;
+    const bool wside = i < ntok;
+    const int K = wside ? W : R;
+    const int32_t* lst = wside ? w_idx + i * W : r_idx + (i - ntok) * R;
+    unsigned int bad = 0u;
+    for (int a = 0; a < K; ++a) {
+        const int32_t s = lst[a];
+        if (s < 0 || s >= N) bad |= 1u;
+        for (int b = a + 1; b < K; ++b)
+            if (lst[b] == s) bad |= 2u;
+    }
+    if (bad) atomicOr(flag, bad);
+}
+}  // namespace
+
+hipError_t sdm_launch_check_ids(const int32_t* w_idx, int W, const int32_t* r_idx, int R, int64_t ntok,
+                                int64_t N, unsigned int* flag, hipStream_t st) {
+    const int64_t n = 2 * ntok;
+    const unsigned int blocks = (unsigned int)((n + 255) / 256);
+    hipLaunchKernelGGL(check_ids_kernel, dim3(blocks), dim3(256), 0, st, w_idx, W, r_idx, R, ntok, N, flag);
+    return hipGetLastError();
+}
+
 template hipError_t sdm_launch_fwd_prep<SDM_FWD_PD>(const ScanFwdArgs&, hipStream_t);
 template hipError_t sdm_launch_bwd_prep<SDM_BWD_PD>(const ScanBwdArgs&, hipStream_t);
 template hipError_t sdm_launch_bwd_prep<2>(const ScanBwdArgs&, hipStream_t);

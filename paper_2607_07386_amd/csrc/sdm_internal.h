@@ -158,10 +158,26 @@ hipError_t sdm_launch_bwd_prep(const ScanBwdArgs& a, hipStream_t st);
 bool sdm_bwd_plan_ok(int W, int R, int dv, int in_dtype);
 size_t sdm_bwd_ws_bytes(int B, int H, int T, int W, int R, int dv);
 
+// Debug check of slot lists (range and distinctness within each token's list):
+// ORs bit 0 (out of range) and bit 1 (repeated id) into *flag.
+hipError_t sdm_launch_check_ids(const int32_t* w_idx, int W, const int32_t* r_idx, int R, int64_t ntok,
+                                int64_t N, unsigned int* flag, hipStream_t st);
+
 hipError_t sdm_launch_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int dv,
                                hipStream_t st);
 hipError_t sdm_launch_copy(float* dst, const float* src, size_t n, hipStream_t st);
 hipError_t sdm_launch_zero_words(void* p, int n, hipStream_t st);
+
+// The body of sdm_forward.  pipelined = false runs every step on `stream` in
+// one stage (no second stream, no events): the path of the allocation-free
+// entry point.
+int sdm_forward_impl(const void* q, const void* k, int x_dtype, const void* cb_q, const void* cb_k, int d_k,
+                     int topk, const void* v, const void* alpha, const void* beta, int in_dtype, float* mem,
+                     int B, int H, int T, int d_v, int64_t N, int32_t* r_idx, float* r_val, int32_t* w_idx,
+                     float* w_val, float* y, float* saved, size_t saved_bytes, int chunk, void* workspace,
+                     size_t ws_bytes, void* stream, bool pipelined);
+// Sets the thread's sdm_last_error() text and returns status.
+int sdm_set_error(int status, const char* msg);
 
 // Event bracketing of kernel launches (active only while profiling is enabled).
 void sdm_prof_begin(int kernel, hipStream_t st);

@@ -1,7 +1,8 @@
 """Python binding of libsdm.so: argument marshalling only.
 
 Every step of the SDM path runs in the HIP kernels behind the C ABI declared
-in ``include/sdm.h``; this module checks tensor placement/dtypes, allocates
+in ``include/sdm.h``; this module checks every tensor's shape, dtype and
+placement against the sizes it passes (before any launch), allocates
 outputs and workspaces with torch (device memory), and passes raw pointers and
 the current HIP stream.  There is no fallback: if the library is missing or a
 call fails, an exception is raised.
@@ -117,6 +118,70 @@ def _dev(*ts):
     return dev
 
 
+def _expect(t, name: str, shape, dtypes):
+    """Raise unless t is a tensor of exactly this shape and one of these dtypes.
+    The C ABI sees only pointers and the sizes derived from one tensor, so
+    every other tensor must agree with them before anything is launched."""
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {[str(d) for d in dtypes]}")
+
+
+_IN = (torch.float32, torch.bfloat16)
+_F32 = (torch.float32,)
+_I32 = (torch.int32,)
+
+
+def _expect_dims(t, name: str, nd: int):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dim() != nd:
+        raise ValueError(f"{name} must have {nd} dimensions, got shape {tuple(t.shape)}")
+
+
+def _check_scan_args(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem):
+    """Shapes and dtypes of a scan's inputs; returns (B, H, T, d_v, W, R, N)."""
+    _expect_dims(v, "v", 4)
+    _expect_dims(mem, "mem", 4)
+    _expect_dims(w_idx, "w_idx", 4)
+    _expect_dims(r_idx, "r_idx", 4)
+    B, H, T, dv = v.shape
+    W, R = w_idx.shape[-1], r_idx.shape[-1]
+    N = mem.shape[-2]
+    if v.dtype not in _IN:
+        raise TypeError(f"v has dtype {v.dtype}, expected float32 or bfloat16")
+    _expect(alpha, "alpha", (B, H, T), (v.dtype,))
+    _expect(beta, "beta", (B, H, T), (v.dtype,))
+    _expect(w_idx, "w_idx", (B, H, T, W), _I32)
+    _expect(w_val, "w_val", (B, H, T, W), _F32)
+    _expect(r_idx, "r_idx", (B, H, T, R), _I32)
+    _expect(r_val, "r_val", (B, H, T, R), _F32)
+    _expect(mem, "mem", (B, H, N, dv), _F32)
+    return B, H, T, dv, W, R, N
+
+
+def _check_codebook(cb, name, x, N):
+    if cb is None:
+        return
+    s = int(round(N ** 0.5))
+    dk = x.shape[-1]
+    _expect(cb, name, (x.shape[1], 2, s, dk // 2), (x.dtype,))
+
+
+def _check_ws(ws, need: int, name="workspace"):
+    if ws is None:
+        return
+    if not isinstance(ws, torch.Tensor) or ws.dtype != torch.uint8 or ws.dim() != 1:
+        raise TypeError(f"{name} must be a 1-D uint8 tensor")
+    if ws.numel() < need:
+        raise ValueError(f"{name} holds {ws.numel()} bytes, {need} needed")
+
+
 def _ws(nbytes: int, device) -> torch.Tensor:
     # torch's caching allocator returns 256-byte (or better) aligned blocks
     return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
@@ -126,13 +191,15 @@ def address(x: torch.Tensor, codebook: torch.Tensor | None, N: int, topk: int,
             want_score: bool = False):
     """Product-key addressing of one side.  x [B,H,T,d_k]; codebook [H,2,sqrtN,d_k/2]
     (same dtype) or None for direct mode.  Returns (idx int32, val fp32[, score])."""
+    _expect_dims(x, "x", 4)
+    if x.dtype not in _IN:
+        raise TypeError(f"x has dtype {x.dtype}, expected float32 or bfloat16")
+    _check_codebook(codebook, "codebook", x, N)
     dev = _dev(x, codebook)
     B, H, T, dk = x.shape
     idx = torch.empty((B, H, T, topk), dtype=torch.int32, device=dev)
     val = torch.empty((B, H, T, topk), dtype=torch.float32, device=dev)
     score = torch.empty_like(val) if want_score else None
-    if codebook is not None and codebook.dtype != x.dtype:
-        raise TypeError("codebook dtype must match x")
     rc = lib().sdm_address(_ptr(x), _dtype_code(x), _ptr(codebook), B, H, T, dk, N, topk,
                            _ptr(idx), _ptr(val), _ptr(score), _stream(dev))
     _check("sdm_address", rc)
@@ -149,14 +216,13 @@ def saved_buffer(B, H, T, W, d_v, device) -> torch.Tensor:
 
 def scan_fwd(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, saved=None, workspace=None, y=None):
     """Sparse gated-delta scan, in place on mem (M_0 -> M_T).  Returns y [B,H,T,d_v] fp32."""
+    B, H, T, dv, W, R, N = _check_scan_args(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem)
+    if saved is not None:
+        _expect(saved, "saved", (B, H, T, W, dv), _F32)
+    if y is not None:
+        _expect(y, "y", (B, H, T, dv), _F32)
+    _check_ws(workspace, lib().sdm_scan_fwd_workspace_bytes(B, H, T, W, R) if workspace is not None else 0)
     dev = _dev(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, saved, y)
-    B, H, T, dv = v.shape
-    W, R = w_idx.shape[-1], r_idx.shape[-1]
-    N = mem.shape[-2]
-    if not (v.dtype == alpha.dtype == beta.dtype):
-        raise TypeError("v, alpha, beta must share a dtype")
-    if mem.dtype != torch.float32:
-        raise TypeError("mem must be fp32")
     if y is None:
         y = torch.empty((B, H, T, dv), dtype=torch.float32, device=dev)
     if workspace is None:
@@ -177,14 +243,11 @@ def chunked_workspace(B, H, T, W, R, device) -> torch.Tensor:
 def scan_fwd_chunked(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, workspace=None, y=None):
     """The same recurrence as scan_fwd by the chunk-parallel form (64-token chunks), in place on
     mem.  Inference only (no undo log); W, R <= 64.  Returns y [B,H,T,d_v] fp32."""
+    B, H, T, dv, W, R, N = _check_scan_args(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem)
+    if y is not None:
+        _expect(y, "y", (B, H, T, dv), _F32)
+    _check_ws(workspace, lib().sdm_scan_fwd_chunked_workspace_bytes(B, H, T, W, R) if workspace is not None else 0)
     dev = _dev(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, y)
-    B, H, T, dv = v.shape
-    W, R = w_idx.shape[-1], r_idx.shape[-1]
-    N = mem.shape[-2]
-    if not (v.dtype == alpha.dtype == beta.dtype):
-        raise TypeError("v, alpha, beta must share a dtype")
-    if mem.dtype != torch.float32:
-        raise TypeError("mem must be fp32")
     if y is None:
         y = torch.empty((B, H, T, dv), dtype=torch.float32, device=dev)
     if workspace is None:
@@ -196,31 +259,53 @@ def scan_fwd_chunked(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, workspace=
     return y
 
 
+def _forward_args(q, k, cb_q, cb_k, v, alpha, beta, mem, N, topk, saved, y, out, workspace):
+    """Checks of sdm_forward's arguments; returns (B, H, T, d_k, d_v, device, outputs)."""
+    _expect_dims(q, "q", 4)
+    _expect_dims(v, "v", 4)
+    _expect_dims(mem, "mem", 4)
+    B, H, T, dk = q.shape
+    dv = v.shape[-1]
+    if q.dtype not in _IN:
+        raise TypeError(f"q has dtype {q.dtype}, expected float32 or bfloat16")
+    _expect(k, "k", (B, H, T, dk), (q.dtype,))
+    _check_codebook(cb_q, "cb_q", q, N)
+    _check_codebook(cb_k, "cb_k", q, N)
+    if v.dtype not in _IN:
+        raise TypeError(f"v has dtype {v.dtype}, expected float32 or bfloat16")
+    _expect(v, "v", (B, H, T, dv), (v.dtype,))
+    _expect(alpha, "alpha", (B, H, T), (v.dtype,))
+    _expect(beta, "beta", (B, H, T), (v.dtype,))
+    _expect(mem, "mem", (B, H, N, dv), _F32)
+    if saved is not None:
+        _expect(saved, "saved", (B, H, T, topk, dv), _F32)
+    o = dict(out or {})
+    if y is not None:
+        o["y"] = y
+    shp = (B, H, T, topk)
+    for name, dt in (("r_idx", _I32), ("w_idx", _I32), ("r_val", _F32), ("w_val", _F32)):
+        if name in o:
+            _expect(o[name], f"out['{name}']", shp, dt)
+    if "y" in o:
+        _expect(o["y"], "y", (B, H, T, dv), _F32)
+    _check_ws(workspace, lib().sdm_scan_fwd_workspace_bytes(B, H, T, topk, topk) if workspace is not None else 0)
+    dev = _dev(q, k, cb_q, cb_k, v, alpha, beta, mem, saved, *o.values())
+    for name, dt in (("r_idx", torch.int32), ("w_idx", torch.int32), ("r_val", torch.float32),
+                     ("w_val", torch.float32)):
+        if name not in o:
+            o[name] = torch.empty(shp, dtype=dt, device=dev)
+    if "y" not in o:
+        o["y"] = torch.empty((B, H, T, dv), dtype=torch.float32, device=dev)
+    return B, H, T, dk, dv, dev, o
+
+
 def forward(q, k, cb_q, cb_k, v, alpha, beta, mem, N: int, topk: int, saved=None, workspace=None,
             y=None, out=None, chunk: int = 0):
     """The layer's memory forward in one call: addressing of q (read side) and k (write side)
     pipelined with the scan over chunks of tokens; in place on mem.  Returns a dict with y,
     r_idx, r_val, w_idx, w_val.  out: optional dict of preallocated outputs of those names."""
-    dev = _dev(q, k, cb_q, cb_k, v, alpha, beta, mem, saved, y)
-    B, H, T, dk = q.shape
-    dv = v.shape[-1]
-    if k.shape != q.shape or k.dtype != q.dtype:
-        raise TypeError("q and k must share shape and dtype")
-    for cb in (cb_q, cb_k):
-        if cb is not None and cb.dtype != q.dtype:
-            raise TypeError("codebook dtype must match q and k")
-    if not (v.dtype == alpha.dtype == beta.dtype):
-        raise TypeError("v, alpha, beta must share a dtype")
-    if mem.dtype != torch.float32:
-        raise TypeError("mem must be fp32")
-    o = dict(out or {})
-    shp = (B, H, T, topk)
-    for name, dt in (("r_idx", torch.int32), ("w_idx", torch.int32), ("r_val", torch.float32),
-                     ("w_val", torch.float32)):
-        if name not in o:
-            o[name] = torch.empty(shp, dtype=dt, device=dev)
-    o["y"] = y if y is not None else o.get("y", torch.empty((B, H, T, dv), dtype=torch.float32, device=dev))
-    _dev(*o.values())
+    B, H, T, dk, dv, dev, o = _forward_args(q, k, cb_q, cb_k, v, alpha, beta, mem, N, topk, saved, y, out,
+                                            workspace)
     if workspace is None:
         workspace = fwd_workspace(B, H, T, topk, topk, dev)
     sb = saved.numel() * 4 if saved is not None else 0
@@ -242,10 +327,23 @@ def scan_bwd(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, saved, dy, dmem_T=
              workspace=None, dmem0=None):
     """Backward of scan_fwd (+ addressing).  mem: M_T in, M_0 out.  Returns a dict of
     gradients: dv, dalpha, dbeta, dmem0, dw_val, dr_val and (if want_dqk) dq, dk."""
-    dev = _dev(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, saved, dy, dmem_T, cb_q, cb_k)
-    B, H, T, dv_ = v.shape
-    W, R = w_idx.shape[-1], r_idx.shape[-1]
-    N = mem.shape[-2]
+    B, H, T, dv_, W, R, N = _check_scan_args(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem)
+    _expect(saved, "saved", (B, H, T, W, dv_), _F32)
+    _expect(dy, "dy", (B, H, T, dv_), _F32)
+    if dmem_T is not None:
+        _expect(dmem_T, "dmem_T", (B, H, N, dv_), _F32)
+    if dmem0 is not None:
+        _expect(dmem0, "dmem0", (B, H, N, dv_), _F32)
+    if want_dqk:
+        if d_k is None:
+            raise ValueError("d_k is required for addressing gradients")
+        for cb, nm in ((cb_q, "cb_q"), (cb_k, "cb_k")):
+            if cb is not None:
+                _expect(cb, nm, (H, 2, int(round(N ** 0.5)), d_k // 2), _IN)
+        if cb_q is not None and cb_k is not None and cb_q.dtype != cb_k.dtype:
+            raise TypeError("cb_q and cb_k must share a dtype")
+    _check_ws(workspace, lib().sdm_scan_bwd_workspace_bytes(B, H, T, W, R, dv_) if workspace is not None else 0)
+    dev = _dev(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, saved, dy, dmem_T, cb_q, cb_k, dmem0)
     f32 = dict(dtype=torch.float32, device=dev)
     out = dict(dv=torch.empty((B, H, T, dv_), **f32), dalpha=torch.empty((B, H, T), **f32),
                dbeta=torch.empty((B, H, T), **f32),
@@ -254,8 +352,6 @@ def scan_bwd(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, saved, dy, dmem_T=
     dq = dk = None
     cb_dtype = SDM_F32
     if want_dqk:
-        if d_k is None:
-            raise ValueError("d_k is required for addressing gradients")
         dq = torch.empty((B, H, T, d_k), **f32)
         dk = torch.empty((B, H, T, d_k), **f32)
         cb = cb_q if cb_q is not None else cb_k
@@ -277,8 +373,12 @@ def scan_bwd(w_idx, w_val, r_idx, r_val, v, alpha, beta, mem, saved, dy, dmem_T=
 
 def mem_init(dst: torch.Tensor, m0: torch.Tensor | None):
     """dst [B,H,N,d_v] = m0 [H,N,d_v] broadcast over B (or zero when m0 is None)."""
-    dev = _dev(dst, m0)
+    _expect_dims(dst, "dst", 4)
     B, H, N, dv = dst.shape
+    _expect(dst, "dst", (B, H, N, dv), _F32)
+    if m0 is not None:
+        _expect(m0, "m0", (H, N, dv), _F32)
+    dev = _dev(dst, m0)
     rc = lib().sdm_mem_init(_ptr(dst), _ptr(m0), B, H, N, dv, _stream(dev))
     _check("sdm_mem_init", rc)
     return dst

@@ -23,6 +23,12 @@ CASES = {
     # 128 streams: an overlapped stage has more 16-token tiles than the capped addressing grid
     # has workgroups, so workgroups take several tiles
     "bf16-128-streams": synth.Workload("t", B=8, H=16, T=320, d_k=64, d_v=32, N=1024, topk=8, seed=44),
+    # top-64 reads and writes, direct mode: the 64-row line-cooperative scan over token-range stages
+    "bf16-direct-k64": synth.Workload("t", B=2, H=2, T=400, d_k=256, d_v=128, N=16384, topk=64, seed=45,
+                                      codebook=False),
+    # the paper's 1.4B layer (sqrt(N) = 240, d_v = 960, top-64, direct mode) at reduced T
+    "paper-1.4b-layer": synth.Workload("t", B=1, H=2, T=300, d_k=480, d_v=960, N=57600, topk=64, seed=46,
+                                       codebook=False),
 }
 
 
@@ -40,7 +46,7 @@ def _fused(w, inp, chunk, save):
 
 
 @pytest.mark.parametrize("name", list(CASES))
-@pytest.mark.parametrize("chunk", [0, 64, 100, 256, 4096])
+@pytest.mark.parametrize("chunk", [0, 64, 100, 256, 448, 4096])
 def test_fused_forward_matches_separate_calls(name, chunk, slice_width):
     w = CASES[name]
     inp = synth.Inputs(w)

@@ -18,7 +18,8 @@ import torch
 import oracle
 import synth
 from paper_2607_07386_amd import sdm
-from tests.gpu_util import (DEV, compare_address, gpu_forward, rel_err, to_dev, tol_for)
+from tests.gpu_util import (DEV, REGRESSION_TOL, compare_address, gpu_forward, rel_err, to_dev, tol_for,
+                            within)
 
 pytestmark = pytest.mark.gpu
 
@@ -52,12 +53,12 @@ def oracle_address_rows(w, inp, x_st, streams):
 def check_addressing(w, inp, g, streams):
     stats = {}
     for side, x_st, gi, gv in (("read", inp.q, g["r_idx"], g["r_val"]), ("write", inp.k, g["w_idx"], g["w_val"])):
-        (oi, ov, osc), cbs = oracle_address_rows(w, inp, x_st, streams)
-        gidx = np_(gi).reshape(-1, w.T, w.topk)[streams].reshape(-1, w.topk)
-        gval = np_(gv).reshape(-1, w.T, w.topk)[streams].reshape(-1, w.topk)
+        (oi, ov, _), cbs = oracle_address_rows(w, inp, x_st, streams)
+        gidx = rows_of(gi, streams, (w.T, w.topk)).reshape(-1, w.topk)
+        gval = rows_of(gv, streams, (w.T, w.topk)).reshape(-1, w.topk)
         x64 = x_st.f64.reshape(-1, w.T, w.d_k)[streams].reshape(-1, w.d_k)
         st = compare_address(gidx, gval, oi.reshape(-1, w.topk), ov.reshape(-1, w.topk),
-                             osc.reshape(-1, w.topk), x64, lambda r: cbs[r // w.T], w.sqrtN)
+                             x64, lambda r: cbs[r // w.T], w.sqrtN)
         stats[side] = st
     return stats
 
@@ -67,7 +68,7 @@ def oracle_scan_rows(w, inp, g, streams, m0_of_stream, save=False):
     S = len(streams)
 
     def take(t, last):
-        return np_(t).reshape((-1, w.T) + last)[streams]
+        return rows_of(t, streams, (w.T,) + last)
 
     wi, wv = take(g["w_idx"], (w.topk,)), take(g["w_val"], (w.topk,))
     ri, rv = take(g["r_idx"], (w.topk,)), take(g["r_val"], (w.topk,))
@@ -85,10 +86,15 @@ def oracle_scan_rows(w, inp, g, streams, m0_of_stream, save=False):
                 y=res[0] if save else res, saved=res[1] if save else None)
 
 
+def rows_of(t, streams, last):
+    """The sampled (b, h) streams of a device tensor, copied to the host alone."""
+    return np_(t.reshape((-1,) + last)[torch.as_tensor(streams, device=t.device)])
+
+
 def check_scan(w, g, o, streams, name):
     tol = tol_for(w)
-    y = np_(g["y"]).reshape(-1, w.T, w.d_v)[streams]
-    memg = np_(g["mem"]).reshape(-1, w.N, w.d_v)[streams]
+    y = rows_of(g["y"], streams, (w.T, w.d_v))
+    memg = rows_of(g["mem"], streams, (w.N, w.d_v))
     ey, em = rel_err(y, o["y"]), rel_err(memg, o["mem"])
     # rows no token writes: bit-identical to M_0
     untouched_ok = True
@@ -96,8 +102,9 @@ def check_scan(w, g, o, streams, name):
         written = np.zeros(w.N, bool)
         written[o["wi"][i].ravel()] = True
         untouched_ok &= np.array_equal(memg[i][~written], o["m_init"][i][~written].astype(np.float32))
-    report(name, y_rel_err=ey, mem_rel_err=em, tol=tol, untouched_bit_exact=bool(untouched_ok))
-    assert ey <= tol and em <= tol, (ey, em)
+    report(name, y_rel_err=ey, mem_rel_err=em, tol=tol, regression_tol=REGRESSION_TOL,
+           untouched_bit_exact=bool(untouched_ok))
+    assert within(ey, w) and within(em, w), (ey, em)
     assert untouched_ok
 
 
@@ -373,6 +380,52 @@ def test_out_of_range_slot_is_clamped_and_reported():
     sdm.check_device_errors(ws)     # cleared
 
 
+def test_debug_check_rejects_bad_slot_lists(monkeypatch):
+    """SDM_DEBUG=1: a repeated id within a token's list, or an id outside
+    [0, N), makes the scans return SDM_ERR_INVALID_ARG with their outputs
+    untouched; valid lists give the same results as without the check."""
+    S, T, N, W, R, dv = 2, 40, 64, 5, 4, 8
+    rng = np.random.default_rng(3)
+    wi = np.stack([np.stack([np.sort(rng.choice(N, W, replace=False)) for _ in range(T)]) for _ in range(S)])
+    ri = np.stack([np.stack([np.sort(rng.choice(N, R, replace=False)) for _ in range(T)]) for _ in range(S)])
+    t_ = lambda a: torch.from_numpy(np.ascontiguousarray(a))[:, None].to(DEV)
+    wi, ri = t_(wi.astype(np.int32)), t_(ri.astype(np.int32))
+    wv, rv = t_(rng.random((S, T, W)).astype(np.float32)), t_(rng.random((S, T, R)).astype(np.float32))
+    v = t_(rng.standard_normal((S, T, dv)).astype(np.float32))
+    g = t_(rng.uniform(0.1, 1.0, (S, T)).astype(np.float32))
+    m0 = torch.randn((S, 1, N, dv), device=DEV)
+    mem_plain = m0.clone()
+    y_plain = sdm.scan_fwd(wi, wv, ri, rv, v, g, g, mem_plain)
+    monkeypatch.setenv("SDM_DEBUG", "1")
+    mem = m0.clone()
+    y = sdm.scan_fwd(wi, wv, ri, rv, v, g, g, mem)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y_plain) and torch.equal(mem, mem_plain)
+    dup = wi.clone()
+    dup[1, 0, 17, 3] = dup[1, 0, 17, 1]
+    oob = ri.clone()
+    oob[0, 0, 5, 0] = N
+    for wl, rl, what in ((dup, ri, "repeats"), (wi, oob, "outside")):
+        for fn in (lambda m, yy: sdm.scan_fwd(wl, wv, rl, rv, v, g, g, m, y=yy),
+                   lambda m, yy: sdm.scan_fwd_chunked(wl, wv, rl, rv, v, g, g, m, y=yy)):
+            mem = m0.clone()
+            yy = torch.full((S, 1, T, dv), 7.0, device=DEV)
+            with pytest.raises(sdm.SdmError) as e:
+                fn(mem, yy)
+            assert e.value.status == -1 and what in str(e.value)
+            torch.cuda.synchronize()
+            assert torch.equal(mem, m0) and bool((yy == 7.0).all())
+    saved = sdm.saved_buffer(S, 1, T, W, dv, DEV)
+    mem = m0.clone()
+    sdm.scan_fwd(wi, wv, ri, rv, v, g, g, mem, saved=saved)
+    memT = mem.clone()
+    with pytest.raises(sdm.SdmError) as e:
+        sdm.scan_bwd(dup, wv, ri, rv, v, g, g, mem, saved, torch.ones((S, 1, T, dv), device=DEV), want_dqk=False)
+    assert e.value.status == -1
+    torch.cuda.synchronize()
+    assert torch.equal(mem, memT)
+
+
 # --------------------------------------------------------------- backward
 BWD = {
     "bf16-small": synth.Workload("t", B=1, H=2, T=150, d_k=64, d_v=48, N=1024, topk=8, seed=31, train=True),
@@ -391,14 +444,17 @@ BWD = {
 }
 
 
-def run_backward_case(w, inp, streams, chunk=64):
-    g = gpu_forward(w, inp, save=True)
+def run_backward_case(w, inp, streams, chunk=64, fwd_chunk=None):
+    """Forward with the undo log (separate calls, or sdm_forward with stage
+    length fwd_chunk), then sdm_scan_bwd with the given chunk; oracle errors
+    of the sampled streams."""
+    g = gpu_forward(w, inp, save=True, chunk=fwd_chunk)
     dy = torch.from_numpy(inp.dy()).to(DEV)
     gr = sdm.scan_bwd(g["w_idx"], g["w_val"], g["r_idx"], g["r_val"], g["v"], g["alpha"], g["beta"],
                       g["mem"], g["saved"], dy, cb_q=g["cb"], cb_k=g["cb"], d_k=w.d_k, chunk=chunk)
     torch.cuda.synchronize()
     o = oracle_scan_rows(w, inp, g, streams, m0_fn(w, inp), save=True)
-    dy64 = np_(dy).reshape(-1, w.T, w.d_v)[streams].astype(np.float64)
+    dy64 = rows_of(dy, streams, (w.T, w.d_v)).astype(np.float64)
     memT = o["mem"].copy()
     og = oracle.scan_bwd(o["wi"], o["wv"], o["ri"], o["rv"], o["v"], o["al"], o["be"], memT, o["saved"], dy64)
     assert np.array_equal(memT, o["m_init"])
@@ -406,9 +462,9 @@ def run_backward_case(w, inp, streams, chunk=64):
     out = {}
     for name, key, last in (("dv", "dv", (w.d_v,)), ("dalpha", "dalpha", ()), ("dbeta", "dbeta", ()),
                             ("dw_val", "dw_val", (w.topk,)), ("dr_val", "dr_val", (w.topk,))):
-        gg = np_(gr[key]).reshape((-1, w.T) + last)[streams]
+        gg = rows_of(gr[key], streams, (w.T,) + last)
         out[name] = rel_err(gg, og[name])
-    gd = np_(gr["dmem0"]).reshape(-1, w.N, w.d_v)[streams]
+    gd = rows_of(gr["dmem0"], streams, (w.N, w.d_v))
     out["dmem0"] = rel_err(gd, og["dmem0"])
     # addressing gradients of the sampled streams, from the oracle's weight gradients
     for side, idx, val, dval, key in (("dq", o["ri"], o["rv"], og["dr_val"], "dq"),
@@ -417,9 +473,9 @@ def run_backward_case(w, inp, streams, chunk=64):
             oracle.address_bwd(None if cb is None else cb[inp.heads[s]][None], idx[i:i + 1, None],
                                val[i:i + 1, None], dval[i:i + 1, None], w.N, w.d_k)
             for i, s in enumerate(streams)])[:, 0]
-        gg = np_(gr[key]).reshape(-1, w.T, w.d_k)[streams]
+        gg = rows_of(gr[key], streams, (w.T, w.d_k))
         out[side] = rel_err(gg, ref)
-    restored = np_(g["mem"]).reshape(-1, w.N, w.d_v)[streams]
+    restored = rows_of(g["mem"], streams, (w.N, w.d_v))
     out["mem_restored_bit_exact"] = bool(np.array_equal(restored, o["m_init"].astype(np.float32)))
     return out, gr
 
@@ -431,10 +487,9 @@ def test_backward_small(name, slice_width):
     streams = list(range(w.B * w.H))
     errs, _ = run_backward_case(w, inp, streams)
     report(f"{name}/sw{slice_width}/bwd", **errs)
-    tol = tol_for(w)
     for k, e in errs.items():
         if k != "mem_restored_bit_exact":
-            assert e <= tol, (k, e)
+            assert within(e, w), (k, e)
     assert errs["mem_restored_bit_exact"]
 
 
@@ -488,39 +543,59 @@ def test_backward_line_io(name):
     report(f"{name}/bwd-line", **errs)
     for k, e in errs.items():
         if k != "mem_restored_bit_exact":
-            assert e <= tol_for(w), (k, e)
+            assert within(e, w), (k, e)
     assert errs["mem_restored_bit_exact"]
     for k in g_line:
         assert rel_err(np_(g_line[k]), np_(g_wave[k]).astype(np.float64)) <= 1e-5, k
 
 
 # ------------------------------------------------- full-size workloads, sampled streams
-def _full(cfg, streams_of):
+# Each runs the calls bench.py times: the 1.4B-shaped forward as sdm_forward
+# with 448-token stages, the training step as sdm_forward with the undo log
+# (the library's stage choice) and then sdm_scan_bwd with chunk 64.  The
+# long-context and learned-M0 workloads run sdm_forward with the library's
+# stages (a quarter of T).
+def _full(cfg, streams_of, chunk):
     w = synth.WORKLOADS[cfg]
     inp = synth.Inputs(w)
-    g = gpu_forward(w, inp)
+    g = gpu_forward(w, inp, chunk=chunk)
     S = w.B * w.H
     streams = streams_of(S)
     st = check_addressing(w, inp, g, streams)
     report(f"c{cfg}/address", **{f"{k}_{kk}": vv for k, v in st.items() for kk, vv in v.items()})
-    # distinct slots touched, for context
     o = oracle_scan_rows(w, inp, g, streams, m0_fn(w, inp))
     check_scan(w, g, o, streams, f"c{cfg}/scan")
 
 
 @pytest.mark.slow
 def test_full_c1():
-    _full(1, lambda S: [0, S // 2 + 3, S - 1])
+    _full(1, lambda S: [0, S // 2 + 3, S - 1], chunk=448)
 
 
 @pytest.mark.slow
 def test_full_c2():
-    _full(2, lambda S: [5])
+    _full(2, lambda S: [5], chunk=0)
 
 
 @pytest.mark.slow
 def test_full_c3():
-    _full(3, lambda S: [0, S - 1])
+    _full(3, lambda S: [0, S - 1], chunk=0)
+
+
+@pytest.mark.slow
+def test_full_paper_1p4b_layer():
+    """The paper's 1.4B layer shape as bench.py times it: 8 sequences of 4096
+    tokens, sqrt(N) = 240, d_v = 960, top-64 reads and writes, direct mode,
+    one sdm_forward call with the library's stages; two streams sampled."""
+    w = synth.Workload("paper-1.4b-layer", B=8, H=2, T=4096, d_k=480, d_v=960, N=57600, topk=64, seed=6,
+                       codebook=False)
+    inp = synth.Inputs(w)
+    g = gpu_forward(w, inp, chunk=0)
+    streams = [1, 14]
+    st = check_addressing(w, inp, g, streams)
+    report("paper-1.4b/address", **{f"{k}_{kk}": vv for k, v in st.items() for kk, vv in v.items()})
+    o = oracle_scan_rows(w, inp, g, streams, m0_fn(w, inp))
+    check_scan(w, g, o, streams, "paper-1.4b/scan")
 
 
 @pytest.mark.slow
@@ -528,11 +603,11 @@ def test_full_c4_training():
     w = synth.WORKLOADS[4]
     inp = synth.Inputs(w)
     S = w.B * w.H
-    errs, _ = run_backward_case(w, inp, [1, S - 2])
+    errs, _ = run_backward_case(w, inp, [1, S - 2], chunk=w.chunk, fwd_chunk=0)
     report("c4/bwd", **errs)
     for k, e in errs.items():
         if k != "mem_restored_bit_exact":
-            assert e <= tol_for(w), (k, e)
+            assert within(e, w), (k, e)
     assert errs["mem_restored_bit_exact"]
 
 
