@@ -168,6 +168,32 @@ int sdm_forward(const void* q, const void* k, int x_dtype,
 size_t sdm_scan_fwd_workspace_bytes(int B, int H, int T, int W, int R);
 size_t sdm_scan_saved_bytes(int B, int H, int T, int W, int d_v);
 
+/* ------------------------------------------------------------------------
+ * sdm_forward_noalloc — sdm_forward for callers that cannot allocate device
+ * memory or pass a workspace: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Same arguments, results and
+ * validation as sdm_forward without `chunk`, `workspace` and `ws_bytes`: the
+ * per-token records and device-error words live in a fixed device array of
+ * SDM_NOALLOC_SCRATCH_BYTES (64 MiB) that each GPU the library runs on holds
+ * until the process ends.  Sizes whose sdm_scan_fwd_workspace_bytes(B, H, T,
+ * topk, topk) exceeds it return SDM_ERR_UNSUPPORTED before any device call
+ * (at W = R = 32 that is about 102,000 token-heads, e.g. 16 x 16 streams of
+ * 400 tokens; any single-token step of up to 65,535 streams fits).
+ *   - Every step runs on `stream`, in one stage: no second stream, no events
+ *     (with the event profiler off), no hipMalloc, hipFree or other allocating
+ *     call.  The first call on a device looks up the array's address there.
+ *   - All calls on one GPU share its array, which keeps the last call's
+ *     contents (each call rewrites what it reads).  Calls that overlap in time
+ *     on one GPU race: serialise them (one stream, or events).
+ * ---------------------------------------------------------------------- */
+#define SDM_NOALLOC_SCRATCH_BYTES (64u << 20)
+int sdm_forward_noalloc(const void* q, const void* k, int x_dtype,
+                        const void* cb_q, const void* cb_k, int d_k, int topk,
+                        const void* v, const void* alpha, const void* beta, int in_dtype,
+                        float* mem, int B, int H, int T, int d_v, int64_t N,
+                        int32_t* r_idx, float* r_val, int32_t* w_idx, float* w_val,
+                        float* y, float* saved, size_t saved_bytes, void* stream);
+size_t sdm_forward_noalloc_max_bytes(void);
 
 /* ------------------------------------------------------------------------
  * sdm_scan_fwd_chunked — the recurrence of sdm_scan_fwd by the chunk-parallel

@@ -50,6 +50,10 @@ def lib() -> ctypes.CDLL:
         L.sdm_forward.argtypes = [P, P, I, P, P, I, I, P, P, P, I, P, I, I, I, I, I64, P, P, P, P, P, P,
                                   SZ, I, P, SZ, P]
         L.sdm_scan_fwd_chunked.argtypes = [P, P, I, P, P, I, P, P, P, I, P, I, I, I, I, I64, P, P, SZ, P]
+        L.sdm_forward_noalloc.argtypes = [P, P, I, P, P, I, I, P, P, P, I, P, I, I, I, I, I64, P, P, P, P, P,
+                                          P, SZ, P]
+        L.sdm_forward_noalloc_max_bytes.argtypes = []
+        L.sdm_forward_noalloc_max_bytes.restype = SZ
         L.sdm_scan_fwd_workspace_bytes.argtypes = [I, I, I, I, I]
         L.sdm_scan_fwd_chunked_workspace_bytes.argtypes = [I, I, I, I, I]
         L.sdm_scan_saved_bytes.argtypes = [I, I, I, I, I]
@@ -69,6 +73,7 @@ def lib() -> ctypes.CDLL:
         L.sdm_last_error.restype = ctypes.c_char_p
         L.sdm_version.restype = ctypes.c_char_p
         for f in ("sdm_address", "sdm_scan_fwd", "sdm_scan_fwd_chunked", "sdm_scan_bwd", "sdm_mem_init",
+                  "sdm_forward_noalloc",
                   "sdm_check_device_errors",
                   "sdm_profile_enable", "sdm_profile_select", "sdm_profile_read"):
             getattr(L, f).restype = I
@@ -315,6 +320,21 @@ def forward(q, k, cb_q, cb_k, v, alpha, beta, mem, N: int, topk: int, saved=None
                            _ptr(o["y"]), _ptr(saved), sb, int(chunk), _ptr(workspace), workspace.numel(),
                            _stream(dev))
     _check("sdm_forward", rc)
+    return o
+
+
+def forward_noalloc(q, k, cb_q, cb_k, v, alpha, beta, mem, N: int, topk: int, saved=None, y=None, out=None):
+    """sdm_forward_noalloc: the same forward with no workspace (the library's fixed device
+    array holds its records), every step on the current stream.  Outputs not given in
+    out / y are allocated here by torch; the C entry point itself allocates nothing."""
+    B, H, T, dk, dv, dev, o = _forward_args(q, k, cb_q, cb_k, v, alpha, beta, mem, N, topk, saved, y, out,
+                                            None)
+    sb = saved.numel() * 4 if saved is not None else 0
+    rc = lib().sdm_forward_noalloc(_ptr(q), _ptr(k), _dtype_code(q), _ptr(cb_q), _ptr(cb_k), dk, topk, _ptr(v),
+                                   _ptr(alpha), _ptr(beta), _dtype_code(v), _ptr(mem), B, H, T, dv, N,
+                                   _ptr(o["r_idx"]), _ptr(o["r_val"]), _ptr(o["w_idx"]), _ptr(o["w_val"]),
+                                   _ptr(o["y"]), _ptr(saved), sb, _stream(dev))
+    _check("sdm_forward_noalloc", rc)
     return o
 
 

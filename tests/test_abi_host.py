@@ -227,3 +227,17 @@ def test_forward_validation():
         assert fw(**kw) == code, kw
         assert L.sdm_last_error()
     assert fw(T=0) == 0
+
+
+def test_noalloc_refuses_sizes_past_its_array_on_the_host():
+    """sdm_forward_noalloc's size check comes before any device call (CPU only)."""
+    cap = L.sdm_forward_noalloc_max_bytes()
+    assert cap == 64 << 20
+    B, H, T, k = 16, 16, 100000, 32
+    assert L.sdm_scan_fwd_workspace_bytes(B, H, T, k, k) > cap
+    rc = L.sdm_forward_noalloc(A, A, 1, B_, B_, 128, k, A, A, A, 1, A, B, H, T, 128, 65536,
+                               A, A, A, A, A, None, 0, None)
+    assert rc == -2 and b"scratch" in L.sdm_last_error()
+    # an empty call needs nothing and returns at once
+    assert L.sdm_forward_noalloc(A, A, 1, B_, B_, 128, k, A, A, A, 1, A, B, H, 0, 128, 65536,
+                                 A, A, A, A, A, None, 0, None) == 0
