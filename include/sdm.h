@@ -290,6 +290,106 @@ int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k,
 size_t sdm_scan_bwd_workspace_bytes(int B, int H, int T, int W, int R, int d_v);
 
 /* ------------------------------------------------------------------------
+ * The steps either side of the recurrence.
+ *
+ * sdm_gates — the gate producers of Sec. 3.1 step 2, per head and token:
+ *   alpha = exp(-A[h] softplus(a + b_dt[h]))   (forget gate)
+ *   beta  = sigma(b)                           (input gate)
+ * from the pre-activations a = W_a x and b = W_b x, which the caller's input
+ * projection GEMM produces.  A is the learnable decay (Sec. 4 initialises it
+ * in [0, 16]), b_dt the time-step bias (inverse softplus of [0.001, 0.1]).
+ *   a_pre, b_pre  [B, H, T] in dtype;  A, b_dt [H] fp32;
+ *   alpha, beta   out [B, H, T] fp32.
+ * sdm_gates_bwd — its reverse mode: with z = a + b_dt,
+ *   da = dalpha (-A alpha sigma(z)),  db = dbeta beta (1 - beta),
+ *   dA[h] = sum over (b, t) of dalpha (-softplus(z) alpha),  db_dt[h] = sum of da,
+ * the sums over a head's tokens taken in a fixed order (reproducible).
+ *   dalpha, dbeta [B, H, T] fp32;  da, db out [B, H, T];  dA, db_dt out [H].
+ * ---------------------------------------------------------------------- */
+int sdm_gates(const void* a_pre, const void* b_pre, int dtype, const float* A, const float* b_dt,
+              int B, int H, int T, float* alpha, float* beta, void* stream);
+int sdm_gates_bwd(const void* a_pre, const void* b_pre, int dtype, const float* A, const float* b_dt,
+                  const float* dalpha, const float* dbeta, int B, int H, int T,
+                  float* da, float* db, float* dA, float* db_dt, void* stream);
+
+/* ------------------------------------------------------------------------
+ * sdm_norm_gate — the output epilogue of Sec. 3.1 step 4 ("Norm, Gating, and
+ * Head Mixing") and Fig. 2's g (.) Norm(y): per (b, h, t) row of d_v values
+ *   rstd = 1 / sqrt(mean_c y[c]^2 + eps),  o[c] = y[c] rstd gamma[c] phi(g[c]),
+ * phi = identity (act = 0, the element-wise gate as the text states it) or
+ * SiLU g sigma(g) (act = 1).  W_o, which mixes the heads afterwards, is a
+ * plain GEMM outside this library.
+ *   y      [B, H, T, d_v] fp32 (the read of Eq. sdm-read);
+ *   g      [B, H, T, d_v] in g_dtype: the output gate W_g x;
+ *   gamma  [d_v] fp32 norm scale shared by the heads, or NULL (ones);
+ *   o      out [B, H, T, d_v] fp32;  rstd  optional out [B, H, T] fp32.
+ *   d_v % 4 == 0, d_v <= 4096, eps >= 0.
+ * sdm_norm_gate_bwd — its reverse mode, with n = y rstd:
+ *   dg = dout gamma n phi'(g);  dn = dout phi(g) gamma;
+ *   dy = rstd (dn - n mean_c(dn n));  dgamma = sum over rows of dout phi(g) n
+ * (dgamma summed per workgroup, then across workgroups in a fixed order;
+ * NULL skips it).  Workspace: sdm_norm_gate_bwd_workspace_bytes(), 256-B
+ * aligned.
+ * ---------------------------------------------------------------------- */
+int sdm_norm_gate(const float* y, const void* g, int g_dtype, const float* gamma, float eps, int act,
+                  int B, int H, int T, int d_v, float* o, float* rstd, void* stream);
+size_t sdm_norm_gate_bwd_workspace_bytes(int B, int H, int T, int d_v);
+int sdm_norm_gate_bwd(const float* y, const void* g, int g_dtype, const float* gamma, float eps, int act,
+                      const float* dout, int B, int H, int T, int d_v,
+                      float* dy, float* dg, float* dgamma, void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * sdm_layer_fwd — the layer from its projections to the input of W_o
+ * (Sec. 3.1 steps 1-4): addressing of q (top-R) and k (top-W), the gates
+ * formed from their pre-activations inside the scan's per-token records (no
+ * alpha / beta arrays), the recurrence, and the norm-gate epilogue of each
+ * pipeline stage right after that stage's scan.  Pipelined as sdm_forward
+ * (addressing of the next stage on the library's second stream).
+ *   q, k, cb_q, cb_k, x_dtype, d_k, N, chunk: as for sdm_forward; W, R the
+ *     write and read list lengths (may differ).
+ *   v, a_pre, b_pre, g    [B, H, T, d_v] / [B, H, T] / [B, H, T] /
+ *                         [B, H, T, d_v] in in_dtype.
+ *   A, b_dt, gamma, eps, act: as for sdm_gates / sdm_norm_gate.
+ *   mem, saved, saved_bytes: as for sdm_scan_fwd (saved holds W rows per token).
+ *   r_idx, r_val [B,H,T,R], w_idx, w_val [B,H,T,W]: out, as sdm_address.
+ *   y  out [B, H, T, d_v] fp32 (kept for the backward);  o  out, as sdm_norm_gate;
+ *   rstd optional out.
+ *   workspace  at least sdm_scan_fwd_workspace_bytes(B, H, T, W, R) bytes.
+ * A single token (T = 1, no undo log, W = R) takes the one-launch step of
+ * sdm_forward, then the epilogue.
+ * ---------------------------------------------------------------------- */
+int sdm_layer_fwd(const void* q, const void* k, int x_dtype, const void* cb_q, const void* cb_k, int d_k,
+                  int W, int R, const void* v, const void* a_pre, const void* b_pre, const void* g, int in_dtype,
+                  const float* A, const float* b_dt, const float* gamma, float eps, int act,
+                  float* mem, int B, int H, int T, int d_v, int64_t N,
+                  int32_t* r_idx, float* r_val, int32_t* w_idx, float* w_val,
+                  float* y, float* o, float* rstd, float* saved, size_t saved_bytes, int chunk,
+                  void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * sdm_layer_bwd — reverse mode of sdm_layer_fwd: the epilogue's backward over
+ * the whole sequence (dy, dg, dgamma), then sdm_scan_bwd's path with the gates
+ * formed from the pre-activations in its records (dq, dk, dv, dM0; M_T -> M_0
+ * bit-exact), then the gates' backward (da, db, dA, db_dt).
+ *   Inputs as given to sdm_layer_fwd (slot lists and weights as it returned
+ *   them), y as it returned it, dout [B, H, T, d_v] fp32 the gradient of o,
+ *   dmem_T optional (NULL = 0), chunk as for sdm_scan_bwd.
+ *   dq, dk optional; dv; da, db [B,H,T]; dA, db_dt [H]; dg [B,H,T,d_v];
+ *   dgamma [d_v] optional; dmem0 [B,H,N,d_v].
+ *   workspace  at least sdm_layer_bwd_workspace_bytes() bytes, 256-B aligned.
+ * ---------------------------------------------------------------------- */
+size_t sdm_layer_bwd_workspace_bytes(int B, int H, int T, int W, int R, int d_v);
+int sdm_layer_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k,
+                  const int32_t* w_idx, const float* w_val, int W,
+                  const int32_t* r_idx, const float* r_val, int R,
+                  const void* v, const void* a_pre, const void* b_pre, const void* g, int in_dtype,
+                  const float* A, const float* b_dt, const float* gamma, float eps, int act,
+                  float* mem, const float* saved, size_t saved_bytes, const float* y, const float* dout,
+                  const float* dmem_T, int chunk, int B, int H, int T, int d_v, int64_t N,
+                  float* dq, float* dk, float* dv, float* da, float* db, float* dA, float* db_dt,
+                  float* dg, float* dgamma, float* dmem0, void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * sdm_mem_init — initial memory per call.  The learned initial state M_0 of
  * Sec. 3.1 ("Learned Initial State") is one [H, N, d_v] parameter shared by
  * all sequences; every sequence starts from its own copy:
@@ -345,7 +445,8 @@ int sdm_set_scan_line_io(int on);
 enum sdm_kernel {
     SDM_K_ADDRESS = 0, SDM_K_FWD_PREP = 1, SDM_K_FWD_SCAN = 2, SDM_K_BWD_PREP = 3,
     SDM_K_BWD_SCAN = 4, SDM_K_BWD_REDUCE = 5, SDM_K_ADDRESS_BWD = 6, SDM_K_MEM_INIT = 7,
-    SDM_K_DECODE = 8, SDM_K_CHUNK_COEF = 9, SDM_K_CHUNK_SCAN = 10, SDM_K_COUNT = 11
+    SDM_K_DECODE = 8, SDM_K_CHUNK_COEF = 9, SDM_K_CHUNK_SCAN = 10, SDM_K_NORM_GATE = 11, SDM_K_GATES = 12,
+    SDM_K_COUNT = 13
 };
 int sdm_profile_enable(int on);
 /* Which kernel kinds the events bracket while profiling is enabled: bit k for

@@ -17,8 +17,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libsdm.so")
-SOURCES = ["address.hip", "scan_prep.hip", "scan_fwd.hip", "scan_bwd.hip", "scan_chunk.hip", "noalloc.hip",
-           "api.cpp"]
+SOURCES = ["address.hip", "scan_prep.hip", "scan_fwd.hip", "scan_bwd.hip", "scan_chunk.hip", "gates.hip",
+           "noalloc.hip", "api.cpp"]
 ARCH = os.environ.get("SDM_OFFLOAD_ARCH", "gfx950")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

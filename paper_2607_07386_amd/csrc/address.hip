@@ -1043,7 +1043,8 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void decode_kernel(
     int H, int dk, int s, int topk, const void* __restrict__ v, const void* __restrict__ alpha,
     const void* __restrict__ beta, int in_dtype, float* __restrict__ mem, int64_t N, int dv,
     int32_t* __restrict__ r_idx, float* __restrict__ r_val, int32_t* __restrict__ w_idx,
-    float* __restrict__ w_val, float* __restrict__ y, unsigned int* __restrict__ flags) {
+    float* __restrict__ w_val, float* __restrict__ y, unsigned int* __restrict__ flags,
+    const float* __restrict__ gA, const float* __restrict__ gbdt) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int stream = blockIdx.x;
     if (stream == 0 && threadIdx.x < 4) flags[threadIdx.x] = 0u;   // the call's device-error words
@@ -1108,7 +1109,8 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void decode_kernel(
             link[j] = lw[lo] == rslot[j] ? lo : -1;
         }
     }
-    const float al = load_scalar(alpha, in_dtype, stream), be = load_scalar(beta, in_dtype, stream);
+    float al = load_scalar(alpha, in_dtype, stream), be = load_scalar(beta, in_dtype, stream);
+    sdm_gates_of(gA, gbdt, stream % H, al, be);
     float* tab = mem + (size_t)stream * N * dv;
 
     for (int c0 = 0; c0 < dv; c0 += DEC_COLS) {
@@ -1387,7 +1389,8 @@ template <typename XT, int MODE>
 hipError_t launch_decode_m(const void* q, const void* k, const void* cb_q, const void* cb_k, int B, int H,
                            int dk, int s, int topk, const void* v, const void* alpha, const void* beta,
                            int in_dtype, float* mem, int64_t N, int dv, int32_t* r_idx, float* r_val,
-                           int32_t* w_idx, float* w_val, float* y, unsigned int* flags, hipStream_t st) {
+                           int32_t* w_idx, float* w_val, float* y, unsigned int* flags, hipStream_t st,
+                           const float* gA, const float* gbdt) {
     const int E = (s + SDM_WAVE - 1) / SDM_WAVE;
     const XT* qp = static_cast<const XT*>(q);
     const XT* kp = static_cast<const XT*>(k);
@@ -1401,7 +1404,8 @@ hipError_t launch_decode_m(const void* q, const void* k, const void* cb_q, const
                                            (int)sm);                                                      \
         if (e != hipSuccess) return e;                                                                    \
         hipLaunchKernelGGL(kfn, dim3(B * H), dim3(AWAVES * SDM_WAVE), sm, st, qp, kp, cq, ck, H, dk, s,   \
-                           topk, v, alpha, beta, in_dtype, mem, N, dv, r_idx, r_val, w_idx, w_val, y, flags); \
+                           topk, v, alpha, beta, in_dtype, mem, N, dv, r_idx, r_val, w_idx, w_val, y, flags, \
+                           gA, gbdt);                                                                     \
         return hipGetLastError();                                                                         \
     }
     if (topk > MAXK) {   // topk <= sqrt(N), so E >= 2
@@ -1422,21 +1426,22 @@ hipError_t launch_decode_m(const void* q, const void* k, const void* cb_q, const
 hipError_t sdm_launch_decode(const void* q, const void* k, int x_dtype, const void* cb_q, const void* cb_k, int B,
                              int H, int dk, int s, int topk, const void* v, const void* alpha, const void* beta,
                              int in_dtype, float* mem, int64_t N, int dv, int32_t* r_idx, float* r_val,
-                             int32_t* w_idx, float* w_val, float* y, unsigned int* flags, hipStream_t st) {
+                             int32_t* w_idx, float* w_val, float* y, unsigned int* flags, hipStream_t st,
+                             const float* gA, const float* gbdt) {
     if (B * H == 0) return hipSuccess;
     if (x_dtype == SDM_DT_BF16) {
         if (!cb_q)
             return launch_decode_m<bf16_t, 0>(q, k, cb_q, cb_k, B, H, dk, s, topk, v, alpha, beta, in_dtype, mem,
-                                              N, dv, r_idx, r_val, w_idx, w_val, y, flags, st);
+                                              N, dv, r_idx, r_val, w_idx, w_val, y, flags, st, gA, gbdt);
         if ((dk / 2) % 8 == 0)
             return launch_decode_m<bf16_t, 2>(q, k, cb_q, cb_k, B, H, dk, s, topk, v, alpha, beta, in_dtype, mem,
-                                              N, dv, r_idx, r_val, w_idx, w_val, y, flags, st);
+                                              N, dv, r_idx, r_val, w_idx, w_val, y, flags, st, gA, gbdt);
         return launch_decode_m<bf16_t, 1>(q, k, cb_q, cb_k, B, H, dk, s, topk, v, alpha, beta, in_dtype, mem, N,
-                                          dv, r_idx, r_val, w_idx, w_val, y, flags, st);
+                                          dv, r_idx, r_val, w_idx, w_val, y, flags, st, gA, gbdt);
     }
     if (!cb_q)
         return launch_decode_m<float, 0>(q, k, cb_q, cb_k, B, H, dk, s, topk, v, alpha, beta, in_dtype, mem, N,
-                                         dv, r_idx, r_val, w_idx, w_val, y, flags, st);
+                                         dv, r_idx, r_val, w_idx, w_val, y, flags, st, gA, gbdt);
     return launch_decode_m<float, 1>(q, k, cb_q, cb_k, B, H, dk, s, topk, v, alpha, beta, in_dtype, mem, N, dv,
-                                     r_idx, r_val, w_idx, w_val, y, flags, st);
+                                     r_idx, r_val, w_idx, w_val, y, flags, st, gA, gbdt);
 }

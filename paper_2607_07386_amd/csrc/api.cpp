@@ -486,34 +486,73 @@ int sdm_scan_fwd_chunked(const int32_t* w_idx, const float* w_val, int W, const 
 
 // ---- fused forward: addressing pipelined with the scan over chunks of tokens ----
 
+namespace {
+// Validation of the optional steps either side of the scan (gates from
+// pre-activations, the norm-gate epilogue).
+int check_extras(const SdmFwdExtras* ex, int in_dtype, bool tok) {
+    if (!ex) return SDM_OK;
+    if (ex->gate_A || ex->gate_bdt) {
+        if (!ex->gate_A || !ex->gate_bdt) return fail(SDM_ERR_INVALID_ARG, "A and b_dt go together");
+        if (!aligned(ex->gate_A, 4) || !aligned(ex->gate_bdt, 4))
+            return fail(SDM_ERR_INVALID_ARG, "misaligned A or b_dt");
+    }
+    if (ex->o) {
+        if (ex->act != 0 && ex->act != 1) return fail(SDM_ERR_INVALID_ARG, "act must be 0 (identity) or 1 (SiLU)");
+        if (!(ex->eps >= 0.f) || !std::isfinite(ex->eps)) return fail(SDM_ERR_INVALID_ARG, "eps must be finite and >= 0");
+        if (tok && !ex->g) return fail(SDM_ERR_INVALID_ARG, "null output gate g");
+        if (!aligned(ex->o, 16) || !aligned(ex->g, 16) || (ex->gamma && !aligned(ex->gamma, 16)) ||
+            (ex->rstd && !aligned(ex->rstd, 4)))
+            return fail(SDM_ERR_INVALID_ARG, "misaligned epilogue pointer (16-byte alignment required)");
+    }
+    (void)in_dtype;
+    return SDM_OK;
+}
+}  // namespace
+
 int sdm_forward_impl(const void* q, const void* k, int x_dtype, const void* cb_q, const void* cb_k, int d_k,
-                     int topk, const void* v, const void* alpha, const void* beta, int in_dtype, float* mem,
+                     int W, int R, const void* v, const void* alpha, const void* beta, int in_dtype, float* mem,
                      int B, int H, int T, int d_v, int64_t N, int32_t* r_idx, float* r_val, int32_t* w_idx,
                      float* w_val, float* y, float* saved, size_t saved_bytes, int chunk, void* workspace,
-                     size_t ws_bytes, void* stream, bool pipelined) {
+                     size_t ws_bytes, void* stream, bool pipelined, const SdmFwdExtras* ex) {
     g_err[0] = 0;
     int s = 0;
-    int rc = check_address(q, x_dtype, cb_q, B, H, T, d_k, N, topk, r_idx, r_val, nullptr, &s);
+    int rc = check_address(q, x_dtype, cb_q, B, H, T, d_k, N, R, r_idx, r_val, nullptr, &s);
     if (rc != SDM_OK) return rc;
-    rc = check_address(k, x_dtype, cb_k, B, H, T, d_k, N, topk, w_idx, w_val, nullptr, &s);
+    rc = check_address(k, x_dtype, cb_k, B, H, T, d_k, N, W, w_idx, w_val, nullptr, &s);
     if (rc != SDM_OK) return rc;
-    rc = check_scan_common(w_idx, w_val, topk, r_idx, r_val, topk, v, alpha, beta, in_dtype, mem, B, H,
+    rc = check_scan_common(w_idx, w_val, W, r_idx, r_val, R, v, alpha, beta, in_dtype, mem, B, H,
                            T, d_v, N);
     if (rc != SDM_OK) return rc;
     if (chunk < 0) return fail(SDM_ERR_INVALID_ARG, "chunk must be >= 0");
+    if ((rc = check_extras(ex, in_dtype, (int64_t)B * H * T > 0)) != SDM_OK) return rc;
     if ((int64_t)B * H * T == 0) return SDM_OK;
-    rc = check_scan_fwd_rest(topk, topk, in_dtype, B, H, T, d_v, y, saved, saved_bytes, workspace,
+    rc = check_scan_fwd_rest(W, R, in_dtype, B, H, T, d_v, y, saved, saved_bytes, workspace,
                              ws_bytes);
     if (rc != SDM_OK) return rc;
 
     hipStream_t st = (hipStream_t)stream;
-    // one token without an undo log, both sides in the same addressing mode:
-    // addressing and the scan step in one launch
-    if (T == 1 && !saved && (cb_q == nullptr) == (cb_k == nullptr)) {
-        SdmProfScope ps(SDM_K_DECODE, st);
-        hipError_t e = sdm_launch_decode(q, k, x_dtype, cb_q, cb_k, B, H, d_k, s, topk, v, alpha, beta, in_dtype,
-                                         mem, N, d_v, r_idx, r_val, w_idx, w_val, y,
-                                         static_cast<unsigned int*>(workspace), st);
+    const float* gA = ex ? ex->gate_A : nullptr;
+    const float* gbdt = ex ? ex->gate_bdt : nullptr;
+    const bool epi = ex && ex->o;
+    const int S = B * H;
+    // the epilogue of tokens [tb, te), after their scan on the same stream
+    auto epilogue = [&](int tb, int te, hipStream_t sx) -> hipError_t {
+        if (!epi) return hipSuccess;
+        SdmProfScope ps(SDM_K_NORM_GATE, sx);
+        return sdm_launch_norm_gate(y, ex->g, in_dtype, ex->gamma, ex->eps, ex->act, S, T, tb, te - tb, d_v, ex->o,
+                                    ex->rstd, sx);
+    };
+    // one token without an undo log, both sides in the same addressing mode and
+    // W = R: addressing and the scan step in one launch
+    if (T == 1 && !saved && W == R && (cb_q == nullptr) == (cb_k == nullptr)) {
+        hipError_t e;
+        {
+            SdmProfScope ps(SDM_K_DECODE, st);
+            e = sdm_launch_decode(q, k, x_dtype, cb_q, cb_k, B, H, d_k, s, W, v, alpha, beta, in_dtype, mem, N,
+                                  d_v, r_idx, r_val, w_idx, w_val, y, static_cast<unsigned int*>(workspace), st,
+                                  gA, gbdt);
+        }
+        if (e == hipSuccess) e = epilogue(0, 1, st);
         return e == hipSuccess ? SDM_OK : hip_fail(e, "sdm_forward single-token launch");
     }
 
@@ -534,20 +573,21 @@ int sdm_forward_impl(const void* q, const void* k, int x_dtype, const void* cb_q
     ScanFwdArgs a;
     a.w_idx = w_idx; a.w_val = w_val; a.r_idx = r_idx; a.r_val = r_val;
     a.v = v; a.alpha = alpha; a.beta = beta; a.in_dtype = in_dtype;
-    a.mem = mem; a.B = B; a.H = H; a.T = T; a.dv = d_v; a.W = topk; a.R = topk; a.N = N;
+    a.mem = mem; a.B = B; a.H = H; a.T = T; a.dv = d_v; a.W = W; a.R = R; a.N = N;
     a.y = y; a.saved = saved; a.ws = static_cast<unsigned char*>(workspace);
+    a.gate_A = gA; a.gate_bdt = gbdt;
 
     auto stage_front = [&](int tb, int te, hipStream_t sx) -> hipError_t {
         hipError_t ee;
         {
             SdmProfScope ps(SDM_K_ADDRESS, sx);
-            ee = sdm_launch_address(q, x_dtype, cb_q, B, H, T, tb, te - tb, d_k, s, topk, r_idx, r_val,
+            ee = sdm_launch_address(q, x_dtype, cb_q, B, H, T, tb, te - tb, d_k, s, R, r_idx, r_val,
                                     nullptr, sx);
         }
         if (ee != hipSuccess) return ee;
         {
             SdmProfScope ps(SDM_K_ADDRESS, sx);
-            ee = sdm_launch_address(k, x_dtype, cb_k, B, H, T, tb, te - tb, d_k, s, topk, w_idx, w_val,
+            ee = sdm_launch_address(k, x_dtype, cb_k, B, H, T, tb, te - tb, d_k, s, W, w_idx, w_val,
                                     nullptr, sx);
         }
         if (ee != hipSuccess) return ee;
@@ -564,6 +604,7 @@ int sdm_forward_impl(const void* q, const void* k, int x_dtype, const void* cb_q
             a.te = T;
             e = sdm_launch_fwd_scan_range(a, st);
         }
+        if (e == hipSuccess) e = epilogue(0, T, st);
         return e == hipSuccess ? SDM_OK : hip_fail(e, "sdm_forward launch");
     }
 
@@ -585,6 +626,7 @@ int sdm_forward_impl(const void* q, const void* k, int x_dtype, const void* cb_q
         a.tb = tb;
         a.te = te;
         if ((e = sdm_launch_fwd_scan_range(a, st)) != hipSuccess) return hip_fail(e, "sdm_forward launch");
+        if ((e = epilogue(tb, te, st)) != hipSuccess) return hip_fail(e, "sdm_forward epilogue launch");
     }
     return SDM_OK;
 }
@@ -598,19 +640,24 @@ int sdm_forward(const void* q, const void* k, int x_dtype, const void* cb_q, con
                 int B, int H, int T, int d_v, int64_t N, int32_t* r_idx, float* r_val, int32_t* w_idx,
                 float* w_val, float* y, float* saved, size_t saved_bytes, int chunk, void* workspace,
                 size_t ws_bytes, void* stream) {
-    return sdm_forward_impl(q, k, x_dtype, cb_q, cb_k, d_k, topk, v, alpha, beta, in_dtype, mem, B, H, T, d_v,
-                            N, r_idx, r_val, w_idx, w_val, y, saved, saved_bytes, chunk, workspace, ws_bytes,
-                            stream, true);
+    return sdm_forward_impl(q, k, x_dtype, cb_q, cb_k, d_k, topk, topk, v, alpha, beta, in_dtype, mem, B, H, T,
+                            d_v, N, r_idx, r_val, w_idx, w_val, y, saved, saved_bytes, chunk, workspace, ws_bytes,
+                            stream, true, nullptr);
 }
 
-int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, const int32_t* w_idx,
-                 const float* w_val, int W, const int32_t* r_idx, const float* r_val, int R,
-                 const void* v, const void* alpha, const void* beta, int in_dtype, float* mem,
-                 const float* saved, size_t saved_bytes, const float* dy, const float* dmem_T,
-                 int chunk, int B, int H, int T, int d_v, int64_t N, float* dq, float* dk,
-                 float* dv, float* dalpha, float* dbeta, float* dmem0, float* dw_val,
-                 float* dr_val, void* workspace, size_t ws_bytes, void* stream) {
-    g_err[0] = 0;
+}  // extern "C"
+
+namespace {
+// The body of sdm_scan_bwd; gA, gbdt set: alpha and beta hold the gates'
+// pre-activations and the records take the gates formed from them.
+int scan_bwd_impl(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, const int32_t* w_idx,
+                  const float* w_val, int W, const int32_t* r_idx, const float* r_val, int R,
+                  const void* v, const void* alpha, const void* beta, int in_dtype, float* mem,
+                  const float* saved, size_t saved_bytes, const float* dy, const float* dmem_T,
+                  int chunk, int B, int H, int T, int d_v, int64_t N, float* dq, float* dk,
+                  float* dv, float* dalpha, float* dbeta, float* dmem0, float* dw_val,
+                  float* dr_val, void* workspace, size_t ws_bytes, void* stream, const float* gA,
+                  const float* gbdt) {
     int rc = check_scan_common(w_idx, w_val, W, r_idx, r_val, R, v, alpha, beta, in_dtype, mem, B,
                                H, T, d_v, N);
     if (rc != SDM_OK) return rc;
@@ -669,6 +716,8 @@ int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, cons
     a.dw_val = dw_val ? dw_val : spare;
     a.dr_val = dr_val ? dr_val : spare + ST * W;
     a.ws = ws;
+    a.gate_A = gA;
+    a.gate_bdt = gbdt;
     a.line = sdm_bwd_line_io(a) ? 1 : 0;   // one decision for every stage and the reduce
 
     // Stages of tokens from the end of the sequence down: a short first stage,
@@ -767,6 +816,232 @@ int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, cons
     if ((e = hipEventRecord(ev_end, side)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd record");
     if ((e = hipStreamWaitEvent(st, ev_end, 0)) != hipSuccess) return hip_fail(e, "sdm_scan_bwd wait");
     return SDM_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Regions of sdm_layer_bwd's workspace: the scan's, dy, dalpha and dbeta, the
+// epilogue's dgamma partial sums.
+struct LayerBwdWs {
+    size_t scan, dy, dab, part, total;
+};
+LayerBwdWs layer_bwd_ws(int B, int H, int T, int W, int R, int d_v) {
+    LayerBwdWs w;
+    const size_t ST = (size_t)B * H * T;
+    w.scan = 0;
+    w.dy = align256(sdm_bwd_ws_bytes(B, H, T, W, R, d_v));
+    w.dab = w.dy + align256(ST * d_v * sizeof(float));
+    w.part = w.dab + align256(2 * ST * sizeof(float));
+    w.total = w.part + align256(sdm_norm_gate_bwd_ws((int64_t)ST, d_v));
+    return w;
+}
+
+int check_gate_args(const void* a_pre, const void* b_pre, int dtype, const float* A, const float* b_dt, int B,
+                    int H, int T) {
+    if (B < 0 || H < 0 || T < 0) return fail(SDM_ERR_INVALID_ARG, "B, H, T must be >= 0");
+    if ((int64_t)B * H > kMaxStreams) return fail(SDM_ERR_UNSUPPORTED, "B*H must be <= %d", kMaxStreams);
+    if (!valid_dtype(dtype)) return fail(SDM_ERR_INVALID_ARG, "dtype must be SDM_F32 or SDM_BF16");
+    if (H > 0 && (!A || !b_dt)) return fail(SDM_ERR_INVALID_ARG, "null A or b_dt");
+    if ((int64_t)B * H * T > 0 && (!a_pre || !b_pre)) return fail(SDM_ERR_INVALID_ARG, "null pre-activation");
+    if (!aligned(A, 4) || !aligned(b_dt, 4) || !aligned(a_pre, 4) || !aligned(b_pre, 4))
+        return fail(SDM_ERR_INVALID_ARG, "misaligned pointer");
+    return SDM_OK;
+}
+
+int check_norm_gate_args(const float* y, const void* g, int g_dtype, const float* gamma, float eps, int act, int B,
+                         int H, int T, int d_v) {
+    if (B < 0 || H < 0 || T < 0) return fail(SDM_ERR_INVALID_ARG, "B, H, T must be >= 0");
+    if (d_v < 4 || d_v % 4) return fail(SDM_ERR_INVALID_ARG, "d_v must be a positive multiple of 4");
+    if (d_v > 4096) return fail(SDM_ERR_UNSUPPORTED, "d_v must be <= 4096");
+    if (!valid_dtype(g_dtype)) return fail(SDM_ERR_INVALID_ARG, "g_dtype must be SDM_F32 or SDM_BF16");
+    if (act != 0 && act != 1) return fail(SDM_ERR_INVALID_ARG, "act must be 0 (identity) or 1 (SiLU)");
+    if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(SDM_ERR_INVALID_ARG, "eps must be finite and >= 0");
+    if ((int64_t)B * H * T > 0 && (!y || !g)) return fail(SDM_ERR_INVALID_ARG, "null y or g");
+    if (!aligned(y, 16) || !aligned(g, 16) || (gamma && !aligned(gamma, 16)))
+        return fail(SDM_ERR_INVALID_ARG, "misaligned pointer (16-byte alignment required)");
+    return SDM_OK;
+}
+}  // namespace
+
+extern "C" {
+
+int sdm_scan_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, const int32_t* w_idx,
+                 const float* w_val, int W, const int32_t* r_idx, const float* r_val, int R,
+                 const void* v, const void* alpha, const void* beta, int in_dtype, float* mem,
+                 const float* saved, size_t saved_bytes, const float* dy, const float* dmem_T,
+                 int chunk, int B, int H, int T, int d_v, int64_t N, float* dq, float* dk,
+                 float* dv, float* dalpha, float* dbeta, float* dmem0, float* dw_val,
+                 float* dr_val, void* workspace, size_t ws_bytes, void* stream) {
+    return scan_bwd_impl(cb_q, cb_k, cb_dtype, d_k, w_idx, w_val, W, r_idx, r_val, R, v, alpha, beta, in_dtype, mem,
+                         saved, saved_bytes, dy, dmem_T, chunk, B, H, T, d_v, N, dq, dk, dv, dalpha, dbeta, dmem0,
+                         dw_val, dr_val, workspace, ws_bytes, stream, nullptr, nullptr);
+}
+
+// ---- the steps either side of the recurrence (Sec. 3.1 steps 2 and 4) ----
+
+int sdm_gates(const void* a_pre, const void* b_pre, int dtype, const float* A, const float* b_dt, int B, int H,
+              int T, float* alpha, float* beta, void* stream) {
+    g_err[0] = 0;
+    int rc = check_gate_args(a_pre, b_pre, dtype, A, b_dt, B, H, T);
+    if (rc != SDM_OK) return rc;
+    if ((int64_t)B * H * T == 0) return SDM_OK;
+    if (!alpha || !beta || !aligned(alpha, 4) || !aligned(beta, 4))
+        return fail(SDM_ERR_INVALID_ARG, "null or misaligned alpha / beta output");
+    hipError_t e;
+    {
+        SdmProfScope ps(SDM_K_GATES, (hipStream_t)stream);
+        e = sdm_launch_gates(a_pre, b_pre, dtype, A, b_dt, B, H, T, alpha, beta, (hipStream_t)stream);
+    }
+    return e == hipSuccess ? SDM_OK : hip_fail(e, "sdm_gates launch");
+}
+
+int sdm_gates_bwd(const void* a_pre, const void* b_pre, int dtype, const float* A, const float* b_dt,
+                  const float* dalpha, const float* dbeta, int B, int H, int T, float* da, float* db, float* dA,
+                  float* db_dt, void* stream) {
+    g_err[0] = 0;
+    int rc = check_gate_args(a_pre, b_pre, dtype, A, b_dt, B, H, T);
+    if (rc != SDM_OK) return rc;
+    if (H == 0) return SDM_OK;
+    if (!dA || !db_dt || !aligned(dA, 4) || !aligned(db_dt, 4))
+        return fail(SDM_ERR_INVALID_ARG, "null or misaligned dA / db_dt");
+    if ((int64_t)B * T > 0 && (!dalpha || !dbeta || !da || !db || !aligned(dalpha, 4) || !aligned(dbeta, 4) ||
+                               !aligned(da, 4) || !aligned(db, 4)))
+        return fail(SDM_ERR_INVALID_ARG, "null or misaligned gradient pointer");
+    hipError_t e;
+    {
+        SdmProfScope ps(SDM_K_GATES, (hipStream_t)stream);
+        e = sdm_launch_gates_bwd(a_pre, b_pre, dtype, A, b_dt, dalpha, dbeta, B, H, T, da, db, dA, db_dt,
+                                 (hipStream_t)stream);
+    }
+    return e == hipSuccess ? SDM_OK : hip_fail(e, "sdm_gates_bwd launch");
+}
+
+int sdm_norm_gate(const float* y, const void* g, int g_dtype, const float* gamma, float eps, int act, int B, int H,
+                  int T, int d_v, float* o, float* rstd, void* stream) {
+    g_err[0] = 0;
+    int rc = check_norm_gate_args(y, g, g_dtype, gamma, eps, act, B, H, T, d_v);
+    if (rc != SDM_OK) return rc;
+    if ((int64_t)B * H * T == 0) return SDM_OK;
+    if (!o || !aligned(o, 16) || (rstd && !aligned(rstd, 4)))
+        return fail(SDM_ERR_INVALID_ARG, "null or misaligned output");
+    hipError_t e;
+    {
+        SdmProfScope ps(SDM_K_NORM_GATE, (hipStream_t)stream);
+        e = sdm_launch_norm_gate(y, g, g_dtype, gamma, eps, act, (int64_t)B * H, T, 0, T, d_v, o, rstd,
+                                 (hipStream_t)stream);
+    }
+    return e == hipSuccess ? SDM_OK : hip_fail(e, "sdm_norm_gate launch");
+}
+
+size_t sdm_norm_gate_bwd_workspace_bytes(int B, int H, int T, int d_v) {
+    if (B < 0 || H < 0 || T < 0 || d_v < 4) return 0;
+    return align256(sdm_norm_gate_bwd_ws((int64_t)B * H * T, d_v));
+}
+
+int sdm_norm_gate_bwd(const float* y, const void* g, int g_dtype, const float* gamma, float eps, int act,
+                      const float* dout, int B, int H, int T, int d_v, float* dy, float* dg, float* dgamma,
+                      void* workspace, size_t ws_bytes, void* stream) {
+    g_err[0] = 0;
+    int rc = check_norm_gate_args(y, g, g_dtype, gamma, eps, act, B, H, T, d_v);
+    if (rc != SDM_OK) return rc;
+    const bool tok = (int64_t)B * H * T > 0;
+    if (tok && (!dout || !dy || !dg)) return fail(SDM_ERR_INVALID_ARG, "null dout, dy or dg");
+    if (!aligned(dout, 16) || !aligned(dy, 16) || !aligned(dg, 16) || (dgamma && !aligned(dgamma, 4)))
+        return fail(SDM_ERR_INVALID_ARG, "misaligned pointer (16-byte alignment required)");
+    const size_t need = sdm_norm_gate_bwd_workspace_bytes(B, H, T, d_v);
+    if (!workspace || !aligned(workspace, 256))
+        return fail(SDM_ERR_INVALID_ARG, "workspace must be a 256-byte aligned pointer");
+    if (ws_bytes < need) return fail(SDM_ERR_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, need);
+    hipError_t e;
+    {
+        SdmProfScope ps(SDM_K_NORM_GATE, (hipStream_t)stream);
+        e = sdm_launch_norm_gate_bwd(y, g, g_dtype, gamma, eps, act, dout, (int64_t)B * H * T, d_v, dy, dg, dgamma,
+                                     static_cast<float*>(workspace), (hipStream_t)stream);
+    }
+    return e == hipSuccess ? SDM_OK : hip_fail(e, "sdm_norm_gate_bwd launch");
+}
+
+int sdm_layer_fwd(const void* q, const void* k, int x_dtype, const void* cb_q, const void* cb_k, int d_k, int W,
+                  int R, const void* v, const void* a_pre, const void* b_pre, const void* g, int in_dtype,
+                  const float* A, const float* b_dt, const float* gamma, float eps, int act, float* mem, int B,
+                  int H, int T, int d_v, int64_t N, int32_t* r_idx, float* r_val, int32_t* w_idx, float* w_val,
+                  float* y, float* o, float* rstd, float* saved, size_t saved_bytes, int chunk, void* workspace,
+                  size_t ws_bytes, void* stream) {
+    g_err[0] = 0;
+    int rc = check_gate_args(a_pre, b_pre, in_dtype, A, b_dt, B, H, T);
+    if (rc != SDM_OK) return rc;
+    rc = check_norm_gate_args(y, g, in_dtype, gamma, eps, act, B, H, T, d_v);
+    if (rc != SDM_OK) return rc;
+    if ((int64_t)B * H * T > 0 && !o) return fail(SDM_ERR_INVALID_ARG, "null output o");
+    SdmFwdExtras ex;
+    ex.gate_A = A;
+    ex.gate_bdt = b_dt;
+    ex.g = g;
+    ex.gamma = gamma;
+    ex.eps = eps;
+    ex.act = act;
+    ex.o = o;
+    ex.rstd = rstd;
+    return sdm_forward_impl(q, k, x_dtype, cb_q, cb_k, d_k, W, R, v, a_pre, b_pre, in_dtype, mem, B, H, T, d_v, N,
+                            r_idx, r_val, w_idx, w_val, y, saved, saved_bytes, chunk, workspace, ws_bytes, stream,
+                            true, &ex);
+}
+
+size_t sdm_layer_bwd_workspace_bytes(int B, int H, int T, int W, int R, int d_v) {
+    if (B < 0 || H < 0 || T < 0 || W < 1 || R < 1 || d_v < 4) return 0;
+    return layer_bwd_ws(B, H, T, W, R, d_v).total;
+}
+
+int sdm_layer_bwd(const void* cb_q, const void* cb_k, int cb_dtype, int d_k, const int32_t* w_idx,
+                  const float* w_val, int W, const int32_t* r_idx, const float* r_val, int R, const void* v,
+                  const void* a_pre, const void* b_pre, const void* g, int in_dtype, const float* A,
+                  const float* b_dt, const float* gamma, float eps, int act, float* mem, const float* saved,
+                  size_t saved_bytes, const float* y, const float* dout, const float* dmem_T, int chunk, int B,
+                  int H, int T, int d_v, int64_t N, float* dq, float* dk, float* dv, float* da, float* db,
+                  float* dA, float* db_dt, float* dg, float* dgamma, float* dmem0, void* workspace,
+                  size_t ws_bytes, void* stream) {
+    g_err[0] = 0;
+    int rc = check_gate_args(a_pre, b_pre, in_dtype, A, b_dt, B, H, T);
+    if (rc != SDM_OK) return rc;
+    rc = check_norm_gate_args(y, g, in_dtype, gamma, eps, act, B, H, T, d_v);
+    if (rc != SDM_OK) return rc;
+    rc = check_scan_common(w_idx, w_val, W, r_idx, r_val, R, v, a_pre, b_pre, in_dtype, mem, B, H, T, d_v, N);
+    if (rc != SDM_OK) return rc;
+    const bool tok = (int64_t)B * H * T > 0;
+    if (tok && (!dout || !da || !db || !dg)) return fail(SDM_ERR_INVALID_ARG, "null dout, da, db or dg");
+    if (H > 0 && (!dA || !db_dt)) return fail(SDM_ERR_INVALID_ARG, "null dA or db_dt");
+    if (!aligned(dout, 16) || !aligned(dg, 16) || !aligned(da, 4) || !aligned(db, 4) || !aligned(dA, 4) ||
+        !aligned(db_dt, 4) || (dgamma && !aligned(dgamma, 4)))
+        return fail(SDM_ERR_INVALID_ARG, "misaligned pointer");
+    const LayerBwdWs L = layer_bwd_ws(B, H, T, W, R, d_v);
+    if (!workspace || !aligned(workspace, 256))
+        return fail(SDM_ERR_INVALID_ARG, "workspace must be a 256-byte aligned pointer");
+    if (ws_bytes < L.total) return fail(SDM_ERR_WORKSPACE, "workspace too small: %zu < %zu", ws_bytes, L.total);
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    float* dy = reinterpret_cast<float*>(ws + L.dy);
+    float* dal = reinterpret_cast<float*>(ws + L.dab);
+    float* dbe = dal + (size_t)B * H * T;
+    float* part = reinterpret_cast<float*>(ws + L.part);
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e;
+    // 1. epilogue backward over the whole sequence: dy (the scan's upstream gradient), dg, dgamma
+    {
+        SdmProfScope ps(SDM_K_NORM_GATE, st);
+        e = sdm_launch_norm_gate_bwd(y, g, in_dtype, gamma, eps, act, dout, (int64_t)B * H * T, d_v, dy, dg, dgamma,
+                                     part, st);
+    }
+    if (e != hipSuccess) return hip_fail(e, "sdm_layer_bwd epilogue launch");
+    // 2. the recurrence's backward, its records taking the gates formed from the pre-activations
+    rc = scan_bwd_impl(cb_q, cb_k, cb_dtype, d_k, w_idx, w_val, W, r_idx, r_val, R, v, a_pre, b_pre, in_dtype, mem,
+                       saved, saved_bytes, dy, dmem_T, chunk, B, H, T, d_v, N, dq, dk, dv, dal, dbe, dmem0, nullptr,
+                       nullptr, ws, L.dy, stream, A, b_dt);
+    if (rc != SDM_OK) return rc;
+    // 3. the gates' backward: da, db and the per-head sums dA, db_dt
+    {
+        SdmProfScope ps(SDM_K_GATES, st);
+        e = sdm_launch_gates_bwd(a_pre, b_pre, in_dtype, A, b_dt, dal, dbe, B, H, T, da, db, dA, db_dt, st);
+    }
+    return e == hipSuccess ? SDM_OK : hip_fail(e, "sdm_layer_bwd gates launch");
 }
 
 int sdm_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int d_v, void* stream) {

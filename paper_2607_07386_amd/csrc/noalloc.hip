@@ -66,9 +66,9 @@ int sdm_forward_noalloc(const void* q, const void* k, int x_dtype, const void* c
         const int rc = scratch_ptr(&ws);
         if (rc != SDM_OK) return rc;
     }
-    return sdm_forward_impl(q, k, x_dtype, cb_q, cb_k, d_k, topk, v, alpha, beta, in_dtype, mem, B, H, T, d_v, N,
-                            r_idx, r_val, w_idx, w_val, y, saved, saved_bytes, 0, ws, kScratchBytes, stream,
-                            false);
+    return sdm_forward_impl(q, k, x_dtype, cb_q, cb_k, d_k, topk, topk, v, alpha, beta, in_dtype, mem, B, H, T, d_v,
+                            N, r_idx, r_val, w_idx, w_val, y, saved, saved_bytes, 0, ws, kScratchBytes, stream,
+                            false, nullptr);
 }
 
 }  // extern "C"

@@ -86,7 +86,7 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
     const int32_t* __restrict__ w_idx, const float* __restrict__ w_val, const int32_t* __restrict__ r_idx,
     const float* __restrict__ r_val, const VT* __restrict__ alpha, const VT* __restrict__ beta, int T, int W,
     int R, int64_t N, int nch, int cb, int ncr, int P, unsigned char* __restrict__ recs,
-    unsigned int* __restrict__ err) {
+    unsigned int* __restrict__ err, const float* __restrict__ gA, const float* __restrict__ gbdt, int H) {
     // chunks [cb, cb + ncr) of every stream
     extern __shared__ __align__(16) unsigned char smem[];
     const ChunkRec L = chunk_rec_layout(W, R);
@@ -133,13 +133,19 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
         keys[e] = key;
     }
     for (int t = tid; t < CC; t += CT1) {
-        float a = 1.f, b = 0.f;
+        float lg = 0.f, b = 0.f;
         if (t < n) {
-            a = to_f32(alpha[tok0 + t]);
+            const float a = to_f32(alpha[tok0 + t]);
             b = to_f32(beta[tok0 + t]);
-            if (!(a > 0.f)) bad |= 2u;   // the log form needs alpha > 0
+            if (gA) {   // pre-activations: log alpha = -A softplus(a + b_dt) directly
+                lg = sdm_log_alpha(gA, gbdt, s % H, a);
+                b = sdm_sigmoid(b);
+            } else {
+                if (!(a > 0.f)) bad |= 2u;   // the log form needs alpha > 0
+                lg = logf(fmaxf(a, 1e-30f));
+            }
         }
-        la[t] = logf(fmaxf(a, 1e-30f));
+        la[t] = lg;
         bt[t] = b;
     }
     for (int i = tid; i < 3 * CC * CC; i += CT1) A[i] = 0.f;   // A, QK, L
@@ -507,7 +513,7 @@ hipError_t launch_chunk_coef(const ScanFwdArgs& a, hipStream_t st) {
     hipLaunchKernelGGL(kl, dim3((unsigned)(S * (ce - cb))), dim3(CT1), lds, st, a.w_idx, a.w_val, a.r_idx, a.r_val,
                        static_cast<const VT*>(a.alpha), static_cast<const VT*>(a.beta), a.T, a.W, a.R, a.N, nch, cb,
                        ce - cb, P,
-                       a.ws + SDM_WS_HEADER, reinterpret_cast<unsigned int*>(a.ws));
+                       a.ws + SDM_WS_HEADER, reinterpret_cast<unsigned int*>(a.ws), a.gate_A, a.gate_bdt, a.H);
     return hipGetLastError();
 }
 

@@ -80,7 +80,9 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
                                                        const void* __restrict__ beta, int in_dtype,
                                                        int T, int ta, int te, int W, int R, int64_t N,
                                                        unsigned char* __restrict__ recs,
-                                                       unsigned int* __restrict__ err) {
+                                                       unsigned int* __restrict__ err,
+                                                       const float* __restrict__ gA,
+                                                       const float* __restrict__ gbdt, int H) {
     extern __shared__ int sm[];
     const FwdRec L = fwd_rec_layout(W, R);
     const int stream = blockIdx.y;
@@ -145,6 +147,7 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
         } else if (off == L.off_ab || off == L.off_ab + 4) {
             float al, be;
             load_gates(alpha, beta, in_dtype, tok, al, be);
+            sdm_gates_of(gA, gbdt, stream % H, al, be);
             v = __float_as_uint(off == L.off_ab ? al : be);
         }
         out[i] = v;
@@ -170,7 +173,9 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const int32_t* __restrict
                                                        const void* __restrict__ beta, int in_dtype,
                                                        int T, int tb, int te, int W, int R, int64_t N,
                                                        unsigned char* __restrict__ recs,
-                                                       unsigned int* __restrict__ err) {
+                                                       unsigned int* __restrict__ err,
+                                                       const float* __restrict__ gA,
+                                                       const float* __restrict__ gbdt, int H) {
     // records of tokens [tb, te); links only to tokens below te (the backward
     // of later tokens, in an earlier call, left its rows in HBM)
     extern __shared__ int sm[];
@@ -247,6 +252,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const int32_t* __restrict
         } else if (off == L.off_ab || off == L.off_ab + 4) {
             float al, be;
             load_gates(alpha, beta, in_dtype, tok, al, be);
+            sdm_gates_of(gA, gbdt, stream % H, al, be);
             v = __float_as_uint(off == L.off_ab ? al : be);
         }
         out[i] = v;
@@ -277,7 +283,7 @@ hipError_t sdm_launch_fwd_prep(const ScanFwdArgs& a, hipStream_t st) {
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kfn, grid, dim3(256), sm, st, a.w_idx, a.w_val, a.r_idx, a.r_val, a.alpha,
                        a.beta, a.in_dtype, a.T, a.tb, a.te, a.W, a.R, a.N, a.ws + SDM_WS_HEADER,
-                       reinterpret_cast<unsigned int*>(a.ws));
+                       reinterpret_cast<unsigned int*>(a.ws), a.gate_A, a.gate_bdt, a.H);
     return hipGetLastError();
 }
 
@@ -291,7 +297,7 @@ hipError_t sdm_launch_bwd_prep(const ScanBwdArgs& a, hipStream_t st) {
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kfn, grid, dim3(256), sm, st, a.w_idx, a.w_val, a.r_idx, a.r_val, a.alpha,
                        a.beta, a.in_dtype, a.T, a.tb, a.te, a.W, a.R, a.N, a.ws + SDM_WS_HEADER,
-                       reinterpret_cast<unsigned int*>(a.ws));
+                       reinterpret_cast<unsigned int*>(a.ws), a.gate_A, a.gate_bdt, a.H);
     return hipGetLastError();
 }
 

@@ -26,6 +26,26 @@ __device__ __forceinline__ float4 load4(const bf16_t* p) {
     return make_float4(bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y));
 }
 
+// Gate producers of Sec. 3.1 step 2 from their pre-activations: the forget gate
+// alpha = exp(-A softplus(a + b_dt)) and the input gate beta = sigma(b), with A
+// and b_dt per head.  softplus is written so that neither branch overflows.
+__device__ __forceinline__ float sdm_softplus(float z) {
+    return z > 0.f ? z + log1pf(expf(-z)) : log1pf(expf(z));
+}
+__device__ __forceinline__ float sdm_sigmoid(float z) { return 1.f / (1.f + expf(-z)); }
+// (al, be) hold the stored gates, or the pre-activations when A != NULL; on
+// return they are the gates the recurrence uses.
+__device__ __forceinline__ void sdm_gates_of(const float* A, const float* bdt, int head, float& al, float& be) {
+    if (A) {
+        al = expf(-A[head] * sdm_softplus(al + bdt[head]));
+        be = sdm_sigmoid(be);
+    }
+}
+// log alpha of the gates above, without forming alpha (the chunked form's decays)
+__device__ __forceinline__ float sdm_log_alpha(const float* A, const float* bdt, int head, float a_pre) {
+    return -A[head] * sdm_softplus(a_pre + bdt[head]);
+}
+
 // Monotone map of fp32 to uint32 (larger float -> larger key); -0 maps like +0.
 __device__ __forceinline__ uint32_t ord_key(float f) {
     uint32_t u = __float_as_uint(f);

@@ -68,7 +68,8 @@ hipError_t sdm_launch_address(const void* x, int x_dtype, const void* cb, int B,
 hipError_t sdm_launch_decode(const void* q, const void* k, int x_dtype, const void* cb_q, const void* cb_k, int B,
                              int H, int dk, int s, int topk, const void* v, const void* alpha, const void* beta,
                              int in_dtype, float* mem, int64_t N, int dv, int32_t* r_idx, float* r_val,
-                             int32_t* w_idx, float* w_val, float* y, unsigned int* flags, hipStream_t st);
+                             int32_t* w_idx, float* w_val, float* y, unsigned int* flags, hipStream_t st,
+                             const float* gate_A = nullptr, const float* gate_bdt = nullptr);
 hipError_t sdm_launch_address_bwd(const void* cb, int cb_dtype, int B, int H, int T, int tb, int tn, int dk,
                                   int s, int k, const int32_t* idx, const float* val, const float* dval,
                                   float* dx, hipStream_t st);
@@ -89,6 +90,11 @@ struct ScanFwdArgs {
     float* saved;
     unsigned char* ws;   // workspace base (header + records)
     int tb = 0, te = 0;  // tokens processed: [tb, te) (layout strides use T); tb a multiple of SDM_FWD_PD
+    // Gate producers fused into the records: with gate_A set, alpha and beta hold the
+    // gates' pre-activations and alpha = exp(-A softplus(a + b_dt)), beta = sigma(b)
+    // are formed per token (A, b_dt per head, fp32).
+    const float* gate_A = nullptr;
+    const float* gate_bdt = nullptr;
 };
 hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st);   // prep + scan
 // the two halves separately (records of [tb, te), then the scan of [tb, te))
@@ -144,6 +150,8 @@ struct ScanBwdArgs {
     unsigned char* ws;
     int tb = 0, te = 0;  // tokens processed, te-1 down to tb (layout strides use T)
     int line = -1;       // line-cooperative kernel: 1 / 0, or -1 to decide from the shape
+    const float* gate_A = nullptr;     // as in ScanFwdArgs: alpha, beta are pre-activations
+    const float* gate_bdt = nullptr;
 };
 // Backward of tokens a.te-1 down to a.tb, in three steps: records (with links
 // inside the range), the scan, the sum of the partial scalars.  Ranges are run
@@ -158,6 +166,22 @@ hipError_t sdm_launch_bwd_prep(const ScanBwdArgs& a, hipStream_t st);
 bool sdm_bwd_plan_ok(int W, int R, int dv, int in_dtype);
 size_t sdm_bwd_ws_bytes(int B, int H, int T, int W, int R, int dv);
 
+// Gate producers (Sec. 3.1 step 2) and their reverse mode; dA, db_dt are per-head sums.
+hipError_t sdm_launch_gates(const void* a, const void* b, int dtype, const float* A, const float* bdt, int B, int H,
+                            int T, float* alpha, float* beta, hipStream_t st);
+hipError_t sdm_launch_gates_bwd(const void* a, const void* b, int dtype, const float* A, const float* bdt,
+                                const float* dalpha, const float* dbeta, int B, int H, int T, float* da, float* db,
+                                float* dA, float* db_dt, hipStream_t st);
+// Output epilogue (Sec. 3.1 step 4) on tokens [tb, tb + tn) of S streams of T tokens.
+hipError_t sdm_launch_norm_gate(const float* y, const void* g, int g_dtype, const float* gamma, float eps, int act,
+                                int64_t S, int T, int tb, int tn, int dv, float* o, float* rstd, hipStream_t st);
+// Its reverse mode on `rows` contiguous rows; `part` holds sdm_norm_gate_bwd_ws() bytes
+// of per-workgroup dgamma sums.
+size_t sdm_norm_gate_bwd_ws(int64_t rows, int dv);
+hipError_t sdm_launch_norm_gate_bwd(const float* y, const void* g, int g_dtype, const float* gamma, float eps,
+                                    int act, const float* dout, int64_t rows, int dv, float* dy, float* dg,
+                                    float* dgamma, float* part, hipStream_t st);
+
 // Debug check of slot lists (range and distinctness within each token's list):
 // ORs bit 0 (out of range) and bit 1 (repeated id) into *flag.
 hipError_t sdm_launch_check_ids(const int32_t* w_idx, int W, const int32_t* r_idx, int R, int64_t ntok,
@@ -168,14 +192,27 @@ hipError_t sdm_launch_mem_init(float* dst, const float* m0, int B, int H, int64_
 hipError_t sdm_launch_copy(float* dst, const float* src, size_t n, hipStream_t st);
 hipError_t sdm_launch_zero_words(void* p, int n, hipStream_t st);
 
-// The body of sdm_forward.  pipelined = false runs every step on `stream` in
-// one stage (no second stream, no events): the path of the allocation-free
-// entry point.
+// Optional steps either side of the forward scan: the gates formed from their
+// pre-activations (gate_A set: alpha and beta hold a = W_a x, b = W_b x) and the
+// norm-gate epilogue o = norm(y) gamma phi(g) after each stage's scan (o set).
+struct SdmFwdExtras {
+    const float* gate_A = nullptr;
+    const float* gate_bdt = nullptr;
+    const void* g = nullptr;      // [B, H, T, d_v] in the input dtype
+    const float* gamma = nullptr; // [d_v] or NULL (ones)
+    float eps = 0.f;
+    int act = 0;                  // 0 identity, 1 SiLU
+    float* o = nullptr;           // [B, H, T, d_v] fp32
+    float* rstd = nullptr;        // [B, H, T] fp32 or NULL
+};
+// The body of sdm_forward, with separate write and read list lengths.
+// pipelined = false runs every step on `stream` in one stage (no second
+// stream, no events): the path of the allocation-free entry point.
 int sdm_forward_impl(const void* q, const void* k, int x_dtype, const void* cb_q, const void* cb_k, int d_k,
-                     int topk, const void* v, const void* alpha, const void* beta, int in_dtype, float* mem,
+                     int W, int R, const void* v, const void* alpha, const void* beta, int in_dtype, float* mem,
                      int B, int H, int T, int d_v, int64_t N, int32_t* r_idx, float* r_val, int32_t* w_idx,
                      float* w_val, float* y, float* saved, size_t saved_bytes, int chunk, void* workspace,
-                     size_t ws_bytes, void* stream, bool pipelined);
+                     size_t ws_bytes, void* stream, bool pipelined, const SdmFwdExtras* ex);
 // Sets the thread's sdm_last_error() text and returns status.
 int sdm_set_error(int status, const char* msg);
 

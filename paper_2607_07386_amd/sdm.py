@@ -50,6 +50,19 @@ def lib() -> ctypes.CDLL:
         L.sdm_forward.argtypes = [P, P, I, P, P, I, I, P, P, P, I, P, I, I, I, I, I64, P, P, P, P, P, P,
                                   SZ, I, P, SZ, P]
         L.sdm_scan_fwd_chunked.argtypes = [P, P, I, P, P, I, P, P, P, I, P, I, I, I, I, I64, P, P, SZ, P]
+        F = ctypes.c_float
+        L.sdm_gates.argtypes = [P, P, I, P, P, I, I, I, P, P, P]
+        L.sdm_gates_bwd.argtypes = [P, P, I, P, P, P, P, I, I, I, P, P, P, P, P]
+        L.sdm_norm_gate.argtypes = [P, P, I, P, F, I, I, I, I, I, P, P, P]
+        L.sdm_norm_gate_bwd_workspace_bytes.argtypes = [I, I, I, I]
+        L.sdm_norm_gate_bwd_workspace_bytes.restype = SZ
+        L.sdm_norm_gate_bwd.argtypes = [P, P, I, P, F, I, P, I, I, I, I, P, P, P, P, SZ, P]
+        L.sdm_layer_fwd.argtypes = [P, P, I, P, P, I, I, I, P, P, P, P, I, P, P, P, F, I, P, I, I, I, I, I64,
+                                    P, P, P, P, P, P, P, P, SZ, I, P, SZ, P]
+        L.sdm_layer_bwd_workspace_bytes.argtypes = [I, I, I, I, I, I]
+        L.sdm_layer_bwd_workspace_bytes.restype = SZ
+        L.sdm_layer_bwd.argtypes = [P, P, I, I, P, P, I, P, P, I, P, P, P, P, I, P, P, P, F, I, P, P, SZ, P, P,
+                                    P, I, I, I, I, I, I64, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
         L.sdm_forward_noalloc.argtypes = [P, P, I, P, P, I, I, P, P, P, I, P, I, I, I, I, I64, P, P, P, P, P,
                                           P, SZ, P]
         L.sdm_forward_noalloc_max_bytes.argtypes = []
@@ -73,7 +86,8 @@ def lib() -> ctypes.CDLL:
         L.sdm_last_error.restype = ctypes.c_char_p
         L.sdm_version.restype = ctypes.c_char_p
         for f in ("sdm_address", "sdm_scan_fwd", "sdm_scan_fwd_chunked", "sdm_scan_bwd", "sdm_mem_init",
-                  "sdm_forward_noalloc",
+                  "sdm_forward_noalloc", "sdm_gates", "sdm_gates_bwd", "sdm_norm_gate", "sdm_norm_gate_bwd",
+                  "sdm_layer_fwd", "sdm_layer_bwd",
                   "sdm_check_device_errors",
                   "sdm_profile_enable", "sdm_profile_select", "sdm_profile_read"):
             getattr(L, f).restype = I
@@ -338,6 +352,185 @@ def forward_noalloc(q, k, cb_q, cb_k, v, alpha, beta, mem, N: int, topk: int, sa
     return o
 
 
+def _check_gate_params(A, b_dt, H):
+    _expect(A, "A", (H,), _F32)
+    _expect(b_dt, "b_dt", (H,), _F32)
+
+
+def gates(a_pre, b_pre, A, b_dt):
+    """Forget and input gates from their pre-activations (Sec. 3.1 step 2):
+    alpha = exp(-A softplus(a + b_dt)), beta = sigma(b).  a_pre, b_pre [B,H,T];
+    A, b_dt [H] fp32.  Returns (alpha, beta) fp32 [B,H,T]."""
+    _expect_dims(a_pre, "a_pre", 3)
+    B, H, T = a_pre.shape
+    if a_pre.dtype not in _IN:
+        raise TypeError(f"a_pre has dtype {a_pre.dtype}, expected float32 or bfloat16")
+    _expect(b_pre, "b_pre", (B, H, T), (a_pre.dtype,))
+    _check_gate_params(A, b_dt, H)
+    dev = _dev(a_pre, b_pre, A, b_dt)
+    al = torch.empty((B, H, T), dtype=torch.float32, device=dev)
+    be = torch.empty_like(al)
+    _check("sdm_gates", lib().sdm_gates(_ptr(a_pre), _ptr(b_pre), _dtype_code(a_pre), _ptr(A), _ptr(b_dt), B, H, T,
+                                         _ptr(al), _ptr(be), _stream(dev)))
+    return al, be
+
+
+def gates_bwd(a_pre, b_pre, A, b_dt, dalpha, dbeta):
+    """Reverse mode of gates: returns (da, db [B,H,T], dA, db_dt [H]), fp32."""
+    _expect_dims(a_pre, "a_pre", 3)
+    B, H, T = a_pre.shape
+    if a_pre.dtype not in _IN:
+        raise TypeError(f"a_pre has dtype {a_pre.dtype}, expected float32 or bfloat16")
+    _expect(b_pre, "b_pre", (B, H, T), (a_pre.dtype,))
+    _check_gate_params(A, b_dt, H)
+    _expect(dalpha, "dalpha", (B, H, T), _F32)
+    _expect(dbeta, "dbeta", (B, H, T), _F32)
+    dev = _dev(a_pre, b_pre, A, b_dt, dalpha, dbeta)
+    da = torch.empty((B, H, T), dtype=torch.float32, device=dev)
+    db = torch.empty_like(da)
+    dA = torch.empty((H,), dtype=torch.float32, device=dev)
+    dbd = torch.empty_like(dA)
+    _check("sdm_gates_bwd", lib().sdm_gates_bwd(_ptr(a_pre), _ptr(b_pre), _dtype_code(a_pre), _ptr(A), _ptr(b_dt),
+                                                 _ptr(dalpha), _ptr(dbeta), B, H, T, _ptr(da), _ptr(db), _ptr(dA),
+                                                 _ptr(dbd), _stream(dev)))
+    return da, db, dA, dbd
+
+
+def _check_norm_gate(y, g, gamma):
+    _expect_dims(y, "y", 4)
+    B, H, T, dv = y.shape
+    _expect(y, "y", (B, H, T, dv), _F32)
+    _expect(g, "g", (B, H, T, dv), _IN)
+    if gamma is not None:
+        _expect(gamma, "gamma", (dv,), _F32)
+    return B, H, T, dv
+
+
+def norm_gate(y, g, gamma, eps: float, act: int, want_rstd: bool = False):
+    """Output epilogue (Sec. 3.1 step 4): o = y rstd gamma phi(g) per (b,h,t) row,
+    rstd = 1/sqrt(mean(y^2) + eps), phi identity (act 0) or SiLU (act 1).
+    Returns o (and rstd)."""
+    B, H, T, dv = _check_norm_gate(y, g, gamma)
+    dev = _dev(y, g, gamma)
+    o = torch.empty_like(y)
+    rstd = torch.empty((B, H, T), dtype=torch.float32, device=dev) if want_rstd else None
+    _check("sdm_norm_gate", lib().sdm_norm_gate(_ptr(y), _ptr(g), _dtype_code(g), _ptr(gamma), float(eps), int(act),
+                                                 B, H, T, dv, _ptr(o), _ptr(rstd), _stream(dev)))
+    return (o, rstd) if want_rstd else o
+
+
+def norm_gate_bwd(y, g, gamma, eps: float, act: int, dout, want_dgamma: bool = True):
+    """Reverse mode of norm_gate: returns dy, dg and dgamma (None if not wanted)."""
+    B, H, T, dv = _check_norm_gate(y, g, gamma)
+    _expect(dout, "dout", (B, H, T, dv), _F32)
+    dev = _dev(y, g, gamma, dout)
+    dy = torch.empty_like(y)
+    dg = torch.empty_like(y)
+    dgamma = torch.empty((dv,), dtype=torch.float32, device=dev) if want_dgamma else None
+    ws = _ws(lib().sdm_norm_gate_bwd_workspace_bytes(B, H, T, dv), dev)
+    _check("sdm_norm_gate_bwd", lib().sdm_norm_gate_bwd(_ptr(y), _ptr(g), _dtype_code(g), _ptr(gamma), float(eps),
+                                                         int(act), _ptr(dout), B, H, T, dv, _ptr(dy), _ptr(dg),
+                                                         _ptr(dgamma), _ptr(ws), ws.numel(), _stream(dev)))
+    return dy, dg, dgamma
+
+
+def layer_fwd(q, k, cb_q, cb_k, v, a_pre, b_pre, g, A, b_dt, gamma, eps: float, act: int, mem, N: int, W: int,
+              R: int, saved=None, workspace=None, chunk: int = 0, want_rstd: bool = False):
+    """The layer from its projections to W_o's input (Sec. 3.1 steps 1-4): addressing (top-R
+    reads of q, top-W writes of k), gates formed inside the scan's records, the recurrence in
+    place on mem, and the norm-gate epilogue per pipeline stage.  Returns a dict with o, y,
+    r_idx, r_val, w_idx, w_val (and rstd)."""
+    _expect_dims(q, "q", 4)
+    _expect_dims(v, "v", 4)
+    _expect_dims(mem, "mem", 4)
+    B, H, T, dk = q.shape
+    dv = v.shape[-1]
+    if q.dtype not in _IN or v.dtype not in _IN:
+        raise TypeError("q and v must be float32 or bfloat16")
+    _expect(k, "k", (B, H, T, dk), (q.dtype,))
+    _check_codebook(cb_q, "cb_q", q, N)
+    _check_codebook(cb_k, "cb_k", q, N)
+    _expect(v, "v", (B, H, T, dv), (v.dtype,))
+    _expect(a_pre, "a_pre", (B, H, T), (v.dtype,))
+    _expect(b_pre, "b_pre", (B, H, T), (v.dtype,))
+    _expect(g, "g", (B, H, T, dv), (v.dtype,))
+    _check_gate_params(A, b_dt, H)
+    if gamma is not None:
+        _expect(gamma, "gamma", (dv,), _F32)
+    _expect(mem, "mem", (B, H, N, dv), _F32)
+    if saved is not None:
+        _expect(saved, "saved", (B, H, T, W, dv), _F32)
+    _check_ws(workspace, lib().sdm_scan_fwd_workspace_bytes(B, H, T, W, R) if workspace is not None else 0)
+    dev = _dev(q, k, cb_q, cb_k, v, a_pre, b_pre, g, A, b_dt, gamma, mem, saved)
+    f32 = dict(dtype=torch.float32, device=dev)
+    o = dict(r_idx=torch.empty((B, H, T, R), dtype=torch.int32, device=dev), r_val=torch.empty((B, H, T, R), **f32),
+             w_idx=torch.empty((B, H, T, W), dtype=torch.int32, device=dev), w_val=torch.empty((B, H, T, W), **f32),
+             y=torch.empty((B, H, T, dv), **f32), o=torch.empty((B, H, T, dv), **f32))
+    o["rstd"] = torch.empty((B, H, T), **f32) if want_rstd else None
+    if workspace is None:
+        workspace = fwd_workspace(B, H, T, W, R, dev)
+    sb = saved.numel() * 4 if saved is not None else 0
+    rc = lib().sdm_layer_fwd(_ptr(q), _ptr(k), _dtype_code(q), _ptr(cb_q), _ptr(cb_k), dk, W, R, _ptr(v),
+                             _ptr(a_pre), _ptr(b_pre), _ptr(g), _dtype_code(v), _ptr(A), _ptr(b_dt), _ptr(gamma),
+                             float(eps), int(act), _ptr(mem), B, H, T, dv, N, _ptr(o["r_idx"]), _ptr(o["r_val"]),
+                             _ptr(o["w_idx"]), _ptr(o["w_val"]), _ptr(o["y"]), _ptr(o["o"]), _ptr(o["rstd"]),
+                             _ptr(saved), sb, int(chunk), _ptr(workspace), workspace.numel(), _stream(dev))
+    _check("sdm_layer_fwd", rc)
+    return o
+
+
+def layer_bwd(fwd, v, a_pre, b_pre, g, A, b_dt, gamma, eps: float, act: int, mem, saved, dout, dmem_T=None,
+              cb_q=None, cb_k=None, d_k: int | None = None, chunk: int = 64, want_dqk: bool = True,
+              want_dgamma: bool = True, workspace=None):
+    """Reverse mode of layer_fwd (fwd: its returned dict).  mem: M_T in, M_0 out.  Returns a dict
+    with dv, da, db, dA, db_dt, dg, dgamma, dmem0 and (if want_dqk) dq, dk."""
+    w_idx, w_val, r_idx, r_val, y = fwd["w_idx"], fwd["w_val"], fwd["r_idx"], fwd["r_val"], fwd["y"]
+    B, H, T, dv_, W, R, N = _check_scan_args(w_idx, w_val, r_idx, r_val, v, a_pre, b_pre, mem)
+    _expect(g, "g", (B, H, T, dv_), (v.dtype,))
+    _check_gate_params(A, b_dt, H)
+    if gamma is not None:
+        _expect(gamma, "gamma", (dv_,), _F32)
+    _expect(saved, "saved", (B, H, T, W, dv_), _F32)
+    _expect(y, "y", (B, H, T, dv_), _F32)
+    _expect(dout, "dout", (B, H, T, dv_), _F32)
+    if dmem_T is not None:
+        _expect(dmem_T, "dmem_T", (B, H, N, dv_), _F32)
+    if want_dqk:
+        if d_k is None:
+            raise ValueError("d_k is required for addressing gradients")
+        for cb, nm in ((cb_q, "cb_q"), (cb_k, "cb_k")):
+            if cb is not None:
+                _expect(cb, nm, (H, 2, int(round(N ** 0.5)), d_k // 2), _IN)
+    _check_ws(workspace, lib().sdm_layer_bwd_workspace_bytes(B, H, T, W, R, dv_) if workspace is not None else 0)
+    dev = _dev(w_idx, w_val, r_idx, r_val, v, a_pre, b_pre, g, A, b_dt, gamma, mem, saved, y, dout, dmem_T, cb_q,
+               cb_k)
+    f32 = dict(dtype=torch.float32, device=dev)
+    out = dict(dv=torch.empty((B, H, T, dv_), **f32), da=torch.empty((B, H, T), **f32),
+               db=torch.empty((B, H, T), **f32), dA=torch.empty((H,), **f32), db_dt=torch.empty((H,), **f32),
+               dg=torch.empty((B, H, T, dv_), **f32), dmem0=torch.empty((B, H, N, dv_), **f32),
+               dgamma=torch.empty((dv_,), **f32) if want_dgamma else None)
+    dq = dk = None
+    cb_dtype = SDM_F32
+    if want_dqk:
+        dq = torch.empty((B, H, T, d_k), **f32)
+        dk = torch.empty((B, H, T, d_k), **f32)
+        cb = cb_q if cb_q is not None else cb_k
+        cb_dtype = _dtype_code(cb) if cb is not None else SDM_F32
+    if workspace is None:
+        workspace = _ws(lib().sdm_layer_bwd_workspace_bytes(B, H, T, W, R, dv_), dev)
+    rc = lib().sdm_layer_bwd(_ptr(cb_q), _ptr(cb_k), cb_dtype, int(d_k or 0), _ptr(w_idx), _ptr(w_val), W,
+                             _ptr(r_idx), _ptr(r_val), R, _ptr(v), _ptr(a_pre), _ptr(b_pre), _ptr(g), _dtype_code(v),
+                             _ptr(A), _ptr(b_dt), _ptr(gamma), float(eps), int(act), _ptr(mem), _ptr(saved),
+                             saved.numel() * 4, _ptr(y), _ptr(dout), _ptr(dmem_T), int(chunk), B, H, T, dv_, N,
+                             _ptr(dq), _ptr(dk), _ptr(out["dv"]), _ptr(out["da"]), _ptr(out["db"]), _ptr(out["dA"]),
+                             _ptr(out["db_dt"]), _ptr(out["dg"]), _ptr(out["dgamma"]), _ptr(out["dmem0"]),
+                             _ptr(workspace), workspace.numel(), _stream(dev))
+    _check("sdm_layer_bwd", rc)
+    if want_dqk:
+        out["dq"], out["dk"] = dq, dk
+    return out
+
+
 def bwd_workspace(B, H, T, W, R, d_v, device) -> torch.Tensor:
     return _ws(lib().sdm_scan_bwd_workspace_bytes(B, H, T, W, R, d_v), device)
 
@@ -410,7 +603,8 @@ def check_device_errors(workspace: torch.Tensor):
 
 
 KERNELS = {"address": 0, "fwd_prep": 1, "fwd_scan": 2, "bwd_prep": 3, "bwd_scan": 4, "bwd_reduce": 5,
-           "address_bwd": 6, "mem_init": 7, "decode": 8, "chunk_coef": 9, "chunk_scan": 10}
+           "address_bwd": 6, "mem_init": 7, "decode": 8, "chunk_coef": 9, "chunk_scan": 10, "norm_gate": 11,
+           "gates": 12}
 
 
 def set_chunk_scan_cols(cols: int):

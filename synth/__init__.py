@@ -21,6 +21,12 @@ regenerated alone for sampled checks):
 * sub-key codebooks [H, 2, sqrt(N), d_k/2]: N(0, 1) rows, L2-normalised.
 * learned initial memory [H, N, d_v]: N(0, 0.02^2), shared across the batch.
 * upstream output gradient dy: N(0, 1), fp32.
+* inputs of the steps either side of the recurrence (``LayerInputs``): gate
+  pre-activations a, b ~ N(0, 1) [B, H, T]; output gate g ~ N(0, 1)
+  [B, H, T, d_v]; per head A ~ U(0, 16) and b_dt = inverse softplus of
+  U(0.001, 0.1) (the paper's Sec. 4 initialisation); norm scale
+  gamma ~ U(0.5, 1.5) [d_v]; upstream gradient of the epilogue's output
+  N(0, 1), fp32.
 * low-precision workloads round fp64 -> fp32 -> bf16 (round to nearest even);
   fp32 workloads round fp64 -> fp32.  Both sides read the same bits.
 """
@@ -35,6 +41,7 @@ import numpy as np
 
 # tensor ids used in the seed spawn key
 _Q, _K, _V, _BETA, _ALPHA, _CB, _M0, _CENTRES, _ASSIGN, _DY, _DMT, _MNOISE = range(12)
+_APRE, _BPRE, _GATE_OUT, _GATE_PARAM, _GAMMA, _DOUT = range(12, 18)
 
 
 @dataclass(frozen=True)
@@ -273,3 +280,29 @@ def tiny(**kw) -> Workload:
     base = dict(name="tiny", B=1, H=2, T=16, d_k=8, d_v=8, N=64, topk=4, dtype="f32", seed=123)
     base.update(kw)
     return Workload(**base)
+
+
+class LayerInputs:
+    """The inputs of the gate producers and the output epilogue for a
+    workload's streams, drawn as the recipe above states: gate
+    pre-activations ``a_pre``, ``b_pre`` [B, H, T] and the output gate ``g``
+    [B, H, T, d_v] in the workload's dtype; per-head ``A`` and ``b_dt`` [H],
+    the norm scale ``gamma`` [d_v] and ``dout`` [B, H, T, d_v] in fp32."""
+
+    def __init__(self, w: Workload):
+        self.w = w
+        B, H, T, dv = w.B, w.H, w.T, w.d_v
+        a = np.stack([np.stack([_rng(w, _APRE, b, h).standard_normal(T) for h in range(H)]) for b in range(B)])
+        bb = np.stack([np.stack([_rng(w, _BPRE, b, h).standard_normal(T) for h in range(H)]) for b in range(B)])
+        g = np.stack([np.stack([_rng(w, _GATE_OUT, b, h).standard_normal((T, dv)) for h in range(H)])
+                      for b in range(B)])
+        self.a_pre = Stored.from_f64(a.reshape(B, H, T), w.dtype)
+        self.b_pre = Stored.from_f64(bb.reshape(B, H, T), w.dtype)
+        self.g = Stored.from_f64(g.reshape(B, H, T, dv), w.dtype)
+        gp = _rng(w, _GATE_PARAM, 0, 0)
+        self.A = gp.uniform(0.0, 16.0, H).astype(np.float32)
+        dt = gp.uniform(0.001, 0.1, H)
+        self.b_dt = np.log(np.expm1(dt)).astype(np.float32)
+        self.gamma = _rng(w, _GAMMA, 0, 0).uniform(0.5, 1.5, dv).astype(np.float32)
+        self.dout = np.stack([np.stack([_rng(w, _DOUT, b, h).standard_normal((T, dv), dtype=np.float32)
+                                        for h in range(H)]) for b in range(B)]).reshape(B, H, T, dv)

@@ -163,11 +163,12 @@ def test_scan_line_io_setting():
 
 
 def test_profile_select():
+    n = len(sdm.KERNELS)
     assert L.sdm_profile_select(1 << 2) == 0
-    assert L.sdm_profile_select((1 << 11) - 1) == 0
-    assert L.sdm_profile_select(1 << 11) == -1
+    assert L.sdm_profile_select((1 << n) - 1) == 0
+    assert L.sdm_profile_select(1 << n) == -1
     assert b"unknown kernel kinds" in L.sdm_last_error()
-    assert L.sdm_profile_select((1 << 11) - 1) == 0
+    assert L.sdm_profile_select((1 << n) - 1) == 0
 
 
 def test_mem_init_validation():
@@ -241,3 +242,27 @@ def test_noalloc_refuses_sizes_past_its_array_on_the_host():
     # an empty call needs nothing and returns at once
     assert L.sdm_forward_noalloc(A, A, 1, B_, B_, 128, k, A, A, A, 1, A, B, H, 0, 128, 65536,
                                  A, A, A, A, A, None, 0, None) == 0
+
+
+def test_gates_and_epilogue_validation():
+    """Host checks of the gate and epilogue entry points (CPU only)."""
+    F = ctypes.c_float
+    # sdm_gates(a, b, dtype, A, b_dt, B, H, T, alpha, beta, stream)
+    assert L.sdm_gates(A, A, 5, A, A, 1, 2, 8, A, A, None) == -1            # dtype
+    assert L.sdm_gates(A, A, 1, None, A, 1, 2, 8, A, A, None) == -1         # A
+    assert L.sdm_gates(None, A, 1, A, A, 1, 2, 8, A, A, None) == -1         # pre-activation
+    assert L.sdm_gates(A, A, 1, A, A, 1, 2, 8, None, A, None) == -1         # output
+    assert L.sdm_gates(A, A, 1, A, A, 1, 2, 0, None, None, None) == 0       # empty
+    # sdm_norm_gate(y, g, g_dtype, gamma, eps, act, B, H, T, d_v, o, rstd, stream)
+    ng = L.sdm_norm_gate
+    assert ng(A, A, 1, None, F(1e-5), 2, 1, 1, 4, 64, A, None, None) == -1  # act
+    assert ng(A, A, 1, None, F(-1.0), 0, 1, 1, 4, 64, A, None, None) == -1  # eps
+    assert ng(A, A, 1, None, F(1e-5), 0, 1, 1, 4, 66, A, None, None) == -1  # d_v
+    assert ng(A, A, 1, None, F(1e-5), 0, 1, 1, 4, 8192, A, None, None) == -2
+    assert ng(A, A + 4, 1, None, F(1e-5), 0, 1, 1, 4, 64, A, None, None) == -1   # alignment
+    assert ng(A, A, 1, None, F(1e-5), 0, 1, 1, 4, 64, None, None, None) == -1    # o
+    assert ng(A, A, 1, None, F(1e-5), 0, 1, 1, 0, 64, None, None, None) == 0     # empty
+    need = L.sdm_norm_gate_bwd_workspace_bytes(2, 3, 100, 128)
+    assert need >= 128 * 4 and need % 256 == 0
+    assert L.sdm_norm_gate_bwd(A, A, 1, None, F(1e-5), 0, A, 2, 3, 100, 128, A, A, A, A, need - 1, None) == -3
+    assert L.sdm_layer_bwd_workspace_bytes(2, 3, 100, 32, 32, 128) > L.sdm_scan_bwd_workspace_bytes(2, 3, 100, 32, 32, 128)
