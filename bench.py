@@ -14,8 +14,11 @@ work per step does not depend on the table's contents).
 
 Further legs: the training step (forward with the undo log + backward with
 addressing gradients) on the training workload (B=4, H=16, T=4096) under
-"train"; the learned-M0 broadcast of the learned-M0 workload under
-"mem_init"; single-token decode steps under "decode"; the paper's own 1.4B
+"train"; the learned-M0 workload (B=4, H=8, T=8192, N=2^20): its M0
+broadcast under "mem_init" and its forward steps under "learned_m0";
+single-token decode steps under "decode"; the layer with its gate producers
+and norm-gate epilogue fused (sdm_layer_fwd / sdm_layer_bwd) against the bare
+path under "layer"; the paper's own 1.4B
 and 8B layer shapes (H=2, sqrt(N)=240 and 480, d_v=960 and 1920, W=R=64,
 direct-mode addressing; forward and training steps) under "paper_layer"; the
 long-context scan (16 streams of 65536 tokens) by the sequential and the
@@ -83,6 +86,13 @@ def unique_row_bytes(w_idx, r_idx, d_v, in_bytes, window=64):
     rows = distinct(both) + distinct(wi)
     tokens = S * nw * window
     return rows * d_v * 4 + tokens * (d_v * in_bytes + 2 * in_bytes + (W + R) * 8 + d_v * 4), tokens
+
+
+def bwd_scan_bytes_per_token_head(W, R, d_v, in_bytes):
+    """Bytes the backward scan must move per (token, head): rows M_t[j_m],
+    G[j_m] and G[i_n] read, P (the undo log) read, G[j_m], G[i_n] and the undo
+    M[i_n] written, (4W + 3R) fp32 rows of d_v; plus dy and dv (fp32) and v."""
+    return (4 * W + 3 * R) * d_v * 4 + d_v * (4 + 4 + in_bytes)
 
 
 def scoring_mfma(w, call_ms):
@@ -153,7 +163,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-streams", type=int, default=16)
     ap.add_argument("--cpu-tokens", type=int, default=4096)
-    ap.add_argument("--only", choices=["fwd", "train", "init", "decode", "paper", "address", "long"], default=None,
+    ap.add_argument("--only", choices=["fwd", "train", "learned", "decode", "paper", "address", "long", "layer"],
+                    default=None,
                     help="run one leg only (profiling runs)")
     ap.add_argument("--no-sequential", action="store_true",
                     help="skip the reference timing of the forward step as three separate calls")
@@ -364,36 +375,29 @@ def main():
         kern = {n: sdm.profile_read(n) for n in ("address", "fwd_prep", "fwd_scan", "bwd_prep",
                                                    "bwd_scan", "bwd_reduce", "address_bwd", "mem_init")}
         sdm.profile_enable(False)
+        # the backward scan's roofline: its algorithmic bytes per launch (every row the
+        # reverse step touches, plus dy, dv and v) over its mean event-timed duration
+        b_unit = bwd_scan_bytes_per_token_head(wt.topk, wt.topk, wt.d_v, 2)
+        b_launches = max(kern["bwd_scan"][1], 1)
+        b_ms = kern["bwd_scan"][0] / b_launches
+        b_tokens = B * H * T * args.steps / b_launches
+        b_bytes = round(b_unit * b_tokens)
+        b_ach = b_bytes / (b_ms * 1e-3) / 1e9
         out["train"] = {
             "value": round(B * T / (tms * 1e-3), 1), "unit": "tokens/s", "ms_per_step": round(tms, 4),
             "workload": "training step: B=4 H=16 T=4096 d_k=d_v=128 N=65536 top-32, chunk 64; "
                         "address(q,k) + forward with undo log (one sdm_forward call) + backward "
                         "(dq, dk, dv, dalpha, dbeta, dM0)",
             "kernels_ms": {n: round(v[0] / max(v[1], 1), 4) for n, v in kern.items()},
+            "roofline": {"bound": "hbm", "kernel": "bwd_scan", "achieved": round(b_ach, 1), "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": round(b_ach / HBM_PEAK_GBS, 4), "traffic": None,
+                         "algorithmic_bytes_per_token_head": b_unit, "algorithmic_bytes_per_launch": b_bytes,
+                         "kernel_ms": round(b_ms, 4), "launches_per_step": round(b_launches / args.steps, 2)},
         }
     extra = not args.no_extra
-    # ------------------------------------------------------------ memory initialisation (a9)
-    if (extra and args.only is None) or args.only == "init":
-        w3 = synth.WORKLOADS[3]
-        log("timing the learned-M0 broadcast of the learned-M0 workload")
-        m0 = torch.zeros((w3.H, w3.N, w3.d_v), dtype=torch.float32, device=dev)
-        dst = torch.empty((w3.B, w3.H, w3.N, w3.d_v), dtype=torch.float32, device=dev)
-        sdm.mem_init(dst, m0)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(3):
-            sdm.mem_init(dst, m0)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ims = e0.elapsed_time(e1) / 3
-        moved = dst.numel() * 4 + m0.numel() * 4
-        out["mem_init"] = {
-            "workload": f"M0 [H={w3.H}, N={w3.N}, d_v={w3.d_v}] fp32 broadcast to B={w3.B} sequences",
-            "ms": round(ims, 4), "bytes_written": dst.numel() * 4, "bytes_read_unique": m0.numel() * 4,
-            "GB_s": round(moved / (ims * 1e-3) / 1e9, 1)}
-        del m0, dst
-        torch.cuda.empty_cache()
+    # ------------------------------------------------------------ learned M0 (a9 + forward)
+    if (extra and args.only is None) or args.only == "learned":
+        out.update(learned_m0_leg(sdm, to_dev, stream, dev, args))
 
     # ------------------------------------------------------------ decode steps (T = 1)
     if (extra and args.only is None) or args.only == "decode":
@@ -489,12 +493,18 @@ def main():
             torch.cuda.synchronize()
             kms = {kk: round(sdm.profile_read(kk)[0], 3) for kk in kinds}
             sdm.profile_enable(False)
+            gbs = lbytes / (ms * 1e-3) / 1e9
             res[name] = {"ms": round(ms, 3), "tokens_per_s": round(wl.B * wl.T / (ms * 1e-3), 1),
-                         "GB_s": round(lbytes / (ms * 1e-3) / 1e9, 1), "kernels_ms": kms}
+                         "GB_s": round(gbs, 1), "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+                         "kernels_ms": kms}
         res["chunked_speedup"] = round(res["sequential"]["ms"] / res["chunked"]["ms"], 3)
         out["long_context"] = res
         del v, al, be, cb, ri, rv, wi, wv, mem, yl, wsf, wsc
         torch.cuda.empty_cache()
+
+    # ------------------------------------------------------------ the steps either side (gates, epilogue)
+    if (extra and args.only is None) or args.only == "layer":
+        out["layer"] = layer_leg(sdm, to_dev, stream, dev, args)
 
     # ------------------------------------------------------------ the paper's 1.4B and 8B layers
     if (extra and args.only is None) or args.only == "paper":
@@ -510,6 +520,168 @@ def main():
             out["paper_layer"][tag] = paper_layer(sdm, to_dev, wp, tag, root, stream, dev)
 
     print(json.dumps(out), flush=True)
+
+
+def layer_leg(sdm, to_dev, stream, dev, args):
+    """The cost of the steps either side of the recurrence: forward steps of the
+    1.4B-shaped workload through sdm_layer_fwd (gates formed in the scan's
+    records from their pre-activations, norm-gate epilogue per stage) against
+    sdm_forward on precomputed gates; training steps of the training workload
+    through sdm_layer_fwd + sdm_layer_bwd against sdm_forward + sdm_scan_bwd."""
+    import torch
+
+    import synth
+
+    res = {}
+    for tag, wl, train in (("fwd", synth.WORKLOADS[1], False), ("train", synth.WORKLOADS[4], True)):
+        log(f"layer: {tag} inputs")
+        inp = synth.Inputs(wl)
+        li = synth.LayerInputs(wl)
+        q, k, v, cb = to_dev(inp.q), to_dev(inp.k), to_dev(inp.v), to_dev(inp.codebook)
+        a, b, g = to_dev(li.a_pre), to_dev(li.b_pre), to_dev(li.g)
+        A, bdt, gm = (torch.from_numpy(x).to(dev) for x in (li.A, li.b_dt, li.gamma))
+        al, be = sdm.gates(a, b, A, bdt)
+        al16, be16 = al.to(torch.bfloat16), be.to(torch.bfloat16)   # the plain path's gates, in the input dtype
+        B, H, T = wl.B, wl.H, wl.T
+        mem = torch.zeros((B, H, wl.N, wl.d_v), dtype=torch.float32, device=dev)
+        ws = sdm.fwd_workspace(B, H, T, wl.topk, wl.topk, dev)
+        saved = sdm.saved_buffer(B, H, T, wl.topk, wl.d_v, dev) if train else None
+        chunk = args.chunk if not train else args.train_chunk
+        dout = torch.from_numpy(li.dout).to(dev) if train else None
+        dy = torch.from_numpy(inp.dy()).to(dev) if train else None
+        bws = sdm.bwd_workspace(B, H, T, wl.topk, wl.topk, wl.d_v, dev) if train else None
+        lws = (torch.empty(sdm.lib().sdm_layer_bwd_workspace_bytes(B, H, T, wl.topk, wl.topk, wl.d_v),
+                           dtype=torch.uint8, device=dev) if train else None)
+
+        def plain():
+            o = sdm.forward(q, k, cb, cb, v, al16, be16, mem, wl.N, wl.topk, saved=saved, workspace=ws, chunk=chunk)
+            if train:
+                sdm.scan_bwd(o["w_idx"], o["w_val"], o["r_idx"], o["r_val"], v, al16, be16, mem, saved, dy,
+                             cb_q=cb, cb_k=cb, d_k=wl.d_k, chunk=wl.chunk, workspace=bws)
+
+        def layer():
+            o = sdm.layer_fwd(q, k, cb, cb, v, a, b, g, A, bdt, gm, 1e-6, 1, mem, wl.N, wl.topk, wl.topk,
+                              saved=saved, workspace=ws, chunk=chunk)
+            if train:
+                sdm.layer_bwd(o, v, a, b, g, A, bdt, gm, 1e-6, 1, mem, saved, dout, cb_q=cb, cb_k=cb, d_k=wl.d_k,
+                              chunk=wl.chunk, workspace=lws)
+
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        times = {}
+        for name, fn in (("plain", plain), ("layer", layer)):
+            for _ in range(2):
+                fn()
+            torch.cuda.synchronize()
+            n = max(3, args.steps // 2)
+            e0.record(stream)
+            for _ in range(n):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times[name] = e0.elapsed_time(e1) / n
+        sdm.profile_select(["norm_gate", "gates"])
+        sdm.profile_enable(True)
+        layer()
+        torch.cuda.synchronize()
+        kms = {kk: round(sdm.profile_read(kk)[0], 4) for kk in ("norm_gate", "gates")}
+        sdm.profile_enable(False)
+        sdm.profile_select(None)
+        res[tag] = {"workload": f"{wl.name}: B={B} H={H} T={T} d_v={wl.d_v} top-{wl.topk}; gates from bf16 "
+                                f"pre-activations (A, b_dt per head), epilogue RMS norm x SiLU gate, eps 1e-6",
+                    "ms_per_step_layer": round(times["layer"], 4), "ms_per_step_plain": round(times["plain"], 4),
+                    "added_ms": round(times["layer"] - times["plain"], 4),
+                    "tokens_per_s_layer": round(B * T / (times["layer"] * 1e-3), 1),
+                    "kernels_ms_per_step": kms}
+        del q, k, v, cb, a, b, g, A, bdt, gm, al, be, al16, be16, mem, ws, saved, dout, dy, bws, lws
+        torch.cuda.empty_cache()
+    return res
+
+
+def learned_m0_leg(sdm, to_dev, stream, dev, args):
+    """The learned-M0 workload (B=4 H=8 T=8192 N=2^20 d=128 top-32): the shared
+    M0 broadcast to every sequence, timed alone (excluded from the step), and
+    forward steps (one sdm_forward call each, the library's stages) on the
+    resident table, with the scan's roofline."""
+    import torch
+
+    import synth
+
+    w3 = synth.WORKLOADS[3]
+    log("learned M0: generating inputs")
+    inp = synth.Inputs(w3)
+    q, k, v = to_dev(inp.q), to_dev(inp.k), to_dev(inp.v)
+    al, be, cb = to_dev(inp.alpha), to_dev(inp.beta), to_dev(inp.codebook)
+    B, H, T = w3.B, w3.H, w3.T
+    # M0 ~ N(0, 0.02^2), drawn on the device: the bytes moved do not depend on the values
+    # (the parity tests use the seeded host generator)
+    g = torch.Generator(device=dev)
+    g.manual_seed(w3.seed)
+    m0 = torch.randn((H, w3.N, w3.d_v), dtype=torch.float32, device=dev, generator=g).mul_(0.02)
+    mem = torch.empty((B, H, w3.N, w3.d_v), dtype=torch.float32, device=dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    sdm.mem_init(mem, m0)
+    torch.cuda.synchronize()
+    log("learned M0: timing the broadcast")
+    e0.record(stream)
+    for _ in range(3):
+        sdm.mem_init(mem, m0)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ims = e0.elapsed_time(e1) / 3
+    moved = mem.numel() * 4 + m0.numel() * 4
+    res = {"mem_init": {
+        "workload": f"M0 [H={H}, N={w3.N}, d_v={w3.d_v}] fp32 broadcast to B={B} sequences",
+        "ms": round(ims, 4), "bytes_written": mem.numel() * 4, "bytes_read_unique": m0.numel() * 4,
+        "GB_s": round(moved / (ims * 1e-3) / 1e9, 1)}}
+    ws = sdm.fwd_workspace(B, H, T, w3.topk, w3.topk, dev)
+    y = torch.empty((B, H, T, w3.d_v), dtype=torch.float32, device=dev)
+    outs = {n: torch.empty((B, H, T, w3.topk), dtype=dt, device=dev)
+            for n, dt in (("r_idx", torch.int32), ("r_val", torch.float32),
+                          ("w_idx", torch.int32), ("w_val", torch.float32))}
+
+    def step():
+        sdm.forward(q, k, cb, cb, v, al, be, mem, w3.N, w3.topk, workspace=ws, y=y, out=outs)
+
+    sdm.mem_init(mem, m0)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"learned M0: timing {args.steps} forward steps")
+    sdm.profile_select(["fwd_scan"])
+    sdm.profile_enable(True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    t_scan, n_scan = sdm.profile_read("fwd_scan")
+    sdm.profile_enable(False)
+    sdm.profile_select(None)
+    sdm.profile_enable(True)
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    kms = {n: round(sdm.profile_read(n)[0] / 2, 4) for n in ("address", "fwd_prep", "fwd_scan")}
+    sdm.profile_enable(False)
+    n_scan = max(n_scan, 1)
+    scan_ms = t_scan / n_scan
+    unit = fwd_scan_bytes_per_token_head(w3.topk, w3.topk, w3.d_v, 2)
+    launch_bytes = round(unit * B * H * T * args.steps / n_scan)
+    ach = launch_bytes / (scan_ms * 1e-3) / 1e9
+    res["learned_m0"] = {
+        "workload": f"learned initial memory: B={B} H={H} T={T} d_k=d_v={w3.d_v} N={w3.N} top-{w3.topk}, "
+                    "bf16 inputs, fp32 memory (16 GiB); one sdm_forward call per step (library stages), "
+                    "the M0 broadcast excluded (under mem_init)",
+        "value": round(B * T / (ms * 1e-3), 1), "unit": "tokens/s", "ms_per_step": round(ms, 4),
+        "kernels_ms_per_step": kms,
+        "roofline": {"bound": "hbm", "kernel": "fwd_scan", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                     "algorithmic_bytes_per_token_head": unit, "algorithmic_bytes_per_launch": launch_bytes,
+                     "kernel_ms": round(scan_ms, 4), "launches_per_step": round(n_scan / args.steps, 2)}}
+    del q, k, v, al, be, cb, m0, mem, ws, y, outs
+    torch.cuda.empty_cache()
+    return res
 
 
 def paper_layer(sdm, to_dev, wp, tag, root, stream, dev):
