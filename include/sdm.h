@@ -20,8 +20,9 @@
  *     any error nothing is launched, no output is touched, the call returns a
  *     negative status and sdm_last_error() (thread-local) describes it.  No
  *     entry point prints, throws or aborts.
- *   - Process-wide state: three geometry switches (sdm_set_scan_slice_width,
- *     sdm_set_scan_line_io, sdm_set_chunk_scan_cols) choose which scan kernel
+ *   - Process-wide state: four geometry switches (sdm_set_scan_slice_width,
+ *     sdm_set_scan_line_io, sdm_set_scan_prefetch, sdm_set_chunk_scan_cols)
+ *     choose which scan kernel
  *     a later launch runs and so the rounding order of its sums over rows;
  *     the event profiler (sdm_profile_*); and, per device, a second stream
  *     created on first use by the pipelined calls (sdm_forward with more than
@@ -415,6 +416,21 @@ int sdm_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int d_v, 
  * value returns SDM_ERR_INVALID_ARG and keeps the setting.
  * ---------------------------------------------------------------------- */
 int sdm_set_scan_slice_width(int sw);
+
+/* ------------------------------------------------------------------------
+ * Forward prefetch depth: tokens whose table rows are in flight while one is
+ * computed (the prep kernel links rows written within that window to an LDS
+ * ring).  sdm_set_scan_prefetch(pd):
+ *   0   automatic (default): 4, except 16 (8 where LDS does not allow 16) for
+ *       the line-cooperative forward kernel when its launch has fewer waves
+ *       than the device has SIMDs (few streams: each stream's step time is
+ *       then set by the row loads' latency over the tokens in flight);
+ *   4, 8, 16  force that depth for the line-cooperative kernel (the per-wave
+ *       kernel always takes 4).
+ * Results do not depend on it.  Process-wide; applies to launches that start
+ * after the call.  Any other value returns SDM_ERR_INVALID_ARG.
+ * ---------------------------------------------------------------------- */
+int sdm_set_scan_prefetch(int pd);
 
 /* ------------------------------------------------------------------------
  * Table I/O of the scans.  By default each scan runs a four-wave

@@ -18,9 +18,11 @@
 namespace {
 std::atomic<int> g_slice_width{0};
 std::atomic<int> g_line_io{1};
+std::atomic<int> g_prefetch{0};
 }
 
 int sdm_scan_slice_width() { return g_slice_width.load(std::memory_order_relaxed); }
+int sdm_scan_prefetch() { return g_prefetch.load(std::memory_order_relaxed); }
 std::atomic<int> g_chunk_cols{0};
 int sdm_chunk_cols() { return g_chunk_cols.load(std::memory_order_relaxed); }
 bool sdm_line_io_enabled() { return g_line_io.load(std::memory_order_relaxed) != 0; }
@@ -258,6 +260,14 @@ int sdm_set_scan_slice_width(int sw) {
     if (sw != 0 && sw != 8 && sw != 16)
         return fail(SDM_ERR_INVALID_ARG, "sdm_set_scan_slice_width: width must be 0 (automatic), 8 or 16, got %d", sw);
     g_slice_width.store(sw, std::memory_order_relaxed);
+    return SDM_OK;
+}
+
+int sdm_set_scan_prefetch(int pd) {
+    g_err[0] = 0;
+    if (pd != 0 && pd != 4 && pd != 8 && pd != 16)
+        return fail(SDM_ERR_INVALID_ARG, "sdm_set_scan_prefetch: depth must be 0 (automatic), 4, 8 or 16, got %d", pd);
+    g_prefetch.store(pd, std::memory_order_relaxed);
     return SDM_OK;
 }
 

@@ -596,43 +596,52 @@ bool fwd_plan(int S, int W, int R, int dv, int in_dtype, FwdPlan* p) {
 }
 
 // LDS of the line-cooperative forward kernel (shared part, per-wave part).
-template <int SW, int FR>
+template <int SW, int FR, int PD>
 size_t fline_lds(bool save, int in_dtype, size_t* per_wave) {
-    constexpr int NS = stage_slots<FWD_PD>();
+    constexpr int NS = stage_slots<PD>();
     const int vbytes = in_dtype == SDM_DT_BF16 ? 2 : 4;
-    *per_wave = (size_t)NS * SW * vbytes + (size_t)FWD_PD * FR * SW * 4;
+    *per_wave = (size_t)NS * SW * vbytes + (size_t)PD * FR * SW * 4;
     return (size_t)fline_shared_bytes<SW, FR>(save, NS, fwd_rec_layout(FR, FR).bytes) + FLW * *per_wave;
 }
 
 // The line-cooperative kernel's shape: W = R = FR, d_v a multiple of 4 SW
 // (whole workgroups), and its LDS within the limit (at 64 rows, 16 columns
 // and the undo log: 155 KB).
-template <int SW, int FR>
+template <int SW, int FR, int PD>
 bool fline_ok(const ScanFwdArgs& a, const FwdPlan& p, bool save, size_t* lds, size_t* per_wave) {
     if (!sdm_line_io_enabled() || a.W != FR || a.R != FR || a.dv % (FLW * SW) != 0 || p.n_slices % FLW != 0)
         return false;
-    *lds = fline_lds<SW, FR>(save, a.in_dtype, per_wave);
+    *lds = fline_lds<SW, FR, PD>(save, a.in_dtype, per_wave);
     return *lds <= (size_t)LDS_LIMIT;
 }
 
+template <typename VT, int SW, bool SAVE, int FR, int PD>
+hipError_t launch_fline(const ScanFwdArgs& a, const FwdPlan& p, size_t lds, size_t per_wave, hipStream_t st) {
+    auto kl = scan_fwd_line_kernel<VT, SW, PD, SAVE, FR>;
+    hipError_t e = hipFuncSetAttribute((const void*)kl, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kl, dim3(p.n_slices / FLW * (a.B * a.H)), dim3(FLW * SDM_WAVE), lds, st,
+                       a.ws + SDM_WS_HEADER, static_cast<const VT*>(a.v), a.mem, a.y, a.saved, a.T, a.tb, a.te,
+                       a.dv, a.N, p.n_slices, (int)per_wave);
+    return hipGetLastError();
+}
+
 template <typename VT, int SW, int K, bool SAVE>
-hipError_t launch_fwd_k(const ScanFwdArgs& a, const FwdPlan& p, hipStream_t st) {
+hipError_t launch_fwd_k(const ScanFwdArgs& a, const FwdPlan& p, int pd, hipStream_t st) {
     constexpr int NR = nr_for_k<SW>(K);
     const int S = a.B * a.H;
     size_t lds = 0, per_wave = 0;
     constexpr int FR = K * (SDM_WAVE / (SW / 4));   // rows the plan's K passes hold
     if constexpr (FR == 32 || FR == 64) {
-        if (fline_ok<SW, FR>(a, p, SAVE, &lds, &per_wave)) {
-            auto kl = scan_fwd_line_kernel<VT, SW, FWD_PD, SAVE, FR>;
-            hipError_t e =
-                hipFuncSetAttribute((const void*)kl, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-            if (e != hipSuccess) return e;
-            hipLaunchKernelGGL(kl, dim3(p.n_slices / FLW * S), dim3(FLW * SDM_WAVE), lds, st,
-                               a.ws + SDM_WS_HEADER, static_cast<const VT*>(a.v), a.mem, a.y, a.saved, a.T,
-                               a.tb, a.te, a.dv, a.N, p.n_slices, (int)per_wave);
-            return hipGetLastError();
-        }
+        // the prefetch depth was chosen with the same plan (sdm_fwd_pd), so its LDS fits
+        if (pd == 16 && fline_ok<SW, FR, 16>(a, p, SAVE, &lds, &per_wave))
+            return launch_fline<VT, SW, SAVE, FR, 16>(a, p, lds, per_wave, st);
+        if (pd == 8 && fline_ok<SW, FR, 8>(a, p, SAVE, &lds, &per_wave))
+            return launch_fline<VT, SW, SAVE, FR, 8>(a, p, lds, per_wave, st);
+        if (pd == FWD_PD && fline_ok<SW, FR, FWD_PD>(a, p, SAVE, &lds, &per_wave))
+            return launch_fline<VT, SW, SAVE, FR, FWD_PD>(a, p, lds, per_wave, st);
     }
+    if (pd != FWD_PD) return hipErrorInvalidConfiguration;   // the per-wave kernel links over FWD_PD tokens
     dim3 grid((p.n_slices + p.wpb - 1) / p.wpb * S);   // order: scan_wg_coords
     const size_t sm = (size_t)p.lds_per_wave * p.wpb;
     auto kfn = scan_fwd_kernel<VT, SW, FWD_PD, K, NR, SAVE>;
@@ -645,18 +654,50 @@ hipError_t launch_fwd_k(const ScanFwdArgs& a, const FwdPlan& p, hipStream_t st) 
 }
 
 template <typename VT, bool SAVE>
-hipError_t launch_fwd_kk(const ScanFwdArgs& a, const FwdPlan& p, hipStream_t st) {
+hipError_t launch_fwd_kk(const ScanFwdArgs& a, const FwdPlan& p, int pd, hipStream_t st) {
     if (p.SW == 8) {
-        if (p.K == 1) return launch_fwd_k<VT, 8, 1, SAVE>(a, p, st);
-        if (p.K == 2) return launch_fwd_k<VT, 8, 2, SAVE>(a, p, st);
-        return launch_fwd_k<VT, 8, 4, SAVE>(a, p, st);
+        if (p.K == 1) return launch_fwd_k<VT, 8, 1, SAVE>(a, p, pd, st);
+        if (p.K == 2) return launch_fwd_k<VT, 8, 2, SAVE>(a, p, pd, st);
+        return launch_fwd_k<VT, 8, 4, SAVE>(a, p, pd, st);
     }
-    if (p.K == 1) return launch_fwd_k<VT, 16, 1, SAVE>(a, p, st);
-    if (p.K == 2) return launch_fwd_k<VT, 16, 2, SAVE>(a, p, st);
-    return launch_fwd_k<VT, 16, 4, SAVE>(a, p, st);
+    if (p.K == 1) return launch_fwd_k<VT, 16, 1, SAVE>(a, p, pd, st);
+    if (p.K == 2) return launch_fwd_k<VT, 16, 2, SAVE>(a, p, pd, st);
+    return launch_fwd_k<VT, 16, 4, SAVE>(a, p, pd, st);
+}
+
+// Whether the line kernel of this plan can run at prefetch depth PD.
+template <int PD>
+bool fline_fits(const ScanFwdArgs& a, const FwdPlan& p) {
+    size_t lds, pw;
+    const bool save = a.saved != nullptr;
+    if (p.SW == 8) {
+        if (a.W == 32) return fline_ok<8, 32, PD>(a, p, save, &lds, &pw);
+        if (a.W == 64) return fline_ok<8, 64, PD>(a, p, save, &lds, &pw);
+    } else {
+        if (a.W == 32) return fline_ok<16, 32, PD>(a, p, save, &lds, &pw);
+        if (a.W == 64) return fline_ok<16, 64, PD>(a, p, save, &lds, &pw);
+    }
+    return false;
 }
 
 }  // namespace
+
+// Prefetch depth of the forward scan for these arguments (the prep kernel
+// links over the same window).  Four tokens, unless the line-cooperative
+// kernel runs with fewer waves than the device has SIMDs: then each stream's
+// step time is set by the latency of its row loads over the tokens in flight,
+// and a deeper window (16, else 8, as LDS allows) keeps more rows in flight.
+int sdm_fwd_pd(const ScanFwdArgs& a) {
+    FwdPlan p;
+    if (!fwd_plan(a.B * a.H, a.W, a.R, a.dv, a.in_dtype, &p)) return FWD_PD;
+    if (!fline_fits<FWD_PD>(a, p)) return FWD_PD;   // per-wave kernel
+    const int forced = sdm_scan_prefetch();
+    const int want = forced ? forced
+                            : ((int64_t)a.B * a.H * p.n_slices < sdm_device_simds() ? SDM_FWD_PD_DEEP : FWD_PD);
+    if (want >= 16 && fline_fits<16>(a, p)) return 16;
+    if (want >= 8 && fline_fits<8>(a, p)) return 8;
+    return FWD_PD;
+}
 
 size_t sdm_fwd_ws_bytes(int B, int H, int T, int W, int R) {
     return SDM_WS_HEADER + (size_t)B * H * T * fwd_rec_layout(W, R).bytes;
@@ -669,17 +710,22 @@ bool sdm_fwd_plan_ok(int W, int R, int dv, int in_dtype) {
 
 hipError_t sdm_launch_fwd_prep_range(const ScanFwdArgs& a, hipStream_t st) {
     SdmProfScope ps(SDM_K_FWD_PREP, st);
-    return sdm_launch_fwd_prep<FWD_PD>(a, st);
+    switch (sdm_fwd_pd(a)) {
+        case 16: return sdm_launch_fwd_prep<16>(a, st);
+        case 8: return sdm_launch_fwd_prep<8>(a, st);
+        default: return sdm_launch_fwd_prep<FWD_PD>(a, st);
+    }
 }
 
 hipError_t sdm_launch_fwd_scan_range(const ScanFwdArgs& a, hipStream_t st) {
     FwdPlan p;
     if (!fwd_plan(a.B * a.H, a.W, a.R, a.dv, a.in_dtype, &p)) return hipErrorInvalidConfiguration;
     const bool save = a.saved != nullptr;
+    const int pd = sdm_fwd_pd(a);
     SdmProfScope ps(SDM_K_FWD_SCAN, st);
     if (a.in_dtype == SDM_DT_BF16)
-        return save ? launch_fwd_kk<bf16_t, true>(a, p, st) : launch_fwd_kk<bf16_t, false>(a, p, st);
-    return save ? launch_fwd_kk<float, true>(a, p, st) : launch_fwd_kk<float, false>(a, p, st);
+        return save ? launch_fwd_kk<bf16_t, true>(a, p, pd, st) : launch_fwd_kk<bf16_t, false>(a, p, pd, st);
+    return save ? launch_fwd_kk<float, true>(a, p, pd, st) : launch_fwd_kk<float, false>(a, p, pd, st);
 }
 
 hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st) {

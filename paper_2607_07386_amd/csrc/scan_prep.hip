@@ -335,5 +335,7 @@ hipError_t sdm_launch_check_ids(const int32_t* w_idx, int W, const int32_t* r_id
 }
 
 template hipError_t sdm_launch_fwd_prep<SDM_FWD_PD>(const ScanFwdArgs&, hipStream_t);
+template hipError_t sdm_launch_fwd_prep<8>(const ScanFwdArgs&, hipStream_t);
+template hipError_t sdm_launch_fwd_prep<16>(const ScanFwdArgs&, hipStream_t);
 template hipError_t sdm_launch_bwd_prep<SDM_BWD_PD>(const ScanBwdArgs&, hipStream_t);
 template hipError_t sdm_launch_bwd_prep<2>(const ScanBwdArgs&, hipStream_t);

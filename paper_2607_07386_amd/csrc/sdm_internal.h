@@ -11,6 +11,8 @@
 // the prep kernels compute read-after-write links for exactly this window.
 #define SDM_FWD_PD 4
 #define SDM_BWD_PD 4
+// Deeper forward window for launches with fewer waves than SIMDs (latency-bound).
+#define SDM_FWD_PD_DEEP 16
 
 // Per-token record of the forward scan (written by the prep kernel, staged in
 // LDS by the scan): slots and weights of both sides, forwarding links, gates.
@@ -89,7 +91,7 @@ struct ScanFwdArgs {
     float* y;
     float* saved;
     unsigned char* ws;   // workspace base (header + records)
-    int tb = 0, te = 0;  // tokens processed: [tb, te) (layout strides use T); tb a multiple of SDM_FWD_PD
+    int tb = 0, te = 0;  // tokens processed: [tb, te) (layout strides use T); tb a multiple of 16
     // Gate producers fused into the records: with gate_A set, alpha and beta hold the
     // gates' pre-activations and alpha = exp(-A softplus(a + b_dt)), beta = sigma(b)
     // are formed per token (A, b_dt per head, fp32).
@@ -104,6 +106,11 @@ hipError_t sdm_launch_fwd_scan_range(const ScanFwdArgs& a, hipStream_t st);
 int sdm_device_simds();
 // Forced scan slice width (8 or 16), or 0 for the automatic choice.
 int sdm_scan_slice_width();
+// Forced forward prefetch depth (4, 8 or 16), or 0 for the automatic choice.
+int sdm_scan_prefetch();
+// Prefetch depth (tokens in flight) of the forward scan for these arguments;
+// the prep kernel links over the same window.
+int sdm_fwd_pd(const ScanFwdArgs& a);
 // Whether the scans may use their line-cooperative kernels (default: yes).
 bool sdm_line_io_enabled();
 // true if the forward scan has a launch plan for this shape (registers, LDS)

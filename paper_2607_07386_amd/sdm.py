@@ -80,6 +80,7 @@ def lib() -> ctypes.CDLL:
         L.sdm_set_scan_slice_width.argtypes = [I]
         L.sdm_set_scan_line_io.argtypes = [I]
         L.sdm_set_chunk_scan_cols.argtypes = [I]
+        L.sdm_set_scan_prefetch.argtypes = [I]
         L.sdm_profile_read.argtypes = [I, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]
         L.sdm_status_string.argtypes = [I]
         L.sdm_status_string.restype = ctypes.c_char_p
@@ -615,6 +616,11 @@ def set_chunk_scan_cols(cols: int):
 def set_scan_slice_width(sw: int):
     """Columns per scan wave: 0 automatic, or force 8 / 16 (process-wide)."""
     _check("sdm_set_scan_slice_width", lib().sdm_set_scan_slice_width(int(sw)))
+
+
+def set_scan_prefetch(pd: int):
+    """Forward scan prefetch depth: 0 automatic, or force 4 / 8 / 16 (process-wide)."""
+    _check("sdm_set_scan_prefetch", lib().sdm_set_scan_prefetch(int(pd)))
 
 
 def set_scan_line_io(on: bool):

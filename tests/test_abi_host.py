@@ -145,6 +145,14 @@ def test_slice_width_setting():
         assert b"width" in L.sdm_last_error()
 
 
+def test_scan_prefetch_setting():
+    for pd in (4, 8, 16, 0):
+        assert L.sdm_set_scan_prefetch(pd) == 0
+    for pd in (-1, 2, 12, 32):
+        assert L.sdm_set_scan_prefetch(pd) == -1
+        assert b"depth" in L.sdm_last_error()
+
+
 def test_chunk_scan_cols_setting():
     for c in (16, 32, 0):
         assert L.sdm_set_chunk_scan_cols(c) == 0

@@ -199,6 +199,29 @@ def test_forward_line_io(name, save, slice_width):
         assert rel_err(np_(g[k]), np_(gw[k]).astype(np.float64)) <= 1e-5, k
 
 
+@pytest.mark.parametrize("name", ["bf16-fline-ragged", "f32-fline-direct", "bf16-fline64-ragged"])
+def test_forward_prefetch_depths(name):
+    """The line-cooperative forward at prefetch depths 4, 8 and 16 (how many
+    tokens' rows are in flight; rows written inside the window come from the
+    LDS ring): against the oracle, and bit for bit the same at every depth."""
+    w = FLINE[name]
+    inp = synth.Inputs(w)
+    streams = list(range(w.B * w.H))
+    outs = {}
+    try:
+        for pd in (4, 8, 16):
+            sdm.set_scan_prefetch(pd)
+            g = gpu_forward(w, inp, save=True, chunk=64)
+            o = oracle_scan_rows(w, inp, g, streams, m0_fn(w, inp))
+            check_scan(w, g, o, streams, f"{name}/pd{pd}/fline")
+            outs[pd] = {k: np_(g[k]) for k in ("y", "mem", "saved")}
+    finally:
+        sdm.set_scan_prefetch(0)
+    for pd in (8, 16):
+        for k in outs[4]:
+            assert np.array_equal(outs[pd][k], outs[4][k]), (pd, k)
+
+
 def test_empty_sequence_is_noop():
     w = synth.Workload("t", B=1, H=1, T=0, d_k=32, d_v=32, N=256, topk=8)
     dev = DEV
@@ -685,6 +708,39 @@ def _links_bwd(wi, ri, PD, stage_end=None):
         for n in range(W):
             lgw[t, n] = g_source(t, wi[t, n], True)
     return np.concatenate([lm, lgr, lgw], 1)
+
+
+@pytest.mark.parametrize("pd", [8, 16])
+def test_prep_links_deep_window(pd):
+    """Forward links over a window of 8 or 16 tokens (the line-cooperative
+    kernel's deeper prefetch) equal a brute-force search; rows recur within
+    the window (32 of 40 slots written per token)."""
+    rng = np.random.default_rng(91 + pd)
+    S, T, N, W, dv = 2, 150, 40, 32, 32
+    wi = np.stack([np.stack([np.sort(rng.choice(N, W, replace=False)) for _ in range(T)]) for _ in range(S)])
+    ri = np.stack([np.stack([np.sort(rng.choice(N, W, replace=False)) for _ in range(T)]) for _ in range(S)])
+    wi, ri = wi.astype(np.int32), ri.astype(np.int32)
+    t_ = lambda a: torch.from_numpy(np.ascontiguousarray(a))[:, None].to(DEV)
+    wv = t_((rng.random((S, T, W)) * 2 / np.sqrt(W)).astype(np.float32))
+    rv = t_(rng.random((S, T, W)).astype(np.float32))
+    v = t_(rng.standard_normal((S, T, dv)).astype(np.float32))
+    g = t_(rng.uniform(0.1, 1.0, (S, T)).astype(np.float32))
+    mem = torch.zeros((S, 1, N, dv), device=DEV)
+    ws = sdm.fwd_workspace(S, 1, T, W, W, DEV)
+    sdm.set_scan_prefetch(pd)
+    try:
+        y = sdm.scan_fwd(t_(wi), wv, t_(ri), rv, v, g, g, mem, workspace=ws)
+        torch.cuda.synchronize()
+    finally:
+        sdm.set_scan_prefetch(0)
+    off_link, _, rec = _rec_fwd(W, W)
+    raw = np_(ws)[256:256 + S * T * rec].reshape(S, T, rec)
+    got = raw[:, :, off_link:off_link + 2 * (2 * W)].copy().view(np.int16).astype(np.int64)
+    for s_ in range(S):
+        np.testing.assert_array_equal(got[s_], _links_fwd(wi[s_], ri[s_], pd))
+    memo = np.zeros((S, N, dv))
+    yo = oracle.scan_fwd(wi, np_(wv)[:, 0], ri, np_(rv)[:, 0], np_(v)[:, 0], np_(g)[:, 0], np_(g)[:, 0], memo)
+    assert rel_err(np_(y)[:, 0], yo) <= 1e-5 and rel_err(np_(mem)[:, 0], memo) <= 1e-5
 
 
 @pytest.mark.parametrize("sorted_lists", [True, False])
