@@ -207,13 +207,14 @@ size_t sdm_forward_noalloc_max_bytes(void);
  * a triangular product QK x; each slot written in the chunk is then stored
  * once.  The first kernel (all chunks in parallel) builds per-chunk
  * coefficients from the slot lists and gates alone; the second walks the
- * chunks of each stream in order, one workgroup per 32 columns (see
+ * chunks of each stream in order, one workgroup per 8 or 32 columns (see
  * sdm_set_chunk_scan_cols).  With 32 or more chunks both run over 8 chunk
  * ranges, the coefficients of the next range on the library's second stream
  * (as sdm_forward's) beside the scan of the current one; all work is ordered
  * before later work on `stream` when the call returns.  Results equal
  * sdm_scan_fwd's up to the rounding of the reassociated sums and of the
- * triangular solve.
+ * triangular solve (and may vary in the last bits between runs: see
+ * sdm_set_chunk_scan_cols).
  *   Arguments as for sdm_scan_fwd, without the undo log; workspace of at least
  *   sdm_scan_fwd_chunked_workspace_bytes() bytes (256-B aligned), which holds
  *   about (8 C^2 + 8 C (W + R) + 16 C W) bytes per stream and chunk (C = 64).
@@ -227,10 +228,14 @@ int sdm_scan_fwd_chunked(const int32_t* w_idx, const float* w_val, int W,
                          float* mem, int B, int H, int T, int d_v, int64_t N,
                          float* y, void* workspace, size_t ws_bytes, void* stream);
 size_t sdm_scan_fwd_chunked_workspace_bytes(int B, int H, int T, int W, int R);
-/* Columns per workgroup of sdm_scan_fwd_chunked's scan kernel: 32 (a 128-byte
- * piece of every row), 16 (twice the workgroups), or 0 (default), which takes
- * 32.  Process-wide; any other value returns SDM_ERR_INVALID_ARG and keeps the
- * setting. */
+/* Columns per workgroup of sdm_scan_fwd_chunked's scan kernel: 8 (the narrow
+ * kernel: 16 workgroups per 128-column stream, which fill the chip at few
+ * streams; needs d_v % 8 == 0), 16 or 32 (a 128-byte piece of every row), or
+ * 0 (the default), which takes 32.
+ * Process-wide; any other value returns SDM_ERR_INVALID_ARG and keeps the
+ * setting.  The coefficient kernel adds the pair terms of its triangular
+ * system with LDS atomics, so results may differ from run to run in the last
+ * bits (a GPU test bounds the spread at 1e-6 relative). */
 int sdm_set_chunk_scan_cols(int cols);
 
 /* ------------------------------------------------------------------------

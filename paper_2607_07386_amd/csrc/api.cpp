@@ -273,8 +273,8 @@ int sdm_set_scan_prefetch(int pd) {
 
 int sdm_set_chunk_scan_cols(int cols) {
     g_err[0] = 0;
-    if (cols != 0 && cols != 16 && cols != 32)
-        return fail(SDM_ERR_INVALID_ARG, "sdm_set_chunk_scan_cols: expected 0 (automatic), 16 or 32, got %d", cols);
+    if (cols != 0 && cols != 8 && cols != 16 && cols != 32)
+        return fail(SDM_ERR_INVALID_ARG, "sdm_set_chunk_scan_cols: expected 0 (automatic), 8, 16 or 32, got %d", cols);
     g_chunk_cols.store(cols, std::memory_order_relaxed);
     return SDM_OK;
 }

@@ -42,10 +42,13 @@ constexpr int CK_LDS_LIMIT = 160 * 1024;
 
 // Per-chunk record: nseg, then L and QK [C][C], the gather weights
 // exp(lambda) kappa [C][W] and exp(lambda) rho [C][R], then per written slot
-// (sorted by id) its first entry, id and decay exp(lambda_C), and per entry
-// (sorted by slot, then token) its token and scatter weight.
+// (sorted by id) its first entry, id and decay exp(lambda_C), per entry
+// (sorted by slot, then token) its token and scatter weight, and per written
+// slot its first entry as (token W + list position), bit 30 set when the slot
+// has further entries, with that entry's scatter weight.
 struct ChunkRec {
-    int off_l, off_qk, off_cr, off_cy, off_sbeg, off_sslot, off_sdec, off_etok, off_ecoef, bytes;
+    int off_l, off_qk, off_cr, off_cy, off_sbeg, off_sslot, off_sdec, off_etok, off_ecoef, off_sfirst, off_sfcoef,
+        bytes;
 };
 
 __host__ __device__ inline ChunkRec chunk_rec_layout(int W, int R) {
@@ -62,6 +65,8 @@ __host__ __device__ inline ChunkRec chunk_rec_layout(int W, int R) {
     r.off_sdec = o;  o += E * 4;
     r.off_etok = o;  o += E * 4;
     r.off_ecoef = o; o += E * 4;
+    r.off_sfirst = o; o += E * 4;
+    r.off_sfcoef = o; o += E * 4;
     r.bytes = (o + 255) & ~255;
     return r;
 }
@@ -114,6 +119,8 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
     int* g_sslot = reinterpret_cast<int*>(rec + L.off_sslot);
     float* g_sdec = reinterpret_cast<float*>(rec + L.off_sdec);
     int* g_etok = reinterpret_cast<int*>(rec + L.off_etok);
+    int* g_sfirst = reinterpret_cast<int*>(rec + L.off_sfirst);
+    float* g_sfcoef = reinterpret_cast<float*>(rec + L.off_sfcoef);
     float* g_ecoef = reinterpret_cast<float*>(rec + L.off_ecoef);
 
     unsigned int bad = 0;
@@ -199,6 +206,9 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
             g_sbeg[g] = e;
             g_sslot[g] = (int)key_slot(keys[e]);
             g_sdec[g] = expf(lams[f]);
+            const int ft = key_tok(keys[e]), fn = key_ent(keys[e]);
+            g_sfirst[g] = (ft * W + fn) | (f > e ? (1 << 30) : 0);
+            g_sfcoef[g] = kap[ft * W + fn] * expf(lams[f] - lams[e]);   // = the entry's scatter weight
             ++g;
         }
         if (tid == CT1 - 1) {
@@ -500,6 +510,196 @@ __global__ __launch_bounds__(scan_threads<COLS>()) void chunk_scan_kernel(const 
     }
 }
 
+// ---------------------------------------------------------------------------
+// Narrow variant for few streams: one workgroup per (stream, 8-column slice),
+// 512 threads, so a stream of d_v = 128 takes 16 workgroups and the chip fills
+// at 16 streams.  The 16 workgroups of a stream are placed on one XCD (ids
+// congruent mod 8) and read the chunk's record through its L2.  Per chunk:
+//   staging   slot ids and gather weights straight to registers (each thread
+//             its token's rows of its part), L and QK to LDS, v, and the
+//             scatter lists' heads of this thread's segments;
+//   gather    thread (token, part p, quad q) loads rows [NPR p, NPR (p + 1))
+//             of its token, NPR pieces of 16 bytes in flight, and sums them
+//             with their weights; the 4 parts add in LDS;
+//   products  thread (token, column): R = v - retrieved, x = L R, y = inter + QK x;
+//   scatter   thread holds SBN (segment, quad) units: one load each, one store.
+// Every load of a round is issued before its first use, so a chunk costs one
+// dependent memory round trip per phase.
+constexpr int NCOL = 8;                 // columns per workgroup
+constexpr int NT3 = 512;                // threads
+constexpr int NPART = 4;                // row parts per (token, quad) in the gather
+constexpr int SB3 = 8;                  // scatter units in flight per thread
+
+template <typename VT, int NPR, int SBN, bool REUSE>
+__global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
+    const int32_t* __restrict__ w_idx, const int32_t* __restrict__ r_idx, const VT* __restrict__ v,
+    float* __restrict__ mem, float* __restrict__ y, const unsigned char* __restrict__ recs, int T, int W, int R,
+    int64_t N, int dv, int nch, int cb, int ce, int nslice) {
+    __shared__ float Ls[CC * LDP];
+    __shared__ float Qs[CC * LDP];
+    __shared__ __align__(16) float Pret[NPART * CC * NCOL];
+    __shared__ __align__(16) float Pint[NPART * CC * NCOL];
+    __shared__ __align__(16) float Rr[CC * NCOL];
+    __shared__ __align__(16) float Xs[CC * NCOL];
+    // REUSE: the gathered write rows [C][W][NCOL], the chunk-start rows the scatter decays
+    extern __shared__ __align__(16) float Wrow[];
+    const ChunkRec L = chunk_rec_layout(W, R);
+    const int WR = W + R;
+    const int tid = threadIdx.x;
+    int sl, s;
+    scan_wg_coords<true>(nslice, sl, s);
+    // gather mapping
+    const int gt = tid >> 3, gp = (tid >> 1) & 3, gq = tid & 1;
+    // product mapping
+    const int pt = tid >> 3, pc = tid & 7;
+    const int col0 = sl * NCOL;
+    float* ms = mem + (size_t)s * N * dv + col0;
+
+    for (int c = cb; c < ce; ++c) {
+        const unsigned char* rec = recs + ((size_t)s * nch + c) * L.bytes;
+        const int t0 = c * CC, n = min(CC, T - t0);
+        const size_t tk0 = (size_t)s * T + t0;
+        const int nseg = *reinterpret_cast<const int*>(rec);
+        const int* g_sbeg = reinterpret_cast<const int*>(rec + L.off_sbeg);
+        const int* g_sslot = reinterpret_cast<const int*>(rec + L.off_sslot);
+        const float* g_sdec = reinterpret_cast<const float*>(rec + L.off_sdec);
+        const int* g_etok = reinterpret_cast<const int*>(rec + L.off_etok);
+        const float* g_ecoef = reinterpret_cast<const float*>(rec + L.off_ecoef);
+        const int* g_sfirst = reinterpret_cast<const int*>(rec + L.off_sfirst);
+        const float* g_sfcoef = reinterpret_cast<const float*>(rec + L.off_sfcoef);
+        const float* g_cr = reinterpret_cast<const float*>(rec + L.off_cr);
+        const float* g_cy = reinterpret_cast<const float*>(rec + L.off_cy);
+        // ---- staging: every load of the phase first ----
+        const int tg = min(gt, n - 1);            // past the chunk's tokens: token n - 1 (unused)
+        int id[NPR];
+        float wt[NPR];
+#pragma unroll
+        for (int k = 0; k < NPR; ++k) {
+            const int j = gp * NPR + k;
+            const bool wr = j < W;
+            const int jr = wr ? j : min(j - W, R - 1);
+            int64_t x = wr ? w_idx[(tk0 + tg) * W + j] : r_idx[(tk0 + tg) * R + jr];
+            id[k] = (int)(x < 0 ? 0 : (x >= N ? N - 1 : x));
+            wt[k] = j < WR ? (wr ? g_cr[tg * W + j] : g_cy[tg * R + jr]) : 0.f;
+        }
+        float4 la[CC * CC / 4 / NT3], qa[CC * CC / 4 / NT3];
+        {
+            const float4* gl = reinterpret_cast<const float4*>(rec + L.off_l);
+            const float4* gq4 = reinterpret_cast<const float4*>(rec + L.off_qk);
+#pragma unroll
+            for (int k = 0; k < CC * CC / 4 / NT3; ++k) {
+                la[k] = gl[tid + k * NT3];
+                qa[k] = gq4[tid + k * NT3];
+            }
+        }
+        const float vv = to_f32(v[(tk0 + min(pt, n - 1)) * dv + col0 + pc]);
+        int sg_slot[SBN], sg_first[SBN];
+        float sg_dec[SBN], sg_fc[SBN];
+#pragma unroll
+        for (int b = 0; b < SBN; ++b) {
+            const int g = min((tid + NT3 * b) >> 1, max(nseg - 1, 0));
+            sg_slot[b] = g_sslot[g];
+            sg_dec[b] = g_sdec[g];
+            sg_first[b] = g_sfirst[g];
+            sg_fc[b] = g_sfcoef[g];
+        }
+#pragma unroll
+        for (int k = 0; k < CC * CC / 4 / NT3; ++k) {
+            const int i = tid + k * NT3;
+            const int r = (4 * i) / CC, c4 = (4 * i) % CC;
+            float* lrow = Ls + r * LDP + c4;
+            float* qrow = Qs + r * LDP + c4;
+            lrow[0] = la[k].x; lrow[1] = la[k].y; lrow[2] = la[k].z; lrow[3] = la[k].w;
+            qrow[0] = qa[k].x; qrow[1] = qa[k].y; qrow[2] = qa[k].z; qrow[3] = qa[k].w;
+        }
+        // ---- gather: NPR row pieces in flight ----
+        float4 m[NPR];
+#pragma unroll
+        for (int k = 0; k < NPR; ++k) m[k] = load4(ms + (size_t)id[k] * dv + gq * 4);
+        if constexpr (REUSE) {   // write rows -> LDS for the scatter
+#pragma unroll
+            for (int k = 0; k < NPR; ++k) {
+                const int j = gp * NPR + k;
+                if (j < W) *reinterpret_cast<float4*>(&Wrow[(gt * W + j) * NCOL + gq * 4]) = m[k];
+            }
+        }
+        float4 ret = make_float4(0.f, 0.f, 0.f, 0.f), itr = make_float4(0.f, 0.f, 0.f, 0.f);
+        const bool live = gt < n;
+#pragma unroll
+        for (int k = 0; k < NPR; ++k) {
+            const int j = gp * NPR + k;
+            const float w = live ? wt[k] : 0.f;
+            if (j < W) {
+                ret.x += w * m[k].x; ret.y += w * m[k].y; ret.z += w * m[k].z; ret.w += w * m[k].w;
+            } else {
+                itr.x += w * m[k].x; itr.y += w * m[k].y; itr.z += w * m[k].z; itr.w += w * m[k].w;
+            }
+        }
+        *reinterpret_cast<float4*>(&Pret[(gp * CC + gt) * NCOL + gq * 4]) = ret;
+        *reinterpret_cast<float4*>(&Pint[(gp * CC + gt) * NCOL + gq * 4]) = itr;
+        __syncthreads();
+        // ---- R = v - retrieved; the reads' first term ----
+        float inter = 0.f, rsum = 0.f;
+#pragma unroll
+        for (int p = 0; p < NPART; ++p) {
+            rsum += Pret[(p * CC + pt) * NCOL + pc];
+            inter += Pint[(p * CC + pt) * NCOL + pc];
+        }
+        Rr[pt * NCOL + pc] = pt < n ? vv - rsum : 0.f;
+        __syncthreads();
+        // ---- x = L R (L is zero above the diagonal and past the chunk's tokens) ----
+        {
+            float acc = 0.f;
+#pragma unroll 16
+            for (int u = 0; u < CC; ++u) acc += Ls[pt * LDP + u] * Rr[u * NCOL + pc];
+            Xs[pt * NCOL + pc] = acc;
+        }
+        __syncthreads();
+        // ---- y = inter + QK x ----
+        {
+            float acc = inter;
+#pragma unroll 16
+            for (int u = 0; u < CC; ++u) acc += Qs[pt * LDP + u] * Xs[u * NCOL + pc];
+            if (pt < n) y[(tk0 + pt) * dv + col0 + pc] = acc;
+        }
+        // ---- scatter: each written slot once: its chunk-start row (from LDS when
+        //      REUSE, else reloaded, SB3 in flight), decayed, plus its entries' x ----
+#pragma unroll
+        for (int b0 = 0; b0 < SBN; b0 += SB3) {
+            float4 mm[SB3];
+#pragma unroll
+            for (int b = 0; b < SB3; ++b) {
+                const int q = (tid + NT3 * (b0 + b)) & 1;
+                const int fe = sg_first[b0 + b] & 0xffff;   // token W + position of the first entry
+                mm[b] = REUSE ? *reinterpret_cast<const float4*>(&Wrow[fe * NCOL + q * 4])
+                              : load4(ms + (size_t)sg_slot[b0 + b] * dv + q * 4);
+            }
+#pragma unroll
+            for (int b = 0; b < SB3; ++b) {
+                const int u = tid + NT3 * (b0 + b);
+                const int g = u >> 1, q = u & 1;
+                if (g < nseg) {
+                    const int fe = sg_first[b0 + b];
+                    const float d = sg_dec[b0 + b], w = sg_fc[b0 + b];
+                    const float4 x = *reinterpret_cast<const float4*>(&Xs[((fe & 0xffff) / W) * NCOL + q * 4]);
+                    float4 acc = make_float4(d * mm[b].x + w * x.x, d * mm[b].y + w * x.y, d * mm[b].z + w * x.z,
+                                             d * mm[b].w + w * x.w);
+                    if (fe & (1 << 30)) {   // further entries of the slot (rare)
+                        const int f1 = g_sbeg[g + 1];
+                        for (int f = g_sbeg[g] + 1; f < f1; ++f) {
+                            const float wf = g_ecoef[f];
+                            const float4 xf = *reinterpret_cast<const float4*>(&Xs[g_etok[f] * NCOL + q * 4]);
+                            acc.x += wf * xf.x; acc.y += wf * xf.y; acc.z += wf * xf.z; acc.w += wf * xf.w;
+                        }
+                    }
+                    *reinterpret_cast<float4*>(ms + (size_t)sg_slot[b0 + b] * dv + q * 4) = acc;
+                }
+            }
+        }
+        __syncthreads();   // the chunk's stores precede the next chunk's gathers
+    }
+}
+
 template <typename VT>
 hipError_t launch_chunk_coef(const ScanFwdArgs& a, hipStream_t st) {
     const int S = a.B * a.H, nch = (a.T + CC - 1) / CC;
@@ -539,12 +739,56 @@ hipError_t launch_chunk_scan_cols(const ScanFwdArgs& a, hipStream_t st) {
     return hipGetLastError();
 }
 
-// 32-column slices unless 16 are forced.  (At the long-context shape, 16
-// streams of 128 columns, 16-column slices double the workgroups and measured
-// slower: 41.0 against 35.2 ms.)
+template <typename VT, int NPR, int SBN, bool REUSE>
+hipError_t launch_chunk_narrow_t(const ScanFwdArgs& a, hipStream_t st) {
+    const int S = a.B * a.H, nch = (a.T + CC - 1) / CC;
+    const int cb = a.tb / CC, ce = (a.te + CC - 1) / CC;
+    if (ce <= cb) return hipSuccess;
+    const int nslice = a.dv / NCOL;
+    const size_t lds = REUSE ? (size_t)CC * a.W * NCOL * sizeof(float) : 0;
+    auto kl = chunk_scan_narrow_kernel<VT, NPR, SBN, REUSE>;
+    hipError_t e = hipFuncSetAttribute((const void*)kl, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kl, dim3((unsigned)(S * nslice)), dim3(NT3), lds, st, a.w_idx, a.r_idx,
+                       static_cast<const VT*>(a.v), a.mem, a.y, a.ws + SDM_WS_HEADER, a.T, a.W, a.R, a.N, a.dv, nch,
+                       cb, ce, nslice);
+    return hipGetLastError();
+}
+
+// Rows per part cover W + R; scatter units per thread cover 2 C W (one per
+// written slot and quad), in rounds of SB3.  Up to 32 write rows per token the
+// gathered rows stay in LDS (64 KB) for the scatter; past that it reloads them.
+template <typename VT>
+hipError_t launch_chunk_narrow(const ScanFwdArgs& a, hipStream_t st) {
+    const bool rows16 = a.W + a.R <= NPART * 16;
+    if (a.W <= 32) {
+        return rows16 ? launch_chunk_narrow_t<VT, 16, 8, true>(a, st) : launch_chunk_narrow_t<VT, 32, 8, true>(a, st);
+    }
+    return rows16 ? launch_chunk_narrow_t<VT, 16, 16, false>(a, st) : launch_chunk_narrow_t<VT, 32, 16, false>(a, st);
+}
+
+// Workgroup width: 32 columns unless sdm_set_chunk_scan_cols forces 8 (the
+// narrow kernel, d_v a multiple of 8) or 16.  Measured at the long-context
+// shape (16 streams of 128 columns): the narrow kernel's scan takes about
+// 22 ms alone, but its workgroups (117 KB of LDS each, one per CU) leave no
+// room for the next chunk range's coefficients beside it, so the whole call
+// took 32.9 ms against 32.5 ms with 32 columns; at 32 streams (learned-M0
+// shape) its 512 workgroups run in two waves: 8.1 against 5.5 ms.  16-column
+// workgroups of the wide kernel: 41.0 against 35.2 ms.
+int chunk_cols_for(const ScanFwdArgs& a) {
+    const int forced = sdm_chunk_cols();
+    if (forced == 8 && a.dv % NCOL == 0) return 8;
+    if (forced == 16) return 16;
+    return 32;
+}
+
 template <typename VT>
 hipError_t launch_chunk_scan(const ScanFwdArgs& a, hipStream_t st) {
-    return sdm_chunk_cols() == 16 ? launch_chunk_scan_cols<VT, 16>(a, st) : launch_chunk_scan_cols<VT, 32>(a, st);
+    switch (chunk_cols_for(a)) {
+        case 8: return launch_chunk_narrow<VT>(a, st);
+        case 16: return launch_chunk_scan_cols<VT, 16>(a, st);
+        default: return launch_chunk_scan_cols<VT, 32>(a, st);
+    }
 }
 
 }  // namespace

@@ -609,7 +609,7 @@ KERNELS = {"address": 0, "fwd_prep": 1, "fwd_scan": 2, "bwd_prep": 3, "bwd_scan"
 
 
 def set_chunk_scan_cols(cols: int):
-    """Columns per workgroup of the chunked scan: 16, 32, or 0 for the default (32)."""
+    """Columns per workgroup of the chunked scan: 8 (narrow kernel), 16, 32, or 0 for the default (32)."""
     _check("sdm_set_chunk_scan_cols", lib().sdm_set_chunk_scan_cols(int(cols)))
 
 

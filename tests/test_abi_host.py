@@ -154,9 +154,9 @@ def test_scan_prefetch_setting():
 
 
 def test_chunk_scan_cols_setting():
-    for c in (16, 32, 0):
+    for c in (8, 16, 32, 0):
         assert L.sdm_set_chunk_scan_cols(c) == 0
-    for c in (-1, 8, 24, 64):
+    for c in (-1, 4, 24, 64):
         assert L.sdm_set_chunk_scan_cols(c) == -1
         assert b"expected 0" in L.sdm_last_error()
 

@@ -7,7 +7,8 @@ writes, write sets with short periods, and a table of 16 rows where nearly every
 slot is written by several tokens of each chunk.  Workloads through the GPU
 addressing cover ragged chunks and slices, W != R, bf16 inputs and clustered
 keys.  The chunked form reassociates the sums over a chunk and solves its
-triangular system in fp32; the bar is the scans' relative error 1e-4."""
+triangular system in fp32; the bar is the 1e-5 regression bound (the fp32
+bar is 1e-4).  Every case runs at the three workgroup widths."""
 import numpy as np
 import pytest
 import torch
@@ -18,12 +19,15 @@ from tests.gpu_util import DEV, init_memory, rel_err, to_dev
 from paper_2607_07386_amd import sdm
 
 pytestmark = pytest.mark.gpu
-TOL = 1e-4
+# The spec bar for fp32 is 1e-4; held here to the 1e-5 regression bound
+# (measured errors are about 1e-7).
+TOL = 1e-5
 
 
-@pytest.fixture(autouse=True, params=[16, 32], ids=["cols16", "cols32"])
+@pytest.fixture(autouse=True, params=[8, 16, 32], ids=["cols8", "cols16", "cols32"])
 def chunk_cols(request):
-    """Every case at both scan-workgroup widths."""
+    """Every case at each scan-workgroup width: the narrow kernel (8 columns,
+    16 workgroups per 128-column stream) and the wide one at 16 and 32."""
     sdm.set_chunk_scan_cols(request.param)
     yield request.param
     sdm.set_chunk_scan_cols(0)
@@ -208,13 +212,33 @@ def test_chunked_ranges_overlap_coefficients():
     assert ey < TOL and em < TOL
 
 
+def test_chunked_repeat_spread():
+    """The coefficient kernel adds the pair terms of A and QK with LDS atomics,
+    so their rounding order, and the last bits of y and the table, may differ
+    from run to run.  Two runs on the same inputs: the spread is measured and
+    bounded (it stays at fp32 rounding)."""
+    w = WORKLOADS["bf16-clustered"]
+    inp = synth.Inputs(w)
+    q, k, v = to_dev(inp.q), to_dev(inp.k), to_dev(inp.v)
+    al, be, cb = to_dev(inp.alpha), to_dev(inp.beta), to_dev(inp.codebook)
+    r_idx, r_val = sdm.address(q, cb, w.N, w.topk)
+    w_idx, w_val = sdm.address(k, cb, w.N, w.topk)
+    outs = []
+    for _ in range(3):
+        mem = init_memory(w, inp)
+        y = sdm.scan_fwd_chunked(w_idx, w_val, r_idx, r_val, v, al, be, mem)
+        torch.cuda.synchronize()
+        outs.append((np_(y), np_(mem)))
+    spread = max(max(rel_err(o[0], outs[0][0]), rel_err(o[1], outs[0][1])) for o in outs[1:])
+    print(f"chunked/repeat spread: {spread:.2e}", flush=True)
+    assert spread <= 1e-6
+
+
 @pytest.mark.slow
 def test_chunked_full_long_context(chunk_cols):
-    """The long-context workload at full size (16 streams x 65536 tokens, clustered keys) in the
-    launch configuration the bench times (32 columns, 8 chunk ranges); one sampled stream against
-    the oracle fed the GPU's slot lists."""
-    if chunk_cols != 32:
-        pytest.skip("full size runs at the default width, the one the bench times")
+    """The long-context workload at full size (16 streams x 65536 tokens, clustered keys, 8 chunk
+    ranges) at each workgroup width (the bench times the default, 32 columns); one sampled
+    stream against the oracle fed the GPU's slot lists."""
     w = synth.WORKLOADS[2]
     inp = synth.Inputs(w)
     q, k, v = to_dev(inp.q), to_dev(inp.k), to_dev(inp.v)
