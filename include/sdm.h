@@ -217,7 +217,7 @@ size_t sdm_forward_noalloc_max_bytes(void);
  * sdm_set_chunk_scan_cols).
  *   Arguments as for sdm_scan_fwd, without the undo log; workspace of at least
  *   sdm_scan_fwd_chunked_workspace_bytes() bytes (256-B aligned), which holds
- *   about (8 C^2 + 8 C (W + R) + 16 C W) bytes per stream and chunk (C = 64).
+ *   about (8 C^2 + 4 C (W + R) + 40 C W) bytes per stream and chunk (C = 64).
  * Limits: W, R <= 64 (SDM_ERR_UNSUPPORTED beyond); forget gates must be > 0
  * (the decays are taken in log form): a gate <= 0 is treated as 1e-30 and
  * flagged for sdm_check_device_errors, as are out-of-range slot ids (clamped).
@@ -231,7 +231,8 @@ size_t sdm_scan_fwd_chunked_workspace_bytes(int B, int H, int T, int W, int R);
 /* Columns per workgroup of sdm_scan_fwd_chunked's scan kernel: 8 (the narrow
  * kernel: 16 workgroups per 128-column stream, which fill the chip at few
  * streams; needs d_v % 8 == 0), 16 or 32 (a 128-byte piece of every row), or
- * 0 (the default), which takes 32.
+ * 0 (the default): 8 when d_v % 8 == 0, W <= 32 and the narrow workgroups
+ * (B H d_v / 8) fit the device at one per compute unit, else 32.
  * Process-wide; any other value returns SDM_ERR_INVALID_ARG and keeps the
  * setting.  The coefficient kernel adds the pair terms of its triangular
  * system with LDS atomics, so results may differ from run to run in the last

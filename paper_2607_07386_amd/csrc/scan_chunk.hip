@@ -33,6 +33,8 @@ namespace {
 
 constexpr int CC = SDM_CHUNK;       // tokens per chunk
 constexpr int CT1 = 256;            // threads of the coefficient kernel
+constexpr int SORT_PAIRS = CC * SDM_CHUNK_MAX_LIST / 2 / CT1;   // compare-exchange pairs per thread and stage
+static_assert(CT1 == 4 * CC, "the substitution takes one quad of threads per column of L");
 // The scan kernel takes COLS = 32 or 16 columns per workgroup (a 128- or
 // 64-byte piece of every row), with one thread per (token, column quad).
 template <int COLS>
@@ -44,11 +46,11 @@ constexpr int CK_LDS_LIMIT = 160 * 1024;
 // exp(lambda) kappa [C][W] and exp(lambda) rho [C][R], then per written slot
 // (sorted by id) its first entry, id and decay exp(lambda_C), per entry
 // (sorted by slot, then token) its token and scatter weight, and per written
-// slot its first entry as (token W + list position), bit 30 set when the slot
-// has further entries, with that entry's scatter weight.
+// slot one 16-byte unit {id, first entry as (token W + list position) with
+// bit 30 set when the slot has further entries, decay, that entry's scatter
+// weight} (the narrow kernel's scatter reads one unit per slot).
 struct ChunkRec {
-    int off_l, off_qk, off_cr, off_cy, off_sbeg, off_sslot, off_sdec, off_etok, off_ecoef, off_sfirst, off_sfcoef,
-        bytes;
+    int off_l, off_qk, off_cr, off_cy, off_sbeg, off_sslot, off_sdec, off_etok, off_ecoef, off_sinfo, bytes;
 };
 
 __host__ __device__ inline ChunkRec chunk_rec_layout(int W, int R) {
@@ -65,8 +67,7 @@ __host__ __device__ inline ChunkRec chunk_rec_layout(int W, int R) {
     r.off_sdec = o;  o += E * 4;
     r.off_etok = o;  o += E * 4;
     r.off_ecoef = o; o += E * 4;
-    r.off_sfirst = o; o += E * 4;
-    r.off_sfcoef = o; o += E * 4;
+    r.off_sinfo = o; o += E * 16;
     r.bytes = (o + 255) & ~255;
     return r;
 }
@@ -119,8 +120,7 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
     int* g_sslot = reinterpret_cast<int*>(rec + L.off_sslot);
     float* g_sdec = reinterpret_cast<float*>(rec + L.off_sdec);
     int* g_etok = reinterpret_cast<int*>(rec + L.off_etok);
-    int* g_sfirst = reinterpret_cast<int*>(rec + L.off_sfirst);
-    float* g_sfcoef = reinterpret_cast<float*>(rec + L.off_sfcoef);
+    int4* g_sinfo = reinterpret_cast<int4*>(rec + L.off_sinfo);
     float* g_ecoef = reinterpret_cast<float*>(rec + L.off_ecoef);
 
     unsigned int bad = 0;
@@ -158,21 +158,34 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
     for (int i = tid; i < 3 * CC * CC; i += CT1) A[i] = 0.f;   // A, QK, L
     __syncthreads();
 
-    // ---- bitonic sort of the keys, ascending ----
-    for (int k = 2; k <= P; k <<= 1)
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int i = tid; i < P; i += CT1) {
-                const int l = i ^ j;
-                if (l > i) {
-                    const unsigned long long x = keys[i], y = keys[l];
-                    if ((x > y) == ((i & k) == 0)) {
-                        keys[i] = y;
-                        keys[l] = x;
+    // ---- bitonic sort of the keys, ascending: per stage every thread takes up to
+    //      SORT_PAIRS compare-exchange pairs, all loads before any compare ----
+    {
+        const int np = P >> 1;
+        for (int k = 2; k <= P; k <<= 1)
+            for (int j = k >> 1; j > 0; j >>= 1) {
+                unsigned long long x[SORT_PAIRS], y[SORT_PAIRS];
+#pragma unroll
+                for (int u = 0; u < SORT_PAIRS; ++u) {
+                    const int pr = tid + u * CT1;
+                    const int i = ((pr & ~(j - 1)) << 1) | (pr & (j - 1));
+                    if (pr < np) {
+                        x[u] = keys[i];
+                        y[u] = keys[i + j];
                     }
                 }
+#pragma unroll
+                for (int u = 0; u < SORT_PAIRS; ++u) {
+                    const int pr = tid + u * CT1;
+                    const int i = ((pr & ~(j - 1)) << 1) | (pr & (j - 1));
+                    if (pr < np && (x[u] > y[u]) == ((i & k) == 0)) {
+                        keys[i] = y[u];
+                        keys[i + j] = x[u];
+                    }
+                }
+                __syncthreads();
             }
-            __syncthreads();
-        }
+    }
 
     // ---- lambda: running sum of log alpha along each slot's entries (token order) ----
     for (int e = tid; e < E; e += CT1) {
@@ -204,11 +217,14 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
             int f = e;
             while (f + 1 < E && key_slot(keys[f + 1]) == key_slot(keys[e])) ++f;
             g_sbeg[g] = e;
-            g_sslot[g] = (int)key_slot(keys[e]);
-            g_sdec[g] = expf(lams[f]);
+            const int slot = (int)key_slot(keys[e]);
+            const float dec = expf(lams[f]);
+            g_sslot[g] = slot;
+            g_sdec[g] = dec;
             const int ft = key_tok(keys[e]), fn = key_ent(keys[e]);
-            g_sfirst[g] = (ft * W + fn) | (f > e ? (1 << 30) : 0);
-            g_sfcoef[g] = kap[ft * W + fn] * expf(lams[f] - lams[e]);   // = the entry's scatter weight
+            const float fc = kap[ft * W + fn] * expf(lams[f] - lams[e]);   // = the entry's scatter weight
+            g_sinfo[g] = make_int4(slot, (ft * W + fn) | (f > e ? (1 << 30) : 0), __float_as_int(dec),
+                                   __float_as_int(fc));
             ++g;
         }
         if (tid == CT1 - 1) {
@@ -261,15 +277,34 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
     }
     __syncthreads();
 
-    // ---- L = (I + diag(beta) A)^-1 diag(beta): one column per thread, forward substitution ----
-    if (tid < n) {
-        const int cc = tid;
-        Lm[cc * CC + cc] = bt[cc];
-        for (int t = cc + 1; t < n; ++t) {
-            float acc = 0.f;
-            for (int u = cc; u < t; ++u) acc += A[t * CC + u] * Lm[u * CC + cc];
-            Lm[t * CC + cc] = -bt[t] * acc;
+    // ---- L = (I + diag(beta) A)^-1 diag(beta) by forward substitution over rows,
+    //      L[t][c] = beta_t (delta_tc - sum_{u<t} A[t][u] L[u][c]): column c on the
+    //      4 lanes of a quad, lane p holding rows [16 p, 16 p + 16) in registers;
+    //      each row's sum is 4 partial sums added across the quad.  A is zero on
+    //      and above the diagonal and rows not yet formed are zero, so every step
+    //      takes all 16 terms.  beta is 0 past the chunk's tokens, so those rows
+    //      and columns come out zero. ----
+    {
+        const int cc = tid >> 2, p = tid & 3;
+        float lr[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) lr[i] = 0.f;
+#pragma unroll
+        for (int t = 0; t < CC; ++t) {
+            const float4* arow = reinterpret_cast<const float4*>(A + t * CC + 16 * p);
+            float part = 0.f;
+#pragma unroll
+            for (int i4 = 0; i4 < 4; ++i4) {
+                const float4 a4 = arow[i4];
+                part += a4.x * lr[4 * i4] + a4.y * lr[4 * i4 + 1] + a4.z * lr[4 * i4 + 2] + a4.w * lr[4 * i4 + 3];
+            }
+            part += xor_lane_f(part, 1);
+            part += xor_lane_f(part, 2);
+            const float val = bt[t] * ((t == cc ? 1.f : 0.f) - part);
+            if (p == (t >> 4)) lr[t & 15] = val;
         }
+#pragma unroll
+        for (int i = 0; i < 16; ++i) Lm[(16 * p + i) * CC + cc] = lr[i];
     }
     __syncthreads();
     {
@@ -516,21 +551,99 @@ __global__ __launch_bounds__(scan_threads<COLS>()) void chunk_scan_kernel(const 
 // at 16 streams.  The 16 workgroups of a stream are placed on one XCD (ids
 // congruent mod 8) and read the chunk's record through its L2.  Per chunk:
 //   staging   slot ids and gather weights straight to registers (each thread
-//             its token's rows of its part), L and QK to LDS, v, and the
-//             scatter lists' heads of this thread's segments;
+//             its token's rows of its part), L and QK, v, and this thread's
+//             scatter units; none of it depends on an earlier chunk, so chunk
+//             c + 1's is loaded while chunk c computes and scatters;
 //   gather    thread (token, part p, quad q) loads rows [NPR p, NPR (p + 1))
 //             of its token, NPR pieces of 16 bytes in flight, and sums them
 //             with their weights; the 4 parts add in LDS;
 //   products  thread (token, column): R = v - retrieved, x = L R, y = inter + QK x;
 //   scatter   thread holds SBN (segment, quad) units: one load each, one store.
-// Every load of a round is issued before its first use, so a chunk costs one
-// dependent memory round trip per phase.
+// Every load of a round is issued before its first use, so a chunk costs two
+// dependent memory round trips on its path: the gather, and the stores that
+// the next chunk's gather must see.
 constexpr int NCOL = 8;                 // columns per workgroup
 constexpr int NT3 = 512;                // threads
 constexpr int NPART = 4;                // row parts per (token, quad) in the gather
 constexpr int SB3 = 8;                  // scatter units in flight per thread
+constexpr int NLQ = CC * CC / 4 / NT3;  // float4 of L (and of QK) per thread
 
-template <typename VT, int NPR, int SBN, bool REUSE>
+// One chunk's staged registers (see above).
+template <int NPR, int SBN>
+struct NarrowStage {
+    int id[NPR];
+    float wt[NPR];
+    float4 la[NLQ], qa[NLQ];
+    float vv;
+    int4 sg[SBN];   // {slot, first entry | flags, decay, first entry's weight}
+    int nseg;
+};
+
+// Loads chunk c's staging.  VEC: W and R multiples of 4 and 16-byte aligned
+// slot lists, so a part's ids and weights go as 16-byte loads.  The scatter
+// units are loaded up to the record's capacity (C W), whatever the chunk's
+// segment count: units past it are never used.
+template <typename VT, int NPR, int SBN, bool VEC>
+__device__ __forceinline__ void narrow_stage(NarrowStage<NPR, SBN>& st, const int32_t* __restrict__ w_idx,
+                                             const int32_t* __restrict__ r_idx, const VT* __restrict__ v,
+                                             const unsigned char* __restrict__ recs, const ChunkRec& L, int s,
+                                             int c, int nch, int T, int W, int R, int64_t N, int dv, int col0) {
+    const int tid = threadIdx.x;
+    const int gt = tid >> 3, gp = (tid >> 1) & 3;
+    const int pt = tid >> 3, pc = tid & 7;
+    const unsigned char* rec = recs + ((size_t)s * nch + c) * L.bytes;
+    const int t0 = c * CC, n = min(CC, T - t0);
+    const size_t tk0 = (size_t)s * T + t0;
+    const int WR = W + R;
+    const int tg = min(gt, n - 1);            // past the chunk's tokens: token n - 1 (unused)
+    const float* g_cr = reinterpret_cast<const float*>(rec + L.off_cr);
+    const float* g_cy = reinterpret_cast<const float*>(rec + L.off_cy);
+    if constexpr (VEC) {
+#pragma unroll
+        for (int k = 0; k < NPR; k += 4) {
+            const int j = gp * NPR + k;       // a group of 4 lies in one list (W % 4 == 0)
+            const bool wr = j < W, rd = !wr && j < WR;
+            const int jr = rd ? j - W : 0;
+            const int4 x = wr ? *reinterpret_cast<const int4*>(w_idx + (tk0 + tg) * W + j)
+                              : *reinterpret_cast<const int4*>(r_idx + (tk0 + tg) * R + jr);
+            const float4 w = wr ? *reinterpret_cast<const float4*>(g_cr + tg * W + j)
+                                : *reinterpret_cast<const float4*>(g_cy + tg * R + jr);
+            const int xs[4] = {x.x, x.y, x.z, x.w};
+            const float ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int64_t xi = xs[u];
+                st.id[k + u] = (int)(xi < 0 ? 0 : (xi >= N ? N - 1 : xi));
+                st.wt[k + u] = (wr || rd) ? ws[u] : 0.f;
+            }
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < NPR; ++k) {
+            const int j = gp * NPR + k;
+            const bool wr = j < W;
+            const int jr = wr ? j : min(j - W, R - 1);
+            const int64_t x = wr ? w_idx[(tk0 + tg) * W + j] : r_idx[(tk0 + tg) * R + jr];
+            st.id[k] = (int)(x < 0 ? 0 : (x >= N ? N - 1 : x));
+            st.wt[k] = j < WR ? (wr ? g_cr[tg * W + j] : g_cy[tg * R + jr]) : 0.f;
+        }
+    }
+    const float4* gl = reinterpret_cast<const float4*>(rec + L.off_l);
+    const float4* gq4 = reinterpret_cast<const float4*>(rec + L.off_qk);
+#pragma unroll
+    for (int k = 0; k < NLQ; ++k) {
+        st.la[k] = gl[tid + k * NT3];
+        st.qa[k] = gq4[tid + k * NT3];
+    }
+    st.vv = to_f32(v[(tk0 + min(pt, n - 1)) * dv + col0 + pc]);
+    const int4* g_sinfo = reinterpret_cast<const int4*>(rec + L.off_sinfo);
+    const int gmax = CC * W - 1;
+#pragma unroll
+    for (int b = 0; b < SBN; ++b) st.sg[b] = g_sinfo[min((tid + NT3 * b) >> 1, gmax)];
+    st.nseg = *reinterpret_cast<const int*>(rec);
+}
+
+template <typename VT, int NPR, int SBN, bool REUSE, bool VEC>
 __global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
     const int32_t* __restrict__ w_idx, const int32_t* __restrict__ r_idx, const VT* __restrict__ v,
     float* __restrict__ mem, float* __restrict__ y, const unsigned char* __restrict__ recs, int T, int W, int R,
@@ -544,7 +657,6 @@ __global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
     // REUSE: the gathered write rows [C][W][NCOL], the chunk-start rows the scatter decays
     extern __shared__ __align__(16) float Wrow[];
     const ChunkRec L = chunk_rec_layout(W, R);
-    const int WR = W + R;
     const int tid = threadIdx.x;
     int sl, s;
     scan_wg_coords<true>(nslice, sl, s);
@@ -555,67 +667,26 @@ __global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
     const int col0 = sl * NCOL;
     float* ms = mem + (size_t)s * N * dv + col0;
 
+    NarrowStage<NPR, SBN> cur;
+    narrow_stage<VT, NPR, SBN, VEC>(cur, w_idx, r_idx, v, recs, L, s, cb, nch, T, W, R, N, dv, col0);
     for (int c = cb; c < ce; ++c) {
         const unsigned char* rec = recs + ((size_t)s * nch + c) * L.bytes;
         const int t0 = c * CC, n = min(CC, T - t0);
         const size_t tk0 = (size_t)s * T + t0;
-        const int nseg = *reinterpret_cast<const int*>(rec);
-        const int* g_sbeg = reinterpret_cast<const int*>(rec + L.off_sbeg);
-        const int* g_sslot = reinterpret_cast<const int*>(rec + L.off_sslot);
-        const float* g_sdec = reinterpret_cast<const float*>(rec + L.off_sdec);
-        const int* g_etok = reinterpret_cast<const int*>(rec + L.off_etok);
-        const float* g_ecoef = reinterpret_cast<const float*>(rec + L.off_ecoef);
-        const int* g_sfirst = reinterpret_cast<const int*>(rec + L.off_sfirst);
-        const float* g_sfcoef = reinterpret_cast<const float*>(rec + L.off_sfcoef);
-        const float* g_cr = reinterpret_cast<const float*>(rec + L.off_cr);
-        const float* g_cy = reinterpret_cast<const float*>(rec + L.off_cy);
-        // ---- staging: every load of the phase first ----
-        const int tg = min(gt, n - 1);            // past the chunk's tokens: token n - 1 (unused)
-        int id[NPR];
-        float wt[NPR];
+        // ---- L and QK to LDS (the previous chunk's products ended before its last barrier) ----
 #pragma unroll
-        for (int k = 0; k < NPR; ++k) {
-            const int j = gp * NPR + k;
-            const bool wr = j < W;
-            const int jr = wr ? j : min(j - W, R - 1);
-            int64_t x = wr ? w_idx[(tk0 + tg) * W + j] : r_idx[(tk0 + tg) * R + jr];
-            id[k] = (int)(x < 0 ? 0 : (x >= N ? N - 1 : x));
-            wt[k] = j < WR ? (wr ? g_cr[tg * W + j] : g_cy[tg * R + jr]) : 0.f;
-        }
-        float4 la[CC * CC / 4 / NT3], qa[CC * CC / 4 / NT3];
-        {
-            const float4* gl = reinterpret_cast<const float4*>(rec + L.off_l);
-            const float4* gq4 = reinterpret_cast<const float4*>(rec + L.off_qk);
-#pragma unroll
-            for (int k = 0; k < CC * CC / 4 / NT3; ++k) {
-                la[k] = gl[tid + k * NT3];
-                qa[k] = gq4[tid + k * NT3];
-            }
-        }
-        const float vv = to_f32(v[(tk0 + min(pt, n - 1)) * dv + col0 + pc]);
-        int sg_slot[SBN], sg_first[SBN];
-        float sg_dec[SBN], sg_fc[SBN];
-#pragma unroll
-        for (int b = 0; b < SBN; ++b) {
-            const int g = min((tid + NT3 * b) >> 1, max(nseg - 1, 0));
-            sg_slot[b] = g_sslot[g];
-            sg_dec[b] = g_sdec[g];
-            sg_first[b] = g_sfirst[g];
-            sg_fc[b] = g_sfcoef[g];
-        }
-#pragma unroll
-        for (int k = 0; k < CC * CC / 4 / NT3; ++k) {
+        for (int k = 0; k < NLQ; ++k) {
             const int i = tid + k * NT3;
             const int r = (4 * i) / CC, c4 = (4 * i) % CC;
             float* lrow = Ls + r * LDP + c4;
             float* qrow = Qs + r * LDP + c4;
-            lrow[0] = la[k].x; lrow[1] = la[k].y; lrow[2] = la[k].z; lrow[3] = la[k].w;
-            qrow[0] = qa[k].x; qrow[1] = qa[k].y; qrow[2] = qa[k].z; qrow[3] = qa[k].w;
+            lrow[0] = cur.la[k].x; lrow[1] = cur.la[k].y; lrow[2] = cur.la[k].z; lrow[3] = cur.la[k].w;
+            qrow[0] = cur.qa[k].x; qrow[1] = cur.qa[k].y; qrow[2] = cur.qa[k].z; qrow[3] = cur.qa[k].w;
         }
         // ---- gather: NPR row pieces in flight ----
         float4 m[NPR];
 #pragma unroll
-        for (int k = 0; k < NPR; ++k) m[k] = load4(ms + (size_t)id[k] * dv + gq * 4);
+        for (int k = 0; k < NPR; ++k) m[k] = load4(ms + (size_t)cur.id[k] * dv + gq * 4);
         if constexpr (REUSE) {   // write rows -> LDS for the scatter
 #pragma unroll
             for (int k = 0; k < NPR; ++k) {
@@ -628,7 +699,7 @@ __global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
 #pragma unroll
         for (int k = 0; k < NPR; ++k) {
             const int j = gp * NPR + k;
-            const float w = live ? wt[k] : 0.f;
+            const float w = live ? cur.wt[k] : 0.f;
             if (j < W) {
                 ret.x += w * m[k].x; ret.y += w * m[k].y; ret.z += w * m[k].z; ret.w += w * m[k].w;
             } else {
@@ -637,6 +708,13 @@ __global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
         }
         *reinterpret_cast<float4*>(&Pret[(gp * CC + gt) * NCOL + gq * 4]) = ret;
         *reinterpret_cast<float4*>(&Pint[(gp * CC + gt) * NCOL + gq * 4]) = itr;
+        // ---- the next chunk's staging (the last chunk reloads its own), in flight from
+        //      here (not hoisted above the gather, where it would hold its registers
+        //      beside the gathered rows) ----
+        __builtin_amdgcn_sched_barrier(0);
+        NarrowStage<NPR, SBN> nxt;
+        narrow_stage<VT, NPR, SBN, VEC>(nxt, w_idx, r_idx, v, recs, L, s, min(c + 1, ce - 1), nch, T, W, R, N, dv,
+                                        col0);
         __syncthreads();
         // ---- R = v - retrieved; the reads' first term ----
         float inter = 0.f, rsum = 0.f;
@@ -645,7 +723,7 @@ __global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
             rsum += Pret[(p * CC + pt) * NCOL + pc];
             inter += Pint[(p * CC + pt) * NCOL + pc];
         }
-        Rr[pt * NCOL + pc] = pt < n ? vv - rsum : 0.f;
+        Rr[pt * NCOL + pc] = pt < n ? cur.vv - rsum : 0.f;
         __syncthreads();
         // ---- x = L R (L is zero above the diagonal and past the chunk's tokens) ----
         {
@@ -664,27 +742,34 @@ __global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
         }
         // ---- scatter: each written slot once: its chunk-start row (from LDS when
         //      REUSE, else reloaded, SB3 in flight), decayed, plus its entries' x ----
+        const int nseg = cur.nseg;
 #pragma unroll
         for (int b0 = 0; b0 < SBN; b0 += SB3) {
             float4 mm[SB3];
 #pragma unroll
             for (int b = 0; b < SB3; ++b) {
                 const int q = (tid + NT3 * (b0 + b)) & 1;
-                const int fe = sg_first[b0 + b] & 0xffff;   // token W + position of the first entry
+                // token W + position of the first entry (clamped: units past the
+                // chunk's segments hold whatever the record's tail holds)
+                const int fe = min(cur.sg[b0 + b].y & 0xffff, CC * W - 1);
                 mm[b] = REUSE ? *reinterpret_cast<const float4*>(&Wrow[fe * NCOL + q * 4])
-                              : load4(ms + (size_t)sg_slot[b0 + b] * dv + q * 4);
+                              : load4(ms + (size_t)min(max(cur.sg[b0 + b].x, 0), (int)(N - 1)) * dv + q * 4);
             }
 #pragma unroll
             for (int b = 0; b < SB3; ++b) {
                 const int u = tid + NT3 * (b0 + b);
                 const int g = u >> 1, q = u & 1;
                 if (g < nseg) {
-                    const int fe = sg_first[b0 + b];
-                    const float d = sg_dec[b0 + b], w = sg_fc[b0 + b];
+                    const int4 si = cur.sg[b0 + b];
+                    const int fe = si.y;
+                    const float d = __int_as_float(si.z), w = __int_as_float(si.w);
                     const float4 x = *reinterpret_cast<const float4*>(&Xs[((fe & 0xffff) / W) * NCOL + q * 4]);
                     float4 acc = make_float4(d * mm[b].x + w * x.x, d * mm[b].y + w * x.y, d * mm[b].z + w * x.z,
                                              d * mm[b].w + w * x.w);
                     if (fe & (1 << 30)) {   // further entries of the slot (rare)
+                        const int* g_sbeg = reinterpret_cast<const int*>(rec + L.off_sbeg);
+                        const int* g_etok = reinterpret_cast<const int*>(rec + L.off_etok);
+                        const float* g_ecoef = reinterpret_cast<const float*>(rec + L.off_ecoef);
                         const int f1 = g_sbeg[g + 1];
                         for (int f = g_sbeg[g] + 1; f < f1; ++f) {
                             const float wf = g_ecoef[f];
@@ -692,11 +777,12 @@ __global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
                             acc.x += wf * xf.x; acc.y += wf * xf.y; acc.z += wf * xf.z; acc.w += wf * xf.w;
                         }
                     }
-                    *reinterpret_cast<float4*>(ms + (size_t)sg_slot[b0 + b] * dv + q * 4) = acc;
+                    *reinterpret_cast<float4*>(ms + (size_t)si.x * dv + q * 4) = acc;
                 }
             }
         }
         __syncthreads();   // the chunk's stores precede the next chunk's gathers
+        cur = nxt;
     }
 }
 
@@ -746,7 +832,10 @@ hipError_t launch_chunk_narrow_t(const ScanFwdArgs& a, hipStream_t st) {
     if (ce <= cb) return hipSuccess;
     const int nslice = a.dv / NCOL;
     const size_t lds = REUSE ? (size_t)CC * a.W * NCOL * sizeof(float) : 0;
-    auto kl = chunk_scan_narrow_kernel<VT, NPR, SBN, REUSE>;
+    const bool vec = a.W % 4 == 0 && a.R % 4 == 0 && (reinterpret_cast<uintptr_t>(a.w_idx) & 15) == 0 &&
+                     (reinterpret_cast<uintptr_t>(a.r_idx) & 15) == 0;
+    auto kl = vec ? chunk_scan_narrow_kernel<VT, NPR, SBN, REUSE, true>
+                  : chunk_scan_narrow_kernel<VT, NPR, SBN, REUSE, false>;
     hipError_t e = hipFuncSetAttribute((const void*)kl, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kl, dim3((unsigned)(S * nslice)), dim3(NT3), lds, st, a.w_idx, a.r_idx,
@@ -767,18 +856,22 @@ hipError_t launch_chunk_narrow(const ScanFwdArgs& a, hipStream_t st) {
     return rows16 ? launch_chunk_narrow_t<VT, 16, 16, false>(a, st) : launch_chunk_narrow_t<VT, 32, 16, false>(a, st);
 }
 
-// Workgroup width: 32 columns unless sdm_set_chunk_scan_cols forces 8 (the
-// narrow kernel, d_v a multiple of 8) or 16.  Measured at the long-context
-// shape (16 streams of 128 columns): the narrow kernel's scan takes about
-// 22 ms alone, but its workgroups (117 KB of LDS each, one per CU) leave no
-// room for the next chunk range's coefficients beside it, so the whole call
-// took 32.9 ms against 32.5 ms with 32 columns; at 32 streams (learned-M0
-// shape) its 512 workgroups run in two waves: 8.1 against 5.5 ms.  16-column
-// workgroups of the wide kernel: 41.0 against 35.2 ms.
+// Workgroup width.  sdm_set_chunk_scan_cols forces 8 (the narrow kernel, d_v a
+// multiple of 8), 16 or 32 columns.  Otherwise the narrow kernel runs when its
+// workgroups fit the chip at one per CU and it keeps the gathered write rows in
+// LDS (W <= 32), and 32 columns run elsewhere.  Measured (whole call, chunk
+// coefficients included): long-context shape, 16 streams of 128 columns (256
+// narrow workgroups): 27.4 ms narrow against 32.5 ms at 32 columns, the narrow
+// kernel at 21.6 us per chunk against 31.0; learned-M0 shape, 32 streams (512
+// narrow workgroups, two rounds): 6.8 against 5.4 ms.  The narrow workgroups
+// hold 117 KB of LDS, so the next range's coefficient workgroups do not run
+// beside them.  16-column workgroups of the wide kernel: 41.0 against 35.2 ms.
 int chunk_cols_for(const ScanFwdArgs& a) {
     const int forced = sdm_chunk_cols();
     if (forced == 8 && a.dv % NCOL == 0) return 8;
-    if (forced == 16) return 16;
+    if (forced == 16 || forced == 32) return forced;
+    const int64_t wgs = (int64_t)a.B * a.H * (a.dv / NCOL);
+    if (a.dv % NCOL == 0 && a.W <= 32 && wgs <= sdm_device_simds() / 4) return 8;
     return 32;
 }
 
