@@ -33,7 +33,6 @@ namespace {
 
 constexpr int CC = SDM_CHUNK;       // tokens per chunk
 constexpr int CT1 = 256;            // threads of the coefficient kernel
-constexpr int SORT_PAIRS = CC * SDM_CHUNK_MAX_LIST / 2 / CT1;   // compare-exchange pairs per thread and stage
 static_assert(CT1 == 4 * CC, "the substitution takes one quad of threads per column of L");
 // The scan kernel takes COLS = 32 or 16 columns per workgroup (a 128- or
 // 64-byte piece of every row), with one thread per (token, column quad).
@@ -72,8 +71,9 @@ __host__ __device__ inline ChunkRec chunk_rec_layout(int W, int R) {
     return r;
 }
 
+// Sort length of the coefficient kernel: a power of two, at least one key per thread.
 inline int pow2_at_least(int x) {
-    int p = 64;
+    int p = CT1;
     while (p < x) p <<= 1;
     return p;
 }
@@ -86,6 +86,82 @@ inline size_t coef_lds_bytes(int W) {
 __device__ __forceinline__ unsigned long long key_slot(unsigned long long k) { return k >> 16; }
 __device__ __forceinline__ int key_tok(unsigned long long k) { return (int)((k >> 8) & 255); }
 __device__ __forceinline__ int key_ent(unsigned long long k) { return (int)(k & 255); }
+
+// One stage (block size KB, distance J) of the ascending bitonic network over
+// CT1 K keys, thread t holding keys [t K, t K + K): J < K compares a thread's
+// own keys, J < 64 K exchanges with lane ^ (J / K) of the same wave, larger J
+// goes through LDS (keys[] as the exchange buffer).
+template <int K, int KB, int J>
+__device__ __forceinline__ void sort_stage(unsigned long long (&kr)[K], unsigned long long* keys, int tid) {
+    if constexpr (J < K) {
+#pragma unroll
+        for (int r = 0; r < K; ++r) {
+            if ((r & J) == 0) {
+                const bool up = ((tid * K + r) & KB) == 0;
+                const unsigned long long a = kr[r], b = kr[r + J];
+                const bool sw = (a > b) == up;
+                kr[r] = sw ? b : a;
+                kr[r + J] = sw ? a : b;
+            }
+        }
+    } else {
+        unsigned long long o[K];
+        if constexpr (J < 64 * K) {
+#pragma unroll
+            for (int r = 0; r < K; ++r)
+                o[r] = ((unsigned long long)xor_lane<J / K>((uint32_t)(kr[r] >> 32)) << 32) |
+                       xor_lane<J / K>((uint32_t)kr[r]);
+        } else {
+#pragma unroll
+            for (int r = 0; r < K; ++r) keys[tid * K + r] = kr[r];
+            __syncthreads();
+#pragma unroll
+            for (int r = 0; r < K; ++r) o[r] = keys[(tid * K + r) ^ J];
+            __syncthreads();
+        }
+        // the lower index of a pair keeps the minimum in ascending blocks
+        const bool keep_min = (((tid * K) & J) == 0) == (((tid * K) & KB) == 0);
+#pragma unroll
+        for (int r = 0; r < K; ++r) {
+            const unsigned long long a = kr[r];
+            kr[r] = keep_min ? (o[r] < a ? o[r] : a) : (o[r] > a ? o[r] : a);
+        }
+    }
+    if constexpr (J > 1) sort_stage<K, KB, J / 2>(kr, keys, tid);
+    else if constexpr (KB < CT1 * K) sort_stage<K, KB * 2, KB>(kr, keys, tid);
+}
+
+// The chunk's write entries as sort keys (slot, token, entry), sorted
+// ascending into keys[0 .. CT1 K) (entries past E: all-ones keys, last), with
+// kappa per entry into kap[].  Returns the out-of-range id flag (ids clamped).
+template <int K>
+__device__ unsigned int sorted_write_keys(const int32_t* __restrict__ w_idx, const float* __restrict__ w_val,
+                                          size_t tok0, int W, int E, int64_t N, float* kap,
+                                          unsigned long long* keys) {
+    const int tid = threadIdx.x;
+    unsigned int bad = 0;
+    unsigned long long kr[K];
+#pragma unroll
+    for (int r = 0; r < K; ++r) {
+        const int e = tid * K + r;
+        unsigned long long key = ~0ull;
+        if (e < E) {
+            const int t = e / W, j = e - t * W;
+            int64_t id = w_idx[(tok0 + t) * W + j];
+            if (id < 0 || id >= N) {
+                bad |= 1u;
+                id = id < 0 ? 0 : N - 1;
+            }
+            key = ((unsigned long long)id << 16) | (unsigned long long)(t << 8) | (unsigned long long)j;
+            kap[e] = w_val[(tok0 + t) * W + j];
+        }
+        kr[r] = key;
+    }
+    sort_stage<K, 2, 1>(kr, keys, tid);
+#pragma unroll
+    for (int r = 0; r < K; ++r) keys[tid * K + r] = kr[r];
+    return bad;
+}
 
 template <typename VT>
 __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
@@ -123,22 +199,16 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
     int4* g_sinfo = reinterpret_cast<int4*>(rec + L.off_sinfo);
     float* g_ecoef = reinterpret_cast<float*>(rec + L.off_ecoef);
 
-    unsigned int bad = 0;
-    // ---- write entries as sort keys (slot, token, entry); gates ----
-    for (int e = tid; e < P; e += CT1) {
-        unsigned long long key = ~0ull;
-        if (e < E) {
-            const int t = e / W, j = e - t * W;
-            int64_t id = w_idx[(tok0 + t) * W + j];
-            if (id < 0 || id >= N) {
-                bad |= 1u;
-                id = id < 0 ? 0 : N - 1;
-            }
-            key = ((unsigned long long)id << 16) | (unsigned long long)(t << 8) | (unsigned long long)j;
-            kap[e] = w_val[(tok0 + t) * W + j];
-        }
-        keys[e] = key;
+    // ---- write entries as sort keys (slot, token, entry), sorted ascending ----
+    unsigned int bad;
+    switch (P / CT1) {
+        case 1: bad = sorted_write_keys<1>(w_idx, w_val, tok0, W, E, N, kap, keys); break;
+        case 2: bad = sorted_write_keys<2>(w_idx, w_val, tok0, W, E, N, kap, keys); break;
+        case 4: bad = sorted_write_keys<4>(w_idx, w_val, tok0, W, E, N, kap, keys); break;
+        case 8: bad = sorted_write_keys<8>(w_idx, w_val, tok0, W, E, N, kap, keys); break;
+        default: bad = sorted_write_keys<16>(w_idx, w_val, tok0, W, E, N, kap, keys); break;
     }
+    // ---- gates ----
     for (int t = tid; t < CC; t += CT1) {
         float lg = 0.f, b = 0.f;
         if (t < n) {
@@ -157,35 +227,6 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
     }
     for (int i = tid; i < 3 * CC * CC; i += CT1) A[i] = 0.f;   // A, QK, L
     __syncthreads();
-
-    // ---- bitonic sort of the keys, ascending: per stage every thread takes up to
-    //      SORT_PAIRS compare-exchange pairs, all loads before any compare ----
-    {
-        const int np = P >> 1;
-        for (int k = 2; k <= P; k <<= 1)
-            for (int j = k >> 1; j > 0; j >>= 1) {
-                unsigned long long x[SORT_PAIRS], y[SORT_PAIRS];
-#pragma unroll
-                for (int u = 0; u < SORT_PAIRS; ++u) {
-                    const int pr = tid + u * CT1;
-                    const int i = ((pr & ~(j - 1)) << 1) | (pr & (j - 1));
-                    if (pr < np) {
-                        x[u] = keys[i];
-                        y[u] = keys[i + j];
-                    }
-                }
-#pragma unroll
-                for (int u = 0; u < SORT_PAIRS; ++u) {
-                    const int pr = tid + u * CT1;
-                    const int i = ((pr & ~(j - 1)) << 1) | (pr & (j - 1));
-                    if (pr < np && (x[u] > y[u]) == ((i & k) == 0)) {
-                        keys[i] = y[u];
-                        keys[i + j] = x[u];
-                    }
-                }
-                __syncthreads();
-            }
-    }
 
     // ---- lambda: running sum of log alpha along each slot's entries (token order) ----
     for (int e = tid; e < E; e += CT1) {
