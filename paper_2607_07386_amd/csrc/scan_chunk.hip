@@ -608,6 +608,8 @@ constexpr int NT3 = 512;                // threads
 constexpr int NPART = 4;                // row parts per (token, quad) in the gather
 constexpr int SB3 = 8;                  // scatter units in flight per thread
 constexpr int NLQ = CC * CC / 4 / NT3;  // float4 of L (and of QK) per thread
+constexpr int LDN = CC + 4;             // row stride of L, QK and the column-major R, x in
+                                        // LDS: 16-byte rows, 8 rows on distinct banks
 
 // One chunk's staged registers (see above).
 template <int NPR, int SBN>
@@ -689,12 +691,13 @@ __global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
     const int32_t* __restrict__ w_idx, const int32_t* __restrict__ r_idx, const VT* __restrict__ v,
     float* __restrict__ mem, float* __restrict__ y, const unsigned char* __restrict__ recs, int T, int W, int R,
     int64_t N, int dv, int nch, int cb, int ce, int nslice) {
-    __shared__ float Ls[CC * LDP];
-    __shared__ float Qs[CC * LDP];
+    __shared__ __align__(16) float Ls[CC * LDN];
+    __shared__ __align__(16) float Qs[CC * LDN];
     __shared__ __align__(16) float Pret[NPART * CC * NCOL];
     __shared__ __align__(16) float Pint[NPART * CC * NCOL];
-    __shared__ __align__(16) float Rr[CC * NCOL];
-    __shared__ __align__(16) float Xs[CC * NCOL];
+    __shared__ __align__(16) float RrT[NCOL * LDN];   // R by column
+    __shared__ __align__(16) float XsT[NCOL * LDN];   // x by column (the y product)
+    __shared__ __align__(16) float Xs[CC * NCOL];     // x by token (the scatter)
     // REUSE: the gathered write rows [C][W][NCOL], the chunk-start rows the scatter decays
     extern __shared__ __align__(16) float Wrow[];
     const ChunkRec L = chunk_rec_layout(W, R);
@@ -719,10 +722,8 @@ __global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
         for (int k = 0; k < NLQ; ++k) {
             const int i = tid + k * NT3;
             const int r = (4 * i) / CC, c4 = (4 * i) % CC;
-            float* lrow = Ls + r * LDP + c4;
-            float* qrow = Qs + r * LDP + c4;
-            lrow[0] = cur.la[k].x; lrow[1] = cur.la[k].y; lrow[2] = cur.la[k].z; lrow[3] = cur.la[k].w;
-            qrow[0] = cur.qa[k].x; qrow[1] = cur.qa[k].y; qrow[2] = cur.qa[k].z; qrow[3] = cur.qa[k].w;
+            *reinterpret_cast<float4*>(Ls + r * LDN + c4) = cur.la[k];
+            *reinterpret_cast<float4*>(Qs + r * LDN + c4) = cur.qa[k];
         }
         // ---- gather: NPR row pieces in flight ----
         float4 m[NPR];
@@ -764,21 +765,30 @@ __global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
             rsum += Pret[(p * CC + pt) * NCOL + pc];
             inter += Pint[(p * CC + pt) * NCOL + pc];
         }
-        Rr[pt * NCOL + pc] = pt < n ? cur.vv - rsum : 0.f;
+        RrT[pc * LDN + pt] = pt < n ? cur.vv - rsum : 0.f;
         __syncthreads();
         // ---- x = L R (L is zero above the diagonal and past the chunk's tokens) ----
         {
             float acc = 0.f;
-#pragma unroll 16
-            for (int u = 0; u < CC; ++u) acc += Ls[pt * LDP + u] * Rr[u * NCOL + pc];
+#pragma unroll
+            for (int u = 0; u < CC; u += 4) {
+                const float4 l4 = *reinterpret_cast<const float4*>(Ls + pt * LDN + u);
+                const float4 r4 = *reinterpret_cast<const float4*>(RrT + pc * LDN + u);
+                acc += l4.x * r4.x + l4.y * r4.y + l4.z * r4.z + l4.w * r4.w;
+            }
             Xs[pt * NCOL + pc] = acc;
+            XsT[pc * LDN + pt] = acc;
         }
         __syncthreads();
         // ---- y = inter + QK x ----
         {
             float acc = inter;
-#pragma unroll 16
-            for (int u = 0; u < CC; ++u) acc += Qs[pt * LDP + u] * Xs[u * NCOL + pc];
+#pragma unroll
+            for (int u = 0; u < CC; u += 4) {
+                const float4 q4 = *reinterpret_cast<const float4*>(Qs + pt * LDN + u);
+                const float4 x4 = *reinterpret_cast<const float4*>(XsT + pc * LDN + u);
+                acc += q4.x * x4.x + q4.y * x4.y + q4.z * x4.z + q4.w * x4.w;
+            }
             if (pt < n) y[(tk0 + pt) * dv + col0 + pc] = acc;
         }
         // ---- scatter: each written slot once: its chunk-start row (from LDS when
