@@ -597,7 +597,7 @@ __global__ __launch_bounds__(scan_threads<COLS>()) void chunk_scan_kernel(const 
 //             c + 1's is loaded while chunk c computes and scatters;
 //   gather    thread (token, part p, quad q) loads rows [NPR p, NPR (p + 1))
 //             of its token, NPR pieces of 16 bytes in flight, and sums them
-//             with their weights; the 4 parts add in LDS;
+//             with their weights; the 4 parts add across lanes;
 //   products  thread (token, column): R = v - retrieved, x = L R, y = inter + QK x;
 //   scatter   thread holds SBN (segment, quad) units: one load each, one store.
 // Every load of a round is issued before its first use, so a chunk costs two
@@ -610,6 +610,19 @@ constexpr int SB3 = 8;                  // scatter units in flight per thread
 constexpr int NLQ = CC * CC / 4 / NT3;  // float4 of L (and of QK) per thread
 constexpr int LDN = CC + 4;             // row stride of L, QK and the column-major R, x in
                                         // LDS: 16-byte rows, 8 rows on distinct banks
+
+// Column of the product mapping (token tid / 8): the lane order of the
+// gather's (part p, quad q) pairs, 2 p + q -> column 4 q + p, so that a
+// gather lane's cross-lane sums are already its product column's.
+__device__ __forceinline__ int narrow_pc(int tid) { return 4 * (tid & 1) + ((tid >> 1) & 3); }
+__device__ __forceinline__ float4 f4_add_lanes(float4 a) {   // sum over lane bits 1 and 2
+    auto add = [](float x) {
+        x += __uint_as_float(xor_lane<2>(__float_as_uint(x)));
+        return x + __uint_as_float(xor_lane<4>(__float_as_uint(x)));
+    };
+    return make_float4(add(a.x), add(a.y), add(a.z), add(a.w));
+}
+__device__ __forceinline__ float f4_elem(float4 a, int e) { return e == 0 ? a.x : e == 1 ? a.y : e == 2 ? a.z : a.w; }
 
 // One chunk's staged registers (see above).
 template <int NPR, int SBN>
@@ -633,7 +646,7 @@ __device__ __forceinline__ void narrow_stage(NarrowStage<NPR, SBN>& st, const in
                                              int c, int nch, int T, int W, int R, int64_t N, int dv, int col0) {
     const int tid = threadIdx.x;
     const int gt = tid >> 3, gp = (tid >> 1) & 3;
-    const int pt = tid >> 3, pc = tid & 7;
+    const int pt = tid >> 3, pc = narrow_pc(tid);
     const unsigned char* rec = recs + ((size_t)s * nch + c) * L.bytes;
     const int t0 = c * CC, n = min(CC, T - t0);
     const size_t tk0 = (size_t)s * T + t0;
@@ -693,8 +706,6 @@ __global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
     int64_t N, int dv, int nch, int cb, int ce, int nslice) {
     __shared__ __align__(16) float Ls[CC * LDN];
     __shared__ __align__(16) float Qs[CC * LDN];
-    __shared__ __align__(16) float Pret[NPART * CC * NCOL];
-    __shared__ __align__(16) float Pint[NPART * CC * NCOL];
     __shared__ __align__(16) float RrT[NCOL * LDN];   // R by column
     __shared__ __align__(16) float XsT[NCOL * LDN];   // x by column (the y product)
     __shared__ __align__(16) float Xs[CC * NCOL];     // x by token (the scatter)
@@ -707,7 +718,7 @@ __global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
     // gather mapping
     const int gt = tid >> 3, gp = (tid >> 1) & 3, gq = tid & 1;
     // product mapping
-    const int pt = tid >> 3, pc = tid & 7;
+    const int pt = tid >> 3, pc = narrow_pc(tid);
     const int col0 = sl * NCOL;
     float* ms = mem + (size_t)s * N * dv + col0;
 
@@ -748,8 +759,11 @@ __global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
                 itr.x += w * m[k].x; itr.y += w * m[k].y; itr.z += w * m[k].z; itr.w += w * m[k].w;
             }
         }
-        *reinterpret_cast<float4*>(&Pret[(gp * CC + gt) * NCOL + gq * 4]) = ret;
-        *reinterpret_cast<float4*>(&Pint[(gp * CC + gt) * NCOL + gq * 4]) = itr;
+        // the 4 parts of a (token, quad) are lanes 2 p + q of the token's 8: add
+        // them across lanes; lane (p, q) then holds column 4 q + p = pc
+        ret = f4_add_lanes(ret);
+        itr = f4_add_lanes(itr);
+        const float rsum = f4_elem(ret, gp), inter = f4_elem(itr, gp);
         // ---- the next chunk's staging (the last chunk reloads its own), in flight from
         //      here (not hoisted above the gather, where it would hold its registers
         //      beside the gathered rows) ----
@@ -757,14 +771,7 @@ __global__ __launch_bounds__(NT3) void chunk_scan_narrow_kernel(
         NarrowStage<NPR, SBN> nxt;
         narrow_stage<VT, NPR, SBN, VEC>(nxt, w_idx, r_idx, v, recs, L, s, min(c + 1, ce - 1), nch, T, W, R, N, dv,
                                         col0);
-        __syncthreads();
-        // ---- R = v - retrieved; the reads' first term ----
-        float inter = 0.f, rsum = 0.f;
-#pragma unroll
-        for (int p = 0; p < NPART; ++p) {
-            rsum += Pret[(p * CC + pt) * NCOL + pc];
-            inter += Pint[(p * CC + pt) * NCOL + pc];
-        }
+        // ---- R = v - retrieved ----
         RrT[pc * LDN + pt] = pt < n ? cur.vv - rsum : 0.f;
         __syncthreads();
         // ---- x = L R (L is zero above the diagonal and past the chunk's tokens) ----
