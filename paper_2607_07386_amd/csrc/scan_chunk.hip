@@ -225,7 +225,8 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
         la[t] = lg;
         bt[t] = b;
     }
-    for (int i = tid; i < 3 * CC * CC; i += CT1) A[i] = 0.f;   // A, QK, L
+    for (int i = tid; i < 2 * CC * CC / 4; i += CT1)   // A, QK (L is written whole below)
+        reinterpret_cast<float4*>(A)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     __syncthreads();
 
     // ---- lambda: running sum of log alpha along each slot's entries (token order) ----
@@ -243,16 +244,25 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
     const int e0 = min(E, tid * ept), e1 = min(E, e0 + ept);
     int ns = 0;
     for (int e = e0; e < e1; ++e) ns += (e == 0 || key_slot(keys[e]) != key_slot(keys[e - 1])) ? 1 : 0;
-    cnt[tid] = ns;
+    // exclusive prefix of ns over the threads: within the wave by lane shifts,
+    // then the totals of the earlier waves
+    int incl = ns;
+    const int lane = tid & (SDM_WAVE - 1), wave = tid / SDM_WAVE;
+#pragma unroll
+    for (int d = 1; d < SDM_WAVE; d <<= 1) {
+        const int up = __shfl_up(incl, d, SDM_WAVE);
+        if (lane >= d) incl += up;
+    }
+    if (lane == SDM_WAVE - 1) cnt[wave] = incl;
     __syncthreads();
-    for (int d = 1; d < CT1; d <<= 1) {
-        const int v = cnt[tid] + (tid >= d ? cnt[tid - d] : 0);
-        __syncthreads();
-        cnt[tid] = v;
-        __syncthreads();
+    int before = 0, nseg = 0;
+#pragma unroll
+    for (int w = 0; w < CT1 / SDM_WAVE; ++w) {
+        before += w < wave ? cnt[w] : 0;
+        nseg += cnt[w];
     }
     {
-        int g = cnt[tid] - ns;
+        int g = before + incl - ns;
         for (int e = e0; e < e1; ++e) {
             if (!(e == 0 || key_slot(keys[e]) != key_slot(keys[e - 1]))) continue;
             int f = e;
@@ -269,8 +279,8 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
             ++g;
         }
         if (tid == CT1 - 1) {
-            g_sbeg[cnt[CT1 - 1]] = E;
-            *reinterpret_cast<int*>(rec) = cnt[CT1 - 1];
+            g_sbeg[nseg] = E;
+            *reinterpret_cast<int*>(rec) = nseg;
         }
     }
 
