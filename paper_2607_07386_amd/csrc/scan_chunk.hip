@@ -163,6 +163,23 @@ __device__ unsigned int sorted_write_keys(const int32_t* __restrict__ w_idx, con
     return bad;
 }
 
+// One read entry (token t, position m, slot id, weight rho) whose slot's first
+// sorted key is at lo: the slot's decay after token t, the gather weight, and
+// its QK terms from the slot's writers up to t.
+__device__ __forceinline__ void read_side_entry(const unsigned long long* keys, const float* kap, const float* lams,
+                                                float* QK, float* g_cy, int E, int W, int R, int t, int m,
+                                                int64_t id, float rho, int lo) {
+    int last = lo - 1;
+    while (last + 1 < E && key_slot(keys[last + 1]) == (unsigned long long)id && key_tok(keys[last + 1]) <= t)
+        ++last;
+    const float lr = last >= lo ? lams[last] : 0.f;
+    g_cy[t * R + m] = rho * expf(lr);
+    for (int f = lo; f <= last; ++f) {
+        const unsigned long long kf = keys[f];
+        atomicAdd(&QK[t * CC + key_tok(kf)], rho * kap[key_tok(kf) * W + key_ent(kf)] * expf(lr - lams[f]));
+    }
+}
+
 template <typename VT>
 __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
     const int32_t* __restrict__ w_idx, const float* __restrict__ w_val, const int32_t* __restrict__ r_idx,
@@ -301,29 +318,40 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
     }
     // ---- gather weights of the write side ----
     for (int e = tid; e < E; e += CT1) g_cr[e] = kap[e] * expf(lamw[e]);
-    // ---- read side: lambda of the read slot after token t, gather weight, QK ----
-    for (int e = tid; e < n * R; e += CT1) {
-        const int t = e / R, m = e - t * R;
-        int64_t id = r_idx[(tok0 + t) * R + m];
-        if (id < 0 || id >= N) {
-            bad |= 1u;
-            id = id < 0 ? 0 : N - 1;
+    // ---- read side: lambda of the read slot after token t, gather weight, QK.
+    //      Entries go RB at a time, their searches interleaved: the first key of
+    //      the slot by a branch-free lower bound over the P sorted keys (the
+    //      padding keys past E sort last and are never below an id) ----
+    constexpr int RB = 4;
+    for (int e0 = tid; e0 < n * R; e0 += RB * CT1) {
+        int64_t ids[RB];
+        int pos[RB];
+#pragma unroll
+        for (int b = 0; b < RB; ++b) {
+            const int e = min(e0 + b * CT1, n * R - 1);
+            const int t = e / R, m = e - t * R;
+            int64_t id = r_idx[(tok0 + t) * R + m];
+            if (id < 0 || id >= N) {
+                bad |= 1u;
+                id = id < 0 ? 0 : N - 1;
+            }
+            ids[b] = id;
+            pos[b] = 0;
         }
-        const float rho = r_val[(tok0 + t) * R + m];
-        int lo = 0, hi = E;
-        while (lo < hi) {
-            const int mid = (lo + hi) >> 1;
-            if (key_slot(keys[mid]) < (unsigned long long)id) lo = mid + 1;
-            else hi = mid;
+        for (int step = P >> 1; step >= 1; step >>= 1) {
+#pragma unroll
+            for (int b = 0; b < RB; ++b)
+                if (key_slot(keys[pos[b] + step - 1]) < (unsigned long long)ids[b]) pos[b] += step;
         }
-        int last = lo - 1;
-        while (last + 1 < E && key_slot(keys[last + 1]) == (unsigned long long)id && key_tok(keys[last + 1]) <= t)
-            ++last;
-        const float lr = last >= lo ? lams[last] : 0.f;
-        g_cy[t * R + m] = rho * expf(lr);
-        for (int f = lo; f <= last; ++f) {
-            const unsigned long long kf = keys[f];
-            atomicAdd(&QK[t * CC + key_tok(kf)], rho * kap[key_tok(kf) * W + key_ent(kf)] * expf(lr - lams[f]));
+#pragma unroll
+        for (int b = 0; b < RB; ++b) {
+            const int e = e0 + b * CT1;
+            if (e >= n * R) break;
+            const int t = e / R, m = e - t * R;
+            const int64_t id = ids[b];
+            const float rho = r_val[(tok0 + t) * R + m];
+            const int lo = pos[b];
+            read_side_entry(keys, kap, lams, QK, g_cy, E, W, R, t, m, id, rho, lo);
         }
     }
     __syncthreads();
@@ -343,12 +371,20 @@ __global__ __launch_bounds__(CT1) void chunk_coef_kernel(
 #pragma unroll
         for (int t = 0; t < CC; ++t) {
             const float4* arow = reinterpret_cast<const float4*>(A + t * CC + 16 * p);
-            float part = 0.f;
+            float pr[16];
 #pragma unroll
             for (int i4 = 0; i4 < 4; ++i4) {
                 const float4 a4 = arow[i4];
-                part += a4.x * lr[4 * i4] + a4.y * lr[4 * i4 + 1] + a4.z * lr[4 * i4 + 2] + a4.w * lr[4 * i4 + 3];
+                pr[4 * i4] = a4.x * lr[4 * i4];
+                pr[4 * i4 + 1] = a4.y * lr[4 * i4 + 1];
+                pr[4 * i4 + 2] = a4.z * lr[4 * i4 + 2];
+                pr[4 * i4 + 3] = a4.w * lr[4 * i4 + 3];
             }
+#pragma unroll
+            for (int h = 8; h >= 1; h >>= 1)   // pairwise: a short dependent chain per row
+#pragma unroll
+                for (int i = 0; i < h; ++i) pr[i] += pr[i + h];
+            float part = pr[0];
             part += xor_lane_f(part, 1);
             part += xor_lane_f(part, 2);
             const float val = bt[t] * ((t == cc ? 1.f : 0.f) - part);
