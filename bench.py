@@ -427,10 +427,34 @@ def main():
         e1.record(stream)
         torch.cuda.synchronize()
         dms = e0.elapsed_time(e1) / nd
+        # the same steps replayed from a HIP graph of 20 captured calls: the device's
+        # time per step, without the per-call host work (argument checks, launch)
+        gsteps = 20
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            dstep()
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(gsteps):
+                dstep()
+        graph.replay()
+        torch.cuda.synchronize()
+        nrep = 10
+        e0.record(stream)
+        for _ in range(nrep):
+            graph.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        gms = e0.elapsed_time(e1) / (nrep * gsteps)
+        del graph
         out["decode"] = {
             "workload": f"one token per step for B={wd.B} sequences, H={wd.H}, N={wd.N}, d={wd.d_v}, "
                         f"top-{wd.topk}; memory resident; one sdm_forward call per step (T = 1: one fused launch)",
-            "us_per_step": round(dms * 1e3, 2), "tokens_per_s": round(wd.B / (dms * 1e-3), 1)}
+            "us_per_step": round(dms * 1e3, 2), "tokens_per_s": round(wd.B / (dms * 1e-3), 1),
+            "us_per_step_graph": round(gms * 1e3, 2), "tokens_per_s_graph": round(wd.B / (gms * 1e-3), 1)}
         del q, k, v, al, be, cb, mem, ws, y, douts
         torch.cuda.empty_cache()
 

@@ -385,33 +385,33 @@ __device__ __forceinline__ bool fast_topk(const float (&sc)[E], const uint32_t (
     return true;
 }
 
-// One token, k <= 32 and s <= SP = 64 E: stage 1 on both halves (rows padded
-// to SP with -inf), stage 2 over the pruned pairs (pi, pj: this lane's pair
-// ranks; pairs past the count point at a -inf list entry), id sort and
-// softmax, outputs written.  Returns false when a selection overflowed (the
-// caller then runs the general path for this token).
+// Stage 1 of one half on the fast path (k <= 32, s <= 64 E, the half's row
+// padded with -inf): its ranked top-k into out[0 .. k).  False when the
+// candidates overflowed.
 template <int E>
-__device__ __forceinline__ bool token_fast(const float* row, int s, int k, const uint32_t (&pi)[3],
-                                           const uint32_t (&pj)[3], Entry* listA, Entry* listB,
-                                           uint2* kbuf, int32_t* idx_out, float* val_out,
-                                           float* score_out) {
-    constexpr int SP = E * SDM_WAVE;
+__device__ __forceinline__ bool half_fast(const float* hrow, int k, uint2* kbuf, Entry* out) {
     const int lane = lane_id();
+    float sc[E];
+    uint32_t gid[E];
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-        float sc[E];
-        uint32_t gid[E];
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-            sc[e] = row[half * SP + e * SDM_WAVE + lane];
-            gid[e] = e * SDM_WAVE + lane;
-        }
-        uint32_t th, tl;
-        if (!fast_topk<E>(sc, gid, k, kbuf, th, tl)) return false;
-        Entry* out = half ? listB : listA;
-        if (lane < k) out[lane] = Entry{key_to_float(th), (int)~tl};
+    for (int e = 0; e < E; ++e) {
+        sc[e] = hrow[e * SDM_WAVE + lane];
+        gid[e] = e * SDM_WAVE + lane;
     }
-    __builtin_amdgcn_wave_barrier();
+    uint32_t th, tl;
+    if (!fast_topk<E>(sc, gid, k, kbuf, th, tl)) return false;
+    if (lane < k) out[lane] = Entry{key_to_float(th), (int)~tl};
+    return true;
+}
+
+// Stage 2 on the fast path from the two ranked shortlists (pi, pj: this
+// lane's pair ranks; pairs past the count point at a -inf list entry): the
+// top-k of the pruned pairs, id sort and softmax, outputs written.  False when
+// a selection overflowed or the k-th place is tied.
+__device__ __forceinline__ bool pairs_fast(int s, int k, const uint32_t (&pi)[3], const uint32_t (&pj)[3],
+                                           const Entry* listA, const Entry* listB, uint2* kbuf,
+                                           int32_t* idx_out, float* val_out, float* score_out) {
+    const int lane = lane_id();
     float sc[3];
     uint32_t gid[3];
 #pragma unroll
@@ -452,6 +452,20 @@ __device__ __forceinline__ bool token_fast(const float* row, int s, int k, const
         if (score_out) score_out[lane] = my_sc;
     }
     return true;
+}
+
+// One token, k <= 32 and s <= SP = 64 E: stage 1 on both halves, then stage
+// 2.  Returns false when a selection overflowed (the caller then runs the
+// general path for this token).
+template <int E>
+__device__ __forceinline__ bool token_fast(const float* row, int s, int k, const uint32_t (&pi)[3],
+                                           const uint32_t (&pj)[3], Entry* listA, Entry* listB,
+                                           uint2* kbuf, int32_t* idx_out, float* val_out,
+                                           float* score_out) {
+    constexpr int SP = E * SDM_WAVE;
+    if (!half_fast<E>(row, k, kbuf, listA) || !half_fast<E>(row + SP, k, kbuf, listB)) return false;
+    __builtin_amdgcn_wave_barrier();
+    return pairs_fast(s, k, pi, pj, listA, listB, kbuf, idx_out, val_out, score_out);
 }
 
 // Stage 2 of one token (k <= 64) on this wave, from the ranked shortlists of
@@ -1014,6 +1028,62 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __
 }
 
 // ---- one token per stream (decode) ----------------------------------------
+// Scores of the decode step's two rows (read query with cb_q, write key with
+// cb_k) on the matrix cores, bf16 codebooks with d_k / 2 <= 64 and E <= 4:
+// every operand of this wave's tiles, both rows and both halves, is loaded
+// before the first MFMA, so the step pays one load latency for its scores
+// (the token is row 0 of each 16-row tile).  Rows [row][half][SP], -inf past s.
+template <int E>
+__device__ __forceinline__ void decode_scores_mfma(const bf16_t* __restrict__ xq, const bf16_t* __restrict__ xk,
+                                                   const bf16_t* __restrict__ cq, const bf16_t* __restrict__ ck,
+                                                   int dk, int s, float* scores) {
+    constexpr int SP = E * SDM_WAVE;
+    const int wave = threadIdx.x / SDM_WAVE, lane = lane_id();
+    const int dh = dk / 2, r16 = lane % 16, q4 = lane / 16;
+    sdm_bf16x8 a[2][2][2], b[2][2][E][2];
+#pragma unroll
+    for (int sd = 0; sd < 2; ++sd) {
+        const bf16_t* x = sd ? xk : xq;
+        const bf16_t* cb = sd ? ck : cq;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                const int kc = ks * 32 + 8 * q4;
+                a[sd][h][ks] = sdm_bf16x8{};
+                if (r16 == 0 && kc < dh) a[sd][h][ks] = *reinterpret_cast<const sdm_bf16x8*>(x + h * dh + kc);
+            }
+#pragma unroll
+            for (int i = 0; i < E; ++i) {
+                const int j = (wave + AWAVES * i) * 16 + r16;
+                const bf16_t* crow = cb + ((size_t)h * s + min(j, s - 1)) * dh;
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) {
+                    const int kc = ks * 32 + 8 * q4;
+                    b[sd][h][i][ks] = sdm_bf16x8{};
+                    if (j < s && kc < dh) b[sd][h][i][ks] = *reinterpret_cast<const sdm_bf16x8*>(crow + kc);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int sd = 0; sd < 2; ++sd)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int i = 0; i < E; ++i) {
+                const int j = (wave + AWAVES * i) * 16 + r16;
+                sdm_f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[sd][h][0], b[sd][h][i][0], acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[sd][h][1], b[sd][h][i][1], acc, 0, 0, 0);
+                if (q4 == 0 && j < s) scores[(sd * 2 + h) * SP + j] = acc[0];
+            }
+    if (s < SP) {
+        const int pad = SP - s;
+        for (int i = threadIdx.x; i < 4 * pad; i += blockDim.x) scores[(i / pad) * SP + s + i % pad] = -INFINITY;
+    }
+}
+
 // One workgroup per (b, h) stream does the whole layer step for its single
 // token: addressing of the read query and of the write key (their scores as
 // two rows of one tile, then the two selections on two waves at once), then
@@ -1037,6 +1107,25 @@ __device__ __forceinline__ v4f load_quad(const void* p, int in_dtype, size_t i) 
     return in_dtype == SDM_DT_BF16 ? ld4v(static_cast<const bf16_t*>(p) + i) : ld4v(static_cast<const float*>(p) + i);
 }
 
+// LDS of a tile: padded score rows, per-wave lists and sort buffer, and for
+// k > 64 the pair list.
+__host__ __device__ constexpr size_t address_lds_bytes(int E, int AT, int KM) {
+    return (size_t)AT * 2 * E * SDM_WAVE * sizeof(float) + AWAVES * 3 * KM * sizeof(Entry) +
+           AWAVES * SDM_WAVE * sizeof(uint64_t) + (KM > MAXK ? MAXCAND_BIG * SDM_WAVE * sizeof(uint16_t) : 0);
+}
+__host__ __device__ constexpr size_t decode_scan_lds_bytes(int W) {
+    return (size_t)(MAXK_BIG + DEC_RG * DEC_COLS + (size_t)W * DEC_COLS) * sizeof(float);
+}
+// The decode step's slot lists and weights of its two rows, and two words of
+// flags, past both phases' LDS.
+__host__ __device__ constexpr size_t decode_sel_offset(int E, int KM, int W) {
+    const size_t a = address_lds_bytes(E, E <= 4 ? ATILE : (E <= 8 ? 8 : 4), KM), b = decode_scan_lds_bytes(W);
+    return ((a > b ? a : b) + 15) & ~(size_t)15;
+}
+__host__ __device__ constexpr size_t decode_lds_bytes(int E, int KM, int W) {
+    return decode_sel_offset(E, KM, W) + (size_t)2 * KM * (sizeof(int32_t) + sizeof(float)) + 2 * sizeof(int);
+}
+
 template <typename XT, int MODE, int E, int KM>
 __global__ __launch_bounds__(AWAVES * SDM_WAVE) void decode_kernel(
     const XT* __restrict__ q, const XT* __restrict__ kx, const XT* __restrict__ cb_q, const XT* __restrict__ cb_k,
@@ -1048,9 +1137,16 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void decode_kernel(
     extern __shared__ __align__(16) unsigned char smem[];
     const int stream = blockIdx.x;
     if (stream == 0 && threadIdx.x < 4) flags[threadIdx.x] = 0u;   // the call's device-error words
+    // the two rows' slot lists and weights, past both phases' LDS: [read, write][KM]
+    int32_t* sel_id = reinterpret_cast<int32_t*>(smem + decode_sel_offset(E, KM, topk));
+    float* sel_val = reinterpret_cast<float*>(sel_id + 2 * KM);
+    int* fail = reinterpret_cast<int*>(sel_val + 2 * KM);           // [2] fast stage 1 overflowed, per row
+    // the token's gates and its first column chunk of v, loaded before any other work
+    float al = load_scalar(alpha, in_dtype, stream), be = load_scalar(beta, in_dtype, stream);
+    const v4f v_first = load_quad(v, in_dtype, (size_t)stream * dv + min((int)(threadIdx.x % 32) * 4, dv - 4));
     {
-        // both sides at once: score rows 0 (read query) and 1 (write key), then
-        // phases B, C of the two on waves 0 and 1
+        // both rows at once: score rows 0 (read query) and 1 (write key), then
+        // phases B, C
         constexpr int AT = atile<E>();
         constexpr int SP = E * SDM_WAVE;
         float* scores = reinterpret_cast<float*>(smem);
@@ -1060,34 +1156,69 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void decode_kernel(
         int ncand;
         tile_pairs<KM>(topk, reinterpret_cast<uint16_t*>(kbufs + AWAVES * SDM_WAVE), pairs, ncand);
         const size_t hc = (size_t)(stream % H) * 2 * s * (dk / 2);
-        tile_scores<XT, MODE, E>(q + (size_t)stream * dk, MODE == 0 ? cb_q : cb_q + hc, 0, 1, dk, s, scores);
-        tile_scores<XT, MODE, E>(kx + (size_t)stream * dk, MODE == 0 ? cb_k : cb_k + hc, 0, 1, dk, s,
-                                 scores + 2 * SP);
+        bool joint = false;
+        if constexpr (MODE == 2 && E <= 4) {
+            if (dk / 2 <= 64) {
+                decode_scores_mfma<E>(q + (size_t)stream * dk, kx + (size_t)stream * dk, cb_q + hc, cb_k + hc, dk,
+                                      s, scores);
+                joint = true;
+            }
+        }
+        if (!joint) {
+            tile_scores<XT, MODE, E>(q + (size_t)stream * dk, MODE == 0 ? cb_q : cb_q + hc, 0, 1, dk, s, scores);
+            tile_scores<XT, MODE, E>(kx + (size_t)stream * dk, MODE == 0 ? cb_k : cb_k + hc, 0, 1, dk, s,
+                                     scores + 2 * SP);
+        }
+        if (threadIdx.x < 2) fail[threadIdx.x] = 0;
         __syncthreads();
         const int wave = threadIdx.x / SDM_WAVE;
+        SelWave w;
+        if (wave < 2) select_init<KM>(w, scratch, kbufs, wave, topk, ncand, pairs);
+        bool four = false;   // stage 1 of the 2 rows x 2 halves on the four waves
+        if constexpr (E <= 4 && KM <= MAXK) four = topk <= 32 && topk <= s;
+        if (four) {
+            const int sd = wave >> 1, hf = wave & 1;
+            Entry* lst = scratch + sd * 3 * KM + (1 + hf) * KM;   // row sd's list of half hf
+            if (!half_fast<E>(scores + (sd * 2 + hf) * SP, topk, reinterpret_cast<uint2*>(kbufs + wave * SDM_WAVE),
+                              lst) && lane_id() == 0)
+                fail[sd] = 1;
+            __syncthreads();
+        }
         if (wave < 2) {
-            SelWave w;
-            select_init<KM>(w, scratch, kbufs, wave, topk, ncand, pairs);
-            const size_t o = (size_t)stream * topk;
-            if (wave == 0)
-                select_token<E, KM>(w, scores, s, topk, ncand, pairs, r_idx + o, r_val + o, nullptr);
-            else
-                select_token<E, KM>(w, scores + 2 * SP, s, topk, ncand, pairs, w_idx + o, w_val + o, nullptr);
+            int32_t* io = sel_id + wave * KM;
+            float* vo = sel_val + wave * KM;
+            const float* row = scores + wave * 2 * SP;
+            if (four) {
+                if (fail[wave] ||
+                    !pairs_fast(s, topk, w.pi, w.pj, w.listA, w.listB, reinterpret_cast<uint2*>(w.kbuf), io, vo,
+                                nullptr)) {
+                    token_general<E>(row, s, SP, topk, ncand, pairs, w.scr, w.listA, w.listB, w.kbuf, io, vo,
+                                     nullptr);
+                    wait_lds();
+                    __builtin_amdgcn_wave_barrier();
+                }
+            } else {
+                select_token<E, KM>(w, row, s, topk, ncand, pairs, io, vo, nullptr);
+            }
         }
     }
-    __syncthreads();   // the slot lists in global memory are complete and visible to the workgroup
+    __syncthreads();   // the slot lists are complete in LDS
 
     const int W = topk, R = topk;
     const int tid = threadIdx.x, rg = tid / 32, cq = tid % 32;
-    const int32_t* wi = w_idx + (size_t)stream * W;
-    const int32_t* ri = r_idx + (size_t)stream * R;
-    const float* wv = w_val + (size_t)stream * W;
-    const float* rv = r_val + (size_t)stream * R;
-    int* lw = reinterpret_cast<int*>(smem);                          // [MAXK_BIG] write slots
-    float* red = reinterpret_cast<float*>(lw + MAXK_BIG);            // [DEC_RG][DEC_COLS] partial sums
+    for (int i = tid; i < 2 * topk; i += blockDim.x) {   // the lists out to the caller
+        const int sd = i >= topk, j = i - sd * topk;
+        const size_t o = (size_t)stream * topk + j;
+        (sd ? w_idx : r_idx)[o] = sel_id[sd * KM + j];
+        (sd ? w_val : r_val)[o] = sel_val[sd * KM + j];
+    }
+    const int32_t* wi = sel_id + KM;
+    const int32_t* ri = sel_id;
+    const float* wv = sel_val + KM;
+    const float* rv = sel_val;
+    const int* lw = wi;                                              // write slots (ascending)
+    float* red = reinterpret_cast<float*>(smem + MAXK_BIG * sizeof(int));   // [DEC_RG][DEC_COLS] partial sums
     float* nrow = red + DEC_RG * DEC_COLS;                           // [W][DEC_COLS] written rows
-    for (int i = tid; i < W; i += blockDim.x) lw[i] = wi[i];
-    __syncthreads();
 
     int wslot[DEC_ROWS], rslot[DEC_ROWS], link[DEC_ROWS];
     float kap[DEC_ROWS], rho[DEC_ROWS];
@@ -1098,6 +1229,22 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void decode_kernel(
         kap[j] = n < W ? wv[n] : 0.f;
         rslot[j] = n < R ? min(max(ri[n], 0), (int)(N - 1)) : 0;
         rho[j] = n < R ? rv[n] : 0.f;
+    }
+    float* tab = mem + (size_t)stream * N * dv;
+    // the first column chunk's rows, in flight while the links are found
+    v4f P[DEC_ROWS], Q[DEC_ROWS];
+    {
+        const int cl = min(cq * 4, dv - 4);
+#pragma unroll
+        for (int j = 0; j < DEC_ROWS; ++j) {
+            const int n = rg + DEC_RG * j;
+            if (n < W) P[j] = ld4(tab + (size_t)wslot[j] * dv + cl);
+            if (n < R) Q[j] = ld4(tab + (size_t)rslot[j] * dv + cl);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < DEC_ROWS; ++j) {
+        const int n = rg + DEC_RG * j;
         link[j] = -1;
         if (n < R) {   // position of the read slot in the ascending write list
             int lo = 0;
@@ -1109,20 +1256,19 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void decode_kernel(
             link[j] = lw[lo] == rslot[j] ? lo : -1;
         }
     }
-    float al = load_scalar(alpha, in_dtype, stream), be = load_scalar(beta, in_dtype, stream);
     sdm_gates_of(gA, gbdt, stream % H, al, be);
-    float* tab = mem + (size_t)stream * N * dv;
 
     for (int c0 = 0; c0 < dv; c0 += DEC_COLS) {
         const int col = c0 + cq * 4;
         const bool colok = col < dv;      // d_v is a multiple of 4: whole quads
         const int cl = colok ? col : dv - 4;
-        v4f P[DEC_ROWS], Q[DEC_ROWS];
+        if (c0 > 0) {
 #pragma unroll
-        for (int j = 0; j < DEC_ROWS; ++j) {
-            const int n = rg + DEC_RG * j;
-            if (n < W) P[j] = ld4(tab + (size_t)wslot[j] * dv + cl);
-            if (n < R) Q[j] = ld4(tab + (size_t)rslot[j] * dv + cl);
+            for (int j = 0; j < DEC_ROWS; ++j) {
+                const int n = rg + DEC_RG * j;
+                if (n < W) P[j] = ld4(tab + (size_t)wslot[j] * dv + cl);
+                if (n < R) Q[j] = ld4(tab + (size_t)rslot[j] * dv + cl);
+            }
         }
         v4f up = v4zero();
 #pragma unroll
@@ -1133,7 +1279,7 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void decode_kernel(
         v4f u = v4zero();
 #pragma unroll
         for (int g = 0; g < DEC_RG; ++g) u += ld4(red + g * DEC_COLS + cq * 4);
-        const v4f e = be * (load_quad(v, in_dtype, (size_t)stream * dv + cl) - u);
+        const v4f e = be * ((c0 == 0 ? v_first : load_quad(v, in_dtype, (size_t)stream * dv + cl)) - u);
 #pragma unroll
         for (int j = 0; j < DEC_ROWS; ++j) {
             const int n = rg + DEC_RG * j;
@@ -1164,9 +1310,6 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void decode_kernel(
     }
 }
 
-constexpr size_t decode_scan_lds_bytes(int W) {
-    return (size_t)(MAXK_BIG + DEC_RG * DEC_COLS + (size_t)W * DEC_COLS) * sizeof(float);
-}
 
 // Backward of the weights through softmax and the sub-key scores: one wave
 // per token.  Lane l first forms, for slots n = 64 r + l < k (r < KR),
@@ -1265,12 +1408,6 @@ __global__ __launch_bounds__(256) void address_bwd_kernel(const XT* __restrict__
     }
 }
 
-// LDS of a tile: padded score rows, per-wave lists and sort buffer, and for
-// k > 64 the pair list.
-constexpr size_t address_lds_bytes(int E, int AT, int KM) {
-    return (size_t)AT * 2 * E * SDM_WAVE * sizeof(float) + AWAVES * 3 * KM * sizeof(Entry) +
-           AWAVES * SDM_WAVE * sizeof(uint64_t) + (KM > MAXK ? MAXCAND_BIG * SDM_WAVE * sizeof(uint16_t) : 0);
-}
 // The same for address_kernel's tile (one half of scores and the shortlists
 // for half_seq shapes).
 template <int E, int KM>
@@ -1398,7 +1535,7 @@ hipError_t launch_decode_m(const void* q, const void* k, const void* cb_q, const
     const XT* ck = static_cast<const XT*>(cb_k);
 #define SDM_DEC_CASE(EE, KM)                                                                              \
     {                                                                                                     \
-        const size_t sm = std::max(address_lds_bytes(EE, atile<EE>(), KM), decode_scan_lds_bytes(topk)); \
+        const size_t sm = decode_lds_bytes(EE, KM, topk);                                                  \
         auto kfn = decode_kernel<XT, MODE, EE, KM>;                                                       \
         hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize,  \
                                            (int)sm);                                                      \

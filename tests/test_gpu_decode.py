@@ -104,3 +104,62 @@ def test_decode_with_undo_log_takes_the_pipelined_path():
     n_dec, n_scan = sdm.profile_read("decode")[1], sdm.profile_read("fwd_scan")[1]
     sdm.profile_enable(False)
     assert n_dec == 0 and n_scan == 1
+
+
+def test_decode_graph_replays_match_eager():
+    """One decode step captured in a HIP graph (the fused single-token launch) and
+    replayed token after token: each replay's ids, weights and y, and the memory at
+    the end, equal the same steps run eagerly on a copy of the memory, bit for bit.
+    Between replays the inputs of the next token are copied into the captured
+    buffers and other eager work runs."""
+    w = CASES["bf16-mfma-k32"]
+    inp = synth.Inputs(w)
+    g = dict(q=to_dev(inp.q), k=to_dev(inp.k), v=to_dev(inp.v), al=to_dev(inp.alpha), be=to_dev(inp.beta))
+    cb = to_dev(inp.codebook)
+    mem0 = init_memory(w, inp)
+    Bx, Hx = inp.shape_bh
+    names = ("q", "k", "v", "al", "be")
+    # eager steps on a copy
+    mem_e = mem0.clone()
+    ws_e = sdm.fwd_workspace(Bx, Hx, 1, w.topk, w.topk, DEV)
+    eager = []
+    for t in range(w.T):
+        q, k, v, al, be = (_token(g[n], t) for n in names)
+        o = sdm.forward(q, k, cb, cb, v, al, be, mem_e, w.N, w.topk, workspace=ws_e)
+        torch.cuda.synchronize()
+        eager.append({kk: o[kk].clone() for kk in ("r_idx", "r_val", "w_idx", "w_val", "y")})
+    # the captured step: fixed input, output and state buffers
+    buf = {n: _token(g[n], 0).clone() for n in names}
+    mem_g = mem0.clone()
+    ws_g = sdm.fwd_workspace(Bx, Hx, 1, w.topk, w.topk, DEV)
+    y = torch.empty((Bx, Hx, 1, w.d_v), dtype=torch.float32, device=DEV)
+    outs = {n: torch.empty((Bx, Hx, 1, w.topk), dtype=dt, device=DEV)
+            for n, dt in (("r_idx", torch.int32), ("r_val", torch.float32), ("w_idx", torch.int32),
+                          ("w_val", torch.float32))}
+
+    def step():
+        sdm.forward(buf["q"], buf["k"], cb, cb, buf["v"], buf["al"], buf["be"], mem_g, w.N, w.topk,
+                    workspace=ws_g, y=y, out=outs)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()   # warm-up outside the capture
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    torch.cuda.synchronize()
+    mem_g.copy_(mem0)   # the warm-up step changed the state; the capture ran nothing
+    scratch = torch.zeros(1 << 20, device=DEV)
+    for t in range(w.T):
+        for n in names:
+            buf[n].copy_(_token(g[n], t))
+        scratch.add_(1.0)   # other eager work between replays
+        graph.replay()
+        torch.cuda.synchronize()
+        for kk in ("r_idx", "r_val", "w_idx", "w_val"):
+            assert torch.equal(outs[kk], eager[t][kk]), (t, kk)
+        assert torch.equal(y, eager[t]["y"]), t
+    assert torch.equal(mem_g, mem_e)
