@@ -129,7 +129,7 @@ __device__ __forceinline__ void fwd_token(const FwdCtx<VT, SW, PD, K, SAVE>& c, 
         const bool rok = n < c.W;
         const int nn = rok ? n : 0;
         const int l = lk[nn];
-        const int fidx = l >= 0 ? (((t - (l >> 8)) & (PD - 1)) * c.W + min(l & 255, c.W - 1)) : 0;
+        const int fidx = l >= 0 ? min(l, PD * c.W - 1) : 0;   // the writer's ring row
         const v4f f = ld4(c.fring + fidx * SW + c.cq * 4);
         v4f P = v4sel(l >= 0, f, Pw[k]);
         P = v4sel(rok, P, v4zero());
@@ -159,7 +159,7 @@ __device__ __forceinline__ void fwd_token(const FwdCtx<VT, SW, PD, K, SAVE>& c, 
         const bool rok = m < c.R;
         const int mm = rok ? m : 0;
         const int l = lk[c.W + mm];
-        const int fidx = l >= 0 ? (((t - (l >> 8)) & (PD - 1)) * c.W + min(l & 255, c.W - 1)) : 0;
+        const int fidx = l >= 0 ? min(l, PD * c.W - 1) : 0;
         const v4f f = ld4(c.fring + fidx * SW + c.cq * 4);
         const v4f P = v4sel(l >= 0, f, Pr[k]);
         const float rho = rok ? reinterpret_cast<const float*>(rec + L.off_rval)[mm] : 0.f;
@@ -377,21 +377,47 @@ __device__ __forceinline__ void fwd_token_line(const FwdCtx<VT, SW, PD, 2, SAVE>
     const float be = reinterpret_cast<const float*>(rec + L.off_ab)[1];
     const short* lk = reinterpret_cast<const short*>(rec + L.off_link);
 
+    // pre-write value of write entry n: a ring row if a token still in flight
+    // wrote it, else the row loaded from HBM
+    auto pre_write = [&](int n) -> v4f {
+        const int l = lk[n];
+        const int fidx = l >= 0 ? min(l, PD * FR - 1) : 0;   // the writer's ring row
+        return v4sel(l >= 0, ld4(c.fring + fidx * SW + c.cq * 4), fl_ld<SW, FR>(lb, 0, n, q));
+    };
+    const int own0 = (t & (PD - 1)) * FR;   // this token's rows in the ring
     v4f D[K];
     float kap[K];
     v4f up = v4zero();
 #pragma unroll
     for (int k = 0; k < K; ++k) {
         const int n = c.rg + RG * k;
-        const int l = lk[n];
-        const int fidx = l >= 0 ? (((t - (l >> 8)) & (PD - 1)) * FR + min(l & 255, FR - 1)) : 0;
-        const v4f P = v4sel(l >= 0, ld4(c.fring + fidx * SW + c.cq * 4), fl_ld<SW, FR>(lb, 0, n, q));
+        const v4f P = pre_write(n);
         kap[k] = reinterpret_cast<const float*>(rec + L.off_wval)[n];
         if (SAVE) fl_st<SW, FR>(sb, 1, n, q, P);
         D[k] = al * P;
         up = v4fma(kap[k], D[k], up);
     }
-    rows_allreduce4<CQ>(up);
+    // read rows on the post-write memory, taken before the write: a row this
+    // token does not write has its value now; a row it writes (link to its own
+    // write entry n) ends as D_n + kappa_n e, so it adds rho D_n now and
+    // rho kappa_n times e once e is known (yc, the same for every column)
+    v4f yp = v4zero();
+    float yc = 0.f;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        const int m = c.rg + RG * k;
+        const int l = lk[FR + m];
+        const float rho = reinterpret_cast<const float*>(rec + L.off_rval)[m];
+        const bool own = (unsigned)(l - own0) < (unsigned)FR;   // a row this token writes (entry l - own0)
+        const int n = own ? l - own0 : 0;
+        const int fidx = l >= 0 ? min(l, PD * FR - 1) : 0;
+        const v4f Pr = v4sel(l >= 0, ld4(c.fring + fidx * SW + c.cq * 4), fl_ld<SW, FR>(lb, 1, m, q));
+        const v4f Pn = pre_write(own ? n : 0);
+        yp = v4fma(rho, v4sel(own, al * Pn, Pr), yp);
+        yc += own ? rho * reinterpret_cast<const float*>(rec + L.off_wval)[n] : 0.f;
+    }
+    rows_allreduce8<CQ>(up, yp);
+    yc = class_sum<CQ>(yc);
     const v4f vv = ld4v(reinterpret_cast<const VT*>(c.vring + (t & (NS - 1)) * VB) + c.cq * 4);
     const v4f e = be * (vv - up);
 #pragma unroll
@@ -401,17 +427,7 @@ __device__ __forceinline__ void fwd_token_line(const FwdCtx<VT, SW, PD, 2, SAVE>
         st4(c.fring + ((t & (PD - 1)) * FR + n) * SW + c.cq * 4, nw);
         fl_st<SW, FR>(sb, 0, n, q, nw);
     }
-    v4f yp = v4zero();
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-        const int m = c.rg + RG * k;
-        const int l = lk[FR + m];
-        const int fidx = l >= 0 ? (((t - (l >> 8)) & (PD - 1)) * FR + min(l & 255, FR - 1)) : 0;
-        const v4f P = v4sel(l >= 0, ld4(c.fring + fidx * SW + c.cq * 4), fl_ld<SW, FR>(lb, 1, m, q));
-        yp = v4fma(reinterpret_cast<const float*>(rec + L.off_rval)[m], P, yp);
-    }
-    rows_allreduce4<CQ>(yp);
-    if (c.rg == 0) st4(c.ystream + (size_t)t * c.dv, yp);
+    if (c.rg == 0) st4(c.ystream + (size_t)t * c.dv, v4fma(yc, e, yp));
 }
 
 template <typename VT, int SW, int PD, bool SAVE, int NS, int FR>

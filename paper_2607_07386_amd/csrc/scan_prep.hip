@@ -5,8 +5,9 @@
 // are clamped to [0, N) (a bad id is flagged, never dereferenced).  For every
 // row a scan token reads, the record says where its current value lives when
 // the token in flight that last modified it is still inside the scan's
-// prefetch window: the link (d << 8 | entry) names that token (d tokens
-// away) and its ring entry; -1 means the row is read from HBM.
+// prefetch window: the forward's link is that token's row in the scan's ring
+// ((t - d) mod PD) W + entry, d tokens away; the backward's names the token and
+// entry as (d << 8 | entry); -1 means the row is read from HBM.
 //
 // One thread per (token, row) searches the slot lists of the candidate tokens
 // in the window.  Addressing returns every list in ascending slot order, so a
@@ -71,7 +72,9 @@ __device__ __forceinline__ void mark_sorted(const int* lst, int nl, int len, int
 // ---------------------------------------------------------------- forward
 // Token t, write row n: latest writer t-d, 1 <= d < PD, of the same slot.
 // Token t, read row m: latest writer t-d, 0 <= d < PD (d = 0: t itself).
-// Entry = position of the slot in that writer's write list.  Records are made
+// The link is that writer's row in the scan's ring of written rows,
+// ((t - d) mod PD) W + e, with e the position of the slot in the writer's
+// write list, so the scan reads the ring without index arithmetic.  Records are made
 // for tokens [ta, te) of each stream; writers before ta are not linked (a scan
 // started at ta finds their rows in HBM).
 template <int PD>
@@ -121,7 +124,7 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
         for (int d = dhi; d >= dlo; --d) {
             const int u = tl + PD - 1 - d;       // write list of token t - d
             const int n = find_slot(wl + u * W, W, wsrt[u] != 0, slot);
-            if (n >= 0) link = (short)((d << 8) | n);
+            if (n >= 0) link = (short)(((t0 + tl - d) & (PD - 1)) * W + n);   // ring row of (t - d, n)
         }
         lk[i] = link;
     }

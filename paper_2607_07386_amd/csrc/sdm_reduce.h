@@ -99,6 +99,12 @@ __device__ __forceinline__ void rows_allreduce8(v4f& a, v4f& b) {
     b = v4f{o0[2], o1[2], o0[3], o1[3]};
 }
 
+// The sum of v over the lanes of this lane's class (lane % CQ), in every lane.
+template <int CQ>
+__device__ __forceinline__ float class_sum(float v) {
+    return add_xor<32>(add_xor<16>(row_sum_from<CQ>(v)));
+}
+
 // Same for the four floats of one v4f (16 VALU instructions at CQ = 2).
 template <int CQ>
 __device__ __forceinline__ void rows_allreduce4(v4f& a) {

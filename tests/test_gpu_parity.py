@@ -662,7 +662,7 @@ def _links_fwd(wi, ri, PD):
                     break
                 hit = np.nonzero(wi[t - d] == slot)[0]
                 if hit.size:
-                    out[t, r] = (d << 8) | hit[0]
+                    out[t, r] = ((t - d) % PD) * W + hit[0]   # the writer's row in the scan's ring
                     break
     return out
 
