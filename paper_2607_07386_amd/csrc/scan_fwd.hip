@@ -151,7 +151,9 @@ __device__ __forceinline__ void fwd_token(const FwdCtx<VT, SW, PD, K, SAVE>& c, 
             if (c.colok) st4(c.tab + (size_t)reinterpret_cast<const int*>(rec)[n] * c.dv, nw);
         }
     }
-    // read rows on the post-write memory
+    // read rows on the post-write memory, y = sum rho' P + yc e: P the value
+    // before the token (a row the token writes carries rho alpha as rho', and
+    // its rho kappa in yc)
     v4f yp = v4zero();
 #pragma unroll
     for (int k = 0; k < K; ++k) {
@@ -167,7 +169,8 @@ __device__ __forceinline__ void fwd_token(const FwdCtx<VT, SW, PD, K, SAVE>& c, 
     }
 #pragma unroll
     for (int m = CQ; m < SDM_WAVE; m <<= 1) yp += v4shfl_xor(yp, m);
-    if (c.rg == 0 && c.colok) st4(c.ystream + (size_t)t * c.dv, yp);
+    const float yc = reinterpret_cast<const float*>(rec + L.off_ab)[2];
+    if (c.rg == 0 && c.colok) st4(c.ystream + (size_t)t * c.dv, v4fma(yc, e, yp));
 }
 
 template <typename VT, int SW, int PD, int K, int NR, bool SAVE>
@@ -384,7 +387,6 @@ __device__ __forceinline__ void fwd_token_line(const FwdCtx<VT, SW, PD, 2, SAVE>
         const int fidx = l >= 0 ? min(l, PD * FR - 1) : 0;   // the writer's ring row
         return v4sel(l >= 0, ld4(c.fring + fidx * SW + c.cq * 4), fl_ld<SW, FR>(lb, 0, n, q));
     };
-    const int own0 = (t & (PD - 1)) * FR;   // this token's rows in the ring
     v4f D[K];
     float kap[K];
     v4f up = v4zero();
@@ -397,27 +399,20 @@ __device__ __forceinline__ void fwd_token_line(const FwdCtx<VT, SW, PD, 2, SAVE>
         D[k] = al * P;
         up = v4fma(kap[k], D[k], up);
     }
-    // read rows on the post-write memory, taken before the write: a row this
-    // token does not write has its value now; a row it writes (link to its own
-    // write entry n) ends as D_n + kappa_n e, so it adds rho D_n now and
-    // rho kappa_n times e once e is known (yc, the same for every column)
+    // read rows on the post-write memory, before the write: y = sum rho' P +
+    // yc e, P the row's value before the token (a row the token writes carries
+    // rho alpha as rho', and its rho kappa in the record's yc)
     v4f yp = v4zero();
-    float yc = 0.f;
 #pragma unroll
     for (int k = 0; k < K; ++k) {
         const int m = c.rg + RG * k;
         const int l = lk[FR + m];
         const float rho = reinterpret_cast<const float*>(rec + L.off_rval)[m];
-        const bool own = (unsigned)(l - own0) < (unsigned)FR;   // a row this token writes (entry l - own0)
-        const int n = own ? l - own0 : 0;
         const int fidx = l >= 0 ? min(l, PD * FR - 1) : 0;
-        const v4f Pr = v4sel(l >= 0, ld4(c.fring + fidx * SW + c.cq * 4), fl_ld<SW, FR>(lb, 1, m, q));
-        const v4f Pn = pre_write(own ? n : 0);
-        yp = v4fma(rho, v4sel(own, al * Pn, Pr), yp);
-        yc += own ? rho * reinterpret_cast<const float*>(rec + L.off_wval)[n] : 0.f;
+        yp = v4fma(rho, v4sel(l >= 0, ld4(c.fring + fidx * SW + c.cq * 4), fl_ld<SW, FR>(lb, 1, m, q)), yp);
     }
     rows_allreduce8<CQ>(up, yp);
-    yc = class_sum<CQ>(yc);
+    const float yc = reinterpret_cast<const float*>(rec + L.off_ab)[2];
     const v4f vv = ld4v(reinterpret_cast<const VT*>(c.vring + (t & (NS - 1)) * VB) + c.cq * 4);
     const v4f e = be * (vv - up);
 #pragma unroll
@@ -473,7 +468,7 @@ __global__ __launch_bounds__(FLW * SDM_WAVE) void scan_fwd_line_kernel(
     static_assert(NS >= LEAD && NS >= PD, "record ring too small");
     static_assert(FLine<SW, FR>::NLI * FLine<SW, FR>::LRI * FLW == FR, "FR / 4 rows per wave");
     // records of G tokens in NC 16-byte chunks per lane of the workgroup
-    constexpr int NC = (G * ((20 * FR + 8 + 15) / 16 * 16) + FLW * SDM_WAVE * 16 - 1) / (FLW * SDM_WAVE * 16);
+    constexpr int NC = (G * ((20 * FR + 12 + 15) / 16 * 16) + FLW * SDM_WAVE * 16 - 1) / (FLW * SDM_WAVE * 16);
 
     // In the pipelined forward the next stage's addressing and records share the
     // CUs; the scan waves are latency-bound and go first at each issue slot
@@ -555,11 +550,11 @@ constexpr int FWD_PD = SDM_FWD_PD;
 
 // Staging registers per lane (16 bytes each) for a block of G records: enough
 // for every record of a shape with max(W, R) <= K RG, whose record takes at
-// most 20 K RG + 8 bytes rounded up to 16.
+// most 20 K RG + 12 bytes rounded up to 16.
 template <int SW>
 constexpr int nr_for_k(int K) {
     constexpr int RG = SDM_WAVE / (SW / 4);
-    return (G * ((20 * K * RG + 8 + 15) / 16 * 16) + SDM_WAVE * 16 - 1) / (SDM_WAVE * 16);
+    return (G * ((20 * K * RG + 12 + 15) / 16 * 16) + SDM_WAVE * 16 - 1) / (SDM_WAVE * 16);
 }
 
 struct FwdPlan {

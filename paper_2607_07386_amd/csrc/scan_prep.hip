@@ -70,13 +70,17 @@ __device__ __forceinline__ void mark_sorted(const int* lst, int nl, int len, int
 }
 
 // ---------------------------------------------------------------- forward
-// Token t, write row n: latest writer t-d, 1 <= d < PD, of the same slot.
-// Token t, read row m: latest writer t-d, 0 <= d < PD (d = 0: t itself).
-// The link is that writer's row in the scan's ring of written rows,
-// ((t - d) mod PD) W + e, with e the position of the slot in the writer's
-// write list, so the scan reads the ring without index arithmetic.  Records are made
-// for tokens [ta, te) of each stream; writers before ta are not linked (a scan
-// started at ta finds their rows in HBM).
+// Token t, row n of either list: the latest writer t-d, 1 <= d < PD, of the
+// same slot, as that writer's row in the scan's ring of written rows,
+// ((t - d) mod PD) W + e, with e the position of the slot in its write list,
+// so the scan reads the ring without index arithmetic.  A read row whose slot
+// token t itself writes (entry n) ends the token at alpha P + kappa_n e, with P
+// the slot's value before the token, which is where the link points: its
+// weight in the record is rho alpha, and the token's record holds
+// yc = sum of rho kappa_n over such rows, so that y = sum rho' P + yc e needs
+// nothing the token writes.  Records are made for tokens [ta, te) of each
+// stream; writers before ta are not linked (a scan started at ta finds their
+// rows in HBM).
 template <int PD>
 __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict__ w_idx,
                                                        const float* __restrict__ w_val,
@@ -89,7 +93,7 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
                                                        unsigned int* __restrict__ err,
                                                        const float* __restrict__ gA,
                                                        const float* __restrict__ gbdt, int H) {
-    extern __shared__ int sm[];
+    extern __shared__ __align__(16) int sm[];
     const FwdRec L = fwd_rec_layout(W, R);
     const int stream = blockIdx.y;
     const int t0 = ta + blockIdx.x * PT;
@@ -100,7 +104,9 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
     int* wl = sm;                                        // [PT+PD-1][W]
     int* rl = wl + (PT + PD - 1) * W;                    // [PT][R]
     int* wsrt = rl + PT * R;                             // [PT+PD-1]
-    short* lk = reinterpret_cast<short*>(wsrt + PT + PD - 1);   // [PT][W + R] links
+    float* gab = reinterpret_cast<float*>(wsrt + PT + PD - 1);   // [PT][3]: alpha, beta, yc
+    short* own = reinterpret_cast<short*>(gab + 3 * PT);         // [PT][R] own write entry of a read row, or -1
+    short* lk = own + PT * R;                                     // [PT][W + R] links
     const size_t sbase = (size_t)stream * T;
     unsigned int bad = 0u;
 
@@ -110,6 +116,13 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
     }
     for (int i = threadIdx.x; i < ntok * R; i += blockDim.x)
         rl[i] = clamp_slot(r_idx[(sbase + t0) * R + i], N, bad);
+    for (int tl = threadIdx.x; tl < ntok; tl += blockDim.x) {
+        float al, be;
+        load_gates(alpha, beta, in_dtype, sbase + t0 + tl, al, be);
+        sdm_gates_of(gA, gbdt, stream % H, al, be);
+        gab[3 * tl] = al;
+        gab[3 * tl + 1] = be;
+    }
     __syncthreads();
     mark_sorted(wl, nw, W, wsrt);
     __syncthreads();
@@ -118,15 +131,29 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
         const int tl = i / nrow, r = i % nrow;
         const bool wrow = r < W;
         const int slot = wrow ? wl[(tl + PD - 1) * W + r] : rl[tl * R + (r - W)];
-        const int dlo = wrow ? 1 : 0;           // a read row may hit its own token
         const int dhi = min(PD - 1, t0 + tl - ta);   // no writer before token ta
         short link = -1;
-        for (int d = dhi; d >= dlo; --d) {
+        for (int d = dhi; d >= 1; --d) {
             const int u = tl + PD - 1 - d;       // write list of token t - d
             const int n = find_slot(wl + u * W, W, wsrt[u] != 0, slot);
             if (n >= 0) link = (short)(((t0 + tl - d) & (PD - 1)) * W + n);   // ring row of (t - d, n)
         }
         lk[i] = link;
+        if (!wrow) {
+            const int u = tl + PD - 1;           // this token's own write list
+            own[tl * R + (r - W)] = (short)find_slot(wl + u * W, W, wsrt[u] != 0, slot);
+        }
+    }
+    __syncthreads();
+    // yc of each token, its read rows in order
+    for (int tl = threadIdx.x; tl < ntok; tl += blockDim.x) {
+        const size_t tok = sbase + t0 + tl;
+        float yc = 0.f;
+        for (int m = 0; m < R; ++m) {
+            const int n = own[tl * R + m];
+            if (n >= 0) yc += r_val[tok * R + m] * w_val[tok * W + n];
+        }
+        gab[3 * tl + 2] = yc;
     }
     __syncthreads();
 
@@ -144,17 +171,16 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
         } else if (off < L.off_rval) {
             v = (uint32_t)rl[tl * R + (off - L.off_rslot) / 4];
         } else if (off < L.off_link) {
-            v = __float_as_uint(r_val[tok * R + (off - L.off_rval) / 4]);
+            const int m = (off - L.off_rval) / 4;
+            const float rho = r_val[tok * R + m];
+            v = __float_as_uint(own[tl * R + m] >= 0 ? rho * gab[3 * tl] : rho);
         } else if (off < L.off_link + 2 * nrow) {
             const int e = (off - L.off_link) / 2;   // two int16 links per word
             const uint32_t l0 = (uint16_t)lk[tl * nrow + e];
             const uint32_t l1 = e + 1 < nrow ? (uint16_t)lk[tl * nrow + e + 1] : 0xffffu;
             v = l0 | (l1 << 16);
-        } else if (off == L.off_ab || off == L.off_ab + 4) {
-            float al, be;
-            load_gates(alpha, beta, in_dtype, tok, al, be);
-            sdm_gates_of(gA, gbdt, stream % H, al, be);
-            v = __float_as_uint(off == L.off_ab ? al : be);
+        } else if (off >= L.off_ab && off < L.off_ab + 12) {
+            v = __float_as_uint(gab[3 * tl + (off - L.off_ab) / 4]);   // alpha, beta, yc
         }
         out[i] = v;
     }
@@ -302,8 +328,8 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const int32_t* __restrict
 
 template <int PD>
 size_t fwd_prep_lds(int W, int R) {
-    return sizeof(int) * ((size_t)(PT + PD - 1) * (W + 1) + (size_t)PT * R) +
-           sizeof(short) * (size_t)PT * (W + R);
+    return sizeof(int) * ((size_t)(PT + PD - 1) * (W + 1) + (size_t)PT * R + 3 * PT) +
+           sizeof(short) * (size_t)PT * (W + 2 * R);
 }
 template <int PD>
 size_t bwd_prep_lds(int W, int R) {

@@ -15,7 +15,9 @@
 #define SDM_FWD_PD_DEEP 16
 
 // Per-token record of the forward scan (written by the prep kernel, staged in
-// LDS by the scan): slots and weights of both sides, forwarding links, gates.
+// LDS by the scan): slots and weights of both sides (a read row whose slot the
+// token writes weighted rho alpha), forwarding links, gates and yc, the sum of
+// rho kappa over those rows.
 struct FwdRec {
     int W, R;
     int off_wval, off_rslot, off_rval, off_link, off_ab, bytes;
@@ -29,8 +31,8 @@ __host__ __device__ inline FwdRec fwd_rec_layout(int W, int R) {
     r.off_rslot = 8 * W;
     r.off_rval = 8 * W + 4 * R;
     r.off_link = 8 * W + 8 * R;
-    r.off_ab = (r.off_link + 2 * (W + R) + 3) & ~3;
-    r.bytes = (r.off_ab + 8 + 15) & ~15;
+    r.off_ab = (r.off_link + 2 * (W + R) + 3) & ~3;   // alpha, beta, yc
+    r.bytes = (r.off_ab + 12 + 15) & ~15;
     return r;
 }
 

@@ -657,7 +657,7 @@ def _links_fwd(wi, ri, PD):
     for t in range(T):
         for r in range(W + R):
             slot = wi[t, r] if r < W else ri[t, r - W]
-            for d in range(1 if r < W else 0, PD):
+            for d in range(1, PD):   # earlier writers only, for both lists
                 if t - d < 0:
                     break
                 hit = np.nonzero(wi[t - d] == slot)[0]
