@@ -104,11 +104,12 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
     int* wl = sm;                                        // [PT+PD-1][W]
     int* rl = wl + (PT + PD - 1) * W;                    // [PT][R]
     int* wsrt = rl + PT * R;                             // [PT+PD-1]
-    float* gab = reinterpret_cast<float*>(wsrt + PT + PD - 1);   // [PT][3]: alpha, beta, yc
-    short* own = reinterpret_cast<short*>(gab + 3 * PT);         // [PT][R] own write entry of a read row, or -1
-    short* lk = own + PT * R;                                     // [PT][W + R] links
+    const int MW = (R + 31) / 32;
+    unsigned int* omask = reinterpret_cast<unsigned int*>(wsrt + PT + PD - 1);   // [PT][MW]: read rows the token writes
+    short* lk = reinterpret_cast<short*>(omask + PT * MW);       // [PT][W + R] links
     const size_t sbase = (size_t)stream * T;
     unsigned int bad = 0u;
+    for (int i = threadIdx.x; i < PT * MW; i += blockDim.x) omask[i] = 0u;
 
     for (int i = threadIdx.x; i < nw * W; i += blockDim.x) {
         const int t = tb + i / W;
@@ -116,13 +117,6 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
     }
     for (int i = threadIdx.x; i < ntok * R; i += blockDim.x)
         rl[i] = clamp_slot(r_idx[(sbase + t0) * R + i], N, bad);
-    for (int tl = threadIdx.x; tl < ntok; tl += blockDim.x) {
-        float al, be;
-        load_gates(alpha, beta, in_dtype, sbase + t0 + tl, al, be);
-        sdm_gates_of(gA, gbdt, stream % H, al, be);
-        gab[3 * tl] = al;
-        gab[3 * tl + 1] = be;
-    }
     __syncthreads();
     mark_sorted(wl, nw, W, wsrt);
     __syncthreads();
@@ -140,20 +134,9 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
         }
         lk[i] = link;
         if (!wrow) {
-            const int u = tl + PD - 1;           // this token's own write list
-            own[tl * R + (r - W)] = (short)find_slot(wl + u * W, W, wsrt[u] != 0, slot);
+            const int u = tl + PD - 1, m = r - W;   // this token's own write list
+            if (find_slot(wl + u * W, W, wsrt[u] != 0, slot) >= 0) atomicOr(&omask[tl * MW + m / 32], 1u << (m % 32));
         }
-    }
-    __syncthreads();
-    // yc of each token, its read rows in order
-    for (int tl = threadIdx.x; tl < ntok; tl += blockDim.x) {
-        const size_t tok = sbase + t0 + tl;
-        float yc = 0.f;
-        for (int m = 0; m < R; ++m) {
-            const int n = own[tl * R + m];
-            if (n >= 0) yc += r_val[tok * R + m] * w_val[tok * W + n];
-        }
-        gab[3 * tl + 2] = yc;
     }
     __syncthreads();
 
@@ -172,15 +155,36 @@ __global__ __launch_bounds__(256) void fwd_prep_kernel(const int32_t* __restrict
             v = (uint32_t)rl[tl * R + (off - L.off_rslot) / 4];
         } else if (off < L.off_link) {
             const int m = (off - L.off_rval) / 4;
-            const float rho = r_val[tok * R + m];
-            v = __float_as_uint(own[tl * R + m] >= 0 ? rho * gab[3 * tl] : rho);
+            float rho = r_val[tok * R + m];
+            if ((omask[tl * MW + m / 32] >> (m % 32)) & 1u) {   // rare: rho alpha
+                float al, be;
+                load_gates(alpha, beta, in_dtype, tok, al, be);
+                sdm_gates_of(gA, gbdt, stream % H, al, be);
+                rho *= al;
+            }
+            v = __float_as_uint(rho);
         } else if (off < L.off_link + 2 * nrow) {
             const int e = (off - L.off_link) / 2;   // two int16 links per word
             const uint32_t l0 = (uint16_t)lk[tl * nrow + e];
             const uint32_t l1 = e + 1 < nrow ? (uint16_t)lk[tl * nrow + e + 1] : 0xffffu;
             v = l0 | (l1 << 16);
-        } else if (off >= L.off_ab && off < L.off_ab + 12) {
-            v = __float_as_uint(gab[3 * tl + (off - L.off_ab) / 4]);   // alpha, beta, yc
+        } else if (off == L.off_ab || off == L.off_ab + 4) {
+            float al, be;
+            load_gates(alpha, beta, in_dtype, tok, al, be);
+            sdm_gates_of(gA, gbdt, stream % H, al, be);
+            v = __float_as_uint(off == L.off_ab ? al : be);
+        } else if (off == L.off_ab + 8) {
+            // yc: rho kappa_n summed over the (rare) read rows of slots the token writes, in row order
+            const int u = tl + PD - 1;
+            float yc = 0.f;
+            for (int wd = 0; wd < MW; ++wd) {
+                for (unsigned int b = omask[tl * MW + wd]; b; b &= b - 1) {
+                    const int m = 32 * wd + __ffs((int)b) - 1;
+                    const int n = find_slot(wl + u * W, W, wsrt[u] != 0, rl[tl * R + m]);
+                    yc += r_val[tok * R + m] * w_val[tok * W + n];
+                }
+            }
+            v = __float_as_uint(yc);
         }
         out[i] = v;
     }
@@ -328,8 +332,8 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const int32_t* __restrict
 
 template <int PD>
 size_t fwd_prep_lds(int W, int R) {
-    return sizeof(int) * ((size_t)(PT + PD - 1) * (W + 1) + (size_t)PT * R + 3 * PT) +
-           sizeof(short) * (size_t)PT * (W + 2 * R);
+    return sizeof(int) * ((size_t)(PT + PD - 1) * (W + 1) + (size_t)PT * R + (size_t)PT * ((R + 31) / 32)) +
+           sizeof(short) * (size_t)PT * (W + R);
 }
 template <int PD>
 size_t bwd_prep_lds(int W, int R) {
