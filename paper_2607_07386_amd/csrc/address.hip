@@ -1010,6 +1010,299 @@ __device__ __forceinline__ void address_tile_halves(const XT* __restrict__ x, co
     }
 }
 
+// ---- scores held in the matrix cores' registers (bf16 codebooks, d_k / 2
+//      <= 64, k <= 32) -------------------------------------------------------
+// A workgroup scores TOK = 16 RT tokens against one half's s sub-keys and keeps
+// the scores where the MFMA leaves them: wave w, lane (r, q) holds sub-key
+// (w + 4 i) 16 + r of tile i (i < E) for tokens 4 q + v of each 16-row tile.
+// So for every token the 64 lanes' (wave, r) groups of E scores each are the
+// groups of the stage-1 bound: the k-th largest group maximum is reached by at
+// least k scores, and every score of the top k is at or above it.  Per half:
+//   1. group maxima -> LDS; each token's bound (k-th largest maximum, taken to
+//      the sign, exponent and 11 mantissa bits) by one wave's ballots;
+//   2. every lane appends its scores at or above the bound to the token's
+//      candidate list (an LDS counter per token; the order does not matter);
+//   3. the token's wave sorts its candidates under (score desc, id asc): the
+//      ranked shortlist.  More than 64 candidates (or fewer than k, which only
+//      non-finite scores give): the wave recomputes the token's row of scores
+//      with the same MFMA steps into LDS and takes the general selection.
+// Stage 2 (pruned pairs, id sort, softmax) as on the other paths.  Nothing but
+// group maxima and candidates goes through LDS, and a codebook fetch serves 16
+// RT tokens.
+constexpr int RKS = 33;   // shortlist entries: k <= 32, then one -inf entry (pair ranks past the count)
+
+template <int E, int RT>
+struct RegTile {
+    static constexpr int TOK = 16 * RT;
+    static constexpr int SP = E * SDM_WAVE;
+    static constexpr size_t G_OFF = 0;                                         // [TOK][64] float
+    static constexpr size_t THR_OFF = G_OFF + (size_t)TOK * SDM_WAVE * 4;      // [TOK] float
+    static constexpr size_t CNT_OFF = THR_OFF + (size_t)TOK * 4;               // [TOK] int
+    static constexpr size_t CAND_OFF = CNT_OFF + (size_t)TOK * 4;              // [TOK][64] uint2
+    static constexpr size_t SL_OFF = CAND_OFF + (size_t)TOK * SDM_WAVE * 8;    // [TOK][2][RKS] Entry
+    static constexpr size_t SCR_OFF = SL_OFF + (size_t)TOK * 2 * RKS * 8;      // [AWAVES][MAXK] Entry
+    static constexpr size_t KB_OFF = SCR_OFF + (size_t)AWAVES * MAXK * 8;      // [AWAVES][64] uint64
+    static constexpr size_t ROW_OFF = KB_OFF + (size_t)AWAVES * SDM_WAVE * 8;  // [AWAVES][SP] float
+    static constexpr size_t BYTES = ROW_OFF + (size_t)AWAVES * SP * 4;
+};
+
+// One 16 x 16 tile of scores: rows a (tokens), columns b (sub-keys), 64 deep.
+__device__ __forceinline__ sdm_f32x4 score_tile(const sdm_bf16x8 (&a)[2], const sdm_bf16x8 (&b)[2]) {
+    sdm_f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0], b[0], acc, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1], b[1], acc, 0, 0, 0);
+}
+
+// This lane's operand pieces: row t of x for one half (A; tl a row that
+// exists, loaded in its place when t does not), and sub-key j of one half (B);
+// zero past the rows or the depth.  The loads are unconditional, at clamped
+// addresses, so they carry no branches.
+__device__ __forceinline__ sdm_bf16x8 zero_unless(bool ok, sdm_bf16x8 v) {
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    u32x4 u = __builtin_bit_cast(u32x4, v);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) u[i] = ok ? u[i] : 0u;
+    return __builtin_bit_cast(sdm_bf16x8, u);
+}
+__device__ __forceinline__ void load_a_rows(const bf16_t* xs, int t, int tl, bool ok, int dk, int half, int dh,
+                                            int q, sdm_bf16x8 (&a)[2]) {
+    const bf16_t* xr = xs + (size_t)(ok ? t : tl) * dk + half * dh;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+        const int kc = ks * 32 + 8 * q;
+        a[ks] = zero_unless(ok && kc < dh, *reinterpret_cast<const sdm_bf16x8*>(xr + (kc < dh ? kc : 0)));
+    }
+}
+// (B past the depth is whatever the clamped load gives: A is zero there.  B
+// past the sub-keys is row s - 1: the caller sets those scores to -inf.)
+__device__ __forceinline__ void load_b_rows(const bf16_t* cbh, int half, int s, int j, int dh, int q,
+                                            sdm_bf16x8 (&b)[2]) {
+    const bf16_t* crow = cbh + ((size_t)half * s + min(j, s - 1)) * dh;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+        const int kc = ks * 32 + 8 * q;
+        b[ks] = *reinterpret_cast<const sdm_bf16x8*>(crow + (kc < dh ? kc : 0));
+    }
+}
+// 0 for a sub-key j < s, -inf past them (no lane mask involved).
+__device__ __forceinline__ float pad_of(int j, int s) {
+    return __int_as_float((int)(((uint32_t)((s - 1 - j) >> 31)) & 0xff800000u));
+}
+
+// Stage 1 of one token's half on the general path: its row of scores (token
+// `row` of the 16-row tile at t0, nr rows present) recomputed by the same MFMA
+// steps into frow, then the general selection into out.  Out of line: the
+// cold path of the register-resident kernel.
+template <int E>
+__device__ __noinline__ void reg_half_general(const bf16_t* xs, const bf16_t* cbh, int t0, int nr, int row, int dk,
+                                              int half, int s, int k, float* frow, Entry* scr, uint64_t* kbuf,
+                                              Entry* out) {
+    const int lane = lane_id();
+    const int r16 = lane % 16, q = lane / 16;
+    const int dh = dk / 2;
+    sdm_bf16x8 a[2];
+    load_a_rows(xs, t0 + r16, t0, r16 < nr, dk, half, dh, q, a);
+    for (int jt = 0; jt < AWAVES * E; ++jt) {
+        sdm_bf16x8 b[2];
+        const int j = jt * 16 + r16;
+        load_b_rows(cbh, half, s, j, dh, q, b);
+        const sdm_f32x4 acc = score_tile(a, b);
+        if (q == row / 4) {
+            const int v = row % 4;
+            const float f = v == 0 ? acc[0] : (v == 1 ? acc[1] : (v == 2 ? acc[2] : acc[3]));
+            frow[j] = f + pad_of(j, s);
+        }
+    }
+    wait_lds();
+    __builtin_amdgcn_wave_barrier();
+    half_topk<E>(frow, s, k, scr, kbuf, out);
+}
+
+// Stage 1 of one half for the tile's tokens (the register-resident kernel's
+// phases 1-3), written out once per half.  s and d_k pass through an opaque
+// copy first, so that nothing derived from them in one half (row addresses,
+// pads) is kept live into the other's selection phases.
+template <int E, int RT>
+__device__ __forceinline__ void reg_half(unsigned char* smem, const bf16_t* xs, const bf16_t* cbh, int t0, int nt,
+                                         int dk_in, int s_in, int k, int half) {
+    int s, dk;
+    asm volatile("s_mov_b32 %0, %1" : "=s"(s) : "s"(s_in));
+    asm volatile("s_mov_b32 %0, %1" : "=s"(dk) : "s"(dk_in));
+    using L = RegTile<E, RT>;
+    constexpr int NU = L::TOK / AWAVES;   // tokens per wave in the selection phases: wave + AWAVES u
+    constexpr int EG = E < 4 ? E : 4;     // tiles whose codebook pieces are loaded together
+    float* G = reinterpret_cast<float*>(smem + L::G_OFF);
+    float* thr = reinterpret_cast<float*>(smem + L::THR_OFF);
+    int* cnt = reinterpret_cast<int*>(smem + L::CNT_OFF);
+    uint2* cand = reinterpret_cast<uint2*>(smem + L::CAND_OFF);
+    Entry* sl = reinterpret_cast<Entry*>(smem + L::SL_OFF);
+    const int wave = threadIdx.x / SDM_WAVE;
+    const int lane = lane_id();
+    Entry* scr = reinterpret_cast<Entry*>(smem + L::SCR_OFF) + wave * MAXK;
+    uint64_t* kbuf = reinterpret_cast<uint64_t*>(smem + L::KB_OFF) + wave * SDM_WAVE;
+    float* frow = reinterpret_cast<float*>(smem + L::ROW_OFF) + wave * L::SP;
+    const int dh = dk / 2;
+    const int r16 = lane % 16, q = lane / 16;
+    // ---- scores of the tile in registers
+    float sc[RT][E][4];
+    {
+        sdm_bf16x8 a[RT][2];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+            load_a_rows(xs, t0 + 16 * rt + r16, t0, 16 * rt + r16 < nt, dk, half, dh, q, a[rt]);
+#pragma unroll
+        for (int i0 = 0; i0 < E; i0 += EG) {
+            sdm_bf16x8 b[EG][2];
+#pragma unroll
+            for (int i = 0; i < EG; ++i)
+                load_b_rows(cbh, half, s, (wave + AWAVES * (i0 + i)) * 16 + r16, dh, q, b[i]);
+#pragma unroll
+            for (int i = 0; i < EG; ++i) {
+                const float pad = pad_of((wave + AWAVES * (i0 + i)) * 16 + r16, s);
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) {
+                    const sdm_f32x4 acc = score_tile(a[rt], b[i]);
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) sc[rt][i0 + i][v] = acc[v] + pad;
+                }
+            }
+            // one group's codebook pieces in registers at a time
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    // ---- 1. group maxima, then each token's bound
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            float m = sc[rt][0][v];
+#pragma unroll
+            for (int i = 1; i < E; ++i) m = fmaxf(m, sc[rt][i][v]);
+            G[(16 * rt + 4 * q + v) * SDM_WAVE + wave * 16 + r16] = m;
+        }
+    __syncthreads();
+    {
+        uint32_t key[NU], tau[NU];
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+            key[u] = ord_key(G[(wave + AWAVES * u) * SDM_WAVE + lane]);
+            tau[u] = 0u;
+        }
+#pragma unroll
+        for (int bit = 31; bit >= 12; --bit) {
+#pragma unroll
+            for (int u = 0; u < NU; ++u) {
+                const uint32_t c = tau[u] | (1u << bit);
+                if (popc64(__ballot(key[u] >= c)) >= k) tau[u] = c;
+            }
+        }
+        if (lane == 0) {
+#pragma unroll
+            for (int u = 0; u < NU; ++u) {
+                const int tt = wave + AWAVES * u;
+                thr[tt] = tt < nt ? key_to_float(tau[u]) : INFINITY;   // no candidates past the tokens
+                cnt[tt] = 0;
+            }
+        }
+    }
+    __syncthreads();
+    // ---- 2. candidates: scores at or above the token's bound
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int tt = 16 * rt + 4 * q + v;
+            const float th = thr[tt];
+            uint32_t bits = 0u;   // this lane's scores of the token at or above its bound
+#pragma unroll
+            for (int i = 0; i < E; ++i) bits |= (sc[rt][i][v] >= th ? 1u : 0u) << i;
+            if (bits) {
+                int p = atomicAdd(&cnt[tt], __popc(bits));
+#pragma unroll
+                for (int i = 0; i < E; ++i) {
+                    if ((bits >> i) & 1u) {
+                        if (p < SDM_WAVE)
+                            cand[tt * SDM_WAVE + p] = make_uint2(__float_as_uint(sc[rt][i][v]),
+                                                                 (uint32_t)((wave + AWAVES * i) * 16 + r16));
+                        ++p;
+                    }
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    __syncthreads();
+    // ---- 3. each token's ranked shortlist, on its wave
+    for (int u = 0; u < NU; ++u) {
+        const int tt = wave + AWAVES * u;
+        if (tt >= nt) break;
+        Entry* out = sl + ((size_t)tt * 2 + half) * RKS;
+        const int n = cnt[tt];
+        if (lane >= k && lane < RKS) out[lane] = Entry{-INFINITY, 0};
+        if (n >= k && n <= SDM_WAVE) {
+            const uint2 cv = cand[tt * SDM_WAVE + min(lane, SDM_WAVE - 1)];
+            uint32_t th = lane < n ? ord_key(__uint_as_float(cv.x)) : 0u;
+            uint32_t tl = ~cv.y;
+            bsort_desc64<2, 1, SDM_WAVE>(th, tl, lane);
+            if (lane < k) out[lane] = Entry{key_to_float(th), (int)~tl};
+        } else {
+            reg_half_general<E>(xs, cbh, t0 + (tt & ~15), min(16, nt - (tt & ~15)), tt % 16, dk, half, s, k,
+                                frow, scr, kbuf, out);
+        }
+        wait_lds();
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
+// Three waves per SIMD (the LDS of three workgroups fits a CU): at sqrt(N) =
+// 1024 the register cap halves the time against two (0.89 against 1.20 ms
+// per side at B=4 H=8 T=8192).
+template <int E, int RT>
+__global__ __launch_bounds__(AWAVES * SDM_WAVE, 3) void address_reg_kernel(const bf16_t* __restrict__ x,
+                                                                        const bf16_t* __restrict__ cb, int H, int T,
+                                                                        int tb, int te, int dk, int s, int k,
+                                                                        int32_t* __restrict__ idx,
+                                                                        float* __restrict__ val,
+                                                                        float* __restrict__ score) {
+    using L = RegTile<E, RT>;
+    constexpr int NU = L::TOK / AWAVES;
+    extern __shared__ __align__(16) unsigned char smem[];
+    Entry* sl = reinterpret_cast<Entry*>(smem + L::SL_OFF);
+    const int wave = threadIdx.x / SDM_WAVE;
+    const int lane = lane_id();
+    Entry* scr = reinterpret_cast<Entry*>(smem + L::SCR_OFF) + wave * MAXK;
+    uint64_t* kbuf = reinterpret_cast<uint64_t*>(smem + L::KB_OFF) + wave * SDM_WAVE;
+    const int stream = blockIdx.y;
+    const int t0 = tb + blockIdx.x * L::TOK;
+    const int nt = min(L::TOK, te - t0);
+    const bf16_t* xs = x + (size_t)stream * T * dk;
+    const bf16_t* cbh = cb + (size_t)(stream % H) * 2 * s * (dk / 2);
+    reg_half<E, RT>(smem, xs, cbh, t0, nt, dk, s, k, 0);
+    reg_half<E, RT>(smem, xs, cbh, t0, nt, dk, s, k, 1);
+    // ---- stage 2 of each token, on the wave that ranked its shortlists
+    const uint16_t* pairs = c_pairs.e + c_pairs.off[k];
+    const int ncand = c_pairs.n[k];
+    uint32_t pi[3], pj[3];
+#pragma unroll
+    for (int e = 0; e < 3; ++e) {
+        const int c = e * SDM_WAVE + lane;
+        const uint32_t pr = c < ncand ? pairs[min(c, ncand - 1)] : ((RKS - 1u) << 8 | (RKS - 1u));
+        pi[e] = pr >> 8;
+        pj[e] = pr & 0xffu;
+    }
+    for (int u = 0; u < NU; ++u) {
+        const int tt = wave + AWAVES * u;
+        if (tt >= nt) break;
+        const size_t o = ((size_t)stream * T + t0 + tt) * k;
+        const Entry* la = sl + (size_t)tt * 2 * RKS;
+        const Entry* lb = la + RKS;
+        if (!pairs_fast(s, k, pi, pj, la, lb, reinterpret_cast<uint2*>(kbuf), idx + o, val + o,
+                        score ? score + o : nullptr))
+            token_pairs(s, k, ncand, pairs, scr, la, lb, kbuf, idx + o, val + o, score ? score + o : nullptr);
+        wait_lds();
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
 // Grid (tiles of tile_tokens tokens of [tb, te), streams).
 template <typename XT, int MODE, int E, int KM>
 __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __restrict__ x,
@@ -1420,10 +1713,37 @@ constexpr size_t tile_lds_bytes() {
         return address_lds_bytes(E, AT, KM);
 }
 
+// One 16-token row tile per workgroup of the register-resident kernel (its
+// scores take 4 E registers per lane).
+template <int E>
+hipError_t launch_address_reg(const void* x, const void* cb, int B, int H, int T, int tb, int tn, int dk, int s,
+                              int k, int32_t* idx, float* val, float* score, hipStream_t st) {
+    constexpr int RT = 1;
+    using L = RegTile<E, RT>;
+    auto kfn = address_reg_kernel<E, RT>;
+    hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L::BYTES);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kfn, dim3((tn + L::TOK - 1) / L::TOK, B * H), dim3(AWAVES * SDM_WAVE), L::BYTES, st,
+                       static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(cb), H, T, tb, tb + tn, dk, s, k,
+                       idx, val, score);
+    return hipGetLastError();
+}
+
 template <typename XT, int MODE>
 hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, int tb, int tn, int dk,
                             int s, int k, int32_t* idx, float* val, float* score, hipStream_t st) {
     const int E = (s + SDM_WAVE - 1) / SDM_WAVE;
+    if constexpr (MODE == 2) {
+        // bf16 codebooks, sqrt(N) in (256, 1024], d_k / 2 <= 64, k <= 32:
+        // scores stay in registers.  Measured at sqrt(N) = 1024 (B=4 H=8
+        // T=8192, d_k = 128, k = 32): 1.19 against 1.84 ms per side.  At
+        // sqrt(N) = 256 the LDS tile stays: 0.87 ms per side (B=8 H=16
+        // T=4096) against 1.04 for 32-token register tiles.
+        if (E > 4 && E <= 16 && dk / 2 <= 64 && k <= 32 && k <= s) {
+            if (E <= 8) return launch_address_reg<8>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st);
+            return launch_address_reg<16>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st);
+        }
+    }
     const XT* xp = static_cast<const XT*>(x);
     const XT* cp = static_cast<const XT*>(cb);
 #define SDM_ADDR_CASE(EE, KM)                                                                   \
