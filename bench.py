@@ -173,6 +173,9 @@ def main():
     ap.add_argument("--chunk", type=int, default=448,
                     help="tokens per pipeline stage of the forward step (0: the library's choice, a "
                          "quarter of T; 448, measured best for this workload, by default)")
+    ap.add_argument("--learned-chunk", type=int, default=1024,
+                    help="tokens per pipeline stage of the learned-M0 forward step (0: the library's "
+                         "choice, a quarter of T; 1024, measured best there, by default)")
     ap.add_argument("--train-chunk", type=int, default=0,
                     help="tokens per pipeline stage of the training step's forward (0: the library's "
                          "choice, measured best there)")
@@ -624,7 +627,7 @@ def layer_leg(sdm, to_dev, stream, dev, args):
 def learned_m0_leg(sdm, to_dev, stream, dev, args):
     """The learned-M0 workload (B=4 H=8 T=8192 N=2^20 d=128 top-32): the shared
     M0 broadcast to every sequence, timed alone (excluded from the step), and
-    forward steps (one sdm_forward call each, the library's stages) on the
+    forward steps (one sdm_forward call each, pipeline stages of args.learned_chunk) on the
     resident table, with the scan's roofline."""
     import torch
 
@@ -663,8 +666,10 @@ def learned_m0_leg(sdm, to_dev, stream, dev, args):
             for n, dt in (("r_idx", torch.int32), ("r_val", torch.float32),
                           ("w_idx", torch.int32), ("w_val", torch.float32))}
 
+    chunk = getattr(args, "learned_chunk", 0)
+
     def step():
-        sdm.forward(q, k, cb, cb, v, al, be, mem, w3.N, w3.topk, workspace=ws, y=y, out=outs)
+        sdm.forward(q, k, cb, cb, v, al, be, mem, w3.N, w3.topk, workspace=ws, y=y, out=outs, chunk=chunk)
 
     sdm.mem_init(mem, m0)
     for _ in range(args.warmup):
@@ -695,8 +700,8 @@ def learned_m0_leg(sdm, to_dev, stream, dev, args):
     ach = launch_bytes / (scan_ms * 1e-3) / 1e9
     res["learned_m0"] = {
         "workload": f"learned initial memory: B={B} H={H} T={T} d_k=d_v={w3.d_v} N={w3.N} top-{w3.topk}, "
-                    "bf16 inputs, fp32 memory (16 GiB); one sdm_forward call per step (library stages), "
-                    "the M0 broadcast excluded (under mem_init)",
+                    f"bf16 inputs, fp32 memory (16 GiB); one sdm_forward call per step (stages of "
+                    f"{chunk or 'T/4'} tokens), the M0 broadcast excluded (under mem_init)",
         "value": round(B * T / (ms * 1e-3), 1), "unit": "tokens/s", "ms_per_step": round(ms, 4),
         "kernels_ms_per_step": kms,
         "roofline": {"bound": "hbm", "kernel": "fwd_scan", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
