@@ -424,15 +424,17 @@ int sdm_mem_init(float* dst, const float* m0, int B, int H, int64_t N, int d_v, 
 int sdm_set_scan_slice_width(int sw);
 
 /* ------------------------------------------------------------------------
- * Forward prefetch depth: tokens whose table rows are in flight while one is
- * computed (the prep kernel links rows written within that window to an LDS
- * ring).  sdm_set_scan_prefetch(pd):
+ * Scan prefetch depth: tokens whose table rows are in flight while one is
+ * computed (the prep kernels link rows written within that window to LDS
+ * rings).  sdm_set_scan_prefetch(pd):
  *   0   automatic (default): 4, except 16 (8 where LDS does not allow 16) for
  *       the line-cooperative forward kernel when its launch has fewer waves
  *       than the device has SIMDs (few streams: each stream's step time is
  *       then set by the row loads' latency over the tokens in flight);
- *   4, 8, 16  force that depth for the line-cooperative kernel (the per-wave
- *       kernel always takes 4).
+ *   4, 8, 16  force that depth for the line-cooperative forward kernel (the
+ *       per-wave kernels always take 4, or 2 for four-pass backward shapes);
+ *       8 and 16 also give the line-cooperative backward kernel a depth of 8
+ *       (its default is 4).
  * Results do not depend on it.  Process-wide; applies to launches that start
  * after the call.  Any other value returns SDM_ERR_INVALID_ARG.
  * ---------------------------------------------------------------------- */

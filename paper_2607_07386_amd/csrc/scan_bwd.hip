@@ -432,6 +432,53 @@ __device__ __forceinline__ void bwd_token_line(const BwdCtx& c, const unsigned c
     }
 }
 
+// Staging for the line kernel: the records of the G tokens [u1 - G + 1, u1]
+// (clamped at lo) go to one ring that the workgroup's waves share (they read
+// the same records), 16-byte chunk w 64 + lane + 256 j, j < NC, per lane; each
+// wave stages the v slices of its own columns.  Loads are unconditional at
+// clamped indices; the surplus is never stored.
+template <typename VT, int NC>
+__device__ __forceinline__ void bline_stage_load(u4v (&st)[NC], u2v& stv, const unsigned char* srec,
+                                                 const VT* sv, int u1, int lo, int dv, int slice, int rec_bytes,
+                                                 int w, int lane) {
+    constexpr int SW = 8;
+    constexpr int VB = SW * (int)sizeof(VT);
+    constexpr int ppt = VB / 8;
+    const int ub1 = max(u1, lo);
+    const int u0 = max(lo, ub1 - G + 1);
+    const int cnt = ub1 - u0 + 1;
+    const u4v* src = reinterpret_cast<const u4v*>(srec + (size_t)u0 * rec_bytes);
+    const int last = cnt * rec_bytes / 16 - 1;
+#pragma unroll
+    for (int j = 0; j < NC; ++j) st[j] = src[min(w * SDM_WAVE + lane + j * LW * SDM_WAVE, last)];
+    const int tk = min(lane / ppt, cnt - 1);
+    const int pc = min(lane % ppt, (dv - slice * SW) * (int)sizeof(VT) / 8 - 1);
+    stv = *reinterpret_cast<const u2v*>(
+        reinterpret_cast<const unsigned char*>(sv + (size_t)(u0 + tk) * dv) + pc * 8);
+}
+template <typename VT, int NS, int NC>
+__device__ __forceinline__ void bline_stage_store(const u4v (&st)[NC], u2v stv, unsigned char* rring,
+                                                  unsigned char* vring, int u1, int lo, int rec_bytes, int w,
+                                                  int lane) {
+    constexpr int VB = 8 * (int)sizeof(VT);
+    constexpr int ppt = VB / 8;
+    if (u1 < lo) return;
+    const int u0 = max(lo, u1 - G + 1);
+    const int cnt = u1 - u0 + 1;
+    const int nchunk = cnt * rec_bytes / 16;   // <= NC * 256 (checked by the host)
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+        const int c = w * SDM_WAVE + lane + j * LW * SDM_WAVE;
+        if (c < nchunk) {
+            const int tk = (c * 16) / rec_bytes;   // records are whole 16-byte chunks
+            const int within = c * 16 - tk * rec_bytes;
+            *reinterpret_cast<u4v*>(rring + ((u0 + tk) & (NS - 1)) * rec_bytes + within) = st[j];
+        }
+    }
+    const int tk = lane / ppt, pc = lane % ppt;
+    if (tk < cnt) *reinterpret_cast<u2v*>(vring + ((u0 + tk) & (NS - 1)) * VB + pc * 8) = stv;
+}
+
 // Slot ids (this lane's line row) of token u's read row and written row.
 __device__ __forceinline__ int2 line_slots(const BwdCtx& c, int u, int rl, int NS) {
     const unsigned char* rec = c.rring + (u & (NS - 1)) * c.L.bytes;
@@ -482,12 +529,12 @@ __device__ __forceinline__ void line_step(const BwdCtx& c, const LinePtrs& p, un
     st4(p.mt + (size_t)st_sl.y * c.dv, lds4(sb, 2, p.rl, p.lq));
 }
 
-template <typename VT, int PD, int NR>
+template <typename VT, int PD, int NC>
 __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
     const unsigned char* __restrict__ recs, const VT* __restrict__ v, float* __restrict__ mem,
     const float* __restrict__ saved, const float* __restrict__ dy, float* __restrict__ Gtab,
     float* __restrict__ dv_out, float* __restrict__ part, int T, int tb, int te, int dv, int64_t N,
-    int n_slices, int S, int lds_per_wave) {
+    int n_slices, int S, int per_wave_lds) {
     // tokens te-1 down to tb of each stream (layout strides use T)
     constexpr int SW = 8;
     constexpr int LEAD = bstage_lead<PD>();
@@ -512,9 +559,11 @@ __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
     c.colok = true;
     const int col = slice * SW + c.cq * 4;
 
+    // LDS: the shared record ring, then per wave its v ring, adjoint ring and
+    // undo ring, then the row and staging buffers, flags and partial sums
     extern __shared__ __align__(16) unsigned char smem[];
-    unsigned char* rring = smem + (size_t)w * lds_per_wave;
-    unsigned char* vring = rring + NS * c.L.bytes;
+    unsigned char* rring = smem;
+    unsigned char* vring = smem + (size_t)NS * c.L.bytes + (size_t)w * per_wave_lds;
     c.rring = rring;
     c.vring = vring;
     c.gring = reinterpret_cast<float*>(vring + NS * VB);
@@ -525,7 +574,7 @@ __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
     c.sdy = dy + (size_t)stream * T * dv + col;
     c.sdv = dv_out + (size_t)stream * T * dv + col;
     c.spart = part + ((size_t)group * S + stream) * T * LPART;   // per workgroup (4 slices)
-    unsigned char* lb = smem + (size_t)LW * lds_per_wave;
+    unsigned char* lb = smem + (size_t)NS * c.L.bytes + (size_t)LW * per_wave_lds;
     unsigned char* sb = lb + 4 * LROWS * LROWB;
     int* flags = reinterpret_cast<int*>(sb + 3 * LROWS * LROWB);
     float* psum = reinterpret_cast<float*>(flags + LFLAGS);
@@ -543,16 +592,17 @@ __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
 
     const unsigned char* srec = recs + (size_t)stream * T * c.L.bytes;
     const VT* sv = v + (size_t)stream * T * dv + slice * SW;
-    u4v st[NR];
+    u4v st[NC];
     u2v stv;
     LineBuf buf[PD];
 
     const int T1 = te - 1;
     for (int i0 = 0; i0 < LEAD - G; i0 += G) {
-        bstage_load<VT, SW, NR>(st, stv, srec, sv, T1 - i0, tb, dv, slice, c.L.bytes, lane);
-        bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, T1 - i0, tb, c.L.bytes, lane);
+        bline_stage_load<VT, NC>(st, stv, srec, sv, T1 - i0, tb, dv, slice, c.L.bytes, w, lane);
+        bline_stage_store<VT, NS, NC>(st, stv, rring, vring, T1 - i0, tb, c.L.bytes, w, lane);
     }
-    bstage_load<VT, SW, NR>(st, stv, srec, sv, T1 - (LEAD - G), tb, dv, slice, c.L.bytes, lane);
+    bline_stage_load<VT, NC>(st, stv, srec, sv, T1 - (LEAD - G), tb, dv, slice, c.L.bytes, w, lane);
+    __syncthreads();   // the first records staged by every wave
 #pragma unroll
     for (int j = 0; j < PD - 1; ++j) {
         const int u = max(T1 - j, tb);
@@ -569,8 +619,8 @@ __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
         for (int j = 0; j < PD; ++j) {
             const int t = T1 - (i0 + j);
             if (j % G == 0) {
-                bstage_store<VT, SW, NS, NR>(st, stv, rring, vring, t - (LEAD - G), tb, c.L.bytes, lane);
-                bstage_load<VT, SW, NR>(st, stv, srec, sv, t - LEAD, tb, dv, slice, c.L.bytes, lane);
+                bline_stage_store<VT, NS, NC>(st, stv, rring, vring, t - (LEAD - G), tb, c.L.bytes, w, lane);
+                bline_stage_load<VT, NC>(st, stv, srec, sv, t - LEAD, tb, dv, slice, c.L.bytes, w, lane);
             }
             line_step<VT, PD, NS>(c, p, lb, sb, flags, psum, buf[j], buf[(j + PD - 1) % PD], t, tb, w, lane, true);
         }
@@ -613,6 +663,7 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(const float* __restrict
 }
 
 constexpr int BPD = SDM_BWD_PD;
+constexpr int BPD_LINE = 8;   // the line-cooperative kernel's deeper window
 constexpr int BSW_MIN = 8;   // narrowest slice: sizes the per-slice partials
 // Prefetch depth of the per-wave kernel with K row passes: BPD tokens, or 2 at
 // K = 4 (64 rows at 16 columns, 128 at 8), where BPD tokens of prefetched rows
@@ -665,11 +716,35 @@ bool bwd_plan(int S, int W, int R, int dv, int in_dtype, BwdPlan* p) {
     return bwd_plan_sw<BSW_MIN>(W, R, dv, in_dtype, p) || bwd_plan_sw<16>(W, R, dv, in_dtype, p);
 }
 
+// LDS of the line-cooperative kernel at prefetch depth PD: the shared record
+// ring, each wave's v, adjoint and undo rings, the row and staging buffers.
+template <int PD>
+size_t line_per_wave(int in_dtype) {
+    const int vbytes = in_dtype == SDM_DT_BF16 ? 2 : 4;
+    return (size_t)bstage_slots<PD>() * 8 * vbytes + (size_t)PD * 2 * LROWS * 8 * 4 + (size_t)PD * LROWS * 8 * 4;
+}
+template <int PD>
+size_t line_lds(int in_dtype) {
+    return (size_t)bstage_slots<PD>() * bwd_rec_layout(LROWS, LROWS).bytes + LW * line_per_wave<PD>(in_dtype) +
+           line_shared_bytes();
+}
+constexpr int LNC = 1;   // 16-byte record chunks per lane for G records of W = R = 32
+static_assert(G * ((22 * LROWS + 8 + 15) / 16 * 16) <= LNC * LW * SDM_WAVE * 16, "line staging chunks");
+
 // The line-cooperative kernel's shape: 8-column slices, W = R = 32, d_v a
 // multiple of 32 (whole lines per workgroup), and its LDS within the limit.
 bool line_shape_ok(const ScanBwdArgs& a, const BwdPlan& p) {
     return p.SW == 8 && p.K == 1 && a.W == LROWS && a.R == LROWS && a.dv % 32 == 0 && p.n_slices % LW == 0 &&
-           (size_t)p.lds_per_wave * LW + line_shared_bytes() <= (size_t)LDS_LIMIT;
+           line_lds<BPD>(a.in_dtype) <= (size_t)LDS_LIMIT;
+}
+// Prefetch depth of the line-cooperative kernel: 4 tokens, or 8 when
+// sdm_set_scan_prefetch forces 8 or 16 (the shared record ring leaves LDS for
+// the deeper adjoint and undo rings).  At the training workload 8 measured no
+// faster (1.13 against 1.12 ms per stage) and doubled the records' link search
+// (0.83 against 0.39 ms per stage beside the scan).
+int line_pd(const ScanBwdArgs& a) {
+    const int forced = sdm_scan_prefetch();
+    return forced >= 8 && line_lds<BPD_LINE>(a.in_dtype) <= (size_t)LDS_LIMIT ? BPD_LINE : BPD;
 }
 bool line_io_ok(const ScanBwdArgs& a, const BwdPlan& p) { return sdm_line_io_enabled() && line_shape_ok(a, p); }
 // a.line >= 0: the caller's decision (one per call, so that every range and the
@@ -689,13 +764,15 @@ hipError_t launch_bwd_k(const ScanBwdArgs& a, const BwdPlan& p, bool line, float
     const size_t sm = (size_t)p.lds_per_wave * p.wpb;
     if constexpr (SW == 8 && K == 1) {
         if (line) {
-            auto kl = scan_bwd_line_kernel<VT, BPD, NR>;
-            const size_t sml = (size_t)p.lds_per_wave * LW + line_shared_bytes();
+            const bool deep = line_pd(a) == BPD_LINE;
+            auto kl = deep ? scan_bwd_line_kernel<VT, BPD_LINE, LNC> : scan_bwd_line_kernel<VT, BPD, LNC>;
+            const size_t sml = deep ? line_lds<BPD_LINE>(a.in_dtype) : line_lds<BPD>(a.in_dtype);
+            const size_t pw = deep ? line_per_wave<BPD_LINE>(a.in_dtype) : line_per_wave<BPD>(a.in_dtype);
             hipError_t e = hipFuncSetAttribute((const void*)kl, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sml);
             if (e != hipSuccess) return e;
             hipLaunchKernelGGL(kl, dim3(p.n_slices / LW * S), dim3(LW * SDM_WAVE), sml, st, a.ws + SDM_WS_HEADER,
                                static_cast<const VT*>(a.v), a.mem, a.saved, a.dy, a.G, a.dv_out, part, a.T,
-                               a.tb, a.te, a.dv, a.N, p.n_slices, S, p.lds_per_wave);
+                               a.tb, a.te, a.dv, a.N, p.n_slices, S, (int)pw);
             return hipGetLastError();
         }
     }
@@ -749,7 +826,11 @@ bool sdm_bwd_line_io(const ScanBwdArgs& a) {
 hipError_t sdm_launch_bwd_prep_range(const ScanBwdArgs& a, hipStream_t st) {
     BwdPlan plan;   // the links' window is the scan's prefetch depth
     if (!bwd_plan(a.B * a.H, a.W, a.R, a.dv, a.in_dtype, &plan)) return hipErrorInvalidConfiguration;
+    bool ok;
+    const bool line = use_line(a, plan, &ok);
+    if (!ok) return hipErrorInvalidConfiguration;
     SdmProfScope ps(SDM_K_BWD_PREP, st);
+    if (line && line_pd(a) == BPD_LINE) return sdm_launch_bwd_prep<BPD_LINE>(a, st);
     return plan.PD == 2 ? sdm_launch_bwd_prep<2>(a, st) : sdm_launch_bwd_prep<BPD>(a, st);
 }
 

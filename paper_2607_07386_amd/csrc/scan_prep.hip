@@ -412,3 +412,4 @@ template hipError_t sdm_launch_fwd_prep<8>(const ScanFwdArgs&, hipStream_t);
 template hipError_t sdm_launch_fwd_prep<16>(const ScanFwdArgs&, hipStream_t);
 template hipError_t sdm_launch_bwd_prep<SDM_BWD_PD>(const ScanBwdArgs&, hipStream_t);
 template hipError_t sdm_launch_bwd_prep<2>(const ScanBwdArgs&, hipStream_t);
+template hipError_t sdm_launch_bwd_prep<8>(const ScanBwdArgs&, hipStream_t);

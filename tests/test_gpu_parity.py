@@ -572,6 +572,32 @@ def test_backward_line_io(name):
         assert rel_err(np_(g_line[k]), np_(g_wave[k]).astype(np.float64)) <= 1e-5, k
 
 
+@pytest.mark.parametrize("name", list(LINE))
+def test_backward_line_prefetch_depths(name):
+    """The line-cooperative backward at its default prefetch depth (4 tokens)
+    and at 8: both against the oracle, and bit for bit the same (rows written
+    inside the window come from the LDS rings at either depth)."""
+    w = LINE[name]
+    inp = synth.Inputs(w)
+    streams = list(range(w.B * w.H))
+    sdm.set_scan_slice_width(8)
+    try:
+        errs4, g4 = run_backward_case(w, inp, streams)
+        sdm.set_scan_prefetch(8)
+        errs8, g8 = run_backward_case(w, inp, streams)
+    finally:
+        sdm.set_scan_prefetch(0)
+        sdm.set_scan_slice_width(0)
+    for tag, errs in (("pd8", errs8), ("pd4", errs4)):
+        report(f"{name}/bwd-line-{tag}", **errs)
+        for k, e in errs.items():
+            if k != "mem_restored_bit_exact":
+                assert within(e, w), (tag, k, e)
+        assert errs["mem_restored_bit_exact"], tag
+    for k in g8:
+        assert torch.equal(g8[k], g4[k]), k
+
+
 # ------------------------------------------------- full-size workloads, sampled streams
 # Each runs the calls bench.py times: the 1.4B-shaped forward as sdm_forward
 # with 448-token stages, the training step as sdm_forward with the undo log
