@@ -18,7 +18,11 @@
 //     (every other pair has >= k pairs ranked above it), selected the same
 //     way, then sorted by slot id and softmax-normalised.
 // k in (64, 128] runs a kernel of its own: lists of two entries per lane,
-// exact bisection selection, 128-wide bitonic sorts.
+// exact bisection selection, 128-wide bitonic sorts.  For sqrt(N) in
+// (256, 1024] with bf16 codebooks, d_k / 2 <= 64 and k <= 32, a third kernel
+// (address_reg_kernel) keeps a 16-token tile's scores in the MFMA result
+// registers: the groups of B's bound are the lanes' own scores, so only the
+// group maxima and the candidates pass through LDS.
 #include <algorithm>
 
 #include "sdm_common.h"
