@@ -1170,8 +1170,6 @@ __device__ __forceinline__ void reg_half(unsigned char* smem, const bf16_t* xs, 
                     for (int v = 0; v < 4; ++v) sc[rt][i0 + i][v] = acc[v] + pad;
                 }
             }
-            // one group's codebook pieces in registers at a time
-            __builtin_amdgcn_sched_barrier(0);
         }
     }
     // ---- 1. group maxima, then each token's bound
@@ -1232,7 +1230,6 @@ __device__ __forceinline__ void reg_half(unsigned char* smem, const bf16_t* xs, 
                     }
                 }
             }
-            __builtin_amdgcn_sched_barrier(0);
         }
     __syncthreads();
     // ---- 3. each token's ranked shortlist, on its wave
