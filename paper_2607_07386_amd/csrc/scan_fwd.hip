@@ -10,11 +10,15 @@
 //    one 16-byte piece per lane, CQ lanes per row slice) while token t is
 //    computed;
 //  * a row loaded for token u before tokens u-PD+1 .. u-1 have written it
-//    would be stale.  The prep kernel records, per row, the latest writer
-//    within that window (or the token itself, for reads); such rows are
-//    taken from an LDS ring holding the last PD tokens' written rows.  Older
-//    writers stored before the load was issued, in program order of the same
-//    wave, so the load returns their value;
+//    would be stale.  The prep kernel records, per row of either list, the
+//    latest writer within that window; such rows are taken from an LDS ring
+//    holding the last PD tokens' written rows.  Older writers stored before
+//    the load was issued, in program order of the same wave, so the load
+//    returns their value;
+//  * read rows are taken at their value before the token, P: a read row the
+//    token itself writes ends at alpha P + kappa_n e, so its record weight is
+//    rho alpha and the token's record carries yc = sum of rho kappa_n over
+//    such rows, and y = sum rho' P + yc e (Eqs. sdm-write, sdm-read);
 //  * per-token records (slots, weights, links, gates) are staged in LDS in
 //    blocks of G tokens, loaded L tokens ahead with 16-byte loads.
 #include <algorithm>
