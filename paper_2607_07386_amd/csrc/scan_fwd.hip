@@ -320,7 +320,27 @@ struct FLinePtrs {
     float* tab;        // the stream's table at this lane's line columns
     float* sv;         // the stream's saved rows, same columns
     int r0, lq;        // first line row of this lane, quad within the row
+    // The table rows through buffer instructions: the stream's table (below
+    // 2 GiB, checked on the host) as the descriptor's base, a row's byte
+    // offset slot * 4 d_v + 4 column in one 32-bit register (one 24-bit
+    // multiply-add per row instead of 64-bit address arithmetic).
+    __amdgpu_buffer_rsrc_t trs;
+    uint32_t dv4, lc4;
 };
+
+template <int SW>
+__device__ __forceinline__ uint32_t fl_row_off(const FLinePtrs<SW>& p, int slot) {
+    return __umul24((uint32_t)slot, p.dv4) + p.lc4;
+}
+template <int SW>
+__device__ __forceinline__ v4f fl_tab_ld(const FLinePtrs<SW>& p, int slot) {
+    return __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(p.trs, (int)fl_row_off(p, slot), 0, 0));
+}
+template <int SW>
+__device__ __forceinline__ void fl_tab_st(const FLinePtrs<SW>& p, int slot, v4f v) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), p.trs, (int)fl_row_off(p, slot), 0, 0);
+}
 
 // Staging of G records, shared by the workgroup: wave w moves 16-byte chunks
 // w 64 + lane + 256 j, j < NC (NC chunks per lane cover G records up to NC 4
@@ -363,8 +383,8 @@ __device__ __forceinline__ void fl_issue(FLine<SW, FR>& b, const unsigned char* 
 #pragma unroll
     for (int i = 0; i < FLine<SW, FR>::NLI; ++i) {
         const int r = p.r0 + FLine<SW, FR>::LRI * i;
-        b.Pw[i] = ld4(p.tab + (size_t)reinterpret_cast<const int*>(rec)[r] * dv);
-        b.Pr[i] = ld4(p.tab + (size_t)reinterpret_cast<const int*>(rec + L.off_rslot)[r] * dv);
+        b.Pw[i] = fl_tab_ld(p, reinterpret_cast<const int*>(rec)[r]);
+        b.Pr[i] = fl_tab_ld(p, reinterpret_cast<const int*>(rec + L.off_rslot)[r]);
     }
 }
 
@@ -452,7 +472,7 @@ __device__ __forceinline__ void fl_step(const FwdCtx<VT, SW, PD, 2, SAVE>& c, co
 #pragma unroll
     for (int i = 0; i < NLI; ++i) {
         const int r = p.r0 + LRI * i;
-        st4(p.tab + (size_t)wslot[i] * c.dv, fl_ld<SW, FR>(sb, 0, r, p.lq));
+        fl_tab_st(p, wslot[i], fl_ld<SW, FR>(sb, 0, r, p.lq));
         if (SAVE) st4(p.sv + ((size_t)t * FR + r) * c.dv, fl_ld<SW, FR>(sb, 1, r, p.lq));
     }
 }
@@ -512,6 +532,10 @@ __global__ __launch_bounds__(FLW * SDM_WAVE) void scan_fwd_line_kernel(
     p.lq = lane % FLine<SW, FR>::LQ;
     const size_t lcol = (size_t)group * FLW * SW + p.lq * 4;
     p.tab = mem + (size_t)stream * N * dv + lcol;
+    p.trs = __builtin_amdgcn_make_buffer_rsrc(mem + (size_t)stream * N * dv, 0, (int)((size_t)N * dv * 4),
+                                              0x00020000);
+    p.dv4 = (uint32_t)dv * 4;
+    p.lc4 = (uint32_t)lcol * 4;
     p.sv = SAVE ? saved + (size_t)stream * T * FR * dv + lcol : nullptr;
 
     const unsigned char* srec = recs + (size_t)stream * T * c.L.bytes;
@@ -626,6 +650,8 @@ template <int SW, int FR, int PD>
 bool fline_ok(const ScanFwdArgs& a, const FwdPlan& p, bool save, size_t* lds, size_t* per_wave) {
     if (!sdm_line_io_enabled() || a.W != FR || a.R != FR || a.dv % (FLW * SW) != 0 || p.n_slices % FLW != 0)
         return false;
+    // the table rows' 32-bit offsets (and the 24-bit multiply: N < 2^24)
+    if ((size_t)a.N * a.dv * 4 >= ((size_t)1 << 31) || a.N >= (1 << 24)) return false;
     *lds = fline_lds<SW, FR, PD>(save, a.in_dtype, per_wave);
     return *lds <= (size_t)LDS_LIMIT;
 }
