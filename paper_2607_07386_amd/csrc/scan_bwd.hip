@@ -485,19 +485,34 @@ __device__ __forceinline__ int2 line_slots(const BwdCtx& c, int u, int rl, int N
     return make_int2(reinterpret_cast<const int*>(rec + c.L.off_rslot)[rl], reinterpret_cast<const int*>(rec)[rl]);
 }
 
+// The stream's memory table, adjoint table and saved rows as buffers (each below
+// 2 GiB, rows below 2^24): row s of a table at byte offset s 4 d_v + 4 lc, with
+// lc this lane's first line column, saved row (u, r) at (32 u + r) 4 d_v + 4 lc.
+// 32-bit offsets through a 24-bit multiply keep the address arithmetic off the
+// latency-bound token chain.
 struct LinePtrs {
-    float* mt;          // memory table of the stream, at this lane's line columns
-    float* gt;          // adjoint table, same
-    const float* sv;    // saved rows of the stream, same
+    __amdgpu_buffer_rsrc_t mt, gt, sv;
+    uint32_t dv4, lc4;
     int rl;             // this lane's line row (0..31)
     int lq;             // this lane's column quad within the line
 };
 
+typedef unsigned int lu32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ v4f lbuf_ld(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+__device__ __forceinline__ void lbuf_st(__amdgpu_buffer_rsrc_t r, uint32_t off, v4f x) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(lu32x4, x), r, (int)off, 0, 0);
+}
+__device__ __forceinline__ uint32_t lrow_off(const LinePtrs& p, int row) {
+    return __umul24((uint32_t)row, p.dv4) + p.lc4;
+}
+
 __device__ __forceinline__ void line_issue(LineBuf& b, const BwdCtx& c, const LinePtrs& p, int2 sl, int u) {
-    b.Mr = ld4(p.mt + (size_t)sl.x * c.dv);
-    b.Gr = ld4(p.gt + (size_t)sl.x * c.dv);
-    b.Gw = ld4(p.gt + (size_t)sl.y * c.dv);
-    b.Ps = ld4(p.sv + ((size_t)u * LROWS + p.rl) * c.dv);
+    b.Mr = lbuf_ld(p.mt, lrow_off(p, sl.x));
+    b.Gr = lbuf_ld(p.gt, lrow_off(p, sl.x));
+    b.Gw = lbuf_ld(p.gt, lrow_off(p, sl.y));
+    b.Ps = lbuf_ld(p.sv, lrow_off(p, u * LROWS + p.rl));
     b.Dy = ld4(c.sdy + (size_t)u * c.dv);
 }
 
@@ -524,9 +539,9 @@ __device__ __forceinline__ void line_step(const BwdCtx& c, const LinePtrs& p, un
     const int pi = 17 * w + lane;
     if (lane < 17 && pi < LPART)
         c.spart[(size_t)t * LPART + pi] = ((psum[pi] + psum[LPART + pi]) + psum[2 * LPART + pi]) + psum[3 * LPART + pi];
-    if (flags[p.rl] != t) st4(p.gt + (size_t)st_sl.x * c.dv, lds4(sb, 0, p.rl, p.lq));
-    st4(p.gt + (size_t)st_sl.y * c.dv, lds4(sb, 1, p.rl, p.lq));
-    st4(p.mt + (size_t)st_sl.y * c.dv, lds4(sb, 2, p.rl, p.lq));
+    if (flags[p.rl] != t) lbuf_st(p.gt, lrow_off(p, st_sl.x), lds4(sb, 0, p.rl, p.lq));
+    lbuf_st(p.gt, lrow_off(p, st_sl.y), lds4(sb, 1, p.rl, p.lq));
+    lbuf_st(p.mt, lrow_off(p, st_sl.y), lds4(sb, 2, p.rl, p.lq));
 }
 
 template <typename VT, int PD, int NC>
@@ -582,10 +597,14 @@ __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
     LinePtrs p;
     p.rl = 8 * w + lane / 8;
     p.lq = lane % 8;
-    const size_t lcol = (size_t)group * 32 + p.lq * 4;
-    p.mt = mem + (size_t)stream * N * dv + lcol;
-    p.gt = Gtab + (size_t)stream * N * dv + lcol;
-    p.sv = saved + (size_t)stream * T * LROWS * dv + lcol;
+    const uint32_t lcol = (uint32_t)group * 32 + p.lq * 4;
+    const int tbytes = (int)((size_t)N * dv * 4);
+    p.mt = __builtin_amdgcn_make_buffer_rsrc(mem + (size_t)stream * N * dv, 0, tbytes, 0x00020000);
+    p.gt = __builtin_amdgcn_make_buffer_rsrc(Gtab + (size_t)stream * N * dv, 0, tbytes, 0x00020000);
+    p.sv = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(saved) + (size_t)stream * T * LROWS * dv, 0,
+                                             (int)((size_t)T * LROWS * dv * 4), 0x00020000);
+    p.dv4 = (uint32_t)dv * 4;
+    p.lc4 = lcol * 4;
 
     if (w == 0)
         for (int i = lane; i < LFLAGS; i += SDM_WAVE) flags[i] = -1;
@@ -733,7 +752,12 @@ static_assert(G * ((22 * LROWS + 8 + 15) / 16 * 16) <= LNC * LW * SDM_WAVE * 16,
 
 // The line-cooperative kernel's shape: 8-column slices, W = R = 32, d_v a
 // multiple of 32 (whole lines per workgroup), and its LDS within the limit.
+// Its table and saved-row offsets are 32-bit: each stream's tables and saved
+// rows below 2 GiB, their row counts below 2^24.
 bool line_shape_ok(const ScanBwdArgs& a, const BwdPlan& p) {
+    const size_t two_gib = (size_t)1 << 31;
+    if ((size_t)a.N * a.dv * 4 >= two_gib || a.N >= (1 << 24)) return false;
+    if ((size_t)a.T * LROWS * a.dv * 4 >= two_gib || (size_t)a.T * LROWS >= ((size_t)1 << 24)) return false;
     return p.SW == 8 && p.K == 1 && a.W == LROWS && a.R == LROWS && a.dv % 32 == 0 && p.n_slices % LW == 0 &&
            line_lds<BPD>(a.in_dtype) <= (size_t)LDS_LIMIT;
 }

@@ -103,6 +103,10 @@ struct FwdCtx {
     float* fring;
     float* tab;       // this lane's columns of row 0 of the stream's table
     float* ystream;   // y of the stream, this lane's columns
+    // line kernel: y of the stream as a buffer (below 2 GiB), its row t at byte
+    // offset t 4 d_v + 4 column
+    __amdgpu_buffer_rsrc_t yrs;
+    uint32_t dv4, ycol4;
     float* sstream;   // saved of the stream, this lane's columns
     FwdRec L;
     int dv, W, R, rg, cq;
@@ -406,9 +410,10 @@ __device__ __forceinline__ void fwd_token_line(const FwdCtx<VT, SW, PD, 2, SAVE>
 
     // pre-write value of write entry n: a ring row if a token still in flight
     // wrote it, else the row loaded from HBM
+    static_assert((PD * FR & (PD * FR - 1)) == 0, "ring rows a power of two");
     auto pre_write = [&](int n) -> v4f {
         const int l = lk[n];
-        const int fidx = l >= 0 ? min(l, PD * FR - 1) : 0;   // the writer's ring row
+        const int fidx = l & (PD * FR - 1);   // the writer's ring row (no link: any row, unused)
         return v4sel(l >= 0, ld4(c.fring + fidx * SW + c.cq * 4), fl_ld<SW, FR>(lb, 0, n, q));
     };
     v4f D[K];
@@ -432,7 +437,7 @@ __device__ __forceinline__ void fwd_token_line(const FwdCtx<VT, SW, PD, 2, SAVE>
         const int m = c.rg + RG * k;
         const int l = lk[FR + m];
         const float rho = reinterpret_cast<const float*>(rec + L.off_rval)[m];
-        const int fidx = l >= 0 ? min(l, PD * FR - 1) : 0;
+        const int fidx = l & (PD * FR - 1);
         yp = v4fma(rho, v4sel(l >= 0, ld4(c.fring + fidx * SW + c.cq * 4), fl_ld<SW, FR>(lb, 1, m, q)), yp);
     }
     rows_allreduce8<CQ>(up, yp);
@@ -446,7 +451,11 @@ __device__ __forceinline__ void fwd_token_line(const FwdCtx<VT, SW, PD, 2, SAVE>
         st4(c.fring + ((t & (PD - 1)) * FR + n) * SW + c.cq * 4, nw);
         fl_st<SW, FR>(sb, 0, n, q, nw);
     }
-    if (c.rg == 0) st4(c.ystream + (size_t)t * c.dv, v4fma(yc, e, yp));
+    if (c.rg == 0) {
+        typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v4fma(yc, e, yp)), c.yrs,
+                                               (int)(__umul24((uint32_t)t, c.dv4) + c.ycol4), 0, 0);
+    }
 }
 
 template <typename VT, int SW, int PD, bool SAVE, int NS, int FR>
@@ -525,6 +534,9 @@ __global__ __launch_bounds__(FLW * SDM_WAVE) void scan_fwd_line_kernel(
     c.fring = reinterpret_cast<float*>(vring + NS * VB);           // [PD][32][SW] written rows
     c.tab = mem + (size_t)stream * N * dv + col;
     c.ystream = y + (size_t)stream * T * dv + col;
+    c.yrs = __builtin_amdgcn_make_buffer_rsrc(y + (size_t)stream * T * dv, 0, (int)((size_t)T * dv * 4), 0x00020000);
+    c.dv4 = (uint32_t)dv * 4;
+    c.ycol4 = (uint32_t)col * 4;
     c.sstream = nullptr;
 
     FLinePtrs<SW> p;
@@ -650,8 +662,9 @@ template <int SW, int FR, int PD>
 bool fline_ok(const ScanFwdArgs& a, const FwdPlan& p, bool save, size_t* lds, size_t* per_wave) {
     if (!sdm_line_io_enabled() || a.W != FR || a.R != FR || a.dv % (FLW * SW) != 0 || p.n_slices % FLW != 0)
         return false;
-    // the table rows' 32-bit offsets (and the 24-bit multiply: N < 2^24)
+    // the table rows' and y's 32-bit offsets (and the 24-bit multiplies: N, T < 2^24)
     if ((size_t)a.N * a.dv * 4 >= ((size_t)1 << 31) || a.N >= (1 << 24)) return false;
+    if ((size_t)a.T * a.dv * 4 >= ((size_t)1 << 31) || a.T >= (1 << 24)) return false;
     *lds = fline_lds<SW, FR, PD>(save, a.in_dtype, per_wave);
     return *lds <= (size_t)LDS_LIMIT;
 }
