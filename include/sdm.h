@@ -445,9 +445,12 @@ int sdm_set_scan_prefetch(int pd);
  * line-cooperative kernel where the shape allows it: the waves of four
  * adjacent column slices (4 x 8 or 4 x 16 columns: one or two 128-byte lines
  * of every table row) move table rows between HBM and LDS as whole lines and
- * exchange their pieces in LDS.  Forward: W = R = 32 and d_v a multiple of 4
- * times the slice width; backward: 8-column slices, W = R = 32 and d_v a
- * multiple of 32.  sdm_set_scan_line_io(0) always uses the per-wave kernels
+ * exchange their pieces in LDS.  Forward: W = R = 32 or 64 and d_v a
+ * multiple of 4 times the slice width; backward: 8-column slices, W = R = 32
+ * (where the per-wave plan takes 8-column slices) or 64, and d_v a multiple of
+ * 32.  Each stream's table and saved rows must stay below 2 GiB (32-bit
+ * offsets), else the per-wave kernels run.  sdm_set_scan_line_io(0) always
+ * uses the per-wave kernels
  * (each wave moves its own pieces of the rows), 1 restores the default.  The
  * two do the same arithmetic per slice; results agree to rounding (the sums
  * over rows are taken in a different order, and the compiler may fuse a

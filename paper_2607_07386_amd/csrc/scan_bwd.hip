@@ -305,7 +305,8 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Line-cooperative variant (8-column slices, W = R = 32, d_v a multiple of 32).
+// Line-cooperative variant (8-column slices, W = R = 32 or 64, d_v a multiple
+// of 32).
 //
 // The four waves of a workgroup are four consecutive 8-column slices of one
 // stream, i.e. 32 columns: one 128-byte line of every table row.  With each
@@ -313,8 +314,8 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
 // the 4 lines of a row at different times, and the memory system then serves
 // the scattered rows at about 3.9 TB/s; moving whole lines it serves the same
 // bytes at about 5 TB/s.  So global table loads and stores go through LDS:
-// each wave loads (and stores) 8 of the 32 rows of a token as whole lines,
-// and the pieces a wave computes on are exchanged through LDS, with two
+// each wave loads (and stores) a quarter of the rows of a token as whole
+// lines, and the pieces a wave computes on are exchanged through LDS, with two
 // workgroup barriers per token.  The recurrence itself (links, rings, per-token
 // arithmetic) is the same as in scan_bwd_kernel, per wave and per slice.
 //
@@ -322,10 +323,16 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
 //   S1  this wave's line rows of token t (loaded earlier) -> LDS row buffer
 //   B1
 //   S2  line loads of token t - PD + 1
-//   S3  each wave reads its pieces, runs the token, writes its output pieces
-//       (G rows read, G rows written, undo M rows) to the LDS staging buffer
+//   S3  each wave reads its pieces, runs the token, and writes its output
+//       pieces (G rows read, G rows written) over the pieces it read
 //   B2
-//   S4  each wave stores 8 staged rows of each output as whole lines
+//   S4  each wave stores its line rows of each output as whole lines; the
+//       undo rows (M rows written) are the saved rows it loaded, stored from
+//       its registers
+// Every LDS position of the row buffer has one owner lane in the line layout
+// (S1, S4) and one in the piece layout (S3), so the outputs can take the
+// inputs' place: S3 overwrites only pieces its own lane has read, and S4 and
+// the next S1 touch only the lane's own line positions.
 // A load issued in S2 sees the stores of tokens >= t + 1 (every wave stored
 // those before B1), and the tokens t .. t - PD + 2 that it does not see are
 // exactly the PD - 1 tokens the prep kernel links to the LDS rings, as in
@@ -336,98 +343,131 @@ __global__ __launch_bounds__(MAX_WPB * SDM_WAVE) void scan_bwd_kernel(
 constexpr int LW = 4;          // waves (slices) per workgroup
 constexpr int LROWB = 160;     // LDS bytes per staged row: 128 + 32 of padding, so that
                                // the per-slice piece reads (stride of one row) hit distinct banks
-constexpr int LROWS = 32;      // rows per token (W = R)
-constexpr int LFLAGS = LROWS + SDM_WAVE;   // read-row marks, then one dummy entry per lane
-constexpr int LPART = 2 * LROWS + 2;       // per-token partial sums: rbar[32], kbar[32], dbeta, dalpha
-constexpr int line_shared_bytes() { return (4 + 3) * LROWS * LROWB + LFLAGS * 4 + LW * LPART * 4; }
+// Rows per token (W = R = LR, 32 or 64); each lane holds LR / 32 of them in both layouts.
+template <int LR>
+constexpr int lflags() { return LR + SDM_WAVE; }   // read-row marks, then one dummy entry per lane
+template <int LR>
+constexpr int lpart() { return 2 * LR + 2; }       // per-token partial sums: rbar[LR], kbar[LR], dbeta, dalpha
+template <int LR>
+constexpr int line_shared_bytes() { return 4 * LR * LROWB + lflags<LR>() * 4 + LW * lpart<LR>() * 4; }
 
+template <int KR>
 struct LineBuf {
-    v4f Mr, Gr, Gw, Ps;   // line layout: row 8 w + lane / 8, columns 4 (lane % 8) of the 32
-    v4f Dy;               // piece layout: this lane's 4 columns of dy
+    v4f Mr[KR], Gr[KR], Gw[KR], Ps[KR];   // line layout: rows 8 w + lane / 8 + 32 k, columns 4 (lane % 8)
+    v4f Dy;                               // piece layout: this lane's 4 columns of dy
 };
 
+// Row buffer: [4][LR] rows of LROWB bytes (M read, G read -> G read out,
+// G written -> G written out, saved row).
+template <int LR>
 __device__ __forceinline__ v4f lds4(const unsigned char* base, int a, int r, int q) {
-    return *reinterpret_cast<const v4f*>(base + (a * LROWS + r) * LROWB + q * 16);
+    return *reinterpret_cast<const v4f*>(base + (a * LR + r) * LROWB + q * 16);
 }
+template <int LR>
 __device__ __forceinline__ void lds4_st(unsigned char* base, int a, int r, int q, v4f v) {
-    *reinterpret_cast<v4f*>(base + (a * LROWS + r) * LROWB + q * 16) = v;
+    *reinterpret_cast<v4f*>(base + (a * LR + r) * LROWB + q * 16) = v;
 }
 
-// Record fields of one token for this lane's row, read before the token's
+// Record fields of one token for this lane's rows, read before the token's
 // first barrier so that their LDS latency overlaps the barrier wait.
-struct LineTok {
-    float al, be, rho, kap;
+struct LineRow {
+    float rho, kap;
     int l1, l2, lw;   // links of M_t[j_m], G[j_m], G[i_n]
+};
+template <int KR>
+struct LineTok {
+    LineRow r[KR];   // rows rg + 32 k
     v4f vv;
 };
 
-template <typename VT, int NS>
-__device__ __forceinline__ void line_read_tok(LineTok& x, const BwdCtx& c, int t) {
+template <typename VT, int NS, int KR>
+__device__ __forceinline__ void line_read_tok(LineTok<KR>& x, float& al, float& be, const BwdCtx& c, int t) {
     constexpr int VB = 8 * (int)sizeof(VT);
     const BwdRec& L = c.L;
     const unsigned char* rec = c.rring + (t & (NS - 1)) * L.bytes;
-    const int m = c.rg;
-    x.al = reinterpret_cast<const float*>(rec + L.off_ab)[0];
-    x.be = reinterpret_cast<const float*>(rec + L.off_ab)[1];
-    x.rho = reinterpret_cast<const float*>(rec + L.off_rval)[m];
-    x.kap = reinterpret_cast<const float*>(rec + L.off_wval)[m];
-    x.l1 = reinterpret_cast<const short*>(rec + L.off_lm)[m];
-    x.l2 = reinterpret_cast<const short*>(rec + L.off_lgr)[m];
-    x.lw = reinterpret_cast<const short*>(rec + L.off_lgw)[m];
+    al = reinterpret_cast<const float*>(rec + L.off_ab)[0];
+    be = reinterpret_cast<const float*>(rec + L.off_ab)[1];
+#pragma unroll
+    for (int k = 0; k < KR; ++k) {
+        const int m = c.rg + 32 * k;
+        x.r[k].rho = reinterpret_cast<const float*>(rec + L.off_rval)[m];
+        x.r[k].kap = reinterpret_cast<const float*>(rec + L.off_wval)[m];
+        x.r[k].l1 = reinterpret_cast<const short*>(rec + L.off_lm)[m];
+        x.r[k].l2 = reinterpret_cast<const short*>(rec + L.off_lgr)[m];
+        x.r[k].lw = reinterpret_cast<const short*>(rec + L.off_lgw)[m];
+    }
     x.vv = ld4v(reinterpret_cast<const VT*>(c.vring + (t & (NS - 1)) * VB) + c.cq * 4);
 }
 
-// One token on the pieces (row rg, columns 4 cq.. of slice w) read from the
-// row buffer; outputs to the staging buffer and the per-wave rings.
-template <int PD>
-__device__ __forceinline__ void bwd_token_line(const BwdCtx& c, const unsigned char* lb, unsigned char* sb,
-                                               int* flags, float* psum, const LineTok& x, v4f yb, int t, int w,
-                                               int lane) {
+// One token on the pieces (rows rg + 32 k, columns 4 cq.. of slice w) read from
+// the row buffer; outputs over those pieces and to the per-wave rings.
+template <int LR, int PD>
+__device__ __forceinline__ void bwd_token_line(const BwdCtx& c, unsigned char* lb, int* flags, float* psum,
+                                               const LineTok<LR / 32>& x, float al, float be, v4f yb, int t,
+                                               int w, int lane) {
     using namespace sdm_reduce;
     constexpr int SW = 8;
-    const int RW = 2 * LROWS;
-    const int m = c.rg;                 // read row and write row of this lane (W = R = 32)
-    const int q = 2 * w + c.cq;         // this lane's column quad within the line
-    float* prow = psum + w * LPART;   // this slice's partial sums of the token (LDS)
+    constexpr int KR = LR / 32;
+    constexpr int RW = 2 * LR;
+    const int q = 2 * w + c.cq;           // this lane's column quad within the line
+    float* prow = psum + w * lpart<LR>();   // this slice's partial sums of the token (LDS)
     float* gring_t = c.gring + (size_t)((t & (PD - 1)) * RW) * SW + c.cq * 4;
 
     // ---- read adjoint: rbar_m = <dy, M_t[j_m]>, G[j_m] += rho_m dy ----
-    const int i1 = x.l1 >= 0 ? (((t + (x.l1 >> 8)) & (PD - 1)) * LROWS + min(x.l1 & 255, LROWS - 1)) : 0;
-    const v4f Mv = v4sel(x.l1 >= 0, ld4(c.pring + i1 * SW + c.cq * 4), lds4(lb, 0, m, q));
-    const float rb = add_xor<1>(v4dot(yb, Mv));
-    const int i2 = x.l2 >= 0 ? (((t + (x.l2 >> 8)) & (PD - 1)) * RW + min(x.l2 & 255, RW - 1)) : 0;
-    v4f g = v4sel(x.l2 >= 0, ld4(c.gring + i2 * SW + c.cq * 4), lds4(lb, 1, m, q));
-    g = v4fma(x.rho, yb, g);
-    st4(gring_t + m * SW, g);
-    lds4_st(sb, 0, m, q, g);
+#pragma unroll
+    for (int k = 0; k < KR; ++k) {
+        const int m = c.rg + 32 * k;
+        const int l1 = x.r[k].l1, l2 = x.r[k].l2;
+        const int i1 = l1 >= 0 ? (((t + (l1 >> 8)) & (PD - 1)) * LR + min(l1 & 255, LR - 1)) : 0;
+        const v4f Mv = v4sel(l1 >= 0, ld4(c.pring + i1 * SW + c.cq * 4), lds4<LR>(lb, 0, m, q));
+        const float rb = add_xor<1>(v4dot(yb, Mv));
+        const int i2 = l2 >= 0 ? (((t + (l2 >> 8)) & (PD - 1)) * RW + min(l2 & 255, RW - 1)) : 0;
+        v4f g = v4sel(l2 >= 0, ld4(c.gring + i2 * SW + c.cq * 4), lds4<LR>(lb, 1, m, q));
+        g = v4fma(x.r[k].rho, yb, g);
+        st4(gring_t + m * SW, g);
+        lds4_st<LR>(lb, 1, m, q, g);
+        if (c.cq == 0) prow[m] = rb;
+    }
 
     // ---- write adjoint ----
-    const int ig = x.lw >= 0 ? (((t + (x.lw >> 8)) & (PD - 1)) * RW + min(x.lw & 255, RW - 1)) : 0;
-    const v4f gn = v4sel(x.lw >= 0, ld4(c.gring + ig * SW + c.cq * 4), lds4(lb, 2, m, q));
-    const v4f Ps = lds4(lb, 3, m, q);
-    const v4f D = x.al * Ps;
-    v4f up = x.kap * D, ebp = x.kap * gn;
+    v4f gn[KR], D[KR], Ps[KR];
+    v4f up = v4zero(), ebp = v4zero();
+#pragma unroll
+    for (int k = 0; k < KR; ++k) {
+        const int n = c.rg + 32 * k;
+        const int l = x.r[k].lw;
+        const int ig = l >= 0 ? (((t + (l >> 8)) & (PD - 1)) * RW + min(l & 255, RW - 1)) : 0;
+        gn[k] = v4sel(l >= 0, ld4(c.gring + ig * SW + c.cq * 4), lds4<LR>(lb, 2, n, q));
+        Ps[k] = lds4<LR>(lb, 3, n, q);
+        D[k] = al * Ps[k];
+        up = v4fma(x.r[k].kap, D[k], up);
+        ebp = v4fma(x.r[k].kap, gn[k], ebp);
+    }
     rows_allreduce8<2>(up, ebp);
     const v4f vmu = x.vv - up;
-    const v4f e = x.be * vmu;
+    const v4f e = be * vmu;
     const float bb = add_xor<1>(v4dot(ebp, vmu));
-    const float kb = add_xor<1>(v4dot(gn, e) - x.be * v4dot(ebp, D));
-    const v4f Db = v4fma(-x.be * x.kap, ebp, gn);
-    const float ab = wave_sum(v4dot(Db, Ps));
-    const v4f gnew = x.al * Db;
-    st4(gring_t + (LROWS + m) * SW, gnew);
-    st4(c.pring + ((t & (PD - 1)) * LROWS + m) * SW + c.cq * 4, Ps);
-    lds4_st(sb, 1, m, q, gnew);
-    lds4_st(sb, 2, m, q, Ps);
-    // a d = 0 link into the read part: this token also reads the slot it writes
-    const bool same = x.lw >= 0 && (x.lw >> 8) == 0 && (x.lw & 255) < LROWS;
-    flags[same ? (x.lw & 255) : LROWS + lane] = t;
-    // partial sums of this slice: the two lanes of row m hold rbar_m and kbar_m
-    // (each lane writes one); row 0 also writes dbeta and dalpha, and stores
-    // this slice's dv of the token
-    prow[c.cq * LROWS + m] = c.cq ? kb : rb;
+    float abl = 0.f;
+#pragma unroll
+    for (int k = 0; k < KR; ++k) {
+        const int n = c.rg + 32 * k;
+        const float kb = add_xor<1>(v4dot(gn[k], e) - be * v4dot(ebp, D[k]));
+        const v4f Db = v4fma(-be * x.r[k].kap, ebp, gn[k]);
+        abl += v4dot(Db, Ps[k]);
+        const v4f gnew = al * Db;
+        st4(gring_t + (LR + n) * SW, gnew);
+        st4(c.pring + ((t & (PD - 1)) * LR + n) * SW + c.cq * 4, Ps[k]);
+        lds4_st<LR>(lb, 2, n, q, gnew);
+        // a d = 0 link into the read part: this token also reads the slot it writes
+        const int l = x.r[k].lw;
+        const bool same = l >= 0 && (l >> 8) == 0 && (l & 255) < LR;
+        flags[same ? (l & 255) : LR + lane] = t;
+        if (c.cq == 1) prow[LR + n] = kb;
+    }
+    const float ab = wave_sum(abl);
+    // row 0 also writes dbeta and dalpha, and stores this slice's dv of the token
     if (lane < 2) {
-        st4(c.sdv + (size_t)t * c.dv, x.be * ebp);
+        st4(c.sdv + (size_t)t * c.dv, be * ebp);
         prow[RW + lane] = lane ? ab : bb;
     }
 }
@@ -479,21 +519,25 @@ __device__ __forceinline__ void bline_stage_store(const u4v (&st)[NC], u2v stv, 
     if (tk < cnt) *reinterpret_cast<u2v*>(vring + ((u0 + tk) & (NS - 1)) * VB + pc * 8) = stv;
 }
 
-// Slot ids (this lane's line row) of token u's read row and written row.
-__device__ __forceinline__ int2 line_slots(const BwdCtx& c, int u, int rl, int NS) {
+// Slot ids (this lane's line rows) of token u's read rows and written rows.
+template <int KR>
+__device__ __forceinline__ void line_slots(int2 (&sl)[KR], const BwdCtx& c, int u, int rl, int NS) {
     const unsigned char* rec = c.rring + (u & (NS - 1)) * c.L.bytes;
-    return make_int2(reinterpret_cast<const int*>(rec + c.L.off_rslot)[rl], reinterpret_cast<const int*>(rec)[rl]);
+#pragma unroll
+    for (int k = 0; k < KR; ++k)
+        sl[k] = make_int2(reinterpret_cast<const int*>(rec + c.L.off_rslot)[rl + 32 * k],
+                          reinterpret_cast<const int*>(rec)[rl + 32 * k]);
 }
 
 // The stream's memory table, adjoint table and saved rows as buffers (each below
 // 2 GiB, rows below 2^24): row s of a table at byte offset s 4 d_v + 4 lc, with
-// lc this lane's first line column, saved row (u, r) at (32 u + r) 4 d_v + 4 lc.
+// lc this lane's first line column, saved row (u, r) at (LR u + r) 4 d_v + 4 lc.
 // 32-bit offsets through a 24-bit multiply keep the address arithmetic off the
 // latency-bound token chain.
 struct LinePtrs {
     __amdgpu_buffer_rsrc_t mt, gt, sv;
     uint32_t dv4, lc4;
-    int rl;             // this lane's line row (0..31)
+    int rl;             // this lane's first line row (0..31)
     int lq;             // this lane's column quad within the line
 };
 
@@ -508,43 +552,61 @@ __device__ __forceinline__ uint32_t lrow_off(const LinePtrs& p, int row) {
     return __umul24((uint32_t)row, p.dv4) + p.lc4;
 }
 
-__device__ __forceinline__ void line_issue(LineBuf& b, const BwdCtx& c, const LinePtrs& p, int2 sl, int u) {
-    b.Mr = lbuf_ld(p.mt, lrow_off(p, sl.x));
-    b.Gr = lbuf_ld(p.gt, lrow_off(p, sl.x));
-    b.Gw = lbuf_ld(p.gt, lrow_off(p, sl.y));
-    b.Ps = lbuf_ld(p.sv, lrow_off(p, u * LROWS + p.rl));
+template <int LR>
+__device__ __forceinline__ void line_issue(LineBuf<LR / 32>& b, const BwdCtx& c, const LinePtrs& p,
+                                           const int2 (&sl)[LR / 32], int u) {
+#pragma unroll
+    for (int k = 0; k < LR / 32; ++k) {
+        b.Mr[k] = lbuf_ld(p.mt, lrow_off(p, sl[k].x));
+        b.Gr[k] = lbuf_ld(p.gt, lrow_off(p, sl[k].x));
+        b.Gw[k] = lbuf_ld(p.gt, lrow_off(p, sl[k].y));
+        b.Ps[k] = lbuf_ld(p.sv, lrow_off(p, u * LR + p.rl + 32 * k));
+    }
     b.Dy = ld4(c.sdy + (size_t)u * c.dv);
 }
 
-template <typename VT, int PD, int NS>
-__device__ __forceinline__ void line_step(const BwdCtx& c, const LinePtrs& p, unsigned char* lb,
-                                          unsigned char* sb, int* flags, float* psum, const LineBuf& cur,
-                                          LineBuf& nxt, int t, int tb, int w, int lane, bool issue) {
+template <typename VT, int LR, int PD, int NS>
+__device__ __forceinline__ void line_step(const BwdCtx& c, const LinePtrs& p, unsigned char* lb, int* flags,
+                                          float* psum, const LineBuf<LR / 32>& cur, LineBuf<LR / 32>& nxt, int t,
+                                          int tb, int w, int lane, bool issue) {
+    constexpr int KR = LR / 32;
+    constexpr int LP = lpart<LR>();
+    constexpr int PPW = (LP + LW - 1) / LW;   // partial sums each wave adds up
     const int u = max(t - PD + 1, tb);
-    LineTok x;
-    line_read_tok<VT, NS>(x, c, t);
-    const int2 st_sl = line_slots(c, t, p.rl, NS);
-    const int2 ld_sl = line_slots(c, u, p.rl, NS);
-    lds4_st(lb, 0, p.rl, p.lq, cur.Mr);
-    lds4_st(lb, 1, p.rl, p.lq, cur.Gr);
-    lds4_st(lb, 2, p.rl, p.lq, cur.Gw);
-    lds4_st(lb, 3, p.rl, p.lq, cur.Ps);
+    LineTok<KR> x;
+    float al, be;   // kept out of the struct: splats of struct fields become vector loads that pin it to memory
+    line_read_tok<VT, NS, KR>(x, al, be, c, t);
+    int2 st_sl[KR], ld_sl[KR];
+    line_slots<KR>(st_sl, c, t, p.rl, NS);
+    line_slots<KR>(ld_sl, c, u, p.rl, NS);
+#pragma unroll
+    for (int k = 0; k < KR; ++k) {
+        const int r = p.rl + 32 * k;
+        lds4_st<LR>(lb, 0, r, p.lq, cur.Mr[k]);
+        lds4_st<LR>(lb, 1, r, p.lq, cur.Gr[k]);
+        lds4_st<LR>(lb, 2, r, p.lq, cur.Gw[k]);
+        lds4_st<LR>(lb, 3, r, p.lq, cur.Ps[k]);
+    }
     __syncthreads();
     // every wave stored token t + 1 before the barrier: the loads may go now
-    if (issue) line_issue(nxt, c, p, ld_sl, u);
-    bwd_token_line<PD>(c, lb, sb, flags, psum, x, cur.Dy, t, w, lane);
+    if (issue) line_issue<LR>(nxt, c, p, ld_sl, u);
+    bwd_token_line<LR, PD>(c, lb, flags, psum, x, al, be, cur.Dy, t, w, lane);
     __syncthreads();
-    // the workgroup's partial sums of the token: wave w adds entries 17 w .. 17 w + 16
-    // of the four slices and stores them
-    const int pi = 17 * w + lane;
-    if (lane < 17 && pi < LPART)
-        c.spart[(size_t)t * LPART + pi] = ((psum[pi] + psum[LPART + pi]) + psum[2 * LPART + pi]) + psum[3 * LPART + pi];
-    if (flags[p.rl] != t) lbuf_st(p.gt, lrow_off(p, st_sl.x), lds4(sb, 0, p.rl, p.lq));
-    lbuf_st(p.gt, lrow_off(p, st_sl.y), lds4(sb, 1, p.rl, p.lq));
-    lbuf_st(p.mt, lrow_off(p, st_sl.y), lds4(sb, 2, p.rl, p.lq));
+    // the workgroup's partial sums of the token: wave w adds entries PPW w ..
+    // PPW w + PPW - 1 of the four slices and stores them
+    const int pi = PPW * w + lane;
+    if (lane < PPW && pi < LP)
+        c.spart[(size_t)t * LP + pi] = ((psum[pi] + psum[LP + pi]) + psum[2 * LP + pi]) + psum[3 * LP + pi];
+#pragma unroll
+    for (int k = 0; k < KR; ++k) {
+        const int r = p.rl + 32 * k;
+        if (flags[r] != t) lbuf_st(p.gt, lrow_off(p, st_sl[k].x), lds4<LR>(lb, 1, r, p.lq));
+        lbuf_st(p.gt, lrow_off(p, st_sl[k].y), lds4<LR>(lb, 2, r, p.lq));
+        lbuf_st(p.mt, lrow_off(p, st_sl[k].y), cur.Ps[k]);
+    }
 }
 
-template <typename VT, int PD, int NC>
+template <typename VT, int LR, int PD, int NC>
 __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
     const unsigned char* __restrict__ recs, const VT* __restrict__ v, float* __restrict__ mem,
     const float* __restrict__ saved, const float* __restrict__ dy, float* __restrict__ Gtab,
@@ -552,9 +614,11 @@ __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
     int n_slices, int S, int per_wave_lds) {
     // tokens te-1 down to tb of each stream (layout strides use T)
     constexpr int SW = 8;
+    constexpr int KR = LR / 32;
     constexpr int LEAD = bstage_lead<PD>();
     constexpr int NS = bstage_slots<PD>();
     constexpr int VB = SW * (int)sizeof(VT);
+    static_assert(LR == 32 || LR == 64, "32 or 64 rows per token");
     static_assert(PD % G == 0, "prefetch depth must be a multiple of the staging block");
     static_assert(NS >= LEAD && NS >= PD, "record ring too small");
 
@@ -565,34 +629,33 @@ __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
     const int slice = group * LW + w;   // n_slices is a multiple of LW: every wave exists
 
     BwdCtx c;
-    c.L = bwd_rec_layout(LROWS, LROWS);
+    c.L = bwd_rec_layout(LR, LR);
     c.dv = dv;
-    c.W = LROWS;
-    c.R = LROWS;
+    c.W = LR;
+    c.R = LR;
     c.rg = lane / 2;
     c.cq = lane % 2;
     c.colok = true;
     const int col = slice * SW + c.cq * 4;
 
     // LDS: the shared record ring, then per wave its v ring, adjoint ring and
-    // undo ring, then the row and staging buffers, flags and partial sums
+    // undo ring, then the row buffer, flags and partial sums
     extern __shared__ __align__(16) unsigned char smem[];
     unsigned char* rring = smem;
     unsigned char* vring = smem + (size_t)NS * c.L.bytes + (size_t)w * per_wave_lds;
     c.rring = rring;
     c.vring = vring;
     c.gring = reinterpret_cast<float*>(vring + NS * VB);
-    c.pring = c.gring + PD * 2 * LROWS * SW;
+    c.pring = c.gring + PD * 2 * LR * SW;
     c.mtab = mem + (size_t)stream * N * dv + col;
     c.gtab = Gtab + (size_t)stream * N * dv + col;
-    c.ssaved = saved + (size_t)stream * T * LROWS * dv + col;
+    c.ssaved = saved + (size_t)stream * T * LR * dv + col;
     c.sdy = dy + (size_t)stream * T * dv + col;
     c.sdv = dv_out + (size_t)stream * T * dv + col;
-    c.spart = part + ((size_t)group * S + stream) * T * LPART;   // per workgroup (4 slices)
+    c.spart = part + ((size_t)group * S + stream) * T * lpart<LR>();   // per workgroup (4 slices)
     unsigned char* lb = smem + (size_t)NS * c.L.bytes + (size_t)LW * per_wave_lds;
-    unsigned char* sb = lb + 4 * LROWS * LROWB;
-    int* flags = reinterpret_cast<int*>(sb + 3 * LROWS * LROWB);
-    float* psum = reinterpret_cast<float*>(flags + LFLAGS);
+    int* flags = reinterpret_cast<int*>(lb + 4 * LR * LROWB);
+    float* psum = reinterpret_cast<float*>(flags + lflags<LR>());
 
     LinePtrs p;
     p.rl = 8 * w + lane / 8;
@@ -601,19 +664,19 @@ __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
     const int tbytes = (int)((size_t)N * dv * 4);
     p.mt = __builtin_amdgcn_make_buffer_rsrc(mem + (size_t)stream * N * dv, 0, tbytes, 0x00020000);
     p.gt = __builtin_amdgcn_make_buffer_rsrc(Gtab + (size_t)stream * N * dv, 0, tbytes, 0x00020000);
-    p.sv = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(saved) + (size_t)stream * T * LROWS * dv, 0,
-                                             (int)((size_t)T * LROWS * dv * 4), 0x00020000);
+    p.sv = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(saved) + (size_t)stream * T * LR * dv, 0,
+                                             (int)((size_t)T * LR * dv * 4), 0x00020000);
     p.dv4 = (uint32_t)dv * 4;
     p.lc4 = lcol * 4;
 
     if (w == 0)
-        for (int i = lane; i < LFLAGS; i += SDM_WAVE) flags[i] = -1;
+        for (int i = lane; i < lflags<LR>(); i += SDM_WAVE) flags[i] = -1;
 
     const unsigned char* srec = recs + (size_t)stream * T * c.L.bytes;
     const VT* sv = v + (size_t)stream * T * dv + slice * SW;
     u4v st[NC];
     u2v stv;
-    LineBuf buf[PD];
+    LineBuf<KR> buf[PD];
 
     const int T1 = te - 1;
     for (int i0 = 0; i0 < LEAD - G; i0 += G) {
@@ -625,7 +688,9 @@ __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
 #pragma unroll
     for (int j = 0; j < PD - 1; ++j) {
         const int u = max(T1 - j, tb);
-        line_issue(buf[j], c, p, line_slots(c, u, p.rl, NS), u);
+        int2 sl[KR];
+        line_slots<KR>(sl, c, u, p.rl, NS);
+        line_issue<LR>(buf[j], c, p, sl, u);
     }
     __syncthreads();   // flags initialised
 
@@ -641,13 +706,16 @@ __global__ __launch_bounds__(LW * SDM_WAVE) void scan_bwd_line_kernel(
                 bline_stage_store<VT, NS, NC>(st, stv, rring, vring, t - (LEAD - G), tb, c.L.bytes, w, lane);
                 bline_stage_load<VT, NC>(st, stv, srec, sv, t - LEAD, tb, dv, slice, c.L.bytes, w, lane);
             }
-            line_step<VT, PD, NS>(c, p, lb, sb, flags, psum, buf[j], buf[(j + PD - 1) % PD], t, tb, w, lane, true);
+            line_step<VT, LR, PD, NS>(c, p, lb, flags, psum, buf[j], buf[(j + PD - 1) % PD], t, tb, w, lane,
+                                      true);
         }
     }
 #pragma unroll
     for (int j = 0; j < PD; ++j) {
         const int i = nfull + j;
-        if (i < n) line_step<VT, PD, NS>(c, p, lb, sb, flags, psum, buf[j], buf[(j + PD - 1) % PD], T1 - i, tb, w, lane, false);
+        if (i < n)
+            line_step<VT, LR, PD, NS>(c, p, lb, flags, psum, buf[j], buf[(j + PD - 1) % PD], T1 - i, tb, w, lane,
+                                      false);
     }
 }
 
@@ -735,40 +803,52 @@ bool bwd_plan(int S, int W, int R, int dv, int in_dtype, BwdPlan* p) {
     return bwd_plan_sw<BSW_MIN>(W, R, dv, in_dtype, p) || bwd_plan_sw<16>(W, R, dv, in_dtype, p);
 }
 
-// LDS of the line-cooperative kernel at prefetch depth PD: the shared record
-// ring, each wave's v, adjoint and undo rings, the row and staging buffers.
-template <int PD>
+// LDS of the line-cooperative kernel at LR rows and prefetch depth PD: the
+// shared record ring, each wave's v, adjoint and undo rings, the row buffer.
+template <int LR, int PD>
 size_t line_per_wave(int in_dtype) {
     const int vbytes = in_dtype == SDM_DT_BF16 ? 2 : 4;
-    return (size_t)bstage_slots<PD>() * 8 * vbytes + (size_t)PD * 2 * LROWS * 8 * 4 + (size_t)PD * LROWS * 8 * 4;
+    return (size_t)bstage_slots<PD>() * 8 * vbytes + (size_t)PD * 2 * LR * 8 * 4 + (size_t)PD * LR * 8 * 4;
 }
-template <int PD>
+template <int LR, int PD>
 size_t line_lds(int in_dtype) {
-    return (size_t)bstage_slots<PD>() * bwd_rec_layout(LROWS, LROWS).bytes + LW * line_per_wave<PD>(in_dtype) +
-           line_shared_bytes();
+    return (size_t)bstage_slots<PD>() * bwd_rec_layout(LR, LR).bytes + LW * line_per_wave<LR, PD>(in_dtype) +
+           line_shared_bytes<LR>();
 }
-constexpr int LNC = 1;   // 16-byte record chunks per lane for G records of W = R = 32
-static_assert(G * ((22 * LROWS + 8 + 15) / 16 * 16) <= LNC * LW * SDM_WAVE * 16, "line staging chunks");
+// 16-byte record chunks per lane for G records of W = R = LR
+template <int LR>
+constexpr int line_nc() {
+    return (G * ((22 * LR + 8 + 15) / 16 * 16) + LW * SDM_WAVE * 16 - 1) / (LW * SDM_WAVE * 16);
+}
+static_assert(line_nc<32>() == 1 && line_nc<64>() == 2, "line staging chunks");
 
-// The line-cooperative kernel's shape: 8-column slices, W = R = 32, d_v a
-// multiple of 32 (whole lines per workgroup), and its LDS within the limit.
-// Its table and saved-row offsets are 32-bit: each stream's tables and saved
-// rows below 2 GiB, their row counts below 2^24.
+// Rows per token of the line-cooperative kernel for this shape, or 0.
+int line_rows(const ScanBwdArgs& a) { return a.W == a.R && (a.W == 32 || a.W == 64) ? a.W : 0; }
+
+// The line-cooperative kernel's shape: W = R = 32 (where the per-wave plan
+// takes 8-column slices) or 64, d_v a multiple of 32 (whole lines per
+// workgroup of four 8-column slices), and its LDS within the limit.  Its table
+// and saved-row offsets are 32-bit: each stream's tables and saved rows below
+// 2 GiB, their row counts below 2^24.
 bool line_shape_ok(const ScanBwdArgs& a, const BwdPlan& p) {
+    const int LR = line_rows(a);
+    if (LR == 0 || a.dv % 32 != 0) return false;
     const size_t two_gib = (size_t)1 << 31;
     if ((size_t)a.N * a.dv * 4 >= two_gib || a.N >= (1 << 24)) return false;
-    if ((size_t)a.T * LROWS * a.dv * 4 >= two_gib || (size_t)a.T * LROWS >= ((size_t)1 << 24)) return false;
-    return p.SW == 8 && p.K == 1 && a.W == LROWS && a.R == LROWS && a.dv % 32 == 0 && p.n_slices % LW == 0 &&
-           line_lds<BPD>(a.in_dtype) <= (size_t)LDS_LIMIT;
+    if ((size_t)a.T * LR * a.dv * 4 >= two_gib || (size_t)a.T * LR >= ((size_t)1 << 24)) return false;
+    if (LR == 32) return p.SW == 8 && line_lds<32, BPD>(a.in_dtype) <= (size_t)LDS_LIMIT;
+    return line_lds<64, BPD>(a.in_dtype) <= (size_t)LDS_LIMIT;
 }
 // Prefetch depth of the line-cooperative kernel: 4 tokens, or 8 when
-// sdm_set_scan_prefetch forces 8 or 16 (the shared record ring leaves LDS for
-// the deeper adjoint and undo rings).  At the training workload 8 measured no
-// faster (1.13 against 1.12 ms per stage) and doubled the records' link search
-// (0.83 against 0.39 ms per stage beside the scan).
+// sdm_set_scan_prefetch forces 8 or 16 and the LDS holds it (32 rows: the
+// shared record ring leaves LDS for the deeper adjoint and undo rings).  At the
+// training workload 8 measured no faster (1.13 against 1.12 ms per stage) and
+// doubled the records' link search (0.83 against 0.39 ms per stage beside the
+// scan).
 int line_pd(const ScanBwdArgs& a) {
     const int forced = sdm_scan_prefetch();
-    return forced >= 8 && line_lds<BPD_LINE>(a.in_dtype) <= (size_t)LDS_LIMIT ? BPD_LINE : BPD;
+    return forced >= 8 && line_rows(a) == 32 && line_lds<32, BPD_LINE>(a.in_dtype) <= (size_t)LDS_LIMIT ? BPD_LINE
+                                                                                                        : BPD;
 }
 bool line_io_ok(const ScanBwdArgs& a, const BwdPlan& p) { return sdm_line_io_enabled() && line_shape_ok(a, p); }
 // a.line >= 0: the caller's decision (one per call, so that every range and the
@@ -778,28 +858,33 @@ bool use_line(const ScanBwdArgs& a, const BwdPlan& p, bool* ok) {
     return a.line >= 0 ? (a.line != 0 && *ok) : line_io_ok(a, p);
 }
 
-// line: run the line-cooperative kernel (line_io_ok held); its partial sums
-// are per workgroup of LW slices.
+// The line-cooperative kernel (line_shape_ok held): d_v / 32 workgroups of four
+// 8-column slices per stream, whose partial sums are per workgroup.  It asks
+// for more than half a CU's LDS, so that no two of its workgroups share a CU:
+// at the 32-row training workload (256 workgroups) two per CU took the scan
+// from 1.13 to 1.38 ms per stage, their token chains sharing the SIMDs while
+// other CUs idled.
+template <typename VT, int LR, int PD>
+hipError_t launch_bwd_line(const ScanBwdArgs& a, float* part, hipStream_t st) {
+    auto kl = scan_bwd_line_kernel<VT, LR, PD, line_nc<LR>()>;
+    const size_t sml = std::max(line_lds<LR, PD>(a.in_dtype), (size_t)LDS_LIMIT / 2 + 1024);
+    const size_t pw = line_per_wave<LR, PD>(a.in_dtype);
+    hipError_t e = hipFuncSetAttribute((const void*)kl, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sml);
+    if (e != hipSuccess) return e;
+    const int S = a.B * a.H;
+    const int n_slices = a.dv / 8;
+    hipLaunchKernelGGL(kl, dim3(n_slices / LW * S), dim3(LW * SDM_WAVE), sml, st, a.ws + SDM_WS_HEADER,
+                       static_cast<const VT*>(a.v), a.mem, a.saved, a.dy, a.G, a.dv_out, part, a.T, a.tb, a.te,
+                       a.dv, a.N, n_slices, S, (int)pw);
+    return hipGetLastError();
+}
+
 template <typename VT, int SW, int K>
-hipError_t launch_bwd_k(const ScanBwdArgs& a, const BwdPlan& p, bool line, float* part, hipStream_t st) {
+hipError_t launch_bwd_k(const ScanBwdArgs& a, const BwdPlan& p, float* part, hipStream_t st) {
     constexpr int NR = bnr_for_k<SW>(K);
     const int S = a.B * a.H;
     dim3 grid((p.n_slices + p.wpb - 1) / p.wpb * S);   // XCD-aware order: scan_wg_coords<true>
     const size_t sm = (size_t)p.lds_per_wave * p.wpb;
-    if constexpr (SW == 8 && K == 1) {
-        if (line) {
-            const bool deep = line_pd(a) == BPD_LINE;
-            auto kl = deep ? scan_bwd_line_kernel<VT, BPD_LINE, LNC> : scan_bwd_line_kernel<VT, BPD, LNC>;
-            const size_t sml = deep ? line_lds<BPD_LINE>(a.in_dtype) : line_lds<BPD>(a.in_dtype);
-            const size_t pw = deep ? line_per_wave<BPD_LINE>(a.in_dtype) : line_per_wave<BPD>(a.in_dtype);
-            hipError_t e = hipFuncSetAttribute((const void*)kl, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sml);
-            if (e != hipSuccess) return e;
-            hipLaunchKernelGGL(kl, dim3(p.n_slices / LW * S), dim3(LW * SDM_WAVE), sml, st, a.ws + SDM_WS_HEADER,
-                               static_cast<const VT*>(a.v), a.mem, a.saved, a.dy, a.G, a.dv_out, part, a.T,
-                               a.tb, a.te, a.dv, a.N, p.n_slices, S, (int)pw);
-            return hipGetLastError();
-        }
-    }
     auto kfn = scan_bwd_kernel<VT, SW, bpd_for_k(K), K, NR>;
     hipError_t e = hipFuncSetAttribute((const void*)kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
     if (e != hipSuccess) return e;
@@ -811,14 +896,19 @@ hipError_t launch_bwd_k(const ScanBwdArgs& a, const BwdPlan& p, bool line, float
 
 template <typename VT>
 hipError_t launch_bwd_kk(const ScanBwdArgs& a, const BwdPlan& p, bool line, float* part, hipStream_t st) {
-    if (p.SW == 8) {
-        if (p.K == 1) return launch_bwd_k<VT, 8, 1>(a, p, line, part, st);
-        if (p.K == 2) return launch_bwd_k<VT, 8, 2>(a, p, false, part, st);
-        return launch_bwd_k<VT, 8, 4>(a, p, false, part, st);
+    if (line) {
+        if (line_rows(a) == 64) return launch_bwd_line<VT, 64, BPD>(a, part, st);
+        return line_pd(a) == BPD_LINE ? launch_bwd_line<VT, 32, BPD_LINE>(a, part, st)
+                                      : launch_bwd_line<VT, 32, BPD>(a, part, st);
     }
-    if (p.K == 1) return launch_bwd_k<VT, 16, 1>(a, p, false, part, st);
-    if (p.K == 2) return launch_bwd_k<VT, 16, 2>(a, p, false, part, st);
-    return launch_bwd_k<VT, 16, 4>(a, p, false, part, st);
+    if (p.SW == 8) {
+        if (p.K == 1) return launch_bwd_k<VT, 8, 1>(a, p, part, st);
+        if (p.K == 2) return launch_bwd_k<VT, 8, 2>(a, p, part, st);
+        return launch_bwd_k<VT, 8, 4>(a, p, part, st);
+    }
+    if (p.K == 1) return launch_bwd_k<VT, 16, 1>(a, p, part, st);
+    if (p.K == 2) return launch_bwd_k<VT, 16, 2>(a, p, part, st);
+    return launch_bwd_k<VT, 16, 4>(a, p, part, st);
 }
 
 size_t bwd_part_offset(int B, int H, int T, int W, int R) {
@@ -854,7 +944,7 @@ hipError_t sdm_launch_bwd_prep_range(const ScanBwdArgs& a, hipStream_t st) {
     const bool line = use_line(a, plan, &ok);
     if (!ok) return hipErrorInvalidConfiguration;
     SdmProfScope ps(SDM_K_BWD_PREP, st);
-    if (line && line_pd(a) == BPD_LINE) return sdm_launch_bwd_prep<BPD_LINE>(a, st);
+    if (line) return line_pd(a) == BPD_LINE ? sdm_launch_bwd_prep<BPD_LINE>(a, st) : sdm_launch_bwd_prep<BPD>(a, st);
     return plan.PD == 2 ? sdm_launch_bwd_prep<2>(a, st) : sdm_launch_bwd_prep<BPD>(a, st);
 }
 
@@ -876,7 +966,7 @@ hipError_t sdm_launch_bwd_reduce_range(const ScanBwdArgs& a, hipStream_t st) {
     bool ok;
     const bool line = use_line(a, plan, &ok);
     if (!ok) return hipErrorInvalidConfiguration;
-    const int n_parts = line ? plan.n_slices / LW : plan.n_slices;   // partial sums per (stream, token)
+    const int n_parts = line ? a.dv / 32 : plan.n_slices;   // partial sums per (stream, token)
     const float* part = reinterpret_cast<const float*>(a.ws + bwd_part_offset(a.B, a.H, a.T, a.W, a.R));
     const int S = a.B * a.H, n = a.te - a.tb;
     if (S == 0 || n <= 0) return hipSuccess;

@@ -531,11 +531,11 @@ def test_backward_chunk_invariance(name):
             assert np.array_equal(o[k], outs[0][k]), k
 
 
-# Line-cooperative backward kernel (8-column slices, W = R = 32, d_v a multiple of 32):
-# against the oracle, and against the per-wave kernel (same arithmetic per slice; the
+# Line-cooperative backward kernel (8-column slices, W = R = 32 or 64, d_v a multiple of
+# 32): against the oracle, and against the per-wave kernel (same arithmetic per slice; the
 # compiler may contract a product into an fma differently, so to 1e-5, not bit for bit).  N = 1024 with 32
-# slots per side makes a token's read and write sets share a slot in most tokens and
-# rows recur within the prefetch window; T = 3 is shorter than the load lead.
+# slots per side (4096 with 64) makes a token's read and write sets share a slot in most
+# tokens and rows recur within the prefetch window; T = 3 is shorter than the load lead.
 LINE = {
     "bf16-line-ragged": synth.Workload("t", B=1, H=2, T=203, d_k=64, d_v=64, N=1024, topk=32, seed=41,
                                        train=True),
@@ -543,6 +543,12 @@ LINE = {
                                       seed=42, codebook=False, train=True),
     "bf16-line-T3": synth.Workload("t", B=1, H=1, T=3, d_k=32, d_v=96, N=1024, topk=32, seed=43,
                                    m0="shared", train=True),
+    "bf16-line64-ragged": synth.Workload("t", B=1, H=2, T=131, d_k=64, d_v=64, N=4096, topk=64, seed=44,
+                                         train=True),
+    "f32-line64-direct": synth.Workload("t", B=2, H=1, T=57, d_k=128, d_v=96, N=4096, topk=64, dtype="f32",
+                                        seed=45, codebook=False, train=True),
+    "bf16-line64-T3": synth.Workload("t", B=1, H=1, T=3, d_k=32, d_v=32, N=4096, topk=64, seed=46,
+                                     m0="shared", train=True),
 }
 
 
