@@ -179,6 +179,8 @@ def main():
     ap.add_argument("--train-chunk", type=int, default=0,
                     help="tokens per pipeline stage of the training step's forward (0: the library's "
                          "choice, measured best there)")
+    ap.add_argument("--paper-shapes", default="1.4b,8b",
+                    help="the paper's layer shapes the paper leg times (comma-separated: 1.4b, 8b)")
     ap.add_argument("--calib", action="store_true",
                     help="first run one plain 512 MiB copy (sdm_mem_init from a [16, 65536, 128] fp32 "
                          "source): the reference dispatch for scaling HBM counters")
@@ -543,8 +545,10 @@ def main():
                   ("8b", 480, synth.Workload("paper-8b-layer", B=4, H=2, T=4096, d_k=960, d_v=1920,
                                              N=230400, topk=64, seed=8, codebook=False)))
         out["paper_layer"] = {}
+        want = set(args.paper_shapes.split(","))
         for tag, root, wp in shapes:
-            out["paper_layer"][tag] = paper_layer(sdm, to_dev, wp, tag, root, stream, dev)
+            if tag in want:
+                out["paper_layer"][tag] = paper_layer(sdm, to_dev, wp, tag, root, stream, dev)
 
     print(json.dumps(out), flush=True)
 
