@@ -516,7 +516,7 @@ def test_backward_small(name, slice_width):
     assert errs["mem_restored_bit_exact"]
 
 
-@pytest.mark.parametrize("name", ["bf16-small", "bf16-line-ragged"])
+@pytest.mark.parametrize("name", ["bf16-small", "bf16-line-ragged", "bf16-line64-ragged"])
 def test_backward_chunk_invariance(name):
     """chunk sets the backward's pipeline stages (chunk >= T: one stage); results
     are the same bit for bit (per-wave kernel, and the line-cooperative one)."""
@@ -660,6 +660,22 @@ def test_full_c4_training():
     S = w.B * w.H
     errs, _ = run_backward_case(w, inp, [1, S - 2], chunk=w.chunk, fwd_chunk=0)
     report("c4/bwd", **errs)
+    for k, e in errs.items():
+        if k != "mem_restored_bit_exact":
+            assert within(e, w), (k, e)
+    assert errs["mem_restored_bit_exact"]
+
+
+def test_full_paper_1p4b_training():
+    """The paper's 1.4B layer (W = R = 64, d_v = 960, direct addressing) at full size through
+    the bench's training calls: sdm_forward with the undo log, then the staged backward
+    (chunk 64), which runs the 64-row line-cooperative kernel; two sampled streams against
+    the oracle's reverse pass on the GPU's own slot lists."""
+    w = synth.Workload("paper-1.4b-layer", B=8, H=2, T=4096, d_k=480, d_v=960, N=57600, topk=64, seed=6,
+                       codebook=False, train=True)
+    inp = synth.Inputs(w)
+    errs, _ = run_backward_case(w, inp, [3, 12], chunk=64, fwd_chunk=0)
+    report("paper-1.4b/bwd", **errs)
     for k, e in errs.items():
         if k != "mem_restored_bit_exact":
             assert within(e, w), (k, e)
