@@ -433,8 +433,8 @@ int sdm_set_scan_slice_width(int sw);
  *       then set by the row loads' latency over the tokens in flight);
  *   4, 8, 16  force that depth for the line-cooperative forward kernel (the
  *       per-wave kernels always take 4, or 2 for four-pass backward shapes);
- *       8 and 16 also give the line-cooperative backward kernel a depth of 8
- *       (its default is 4).
+ *       8 and 16 also give the line-cooperative backward kernel at 32 rows a
+ *       depth of 8 (its default, and its depth at 64 rows, is 4).
  * Results do not depend on it.  Process-wide; applies to launches that start
  * after the call.  Any other value returns SDM_ERR_INVALID_ARG.
  * ---------------------------------------------------------------------- */

@@ -625,7 +625,6 @@ int sdm_forward_impl(const void* q, const void* k, int x_dtype, const void* cb_q
     int dev = 0;
     if ((e = side_get(sp, nchunks + 1, &side, &evp, &dev)) != hipSuccess) return hip_fail(e, "sdm_forward side stream");
     std::vector<hipEvent_t>& ev = *evp;
-    a.beside = true;   // every stage's records and scan share the depth chosen beside the addressing
     // the side stream starts after the caller's earlier work; chunk c's scan waits for its front
     if ((e = hipEventRecord(ev[0], st)) != hipSuccess) return hip_fail(e, "sdm_forward record");
     if ((e = hipStreamWaitEvent(side, ev[0], 0)) != hipSuccess) return hip_fail(e, "sdm_forward wait");

@@ -746,8 +746,8 @@ int sdm_fwd_pd(const ScanFwdArgs& a) {
     if (!fwd_plan(a.B * a.H, a.W, a.R, a.dv, a.in_dtype, &p)) return FWD_PD;
     if (!fline_fits<FWD_PD>(a, p)) return FWD_PD;   // per-wave kernel
     const int forced = sdm_scan_prefetch();
-    const int deep = a.beside ? 8 : SDM_FWD_PD_DEEP;
-    const int want = forced ? forced : ((int64_t)a.B * a.H * p.n_slices < sdm_device_simds() ? deep : FWD_PD);
+    const int want =
+        forced ? forced : ((int64_t)a.B * a.H * p.n_slices < sdm_device_simds() ? SDM_FWD_PD_DEEP : FWD_PD);
     if (want >= 16 && fline_fits<16>(a, p)) return 16;
     if (want >= 8 && fline_fits<8>(a, p)) return 8;
     return FWD_PD;

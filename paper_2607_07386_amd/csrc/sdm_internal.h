@@ -99,10 +99,6 @@ struct ScanFwdArgs {
     // are formed per token (A, b_dt per head, fp32).
     const float* gate_A = nullptr;
     const float* gate_bdt = nullptr;
-    // The scan runs beside the next stage's addressing (sdm_forward's pipeline):
-    // the automatic prefetch depth for launches with fewer waves than SIMDs is
-    // then 8, whose LDS leaves room for the addressing workgroups.
-    bool beside = false;
 };
 hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st);   // prep + scan
 // the two halves separately (records of [tb, te), then the scan of [tb, te))
