@@ -170,9 +170,9 @@ def main():
                     help="skip the reference timing of the forward step as three separate calls")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the memory-initialisation and decode legs")
-    ap.add_argument("--chunk", type=int, default=448,
+    ap.add_argument("--chunk", type=int, default=384,
                     help="tokens per pipeline stage of the forward step (0: the library's choice, a "
-                         "quarter of T; 448, measured best for this workload, by default)")
+                         "quarter of T; 384, measured best for this workload, by default)")
     ap.add_argument("--learned-chunk", type=int, default=1024,
                     help="tokens per pipeline stage of the learned-M0 forward step (0: the library's "
                          "choice, a quarter of T; 1024, measured best there, by default)")

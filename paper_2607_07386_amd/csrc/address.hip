@@ -1321,6 +1321,31 @@ __global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel(const XT* __
                                       score, smem);
 }
 
+// The same tiles (not half_seq shapes) from a grid of at most gridDim.x
+// workgroups, for a launch that shares the CUs with other work: each
+// workgroup takes tiles, stream-major, at the grid's stride.  Beside the
+// pipelined forward's scan the grid is the workgroups that fit in the LDS the
+// scan leaves on each CU.  With one workgroup per tile, addressing
+// workgroups took the LDS that the next scan stage's workgroups waited for:
+// at the 1.4B-shaped workload the scan stages ran at 0.62 instead of 0.55 ms.
+template <typename XT, int MODE, int E, int KM>
+__global__ __launch_bounds__(AWAVES * SDM_WAVE) void address_kernel_looped(const XT* __restrict__ x,
+                                                                           const XT* __restrict__ cb, int H, int T,
+                                                                           int tb, int te, int dk, int s, int k,
+                                                                           int32_t* __restrict__ idx,
+                                                                           float* __restrict__ val,
+                                                                           float* __restrict__ score, int nstreams) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int ntiles = (te - tb + atile<E>() - 1) / atile<E>();
+    const int total = ntiles * nstreams;
+    for (int id = blockIdx.x; id < total; id += gridDim.x) {
+        const int stream = id / ntiles, tile = id - stream * ntiles;
+        address_tile<XT, MODE, E, KM>(x, cb, H, T, stream, tb + tile * atile<E>(), te, dk, s, k, idx, val, score,
+                                      smem);
+        __syncthreads();   // every wave is done with this tile's LDS before the next tile's scores
+    }
+}
+
 // ---- one token per stream (decode) ----------------------------------------
 // Scores of the decode step's two rows (read query with cb_q, write key with
 // cb_k) on the matrix cores, bf16 codebooks with d_k / 2 <= 64 and E <= 4:
@@ -1732,7 +1757,8 @@ hipError_t launch_address_reg(const void* x, const void* cb, int B, int H, int T
 
 template <typename XT, int MODE>
 hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, int tb, int tn, int dk,
-                            int s, int k, int32_t* idx, float* val, float* score, hipStream_t st) {
+                            int s, int k, int32_t* idx, float* val, float* score, hipStream_t st,
+                            size_t lds_free) {
     const int E = (s + SDM_WAVE - 1) / SDM_WAVE;
     if constexpr (MODE == 2) {
         // bf16 codebooks, sqrt(N) in (256, 1024], d_k / 2 <= 64, k <= 32:
@@ -1751,6 +1777,20 @@ hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, 
     {                                                                                           \
         constexpr int AT = tile_tokens<EE, KM>();                                               \
         const size_t sm = tile_lds_bytes<EE, KM>();                                             \
+        if constexpr (!half_seq<EE, KM>()) {                                                     \
+            /* beside other work: the workgroups that fit in the LDS it leaves on each CU, */  \
+            /* when two or more do (with one per CU the paper's 1.4B layer measured slower) */  \
+            const int cap = (int)(lds_free / sm) * (sdm_device_simds() / 4);                    \
+            if (lds_free >= 2 * sm && (int64_t)((tn + AT - 1) / AT) * B * H > cap) {            \
+                auto kl = address_kernel_looped<XT, MODE, EE, KM>;                              \
+                hipError_t e = hipFuncSetAttribute((const void*)kl,                             \
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm); \
+                if (e != hipSuccess) return e;                                                  \
+                hipLaunchKernelGGL(kl, dim3(cap), dim3(AWAVES * SDM_WAVE), sm, st, xp, cp, H, T, tb, tb + tn, \
+                                   dk, s, k, idx, val, score, B * H);                           \
+                return hipGetLastError();                                                       \
+            }                                                                                   \
+        }                                                                                       \
         auto kfn = address_kernel<XT, MODE, EE, KM>;                                            \
         hipError_t e = hipFuncSetAttribute((const void*)kfn,                                    \
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm); \
@@ -1777,16 +1817,16 @@ hipError_t launch_address_e(const void* x, const void* cb, int B, int H, int T, 
 
 hipError_t sdm_launch_address(const void* x, int x_dtype, const void* cb, int B, int H, int T,
                               int tb, int tn, int dk, int s, int k, int32_t* idx, float* val,
-                              float* score, hipStream_t st) {
+                              float* score, hipStream_t st, size_t lds_free) {
     if (tn <= 0) return hipSuccess;
     if (x_dtype == SDM_DT_BF16) {
-        if (!cb) return launch_address_e<bf16_t, 0>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st);
+        if (!cb) return launch_address_e<bf16_t, 0>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st, lds_free);
         if ((dk / 2) % 8 == 0)
-            return launch_address_e<bf16_t, 2>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st);
-        return launch_address_e<bf16_t, 1>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st);
+            return launch_address_e<bf16_t, 2>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st, lds_free);
+        return launch_address_e<bf16_t, 1>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st, lds_free);
     }
-    if (!cb) return launch_address_e<float, 0>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st);
-    return launch_address_e<float, 1>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st);
+    if (!cb) return launch_address_e<float, 0>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st, lds_free);
+    return launch_address_e<float, 1>(x, cb, B, H, T, tb, tn, dk, s, k, idx, val, score, st, lds_free);
 }
 
 namespace {

@@ -216,6 +216,7 @@ int check_scan_fwd_rest(int W, int R, int in_dtype, int B, int H, int T, int d_v
 // ---- state of the fused forward's pipeline ----
 namespace {
 constexpr int kMaxChunks = 64;
+constexpr size_t kCuLds = 160 * 1024;   // LDS per CU (gfx950)
 constexpr int kMaxDevices = 64;
 struct SidePipe {
     std::mutex mu;
@@ -587,18 +588,20 @@ int sdm_forward_impl(const void* q, const void* k, int x_dtype, const void* cb_q
     a.y = y; a.saved = saved; a.ws = static_cast<unsigned char*>(workspace);
     a.gate_A = gA; a.gate_bdt = gbdt;
 
-    auto stage_front = [&](int tb, int te, hipStream_t sx) -> hipError_t {
+    // lds_free > 0: the stage's addressing runs beside a scan stage, which holds
+    // the rest of every CU's LDS
+    auto stage_front = [&](int tb, int te, hipStream_t sx, size_t lds_free) -> hipError_t {
         hipError_t ee;
         {
             SdmProfScope ps(SDM_K_ADDRESS, sx);
             ee = sdm_launch_address(q, x_dtype, cb_q, B, H, T, tb, te - tb, d_k, s, R, r_idx, r_val,
-                                    nullptr, sx);
+                                    nullptr, sx, lds_free);
         }
         if (ee != hipSuccess) return ee;
         {
             SdmProfScope ps(SDM_K_ADDRESS, sx);
             ee = sdm_launch_address(k, x_dtype, cb_k, B, H, T, tb, te - tb, d_k, s, W, w_idx, w_val,
-                                    nullptr, sx);
+                                    nullptr, sx, lds_free);
         }
         if (ee != hipSuccess) return ee;
         ScanFwdArgs ac = a;
@@ -608,7 +611,7 @@ int sdm_forward_impl(const void* q, const void* k, int x_dtype, const void* cb_q
     };
 
     if (nchunks == 1) {
-        e = stage_front(0, T, st);
+        e = stage_front(0, T, st, 0);
         if (e == hipSuccess) {
             a.tb = 0;
             a.te = T;
@@ -628,9 +631,13 @@ int sdm_forward_impl(const void* q, const void* k, int x_dtype, const void* cb_q
     // the side stream starts after the caller's earlier work; chunk c's scan waits for its front
     if ((e = hipEventRecord(ev[0], st)) != hipSuccess) return hip_fail(e, "sdm_forward record");
     if ((e = hipStreamWaitEvent(side, ev[0], 0)) != hipSuccess) return hip_fail(e, "sdm_forward wait");
+    const size_t scan_lds = sdm_fwd_scan_lds(a);
+    const size_t lds_beside = scan_lds < kCuLds ? kCuLds - scan_lds : 0;
     for (int c = 0; c < nchunks; ++c) {
         const int tb = stage_begin(c), te = stage_begin(c + 1) > tb ? stage_begin(c + 1) : T;
-        if ((e = stage_front(tb, te, side)) != hipSuccess) return hip_fail(e, "sdm_forward launch");
+        // stage 0's addressing has the device to itself; later stages' run beside the previous scan
+        if ((e = stage_front(tb, te, side, c == 0 ? 0 : lds_beside)) != hipSuccess)
+            return hip_fail(e, "sdm_forward launch");
         if ((e = hipEventRecord(ev[c + 1], side)) != hipSuccess) return hip_fail(e, "sdm_forward record");
         if ((e = hipStreamWaitEvent(st, ev[c + 1], 0)) != hipSuccess) return hip_fail(e, "sdm_forward wait");
         a.tb = tb;

@@ -782,6 +782,37 @@ hipError_t sdm_launch_fwd_scan_range(const ScanFwdArgs& a, hipStream_t st) {
     return save ? launch_fwd_kk<float, true>(a, p, pd, st) : launch_fwd_kk<float, false>(a, p, pd, st);
 }
 
+namespace {
+template <int SW, int K>
+size_t fwd_lds_k(const ScanFwdArgs& a, const FwdPlan& p, int pd, bool save) {
+    constexpr int FR = K * (SDM_WAVE / (SW / 4));
+    size_t lds = 0, per_wave = 0;
+    if constexpr (FR == 32 || FR == 64) {
+        if (pd == 16 && fline_ok<SW, FR, 16>(a, p, save, &lds, &per_wave)) return lds;
+        if (pd == 8 && fline_ok<SW, FR, 8>(a, p, save, &lds, &per_wave)) return lds;
+        if (pd == FWD_PD && fline_ok<SW, FR, FWD_PD>(a, p, save, &lds, &per_wave)) return lds;
+    }
+    return (size_t)p.lds_per_wave * p.wpb;
+}
+}  // namespace
+
+// LDS of one workgroup of the forward scan these arguments launch (the kernel
+// and depth sdm_launch_fwd_scan_range picks).
+size_t sdm_fwd_scan_lds(const ScanFwdArgs& a) {
+    FwdPlan p;
+    if (!fwd_plan(a.B * a.H, a.W, a.R, a.dv, a.in_dtype, &p)) return 0;
+    const int pd = sdm_fwd_pd(a);
+    const bool save = a.saved != nullptr;
+    if (p.SW == 8) {
+        if (p.K == 1) return fwd_lds_k<8, 1>(a, p, pd, save);
+        if (p.K == 2) return fwd_lds_k<8, 2>(a, p, pd, save);
+        return fwd_lds_k<8, 4>(a, p, pd, save);
+    }
+    if (p.K == 1) return fwd_lds_k<16, 1>(a, p, pd, save);
+    if (p.K == 2) return fwd_lds_k<16, 2>(a, p, pd, save);
+    return fwd_lds_k<16, 4>(a, p, pd, save);
+}
+
 hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st) {
     hipError_t e = sdm_launch_fwd_prep_range(a, st);
     if (e != hipSuccess) return e;

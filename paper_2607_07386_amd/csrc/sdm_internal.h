@@ -62,9 +62,13 @@ __host__ __device__ inline BwdRec bwd_rec_layout(int W, int R) {
 #define SDM_WS_HEADER 256
 
 // Tokens [tb, tb + tn) of every stream (layout strides use T).
+// lds_free > 0: the launch shares every CU with work that holds the rest of its
+// LDS (the pipelined forward's scan), and keeps to the workgroups that fit
+// beside it (when two or more do), each looping over tiles (0: one workgroup
+// per tile).
 hipError_t sdm_launch_address(const void* x, int x_dtype, const void* cb, int B, int H, int T,
                               int tb, int tn, int dk, int s, int k, int32_t* idx, float* val,
-                              float* score, hipStream_t st);
+                              float* score, hipStream_t st, size_t lds_free = 0);
 // token-sides (b, h, t) for t in [tb, tb + tn)
 // One token per stream (T = 1, no undo log): addressing of both sides and the
 // scan step in one launch, one workgroup per stream.  cb_q and cb_k are both
@@ -101,6 +105,7 @@ struct ScanFwdArgs {
     const float* gate_bdt = nullptr;
 };
 hipError_t sdm_launch_scan_fwd(const ScanFwdArgs& a, hipStream_t st);   // prep + scan
+size_t sdm_fwd_scan_lds(const ScanFwdArgs& a);   // LDS of one workgroup of that scan
 // the two halves separately (records of [tb, te), then the scan of [tb, te))
 hipError_t sdm_launch_fwd_prep_range(const ScanFwdArgs& a, hipStream_t st);
 hipError_t sdm_launch_fwd_scan_range(const ScanFwdArgs& a, hipStream_t st);

@@ -46,7 +46,7 @@ def _fused(w, inp, chunk, save):
 
 
 @pytest.mark.parametrize("name", list(CASES))
-@pytest.mark.parametrize("chunk", [0, 64, 100, 256, 448, 4096])
+@pytest.mark.parametrize("chunk", [0, 64, 100, 256, 384, 448, 4096])
 def test_fused_forward_matches_separate_calls(name, chunk, slice_width):
     w = CASES[name]
     inp = synth.Inputs(w)

@@ -606,7 +606,7 @@ def test_backward_line_prefetch_depths(name):
 
 # ------------------------------------------------- full-size workloads, sampled streams
 # Each runs the calls bench.py times: the 1.4B-shaped forward as sdm_forward
-# with 448-token stages, the training step as sdm_forward with the undo log
+# with 384-token stages, the training step as sdm_forward with the undo log
 # (the library's stage choice) and then sdm_scan_bwd with chunk 64.  The
 # long-context and learned-M0 workloads run sdm_forward with the library's
 # stages (a quarter of T).
@@ -624,7 +624,7 @@ def _full(cfg, streams_of, chunk):
 
 @pytest.mark.slow
 def test_full_c1():
-    _full(1, lambda S: [0, S // 2 + 3, S - 1], chunk=448)
+    _full(1, lambda S: [0, S // 2 + 3, S - 1], chunk=384)
 
 
 @pytest.mark.slow
