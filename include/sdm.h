@@ -144,9 +144,9 @@ int sdm_scan_fwd(const int32_t* w_idx, const float* w_val, int W,
  *                 as for sdm_scan_fwd (workspace of
  *                 sdm_scan_fwd_workspace_bytes(B, H, T, topk, topk)).
  *   chunk         tokens per pipeline stage, rounded up to a multiple of 64
- *                 and to at most 64 stages; the first stage is a quarter of
- *                 that (its addressing has nothing to overlap).  0 picks T/4
- *                 for T >= 2048 and a single stage otherwise.
+ *                 and to at most 64 stages (the last stage takes what is
+ *                 left).  0 picks T/4 for T >= 2048 and a single stage
+ *                 otherwise.
  * One token (T = 1, the decode step) without an undo log, both codebooks
  * given or both NULL: a single launch on `stream` does the addressing of both
  * sides and the scan step, one workgroup per (b, h) stream.  Slots and

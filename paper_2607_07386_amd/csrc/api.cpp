@@ -567,15 +567,17 @@ int sdm_forward_impl(const void* q, const void* k, int x_dtype, const void* cb_q
         return e == hipSuccess ? SDM_OK : hip_fail(e, "sdm_forward single-token launch");
     }
 
-    // pipeline stages: a short first stage (a quarter of the stage length; its
-    // addressing cannot overlap anything), then stages of len tokens; all
-    // multiples of 64 tokens, at most kMaxChunks of them
+    // pipeline stages of len tokens (multiples of 64 tokens, at most kMaxChunks
+    // of them), the last one shorter.  The first stage's addressing overlaps
+    // nothing; a shorter first stage (a quarter of len) left the scan idle
+    // while the second stage's addressing ran beside the short first scan:
+    // 1.4B-shaped step 6.27 against 6.15 ms, learned-M0 5.54 against 5.38.
     int len = T, first = T, nchunks = 1;
     if (pipelined && (chunk > 0 || T >= 2048)) {
         len = chunk > 0 ? round_up(chunk, 64) : round_up((T + 3) / 4, 64);
-        len = std::max(len, round_up((T + kMaxChunks - 2) / (kMaxChunks - 1), 64));
-        first = std::min(T, round_up(std::max(len / 4, 64), 64));
-        nchunks = first >= T ? 1 : 1 + (T - first + len - 1) / len;
+        len = std::max(len, round_up((T + kMaxChunks - 1) / kMaxChunks, 64));
+        first = std::min(T, len);
+        nchunks = (T + len - 1) / len;
     }
     auto stage_begin = [&](int c) { return c == 0 ? 0 : std::min(T, first + (c - 1) * len); };
 
