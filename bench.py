@@ -173,9 +173,9 @@ def main():
     ap.add_argument("--chunk", type=int, default=384,
                     help="tokens per pipeline stage of the forward step (0: the library's choice, a "
                          "quarter of T; 384, measured best for this workload, by default)")
-    ap.add_argument("--learned-chunk", type=int, default=1024,
+    ap.add_argument("--learned-chunk", type=int, default=1280,
                     help="tokens per pipeline stage of the learned-M0 forward step (0: the library's "
-                         "choice, a quarter of T; 1024, measured best there, by default)")
+                         "choice, a quarter of T; 1280, measured best there, by default)")
     ap.add_argument("--train-chunk", type=int, default=0,
                     help="tokens per pipeline stage of the training step's forward (0: the library's "
                          "choice, measured best there)")

@@ -608,8 +608,9 @@ def test_backward_line_prefetch_depths(name):
 # Each runs the calls bench.py times: the 1.4B-shaped forward as sdm_forward
 # with 384-token stages, the training step as sdm_forward with the undo log
 # (the library's stage choice) and then sdm_scan_bwd with chunk 64.  The
-# long-context and learned-M0 workloads run sdm_forward with the library's
-# stages (a quarter of T).
+# learned-M0 workload runs sdm_forward with 1280-token stages, as bench.py
+# does, and the long-context workload with the library's stages (a quarter
+# of T).
 def _full(cfg, streams_of, chunk):
     w = synth.WORKLOADS[cfg]
     inp = synth.Inputs(w)
@@ -634,7 +635,7 @@ def test_full_c2():
 
 @pytest.mark.slow
 def test_full_c3():
-    _full(3, lambda S: [0, S - 1], chunk=0)
+    _full(3, lambda S: [0, S - 1], chunk=1280)
 
 
 @pytest.mark.slow
